@@ -1,0 +1,156 @@
+"""Pins for the oracle's block quantizers, centroid state and demotion (CPU only)."""
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle import fp16, quant
+from paper_2608_23599_amd import synth
+
+
+def _block(seed=0, scale=1.0):
+    k, _ = synth.kv_unit(100 + seed, 0, 0, 64)
+    x = fp16.to_f64(k) * scale
+    return fp16.to_f64(fp16.from_f64(x))
+
+
+@pytest.mark.parametrize("bits", [8, 4, 2])
+def test_scalar_codes_are_nearest_levels(bits):
+    """Brute force: each code is the reconstruction level c*s16+z16 nearest to x,
+    computed with exact rationals (the rint/division/clamp must implement this)."""
+    x = _block(1)[:, :16]
+    codes, s16, z16 = quant.quantize_scalar(x, bits)
+    s = fp16.to_f64(s16)
+    z = fp16.to_f64(z16)
+    qmax = (1 << bits) - 1
+    for d in range(x.shape[1]):
+        lv = [Fraction(c) * Fraction(s[d]) + Fraction(z[d]) for c in range(qmax + 1)]
+        for j in range(x.shape[0]):
+            fx = Fraction(x[j, d])
+            errs = [abs(fx - v) for v in lv]
+            best = min(errs)
+            cands = [c for c in range(qmax + 1) if errs[c] == best]
+            assert codes[j, d] in cands
+
+
+@pytest.mark.parametrize("bits", [8, 4, 2])
+def test_scalar_error_bound_and_range(bits):
+    x = _block(2)
+    codes, s16, z16 = quant.quantize_scalar(x, bits)
+    qmax = (1 << bits) - 1
+    assert codes.min() >= 0 and codes.max() <= qmax
+    s = fp16.to_f64(s16)
+    s64 = (x.max(0) - x.min(0)) / qmax
+    xh = quant.dequant_scalar(codes, s16, z16)
+    bound = s / 2 + qmax * np.abs(s64 - s) + 1e-12
+    assert np.all(np.abs(x - xh) <= bound[None, :])
+    # the minimum of every channel is stored exactly as the zero and gets code 0
+    assert np.array_equal(fp16.to_f64(z16), x.min(0))
+    assert np.all(codes[x.argmin(0), np.arange(x.shape[1])] == 0)
+
+
+def test_dequant_is_exact_in_fp64():
+    x = _block(3, scale=37.0)
+    for bits in (8, 4, 2):
+        codes, s16, z16 = quant.quantize_scalar(x, bits)
+        xh = quant.dequant_scalar(codes, s16, z16)
+        s, z = fp16.to_f64(s16), fp16.to_f64(z16)
+        for j in range(0, 64, 7):
+            for d in range(0, 128, 5):
+                assert Fraction(xh[j, d]) == Fraction(int(codes[j, d])) * Fraction(s[d]) + Fraction(z[d])
+
+
+def test_constant_channel_and_scale_rounding():
+    x = _block(4)
+    x[:, 5] = 1.5
+    codes, s16, z16 = quant.quantize_scalar(x, 4)
+    assert s16[5] == 0 and np.all(codes[:, 5] == 0)
+    assert fp16.to_f64(z16)[5] == 1.5
+    # the scale is one RNE rounding of the fp64 quotient
+    rng_ = x.max(0) - x.min(0)
+    assert np.array_equal(s16, fp16.from_f64(rng_ / 15.0))
+
+
+@pytest.mark.parametrize("bits", [8, 4, 2])
+def test_requantize_same_level_is_identity(bits):
+    qmax = (1 << bits) - 1
+    r = np.random.default_rng(bits)
+    codes = r.integers(0, qmax + 1, size=(64, 128))
+    codes[0] = 0
+    codes[1] = qmax      # both extreme codes present in every channel
+    s16 = fp16.from_f64(r.uniform(0.01, 2.0, 128))
+    z16 = fp16.from_f64(r.standard_normal(128))
+    xh = quant.dequant_scalar(codes, s16, z16)
+    c2, s2, z2 = quant.quantize_scalar(xh, bits)
+    assert np.array_equal(c2, codes) and np.array_equal(s2, s16) and np.array_equal(z2, z16)
+
+
+def test_centroids_recover_separated_clusters():
+    r = np.random.default_rng(11)
+    protos = r.standard_normal((4, 128)) * 20
+    member = np.array([j % 4 for j in range(64)])
+    r.shuffle(member[4:])
+    member[[0, 16, 32, 48]] = [0, 1, 2, 3]
+    x = protos[member] + r.standard_normal((64, 128)) * 0.01
+    x = fp16.to_f64(fp16.from_f64(x))
+    cent16, ids = quant.kmeans_centroids(x)
+    assert np.array_equal(ids, member)
+    for k in range(4):
+        m = x[member == k].mean(0)
+        # the stored centroid is the cluster mean rounded once to fp16 (half an ulp)
+        assert np.all(np.abs(fp16.to_f64(cent16[k]) - m) <= np.abs(m) * 2.0 ** -11 + 2.0 ** -24)
+
+
+def test_centroid_ids_are_argmin_of_stored_centroids():
+    x = _block(5)
+    cent16, ids = quant.kmeans_centroids(x)
+    c = fp16.to_f64(cent16)
+    for j in range(64):
+        dist = [sum((Fraction(x[j, d]) - Fraction(c[k, d])) ** 2 for d in range(128)) for k in range(4)]
+        best = min(dist)
+        # channel-sequential fp64 distances can only tie-break differently when the
+        # exact distances are within rounding of each other
+        assert dist[ids[j]] <= best * (1 + 1e-12)
+
+
+def test_k1_centroid_is_block_mean():
+    x = _block(6)
+    cent16, ids = quant.kmeans_centroids(x, k=1)
+    exact_mean = [sum(Fraction(v) for v in x[:, d]) / 64 for d in range(128)]
+    assert np.array_equal(cent16[0], fp16.from_f64(np.array([float(m) for m in exact_mean])))
+    assert np.all(ids == 0)
+
+
+def test_lloyd_objective_does_not_increase():
+    x = _block(7)
+    c = x[[0, 16, 32, 48]].copy()
+    prev = np.inf
+    for _ in range(10):
+        d = quant._sq_dist(x, c)
+        a = d.argmin(1)
+        obj = d[np.arange(64), a].sum()
+        assert obj <= prev * (1 + 1e-12)
+        prev = obj
+        for k in range(4):
+            if np.any(a == k):
+                c[k] = x[a == k].mean(0)
+
+
+def test_demote_chain_and_no_promotion():
+    x = _block(8)
+    rec = quant.encode_fp16(16, fp16.from_f64(x))
+    chain = [8, 4, 2, 1]
+    for lv in chain:
+        rec = quant.demote(rec, lv)
+        assert rec.level == lv
+    with pytest.raises(quant.NotMonotone):
+        quant.demote(rec, 2)
+    r8 = quant.encode(8, x)
+    with pytest.raises(quant.NotMonotone):
+        quant.demote(r8, 8)
+    with pytest.raises(quant.NotMonotone):
+        quant.demote(r8, 16)
+    # demotion re-encodes the current (already quantized) values
+    d4 = quant.demote(r8, 4)
+    c, s, z = quant.quantize_scalar(quant.decode(r8), 4)
+    assert np.array_equal(d4.codes, c) and np.array_equal(d4.s16, s) and np.array_equal(d4.z16, z)

@@ -1,0 +1,177 @@
+"""Pins for the oracle's Quest ranking, attention, residual, certificate and
+rate accounting (CPU only)."""
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle import fp16, quant, quest, attention, residual, accounting, certificate, cache
+from oracle.ladder import ladder
+from paper_2608_23599_amd import synth
+
+GOLD = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_rates.json")))
+
+
+def _seq_dot(q, k):
+    acc = 0.0
+    for a, b in zip(q, k):
+        acc = acc + a * b
+    return acc
+
+
+def test_box_bound_never_below_true_score():
+    k, _ = synth.kv_unit(201, 0, 0, 512)
+    q = synth.queries(201, 1, 4)[0]
+    kmin, kmax = quest.page_boxes(k)
+    ub = quest.box_upper_bounds(q, kmin, kmax)
+    kf, qf = fp16.to_f64(k), fp16.to_f64(q)
+    for g in range(4):
+        for p in range(kmin.shape[0]):
+            best = max(_seq_dot(qf[g], kf[j]) for j in range(16 * p, 16 * p + 16))
+            assert ub[g, p] >= best
+    assert np.all(fp16.to_f64(kmin)[:, None, :] <= fp16.to_f64(k).reshape(32, 16, 128))
+
+
+def test_page_size_one_is_exact_topk():
+    r = np.random.default_rng(3)
+    k = fp16.from_f64(r.integers(-8, 9, size=(300, 128)).astype(np.float64))
+    q = fp16.from_f64(r.integers(-4, 5, size=(1, 128)).astype(np.float64))
+    kmin, kmax = quest.page_boxes(k, page=1)
+    sel = quest.quest_select(q, kmin, kmax, T=300, k=20, page=1)
+    exact = [sum(Fraction(int(a)) * Fraction(int(b)) for a, b in zip(fp16.to_f64(q)[0], fp16.to_f64(k)[j]))
+             for j in range(299)]
+    order = sorted(range(299), key=lambda j: (-exact[j], j))
+    assert list(sel) == sorted(order[:20])
+
+
+def test_ties_go_to_lower_page_and_padding():
+    k, _ = synth.kv_unit(202, 0, 0, 256)
+    k = k.copy()
+    k[64:80] = k[16:32]   # page 4 duplicates page 1
+    kmin, kmax = quest.page_boxes(k)
+    q = synth.queries(202, 1, 2)[0]
+    s = quest.page_scores(q, kmin, kmax)
+    assert s[1] == s[4]
+    top = np.lexsort((np.arange(len(s)), -s))
+    pos1, pos4 = list(top).index(1), list(top).index(4)
+    assert pos1 < pos4
+    sel = quest.select_top(s, 40)
+    assert list(sel[:len(s)]) == list(range(len(s))) and np.all(sel[len(s):] == -1)
+
+
+def test_quest_all_pages_equals_dense():
+    k, v = synth.kv_unit(203, 0, 0, 1024)
+    lv = ladder("tiny", 1024)
+    uc = cache.UnitCache(k, v, lv)
+    q = synth.queries(203, 1, 4)[0]
+    kmin, kmax = quest.page_boxes(k)
+    pages = quest.quest_select(q, kmin, kmax, T=1024, k=64)
+    assert np.array_equal(pages[:63], np.arange(63))
+    np.testing.assert_allclose(uc.decode_quest(q, pages), uc.decode_dense(q), rtol=0, atol=1e-14)
+
+
+def test_attention_matches_bruteforce():
+    k, v = synth.kv_unit(204, 0, 0, 96)
+    q = synth.queries(204, 1, 3)[0]
+    kh, vh = fp16.to_f64(k), fp16.to_f64(v)
+    a = attention.attend(fp16.to_f64(q), kh, vh)
+    b = attention.attend_bruteforce(fp16.to_f64(q).tolist(), kh.tolist(), vh.tolist())
+    np.testing.assert_allclose(a, b, rtol=1e-12, atol=1e-13)
+
+
+def test_all_exact_ladder_is_plain_attention():
+    k, v = synth.kv_unit(205, 0, 0, 200)
+    q = synth.queries(205, 1, 2)[0]
+    uc = cache.UnitCache(k, v, ladder("exact", 200))
+    ref = attention.attend_bruteforce(fp16.to_f64(q).tolist(), fp16.to_f64(k).tolist(), fp16.to_f64(v).tolist())
+    np.testing.assert_allclose(uc.decode_dense(q), ref, rtol=1e-12, atol=1e-13)
+
+
+def test_certificate_holds_for_graded_reconstruction():
+    k, v = synth.kv_unit(206, 0, 0, 2048)
+    uc = cache.UnitCache(k, v, ladder("tiny", 2048))
+    kh, vh = uc.khat_vhat()
+    kf, vf = fp16.to_f64(k), fp16.to_f64(v)
+    qs = fp16.to_f64(synth.queries(206, 1, 8)[0])
+    for g in range(8):
+        bnd, err = certificate.bound(qs[g], kf, vf, kh, vh)
+        assert err <= bnd
+        assert err > 0
+
+
+def test_residual_selection_pins():
+    T = 512
+    k, v = synth.kv_unit(207, 0, 0, T)
+    uc = cache.UnitCache(k, v, ladder("tiny", T))
+    m = synth.mass_unit(207, 0, 0, T)
+    n = residual.n_keep(T, 2)
+    assert n == 10
+    idx, s = uc.select_residual(k, v, m, n)
+    lv = np.repeat(uc.levels, 64)[:T]
+    assert np.all(s[lv == 16] == 0)            # exact tokens have no distortion
+    assert len(idx) == n and np.all(np.diff(idx) > 0)
+    brute = sorted(range(T), key=lambda j: (-s[j], j))[:n]
+    assert list(idx) == sorted(brute)
+    # fraction 0 leaves the graded cache unchanged
+    uc0 = cache.UnitCache(k, v, ladder("tiny", T))
+    uc0.select_residual(k, v, m, 0)
+    q = synth.queries(207, 1, 2)[0]
+    np.testing.assert_array_equal(uc0.decode_dense(q), cache.UnitCache(k, v, ladder("tiny", T)).decode_dense(q))
+    # with the residual, selected tokens read their exact values
+    kh, vh = uc.khat_vhat()
+    assert np.array_equal(vh[idx], fp16.to_f64(v[idx]))
+
+
+def test_rd_score_on_centroid_block_is_equation():
+    # for a centroid block the graded value IS the block value centroid of Eq. rdscore
+    k, v = synth.kv_unit(208, 0, 0, 64)
+    rec = quant.encode_fp16(1, v)
+    c = fp16.to_f64(rec.cent16)
+    a = synth.mass_unit(208, 0, 0, 64)
+    s = residual.scores(fp16.to_f64(v), quant.decode(rec), a)
+    for j in (0, 17, 63):
+        e = sum((Fraction(x) - Fraction(y)) ** 2 for x, y in zip(fp16.to_f64(v)[j], c[rec.ids[j]]))
+        assert abs(s[j] - float(a[j]) * float(e)) <= 1e-12 * s[j]
+
+
+# ---------------------------------------------------------------- accounting
+
+
+def test_level_bits_per_value():
+    got = [accounting.block_bits(L) / (64 * 128) for L in (16, 8, 4, 2, 1)]
+    assert got == [16.0, 8.5, 4.5, 2.5, 1.015625]
+
+
+def test_tiny_and_llama_graded_rates():
+    r = accounting.unit_rates(ladder("tiny", 2048), 2048)
+    assert r["resident_bits"] / r["values"] == 6.4375
+    r2 = accounting.unit_rates(ladder("graded", 16384), 16384)
+    assert abs(r2["resident_bits"] / r2["values"] - 5.2613) < 5e-5
+
+
+def test_paper_quest_rates():
+    g = GOLD["quest_setting"]
+    T, page, frac = g["T"], g["page_tokens"], g["page_fraction"]
+    lv = ladder("exact", T)
+    npages = T // page
+    k = int(round(frac * npages))
+    pages = np.arange(k)
+    r = accounting.unit_rates(lv, T, page=page, pages=pages)
+    res = r["resident_bits"] / r["values"]
+    rd = r["read_bits"] / r["values"]
+    assert res == pytest.approx(GOLD["quest_resident_bpv"]["value"], abs=1e-9)
+    assert abs(rd - GOLD["quest_read_bpv_3b"]["value"]) < 0.005
+    assert abs(rd - GOLD["quest_read_bpv_8b"]["value"]) < 0.005
+    assert (accounting.BOX_BITS / (page * 2 * 128)) == GOLD["box_rate_bpv_64token_pages"]["value"]
+
+
+def test_paper_per_token_bytes():
+    for key in ("per_token_kib_qwen3_8b", "per_token_kib_qwen25_3b"):
+        g = GOLD[key]
+        bits = g["layers"] * g["kv_heads"] * 2 * accounting.row_bits(16, g["head_dim"])
+        assert bits / 8 / 1024 == g["value"]
+    g = GOLD["kv_gib_1m_qwen25_7b"]
+    bits = g["tokens"] * g["layers"] * g["kv_heads"] * 2 * accounting.row_bits(16, g["head_dim"])
+    assert round(bits / 8 / 2 ** 30, 2) == g["value"]
