@@ -1,0 +1,251 @@
+/*
+ * gkv.h -- C ABI of the MI355X (gfx950) graded KV-cache decode-attention library.
+ *
+ * Method: Geodesia-KV (arXiv 2608.23599).  One layer's KV cache is cut into
+ * blocks of P = 64 tokens per (sequence b, KV head h); every block holds one level
+ * of a monotone precision ladder (section 3.2): exact fp16, block-scaled 8/4/2-bit
+ * scalar codes with fp16 per-channel scale and zero, or 4 fp16 centroids with
+ * per-token ids.  Single-query (Q = 1) GQA decode attention reads the graded
+ * blocks, dequantizing inside an online-softmax loop (section 3.7); optional
+ * exact per-page key boxes rank pages for a sparse read (Compressed-Quest,
+ * section 3.5); an optional exact residual keeps the tokens with the largest
+ * attention-mass x value-error in fp16 (section 3.4, Eq. rdscore).
+ *
+ * Conventions for every call
+ * --------------------------
+ *  - Pointers named *_host are host memory; every other data pointer is DEVICE
+ *    memory owned by the caller.  No call allocates or frees memory.
+ *  - fp16 values travel as uint16_t bit patterns.
+ *  - Device work is enqueued on `stream` (a hipStream_t; NULL = default stream)
+ *    and is ordered with the caller's other work on that stream.  A call returns
+ *    after enqueueing; its results are valid once the stream reaches that point.
+ *  - Arguments are validated on the host BEFORE anything is enqueued: a call that
+ *    returns an error has enqueued nothing and changed nothing.
+ *  - D (head dimension) must be 128 and P (block tokens) 64.  G = Hq / Hkv query
+ *    heads share KV head h = g / G (GQA, section 3.1); 1 <= G <= 16.
+ *  - Calls are thread-compatible: concurrent calls must not share a cache.
+ */
+#ifndef GKV_H
+#define GKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum gkv_status {
+  GKV_OK = 0,
+  GKV_E_ARG = -1,          /* null pointer, bad enum, non-positive size        */
+  GKV_E_SHAPE = -2,        /* D != 128, G out of range, T / capacity mismatch  */
+  GKV_E_NOT_MONOTONE = -3, /* a demotion that is not strictly downwards        */
+  GKV_E_WORKSPACE = -4,    /* workspace smaller than gkv_workspace_bytes()     */
+  GKV_E_HIP = -5,          /* the HIP runtime reported an error                */
+  GKV_E_UNSUPPORTED = -6   /* valid but not implemented combination            */
+} gkv_status;
+
+/* Ladder levels; the numeric value is the bits of a code (1 = centroid state). */
+typedef enum gkv_level {
+  GKV_CENTROID = 1,
+  GKV_INT2 = 2,
+  GKV_INT4 = 4,
+  GKV_INT8 = 8,
+  GKV_EXACT = 16
+} gkv_level;
+
+typedef enum gkv_tensor { GKV_KEYS = 0, GKV_VALUES = 1 } gkv_tensor;
+
+#define GKV_D 128
+#define GKV_P 64
+#define GKV_KCENT 4
+
+/*
+ * Packed record of one tensor block (64 tokens x 128 channels of K or of V)
+ * -------------------------------------------------------------------------
+ * The layout is chosen so that one 64-lane wavefront loads, with contiguous 16-byte
+ * accesses, exactly the operands of its MFMA instructions.  A block is 4 pages of
+ * 16 tokens; inside a page, lane l (0..63) owns a chunk of 32 elements x_n
+ * (n = 0..31) with kg = l >> 4, m = l & 15:
+ *   keys   : x_n = K[token 16*page + m][channel 32*(n>>3) + 8*kg + (n&7)]
+ *   values : x_n = V[token 16*page + 4*kg + (n&3)][channel 16*(n>>2) + m]
+ * Chunks are stored page-major then lane-major: chunk(page, l) at
+ * (page*64 + l) * chunk_bytes.
+ *
+ * GKV_EXACT   (16384 B): chunks of 32 fp16 values (64 B).
+ * GKV_INT8/4/2 (512 + 1024*b B): scale[128] fp16, zero[128] fp16, then chunks of
+ *   32 codes (4*b bytes, little-endian 32-bit words).  scale and zero are stored
+ *   in lane order: entry 32*kg + n holds the channel of element n of a lane in
+ *   group kg (keys: 32*(n>>3) + 8*kg + (n&7); values: 16*(n>>2) + 4*kg + (n&3)).
+ *   Code x_n sits in word n / (32/b) at bit position
+ *     int8: 8*(n&3)
+ *     int4: {4,20,12,28,0,16,8,24}[n&7]
+ *     int2: {8,24,14,30,6,22,12,28,4,20,10,26,0,16,2,18}[n&15]
+ *   Decoded value = code * scale + zero, exact in fp64 (section 3.2 packed scalar
+ *   quantizers; one group per channel over the block's 64 tokens).
+ * GKV_CENTROID (1040 B): 4 x 128 fp16 centroids, then 64 two-bit ids (16 B; the
+ *   id of token t is bits 2t..2t+1).  Key centroids are stored [centroid][channel];
+ *   value centroids [channel & 15][channel >> 4][centroid].
+ *
+ * Residual rows (section 3.4) are stored as exact-format pseudo-blocks: row r of
+ * (b,h) is "token" r & 63 of pseudo-block r >> 6, whose K record is followed by
+ * its V record (32768 B per pseudo-block).
+ *
+ * Page boxes (section 3.5) are fp16 pairs (kmin, kmax) stored per (b, h) as
+ * [page >> 6][channel][page & 63][2]; npage_cap must be a multiple of 64.
+ */
+
+/* One layer's graded cache.  All device tables are [B][Hkv][capacity]. */
+typedef struct gkv_cache {
+  int32_t B, Hkv, Hq, D;     /* D must be 128                                        */
+  int64_t T;                 /* tokens present (same for every sequence)             */
+  int32_t nblk_cap;          /* block-table capacity per (b,h); >= ceil(T/64)        */
+  int8_t *level;             /* device [B][Hkv][nblk_cap] gkv_level of each block     */
+  int64_t *koff, *voff;      /* device [B][Hkv][nblk_cap] byte offsets into `arena`  */
+  uint8_t *arena;            /* device record storage                                */
+  int64_t arena_bytes;       /* size of `arena` (offset validation)                  */
+  int8_t *level_host;        /* host mirror of `level` (required; kept in sync by the
+                                calls that change levels)                            */
+  int32_t page;              /* Quest page tokens (16, 32 or 64); 0 = no boxes       */
+  int64_t npage_cap;         /* box capacity per (b,h) in pages (multiple of 64)      */
+  uint16_t *boxes;           /* device box storage or NULL                           */
+  int32_t nres;              /* exact residual rows per (b,h); 0 = none               */
+  int32_t nres_cap;          /* residual capacity per (b,h)                           */
+  int32_t *res_idx;          /* device [B][Hkv][nres_cap] token index per row, ascending */
+  uint8_t *res_rows;         /* device [B][Hkv][ceil(nres_cap/64)] pseudo-blocks      */
+  uint64_t *res_mask;        /* device [B][Hkv][nblk_cap] bit t%64 set = token t is
+                                read from the residual instead of its block           */
+} gkv_cache;
+
+/* ---------------------------------------------------------------- host helpers */
+
+const char *gkv_strerror(gkv_status s);
+
+/* Bytes of one tensor-block record at `level` (P = 64, D = 128); 0 for a bad level. */
+int64_t gkv_block_bytes(int32_t level);
+
+/* Ladder profiles (section 3.2; fixed age ladders of the workloads):
+ *   0 "tiny":   newest 4 blocks exact, next 8 int8, next 12 int4, rest int2;
+ *   1 "graded": newest 16 exact; int8 / int4 boundaries at 16 + floor(25R/100) and
+ *               16 + floor(60R/100), R = nblk - 16; oldest floor(10*nblk/100) blocks
+ *               centroid (the exact window takes precedence); rest int2;
+ *   2 "exact":  all exact.
+ * Writes levels for blocks 0..nblk-1 (0 = oldest) of a context of T tokens. */
+gkv_status gkv_ladder_levels(int32_t profile, int64_t T, int8_t *levels_host, int32_t nblk);
+
+/* Ladder crossings of a context growing to T_new tokens (section 3.2 monotone
+ * demotion): compares the profile's levels at T_new with c->level_host for every
+ * existing, complete block of every (b,h) and writes up to max_jobs entries
+ * jobs_host[3*i..3*i+2] = (b, h, blk), to_host[i] = new level.  Returns the number
+ * of crossings (>= 0), or a negative gkv_status; GKV_E_NOT_MONOTONE if the profile
+ * would raise any block's level. */
+int32_t gkv_ladder_crossings(const gkv_cache *c, int32_t profile, int64_t T_new, int32_t *jobs_host,
+                             int8_t *to_host, int32_t max_jobs);
+
+/* Slab arena: per-level pools of fixed-size slots inside one device buffer.
+ * cap[i] = slots for level {16,8,4,2,1}[i].  Offsets are byte offsets into the
+ * arena; the pool is host-only bookkeeping (single-threaded). */
+typedef struct gkv_pool gkv_pool;
+gkv_pool *gkv_pool_create(const int64_t cap_host[5]);
+int64_t gkv_pool_bytes(const gkv_pool *p);
+int64_t gkv_pool_alloc(gkv_pool *p, int32_t level); /* -1 when the pool is full */
+gkv_status gkv_pool_free(gkv_pool *p, int32_t level, int64_t offset);
+int64_t gkv_pool_used(const gkv_pool *p, int32_t level);
+void gkv_pool_destroy(gkv_pool *p);
+
+/* Rate accounting (section 3.5 rate equations; section 4.4 metrics), from the
+ * host level mirror.  pages_host = selected pages [B][Hkv][topk] (-1 padded) for a
+ * Compressed-Quest read, or NULL for a dense read.  Outputs are bit counts and
+ * the number of values B*Hkv*T*2*D. */
+typedef struct gkv_rates {
+  int64_t resident_bits, read_bits, values;
+} gkv_rates;
+gkv_status gkv_account(const gkv_cache *c, const int32_t *pages_host, int32_t topk, gkv_rates *out);
+
+/* Decode one record (host copy) to codes / values, for inspection and tests.
+ * values_host: [64][128] fp64 reconstruction (token-major); codes_host (optional,
+ * int levels): [64][128]; scale_host, zero_host (optional, int levels): [128] fp16
+ * in channel order; ids_host (optional, centroid): [64]; cent_host (optional,
+ * centroid): [4][128] fp16. */
+gkv_status gkv_decode_record(int32_t level, int32_t tensor, const uint8_t *rec_host, double *values_host,
+                             int32_t *codes_host, uint16_t *scale_host, uint16_t *zero_host,
+                             int32_t *ids_host, uint16_t *cent_host);
+
+/* fp64 -> fp16 bits with one round-to-nearest-even (the conversion the kernels use). */
+uint16_t gkv_f64_to_f16(double x);
+
+/* Workspace bytes needed by gkv_quest_select (op 0), gkv_graded_decode_attn (op 1,
+ * topk = 0 for a dense read) and gkv_rd_residual_select (op 2). */
+int64_t gkv_workspace_bytes(const gkv_cache *c, int32_t op, int32_t topk);
+
+/* ---------------------------------------------------------------- device calls */
+
+/* Encode blocks [blk_begin, blk_end) of every (b,h) from exact fp16 source rows at
+ * the level each block holds in c->level_host, into c->arena at koff/voff
+ * (section 3.2 packed quantizers; section 5.7 packed-format constructor).
+ * src: [B][Hkv][T_src][128] fp16 keys (which = GKV_KEYS) or values.  Only an exact
+ * block may extend past T_src (missing rows are stored as zero).  Int levels use
+ * the per-channel asymmetric quantizer z = f16(min), s = f16((max-min)/(2^b-1)),
+ * code = rint((x-z)/s) clamped, in fp64; centroid blocks run 4-means Lloyd in fp64
+ * (rows 0,16,32,48 initial, at most 10 rounds, fp16 centroids, ids re-assigned
+ * against the stored centroids). */
+gkv_status gkv_quantize_block(const gkv_cache *c, int32_t which, const uint16_t *src, int64_t T_src,
+                              int32_t blk_begin, int32_t blk_end, void *stream);
+
+/* Monotone demotion (section 3.2): re-encode n blocks, each given as
+ * jobs_host[3*i .. 3*i+2] = (b, h, blk), from their current record (exact fp64
+ * decode) to to_level_host[i], writing the new K and V records at new_koff_host[i]
+ * / new_voff_host[i] and updating the device and host level / offset tables.
+ * Every job must lower the level (GKV_E_NOT_MONOTONE otherwise; nothing is
+ * enqueued then).  The old slots are free once the stream has passed this call. */
+gkv_status gkv_demote(gkv_cache *c, int32_t n, const int32_t *jobs_host, const int8_t *to_level_host,
+                      const int64_t *new_koff_host, const int64_t *new_voff_host, void *stream);
+
+/* Exact per-page key boxes (section 3.5): for pages [page_begin, page_end) of every
+ * (b,h), per channel min and max of the exact fp16 keys k_src [B][Hkv][T_src][128]
+ * (all tokens of each page must be < T_src). */
+gkv_status gkv_page_boxes(const gkv_cache *c, const uint16_t *k_src, int64_t T_src, int64_t page_begin,
+                          int64_t page_end, void *stream);
+
+/* Append one token per (b,h) (decode step): k_new, v_new [B][Hkv][128] fp16 are
+ * written into the newest block, which must be exact.  When T is a multiple of 64
+ * a new exact block is opened for every (b,h) u at byte offsets new_koff_host[u] /
+ * new_voff_host[u] (arrays of B*Hkv <= 128 entries; ignored otherwise, may be NULL).
+ * When the token completes a page and boxes are kept, that page's box is written
+ * from the exact keys.  c->T is incremented. */
+#define GKV_MAX_APPEND_UNITS 128
+gkv_status gkv_append(gkv_cache *c, const uint16_t *k_new, const uint16_t *v_new, const int64_t *new_koff_host,
+                      const int64_t *new_voff_host, void *stream);
+
+/* Compressed-Quest page selection (section 3.5): for every (b,h), rank the closed
+ * pages 0 .. cur-1 (cur = (T-1)/page is always read, never ranked) by the box upper
+ * bound UB_g(p) = sum_d q_gd * (q_gd >= 0 ? kmax_pd : kmin_pd), accumulated in
+ * fp64 in channel order, maximised over the group's query heads; write the first
+ * topk pages of the order (score desc, page asc) to pages [B][Hkv][topk] in
+ * ascending order, -1 padded.  q: [B][Hq][128] fp16. */
+gkv_status gkv_quest_select(const uint16_t *q, const gkv_cache *c, int32_t topk, int32_t *pages, void *ws,
+                            int64_t ws_bytes, void *stream);
+
+/* Fused dequant + online-softmax GQA decode attention (sections 3.1, 3.7): for every
+ * query head g of every sequence b, out[b][g][:] = sum_j softmax_j(q.k_j/sqrt(128)) v_j
+ * over the read set -- all tokens < T (pages == NULL) or the selected pages
+ * [B][Hkv][topk] plus the current page (section 3.5).  Residual rows override their
+ * tokens' graded entries (dense reads only).  q: [B][Hq][128] fp16;
+ * out: [B][Hq][128] fp32. */
+gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache *c, const int32_t *pages, int32_t topk,
+                                  float *out, void *ws, int64_t ws_bytes, void *stream);
+
+/* Rate-distortion exact residual (section 3.4, Eq. rdscore): score every token
+ * s_j = a_j * sum_d (v_jd - v_hat_jd)^2 (fp64, channel order, no fused multiply-add)
+ * with v_hat its value at its block's level, keep the first nkeep of the order
+ * (score desc, token asc) per (b,h), and store their exact K and V rows, ascending
+ * indices and per-block override masks in the cache.  k_src, v_src:
+ * [B][Hkv][T][128] fp16; mass: [B][Hkv][T] fp32.  Sets c->nres = nkeep. */
+gkv_status gkv_rd_residual_select(gkv_cache *c, const uint16_t *k_src, const uint16_t *v_src,
+                                  const float *mass, int32_t nkeep, void *ws, int64_t ws_bytes,
+                                  void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GKV_H */

@@ -1,0 +1,424 @@
+"""Thin ctypes binding over libgkv's C ABI (include/gkv.h).
+
+torch supplies device memory and the current HIP stream; every step of the decode
+path runs in the library's HIP kernels.  The library must be built
+(``__graft_entry__.build()``); importing this module without it raises.
+
+The function names mirror the C calls (``quantize_block``, ``demote``,
+``page_boxes``, ``quest_select``, ``graded_decode_attn``, ``rd_residual_select``,
+``append``); ``GradedCache`` owns the device tables and the slab arena of one
+layer's cache and marshals them into the ``gkv_cache`` descriptor.
+"""
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "_lib", "libgkv.so")
+if not os.path.exists(_LIB_PATH):
+    raise ImportError(f"{_LIB_PATH} is not built; run __graft_entry__.build()")
+lib = ctypes.CDLL(_LIB_PATH)
+
+EXACT, INT8, INT4, INT2, CENTROID = 16, 8, 4, 2, 1
+LEVELS = (EXACT, INT8, INT4, INT2, CENTROID)
+KEYS, VALUES = 0, 1
+PROFILES = {"tiny": 0, "graded": 1, "exact": 2}
+P, D = 64, 128
+
+_vp, _i32, _i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+
+
+class CacheStruct(ctypes.Structure):
+    _fields_ = [
+        ("B", _i32), ("Hkv", _i32), ("Hq", _i32), ("D", _i32),
+        ("T", _i64), ("nblk_cap", _i32),
+        ("level", _vp), ("koff", _vp), ("voff", _vp), ("arena", _vp), ("arena_bytes", _i64),
+        ("level_host", _vp),
+        ("page", _i32), ("npage_cap", _i64), ("boxes", _vp),
+        ("nres", _i32), ("nres_cap", _i32), ("res_idx", _vp), ("res_rows", _vp), ("res_mask", _vp),
+    ]
+
+
+class Rates(ctypes.Structure):
+    _fields_ = [("resident_bits", _i64), ("read_bits", _i64), ("values", _i64)]
+
+
+def _sig(name, res, args):
+    f = getattr(lib, name)
+    f.restype = res
+    f.argtypes = args
+    return f
+
+
+_P = ctypes.POINTER
+_strerror = _sig("gkv_strerror", ctypes.c_char_p, [_i32])
+_block_bytes = _sig("gkv_block_bytes", _i64, [_i32])
+_ladder_levels = _sig("gkv_ladder_levels", _i32, [_i32, _i64, _vp, _i32])
+_ladder_crossings = _sig("gkv_ladder_crossings", _i32, [_P(CacheStruct), _i32, _i64, _vp, _vp, _i32])
+_pool_create = _sig("gkv_pool_create", _vp, [_vp])
+_pool_bytes = _sig("gkv_pool_bytes", _i64, [_vp])
+_pool_alloc = _sig("gkv_pool_alloc", _i64, [_vp, _i32])
+_pool_free = _sig("gkv_pool_free", _i32, [_vp, _i32, _i64])
+_pool_used = _sig("gkv_pool_used", _i64, [_vp, _i32])
+_pool_destroy = _sig("gkv_pool_destroy", None, [_vp])
+_account = _sig("gkv_account", _i32, [_P(CacheStruct), _vp, _i32, _P(Rates)])
+_decode_record = _sig("gkv_decode_record", _i32, [_i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp])
+_f64_to_f16 = _sig("gkv_f64_to_f16", ctypes.c_uint16, [ctypes.c_double])
+_workspace_bytes = _sig("gkv_workspace_bytes", _i64, [_P(CacheStruct), _i32, _i32])
+_quantize_block = _sig("gkv_quantize_block", _i32, [_P(CacheStruct), _i32, _vp, _i64, _i32, _i32, _vp])
+_demote = _sig("gkv_demote", _i32, [_P(CacheStruct), _i32, _vp, _vp, _vp, _vp, _vp])
+_page_boxes = _sig("gkv_page_boxes", _i32, [_P(CacheStruct), _vp, _i64, _i64, _i64, _vp])
+_append = _sig("gkv_append", _i32, [_P(CacheStruct), _vp, _vp, _vp, _vp, _vp])
+_quest_select = _sig("gkv_quest_select", _i32, [_vp, _P(CacheStruct), _i32, _vp, _vp, _i64, _vp])
+_attn = _sig("gkv_graded_decode_attn", _i32, [_vp, _P(CacheStruct), _vp, _i32, _vp, _vp, _i64, _vp])
+_rd = _sig("gkv_rd_residual_select", _i32, [_P(CacheStruct), _vp, _vp, _vp, _i32, _vp, _i64, _vp])
+
+EXPORTED = [
+    "gkv_strerror", "gkv_block_bytes", "gkv_ladder_levels", "gkv_ladder_crossings", "gkv_pool_create",
+    "gkv_pool_bytes", "gkv_pool_alloc", "gkv_pool_free", "gkv_pool_used", "gkv_pool_destroy", "gkv_account",
+    "gkv_decode_record", "gkv_f64_to_f16", "gkv_workspace_bytes", "gkv_quantize_block", "gkv_demote",
+    "gkv_page_boxes", "gkv_append", "gkv_quest_select", "gkv_graded_decode_attn", "gkv_rd_residual_select",
+]
+
+
+class GkvError(RuntimeError):
+    def __init__(self, status, what):
+        self.status = status
+        super().__init__(f"{what}: {_strerror(status).decode()} ({status})")
+
+
+def _check(st, what):
+    if st != 0:
+        raise GkvError(st, what)
+
+
+def _np_ptr(a):
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def _dptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def block_bytes(level):
+    return int(_block_bytes(level))
+
+
+def f64_to_f16(x):
+    return int(_f64_to_f16(float(x)))
+
+
+def ladder_levels(profile, T):
+    nblk = (int(T) + P - 1) // P
+    out = np.empty(nblk, dtype=np.int8)
+    _check(_ladder_levels(PROFILES.get(profile, profile), int(T), _np_ptr(out), nblk), "ladder_levels")
+    return out
+
+
+def decode_record(level, tensor, rec):
+    """Host decode of one record (bytes / uint8 array) -> dict of numpy arrays."""
+    rec = np.ascontiguousarray(np.frombuffer(bytes(rec), dtype=np.uint8))
+    vals = np.empty((P, D), dtype=np.float64)
+    codes = np.empty((P, D), dtype=np.int32)
+    s = np.empty(D, dtype=np.uint16)
+    z = np.empty(D, dtype=np.uint16)
+    ids = np.empty(P, dtype=np.int32)
+    cent = np.empty((4, D), dtype=np.uint16)
+    _check(_decode_record(level, tensor, _np_ptr(rec), _np_ptr(vals), _np_ptr(codes), _np_ptr(s), _np_ptr(z),
+                          _np_ptr(ids), _np_ptr(cent)), "decode_record")
+    out = {"values": vals}
+    if level in (INT8, INT4, INT2):
+        out.update(codes=codes, s16=s, z16=z)
+    if level == CENTROID:
+        out.update(ids=ids, cent16=cent)
+    return out
+
+
+class Pool:
+    """Per-level slab pools inside one arena (host bookkeeping in the library)."""
+
+    def __init__(self, caps):
+        arr = np.array([int(caps.get(lv, 0)) for lv in LEVELS], dtype=np.int64)
+        self._caps = arr
+        self.h = _pool_create(_np_ptr(arr))
+        if not self.h:
+            raise GkvError(-1, "pool_create")
+
+    @property
+    def bytes(self):
+        return int(_pool_bytes(self.h))
+
+    def alloc(self, level):
+        off = int(_pool_alloc(self.h, level))
+        if off < 0:
+            raise GkvError(-1, f"pool exhausted for level {level}")
+        return off
+
+    def free(self, level, off):
+        _check(_pool_free(self.h, level, int(off)), "pool_free")
+
+    def used(self, level):
+        return int(_pool_used(self.h, level))
+
+    def __del__(self):
+        if getattr(self, "h", None):
+            _pool_destroy(self.h)
+            self.h = None
+
+
+def _as_bits(t, device):
+    """fp16 bit patterns as an int16 device tensor."""
+    if isinstance(t, np.ndarray):
+        t = torch.from_numpy(np.ascontiguousarray(t).view(np.int16))
+    if t.dtype == torch.float16:
+        t = t.view(torch.int16)
+    return t.to(device).contiguous()
+
+
+class GradedCache:
+    """One layer's graded KV cache in device memory (section 3.2 ladder, optional
+    Compressed-Quest boxes and exact residual)."""
+
+    def __init__(self, B, Hkv, Hq, T, nblk_cap, caps, page=0, npage_cap=0, nres_cap=0, device="cuda"):
+        self.device = torch.device(device)
+        self.B, self.Hkv, self.Hq = B, Hkv, Hq
+        self.units = B * Hkv
+        self.nblk_cap = nblk_cap
+        self.pool = Pool(caps)
+        self.arena = torch.empty(max(self.pool.bytes, 256), dtype=torch.uint8, device=self.device)
+        self.level = torch.zeros((B, Hkv, nblk_cap), dtype=torch.int8, device=self.device)
+        self.koff = torch.zeros((B, Hkv, nblk_cap), dtype=torch.int64, device=self.device)
+        self.voff = torch.zeros((B, Hkv, nblk_cap), dtype=torch.int64, device=self.device)
+        self.level_host = np.zeros((B, Hkv, nblk_cap), dtype=np.int8)
+        self.koff_host = np.zeros((B, Hkv, nblk_cap), dtype=np.int64)
+        self.voff_host = np.zeros((B, Hkv, nblk_cap), dtype=np.int64)
+        self.page = page
+        self.npage_cap = npage_cap
+        self.boxes = (torch.zeros((B, Hkv, npage_cap * 2 * D), dtype=torch.int16, device=self.device)
+                      if page else None)
+        self.nres_cap = nres_cap
+        nrb = (nres_cap + P - 1) // P
+        if nres_cap:
+            self.res_idx = torch.zeros((B, Hkv, nres_cap), dtype=torch.int32, device=self.device)
+            self.res_rows = torch.zeros((B, Hkv, nrb * 2 * 16384), dtype=torch.uint8, device=self.device)
+            self.res_mask = torch.zeros((B, Hkv, nblk_cap), dtype=torch.int64, device=self.device)
+        else:
+            self.res_idx = self.res_rows = self.res_mask = None
+        self.c = CacheStruct()
+        self.c.B, self.c.Hkv, self.c.Hq, self.c.D = B, Hkv, Hq, D
+        self.c.T = T
+        self.c.nblk_cap = nblk_cap
+        self.c.level = self.level.data_ptr()
+        self.c.koff = self.koff.data_ptr()
+        self.c.voff = self.voff.data_ptr()
+        self.c.arena = self.arena.data_ptr()
+        self.c.arena_bytes = self.arena.numel()
+        self.c.level_host = self.level_host.ctypes.data
+        self.c.page = page
+        self.c.npage_cap = npage_cap
+        self.c.boxes = self.boxes.data_ptr() if self.boxes is not None else None
+        self.c.nres = 0
+        self.c.nres_cap = nres_cap
+        self.c.res_idx = self.res_idx.data_ptr() if nres_cap else None
+        self.c.res_rows = self.res_rows.data_ptr() if nres_cap else None
+        self.c.res_mask = self.res_mask.data_ptr() if nres_cap else None
+        self._ws = {}
+
+    # ------------------------------------------------------------ construction
+    @classmethod
+    def build(cls, k, v, Hq, levels, page=0, nres_cap=0, device="cuda", extra_blocks=0, slack=None):
+        """k, v: fp16 bits [B][Hkv][T][128] (numpy uint16 or torch int16/float16).
+        levels: per-block levels, [nblk] (shared) or [B][Hkv][nblk].  Encodes every
+        block at its level (gkv_quantize_block) and, with page > 0, writes the page
+        boxes from the exact keys (gkv_page_boxes)."""
+        kd = _as_bits(k, device)
+        vd = _as_bits(v, device)
+        B, Hkv, T, Dd = kd.shape
+        assert Dd == D
+        nblk = (T + P - 1) // P
+        lv = np.asarray(levels, dtype=np.int8)
+        if lv.ndim == 1:
+            lv = np.broadcast_to(lv, (B, Hkv, nblk))
+        assert lv.shape == (B, Hkv, nblk)
+        nblk_cap = nblk + extra_blocks
+        # one slot per tensor block (keys and values separately), plus slack for
+        # demotions and appended blocks
+        caps = {L: 2 * int((lv == L).sum()) for L in LEVELS}
+        for L, n in (slack or {}).items():
+            caps[L] += 2 * n
+        npage_cap = 0
+        if page:
+            npage_cap = (((T + extra_blocks * P) // page) + 63) // 64 * 64
+        self = cls(B, Hkv, Hq, T, nblk_cap, caps, page=page, npage_cap=npage_cap, nres_cap=nres_cap, device=device)
+        for b in range(B):
+            for h in range(Hkv):
+                for i in range(nblk):
+                    L = int(lv[b, h, i])
+                    self.level_host[b, h, i] = L
+                    self.koff_host[b, h, i] = self.pool.alloc(L)
+                    self.voff_host[b, h, i] = self.pool.alloc(L)
+        self._upload_tables()
+        self.quantize_block(KEYS, kd, 0, nblk)
+        self.quantize_block(VALUES, vd, 0, nblk)
+        if page:
+            self.page_boxes(kd, 0, T // page)
+        return self
+
+    def _upload_tables(self):
+        self.level.copy_(torch.from_numpy(self.level_host))
+        self.koff.copy_(torch.from_numpy(self.koff_host))
+        self.voff.copy_(torch.from_numpy(self.voff_host))
+
+    @property
+    def T(self):
+        return int(self.c.T)
+
+    def workspace(self, op, topk=0):
+        n = int(_workspace_bytes(ctypes.byref(self.c), op, topk))
+        if n < 0:
+            raise GkvError(-1, "workspace_bytes")
+        key = (op, topk)
+        ws = self._ws.get(key)
+        if ws is None or ws.numel() < n:
+            ws = torch.empty(max(n, 16), dtype=torch.uint8, device=self.device)
+            self._ws[key] = ws
+        return ws
+
+    # ------------------------------------------------------------ the six calls (+ append)
+    def quantize_block(self, which, src, blk_begin, blk_end):
+        src = _as_bits(src, self.device)
+        _check(_quantize_block(ctypes.byref(self.c), which, _dptr(src), src.shape[2], blk_begin, blk_end, _stream()),
+               "quantize_block")
+
+    def page_boxes(self, k_src, page_begin, page_end):
+        k_src = _as_bits(k_src, self.device)
+        _check(_page_boxes(ctypes.byref(self.c), _dptr(k_src), k_src.shape[2], page_begin, page_end, _stream()),
+               "page_boxes")
+
+    def demote(self, jobs, to_levels):
+        """jobs: [(b, h, blk)], to_levels: levels; allocates the new slots, demotes,
+        and frees the old ones (stream-ordered reuse)."""
+        n = len(jobs)
+        if n == 0:
+            return
+        J = np.ascontiguousarray(np.array(jobs, dtype=np.int32).reshape(n, 3))
+        to = np.ascontiguousarray(np.array(to_levels, dtype=np.int8))
+        old = [(int(self.level_host[b, h, i]), int(self.koff_host[b, h, i]), int(self.voff_host[b, h, i]))
+               for b, h, i in J]
+        nk = np.array([self.pool.alloc(int(t)) for t in to], dtype=np.int64)
+        nv = np.array([self.pool.alloc(int(t)) for t in to], dtype=np.int64)
+        st = _demote(ctypes.byref(self.c), n, _np_ptr(J), _np_ptr(to), _np_ptr(nk), _np_ptr(nv), _stream())
+        if st != 0:
+            for t, a, bb in zip(to, nk, nv):
+                self.pool.free(int(t), int(a))
+                self.pool.free(int(t), int(bb))
+            raise GkvError(st, "demote")
+        for (b, h, i), (L, ko, vo), t, a, bb in zip(J, old, to, nk, nv):
+            self.pool.free(L, ko)
+            self.pool.free(L, vo)
+            self.koff_host[b, h, i] = a
+            self.voff_host[b, h, i] = bb
+
+    def append(self, k_new, v_new, profile=None):
+        """Append one token per (b,h) (k_new, v_new fp16 bits [B][Hkv][128]); then,
+        with a ladder profile, demote every block whose level the profile lowers.
+        Returns the demotions [(b, h, blk, old, new)]."""
+        kd = _as_bits(k_new, self.device)
+        vd = _as_bits(v_new, self.device)
+        T = self.T
+        nk = nv = None
+        if T % P == 0:
+            blk = T // P
+            nk = np.array([self.pool.alloc(EXACT) for _ in range(self.units)], dtype=np.int64)
+            nv = np.array([self.pool.alloc(EXACT) for _ in range(self.units)], dtype=np.int64)
+            self.koff_host[:, :, blk] = nk.reshape(self.B, self.Hkv)
+            self.voff_host[:, :, blk] = nv.reshape(self.B, self.Hkv)
+        _check(_append(ctypes.byref(self.c), _dptr(kd), _dptr(vd), _np_ptr(nk) if nk is not None else None,
+                       _np_ptr(nv) if nv is not None else None, _stream()), "append")
+        moves = []
+        if profile is not None:
+            maxj = self.units * self.nblk_cap
+            jobs = np.empty(3 * 64, dtype=np.int32)
+            to = np.empty(64, dtype=np.int8)
+            n = _ladder_crossings(ctypes.byref(self.c), PROFILES.get(profile, profile), self.T, _np_ptr(jobs),
+                                  _np_ptr(to), 64)
+            if n < 0:
+                raise GkvError(n, "ladder_crossings")
+            if n > 64:
+                jobs = np.empty(3 * n, dtype=np.int32)
+                to = np.empty(n, dtype=np.int8)
+                n = _ladder_crossings(ctypes.byref(self.c), PROFILES.get(profile, profile), self.T, _np_ptr(jobs),
+                                      _np_ptr(to), n)
+            del maxj
+            J = jobs[: 3 * n].reshape(n, 3)
+            olds = [int(self.level_host[b, h, i]) for b, h, i in J]
+            self.demote([tuple(x) for x in J], to[:n])
+            moves = [(int(b), int(h), int(i), o, int(t)) for (b, h, i), o, t in zip(J, olds, to[:n])]
+        return moves
+
+    def quest_select(self, q, topk, out=None):
+        q = _as_bits(q, self.device)
+        if out is None:
+            out = torch.empty((self.B, self.Hkv, topk), dtype=torch.int32, device=self.device)
+        ws = self.workspace(0)
+        _check(_quest_select(_dptr(q), ctypes.byref(self.c), topk, _dptr(out), _dptr(ws), ws.numel(), _stream()),
+               "quest_select")
+        return out
+
+    def graded_decode_attn(self, q, pages=None, out=None):
+        q = _as_bits(q, self.device)
+        topk = int(pages.shape[-1]) if pages is not None else 0
+        if out is None:
+            out = torch.empty((self.B, self.Hq, D), dtype=torch.float32, device=self.device)
+        ws = self.workspace(1, topk)
+        _check(_attn(_dptr(q), ctypes.byref(self.c), _dptr(pages), topk, _dptr(out), _dptr(ws), ws.numel(),
+                     _stream()), "graded_decode_attn")
+        return out
+
+    decode = graded_decode_attn
+
+    def rd_residual_select(self, k_src, v_src, mass, nkeep):
+        kd = _as_bits(k_src, self.device)
+        vd = _as_bits(v_src, self.device)
+        if isinstance(mass, np.ndarray):
+            mass = torch.from_numpy(np.ascontiguousarray(mass, dtype=np.float32))
+        md = mass.to(self.device, torch.float32).contiguous()
+        ws = self.workspace(2)
+        _check(_rd(ctypes.byref(self.c), _dptr(kd), _dptr(vd), _dptr(md), nkeep, _dptr(ws), ws.numel(), _stream()),
+               "rd_residual_select")
+
+    # ------------------------------------------------------------ inspection
+    def account(self, pages=None):
+        r = Rates()
+        if pages is not None:
+            ph = np.ascontiguousarray(pages.cpu().numpy() if torch.is_tensor(pages) else pages, dtype=np.int32)
+            _check(_account(ctypes.byref(self.c), _np_ptr(ph), ph.shape[-1], ctypes.byref(r)), "account")
+        else:
+            _check(_account(ctypes.byref(self.c), None, 0, ctypes.byref(r)), "account")
+        return dict(resident_bits=r.resident_bits, read_bits=r.read_bits, values=r.values,
+                    resident_bpv=r.resident_bits / r.values, read_bpv=r.read_bits / r.values)
+
+    def record_bytes(self, b, h, blk, tensor):
+        L = int(self.level_host[b, h, blk])
+        off = int((self.koff_host if tensor == KEYS else self.voff_host)[b, h, blk])
+        n = block_bytes(L)
+        return L, self.arena[off:off + n].cpu().numpy().tobytes()
+
+    def record(self, b, h, blk, tensor):
+        L, raw = self.record_bytes(b, h, blk, tensor)
+        d = decode_record(L, tensor, raw)
+        d["level"] = L
+        return d
+
+    def boxes_host(self, b, h, npages):
+        """Boxes of (b,h) as (kmin bits [npages][D], kmax bits [npages][D])."""
+        raw = self.boxes[b, h].cpu().numpy().view(np.uint16)
+        g = raw.reshape(-1, D, 64, 2)
+        kmin = g[..., 0].transpose(0, 2, 1).reshape(-1, D)[:npages]
+        kmax = g[..., 1].transpose(0, 2, 1).reshape(-1, D)[:npages]
+        return kmin, kmax

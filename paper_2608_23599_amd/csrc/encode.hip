@@ -1,0 +1,549 @@
+// Block encoders of the precision ladder (section 3.2), monotone demotion, token
+// append, and exact page boxes (section 3.5).
+//
+// Every arithmetic step whose result is stored (scales, zeros, codes, centroids,
+// ids, boxes) is exact-reproducible: fp64 with one rounding per operation, no
+// contraction into fused multiply-adds, channel/token-ascending sequential sums,
+// and one round-to-nearest-even to fp16 (gkv::f64_to_f16).
+#include <hip/hip_runtime.h>
+
+#include "gkv_internal.h"
+
+#pragma clang fp contract(off)
+
+using namespace gkv;
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int XS = D + 1;  // padded LDS row stride (doubles) against bank conflicts
+
+struct EncodeShared {
+  uint16_t xh[P * D];      // source as fp16 bits [token][channel] (rows or exact record)
+  uint8_t xc[P * D];       // source as codes (int-level record being demoted)
+  double xs[D], xz[D];     // source scale / zero for xc
+  int32_t src_int;         // 1: x = xc * xs + xz, 0: x = xh, 2: x = centroid[xc]
+  double sc[KC * D];       // source centroids (fp64) when src_int == 2
+  double c[KC * XS];       // centroids (fp64)
+  double dist[P * KC];     // token x centroid distances
+  double s64[D], z64[D];   // new scale / zero
+  uint16_t s16[D], z16[D];
+  uint8_t codes[P * D];    // new codes (int levels)
+  int32_t assign[P], prev[P];
+  int32_t flag;
+};
+
+// Exact fp64 value of source element (t, d): an fp16 value, or code * scale + zero
+// (both products and the sum are exact in fp64).
+__device__ __forceinline__ double getx(const EncodeShared &S, int t, int d) {
+  if (S.src_int == 2) return S.sc[S.xc[t * D] * D + d];
+  if (S.src_int) {
+    const double prod = (double)S.xc[t * D + d] * S.xs[d];
+    return prod + S.xz[d];
+  }
+  return (double)__builtin_bit_cast(_Float16, S.xh[t * D + d]);
+}
+
+// Load the 64 x 128 block starting at row0 of one (b,h) from token-major fp16 rows;
+// rows at or beyond T_src read as zero.
+__device__ void load_rows(EncodeShared &S, const uint16_t *src, int64_t T_src, int64_t row0) {
+  if (threadIdx.x == 0) S.src_int = 0;
+  for (int i = threadIdx.x; i < P * (D / 8); i += kThreads) {
+    const int t = i / (D / 8), c8 = (i % (D / 8)) * 8;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (row0 + t < T_src) v = *(const uint4 *)(src + (row0 + t) * D + c8);
+    *(uint4 *)(S.xh + t * D + c8) = v;
+  }
+}
+
+// Load a record (exact or int level) as the source.
+__device__ void load_record(EncodeShared &S, const uint8_t *rec, int level, int tensor) {
+  if (level == GKV_EXACT) {
+    if (threadIdx.x == 0) S.src_int = 0;
+    const uint16_t *hh = (const uint16_t *)rec;
+    for (int ck = threadIdx.x; ck < 4 * 64; ck += kThreads) {
+      const int pg = ck >> 6, l = ck & 63;
+      for (int n = 0; n < 32; ++n) {
+        int t, ch;
+        chunk_coord(tensor, pg, l, n, t, ch);
+        S.xh[t * D + ch] = hh[ck * 32 + n];
+      }
+    }
+    return;
+  }
+  if (level == GKV_CENTROID) {
+    if (threadIdx.x == 0) S.src_int = 2;
+    const uint16_t *cc = (const uint16_t *)rec;
+    for (int i = threadIdx.x; i < KC * D; i += kThreads) {
+      const int k = i >> 7, d = i & 127;
+      S.sc[i] = (double)__builtin_bit_cast(_Float16, cc[tensor == GKV_KEYS ? k * D + d : vcent_index(k, d)]);
+    }
+    const uint8_t *idb = rec + KC * D * 2;
+    for (int t = threadIdx.x; t < P; t += kThreads) S.xc[t * D] = (idb[t >> 2] >> (2 * (t & 3))) & 3;
+    return;
+  }
+  if (threadIdx.x == 0) S.src_int = 1;
+  const uint16_t *sz = (const uint16_t *)rec;
+  for (int e = threadIdx.x; e < D; e += kThreads) {
+    const int ch = sz_channel(tensor, e);
+    S.xs[ch] = (double)__builtin_bit_cast(_Float16, sz[e]);
+    S.xz[ch] = (double)__builtin_bit_cast(_Float16, sz[D + e]);
+  }
+  const int bits = level;
+  const uint32_t *w = (const uint32_t *)(rec + kSZBytes);
+  for (int ck = threadIdx.x; ck < 4 * 64; ck += kThreads) {
+    const int pg = ck >> 6, l = ck & 63;
+    for (int n = 0; n < 32; ++n) {
+      int t, ch;
+      chunk_coord(tensor, pg, l, n, t, ch);
+      const uint32_t word = w[ck * bits + code_word(bits, n)];
+      S.xc[t * D + ch] = (uint8_t)((word >> code_pos(bits, n)) & ((1u << bits) - 1u));
+    }
+  }
+}
+
+// Exact level: store the fp16 source in chunk order (source must be fp16).
+__device__ void write_exact(EncodeShared &S, uint8_t *dst, int tensor) {
+  uint16_t *hh = (uint16_t *)dst;
+  for (int ck = threadIdx.x; ck < 4 * 64; ck += kThreads) {
+    const int pg = ck >> 6, l = ck & 63;
+    uint32_t w[16];
+    for (int n = 0; n < 32; n += 2) {
+      int t0, c0, t1, c1;
+      chunk_coord(tensor, pg, l, n, t0, c0);
+      chunk_coord(tensor, pg, l, n + 1, t1, c1);
+      w[n >> 1] = (uint32_t)S.xh[t0 * D + c0] | ((uint32_t)S.xh[t1 * D + c1] << 16);
+    }
+    uint4 *o = (uint4 *)(hh + ck * 32);
+    for (int q = 0; q < 4; ++q) o[q] = make_uint4(w[4 * q], w[4 * q + 1], w[4 * q + 2], w[4 * q + 3]);
+  }
+}
+
+// Scalar quantizer, one group per channel (section 3.2).
+__device__ void encode_int(EncodeShared &S, uint8_t *dst, int bits, int tensor) {
+  const double qmax = (double)((1 << bits) - 1);
+  const int tid = threadIdx.x;
+  if (tid < D) {
+    double mn = getx(S, 0, tid), mx = mn;
+    for (int t = 1; t < P; ++t) {
+      const double v = getx(S, t, tid);
+      mn = v < mn ? v : mn;
+      mx = v > mx ? v : mx;
+    }
+    const double range = mx - mn;
+    const uint16_t z = canon_zero(f64_to_f16(mn));
+    const uint16_t s = canon_zero(f64_to_f16(range / qmax));
+    S.z16[tid] = z;
+    S.s16[tid] = s;
+    S.z64[tid] = f16_to_f64(z);
+    S.s64[tid] = f16_to_f64(s);
+  }
+  __syncthreads();
+  for (int i = tid; i < P * D; i += kThreads) {
+    const int t = i >> 7, d = i & 127;
+    const double s = S.s64[d];
+    uint8_t code = 0;
+    if (s != 0.0) {
+      const double diff = getx(S, t, d) - S.z64[d];
+      double r = __builtin_rint(diff / s);
+      r = r < 0.0 ? 0.0 : r;
+      r = r > qmax ? qmax : r;
+      code = (uint8_t)r;
+    }
+    S.codes[t * D + d] = code;
+  }
+  __syncthreads();
+  uint16_t *sz = (uint16_t *)dst;
+  for (int e = tid; e < D; e += kThreads) {
+    const int ch = sz_channel(tensor, e);
+    sz[e] = S.s16[ch];
+    sz[D + e] = S.z16[ch];
+  }
+  uint32_t *w = (uint32_t *)(dst + kSZBytes);
+  for (int ck = tid; ck < 4 * 64; ck += kThreads) {
+    const int pg = ck >> 6, l = ck & 63;
+    uint32_t words[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int n = 0; n < 32; ++n) {
+      int t, ch;
+      chunk_coord(tensor, pg, l, n, t, ch);
+      words[code_word(bits, n)] |= (uint32_t)S.codes[t * D + ch] << code_pos(bits, n);
+    }
+    for (int q = 0; q < bits; ++q) w[ck * bits + q] = words[q];
+  }
+}
+
+// Squared distances of every token to every centroid, channel-ascending, no FMA.
+__device__ void kmeans_dist(EncodeShared &S) {
+  const int t = threadIdx.x >> 2, k = threadIdx.x & 3;  // 256 threads = 64 tokens x 4
+  double acc = 0.0;
+  for (int d = 0; d < D; ++d) {
+    const double diff = getx(S, t, d) - S.c[k * XS + d];
+    const double sq = diff * diff;
+    acc = acc + sq;
+  }
+  S.dist[t * KC + k] = acc;
+  __syncthreads();
+  if (threadIdx.x < P) {
+    const int tt = threadIdx.x;
+    int best = 0;
+    double bd = S.dist[tt * KC];
+    for (int kk = 1; kk < KC; ++kk)
+      if (S.dist[tt * KC + kk] < bd) {
+        bd = S.dist[tt * KC + kk];
+        best = kk;
+      }
+    S.assign[tt] = best;
+  }
+  __syncthreads();
+}
+
+// Deterministic 4-means Lloyd iteration, then fp16 centroids and re-assigned ids.
+__device__ void encode_centroid(EncodeShared &S, uint8_t *dst, int tensor) {
+  const int tid = threadIdx.x;
+  for (int i = tid; i < KC * D; i += kThreads) {
+    const int k = i >> 7, d = i & 127;
+    S.c[k * XS + d] = getx(S, k * (P / KC), d);
+  }
+  __syncthreads();
+  for (int it = 0; it < 10; ++it) {
+    kmeans_dist(S);
+    if (tid == 0) S.flag = 0;
+    __syncthreads();
+    if (it > 0 && tid < P && S.assign[tid] != S.prev[tid]) atomicOr(&S.flag, 1);
+    __syncthreads();
+    if (it > 0 && S.flag == 0) break;  // assignment repeated: converged
+    if (tid < P) S.prev[tid] = S.assign[tid];
+    __syncthreads();
+    for (int i = tid; i < KC * D; i += kThreads) {
+      const int k = i >> 7, d = i & 127;
+      double acc = 0.0;
+      int n = 0;
+      for (int t = 0; t < P; ++t)
+        if (S.assign[t] == k) {
+          acc = acc + getx(S, t, d);
+          ++n;
+        }
+      if (n > 0) S.c[k * XS + d] = acc / (double)n;
+    }
+    __syncthreads();
+  }
+  // round the centroids to fp16 and assign against what is stored
+  uint16_t *cc = (uint16_t *)dst;
+  for (int i = tid; i < KC * D; i += kThreads) {
+    const int k = i >> 7, d = i & 127;
+    const uint16_t h = canon_zero(f64_to_f16(S.c[k * XS + d]));
+    S.c[k * XS + d] = f16_to_f64(h);
+    cc[tensor == GKV_KEYS ? k * D + d : vcent_index(k, d)] = h;
+  }
+  __syncthreads();
+  kmeans_dist(S);
+  if (tid < P / 16) {
+    uint32_t w = 0;
+    for (int j = 0; j < 16; ++j) w |= (uint32_t)S.assign[tid * 16 + j] << (2 * j);
+    ((uint32_t *)(dst + KC * D * 2))[tid] = w;
+  }
+}
+
+__device__ void encode_to(EncodeShared &S, uint8_t *dst, int level, int tensor) {
+  if (level == GKV_EXACT) write_exact(S, dst, tensor);
+  else if (is_int_level(level)) encode_int(S, dst, level, tensor);
+  else encode_centroid(S, dst, tensor);
+}
+
+// Prefill encode: one workgroup per (block, h, b) of one tensor.
+__global__ void __launch_bounds__(kThreads) quantize_kernel(const uint16_t *__restrict__ src, int64_t T_src,
+                                                            const int8_t *__restrict__ level,
+                                                            const int64_t *__restrict__ off, uint8_t *arena,
+                                                            int Hkv, int nblk_cap, int blk0, int tensor) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  EncodeShared &S = *reinterpret_cast<EncodeShared *>(smem);
+  const int blk = blk0 + blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int64_t u = (int64_t)b * Hkv + h;
+  const int lv = level[u * nblk_cap + blk];
+  load_rows(S, src + u * T_src * D, T_src, (int64_t)blk * P);
+  __syncthreads();
+  encode_to(S, arena + off[u * nblk_cap + blk], lv, tensor);
+}
+
+constexpr int kMaxDemoteJobs = 64;
+struct DemoteJobs {
+  int32_t b[kMaxDemoteJobs], h[kMaxDemoteJobs], blk[kMaxDemoteJobs];
+  int8_t to[kMaxDemoteJobs], cur[kMaxDemoteJobs];  // cur from the host mirror: the key
+                                                    // workgroup rewrites the device level
+  int64_t koff[kMaxDemoteJobs], voff[kMaxDemoteJobs];
+};
+
+// Demotion: grid (jobs, 2 tensors).  Reads the current record through the device
+// tables, writes the new record, then points the tables at it.
+__global__ void __launch_bounds__(kThreads) demote_kernel(DemoteJobs jobs, int8_t *level, int64_t *koff,
+                                                          int64_t *voff, uint8_t *arena, int Hkv,
+                                                          int nblk_cap) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  EncodeShared &S = *reinterpret_cast<EncodeShared *>(smem);
+  const int j = blockIdx.x, tensor = blockIdx.y;
+  const int64_t idx = ((int64_t)jobs.b[j] * Hkv + jobs.h[j]) * nblk_cap + jobs.blk[j];
+  const int cur = jobs.cur[j];
+  int64_t *offt = tensor == GKV_KEYS ? koff : voff;
+  const int64_t dst = tensor == GKV_KEYS ? jobs.koff[j] : jobs.voff[j];
+  load_record(S, arena + offt[idx], cur, tensor);
+  __syncthreads();
+  encode_to(S, arena + dst, jobs.to[j], tensor);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    offt[idx] = dst;
+    if (tensor == GKV_KEYS) level[idx] = jobs.to[j];
+  }
+}
+
+// Append one token per (b,h); grid (Hkv, B), 128 threads (one per channel).
+struct NewSlots {
+  int64_t k[GKV_MAX_APPEND_UNITS], v[GKV_MAX_APPEND_UNITS];
+};
+
+__global__ void __launch_bounds__(128) append_kernel(const uint16_t *__restrict__ k_new,
+                                                     const uint16_t *__restrict__ v_new, int8_t *level,
+                                                     int64_t *koff, int64_t *voff, uint8_t *arena,
+                                                     uint16_t *boxes, int64_t npage_cap, int page, int Hkv,
+                                                     int nblk_cap, int64_t T, int open_block, NewSlots slots) {
+  const int h = blockIdx.x, b = blockIdx.y, d = threadIdx.x;
+  const int64_t u = (int64_t)b * Hkv + h;
+  const int blk = (int)(T / P), tok = (int)(T % P);
+  const int64_t ti = u * nblk_cap + blk;
+  int64_t ko, vo;
+  if (open_block) {
+    ko = slots.k[u];
+    vo = slots.v[u];
+    if (d == 0) {
+      level[ti] = GKV_EXACT;
+      koff[ti] = ko;
+      voff[ti] = vo;
+    }
+  } else {
+    ko = koff[ti];
+    vo = voff[ti];
+  }
+  const uint16_t kv = k_new[u * D + d], vv = v_new[u * D + d];
+  // key element (tok, d): page tok>>4, lane ((d>>3)&3)*16 + (tok&15), n = ((d>>5)<<3) | (d&7)
+  {
+    const int pg = tok >> 4, lane = ((d >> 3) & 3) * 16 + (tok & 15), n = ((d >> 5) << 3) | (d & 7);
+    ((uint16_t *)(arena + ko))[(pg * 64 + lane) * 32 + n] = kv;
+  }
+  // value element (tok, d): page tok>>4, lane ((tok>>2)&3)*16 + (d&15), n = ((d>>4)<<2) | (tok&3)
+  {
+    const int pg = tok >> 4, lane = ((tok >> 2) & 3) * 16 + (d & 15), n = ((d >> 4) << 2) | (tok & 3);
+    ((uint16_t *)(arena + vo))[(pg * 64 + lane) * 32 + n] = vv;
+  }
+  if (boxes && ((T + 1) % page) == 0) {
+    // the page just completed lies in this (exact) block; earlier rows were written
+    // by earlier appends, the newest row is still in registers
+    const int64_t p = (T + 1) / page - 1;
+    const int first = tok + 1 - page;
+    _Float16 mn = __builtin_bit_cast(_Float16, kv), mx = mn;
+    const uint16_t *rec = (const uint16_t *)(arena + ko);
+    for (int t = first; t < tok; ++t) {
+      const int pg = t >> 4, lane = ((d >> 3) & 3) * 16 + (t & 15), n = ((d >> 5) << 3) | (d & 7);
+      const _Float16 v = __builtin_bit_cast(_Float16, rec[(pg * 64 + lane) * 32 + n]);
+      mn = v < mn ? v : mn;
+      mx = v > mx ? v : mx;
+    }
+    uint16_t *bx = boxes + u * npage_cap * 2 * D + box_index(p, d);
+    bx[0] = canon_zero(__builtin_bit_cast(uint16_t, mn));
+    bx[1] = canon_zero(__builtin_bit_cast(uint16_t, mx));
+  }
+}
+
+// Page boxes from token-major exact keys; one workgroup per 64 pages of one (b,h).
+__global__ void __launch_bounds__(kThreads) boxes_kernel(const uint16_t *__restrict__ k_src, int64_t T_src,
+                                                         uint16_t *boxes, int64_t npage_cap, int page, int Hkv,
+                                                         int64_t page_begin, int64_t page_end) {
+  __shared__ uint32_t stage[64 * D];  // [channel][page&63] (kmin | kmax << 16)
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int64_t u = (int64_t)b * Hkv + h;
+  const int64_t g0 = (page_begin >> 6) + blockIdx.x;  // box group
+  const int64_t p_lo = g0 * 64;
+  const uint16_t *src = k_src + u * T_src * D;
+  for (int i = threadIdx.x; i < 64 * D; i += kThreads) {
+    const int pi = i >> 7, d = i & 127;
+    const int64_t p = p_lo + pi;
+    if (p < page_begin || p >= page_end) continue;
+    const uint16_t *row = src + p * page * D + d;
+    _Float16 mn = __builtin_bit_cast(_Float16, row[0]), mx = mn;
+    for (int t = 1; t < page; ++t) {
+      const _Float16 v = __builtin_bit_cast(_Float16, row[(int64_t)t * D]);
+      mn = v < mn ? v : mn;
+      mx = v > mx ? v : mx;
+    }
+    stage[d * 64 + pi] = (uint32_t)canon_zero(__builtin_bit_cast(uint16_t, mn)) |
+                         ((uint32_t)canon_zero(__builtin_bit_cast(uint16_t, mx)) << 16);
+  }
+  __syncthreads();
+  uint32_t *out = (uint32_t *)(boxes + u * npage_cap * 2 * D + box_index(p_lo, 0));
+  for (int i = threadIdx.x; i < 64 * D; i += kThreads) {
+    const int pi = i & 63;
+    const int64_t p = p_lo + pi;
+    if (p < page_begin || p >= page_end) continue;
+    out[i] = stage[i];
+  }
+}
+
+// Rate-distortion token scores (section 3.4, Eq. rdscore) of one block:
+// s_t = a_t * sum_d fl(fl(v_td - v_hat_td)^2), channel-ascending, no FMA, written as
+// order-preserving 64-bit keys.  grid (nblk, Hkv, B).
+__global__ void __launch_bounds__(kThreads) rd_score_kernel(const uint16_t *__restrict__ v_src,
+                                                            const float *__restrict__ mass, int64_t T,
+                                                            const int8_t *__restrict__ level,
+                                                            const int64_t *__restrict__ voff,
+                                                            const uint8_t *__restrict__ arena, int Hkv,
+                                                            int nblk_cap, uint64_t *__restrict__ keys) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  EncodeShared &S = *reinterpret_cast<EncodeShared *>(smem);
+  const int blk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int64_t u = (int64_t)b * Hkv + h;
+  const int64_t ti = u * nblk_cap + blk;
+  load_record(S, arena + voff[ti], level[ti], GKV_VALUES);
+  __syncthreads();
+  const int t = threadIdx.x;
+  const int64_t tok = (int64_t)blk * P + t;
+  if (t < P && tok < T) {
+    const uint16_t *row = v_src + (u * T + tok) * D;
+    double e = 0.0;
+    for (int d = 0; d < D; ++d) {
+      const double diff = (double)__builtin_bit_cast(_Float16, row[d]) - getx(S, t, d);
+      const double sq = diff * diff;
+      e = e + sq;
+    }
+    double sc = (double)mass[u * T + tok] * e;
+    sc = sc + 0.0;  // -0 -> +0
+    uint64_t bits;
+    __builtin_memcpy(&bits, &sc, 8);
+    keys[u * T + tok] = (bits >> 63) ? ~bits : (bits | 0x8000000000000000ull);
+  }
+}
+
+}  // namespace
+
+void gkv_launch_rd_score(const gkv_cache *c, const uint16_t *v_src, const float *mass, uint64_t *keys,
+                         hipStream_t stream) {
+  const int nblk = (int)((c->T + P - 1) / P);
+  hipLaunchKernelGGL(rd_score_kernel, dim3(nblk, c->Hkv, c->B), dim3(kThreads), sizeof(EncodeShared), stream, v_src,
+                     mass, c->T, c->level, c->voff, c->arena, c->Hkv, c->nblk_cap, keys);
+}
+
+// ---------------------------------------------------------------- C ABI
+static gkv_status hip_status() { return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP; }
+
+extern "C" gkv_status gkv_quantize_block(const gkv_cache *c, int32_t which, const uint16_t *src, int64_t T_src,
+                                         int32_t blk_begin, int32_t blk_end, void *stream) {
+  gkv_status st = gkv_validate_cache(c);
+  if (st) return st;
+  if (!src || (which != GKV_KEYS && which != GKV_VALUES) || T_src <= 0) return GKV_E_ARG;
+  if (blk_begin < 0 || blk_end > c->nblk_cap || blk_begin > blk_end) return GKV_E_SHAPE;
+  if (blk_begin == blk_end) return GKV_OK;
+  const int64_t *offt_dev = which == GKV_KEYS ? c->koff : c->voff;
+  for (int b = 0; b < c->B; ++b)
+    for (int h = 0; h < c->Hkv; ++h)
+      for (int blk = blk_begin; blk < blk_end; ++blk) {
+        const int lv = c->level_host[((int64_t)b * c->Hkv + h) * c->nblk_cap + blk];
+        if (level_rank(lv) < 0) return GKV_E_ARG;
+        if ((int64_t)(blk + 1) * P > T_src && lv != GKV_EXACT) return GKV_E_SHAPE;
+        if ((int64_t)blk * P >= T_src) return GKV_E_SHAPE;
+      }
+  (void)offt_dev;
+  dim3 grid(blk_end - blk_begin, c->Hkv, c->B);
+  hipLaunchKernelGGL(quantize_kernel, grid, dim3(kThreads), sizeof(EncodeShared), (hipStream_t)stream, src,
+                     T_src, c->level, which == GKV_KEYS ? c->koff : c->voff, c->arena, c->Hkv, c->nblk_cap,
+                     blk_begin, which);
+  return hip_status();
+}
+
+extern "C" gkv_status gkv_demote(gkv_cache *c, int32_t n, const int32_t *jobs, const int8_t *to,
+                                 const int64_t *nk, const int64_t *nv, void *stream) {
+  gkv_status st = gkv_validate_cache(c);
+  if (st) return st;
+  if (n < 0) return GKV_E_ARG;
+  if (n == 0) return GKV_OK;
+  if (!jobs || !to || !nk || !nv) return GKV_E_ARG;
+  const int64_t nblk = (c->T + P - 1) / P;
+  for (int i = 0; i < n; ++i) {
+    const int b = jobs[3 * i], h = jobs[3 * i + 1], blk = jobs[3 * i + 2];
+    if (b < 0 || b >= c->B || h < 0 || h >= c->Hkv || blk < 0 || blk >= nblk) return GKV_E_SHAPE;
+    const int cur = c->level_host[((int64_t)b * c->Hkv + h) * c->nblk_cap + blk];
+    if (level_rank(to[i]) < 0) return GKV_E_ARG;
+    if (level_rank(to[i]) >= level_rank(cur)) return GKV_E_NOT_MONOTONE;
+    if ((int64_t)(blk + 1) * P > c->T) return GKV_E_SHAPE;  // a partial block stays exact
+    const int64_t bb = block_bytes(to[i]);
+    if (nk[i] < 0 || nv[i] < 0 || nk[i] + bb > c->arena_bytes || nv[i] + bb > c->arena_bytes) return GKV_E_ARG;
+    for (int j = 0; j < i; ++j)
+      if (jobs[3 * j] == b && jobs[3 * j + 1] == h && jobs[3 * j + 2] == blk) return GKV_E_ARG;
+  }
+  for (int base = 0; base < n; base += kMaxDemoteJobs) {
+    const int cnt = n - base < kMaxDemoteJobs ? n - base : kMaxDemoteJobs;
+    DemoteJobs J;
+    for (int i = 0; i < cnt; ++i) {
+      J.b[i] = jobs[3 * (base + i)];
+      J.h[i] = jobs[3 * (base + i) + 1];
+      J.blk[i] = jobs[3 * (base + i) + 2];
+      J.to[i] = to[base + i];
+      J.cur[i] = c->level_host[((int64_t)J.b[i] * c->Hkv + J.h[i]) * c->nblk_cap + J.blk[i]];
+      J.koff[i] = nk[base + i];
+      J.voff[i] = nv[base + i];
+    }
+    hipLaunchKernelGGL(demote_kernel, dim3(cnt, 2), dim3(kThreads), sizeof(EncodeShared), (hipStream_t)stream, J,
+                       c->level, c->koff, c->voff, c->arena, c->Hkv, c->nblk_cap);
+    if (hipGetLastError() != hipSuccess) return GKV_E_HIP;
+  }
+  for (int i = 0; i < n; ++i)
+    c->level_host[((int64_t)jobs[3 * i] * c->Hkv + jobs[3 * i + 1]) * c->nblk_cap + jobs[3 * i + 2]] = to[i];
+  return GKV_OK;
+}
+
+extern "C" gkv_status gkv_page_boxes(const gkv_cache *c, const uint16_t *k_src, int64_t T_src,
+                                     int64_t page_begin, int64_t page_end, void *stream) {
+  gkv_status st = gkv_validate_cache(c);
+  if (st) return st;
+  if (!c->page || !k_src) return GKV_E_ARG;
+  if (page_begin < 0 || page_begin > page_end || page_end > c->npage_cap) return GKV_E_SHAPE;
+  if (page_end * c->page > T_src) return GKV_E_SHAPE;
+  if (page_begin == page_end) return GKV_OK;
+  const int64_t g0 = page_begin >> 6, g1 = (page_end + 63) >> 6;
+  dim3 grid((unsigned)(g1 - g0), c->Hkv, c->B);
+  hipLaunchKernelGGL(boxes_kernel, grid, dim3(kThreads), 0, (hipStream_t)stream, k_src, T_src, c->boxes,
+                     c->npage_cap, c->page, c->Hkv, page_begin, page_end);
+  return hip_status();
+}
+
+extern "C" gkv_status gkv_append(gkv_cache *c, const uint16_t *k_new, const uint16_t *v_new,
+                                 const int64_t *new_koff, const int64_t *new_voff, void *stream) {
+  gkv_status st = gkv_validate_cache(c);
+  if (st) return st;
+  if (!k_new || !v_new) return GKV_E_ARG;
+  const int64_t T = c->T;
+  const int blk = (int)(T / P);
+  if (blk >= c->nblk_cap) return GKV_E_SHAPE;
+  const int open = (T % P) == 0;
+  const int64_t units = (int64_t)c->B * c->Hkv;
+  NewSlots slots;
+  if (open) {
+    if (units > GKV_MAX_APPEND_UNITS) return GKV_E_UNSUPPORTED;
+    if (!new_koff || !new_voff) return GKV_E_ARG;
+    for (int64_t u = 0; u < units; ++u) {
+      if (new_koff[u] < 0 || new_voff[u] < 0 || new_koff[u] + kExactBytes > c->arena_bytes ||
+          new_voff[u] + kExactBytes > c->arena_bytes)
+        return GKV_E_ARG;
+      slots.k[u] = new_koff[u];
+      slots.v[u] = new_voff[u];
+    }
+  } else {
+    for (int64_t u = 0; u < units; ++u)
+      if (c->level_host[u * c->nblk_cap + blk] != GKV_EXACT) return GKV_E_ARG;
+  }
+  if (c->page && (T + 1) / c->page > c->npage_cap) return GKV_E_SHAPE;
+  hipLaunchKernelGGL(append_kernel, dim3(c->Hkv, c->B), dim3(128), 0, (hipStream_t)stream, k_new, v_new, c->level,
+                     c->koff, c->voff, c->arena, c->page ? c->boxes : nullptr, c->npage_cap, c->page ? c->page : 1,
+                     c->Hkv, c->nblk_cap, T, open, slots);
+  if (hipGetLastError() != hipSuccess) return GKV_E_HIP;
+  if (open)
+    for (int64_t u = 0; u < (int64_t)c->B * c->Hkv; ++u) c->level_host[u * c->nblk_cap + blk] = GKV_EXACT;
+  c->T = T + 1;
+  return GKV_OK;
+}

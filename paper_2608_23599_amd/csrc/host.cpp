@@ -1,0 +1,298 @@
+// Host-only parts of libgkv: status strings, ladder profiles, the slab arena pool,
+// rate accounting, the record decoder and argument validation.
+#include <stdlib.h>
+#include <string.h>
+
+#include <vector>
+
+#include "gkv_internal.h"
+
+using namespace gkv;
+
+extern "C" const char *gkv_strerror(gkv_status s) {
+  switch (s) {
+    case GKV_OK: return "ok";
+    case GKV_E_ARG: return "invalid argument";
+    case GKV_E_SHAPE: return "shape mismatch";
+    case GKV_E_NOT_MONOTONE: return "demotion is not strictly downwards";
+    case GKV_E_WORKSPACE: return "workspace too small";
+    case GKV_E_HIP: return "HIP runtime error";
+    case GKV_E_UNSUPPORTED: return "unsupported combination";
+  }
+  return "unknown status";
+}
+
+extern "C" int64_t gkv_block_bytes(int32_t level) { return block_bytes(level); }
+
+extern "C" uint16_t gkv_f64_to_f16(double x) { return f64_to_f16(x); }
+
+// ---------------------------------------------------------------- ladder (section 3.2)
+extern "C" gkv_status gkv_ladder_levels(int32_t profile, int64_t T, int8_t *lv, int32_t nblk) {
+  if (!lv || T < 0 || nblk < 0) return GKV_E_ARG;
+  if ((T + P - 1) / P != nblk) return GKV_E_SHAPE;
+  if (profile == 0) {
+    for (int32_t i = 0; i < nblk; ++i) {
+      const int32_t r = nblk - 1 - i;
+      lv[i] = r < 4 ? GKV_EXACT : r < 12 ? GKV_INT8 : r < 24 ? GKV_INT4 : GKV_INT2;
+    }
+    return GKV_OK;
+  }
+  if (profile == 1) {
+    const int64_t E = 16;
+    const int64_t R = nblk > E ? nblk - E : 0;
+    const int64_t b8 = E + (25 * R) / 100, b4 = E + (60 * R) / 100, nc = (10 * (int64_t)nblk) / 100;
+    for (int32_t i = 0; i < nblk; ++i) {
+      const int64_t r = nblk - 1 - i;
+      int8_t v;
+      if (r < E) v = GKV_EXACT;
+      else if (i < nc) v = GKV_CENTROID;
+      else if (r < b8) v = GKV_INT8;
+      else if (r < b4) v = GKV_INT4;
+      else v = GKV_INT2;
+      lv[i] = v;
+    }
+    return GKV_OK;
+  }
+  if (profile == 2) {
+    for (int32_t i = 0; i < nblk; ++i) lv[i] = GKV_EXACT;
+    return GKV_OK;
+  }
+  return GKV_E_ARG;
+}
+
+extern "C" int32_t gkv_ladder_crossings(const gkv_cache *c, int32_t profile, int64_t T_new, int32_t *jobs,
+                                       int8_t *to, int32_t max_jobs) {
+  gkv_status st = gkv_validate_cache(c);
+  if (st) return st;
+  if (!jobs || !to || max_jobs < 0 || T_new < c->T) return GKV_E_ARG;
+  const int32_t nb_new = (int32_t)((T_new + P - 1) / P);
+  if (nb_new > c->nblk_cap) return GKV_E_SHAPE;
+  std::vector<int8_t> lv(nb_new);
+  st = gkv_ladder_levels(profile, T_new, lv.data(), nb_new);
+  if (st) return st;
+  const int64_t nb_old = (c->T + P - 1) / P;
+  int32_t n = 0;
+  for (int b = 0; b < c->B; ++b)
+    for (int h = 0; h < c->Hkv; ++h)
+      for (int64_t i = 0; i < nb_old; ++i) {
+        const int cur = c->level_host[((int64_t)b * c->Hkv + h) * c->nblk_cap + i];
+        if (lv[i] == cur) continue;
+        if (level_rank(lv[i]) > level_rank(cur)) return GKV_E_NOT_MONOTONE;
+        if (n < max_jobs) {
+          jobs[3 * n] = b;
+          jobs[3 * n + 1] = h;
+          jobs[3 * n + 2] = (int32_t)i;
+          to[n] = lv[i];
+        }
+        ++n;
+      }
+  return n;
+}
+
+// ---------------------------------------------------------------- slab pool
+static const int kLevels[5] = {GKV_EXACT, GKV_INT8, GKV_INT4, GKV_INT2, GKV_CENTROID};
+static int level_slot(int level) {
+  for (int i = 0; i < 5; ++i)
+    if (kLevels[i] == level) return i;
+  return -1;
+}
+
+struct gkv_pool {
+  int64_t base[5], cap[5], bytes;
+  std::vector<int64_t> free_list[5];  // slot indices, popped from the back
+  std::vector<uint8_t> used[5];
+  int64_t nused[5];
+};
+
+extern "C" gkv_pool *gkv_pool_create(const int64_t cap[5]) {
+  if (!cap) return nullptr;
+  gkv_pool *p = new gkv_pool();
+  int64_t off = 0;
+  for (int i = 0; i < 5; ++i) {
+    if (cap[i] < 0) {
+      delete p;
+      return nullptr;
+    }
+    p->base[i] = off;
+    p->cap[i] = cap[i];
+    off += cap[i] * block_bytes(kLevels[i]);
+    off = (off + 255) & ~(int64_t)255;
+    p->free_list[i].resize(cap[i]);
+    for (int64_t s = 0; s < cap[i]; ++s) p->free_list[i][s] = cap[i] - 1 - s;  // lowest slot first
+    p->used[i].assign(cap[i], 0);
+    p->nused[i] = 0;
+  }
+  p->bytes = off;
+  return p;
+}
+
+extern "C" int64_t gkv_pool_bytes(const gkv_pool *p) { return p ? p->bytes : -1; }
+
+extern "C" int64_t gkv_pool_alloc(gkv_pool *p, int32_t level) {
+  const int i = level_slot(level);
+  if (!p || i < 0 || p->free_list[i].empty()) return -1;
+  const int64_t s = p->free_list[i].back();
+  p->free_list[i].pop_back();
+  p->used[i][s] = 1;
+  p->nused[i]++;
+  return p->base[i] + s * block_bytes(level);
+}
+
+extern "C" gkv_status gkv_pool_free(gkv_pool *p, int32_t level, int64_t off) {
+  const int i = level_slot(level);
+  if (!p || i < 0) return GKV_E_ARG;
+  const int64_t bb = block_bytes(level);
+  const int64_t rel = off - p->base[i];
+  if (rel < 0 || rel % bb != 0 || rel / bb >= p->cap[i]) return GKV_E_ARG;
+  const int64_t s = rel / bb;
+  if (!p->used[i][s]) return GKV_E_ARG;
+  p->used[i][s] = 0;
+  p->nused[i]--;
+  p->free_list[i].push_back(s);
+  return GKV_OK;
+}
+
+extern "C" int64_t gkv_pool_used(const gkv_pool *p, int32_t level) {
+  const int i = level_slot(level);
+  if (!p || i < 0) return -1;
+  return p->nused[i];
+}
+
+extern "C" void gkv_pool_destroy(gkv_pool *p) { delete p; }
+
+// ---------------------------------------------------------------- validation
+gkv_status gkv_validate_cache(const gkv_cache *c) {
+  if (!c) return GKV_E_ARG;
+  if (c->D != D) return GKV_E_SHAPE;
+  if (c->B <= 0 || c->Hkv <= 0 || c->Hq <= 0 || c->Hq % c->Hkv) return GKV_E_SHAPE;
+  const int G = c->Hq / c->Hkv;
+  if (G < 1 || G > 16) return GKV_E_SHAPE;
+  if (c->T < 0 || c->nblk_cap <= 0) return GKV_E_SHAPE;
+  if ((c->T + P - 1) / P > c->nblk_cap) return GKV_E_SHAPE;
+  if (!c->level || !c->koff || !c->voff || !c->arena || !c->level_host) return GKV_E_ARG;
+  if (c->page) {
+    if (c->page != 16 && c->page != 32 && c->page != 64) return GKV_E_SHAPE;
+    if (!c->boxes || c->npage_cap <= 0 || c->npage_cap % 64) return GKV_E_ARG;
+    if (c->T / c->page > c->npage_cap) return GKV_E_SHAPE;
+  }
+  if (c->nres < 0 || c->nres > c->nres_cap) return GKV_E_SHAPE;
+  if (c->nres_cap > 0 && (!c->res_idx || !c->res_rows || !c->res_mask)) return GKV_E_ARG;
+  return GKV_OK;
+}
+
+// ---------------------------------------------------------------- accounting
+static int64_t row_bits(int level) {
+  if (level == GKV_EXACT) return D * 16;
+  if (is_int_level(level)) return (int64_t)D * level;
+  if (level == GKV_CENTROID) return 2;
+  return 0;
+}
+static int64_t overhead_bits(int level) {
+  if (is_int_level(level)) return D * 2 * 16;
+  if (level == GKV_CENTROID) return KC * D * 16;
+  return 0;
+}
+
+extern "C" gkv_status gkv_account(const gkv_cache *c, const int32_t *pages, int32_t topk, gkv_rates *out) {
+  gkv_status st = gkv_validate_cache(c);
+  if (st) return st;
+  if (!out) return GKV_E_ARG;
+  if (pages && (!c->page || topk <= 0)) return GKV_E_ARG;
+  const int64_t nblk = (c->T + P - 1) / P;
+  const int64_t box_bits = 2 * D * 16;
+  int64_t resident = 0, read = 0;
+  std::vector<uint8_t> touched;
+  for (int b = 0; b < c->B; ++b)
+    for (int h = 0; h < c->Hkv; ++h) {
+      const int8_t *lv = c->level_host + ((int64_t)b * c->Hkv + h) * c->nblk_cap;
+      int64_t graded = 0;
+      for (int64_t i = 0; i < nblk; ++i) graded += 2 * block_bytes(lv[i]) * 8;
+      const int64_t boxes = c->page ? (c->T / c->page) * box_bits : 0;
+      const int64_t res = c->nres ? (int64_t)c->nres * (2 * D * 16 + 32) + nblk * 64 : 0;
+      resident += graded + boxes + res;
+      if (!pages) {
+        read += graded + res;
+        continue;
+      }
+      const int64_t cur = (c->T - 1) / c->page;
+      int64_t r = boxes + res;
+      touched.assign(nblk, 0);
+      const int32_t *pg = pages + ((int64_t)b * c->Hkv + h) * topk;
+      std::vector<int64_t> list;
+      for (int k = 0; k < topk; ++k)
+        if (pg[k] >= 0 && pg[k] != cur) list.push_back(pg[k]);
+      list.push_back(cur);
+      for (int64_t p : list) {
+        const int64_t t0 = p * c->page, t1 = t0 + c->page < c->T ? t0 + c->page : c->T;
+        for (int64_t t = t0; t < t1; ++t) {
+          r += 2 * row_bits(lv[t / P]);
+          touched[t / P] = 1;
+        }
+      }
+      for (int64_t i = 0; i < nblk; ++i)
+        if (touched[i]) r += 2 * overhead_bits(lv[i]);
+      read += r;
+    }
+  out->resident_bits = resident;
+  out->read_bits = read;
+  out->values = (int64_t)c->B * c->Hkv * c->T * 2 * D;
+  return GKV_OK;
+}
+
+// ---------------------------------------------------------------- record decoder
+extern "C" gkv_status gkv_decode_record(int32_t level, int32_t tensor, const uint8_t *rec, double *vals,
+                                       int32_t *codes, uint16_t *scale, uint16_t *zero, int32_t *ids,
+                                       uint16_t *cent) {
+  if (!rec || !vals || (tensor != GKV_KEYS && tensor != GKV_VALUES)) return GKV_E_ARG;
+  if (level == GKV_EXACT) {
+    const uint16_t *h = (const uint16_t *)rec;
+    for (int pg = 0; pg < 4; ++pg)
+      for (int l = 0; l < 64; ++l)
+        for (int n = 0; n < 32; ++n) {
+          int t, ch;
+          chunk_coord(tensor, pg, l, n, t, ch);
+          vals[t * D + ch] = f16_to_f64(h[(pg * 64 + l) * 32 + n]);
+        }
+    return GKV_OK;
+  }
+  if (is_int_level(level)) {
+    const int bits = level;
+    const uint16_t *sz = (const uint16_t *)rec;
+    uint16_t s[D], z[D];
+    for (int e = 0; e < D; ++e) {
+      const int ch = sz_channel(tensor, e);
+      s[ch] = sz[e];
+      z[ch] = sz[D + e];
+    }
+    const uint32_t *w = (const uint32_t *)(rec + kSZBytes);
+    const int wpc = bits;  // 32 codes * bits / 32 bits per word
+    for (int pg = 0; pg < 4; ++pg)
+      for (int l = 0; l < 64; ++l)
+        for (int n = 0; n < 32; ++n) {
+          int t, ch;
+          chunk_coord(tensor, pg, l, n, t, ch);
+          const uint32_t word = w[(pg * 64 + l) * wpc + code_word(bits, n)];
+          const int c = (int)((word >> code_pos(bits, n)) & ((1u << bits) - 1));
+          if (codes) codes[t * D + ch] = c;
+          vals[t * D + ch] = (double)c * f16_to_f64(s[ch]) + f16_to_f64(z[ch]);
+        }
+    if (scale) memcpy(scale, s, sizeof s);
+    if (zero) memcpy(zero, z, sizeof z);
+    return GKV_OK;
+  }
+  if (level == GKV_CENTROID) {
+    const uint16_t *cc = (const uint16_t *)rec;
+    uint16_t cen[KC][D];
+    for (int k = 0; k < KC; ++k)
+      for (int d = 0; d < D; ++d) cen[k][d] = tensor == GKV_KEYS ? cc[k * D + d] : cc[vcent_index(k, d)];
+    const uint8_t *idb = rec + KC * D * 2;
+    for (int t = 0; t < P; ++t) {
+      const int id = (idb[t >> 2] >> (2 * (t & 3))) & 3;
+      if (ids) ids[t] = id;
+      for (int d = 0; d < D; ++d) vals[t * D + d] = f16_to_f64(cen[id][d]);
+    }
+    if (cent) memcpy(cent, cen, sizeof cen);
+    return GKV_OK;
+  }
+  return GKV_E_ARG;
+}

@@ -1,0 +1,248 @@
+"""GPU parity of every call of the C ABI against the CPU oracle, on seeded
+synthetic workloads at sizes the oracle finishes in seconds (several tiles and a
+ragged tail).  Codes, scales, zeros, centroids, ids, boxes, page sets and residual
+sets must be bit-exact; attention outputs within 2e-3 max-abs."""
+import numpy as np
+import pytest
+
+from oracle import fp16 as ofp16, ladder as olad, quest as oquest, residual as ores, cache as ocache, quant as oquant
+from paper_2608_23599_amd import synth
+from tests._util import TOL, kv_all, oracle_units, compare_record, q_group, max_err
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _build(gpu, ks, vs, Hq, levels, **kw):
+    return gpu.GradedCache.build(ks, vs, Hq=Hq, levels=levels, device="cuda", **kw)
+
+
+@pytest.mark.parametrize("T", [2048, 1000])
+def test_tiny_graded_codes_and_attention(gpu, T):
+    """Workload 1 shapes (8 query / 2 KV heads, tiny ladder); T = 1000 leaves a
+    partial exact block and a partial tile."""
+    B_, Hq, Hkv = 1, 8, 2
+    ks, vs = kv_all(1, B_, Hkv, T)
+    lv = olad.ladder("tiny", T)
+    cache = _build(gpu, ks, vs, Hq, lv)
+    ucs = oracle_units(ks, vs, lv)
+    for (b, h), uc in ucs.items():
+        for blk in range(len(lv)):
+            for tensor in (0, 1):
+                compare_record(cache, uc, b, h, blk, tensor)
+    q = synth.queries(1, B_, Hq)
+    out = cache.decode(q).cpu().numpy()
+    G = Hq // Hkv
+    for (b, h), uc in ucs.items():
+        ref = uc.decode_dense(q_group(q, b, h, G))
+        assert max_err(out[b, h * G:(h + 1) * G], ref) <= TOL
+
+
+def test_llama16k_centroids_and_attention(gpu):
+    """Workload 2: 32 query / 8 KV heads, T = 16384, graded ladder with centroids."""
+    B_, Hq, Hkv, T = 1, 32, 8, 16384
+    ks, vs = kv_all(2, B_, Hkv, T)
+    lv = olad.ladder("graded", T)
+    cache = _build(gpu, ks, vs, Hq, lv)
+    ucs = oracle_units(ks, vs, lv)
+    r = np.random.default_rng(0)
+    for (b, h), uc in ucs.items():
+        blks = set(np.nonzero(lv == 1)[0][:6]) | set(r.choice(len(lv), 6, replace=False)) | {len(lv) - 1}
+        for blk in sorted(blks):
+            for tensor in (0, 1):
+                compare_record(cache, uc, b, h, blk, tensor)
+    q = synth.queries(2, B_, Hq)
+    out = cache.decode(q).cpu().numpy()
+    G = Hq // Hkv
+    errs = []
+    for (b, h), uc in ucs.items():
+        ref = uc.decode_dense(q_group(q, b, h, G))
+        errs.append(max_err(out[b, h * G:(h + 1) * G], ref))
+    assert max(errs) <= TOL, errs
+
+
+@pytest.mark.parametrize("T,topk", [(32768, 128), (4001, 64), (1024, 100)])
+def test_quest_boxes_selection_and_sparse_attention(gpu, T, topk):
+    """Workload 3 shapes: exact 16-token page boxes, box-bound top-k (ties to the
+    lower page), attention over selected + current page.  T = 4001 has a partial
+    current page; T = 1024 with top-100 selects every ranked page (= dense)."""
+    B_, Hq, Hkv, page = 1, 32, 8, 16
+    if T < 32768:
+        Hq, Hkv = 8, 2
+    ks, vs = kv_all(3, B_, Hkv, T)
+    lv = olad.ladder("graded", T)
+    cache = _build(gpu, ks, vs, Hq, lv, page=page)
+    G = Hq // Hkv
+    q = synth.queries(3, B_, Hq)
+    pages = cache.quest_select(q, topk)
+    out = cache.decode(q, pages=pages).cpu().numpy()
+    pages = pages.cpu().numpy()
+    for b in range(B_):
+        for h in range(Hkv):
+            kmin, kmax = oquest.page_boxes(ks[b, h])
+            gmin, gmax = cache.boxes_host(b, h, T // page)
+            np.testing.assert_array_equal(gmin, kmin)
+            np.testing.assert_array_equal(gmax, kmax)
+            want = oquest.quest_select(q_group(q, b, h, G), kmin, kmax, T, topk)
+            np.testing.assert_array_equal(pages[b, h], want)
+            uc = ocache.UnitCache(ks[b, h], vs[b, h], lv)
+            ref = uc.decode_quest(q_group(q, b, h, G), want)
+            assert max_err(out[b, h * G:(h + 1) * G], ref) <= TOL
+            if topk >= (T - 1) // page:
+                assert max_err(out[b, h * G:(h + 1) * G], uc.decode_dense(q_group(q, b, h, G))) <= TOL
+
+
+def test_quest_ties_go_to_lower_page(gpu):
+    T, Hq, Hkv = 2048, 4, 1
+    ks, vs = kv_all(31, 1, Hkv, T)
+    ks[0, 0, 64 * 4:64 * 4 + 16] = ks[0, 0, 16:32]          # page 16 duplicates page 1
+    ks[0, 0, 64 * 8:64 * 8 + 48] = ks[0, 0, 64 * 2:64 * 2 + 48]  # pages 32-34 duplicate 8-10
+    lv = olad.ladder("exact", T)
+    cache = _build(gpu, ks, vs, Hq, lv, page=16)
+    q = synth.queries(31, 1, Hq)
+    kmin, kmax = oquest.page_boxes(ks[0, 0])
+    s = oquest.page_scores(q[0], kmin[:127], kmax[:127])
+    for k in range(1, 127, 9):
+        got = cache.quest_select(q, k).cpu().numpy()[0, 0]
+        np.testing.assert_array_equal(got, oquest.select_top(s, k))
+
+
+@pytest.mark.parametrize("T,Bn", [(8192, 2), (3000, 1)])
+def test_rd_residual_selection_and_attention(gpu, T, Bn):
+    """Workload 4 shapes at reduced length: 28 query / 4 KV heads, 2% residual by
+    attention mass x squared value error."""
+    Hq, Hkv = 28, 4
+    ks, vs = kv_all(4, Bn, Hkv, T)
+    lv = olad.ladder("graded", T)
+    n = ores.n_keep(T, 2)
+    cache = _build(gpu, ks, vs, Hq, lv, nres_cap=n)
+    mass = np.stack([np.stack([synth.mass_unit(4, b, h, T) for h in range(Hkv)]) for b in range(Bn)])
+    cache.rd_residual_select(ks, vs, mass, n)
+    q = synth.queries(4, Bn, Hq)
+    out = cache.decode(q).cpu().numpy()
+    idx = cache.res_idx.cpu().numpy()
+    msk = cache.res_mask.cpu().numpy().view(np.uint64)
+    G = Hq // Hkv
+    for b in range(Bn):
+        for h in range(Hkv):
+            uc = ocache.UnitCache(ks[b, h], vs[b, h], lv)
+            want, _ = uc.select_residual(ks[b, h], vs[b, h], mass[b, h], n)
+            np.testing.assert_array_equal(idx[b, h, :n], want)
+            bits = np.zeros(len(lv), dtype=np.uint64)
+            for t in want:
+                bits[t // 64] |= np.uint64(1) << np.uint64(t % 64)
+            np.testing.assert_array_equal(msk[b, h, :len(lv)], bits)
+            ref = uc.decode_dense(q_group(q, b, h, G))
+            assert max_err(out[b, h * G:(h + 1) * G], ref) <= TOL
+
+
+def test_rd_zero_fraction_is_graded(gpu):
+    T, Hq, Hkv = 2048, 4, 1
+    ks, vs = kv_all(41, 1, Hkv, T)
+    lv = olad.ladder("tiny", T)
+    cache = _build(gpu, ks, vs, Hq, lv, nres_cap=64)
+    q = synth.queries(41, 1, Hq)
+    before = cache.decode(q).cpu().numpy()
+    cache.rd_residual_select(ks, vs, np.ones((1, 1, T), np.float32), 0)
+    after = cache.decode(q).cpu().numpy()
+    np.testing.assert_array_equal(before, after)
+
+
+def test_demote_chain_bit_exact(gpu):
+    """gkv_demote: exact -> int8 -> int4 -> int2 -> centroid, each step re-encoding
+    the current record; a promotion is rejected without touching the cache."""
+    T, Hq, Hkv = 512, 4, 2
+    ks, vs = kv_all(51, 1, Hkv, T)
+    lv = olad.ladder("exact", T)
+    cache = _build(gpu, ks, vs, Hq, lv, slack={8: 16, 4: 16, 2: 16, 1: 16})
+    ucs = oracle_units(ks, vs, lv)
+    for to in (8, 4, 2, 1):
+        jobs = [(0, h, blk) for h in range(Hkv) for blk in (1, 3, 6)]
+        cache.demote(jobs, [to] * len(jobs))
+        for (b, h), uc in ucs.items():
+            for blk in (1, 3, 6):
+                uc.k_recs[blk] = oquant.demote(uc.k_recs[blk], to)
+                uc.v_recs[blk] = oquant.demote(uc.v_recs[blk], to)
+                uc.levels[blk] = to
+                compare_record(cache, uc, b, h, blk, 0)
+                compare_record(cache, uc, b, h, blk, 1)
+    with pytest.raises(Exception):
+        cache.demote([(0, 0, 1)], [2])
+    # demote int8 straight to centroid
+    cache.demote([(0, 0, 2)], [8])
+    cache.demote([(0, 0, 2)], [1])
+    uc = ucs[(0, 0)]
+    uc.k_recs[2] = oquant.demote(oquant.demote(uc.k_recs[2], 8), 1)
+    uc.v_recs[2] = oquant.demote(oquant.demote(uc.v_recs[2], 8), 1)
+    uc.levels[2] = 1
+    compare_record(cache, uc, 0, 0, 2, 0)
+    compare_record(cache, uc, 0, 0, 2, 1)
+    q = synth.queries(51, 1, Hq)
+    out = cache.decode(q).cpu().numpy()
+    for (b, h), uc in ucs.items():
+        assert max_err(out[b, 2 * h:2 * h + 2], uc.decode_dense(q_group(q, b, h, 2))) <= TOL
+
+
+def test_append_demote_boxes_and_quest_steps(gpu):
+    """Workload 5 step at a small length: every step appends one token per KV head
+    (boxes of completed pages, new exact block every 64 tokens), demotes the blocks
+    whose level the ladder lowers, selects pages and decodes; all checked against
+    the oracle at every step."""
+    Hq, Hkv, page, topk = 8, 2, 16, 24
+    T0 = 64 * 40 - 3
+    steps = 70
+    ks, vs = kv_all(5, 1, Hkv, T0 + steps)
+    lv = olad.ladder("graded", T0)
+    cache = _build(gpu, ks[:, :, :T0], vs[:, :, :T0], Hq, lv, page=page, extra_blocks=4,
+                   slack={16: 8, 8: 8, 4: 8, 2: 8, 1: 8})
+    ucs = {(0, h): ocache.UnitCache(ks[0, h, :T0], vs[0, h, :T0], lv) for h in range(Hkv)}
+    G = Hq // Hkv
+    for s in range(steps):
+        t = T0 + s
+        moves = cache.append(ks[:, :, t], vs[:, :, t], profile="graded")
+        omoves = []
+        for h in range(Hkv):
+            omoves = ucs[(0, h)].append(ks[0, h, t], vs[0, h, t], "graded")
+        assert sorted((blk, o, n) for b, h, blk, o, n in moves if h == 0) == sorted(omoves)
+        q = synth.queries(5, 1, Hq, step=s)
+        pages = cache.quest_select(q, topk)
+        out = cache.decode(q, pages=pages).cpu().numpy()
+        pages = pages.cpu().numpy()
+        T = t + 1
+        for h in range(Hkv):
+            uc = ucs[(0, h)]
+            kmin, kmax = oquest.page_boxes(ks[0, h, :T])
+            want = oquest.quest_select(q_group(q, 0, h, G), kmin, kmax, T, topk)
+            np.testing.assert_array_equal(pages[0, h], want)
+            ref = uc.decode_quest(q_group(q, 0, h, G), want)
+            assert max_err(out[0, h * G:(h + 1) * G], ref) <= TOL
+            for b_, h_, blk, o, n in moves:
+                if h_ == h:
+                    compare_record(cache, uc, 0, h, blk, 0)
+                    compare_record(cache, uc, 0, h, blk, 1)
+        dense = cache.decode(q).cpu().numpy()
+        for h in range(Hkv):
+            assert max_err(dense[0, h * G:(h + 1) * G], ucs[(0, h)].decode_dense(q_group(q, 0, h, G))) <= TOL
+    assert T > T0 + 64
+
+
+def test_constant_channel_and_equal_rows(gpu):
+    """Degenerate blocks: constant channels (scale 0, codes 0) and identical rows
+    (every centroid equal, ties to centroid 0)."""
+    T, Hq, Hkv = 256, 4, 1
+    ks, vs = kv_all(61, 1, Hkv, T)
+    ks[0, 0, :, 5] = ofp16.from_f64(np.array([1.5]))[0]
+    vs[0, 0, 64:128] = vs[0, 0, 64]
+    ks[0, 0, 128:192] = ks[0, 0, 130]
+    lv = np.array([2, 1, 1, 16], dtype=np.int8)
+    cache = _build(gpu, ks, vs, Hq, lv)
+    uc = ocache.UnitCache(ks[0, 0], vs[0, 0], lv)
+    for blk in range(4):
+        compare_record(cache, uc, 0, 0, blk, 0)
+        compare_record(cache, uc, 0, 0, blk, 1)
+    q = synth.queries(61, 1, Hq)
+    assert max_err(cache.decode(q).cpu().numpy()[0], uc.decode_dense(q[0])) <= TOL

@@ -1,0 +1,264 @@
+"""Host-side checks of the C ABI (no GPU needed): exported symbols, ladder,
+ladder crossings, slab pool, accounting, the packed-record decoder and argument
+validation.  Expected values come from the oracle or from the layout as the
+header documents it."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import accounting as oacc, fp16 as ofp16, ladder as olad, quant as oquant
+from paper_2608_23599_amd import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gkv.h")
+
+
+@pytest.fixture(scope="module")
+def B():
+    from paper_2608_23599_amd import binding
+    return binding
+
+
+def test_library_exports_every_declared_symbol(B):
+    text = open(HEADER).read()
+    decl = set(re.findall(r"^\s*(?:const\s+)?[\w\s\*]*?\b(gkv_\w+)\s*\(", text, re.M))
+    assert len(decl) >= 20
+    for name in decl:
+        assert hasattr(B.lib, name), name
+    assert decl == set(B.EXPORTED)
+
+
+def test_f64_to_f16_matches_single_rounding(B):
+    r = np.random.default_rng(5)
+    xs = np.concatenate([
+        r.standard_normal(3000) * 10.0 ** r.integers(-9, 5, 3000),
+        (r.integers(-2048, 2048, 500) + 0.5) * 2.0 ** r.integers(-24, 6, 500),
+        [1 + 2.0 ** -11 + 2.0 ** -40, 1 + 2.0 ** -11, 65519.9, 65520.0, 2.0 ** -25, 2.0 ** -25 * 1.0001, 0.0],
+    ])
+    want = xs.astype(np.float16).view(np.uint16)
+    got = np.array([B.f64_to_f16(x) for x in xs], dtype=np.uint16)
+    assert np.array_equal(got, want)
+    assert B.f64_to_f16(-0.0) == 0x8000  # the raw conversion keeps the sign; stores canonicalise
+
+
+@pytest.mark.parametrize("profile,T", [("tiny", 2048), ("tiny", 1000), ("graded", 16384), ("graded", 131072),
+                                       ("graded", 1048576 + 64), ("graded", 5000), ("exact", 300)])
+def test_ladder_matches_oracle(B, profile, T):
+    assert np.array_equal(B.ladder_levels(profile, T), olad.ladder(profile, T))
+
+
+def test_block_bytes(B):
+    for L in B.LEVELS:
+        assert B.block_bytes(L) * 8 == oacc.block_bits(L)
+    assert B.block_bytes(3) == 0
+
+
+def _host_cache(B, Bn, Hkv, Hq, T, levels, page=0, nres=0):
+    """A gkv_cache whose device pointers are host buffers (host-only calls never
+    dereference them)."""
+    nblk = (T + 63) // 64
+    keep = {}
+    c = B.CacheStruct()
+    c.B, c.Hkv, c.Hq, c.D, c.T, c.nblk_cap = Bn, Hkv, Hq, 128, T, nblk + 4
+    lv = np.zeros((Bn, Hkv, nblk + 4), dtype=np.int8)
+    lv[:, :, :nblk] = levels
+    keep["lv"] = lv
+    for name in ("level", "koff", "voff", "arena"):
+        a = np.zeros(64, dtype=np.int64)
+        keep[name] = a
+        setattr(c, name, a.ctypes.data)
+    c.arena_bytes = 1 << 30
+    c.level_host = lv.ctypes.data
+    if page:
+        bx = np.zeros(16, dtype=np.int64)
+        keep["boxes"] = bx
+        c.page, c.npage_cap, c.boxes = page, ((T // page) + 63) // 64 * 64 + 64, bx.ctypes.data
+    if nres:
+        for name in ("res_idx", "res_rows", "res_mask"):
+            a = np.zeros(8, dtype=np.int64)
+            keep[name] = a
+            setattr(c, name, a.ctypes.data)
+        c.nres = c.nres_cap = nres
+    return c, keep
+
+
+@pytest.mark.parametrize("T,page,nres,sel", [(2048, 0, 0, None), (16384, 0, 0, None), (131072, 0, 2621, None),
+                                             (32768, 16, 0, 128), (5000, 16, 0, 40), (16384, 64, 0, 32)])
+def test_account_matches_oracle(B, T, page, nres, sel):
+    prof = "tiny" if T == 2048 else "graded"
+    lv = olad.ladder(prof, T)
+    c, keep = _host_cache(B, 1, 2, 8, T, lv, page=page, nres=nres)
+    pages = None
+    if sel:
+        r = np.random.default_rng(T)
+        cur = (T - 1) // page
+        pages = np.full((1, 2, sel), -1, dtype=np.int32)
+        for h in range(2):
+            pick = np.sort(r.choice(cur, size=min(sel, cur), replace=False))
+            pages[0, h, :len(pick)] = pick
+    rates = B.Rates()
+    st = B._account(ctypes.byref(c), B._np_ptr(pages) if pages is not None else None, sel or 0, ctypes.byref(rates))
+    assert st == 0
+    res, rd = 0, 0
+    for h in range(2):
+        o = oacc.unit_rates(lv, T, page=page or None, nres=nres, pages=None if pages is None else pages[0, h])
+        res += o["resident_bits"]
+        rd += o["read_bits"]
+    assert rates.resident_bits == res and rates.read_bits == rd
+    assert rates.values == 2 * T * 2 * 128
+
+
+def test_ladder_crossings_and_monotone_rejection(B):
+    T = 36 * 64
+    lv = olad.ladder("graded", T)
+    c, keep = _host_cache(B, 1, 2, 8, T, lv)
+    jobs = np.zeros(3 * 64, dtype=np.int32)
+    to = np.zeros(64, dtype=np.int8)
+    n = B._ladder_crossings(ctypes.byref(c), 1, T + 1, B._np_ptr(jobs), B._np_ptr(to), 64)
+    want = olad.crossings("graded", T, T + 1)
+    assert n == 2 * len(want) and n > 0
+    got = sorted((int(jobs[3 * i + 2]), int(to[i])) for i in range(n) if jobs[3 * i + 1] == 0)
+    assert got == sorted((b, new) for b, old, new in want)
+    # a ladder that would promote a block is rejected
+    keep["lv"][:, :, 0] = olad.CENTROID
+    keep["lv"][:, :, 1:36] = olad.INT2
+    n = B._ladder_crossings(ctypes.byref(c), 2, T + 1, B._np_ptr(jobs), B._np_ptr(to), 64)
+    assert n == -3
+
+
+def test_demote_validation_runs_before_launch(B):
+    T = 2048
+    lv = olad.ladder("tiny", T)
+    c, keep = _host_cache(B, 1, 1, 4, T, lv)
+    jobs = np.array([0, 0, 31], dtype=np.int32)       # block 31 is exact
+    nk = np.array([0], dtype=np.int64)
+    for to, want in ((16, -3), (8, None)):
+        t = np.array([to], dtype=np.int8)
+        st = B._demote(ctypes.byref(c), 1, B._np_ptr(jobs), B._np_ptr(t), B._np_ptr(nk), B._np_ptr(nk), None)
+        if want is not None:
+            assert st == want
+    j2 = np.array([0, 0, 0], dtype=np.int32)          # block 0 is int2: int4 would promote
+    t = np.array([4], dtype=np.int8)
+    assert B._demote(ctypes.byref(c), 1, B._np_ptr(j2), B._np_ptr(t), B._np_ptr(nk), B._np_ptr(nk), None) == -3
+    c.D = 64
+    assert B._demote(ctypes.byref(c), 1, B._np_ptr(j2), B._np_ptr(t), B._np_ptr(nk), B._np_ptr(nk), None) == -2
+
+
+def test_call_validation_errors(B):
+    T = 2048
+    c, keep = _host_cache(B, 1, 2, 8, T, olad.ladder("tiny", T), page=16)
+    ws = np.zeros(8, dtype=np.int64)
+    q = np.zeros(8 * 128, dtype=np.uint16)
+    pages = np.zeros(16, dtype=np.int32)
+    out = np.zeros(8 * 128, dtype=np.float32)
+    # top-k of zero, null pointers, undersized workspace
+    assert B._quest_select(B._np_ptr(q), ctypes.byref(c), 0, B._np_ptr(pages), B._np_ptr(ws), 64, None) == -1
+    assert B._quest_select(None, ctypes.byref(c), 4, B._np_ptr(pages), B._np_ptr(ws), 64, None) == -1
+    assert B._quest_select(B._np_ptr(q), ctypes.byref(c), 4, B._np_ptr(pages), B._np_ptr(ws), 64, None) == -4
+    assert B._attn(B._np_ptr(q), ctypes.byref(c), None, 0, B._np_ptr(out), B._np_ptr(ws), 64, None) == -4
+    # quantize: an int block may not extend past the source rows
+    src = np.zeros(16, dtype=np.uint16)
+    assert B._quantize_block(ctypes.byref(c), 0, B._np_ptr(src), 1000, 0, 32, None) == -2
+    # G > 16 and a non-dividing head count
+    c.Hq = 34
+    assert B._attn(B._np_ptr(q), ctypes.byref(c), None, 0, B._np_ptr(out), B._np_ptr(ws), 1 << 30, None) == -2
+    c.Hq = 64
+    assert B._attn(B._np_ptr(q), ctypes.byref(c), None, 0, B._np_ptr(out), B._np_ptr(ws), 1 << 30, None) == -2
+
+
+def test_pool_slots(B):
+    p = B.Pool({16: 2, 8: 3, 1: 1})
+    offs = [p.alloc(8) for _ in range(3)]
+    assert len(set(offs)) == 3 and all(o % 16 == 0 for o in offs)
+    with pytest.raises(B.GkvError):
+        p.alloc(8)
+    p.free(8, offs[1])
+    assert p.alloc(8) == offs[1]
+    with pytest.raises(B.GkvError):
+        p.free(8, offs[0] + 1)
+    assert p.used(8) == 3 and p.used(16) == 0
+    e = [p.alloc(16), p.alloc(16)]
+    c = p.alloc(1)
+    spans = sorted([(o, o + B.block_bytes(8)) for o in offs] + [(o, o + 16384) for o in e] + [(c, c + 1040)])
+    assert all(a[1] <= b[0] for a, b in zip(spans, spans[1:]))
+    assert p.bytes >= spans[-1][1]
+
+
+# ---------------------------------------------------------------- record layout
+def _pack(level, tensor, rec):
+    """Pack an oracle record into the byte layout the header documents
+    (independent of the library's own packer)."""
+    out = bytearray(B_bytes(level))
+
+    def coord(pg, l, n):
+        kg, m = l >> 4, l & 15
+        if tensor == 0:
+            return 16 * pg + m, 32 * (n >> 3) + 8 * kg + (n & 7)
+        return 16 * pg + 4 * kg + (n & 3), 16 * (n >> 2) + m
+
+    if level == 16:
+        a = np.frombuffer(out, dtype=np.uint16) if False else np.zeros(8192, dtype=np.uint16)
+        for pg in range(4):
+            for l in range(64):
+                for n in range(32):
+                    t, ch = coord(pg, l, n)
+                    a[(pg * 64 + l) * 32 + n] = rec.exact[t, ch]
+        return a.tobytes()
+    if level in (8, 4, 2):
+        bits = level
+        pos4 = [4, 20, 12, 28, 0, 16, 8, 24]
+        pos2 = [8, 24, 14, 30, 6, 22, 12, 28, 4, 20, 10, 26, 0, 16, 2, 18]
+        sz = np.zeros(256, dtype=np.uint16)
+        for e in range(128):
+            kg, n = e >> 5, e & 31
+            ch = 32 * (n >> 3) + 8 * kg + (n & 7) if tensor == 0 else 16 * (n >> 2) + 4 * kg + (n & 3)
+            sz[e] = rec.s16[ch]
+            sz[128 + e] = rec.z16[ch]
+        words = np.zeros(256 * bits, dtype=np.uint32)
+        for pg in range(4):
+            for l in range(64):
+                for n in range(32):
+                    t, ch = coord(pg, l, n)
+                    c = int(rec.codes[t, ch])
+                    if bits == 8:
+                        w, p = n >> 2, 8 * (n & 3)
+                    elif bits == 4:
+                        w, p = n >> 3, pos4[n & 7]
+                    else:
+                        w, p = n >> 4, pos2[n & 15]
+                    words[(pg * 64 + l) * bits + w] |= np.uint32(c << p)
+        return sz.tobytes() + words.tobytes()
+    cen = np.zeros(512, dtype=np.uint16)
+    for k in range(4):
+        for d in range(128):
+            idx = k * 128 + d if tensor == 0 else ((d & 15) * 8 + (d >> 4)) * 4 + k
+            cen[idx] = rec.cent16[k, d]
+    ids = np.zeros(16, dtype=np.uint8)
+    for t in range(64):
+        ids[t >> 2] |= np.uint8(int(rec.ids[t]) << (2 * (t & 3)))
+    return cen.tobytes() + ids.tobytes()
+
+
+def B_bytes(level):
+    return oacc.block_bits(level) // 8
+
+
+@pytest.mark.parametrize("level", [16, 8, 4, 2, 1])
+@pytest.mark.parametrize("tensor", [0, 1])
+def test_decode_record_reads_documented_layout(B, level, tensor):
+    k, v = synth.kv_unit(300 + level, 0, 0, 64)
+    rec = oquant.encode_fp16(level, k if tensor == 0 else v)
+    raw = _pack(level, tensor, rec)
+    assert len(raw) == B.block_bytes(level)
+    d = B.decode_record(level, tensor, raw)
+    np.testing.assert_array_equal(d["values"], oquant.decode(rec))
+    if level in (8, 4, 2):
+        np.testing.assert_array_equal(d["codes"], rec.codes)
+        np.testing.assert_array_equal(d["s16"], rec.s16)
+        np.testing.assert_array_equal(d["z16"], rec.z16)
+    if level == 1:
+        np.testing.assert_array_equal(d["ids"], rec.ids)
+        np.testing.assert_array_equal(d["cent16"], rec.cent16)
