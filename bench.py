@@ -1,0 +1,278 @@
+#!/usr/bin/env python3
+"""Decode-attention benchmark on one MI355X.
+
+Headline: single-query GQA decode attention over the graded + exact-residual
+cache at 128k context (Qwen2.5-7B-shaped layer: 28 query / 4 KV heads, head dim
+128, batch 8, 64-token blocks, 2% residual), reported as microseconds per decode
+step, achieved HBM GB/s on the bytes the step must read (the paper's read-rate
+accounting) as a fraction of the 8 TB/s peak, and read / resident bits per value.
+Two identical cache copies are alternated so the 256 MB Infinity Cache cannot
+serve a repeat.  The other rows of the hot path (block quantization and centroid
+encoding, residual selection, demotion, page boxes, Compressed-Quest selection and
+sparse attention at 128k) are timed once each and reported under "phases".
+
+Prints ONE JSON line.  Only one GPU is supported: --gpus N > 1 exits.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "decode-attn µs/step + achieved HBM GB/s (% peak) at 128k ctx; read bits/value"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def gen_inputs(wl_id, B, Hkv, T, device):
+    """Seeded fp16 keys/values [B][Hkv][T][128] on the device, generated per unit."""
+    import numpy as np
+    import torch
+    from paper_2608_23599_amd import synth
+    k = torch.empty((B, Hkv, T, 128), dtype=torch.int16, device=device)
+    v = torch.empty((B, Hkv, T, 128), dtype=torch.int16, device=device)
+    for b in range(B):
+        for h in range(Hkv):
+            kb, vb = synth.kv_unit(wl_id, b, h, T)
+            k[b, h].copy_(torch.from_numpy(kb.view(np.int16)))
+            v[b, h].copy_(torch.from_numpy(vb.view(np.int16)))
+    return k, v
+
+
+def timed(fn, n=1):
+    """Run fn n times between two events on the current stream; returns ms per call."""
+    import torch
+    s = torch.cuda.Event(enable_timing=True)
+    e = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    s.record()
+    for _ in range(n):
+        fn()
+    e.record()
+    torch.cuda.synchronize()
+    return s.elapsed_time(e) / n
+
+
+def step_loop(caches, qs, outs, steps, warmup, pages=None):
+    """Warmup, then `steps` timed decode steps with one event pair each."""
+    import numpy as np
+    import torch
+    nc = len(caches)
+    for i in range(warmup):
+        caches[i % nc].decode(qs[i % len(qs)], pages=None if pages is None else pages[i % nc], out=outs[i % nc])
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for i in range(steps):
+        ev[i][0].record()
+        caches[i % nc].decode(qs[i % len(qs)], pages=None if pages is None else pages[i % nc], out=outs[i % nc])
+        ev[i][1].record()
+    t1.record()
+    torch.cuda.synchronize()
+    per = np.array([a.elapsed_time(b) for a, b in ev]) * 1e3  # us
+    total_ms = t0.elapsed_time(t1)
+    return per, total_ms
+
+
+def cpu_oracle_sample(ks_unit, vs_unit, lv, mass, nres, q_group, out_gpu):
+    """Time the plain oracle on one (b, KV head) unit of the workload (dequantize
+    every block, apply the residual, attend) and check the GPU output of that unit."""
+    import numpy as np
+    from oracle import cache as ocache
+    from threadpoolctl import threadpool_limits
+    with threadpool_limits(limits=1):
+        uc = ocache.UnitCache(ks_unit, vs_unit, lv)
+        uc.select_residual(ks_unit, vs_unit, mass, nres)
+        t0 = time.perf_counter()
+        ref = uc.decode_dense(q_group)
+        dt = time.perf_counter() - t0
+    err = float(np.abs(out_gpu.astype(np.float64) - ref).max())
+    return dt, err
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--no-phases", action="store_true", help="skip the one-off timings of the other rows")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-quest", action="store_true", help="skip the Compressed-Quest 128k point")
+    ap.add_argument("--profile", action="store_true",
+                    help="decode loop only, then a plain 512 MiB device copy as a counter reference")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the decode path runs per (sequence, KV head) on a single "
+              "MI355X and this build has no multi-GPU path (see DESIGN.md, 'How it would shard').",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2608_23599_amd import binding as gkv, synth, workloads
+    from oracle import ladder as olad, residual as ores
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = workloads.RD128K
+    B, Hq, Hkv, T = wl.B, wl.Hq, wl.Hkv, wl.T
+    G = Hq // Hkv
+    log(f"[bench] generating {wl.name}")
+    t0 = time.time()
+    k, v = gen_inputs(wl.id, B, Hkv, T, dev)
+    lv = olad.ladder("graded", T)
+    nres = ores.n_keep(T, wl.rd_percent)
+    mass = np.stack([np.stack([synth.mass_unit(wl.id, b, h, T) for h in range(Hkv)]) for b in range(B)])
+    mass_d = torch.from_numpy(mass).to(dev)
+    log(f"[bench] inputs ready in {time.time() - t0:.1f}s; building caches")
+    phases = {}
+    caches = []
+    for c in range(2):
+        cache = gkv.GradedCache(B, Hkv, Hq, T, len(lv), {L: 2 * B * Hkv * int((lv == L).sum()) for L in gkv.LEVELS},
+                                nres_cap=nres, device=dev)
+        for b in range(B):
+            for h in range(Hkv):
+                for i in range(len(lv)):
+                    cache.level_host[b, h, i] = lv[i]
+                    cache.koff_host[b, h, i] = cache.pool.alloc(int(lv[i]))
+                    cache.voff_host[b, h, i] = cache.pool.alloc(int(lv[i]))
+        cache._upload_tables()
+        qms = timed(lambda: (cache.quantize_block(gkv.KEYS, k, 0, len(lv)),
+                             cache.quantize_block(gkv.VALUES, v, 0, len(lv))))
+        rms = timed(lambda: cache.rd_residual_select(k, v, mass_d, nres))
+        if c == 1:
+            phases["quantize_all_blocks_ms"] = round(qms, 3)
+            phases["rd_residual_select_ms"] = round(rms, 3)
+        caches.append(cache)
+    rates = caches[0].account()
+    alg_bytes = rates["read_bits"] / 8.0
+    qs = [torch.from_numpy(synth.queries(wl.id, B, Hq, step=s).view(np.int16)).to(dev) for s in range(4)]
+    outs = [torch.empty((B, Hq, 128), dtype=torch.float32, device=dev) for _ in range(2)]
+    log(f"[bench] decode loop: {args.warmup} warmup + {args.steps} timed steps")
+    per, total_ms = step_loop(caches, qs, outs, args.steps, args.warmup)
+    med, p90 = float(np.median(per)), float(np.percentile(per, 90))
+    mean_us = float(per.mean())
+    gbps = alg_bytes / (mean_us * 1e-6) / 1e9
+    log(f"[bench] median {med:.1f} us, p90 {p90:.1f} us, mean {mean_us:.1f} us, {gbps:.0f} GB/s")
+
+    if args.profile:
+        # reference for hardware byte counters: one device-to-device copy of 512 MiB
+        src = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        args.no_cpu = args.no_phases = args.no_quest = True
+
+    # parity of the benchmarked launch on one sampled unit, and the CPU baseline
+    cpu = None
+    caches[0].decode(qs[0], out=outs[0])
+    torch.cuda.synchronize()
+    out0 = outs[0].cpu().numpy()
+    if not args.no_cpu:
+        log("[bench] oracle sample (1 unit)")
+        ks0, vs0 = synth.kv_unit(wl.id, 0, 0, T)
+        q0 = synth.queries(wl.id, B, Hq, step=0)[0, 0:G]
+        dt, err = cpu_oracle_sample(ks0, vs0, lv, mass[0, 0], nres, q0, out0[0, 0:G])
+        if err > 2e-3:
+            log(f"[bench] PARITY FAILURE on unit (0,0): max abs err {err}")
+            sys.exit(1)
+        units = B * Hkv
+        cpu = {"value": round(dt * units * 1e6, 1), "unit": "us/step", "cores": 1, "kind": "oracle",
+               "sample": f"1 of {units} (sequence, KV head) units (dequantize + residual + fp64 attention), "
+                         f"scaled x{units}; max abs err of the GPU unit vs oracle {err:.2e}"}
+
+    if not args.no_phases:
+        # demotion: 32 blocks (one per (b, KV head)) exact -> int8, then int8 -> centroid,
+        # on a small all-exact cache with room for the new slots
+        small = gkv.GradedCache.build(k[:, :, :64 * 64], v[:, :, :64 * 64], Hq=Hq,
+                                      levels=np.full(64, gkv.EXACT, np.int8), device=dev,
+                                      slack={gkv.INT8: 64, gkv.INT4: 64, gkv.INT2: 64, gkv.CENTROID: 64})
+        j8 = [(b, h, 10) for b in range(B) for h in range(Hkv)]
+        phases["demote_exact_to_int8_32blocks_us"] = round(timed(lambda: small.demote(j8, [8] * len(j8))) * 1e3, 1)
+        jc = [(b, h, 10) for b in range(B) for h in range(Hkv)]
+        phases["demote_int8_to_centroid_32blocks_us"] = round(timed(lambda: small.demote(jc, [1] * len(jc))) * 1e3, 1)
+        ta = time.perf_counter()
+        for _ in range(100):
+            caches[0].account()
+        phases["accounting_host_us"] = round((time.perf_counter() - ta) / 100 * 1e6, 1)
+        del small
+
+    quest = None
+    if not args.no_quest:
+        wq = workloads.QUEST128K
+        log(f"[bench] {wq.name}")
+        del k, v
+        torch.cuda.empty_cache()
+        kq, vq = gen_inputs(wq.id, wq.B, wq.Hkv, wq.T, dev)
+        lvq = olad.ladder("graded", wq.T)
+        qc = gkv.GradedCache.build(kq, vq, Hq=wq.Hq, levels=lvq, page=wq.page, device=dev)
+        bms = timed(lambda: qc.page_boxes(kq, 0, wq.T // wq.page))
+        qq = torch.from_numpy(synth.queries(wq.id, wq.B, wq.Hq).view(np.int16)).to(dev)
+        # rotate enough identical copies that the step working set exceeds the Infinity Cache
+        copies = [qc] + [qc.clone() for _ in range(11)]
+        pages = [torch.empty((wq.B, wq.Hkv, wq.topk), dtype=torch.int32, device=dev) for _ in copies]
+        qouts = [torch.empty((wq.B, wq.Hq, 128), dtype=torch.float32, device=dev) for _ in copies]
+        n = len(copies)
+        for i in range(10):
+            copies[i % n].quest_select(qq, wq.topk, out=pages[i % n])
+            copies[i % n].decode(qq, pages=pages[i % n], out=qouts[i % n])
+        sel_ms = timed(lambda: [copies[i].quest_select(qq, wq.topk, out=pages[i]) for i in range(n)], 1) / n
+        att_ms = timed(lambda: [copies[i].decode(qq, pages=pages[i], out=qouts[i]) for i in range(n)], 1) / n
+        ev_ms = timed(lambda: [(copies[i].quest_select(qq, wq.topk, out=pages[i]),
+                                copies[i].decode(qq, pages=pages[i], out=qouts[i])) for i in range(n)], 1) / n
+        r = qc.account(pages[0])
+        qbytes = r["read_bits"] / 8.0
+        quest = {"workload": wq.name, "us_per_step": round(ev_ms * 1e3, 2), "select_us": round(sel_ms * 1e3, 2),
+                 "attn_us": round(att_ms * 1e3, 2), "read_bpv": round(r["read_bpv"], 4),
+                 "resident_bpv": round(r["resident_bpv"], 4), "algorithmic_bytes": int(qbytes),
+                 "achieved_GBps": round(qbytes / (ev_ms * 1e-3) / 1e9, 1),
+                 "page_boxes_all_ms": round(bms, 3), "cache_copies_rotated": n}
+        log(f"[bench] quest 128k: {quest['us_per_step']} us/step")
+
+    res = {
+        "metric": METRIC,
+        "value": round(med, 2),
+        "unit": "us/step",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(total_ms / args.steps, 5),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "B": B, "Hq": Hq, "Hkv": Hkv, "T": T, "block": 64,
+                   "residual_percent": wl.rd_percent, "ladder": "graded (16 exact / 25-35-40% int8-int4-int2 / 10% centroid)",
+                   "cache_copies_rotated": 2},
+        "p50_us": round(med, 2),
+        "p90_us": round(p90, 2),
+        "mean_us": round(mean_us, 2),
+        "achieved_GBps": round(gbps, 1),
+        "pct_hbm_peak": round(100 * gbps / HBM_PEAK_GBPS, 2),
+        "read_bpv": round(rates["read_bpv"], 4),
+        "resident_bpv": round(rates["resident_bpv"], 4),
+        "algorithmic_bytes_per_step": int(alg_bytes),
+        "roofline": {"bound": "hbm", "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "kernel": "attn_kernel (one launch per step)"},
+        "cpu_baseline": cpu,
+        "phases": phases,
+        "quest_128k": quest,
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -210,24 +210,45 @@ class GradedCache:
         else:
             self.res_idx = self.res_rows = self.res_mask = None
         self.c = CacheStruct()
-        self.c.B, self.c.Hkv, self.c.Hq, self.c.D = B, Hkv, Hq, D
-        self.c.T = T
-        self.c.nblk_cap = nblk_cap
-        self.c.level = self.level.data_ptr()
-        self.c.koff = self.koff.data_ptr()
-        self.c.voff = self.voff.data_ptr()
-        self.c.arena = self.arena.data_ptr()
-        self.c.arena_bytes = self.arena.numel()
-        self.c.level_host = self.level_host.ctypes.data
-        self.c.page = page
-        self.c.npage_cap = npage_cap
-        self.c.boxes = self.boxes.data_ptr() if self.boxes is not None else None
-        self.c.nres = 0
-        self.c.nres_cap = nres_cap
-        self.c.res_idx = self.res_idx.data_ptr() if nres_cap else None
-        self.c.res_rows = self.res_rows.data_ptr() if nres_cap else None
-        self.c.res_mask = self.res_mask.data_ptr() if nres_cap else None
+        self._bind(T, 0)
         self._ws = {}
+
+    def _bind(self, T, nres):
+        c = self.c
+        c.B, c.Hkv, c.Hq, c.D = self.B, self.Hkv, self.Hq, D
+        c.T = T
+        c.nblk_cap = self.nblk_cap
+        c.level = self.level.data_ptr()
+        c.koff = self.koff.data_ptr()
+        c.voff = self.voff.data_ptr()
+        c.arena = self.arena.data_ptr()
+        c.arena_bytes = self.arena.numel()
+        c.level_host = self.level_host.ctypes.data
+        c.page = self.page
+        c.npage_cap = self.npage_cap
+        c.boxes = self.boxes.data_ptr() if self.boxes is not None else None
+        c.nres = nres
+        c.nres_cap = self.nres_cap
+        c.res_idx = self.res_idx.data_ptr() if self.nres_cap else None
+        c.res_rows = self.res_rows.data_ptr() if self.nres_cap else None
+        c.res_mask = self.res_mask.data_ptr() if self.nres_cap else None
+
+    def clone(self):
+        """A read-only copy in separate device memory (same layout and offsets), for
+        benchmarks that rotate identical caches; it cannot append or demote."""
+        new = object.__new__(GradedCache)
+        new.__dict__.update(self.__dict__)
+        for name in ("arena", "level", "koff", "voff", "boxes", "res_idx", "res_rows", "res_mask"):
+            t = getattr(self, name)
+            setattr(new, name, t.clone() if t is not None else None)
+        new.level_host = self.level_host.copy()
+        new.koff_host = self.koff_host.copy()
+        new.voff_host = self.voff_host.copy()
+        new.pool = None
+        new.c = CacheStruct()
+        new._bind(self.T, int(self.c.nres))
+        new._ws = {}
+        return new
 
     # ------------------------------------------------------------ construction
     @classmethod
@@ -285,7 +306,7 @@ class GradedCache:
         key = (op, topk)
         ws = self._ws.get(key)
         if ws is None or ws.numel() < n:
-            ws = torch.empty(max(n, 16), dtype=torch.uint8, device=self.device)
+            ws = torch.zeros(max(n, 16), dtype=torch.uint8, device=self.device)
             self._ws[key] = ws
         return ws
 

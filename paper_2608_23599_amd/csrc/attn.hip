@@ -6,7 +6,7 @@
 // it that are read) of one (b, KV head) and keeps an online-softmax state for
 // the up-to-16 query heads of the group in MFMA accumulator layout.  The four
 // wavefronts of a workgroup are merged in LDS into one partial (m, l, o) per
-// head; a second kernel merges the partials of a (b, KV head).
+// head; the last workgroup of a (b, KV head) to finish merges its partials.
 //
 // Per 16-token tile the wavefront issues
 //   S[token][head] = sum_d A[token][d] * B[d][head]       (4 x MFMA 16x16x32 f16)
@@ -134,6 +134,8 @@ struct AttnParams {
   const uint8_t *res_rows;
   const int32_t *pages;
   float *part;
+  uint32_t *arrive;  // per (b, KV head) arrival counters; zero between calls
+  float *out;
   int64_t T;
   int nblk_cap, Hkv, G, nres, nrb_cap, topk, page, nsplit;
   float sl2;  // log2(e) / sqrt(D)
@@ -638,27 +640,32 @@ __global__ void __launch_bounds__(kThreads) attn_kernel(AttnParams p) {
       out[g * (D + 2) + 1] = L;
     }
   }
-}
-
-// Merge the nsplit partials of every query head; grid (Hq, B), 128 threads.
-__global__ void __launch_bounds__(128) reduce_kernel(const float *__restrict__ part, float *__restrict__ out,
-                                                     int Hkv, int G, int nsplit) {
-  const int gq = blockIdx.x, b = blockIdx.y, d = threadIdx.x;
-  const int h = gq / G, g = gq % G;
-  const int64_t u = (int64_t)b * Hkv + h;
-  const float *base = part + (u * nsplit * G + g) * (int64_t)(D + 2);
-  const int64_t stride = (int64_t)G * (D + 2);
-  float M = kNegInf;
-  for (int s = 0; s < nsplit; ++s) M = fmaxf(M, base[s * stride]);
-  float L = 0.f, o = 0.f;
-  for (int s = 0; s < nsplit; ++s) {
-    const float ms = base[s * stride];
-    if (ms == kNegInf) continue;
-    const float a = exp2f(ms - M);
-    L = fmaf(base[s * stride + 1], a, L);
-    o = fmaf(base[s * stride + 2 + d], a, o);
+  // ---------------- the last workgroup of this (b, KV head) merges all partials
+  __shared__ int last;
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) last = atomicAdd(p.arrive + u, 1u) == (uint32_t)(p.nsplit - 1);
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+  const float *base = p.part + u * p.nsplit * (int64_t)p.G * (D + 2);
+  const int64_t stride = (int64_t)p.G * (D + 2);
+  for (int i = threadIdx.x; i < p.G * D; i += kThreads) {
+    const int g = i >> 7, d = i & 127;
+    const float *pg = base + g * (D + 2);
+    float M = kNegInf;
+    for (int s = 0; s < p.nsplit; ++s) M = fmaxf(M, __builtin_nontemporal_load(pg + s * stride));
+    float L = 0.f, o = 0.f;
+    for (int s = 0; s < p.nsplit; ++s) {
+      const float ms = __builtin_nontemporal_load(pg + s * stride);
+      if (ms == kNegInf) continue;
+      const float a = exp2f(ms - M);
+      L = fmaf(__builtin_nontemporal_load(pg + s * stride + 1), a, L);
+      o = fmaf(__builtin_nontemporal_load(pg + s * stride + 2 + d), a, o);
+    }
+    p.out[(u * p.G + g) * D + d] = o / L;
   }
-  out[((int64_t)b * Hkv * G + gq) * D + d] = o / L;
+  if (threadIdx.x == 0) p.arrive[u] = 0;  // leave the counter ready for the next call
 }
 
 }  // namespace
@@ -680,9 +687,13 @@ static int attn_nsplit(const gkv_cache *c, int32_t topk) {
   return (int)((waves + kWaves - 1) / kWaves);
 }
 
-int64_t gkv_attn_workspace(const gkv_cache *c, int32_t topk) {
+static int64_t attn_part_bytes(const gkv_cache *c, int32_t topk) {
   const int G = c->Hq / c->Hkv;
-  return (int64_t)c->B * c->Hkv * attn_nsplit(c, topk) * G * (D + 2) * 4;
+  return ((int64_t)c->B * c->Hkv * attn_nsplit(c, topk) * G * (D + 2) * 4 + 255) & ~(int64_t)255;
+}
+
+int64_t gkv_attn_workspace(const gkv_cache *c, int32_t topk) {
+  return attn_part_bytes(c, topk) + (int64_t)c->B * c->Hkv * 4;
 }
 
 extern "C" gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache *c, const int32_t *pages,
@@ -710,6 +721,8 @@ extern "C" gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache 
   p.res_rows = c->res_rows;
   p.pages = pages;
   p.part = (float *)ws;
+  p.arrive = (uint32_t *)((uint8_t *)ws + attn_part_bytes(c, topk));
+  p.out = out;
   p.T = c->T;
   p.nblk_cap = c->nblk_cap;
   p.Hkv = c->Hkv;
@@ -721,7 +734,5 @@ extern "C" gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache 
   p.nsplit = attn_nsplit(c, topk);
   p.sl2 = 1.4426950408889634f / sqrtf((float)D);
   hipLaunchKernelGGL(attn_kernel, dim3(p.nsplit, c->Hkv, c->B), dim3(kThreads), 0, (hipStream_t)stream, p);
-  hipLaunchKernelGGL(reduce_kernel, dim3(c->Hq, c->B), dim3(128), 0, (hipStream_t)stream, (const float *)ws, out,
-                     c->Hkv, p.G, p.nsplit);
   return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP;
 }
