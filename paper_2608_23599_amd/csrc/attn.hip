@@ -1,12 +1,27 @@
 // Fused dequant + online-softmax GQA decode attention over a graded cache
 // (sections 3.1, 3.5 and 3.7), and the split-context reduction.
 //
-// Work split: grid (nsplit, Hkv, B) x 4 wavefronts.  Each wavefront owns a
-// contiguous, byte-balanced range of "visits" (a block plus the 16-token tiles of
-// it that are read) of one (b, KV head) and keeps an online-softmax state for
-// the up-to-16 query heads of the group in MFMA accumulator layout.  The four
-// wavefronts of a workgroup are merged in LDS into one partial (m, l, o) per
-// head; the last workgroup of a (b, KV head) to finish merges its partials.
+// Two kernels per call.  The plan kernel (one workgroup per (b, KV head)) writes a
+// 32-byte descriptor per "visit" (a block and the tokens of it that are read: all
+// valid tokens of a dense read minus the residual rows, or the selected pages of a
+// Compressed-Quest read) and splits the visits over the wavefronts by a cost that
+// counts bytes and pipeline items.  The attention kernel runs grid (nsplit, Hkv, B)
+// x 4 wavefronts; each wavefront keeps an online-softmax state for the up-to-16
+// query heads of the group in MFMA accumulator layout; the four wavefronts of a
+// workgroup are merged in LDS into one partial (m, l, o) per head and the last
+// workgroup of a (b, KV head) to finish merges the partials.
+//
+// Memory pipeline: a visit is a sequence of "items" (an int block's key
+// scale/zero, a 16-token K+V tile, a centroid block).  A producer cursor walks the
+// wavefront's visits and copies items ahead into a private LDS ring with
+// asynchronous global -> LDS loads (global_load_lds_dwordx4: every lane moves 16 B,
+// so one instruction moves 1 KB); the visit descriptors arrive the same way, one
+// 1 KB chunk (32 visits) ahead.  Issued items go through a small LDS queue to the
+// consumer, which waits on the load counter for its item and computes from LDS.
+// The copies are issued from inline assembly so that the compiler does not add a
+// full load-counter wait in front of every LDS read; the waits are explicit, and
+// no other vector-memory instruction runs inside the loop (the load counter
+// retires in order, so any would wait for every copy in flight).
 //
 // Per 16-token tile the wavefront issues
 //   S[token][head] = sum_d A[token][d] * B[d][head]       (4 x MFMA 16x16x32 f16)
@@ -26,6 +41,9 @@
 #include <hip/hip_runtime.h>
 
 #include "gkv_internal.h"
+
+// the asynchronous copies set M0 themselves (see dma16)
+#pragma clang diagnostic ignored "-Winline-asm"
 
 using namespace gkv;
 
@@ -107,6 +125,14 @@ struct Unpack<2> {
   }
 };
 
+// A register holding a constant that the compiler must not hoist out of the item
+// loop (hoisted constants of every level's path would stay live together).
+__device__ __forceinline__ uint32_t opaque(uint32_t c) {
+  uint32_t r;
+  asm volatile("v_mov_b32 %0, %1" : "=v"(r) : "s"(c));
+  return r;
+}
+
 // Offset (as fp16 pair, negated) of code pair q.
 template <int BITS>
 __device__ __forceinline__ uint32_t neg_off_pair(int q) {
@@ -133,14 +159,264 @@ struct AttnParams {
   const uint64_t *res_mask;
   const uint8_t *res_rows;
   const int32_t *pages;
+  uint8_t *plan;   // visit descriptors, vcap per (b, KV head)
+  int32_t *split;  // first visit of each wavefront, W + 1 per (b, KV head)
   float *part;
   uint32_t *arrive;  // per (b, KV head) arrival counters; zero between calls
   float *out;
   int64_t T;
-  int nblk_cap, Hkv, G, nres, nrb_cap, topk, page, nsplit;
+  int nblk_cap, Hkv, G, nres, nrb_cap, topk, nsplit;
+  int64_t vcap;
   float sl2;  // log2(e) / sqrt(D)
 };
 
+constexpr int kRing = 14592;    // staging ring per wavefront (bytes)
+constexpr int kQueue = 16;      // item descriptors in flight per wavefront
+constexpr int kQueueBytes = 32 * kQueue;
+constexpr int kDescBytes = 2048;  // visit-descriptor ring: two 1 KB chunks
+constexpr int kWaveLds = kRing + kQueueBytes + kDescBytes;  // LDS per wavefront
+
+// ---------------------------------------------------------------- async copies
+__device__ __forceinline__ void dma16(const void *g, uint32_t lds_wave_base) {
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane(lds_wave_base);
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(m0v) : "memory", "m0");
+}
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+// Wait until at most n of this wavefront's loads are outstanding (rounded down to
+// an immediate; waiting for more than needed is always safe).
+__device__ __forceinline__ void wait_loads(uint32_t n) {
+  if (n >= 24) vm_wait<24>();
+  else if (n >= 16) vm_wait<16>();
+  else if (n >= 12) vm_wait<12>();
+  else if (n >= 8) vm_wait<8>();
+  else if (n >= 6) vm_wait<6>();
+  else if (n >= 4) vm_wait<4>();
+  else if (n >= 3) vm_wait<3>();
+  else if (n >= 2) vm_wait<2>();
+  else if (n >= 1) vm_wait<1>();
+  else vm_wait<0>();
+}
+
+// ---------------------------------------------------------------- wave-uniform values
+// The walkers' state is the same in every lane; readfirstlane keeps it in scalar
+// registers (the compiler cannot prove uniformity of values loaded from memory).
+__device__ __forceinline__ int32_t uni(int32_t x) { return __builtin_amdgcn_readfirstlane(x); }
+__device__ __forceinline__ int64_t uni64(int64_t x) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)x >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// ---------------------------------------------------------------- item sequence
+enum ItemKind { kHeader = 0, kTile = 1, kCentroid = 2 };
+
+// An item: a 16-byte-aligned span of the ring filled by ceil(bytes/1024) copies.
+// meta packs kind (2 bits), level (5), tile (2), last-of-visit (1) and the tile's
+// valid-token bits (16).
+struct Item {
+  uint32_t lin;      // linear ring position (bytes)
+  uint32_t cnt_end;  // load instructions issued through this item
+  uint32_t meta;
+  __device__ int kind() const { return meta & 3u; }
+  __device__ int lv() const { return (meta >> 2) & 31u; }
+  __device__ int tile() const { return (meta >> 7) & 3u; }
+  __device__ bool last() const { return (meta >> 9) & 1u; }
+  __device__ uint32_t tvalid() const { return meta >> 16; }
+};
+
+// Item sizes: an int block's header carries the key scale/zero; its last tile also
+// carries the value scale/zero, used by the block epilogue.
+__device__ __forceinline__ uint32_t item_bytes(int kind, int lv, bool last) {
+  if (kind == kCentroid) return 2 * kCentBytes;
+  if (kind == kHeader) return kSZBytes;
+  if (lv == GKV_EXACT) return 2 * 4096;
+  return 2 * 256 * lv + (last ? kSZBytes : 0);
+}
+
+// A visit: one block of one (b, KV head) and the tokens of it that are read.  The
+// plan kernel writes one 32-byte descriptor per visit, in visit order, and the
+// split of the visits over the wavefronts.
+struct VisitDesc {
+  uint64_t kp, vp;  // addresses of the K and V records
+  uint64_t valid;   // tokens of the block that are read (bit t = token t)
+  int32_t level;    // storage level of both records
+  uint32_t cost;    // balance cost (plan kernel only)
+};
+static_assert(sizeof(VisitDesc) == 32, "descriptor size");
+constexpr int kDescChunk = 1024 / sizeof(VisitDesc);  // descriptors per copy (one 1 KB copy)
+
+// Walks the visits of one wavefront and the items of each visit.  The wavefront's
+// descriptors stream through a two-slot LDS ring, one 1 KB chunk per copy, each
+// chunk requested one chunk ahead of its first use.
+struct Walker {
+  const uint8_t *dsrc;  // descriptors of this wavefront's visits
+  const uint8_t *dring;  // the descriptor ring (2 x 1 KB of LDS)
+  uint32_t dlds;        // its LDS address
+  uint32_t dcnt0, dcnt1;  // load count through the copy of each slot's chunk
+  uint32_t v, nv;       // next visit (relative), number of visits
+  const uint8_t *kp, *vp;
+  uint64_t valid;
+  uint32_t lin, cnt;  // ring position and loads issued, both through the last item
+  int lv;
+  uint32_t tiles;  // tiles still to emit
+  bool in_visit, need_header;
+
+  __device__ __forceinline__ void fetch_chunk(uint32_t c, int lane) {  // copy descriptor chunk c
+    dma16(dsrc + (size_t)c * 1024 + 16 * lane, dlds + (c & 1) * 1024);
+    ++cnt;
+    if (c & 1) dcnt1 = cnt;
+    else dcnt0 = cnt;
+  }
+
+  // `cnt` equals the number of loads issued whenever the walker runs: the producer
+  // issues every item before asking for the next one.
+  __device__ bool open_visit(int lane) {
+    while (v < nv) {
+      const uint32_t r = v++;
+      const uint32_t c = r / kDescChunk;
+      if (r % kDescChunk == 0) {
+        wait_loads(cnt - ((c & 1) ? dcnt1 : dcnt0));
+        if ((c + 1) * kDescChunk < nv) fetch_chunk(c + 1, lane);  // the other slot is done with
+      }
+      const uint8_t *e = dring + (c & 1) * 1024 + (r % kDescChunk) * 32;
+      const uint4 d0 = *(const uint4 *)e, d1 = *(const uint4 *)(e + 16);
+      kp = (const uint8_t *)(uintptr_t)uni64((int64_t)(((uint64_t)d0.y << 32) | d0.x));
+      vp = (const uint8_t *)(uintptr_t)uni64((int64_t)(((uint64_t)d0.w << 32) | d0.z));
+      const uint64_t va = (uint64_t)uni64((int64_t)(((uint64_t)d1.y << 32) | d1.x));
+      lv = uni((int32_t)d1.z);
+      valid = va;
+      tiles = 0;
+      for (int t = 0; t < 4; ++t)
+        if ((va >> (16 * t)) & 0xFFFFull) tiles |= 1u << t;
+      if (!tiles) continue;
+      need_header = lv != GKV_EXACT;
+      in_visit = true;
+      return true;
+    }
+    return false;
+  }
+
+  __device__ bool next(Item &it, int lane) {
+    if (!in_visit && !open_visit(lane)) return false;
+    uint32_t kind, t = 0, last = 0, tv = 0;
+    if (lv == GKV_CENTROID) {
+      kind = kCentroid;
+      last = 1;
+      in_visit = false;
+    } else if (need_header) {
+      kind = kHeader;
+      need_header = false;
+    } else {
+      kind = kTile;
+      t = __builtin_ctz(tiles);
+      tiles &= tiles - 1;
+      tv = (uint32_t)((valid >> (16 * t)) & 0xFFFFull);
+      last = tiles == 0;
+      if (last) in_visit = false;
+    }
+    const uint32_t size = item_bytes(kind, lv, last);
+    const uint32_t off = lin % kRing;
+    if (off + size > kRing) lin += kRing - off;  // an item never wraps around the ring end
+    it.lin = lin;
+    lin += size;
+    cnt += (size + 1023) / 1024;
+    it.cnt_end = cnt;
+    it.meta = kind | ((uint32_t)lv << 2) | (t << 7) | (last << 9) | (tv << 16);
+    return true;
+  }
+};
+
+// Issue the asynchronous copies of the producer's current item (its K part
+// followed by its V part in LDS).
+__device__ __forceinline__ void issue(const Walker &w, const Item &it, uint32_t ring_base, int lane) {
+  const int kind = it.kind(), lv = it.lv(), t = it.tile();
+  uint32_t kunits, koff;
+  if (kind == kCentroid) {
+    kunits = kCentBytes / 16;
+    koff = 0;
+  } else if (kind == kHeader) {
+    kunits = kSZBytes / 16;
+    koff = 0;
+  } else if (lv == GKV_EXACT) {
+    kunits = 4096 / 16;
+    koff = t * 4096;
+  } else {
+    kunits = 16 * lv;
+    koff = kSZBytes + t * 256 * lv;
+  }
+  // K part, then V part (same offsets), then for an int block's last tile the
+  // value scale/zero; a header has only the key scale/zero
+  const uint32_t vunits = kind == kHeader ? 0 : kunits;
+  const uint32_t xunits = (kind == kTile && lv != GKV_EXACT && it.last()) ? kSZBytes / 16 : 0;
+  const uint32_t units = kunits + vunits + xunits;
+  const uint32_t base = ring_base + it.lin % kRing;
+#pragma unroll 1
+  for (uint32_t i = 0; i * 64 < units; ++i) {
+    const uint32_t uu = i * 64 + lane;
+    if (uu < units) {
+      const uint8_t *src = uu < kunits ? w.kp + koff + 16 * uu
+                           : uu < kunits + vunits ? w.vp + koff + 16 * (uu - kunits)
+                                                  : w.vp + 16 * (uu - kunits - vunits);
+      dma16(src, base + 1024 * i);
+    }
+  }
+}
+
+// ---------------------------------------------------------------- pipeline
+// Producer side of a wavefront's pipeline: the walker, its next item, the ring and
+// a queue of issued item descriptors (lin, cnt_end, meta, -, valid lo, valid hi)
+// that the consumer pops in order.
+struct Pipe {
+  Walker prod;
+  Item pend;
+  bool has_pend;
+  uint32_t issued;  // load instructions issued
+  uint32_t hold;    // ring bytes before this linear position are free
+  uint32_t head, tail;  // queue indices (popped / pushed)
+  uint32_t ring_base;
+  const uint8_t *ring;
+  uint32_t *queue;
+  int lane;
+
+  __device__ __forceinline__ void pump() {
+    while (has_pend && tail - head < (uint32_t)kQueue &&
+           pend.lin + item_bytes(pend.kind(), pend.lv(), pend.last()) - hold <= (uint32_t)kRing) {
+      issue(prod, pend, ring_base, lane);
+      issued = pend.cnt_end;
+      if (lane == 0) {
+        uint32_t *q = queue + 8 * (tail % kQueue);
+        *(uint4 *)q = make_uint4(pend.lin, pend.cnt_end, pend.meta, 0u);
+        *(uint2 *)(q + 4) = make_uint2((uint32_t)prod.valid, (uint32_t)(prod.valid >> 32));
+      }
+      ++tail;
+      has_pend = prod.next(pend, lane);
+    }
+  }
+  // Pop the next item (false when the sequence is exhausted), wait for its copies.
+  __device__ __forceinline__ bool pop(Item &it, uint64_t &valid, const uint8_t *&ip) {
+    pump();
+    if (head == tail) return false;
+    const uint32_t *q = queue + 8 * (head % kQueue);
+    const uint4 e = *(const uint4 *)q;
+    const uint2 vv = *(const uint2 *)(q + 4);
+    it.lin = uni(e.x);
+    it.cnt_end = uni(e.y);
+    it.meta = uni(e.z);
+    valid = ((uint64_t)(uint32_t)uni(vv.y) << 32) | (uint32_t)uni(vv.x);
+    ++head;
+    wait_loads(issued - it.cnt_end);
+    ip = ring + it.lin % kRing;
+    return true;
+  }
+  __device__ __forceinline__ void release(const Item &it) {
+    hold = it.lin + item_bytes(it.kind(), it.lv(), it.last());
+  }
+};
+
+// ---------------------------------------------------------------- per-wave state
 struct State {
   f4 O[8];
   float m, l;
@@ -152,142 +428,117 @@ __device__ __forceinline__ float wave_max16(float x) {  // max over the 4 lanes 
   return x;
 }
 
-// Masks S to the valid tokens, updates the running max (lazily), and returns
-// P (fp16 pairs) in the B-operand layout of the value MFMA.
-__device__ __forceinline__ void softmax_tiles(const AttnParams &p, State &st, f4 *S, uint32_t (*Pw)[2],
-                                              int tiles, uint64_t valid, int kg) {
-  float bm = kNegInf;
-#pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    if (!(tiles & (1 << t))) continue;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int tok = 16 * t + 4 * kg + r;
-      if ((valid >> tok) & 1ull) bm = fmaxf(bm, S[t][r]);
-    }
-  }
-  bm = wave_max16(bm) * p.sl2;
+__device__ __forceinline__ half4 as_h4(uint32_t a, uint32_t b) {
+  U4 u;
+  u.u[0] = a;
+  u.u[1] = b;
+  return u.h;
+}
+
+// Lazy online-softmax rescale: when the block maximum exceeds the running maximum
+// by more than kRescale, move the maximum and rescale the accumulators.
+__device__ __forceinline__ float rescale_factor(State &st, float bm) {
   const bool need = bm > st.m + kRescale;
+  float alpha = 1.0f;
   if (__any(need)) {
     const float mn = need ? bm : st.m;
-    const float alpha = need ? exp2f(st.m - mn) : 1.0f;
+    alpha = need ? __builtin_amdgcn_exp2f(st.m - mn) : 1.0f;
 #pragma unroll
     for (int j = 0; j < 8; ++j) st.O[j] *= alpha;
     st.l *= alpha;
     st.m = mn;
   }
+  return alpha;
+}
+
+// Tile maximum (scaled to log2 units) over the valid tokens, shared by the 4 lanes
+// of each head.
+__device__ __forceinline__ float tile_max(const AttnParams &p, f4 S, bool full, uint32_t mine) {
+  float bm;
+  if (full) {
+    bm = fmaxf(fmaxf(S[0], S[1]), fmaxf(S[2], S[3]));
+  } else {
+    bm = kNegInf;
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    if (!(tiles & (1 << t))) continue;
-    float pv[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int tok = 16 * t + 4 * kg + r;
-      pv[r] = ((valid >> tok) & 1ull) ? exp2f(fmaf(S[t][r], p.sl2, -st.m)) : 0.0f;
-    }
-    U4 u;
-    u.h = half4{(_Float16)pv[0], (_Float16)pv[1], (_Float16)pv[2], (_Float16)pv[3]};
-    Pw[t][0] = u.u[0];
-    Pw[t][1] = u.u[1];
+    for (int r = 0; r < 4; ++r)
+      if (mine & (1u << r)) bm = fmaxf(bm, S[r]);
   }
+  return wave_max16(bm) * p.sl2;
 }
 
-__device__ __forceinline__ half4 as_h4(const uint32_t *w) {
-  U4 u;
-  u.u[0] = w[0];
-  u.u[1] = w[1];
-  return u.h;
+__device__ __forceinline__ half4 tile_probs(const AttnParams &p, const State &st, f4 S, bool full, uint32_t mine) {
+  float pv[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const float e = __builtin_amdgcn_exp2f(fmaf(S[r], p.sl2, -st.m));
+    pv[r] = (full || (mine & (1u << r))) ? e : 0.0f;
+  }
+  return half4{(_Float16)pv[0], (_Float16)pv[1], (_Float16)pv[2], (_Float16)pv[3]};
 }
 
-// ---------------------------------------------------------------- exact blocks
-__device__ void visit_exact(const AttnParams &p, State &st, const half8 *qB, const uint8_t *kp,
-                            const uint8_t *vp, int tiles, uint64_t valid, int lane) {
+__device__ __forceinline__ uint4 lds16(const uint8_t *a) { return *(const uint4 *)a; }
+
+// The group's queries live in LDS, one 272-byte row per head (padded against bank
+// conflicts); lane (head m, kg) reads its B-operand chunk of MFMA i.
+constexpr int kQRow = 272;
+__device__ __forceinline__ half8 qchunk(const uint8_t *qs, int lane, int i) {
+  U8 t;
+  t.v = lds16(qs + (lane & 15) * kQRow + (32 * i + 8 * (lane >> 4)) * 2);
+  return t.h;
+}
+
+constexpr half4 kOnes = half4{(_Float16)1, (_Float16)1, (_Float16)1, (_Float16)1};
+
+// ---------------------------------------------------------------- items
+// Exact block tile: 16 tokens of fp16 K and V.
+__device__ __forceinline__ void exact_tile(const AttnParams &p, State &st, const uint8_t *qs, const uint8_t *ip,
+                                           uint32_t tvalid, int lane) {
   const int kg = lane >> 4;
-  f4 S[4];
-  uint32_t Pw[4][2];
-  const half4 ones = half4{(_Float16)1, (_Float16)1, (_Float16)1, (_Float16)1};
+  U8 a[4];
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    if (!(tiles & (1 << t))) continue;
-    const uint4 *kc = (const uint4 *)(kp + (size_t)(t * 64 + lane) * 64);
-    U8 a[4];
+  for (int i = 0; i < 4; ++i) a[i].v = lds16(ip + lane * 64 + 16 * i);
+  f4 S = {0, 0, 0, 0};
 #pragma unroll
-    for (int i = 0; i < 4; ++i) a[i].v = kc[i];
-    f4 acc = {0, 0, 0, 0};
+  for (int i = 0; i < 4; ++i) S = mfma32(a[i].h, qchunk(qs, lane, i), S);
+  const bool full = tvalid == 0xFFFFu;
+  const uint32_t mine = (tvalid >> (4 * kg)) & 0xFu;
+  rescale_factor(st, tile_max(p, S, full, mine));
+  const half4 P4 = tile_probs(p, st, S, full, mine);
+  const f4 pb = mfma16(kOnes, P4, f4{0, 0, 0, 0});
 #pragma unroll
-    for (int i = 0; i < 4; ++i) acc = mfma32(a[i].h, qB[i], acc);
-    S[t] = acc;
-  }
-  softmax_tiles(p, st, S, Pw, tiles, valid, kg);
-  f4 pb = {0, 0, 0, 0};
+  for (int i = 0; i < 4; ++i) a[i].v = lds16(ip + 4096 + lane * 64 + 16 * i);
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    if (!(tiles & (1 << t))) continue;
-    const half4 P4 = as_h4(Pw[t]);
-    pb = mfma16(ones, P4, pb);
-    const uint4 *vc = (const uint4 *)(vp + (size_t)(t * 64 + lane) * 64);
-    U8 a[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) a[i].v = vc[i];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      U4 v;
-      v.u[0] = a[j >> 1].u[2 * (j & 1)];
-      v.u[1] = a[j >> 1].u[2 * (j & 1) + 1];
-      st.O[j] = mfma16(v.h, P4, st.O[j]);
-    }
-  }
+  for (int j = 0; j < 8; ++j)
+    st.O[j] = mfma16(as_h4(a[j >> 1].u[2 * (j & 1)], a[j >> 1].u[2 * (j & 1) + 1]), P4, st.O[j]);
   st.l += pb[0];
 }
 
-// ---------------------------------------------------------------- scalar-code blocks
+// State of the scalar-code block being read.
+struct IntBlock {
+  half8 qh[4], ql[4];  // q * s as two fp16 terms
+  f4 c0;               // per-block logit constant
+  f4 acc[8], pb;       // block-local P.V on codes and sum of P
+};
+
 template <int BITS>
-__device__ void visit_int(const AttnParams &p, State &st, const half8 *qB, const uint8_t *kp,
-                          const uint8_t *vp, int tiles, uint64_t valid, int lane) {
-  constexpr int NW = Unpack<BITS>::kWords;
+__device__ __forceinline__ void int_header(IntBlock &ib, const uint8_t *qs, const uint8_t *ip, int lane) {
   const int kg = lane >> 4;
-  // key scale / zero for this lane's channels (lane order, 32 entries per kg)
+  half8 qB[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) qB[i] = qchunk(qs, lane, i);
   U8 sK[4], zK[4];
-  {
-    const uint4 *s4 = (const uint4 *)(kp + kg * 64);
-    const uint4 *z4 = (const uint4 *)(kp + 256 + kg * 64);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      sK[i].v = s4[i];
-      zK[i].v = z4[i];
-    }
-  }
-  // key codes of the tiles read
-  uint32_t kw[4][NW];
-#pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    if (!(tiles & (1 << t))) continue;
-    const uint32_t *src = (const uint32_t *)(kp + kSZBytes + (size_t)(t * 64 + lane) * (4 * BITS));
-    if (NW >= 4) {
-#pragma unroll
-      for (int q = 0; q < NW; q += 4) {
-        const uint4 v = *(const uint4 *)(src + q);
-        kw[t][q] = v.x;
-        kw[t][q + 1] = v.y;
-        kw[t][q + 2] = v.z;
-        kw[t][q + 3] = v.w;
-      }
-    } else {
-      const uint2 v = *(const uint2 *)src;
-      kw[t][0] = v.x;
-      kw[t][1] = v.y;
-    }
-  }
-  // q * s split into two fp16 terms, q' = hi + lo: hi = fp16(q * s) and
-  // lo = fp16(q * s - hi) (q * s and q * s - hi are exact in fp32), so the folded
-  // scale keeps ~22 bits; then the per-block constant sum z q - sum off q'.
-  half8 qh[4], ql[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    qh[i] = qB[i] * sK[i].h;
+    sK[i].v = lds16(ip + kg * 64 + 16 * i);
+    zK[i].v = lds16(ip + 256 + kg * 64 + 16 * i);
+  }
+  // q * s as two fp16 terms hi + lo (q * s and q * s - hi are exact in fp32)
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    ib.qh[i] = qB[i] * sK[i].h;
 #pragma unroll
     for (int e = 0; e < 8; ++e)
-      ql[i][e] = (_Float16)__builtin_fmaf((float)qB[i][e], (float)sK[i].h[e], -(float)qh[i][e]);
+      ib.ql[i][e] = (_Float16)__builtin_fmaf((float)qB[i][e], (float)sK[i].h[e], -(float)ib.qh[i][e]);
   }
   f4 c0 = {0, 0, 0, 0};
 #pragma unroll
@@ -296,119 +547,123 @@ __device__ void visit_int(const AttnParams &p, State &st, const half8 *qB, const
   for (int i = 0; i < 4; ++i) {
     U8 o;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) o.u[e] = neg_off_pair<BITS>(4 * i + e);
-    c0 = mfma32(o.h, qh[i], c0);
-    c0 = mfma32(o.h, ql[i], c0);
+    for (int e = 0; e < 4; ++e) o.u[e] = opaque(neg_off_pair<BITS>(4 * i + e));
+    c0 = mfma32(o.h, ib.qh[i], c0);
+    c0 = mfma32(o.h, ib.ql[i], c0);
   }
-  f4 S[4];
+  ib.c0 = c0;
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    if (!(tiles & (1 << t))) continue;
-    f4 acc = c0;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      U8 a;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) a.u[e] = Unpack<BITS>::pair(kw[t], 4 * i + e);
-      acc = mfma32(a.h, qh[i], acc);
-      acc = mfma32(a.h, ql[i], acc);
-    }
-    S[t] = acc;
-  }
-  uint32_t Pw[4][2];
-  softmax_tiles(p, st, S, Pw, tiles, valid, kg);
-  // values
-  U8 sV[4], zV[4];
-  {
-    const uint4 *s4 = (const uint4 *)(vp + kg * 64);
-    const uint4 *z4 = (const uint4 *)(vp + 256 + kg * 64);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      sV[i].v = s4[i];
-      zV[i].v = z4[i];
-    }
-  }
-  const half4 ones = half4{(_Float16)1, (_Float16)1, (_Float16)1, (_Float16)1};
-  f4 pb = {0, 0, 0, 0};
-  f4 acc[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) acc[j] = f4{0, 0, 0, 0};
-#pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    if (!(tiles & (1 << t))) continue;
-    uint32_t vw[NW];
-    const uint32_t *src = (const uint32_t *)(vp + kSZBytes + (size_t)(t * 64 + lane) * (4 * BITS));
-    if (NW >= 4) {
-#pragma unroll
-      for (int q = 0; q < NW; q += 4) {
-        const uint4 v = *(const uint4 *)(src + q);
-        vw[q] = v.x;
-        vw[q + 1] = v.y;
-        vw[q + 2] = v.z;
-        vw[q + 3] = v.w;
-      }
-    } else {
-      const uint2 v = *(const uint2 *)src;
-      vw[0] = v.x;
-      vw[1] = v.y;
-    }
-    const half4 P4 = as_h4(Pw[t]);
-    pb = mfma16(ones, P4, pb);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      U4 a;
-      a.u[0] = Unpack<BITS>::pair(vw, 2 * j);
-      a.u[1] = Unpack<BITS>::pair(vw, 2 * j + 1);
-      acc[j] = mfma16(a.h, P4, acc[j]);
-    }
-  }
-  // epilogue: O[d][h] += s_d * (acc - off * sum p) + z_d * sum p, d = 16j + 4kg + r
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const float off = v_off<BITS>(j);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int n = 4 * j + r;
-      const float s = (float)sV[n >> 3].h[n & 7];
-      const float z = (float)zV[n >> 3].h[n & 7];
-      const float x = fmaf(-off, pb[r], acc[j][r]);
-      st.O[j][r] = fmaf(s, x, fmaf(z, pb[r], st.O[j][r]));
-    }
-  }
-  st.l += pb[0];
+  for (int j = 0; j < 8; ++j) ib.acc[j] = f4{0, 0, 0, 0};
+  ib.pb = f4{0, 0, 0, 0};
 }
 
-// ---------------------------------------------------------------- centroid blocks
-__device__ void visit_centroid(const AttnParams &p, State &st, const half8 *qB, const uint8_t *kp,
-                               const uint8_t *vp, uint64_t valid, int lane) {
+template <int BITS>
+__device__ __forceinline__ void int_tile(const AttnParams &p, State &st, IntBlock &ib, const uint8_t *ip,
+                                         uint32_t tvalid, bool last, int lane) {
+  constexpr int NW = Unpack<BITS>::kWords;
+  const int kg = lane >> 4;
+  const uint8_t *kc = ip + lane * (4 * BITS);
+  const uint8_t *vc = ip + 256 * BITS + lane * (4 * BITS);
+  uint32_t kw[NW];
+  if (NW >= 4) {
+#pragma unroll
+    for (int q = 0; q < NW; q += 4) {
+      const uint4 a = lds16(kc + 4 * q);
+      kw[q] = a.x; kw[q + 1] = a.y; kw[q + 2] = a.z; kw[q + 3] = a.w;
+    }
+  } else {
+    const uint2 a = *(const uint2 *)kc;
+    kw[0] = a.x; kw[1] = a.y;
+  }
+  f4 S = ib.c0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    U8 a;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) a.u[e] = Unpack<BITS>::pair(kw, 4 * i + e);
+    S = mfma32(a.h, ib.qh[i], S);
+    S = mfma32(a.h, ib.ql[i], S);
+  }
+  const bool full = tvalid == 0xFFFFu;
+  const uint32_t mine = (tvalid >> (4 * kg)) & 0xFu;
+  const float alpha = rescale_factor(st, tile_max(p, S, full, mine));
+  if (alpha != 1.0f) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) ib.acc[j] *= alpha;
+    ib.pb *= alpha;
+  }
+  const half4 P4 = tile_probs(p, st, S, full, mine);
+  ib.pb = mfma16(kOnes, P4, ib.pb);
+  uint32_t vw[NW];
+  if (NW >= 4) {
+#pragma unroll
+    for (int q = 0; q < NW; q += 4) {
+      const uint4 a = lds16(vc + 4 * q);
+      vw[q] = a.x; vw[q + 1] = a.y; vw[q + 2] = a.z; vw[q + 3] = a.w;
+    }
+  } else {
+    const uint2 a = *(const uint2 *)vc;
+    vw[0] = a.x; vw[1] = a.y;
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+    ib.acc[j] = mfma16(as_h4(Unpack<BITS>::pair(vw, 2 * j), Unpack<BITS>::pair(vw, 2 * j + 1)), P4, ib.acc[j]);
+  if (last) {
+    // O[d][h] += s_d * (acc - off * sum p) + z_d * sum p,  d = 16j + 4kg + r;
+    // the value scale/zero follow the last tile's codes in LDS
+    const uint8_t *sz = ip + 512 * BITS + kg * 64;
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {  // two halves keep fewer scale/zero registers live
+      U8 sV[2], zV[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        sV[i].v = lds16(sz + 32 * hh + 16 * i);
+        zV[i].v = lds16(sz + 256 + 32 * hh + 16 * i);
+      }
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int j = 4 * hh + jj;
+        const float off = v_off<BITS>(j);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int n = 4 * jj + r;
+          const float x = fmaf(-off, ib.pb[r], ib.acc[j][r]);
+          st.O[j][r] = fmaf((float)sV[n >> 3].h[n & 7], x, fmaf((float)zV[n >> 3].h[n & 7], ib.pb[r], st.O[j][r]));
+        }
+      }
+    }
+    st.l += ib.pb[0];
+  }
+}
+
+// Centroid block: one item with both records.
+__device__ __forceinline__ void centroid_item(const AttnParams &p, State &st, const uint8_t *qs, const uint8_t *ip,
+                                              uint64_t valid, int lane) {
   const int kg = lane >> 4, m16 = lane & 15;
   // logits of the 4 key centroids: rows 4kg + r of A hold centroid r
   f4 sc = {0, 0, 0, 0};
-  {
-    const uint16_t *cen = (const uint16_t *)kp + (m16 & 3) * D + 8 * kg;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      U8 a;
-      a.v = *(const uint4 *)(cen + 32 * i);
-      sc = mfma32(a.h, qB[i], sc);
-    }
+  for (int i = 0; i < 4; ++i) {
+    U8 a;
+    a.v = lds16(ip + ((m16 & 3) * D + 8 * kg + 32 * i) * 2);
+    sc = mfma32(a.h, qchunk(qs, lane, i), sc);
   }
-  // joint (key id, value id) counts over the valid tokens
-  const uint32_t *kid = (const uint32_t *)(kp + KC * D * 2);
-  const uint32_t *vid = (const uint32_t *)(vp + KC * D * 2);
-  const int tk = lane;
-  const uint32_t ki = (kid[tk >> 4] >> (2 * (tk & 15))) & 3u;
-  const uint32_t vi = (vid[tk >> 4] >> (2 * (tk & 15))) & 3u;
-  const bool on = (valid >> tk) & 1ull;
-  float cnt[4][4];
-  float used[4];
+  const uint32_t *kid = (const uint32_t *)(ip + KC * D * 2);
+  const uint32_t *vid = (const uint32_t *)(ip + kCentBytes + KC * D * 2);
+  const uint32_t ki = (kid[lane >> 4] >> (2 * (lane & 15))) & 3u;
+  const uint32_t vi = (vid[lane >> 4] >> (2 * (lane & 15))) & 3u;
+  U8 vc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) vc[i].v = kg == 0 ? lds16(ip + kCentBytes + m16 * 64 + 16 * i) : make_uint4(0, 0, 0, 0);
+  const bool on = (valid >> lane) & 1ull;
+  float cnt[4][4], used[4];
 #pragma unroll
   for (int a = 0; a < 4; ++a) {
     float tot = 0.f;
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      cnt[a][v] = (float)__popcll(__ballot(on && ki == (uint32_t)a && vi == (uint32_t)v));
-      tot += cnt[a][v];
+    for (int b = 0; b < 4; ++b) {
+      cnt[a][b] = (float)__popcll(__ballot(on && ki == (uint32_t)a && vi == (uint32_t)b));
+      tot += cnt[a][b];
     }
     used[a] = tot;
   }
@@ -416,207 +671,145 @@ __device__ void visit_centroid(const AttnParams &p, State &st, const half8 *qB, 
 #pragma unroll
   for (int a = 0; a < 4; ++a)
     if (used[a] > 0.f) bm = fmaxf(bm, sc[a]);
-  bm *= p.sl2;
-  const bool need = bm > st.m + kRescale;
-  if (__any(need)) {
-    const float mn = need ? bm : st.m;
-    const float alpha = need ? exp2f(st.m - mn) : 1.0f;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) st.O[j] *= alpha;
-    st.l *= alpha;
-    st.m = mn;
-  }
+  rescale_factor(st, bm * p.sl2);
   float pk[4];
 #pragma unroll
-  for (int a = 0; a < 4; ++a) pk[a] = used[a] > 0.f ? exp2f(fmaf(sc[a], p.sl2, -st.m)) : 0.f;
+  for (int a = 0; a < 4; ++a) pk[a] = used[a] > 0.f ? __builtin_amdgcn_exp2f(fmaf(sc[a], p.sl2, -st.m)) : 0.f;
   _Float16 wh[4];
   float lsum = 0.f;
 #pragma unroll
-  for (int v = 0; v < 4; ++v) {
+  for (int b = 0; b < 4; ++b) {
     float w = 0.f;
 #pragma unroll
-    for (int a = 0; a < 4; ++a) w = fmaf(cnt[a][v], pk[a], w);
-    wh[v] = (_Float16)w;
-    lsum += (float)wh[v];
+    for (int a = 0; a < 4; ++a) w = fmaf(cnt[a][b], pk[a], w);
+    wh[b] = (_Float16)w;
+    lsum += (float)wh[b];
   }
   // O[d][h] += sum_v W[v][h] * vc[v][d]: rows k = 4kg + r, only kg == 0 carries data
   const half4 zero4 = half4{(_Float16)0, (_Float16)0, (_Float16)0, (_Float16)0};
-  const half4 B = kg == 0 ? half4{wh[0], wh[1], wh[2], wh[3]} : zero4;
-  U8 vc[4];
-  {
-    const uint4 *src = (const uint4 *)((const uint16_t *)vp + m16 * 8 * KC);
+  const half4 Bw = kg == 0 ? half4{wh[0], wh[1], wh[2], wh[3]} : zero4;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) vc[i].v = kg == 0 ? src[i] : make_uint4(0, 0, 0, 0);
-  }
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    U4 a;
-    a.u[0] = vc[j >> 1].u[2 * (j & 1)];
-    a.u[1] = vc[j >> 1].u[2 * (j & 1) + 1];
-    st.O[j] = mfma16(a.h, B, st.O[j]);
-  }
+  for (int j = 0; j < 8; ++j)
+    st.O[j] = mfma16(as_h4(vc[j >> 1].u[2 * (j & 1)], vc[j >> 1].u[2 * (j & 1) + 1]), Bw, st.O[j]);
   st.l += lsum;
 }
 
-__device__ __forceinline__ uint32_t visit_cost(int level) {  // 16-byte units of K + V
-  return (uint32_t)(2 * block_bytes(level) / 16);
+// Runs: process items of one level until the next item has another level (left in
+// `it`, already popped) or the sequence ends (returns false).
+__device__ __forceinline__ bool exact_run(const AttnParams &p, State &st, const uint8_t *qs, Pipe &pp,
+                                          Item &it, uint64_t &valid, const uint8_t *&ip, int lane) {
+  do {
+    exact_tile(p, st, qs, ip, it.tvalid(), lane);
+    pp.release(it);
+    if (!pp.pop(it, valid, ip)) return false;
+  } while (it.lv() == GKV_EXACT);
+  return true;
 }
 
-__device__ void do_visit(const AttnParams &p, State &st, const half8 *qB, int lv, const uint8_t *kp,
-                         const uint8_t *vp, int tiles, uint64_t valid, int lane) {
-  switch (lv) {
-    case GKV_EXACT: visit_exact(p, st, qB, kp, vp, tiles, valid, lane); break;
-    case GKV_INT8: visit_int<8>(p, st, qB, kp, vp, tiles, valid, lane); break;
-    case GKV_INT4: visit_int<4>(p, st, qB, kp, vp, tiles, valid, lane); break;
-    case GKV_INT2: visit_int<2>(p, st, qB, kp, vp, tiles, valid, lane); break;
-    default: visit_centroid(p, st, qB, kp, vp, valid, lane); break;
-  }
+template <int BITS>
+__device__ __forceinline__ bool int_run(const AttnParams &p, State &st, const uint8_t *qs, Pipe &pp,
+                                        Item &it, uint64_t &valid, const uint8_t *&ip, int lane) {
+  IntBlock ib;
+  do {
+    if (it.kind() == kHeader) int_header<BITS>(ib, qs, ip, lane);
+    else int_tile<BITS>(p, st, ib, ip, it.tvalid(), it.last(), lane);
+    pp.release(it);
+    if (!pp.pop(it, valid, ip)) return false;
+  } while (it.lv() == BITS);
+  return true;
 }
 
-__device__ __forceinline__ uint64_t tile_bits(int tiles) {
-  uint64_t m = 0;
-  for (int t = 0; t < 4; ++t)
-    if (tiles & (1 << t)) m |= 0xFFFFull << (16 * t);
-  return m;
+__device__ __forceinline__ bool centroid_run(const AttnParams &p, State &st, const uint8_t *qs, Pipe &pp,
+                                             Item &it, uint64_t &valid, const uint8_t *&ip,
+                                             int lane) {
+  do {
+    centroid_item(p, st, qs, ip, valid, lane);
+    pp.release(it);
+    if (!pp.pop(it, valid, ip)) return false;
+  } while (it.lv() == GKV_CENTROID);
+  return true;
 }
 
-__device__ __forceinline__ int tiles_of(uint64_t valid) {
-  int t = 0;
-  for (int i = 0; i < 4; ++i)
-    if ((valid >> (16 * i)) & 0xFFFFull) t |= 1 << i;
-  return t;
-}
-
-__global__ void __launch_bounds__(kThreads) attn_kernel(AttnParams p) {
+__global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
+  extern __shared__ __align__(16) uint8_t smem[];
   const int sidx = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int kg = lane >> 4, m16 = lane & 15;
   const int64_t u = (int64_t)b * p.Hkv + h;
   const int W = p.nsplit * kWaves, w = sidx * kWaves + wave;
-  const int64_t nblk = (p.T + P - 1) / P;
 
-  half8 qB[4];
-  {
-    const bool hv = m16 < p.G;
-    const uint16_t *qrow = p.q + (u * p.G + (hv ? m16 : 0)) * D + 8 * kg;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      U8 t;
-      t.v = hv ? *(const uint4 *)(qrow + 32 * i) : make_uint4(0, 0, 0, 0);
-      qB[i] = t.h;
-    }
+  // the group's queries (rows of absent heads are zero)
+  uint8_t *qs = smem + kWaves * kWaveLds;
+  for (int i = threadIdx.x; i < 16 * (D / 8); i += kThreads) {
+    const int g = i / (D / 8), c8 = (i % (D / 8)) * 8;
+    const uint4 v = g < p.G ? *(const uint4 *)(p.q + (u * p.G + g) * D + c8) : make_uint4(0, 0, 0, 0);
+    *(uint4 *)(qs + g * kQRow + c8 * 2) = v;
   }
+  __syncthreads();
   State st;
 #pragma unroll
   for (int j = 0; j < 8; ++j) st.O[j] = f4{0, 0, 0, 0};
   st.m = kNegInf;
   st.l = 0.f;
 
-  const int8_t *lvl = p.level + u * p.nblk_cap;
-  const int64_t *ko = p.koff + u * p.nblk_cap;
-  const int64_t *vo = p.voff + u * p.nblk_cap;
+  // this wavefront's visits, from the plan
+  const int32_t *sp = p.split + u * (int64_t)(W + 1);
+  const uint32_t vstart = (uint32_t)uni(sp[w]), vend = (uint32_t)uni(sp[w + 1]);
 
-  if (p.pages == nullptr) {
-    // ---------------- dense read: blocks 0..nblk-1, then residual pseudo-blocks
-    const int nrb = (p.nres + P - 1) / P;
-    const int64_t nvis = nblk + nrb;
-    uint64_t total = 0;
-    for (int64_t base = 0; base < nvis; base += 64) {
-      const int64_t v = base + lane;
-      uint32_t c = 0;
-      if (v < nvis) c = v < nblk ? visit_cost(lvl[v]) : visit_cost(GKV_EXACT);
-      for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o);
-      total += c;
-    }
-    // visit v belongs to wavefront floor(W * (prefix + cost/2) / total)
-    int64_t v0 = nvis, v1 = nvis;
-    uint64_t run = 0;
-    for (int64_t base = 0; base < nvis; base += 64) {
-      const int64_t v = base + lane;
-      uint32_t c = 0;
-      if (v < nvis) c = v < nblk ? visit_cost(lvl[v]) : visit_cost(GKV_EXACT);
-      uint32_t incl = c;
-      for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t y = __shfl_up(incl, o);
-        if (lane >= o) incl += y;
-      }
-      const uint64_t excl = run + incl - c;
-      const int64_t own = v < nvis ? (int64_t)(((uint64_t)W * (2 * excl + c)) / (2 * total)) : (int64_t)W;
-      const uint64_t ge0 = __ballot(own >= w), ge1 = __ballot(own >= w + 1);
-      if (ge0 && v0 == nvis) v0 = base + __ffsll((long long)ge0) - 1;
-      if (ge1) {
-        v1 = base + __ffsll((long long)ge1) - 1;
-        break;
-      }
-      run += __shfl(incl, 63);
-    }
-    for (int64_t v = v0; v < v1; ++v) {
-      int lv;
-      const uint8_t *kp, *vp;
-      uint64_t valid;
-      if (v < nblk) {
-        lv = lvl[v];
-        kp = p.arena + ko[v];
-        vp = p.arena + vo[v];
-        const int64_t left = p.T - v * P;
-        valid = left >= P ? ~0ull : ((1ull << left) - 1);
-        if (p.nres) valid &= ~p.res_mask[u * p.nblk_cap + v];
-      } else {
-        const int64_t rb = v - nblk;
-        lv = GKV_EXACT;
-        kp = p.res_rows + (u * p.nrb_cap + rb) * (2 * kExactBytes);
-        vp = kp + kExactBytes;
-        const int64_t left = p.nres - rb * P;
-        valid = left >= P ? ~0ull : ((1ull << left) - 1);
-      }
-      const int tiles = tiles_of(valid);
-      if (tiles) do_visit(p, st, qB, lv, kp, vp, tiles, valid, lane);
-    }
-  } else {
-    // ---------------- Compressed-Quest read: selected pages (ascending) + current page
-    const int32_t *pg = p.pages + u * p.topk;
-    const int64_t cur = (p.T - 1) / 16;
-    int cnt = 0;  // leading entries that are valid ranked pages
-    for (int base = 0; base < p.topk; base += 64) {
-      const int i = base + lane;
-      const bool bad = i < p.topk && (pg[i] < 0 || pg[i] >= cur);
-      const uint64_t bb = __ballot(bad);
-      if (bb) {
-        cnt = base + __ffsll((long long)bb) - 1;
-        break;
-      }
-      cnt = base + 64 < p.topk ? base + 64 : p.topk;
-    }
-    const int n = cnt + 1;
-    const int e0 = (int)(((int64_t)n * w) / W), e1 = (int)(((int64_t)n * (w + 1)) / W);
-    int64_t cblk = -1;
-    int tiles = 0;
-    for (int e = e0; e <= e1; ++e) {
-      int64_t page = -1;
-      if (e < e1) page = e < cnt ? pg[e] : cur;
-      const int64_t blk = page >= 0 ? page >> 2 : -1;
-      if (blk != cblk && cblk >= 0) {
-        const int64_t left = p.T - cblk * P;
-        uint64_t valid = tile_bits(tiles);
-        if (left < P) valid &= (1ull << left) - 1;
-        do_visit(p, st, qB, lvl[cblk], p.arena + ko[cblk], p.arena + vo[cblk], tiles_of(valid), valid, lane);
-        tiles = 0;
-      }
-      cblk = blk;
-      if (page >= 0) tiles |= 1 << (page & 3);
+  // ---------------- pipelined item loop
+  Pipe pp;
+  pp.prod.dsrc = p.plan + (u * p.vcap + vstart) * (int64_t)sizeof(VisitDesc);
+  pp.prod.dring = smem + wave * kWaveLds + kRing + kQueueBytes;
+  pp.prod.dlds = (uint32_t)(uintptr_t)pp.prod.dring;
+  pp.prod.dcnt0 = pp.prod.dcnt1 = 0;
+  pp.prod.v = 0;
+  pp.prod.nv = vend - vstart;
+  pp.prod.lin = 0;
+  pp.prod.cnt = 0;
+  pp.prod.in_visit = false;
+  pp.prod.need_header = false;
+  pp.prod.tiles = 0;
+  pp.prod.lv = 0;
+  pp.prod.valid = 0;
+  pp.prod.kp = pp.prod.vp = nullptr;
+  pp.ring = smem + wave * kWaveLds;
+  pp.queue = (uint32_t *)(smem + wave * kWaveLds + kRing);
+  pp.ring_base = (uint32_t)(uintptr_t)pp.ring;
+  pp.lane = lane;
+  pp.issued = 0;
+  pp.hold = 0;
+  pp.head = pp.tail = 0;
+  if (pp.prod.nv) pp.prod.fetch_chunk(0, lane);
+  pp.has_pend = pp.prod.next(pp.pend, lane);
+  // Items are processed in runs of one level, each run in a loop specialised for
+  // that level (the constants of one level's path are then live only in its loop).
+  Item it;
+  uint64_t valid;
+  const uint8_t *ip;
+  bool more = pp.pop(it, valid, ip);
+  while (more) {
+    switch (it.lv()) {
+      case GKV_EXACT: more = exact_run(p, st, qs, pp, it, valid, ip, lane); break;
+      case GKV_INT8: more = int_run<8>(p, st, qs, pp, it, valid, ip, lane); break;
+      case GKV_INT4: more = int_run<4>(p, st, qs, pp, it, valid, ip, lane); break;
+      case GKV_INT2: more = int_run<2>(p, st, qs, pp, it, valid, ip, lane); break;
+      default: more = centroid_run(p, st, qs, pp, it, valid, ip, lane); break;
     }
   }
+  vm_wait<0>();
 
   // ---------------- merge the four wavefronts and write one partial per head
-  __shared__ float so[kWaves][16][D + 1];
-  __shared__ float sm[kWaves][16], sl[kWaves][16];
+  __syncthreads();
+  float(*so)[16][D + 1] = (float(*)[16][D + 1])smem;
+  float *sm = (float *)(smem + kWaves * 16 * (D + 1) * 4);
+  float *sl = sm + kWaves * 16;
 #pragma unroll
   for (int j = 0; j < 8; ++j)
 #pragma unroll
     for (int r = 0; r < 4; ++r) so[wave][m16][16 * j + 4 * kg + r] = st.O[j][r];
   if (kg == 0) {
-    sm[wave][m16] = st.m;
-    sl[wave][m16] = st.l;
+    sm[wave * 16 + m16] = st.m;
+    sl[wave * 16 + m16] = st.l;
   }
   __syncthreads();
   float *out = p.part + (u * p.nsplit + sidx) * (int64_t)p.G * (D + 2);
@@ -624,13 +817,13 @@ __global__ void __launch_bounds__(kThreads) attn_kernel(AttnParams p) {
     const int g = i >> 7, d = i & 127;
     float M = kNegInf;
 #pragma unroll
-    for (int q = 0; q < kWaves; ++q) M = fmaxf(M, sm[q][g]);
+    for (int q = 0; q < kWaves; ++q) M = fmaxf(M, sm[q * 16 + g]);
     float L = 0.f, o = 0.f;
     if (M > kNegInf) {
 #pragma unroll
       for (int q = 0; q < kWaves; ++q) {
-        const float a = exp2f(sm[q][g] - M);
-        L = fmaf(sl[q][g], a, L);
+        const float a = __builtin_amdgcn_exp2f(sm[q * 16 + g] - M);
+        L = fmaf(sl[q * 16 + g], a, L);
         o = fmaf(so[q][g][d], a, o);
       }
     }
@@ -641,44 +834,206 @@ __global__ void __launch_bounds__(kThreads) attn_kernel(AttnParams p) {
     }
   }
   // ---------------- the last workgroup of this (b, KV head) merges all partials
-  __shared__ int last;
+  int *last = (int *)(sl + kWaves * 16);  // after the merge buffers, inside the ring space
   __threadfence();
   __syncthreads();
-  if (threadIdx.x == 0) last = atomicAdd(p.arrive + u, 1u) == (uint32_t)(p.nsplit - 1);
+  if (threadIdx.x == 0) *last = atomicAdd(p.arrive + u, 1u) == (uint32_t)(p.nsplit - 1);
   __syncthreads();
-  if (!last) return;
+  if (!*last) return;
   __threadfence();
   const float *base = p.part + u * p.nsplit * (int64_t)p.G * (D + 2);
   const int64_t stride = (int64_t)p.G * (D + 2);
   for (int i = threadIdx.x; i < p.G * D; i += kThreads) {
     const int g = i >> 7, d = i & 127;
-    const float *pg = base + g * (D + 2);
+    const float *pgp = base + g * (D + 2);
     float M = kNegInf;
-    for (int s = 0; s < p.nsplit; ++s) M = fmaxf(M, __builtin_nontemporal_load(pg + s * stride));
+    for (int s = 0; s < p.nsplit; ++s) M = fmaxf(M, __builtin_nontemporal_load(pgp + s * stride));
     float L = 0.f, o = 0.f;
     for (int s = 0; s < p.nsplit; ++s) {
-      const float ms = __builtin_nontemporal_load(pg + s * stride);
+      const float ms = __builtin_nontemporal_load(pgp + s * stride);
       if (ms == kNegInf) continue;
-      const float a = exp2f(ms - M);
-      L = fmaf(__builtin_nontemporal_load(pg + s * stride + 1), a, L);
-      o = fmaf(__builtin_nontemporal_load(pg + s * stride + 2 + d), a, o);
+      const float a = __builtin_amdgcn_exp2f(ms - M);
+      L = fmaf(__builtin_nontemporal_load(pgp + s * stride + 1), a, L);
+      o = fmaf(__builtin_nontemporal_load(pgp + s * stride + 2 + d), a, o);
     }
     p.out[(u * p.G + g) * D + d] = o / L;
   }
   if (threadIdx.x == 0) p.arrive[u] = 0;  // leave the counter ready for the next call
 }
 
+// ---------------------------------------------------------------- plan
+// One workgroup per (b, KV head): writes the visit descriptors in visit order and
+// splits the visits over the W wavefronts by a cost that counts the bytes read and
+// a fixed cost per pipeline item (visit v goes to the wavefront that owns the
+// midpoint of its cost interval).
+constexpr int kPlanThreads = 1024;
+constexpr uint32_t kItemCost = 48;  // per-item pipeline cost, in 16-byte units
+
+__device__ __forceinline__ uint32_t balance_cost(int lv, uint64_t va) {
+  uint32_t tiles = 0;
+  for (int t = 0; t < 4; ++t) tiles += ((va >> (16 * t)) & 0xFFFFull) != 0;
+  if (!tiles) return 0;
+  if (lv == GKV_CENTROID) return 2 * kCentBytes / 16 + kItemCost;
+  if (lv == GKV_EXACT) return tiles * (2 * 4096 / 16 + kItemCost);
+  return 2 * (kSZBytes / 16) + kItemCost + tiles * (32 * lv + kItemCost);
+}
+
+__device__ __forceinline__ uint64_t token_mask(int64_t left) {  // tokens of a block below `left`
+  return left >= P ? ~0ull : ((1ull << left) - 1);
+}
+
+// Inclusive scan over the workgroup; `total` receives the sum over all threads.
+__device__ __forceinline__ uint64_t block_scan(uint64_t x, uint64_t *sh, uint64_t &total) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  constexpr int NW = kPlanThreads / 64;
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint64_t y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) sh[wv] = x;
+  __syncthreads();
+  if (wv == 0) {
+    uint64_t t = lane < NW ? sh[lane] : 0;
+    for (int o = 1; o < NW; o <<= 1) {
+      const uint64_t y = __shfl_up(t, o);
+      if (lane >= o) t += y;
+    }
+    if (lane < NW) sh[NW + lane] = t;
+  }
+  __syncthreads();
+  const uint64_t before = wv ? sh[NW + wv - 1] : 0;
+  total = sh[2 * NW - 1];
+  __syncthreads();
+  return x + before;
+}
+
+__global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
+  __shared__ uint64_t sh[2 * kPlanThreads / 64];
+  __shared__ int s_cnt;
+  const int64_t u = blockIdx.x;
+  const int W = p.nsplit * kWaves;
+  VisitDesc *desc = (VisitDesc *)p.plan + u * p.vcap;
+  int32_t *split = p.split + u * (int64_t)(W + 1);
+  const int64_t nblk = (p.T + P - 1) / P;
+  const int8_t *lvl = p.level + u * p.nblk_cap;
+  const int64_t *ko = p.koff + u * p.nblk_cap, *vo = p.voff + u * p.nblk_cap;
+  int64_t nvis;
+  if (!p.pages) {
+    // dense: blocks 0..nblk-1, then the residual rows as exact pseudo-blocks
+    nvis = nblk + (p.nres + P - 1) / P;
+    for (int64_t v = threadIdx.x; v < nvis; v += kPlanThreads) {
+      VisitDesc d;
+      if (v < nblk) {
+        d.level = lvl[v];
+        d.kp = (uint64_t)(uintptr_t)(p.arena + ko[v]);
+        d.vp = (uint64_t)(uintptr_t)(p.arena + vo[v]);
+        d.valid = token_mask(p.T - v * P);
+        if (p.nres) d.valid &= ~p.res_mask[u * p.nblk_cap + v];
+      } else {
+        const int64_t rb = v - nblk;
+        const uint8_t *kp = p.res_rows + (u * p.nrb_cap + rb) * (2 * kExactBytes);
+        d.level = GKV_EXACT;
+        d.kp = (uint64_t)(uintptr_t)kp;
+        d.vp = (uint64_t)(uintptr_t)(kp + kExactBytes);
+        d.valid = token_mask(p.nres - rb * P);
+      }
+      d.cost = balance_cost(d.level, d.valid);
+      desc[v] = d;
+    }
+  } else {
+    // Compressed-Quest: the leading valid ranked pages (ascending) and the current
+    // page; consecutive pages of one block form one visit
+    const int32_t *pg = p.pages + u * p.topk;
+    const int64_t cur = (p.T - 1) / 16;
+    if (threadIdx.x == 0) s_cnt = p.topk;
+    __syncthreads();
+    for (int i = threadIdx.x; i < p.topk; i += kPlanThreads)
+      if (pg[i] < 0 || pg[i] >= cur) atomicMin(&s_cnt, i);
+    __syncthreads();
+    const int cnt = s_cnt;
+    const int n = cnt + 1;
+    uint64_t vbase = 0;
+    for (int base = 0; base < n; base += kPlanThreads) {
+      const int i = base + threadIdx.x;
+      int64_t blk = -1;
+      bool start = false;
+      if (i < n) {
+        blk = (i < cnt ? pg[i] : cur) >> 2;
+        start = i == 0 || ((i - 1 < cnt ? pg[i - 1] : cur) >> 2) != blk;
+      }
+      uint64_t tot;
+      const uint64_t incl = block_scan(start ? 1 : 0, sh, tot);
+      if (start) {
+        uint32_t tl = 0;
+        for (int j = i; j < n; ++j) {
+          const int64_t pj = j < cnt ? pg[j] : cur;
+          if ((pj >> 2) != blk) break;
+          tl |= 1u << (pj & 3);
+        }
+        VisitDesc d;
+        d.level = lvl[blk];
+        d.kp = (uint64_t)(uintptr_t)(p.arena + ko[blk]);
+        d.vp = (uint64_t)(uintptr_t)(p.arena + vo[blk]);
+        uint64_t va = 0;
+        for (int t = 0; t < 4; ++t)
+          if (tl & (1u << t)) va |= 0xFFFFull << (16 * t);
+        d.valid = va & token_mask(p.T - blk * P);
+        d.cost = balance_cost(d.level, d.valid);
+        desc[vbase + incl - 1] = d;
+      }
+      vbase += tot;
+    }
+    nvis = (int64_t)vbase;
+  }
+  __syncthreads();
+  // total cost, then the owner of every visit
+  uint64_t total = 0;
+  for (int64_t base = 0; base < nvis; base += kPlanThreads) {
+    const int64_t v = base + threadIdx.x;
+    uint64_t tot;
+    block_scan(v < nvis ? desc[v].cost : 0u, sh, tot);
+    total += tot;
+  }
+  auto owner = [&](uint64_t excl, uint32_t c) -> int {
+    if (!total) return 0;
+    const uint64_t o = ((uint64_t)W * (2 * excl + c)) / (2 * total);
+    return o < (uint64_t)W ? (int)o : W - 1;
+  };
+  uint64_t carry = 0;
+  for (int64_t base = 0; base < nvis; base += kPlanThreads) {
+    const int64_t v = base + threadIdx.x;
+    const uint32_t c = v < nvis ? desc[v].cost : 0u;
+    uint64_t tot;
+    const uint64_t excl = carry + block_scan(c, sh, tot) - c;
+    if (v < nvis) {
+      const int own = owner(excl, c);
+      int prev = -1;
+      if (v > 0) {
+        const uint32_t cp = desc[v - 1].cost;
+        prev = owner(excl - cp, cp);
+      }
+      for (int ww = prev + 1; ww <= own; ++ww) split[ww] = (int32_t)v;
+      if (v == nvis - 1)
+        for (int ww = own + 1; ww <= W; ++ww) split[ww] = (int32_t)nvis;
+    }
+    carry += tot;
+  }
+  if (nvis == 0)
+    for (int ww = threadIdx.x; ww <= W; ww += kPlanThreads) split[ww] = 0;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------- C ABI
-static int attn_nsplit(const gkv_cache *c, int32_t topk) {
+// Workgroups per (b, KV head) for a call at context length T: enough wavefronts to
+// fill the chip (2048 over all (b, KV head)), at most one per visit.
+static int attn_nsplit(const gkv_cache *c, int32_t topk, int64_t T) {
   const int64_t units = (int64_t)c->B * c->Hkv;
-  const int64_t nblk = (c->T + P - 1) / P;
   int64_t waves;
   if (topk > 0) {
     waves = (topk + 1 + 3) / 4;
   } else {
-    const int64_t nvis = nblk + (c->nres_cap + P - 1) / P;
+    const int64_t nvis = (T + P - 1) / P + (c->nres_cap + P - 1) / P;
     waves = 2048 / units;
     if (waves > nvis) waves = nvis;
   }
@@ -687,14 +1042,28 @@ static int attn_nsplit(const gkv_cache *c, int32_t topk) {
   return (int)((waves + kWaves - 1) / kWaves);
 }
 
-static int64_t attn_part_bytes(const gkv_cache *c, int32_t topk) {
+// Workspace layout, sized by the cache capacity so that it does not move as T grows:
+// partials | arrival counters | wavefront splits | visit descriptors (+1 KB: the
+// descriptor copies read whole 1 KB chunks).
+struct AttnLayout {
+  int64_t arrive, split, plan, total, vcap;
+  int ncap;
+};
+static int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
+static AttnLayout attn_layout(const gkv_cache *c, int32_t topk) {
+  AttnLayout L;
+  const int64_t units = (int64_t)c->B * c->Hkv;
   const int G = c->Hq / c->Hkv;
-  return ((int64_t)c->B * c->Hkv * attn_nsplit(c, topk) * G * (D + 2) * 4 + 255) & ~(int64_t)255;
+  L.ncap = attn_nsplit(c, topk, (int64_t)c->nblk_cap * P);
+  L.vcap = topk > 0 ? (int64_t)topk + 1 : (int64_t)c->nblk_cap + (c->nres_cap + P - 1) / P;
+  L.arrive = align256(units * L.ncap * G * (D + 2) * 4);
+  L.split = L.arrive + align256(units * 4);
+  L.plan = L.split + align256(units * ((int64_t)L.ncap * kWaves + 1) * 4);
+  L.total = L.plan + units * L.vcap * (int64_t)sizeof(VisitDesc) + 1024;
+  return L;
 }
 
-int64_t gkv_attn_workspace(const gkv_cache *c, int32_t topk) {
-  return attn_part_bytes(c, topk) + (int64_t)c->B * c->Hkv * 4;
-}
+int64_t gkv_attn_workspace(const gkv_cache *c, int32_t topk) { return attn_layout(c, topk).total; }
 
 extern "C" gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache *c, const int32_t *pages,
                                              int32_t topk, float *out, void *ws, int64_t ws_bytes, void *stream) {
@@ -709,8 +1078,8 @@ extern "C" gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache 
   } else {
     topk = 0;
   }
-  const int64_t need = gkv_attn_workspace(c, topk);
-  if (ws_bytes < need) return GKV_E_WORKSPACE;
+  const AttnLayout L = attn_layout(c, topk);
+  if (ws_bytes < L.total) return GKV_E_WORKSPACE;
   AttnParams p;
   p.q = q;
   p.level = c->level;
@@ -721,7 +1090,10 @@ extern "C" gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache 
   p.res_rows = c->res_rows;
   p.pages = pages;
   p.part = (float *)ws;
-  p.arrive = (uint32_t *)((uint8_t *)ws + attn_part_bytes(c, topk));
+  p.arrive = (uint32_t *)((uint8_t *)ws + L.arrive);
+  p.split = (int32_t *)((uint8_t *)ws + L.split);
+  p.plan = (uint8_t *)ws + L.plan;
+  p.vcap = L.vcap;
   p.out = out;
   p.T = c->T;
   p.nblk_cap = c->nblk_cap;
@@ -730,9 +1102,10 @@ extern "C" gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache 
   p.nres = c->nres;
   p.nrb_cap = (c->nres_cap + P - 1) / P;
   p.topk = topk;
-  p.page = 16;
-  p.nsplit = attn_nsplit(c, topk);
+  p.nsplit = attn_nsplit(c, topk, c->T);
   p.sl2 = 1.4426950408889634f / sqrtf((float)D);
-  hipLaunchKernelGGL(attn_kernel, dim3(p.nsplit, c->Hkv, c->B), dim3(kThreads), 0, (hipStream_t)stream, p);
+  hipLaunchKernelGGL(plan_kernel, dim3(c->B * c->Hkv), dim3(kPlanThreads), 0, (hipStream_t)stream, p);
+  const size_t lds = (size_t)kWaves * kWaveLds + 16 * kQRow;  // rings also hold the merge buffers
+  hipLaunchKernelGGL(attn_kernel, dim3(p.nsplit, c->Hkv, c->B), dim3(kThreads), lds, (hipStream_t)stream, p);
   return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP;
 }
