@@ -175,10 +175,10 @@ gkv_status gkv_decode_record(int32_t level, int32_t tensor, const uint8_t *rec_h
 uint16_t gkv_f64_to_f16(double x);
 
 /* Workspace bytes needed by gkv_quest_select (op 0), gkv_graded_decode_attn (op 1,
- * topk = 0 for a dense read) and gkv_rd_residual_select (op 2).  The attention
- * workspace holds per-(b, KV head) arrival counters: zero-fill it before its first
- * use; every call leaves the counters at zero again.  Calls that run concurrently
- * need separate workspaces. */
+ * topk = 0 for a dense read) and gkv_rd_residual_select (op 2).  The size depends on
+ * the cache's capacities (not on T), so one workspace serves a cache as it grows.
+ * Workspaces need no initialisation; calls that run concurrently need separate
+ * workspaces. */
 int64_t gkv_workspace_bytes(const gkv_cache *c, int32_t op, int32_t topk);
 
 /* ---------------------------------------------------------------- device calls */

@@ -1,15 +1,15 @@
 // Fused dequant + online-softmax GQA decode attention over a graded cache
 // (sections 3.1, 3.5 and 3.7), and the split-context reduction.
 //
-// Two kernels per call.  The plan kernel (one workgroup per (b, KV head)) writes a
+// Three kernels per call.  The plan kernel (one workgroup per (b, KV head)) writes a
 // 32-byte descriptor per "visit" (a block and the tokens of it that are read: all
 // valid tokens of a dense read minus the residual rows, or the selected pages of a
 // Compressed-Quest read) and splits the visits over the wavefronts by a cost that
 // counts bytes and pipeline items.  The attention kernel runs grid (nsplit, Hkv, B)
 // x 4 wavefronts; each wavefront keeps an online-softmax state for the up-to-16
 // query heads of the group in MFMA accumulator layout; the four wavefronts of a
-// workgroup are merged in LDS into one partial (m, l, o) per head and the last
-// workgroup of a (b, KV head) to finish merges the partials.
+// workgroup are merged in LDS into one partial (m, l, o) per head, and a merge
+// kernel combines the partials of each (b, KV head).
 //
 // Memory pipeline: a visit is a sequence of "items" (an int block's key
 // scale/zero, a 16-token K+V tile, a centroid block).  A producer cursor walks the
@@ -162,19 +162,19 @@ struct AttnParams {
   uint8_t *plan;   // visit descriptors, vcap per (b, KV head)
   int32_t *split;  // first visit of each wavefront, W + 1 per (b, KV head)
   float *part;
-  uint32_t *arrive;  // per (b, KV head) arrival counters; zero between calls
-  float *out;
   int64_t T;
   int nblk_cap, Hkv, G, nres, nrb_cap, topk, nsplit;
   int64_t vcap;
   float sl2;  // log2(e) / sqrt(D)
 };
 
-constexpr int kRing = 14592;    // staging ring per wavefront (bytes)
+constexpr int kRing = 16384;    // staging ring per wavefront (bytes, a power of two)
 constexpr int kQueue = 16;      // item descriptors in flight per wavefront
 constexpr int kQueueBytes = 32 * kQueue;
 constexpr int kDescBytes = 2048;  // visit-descriptor ring: two 1 KB chunks
 constexpr int kWaveLds = kRing + kQueueBytes + kDescBytes;  // LDS per wavefront
+constexpr int kMaxWaves = 1024;   // wavefronts per (b, KV head)
+
 
 // ---------------------------------------------------------------- async copies
 __device__ __forceinline__ void dma16(const void *g, uint32_t lds_wave_base) {
@@ -211,30 +211,33 @@ __device__ __forceinline__ int64_t uni64(int64_t x) {
 }
 
 // ---------------------------------------------------------------- item sequence
-enum ItemKind { kHeader = 0, kTile = 1, kCentroid = 2 };
+// An item is one unit of the pipeline: a contiguous span of the ring filled by up
+// to four copy segments, and one step of the consumer.
+//   exact tile:   [K tile 4 KB][V tile 4 KB]
+//   int group:    [K scale/zero if first][K codes of n tiles][V codes of n tiles]
+//                 [V scale/zero if last]   (n consecutive read tiles of one block)
+//   centroid:     [K record][V record]
+enum ItemKind { kExactTile = 0, kIntGroup = 1, kCentroid = 2 };
 
-// An item: a 16-byte-aligned span of the ring filled by ceil(bytes/1024) copies.
-// meta packs kind (2 bits), level (5), tile (2), last-of-visit (1) and the tile's
-// valid-token bits (16).
+// meta: kind (2 bits) | level (5) | first (1) | last (1) | tile mask (4) | tile
+// count (3) | exact tile's valid-token bits (16)
 struct Item {
-  uint32_t lin;      // linear ring position (bytes)
+  uint32_t lin;      // linear ring position of the item (bytes)
+  uint32_t end;      // linear ring position after it
   uint32_t cnt_end;  // load instructions issued through this item
   uint32_t meta;
+  uint32_t koff, kun, voff, vun;  // producer only: code segments (offset in record, 16-byte units)
   __device__ int kind() const { return meta & 3u; }
   __device__ int lv() const { return (meta >> 2) & 31u; }
-  __device__ int tile() const { return (meta >> 7) & 3u; }
-  __device__ bool last() const { return (meta >> 9) & 1u; }
+  __device__ bool first() const { return (meta >> 7) & 1u; }
+  __device__ bool last() const { return (meta >> 8) & 1u; }
+  __device__ uint32_t tiles() const { return (meta >> 9) & 15u; }
+  __device__ int ntiles() const { return (meta >> 13) & 7u; }
   __device__ uint32_t tvalid() const { return meta >> 16; }
 };
 
-// Item sizes: an int block's header carries the key scale/zero; its last tile also
-// carries the value scale/zero, used by the block epilogue.
-__device__ __forceinline__ uint32_t item_bytes(int kind, int lv, bool last) {
-  if (kind == kCentroid) return 2 * kCentBytes;
-  if (kind == kHeader) return kSZBytes;
-  if (lv == GKV_EXACT) return 2 * 4096;
-  return 2 * 256 * lv + (last ? kSZBytes : 0);
-}
+// Consecutive read tiles per int item: about 4 KB of codes (K + V).
+__device__ __forceinline__ int group_tiles(int lv) { return lv == 2 ? 4 : (lv == 4 ? 2 : 1); }
 
 // A visit: one block of one (b, KV head) and the tokens of it that are read.  The
 // plan kernel writes one 32-byte descriptor per visit, in visit order, and the
@@ -252,17 +255,17 @@ constexpr int kDescChunk = 1024 / sizeof(VisitDesc);  // descriptors per copy (o
 // descriptors stream through a two-slot LDS ring, one 1 KB chunk per copy, each
 // chunk requested one chunk ahead of its first use.
 struct Walker {
-  const uint8_t *dsrc;  // descriptors of this wavefront's visits
+  const uint8_t *dsrc;   // descriptors of this wavefront's visits
   const uint8_t *dring;  // the descriptor ring (2 x 1 KB of LDS)
-  uint32_t dlds;        // its LDS address
+  uint32_t dlds;         // its LDS address
   uint32_t dcnt0, dcnt1;  // load count through the copy of each slot's chunk
-  uint32_t v, nv;       // next visit (relative), number of visits
+  uint32_t v, nv;         // next visit (relative), number of visits
   const uint8_t *kp, *vp;
   uint64_t valid;
   uint32_t lin, cnt;  // ring position and loads issued, both through the last item
   int lv;
-  uint32_t tiles;  // tiles still to emit
-  bool in_visit, need_header;
+  uint32_t tiles;  // read tiles not yet emitted
+  bool in_visit, first;
 
   __device__ __forceinline__ void fetch_chunk(uint32_t c, int lane) {  // copy descriptor chunk c
     dma16(dsrc + (size_t)c * 1024 + 16 * lane, dlds + (c & 1) * 1024);
@@ -285,14 +288,13 @@ struct Walker {
       const uint4 d0 = *(const uint4 *)e, d1 = *(const uint4 *)(e + 16);
       kp = (const uint8_t *)(uintptr_t)uni64((int64_t)(((uint64_t)d0.y << 32) | d0.x));
       vp = (const uint8_t *)(uintptr_t)uni64((int64_t)(((uint64_t)d0.w << 32) | d0.z));
-      const uint64_t va = (uint64_t)uni64((int64_t)(((uint64_t)d1.y << 32) | d1.x));
+      valid = (uint64_t)uni64((int64_t)(((uint64_t)d1.y << 32) | d1.x));
       lv = uni((int32_t)d1.z);
-      valid = va;
       tiles = 0;
       for (int t = 0; t < 4; ++t)
-        if ((va >> (16 * t)) & 0xFFFFull) tiles |= 1u << t;
+        if ((valid >> (16 * t)) & 0xFFFFull) tiles |= 1u << t;
       if (!tiles) continue;
-      need_header = lv != GKV_EXACT;
+      first = true;
       in_visit = true;
       return true;
     }
@@ -301,80 +303,86 @@ struct Walker {
 
   __device__ bool next(Item &it, int lane) {
     if (!in_visit && !open_visit(lane)) return false;
-    uint32_t kind, t = 0, last = 0, tv = 0;
+    uint32_t kind, taken, n = 1, tv = 0, size, ninstr;
+    bool f = false, l = true;
     if (lv == GKV_CENTROID) {
       kind = kCentroid;
-      last = 1;
-      in_visit = false;
-    } else if (need_header) {
-      kind = kHeader;
-      need_header = false;
-    } else {
-      kind = kTile;
-      t = __builtin_ctz(tiles);
-      tiles &= tiles - 1;
+      taken = tiles;
+      it.koff = it.voff = 0;
+      it.kun = it.vun = kCentBytes / 16;
+      size = 2 * kCentBytes;
+      ninstr = 2 * ((kCentBytes / 16 + 63) / 64);
+    } else if (lv == GKV_EXACT) {
+      kind = kExactTile;
+      const uint32_t t = __builtin_ctz(tiles);
+      taken = 1u << t;
       tv = (uint32_t)((valid >> (16 * t)) & 0xFFFFull);
-      last = tiles == 0;
-      if (last) in_visit = false;
+      it.koff = it.voff = t * 4096;
+      it.kun = it.vun = 256;
+      size = 2 * 4096;
+      ninstr = 8;
+    } else {
+      kind = kIntGroup;
+      const uint32_t t = __builtin_ctz(tiles);
+      const int tg = group_tiles(lv);
+      while ((int)n < tg && ((tiles >> (t + n)) & 1u)) ++n;
+      taken = ((1u << n) - 1) << t;
+      f = first;
+      it.koff = it.voff = kSZBytes + t * 256 * lv;
+      it.kun = it.vun = n * 16 * lv;
+      const uint32_t cu = n * 16 * lv;  // units per code segment (a multiple of 32)
+      l = (tiles & ~taken) == 0;
+      size = 2 * 16 * cu + (f ? kSZBytes : 0) + (l ? kSZBytes : 0);
+      ninstr = 2 * ((cu + 63) / 64) + (f ? 1 : 0) + (l ? 1 : 0);
     }
-    const uint32_t size = item_bytes(kind, lv, last);
-    const uint32_t off = lin % kRing;
+    tiles &= ~taken;
+    first = false;
+    if (!tiles) in_visit = false;
+    const uint32_t off = lin & (kRing - 1);
     if (off + size > kRing) lin += kRing - off;  // an item never wraps around the ring end
     it.lin = lin;
     lin += size;
-    cnt += (size + 1023) / 1024;
+    it.end = lin;
+    cnt += ninstr;
     it.cnt_end = cnt;
-    it.meta = kind | ((uint32_t)lv << 2) | (t << 7) | (last << 9) | (tv << 16);
+    it.meta = kind | ((uint32_t)lv << 2) | ((uint32_t)f << 7) | ((uint32_t)l << 8) | (taken << 9) | (n << 13) |
+              (tv << 16);
     return true;
   }
 };
 
-// Issue the asynchronous copies of the producer's current item (its K part
-// followed by its V part in LDS).
-__device__ __forceinline__ void issue(const Walker &w, const Item &it, uint32_t ring_base, int lane) {
-  const int kind = it.kind(), lv = it.lv(), t = it.tile();
-  uint32_t kunits, koff;
-  if (kind == kCentroid) {
-    kunits = kCentBytes / 16;
-    koff = 0;
-  } else if (kind == kHeader) {
-    kunits = kSZBytes / 16;
-    koff = 0;
-  } else if (lv == GKV_EXACT) {
-    kunits = 4096 / 16;
-    koff = t * 4096;
-  } else {
-    kunits = 16 * lv;
-    koff = kSZBytes + t * 256 * lv;
-  }
-  // K part, then V part (same offsets), then for an int block's last tile the
-  // value scale/zero; a header has only the key scale/zero
-  const uint32_t vunits = kind == kHeader ? 0 : kunits;
-  const uint32_t xunits = (kind == kTile && lv != GKV_EXACT && it.last()) ? kSZBytes / 16 : 0;
-  const uint32_t units = kunits + vunits + xunits;
-  const uint32_t base = ring_base + it.lin % kRing;
+// Copy `units` 16-byte units from `src` to LDS address `dst` (1 KB per instruction).
+__device__ __forceinline__ void copy_segment(const uint8_t *src, uint32_t units, uint32_t dst, int lane) {
 #pragma unroll 1
-  for (uint32_t i = 0; i * 64 < units; ++i) {
-    const uint32_t uu = i * 64 + lane;
-    if (uu < units) {
-      const uint8_t *src = uu < kunits ? w.kp + koff + 16 * uu
-                           : uu < kunits + vunits ? w.vp + koff + 16 * (uu - kunits)
-                                                  : w.vp + 16 * (uu - kunits - vunits);
-      dma16(src, base + 1024 * i);
-    }
+  for (uint32_t i = 0; i * 64 < units; ++i)
+    if (i * 64 + lane < units) dma16(src + 16 * (i * 64 + lane), dst + 1024 * i);
+}
+
+// Issue the copies of the producer's current item.
+__device__ __forceinline__ void issue(const Walker &w, const Item &it, uint32_t ring_base, int lane) {
+  uint32_t dst = ring_base + (it.lin & (kRing - 1));
+  const bool sz = it.kind() == kIntGroup;
+  if (sz && it.first()) {
+    copy_segment(w.kp, kSZBytes / 16, dst, lane);
+    dst += kSZBytes;
   }
+  copy_segment(w.kp + it.koff, it.kun, dst, lane);
+  dst += 16 * it.kun;
+  copy_segment(w.vp + it.voff, it.vun, dst, lane);
+  dst += 16 * it.vun;
+  if (sz && it.last()) copy_segment(w.vp, kSZBytes / 16, dst, lane);
 }
 
 // ---------------------------------------------------------------- pipeline
 // Producer side of a wavefront's pipeline: the walker, its next item, the ring and
-// a queue of issued item descriptors (lin, cnt_end, meta, -, valid lo, valid hi)
+// a queue of issued item descriptors (lin, end, cnt_end, meta, valid lo, valid hi)
 // that the consumer pops in order.
 struct Pipe {
   Walker prod;
   Item pend;
   bool has_pend;
-  uint32_t issued;  // load instructions issued
-  uint32_t hold;    // ring bytes before this linear position are free
+  uint32_t issued;      // load instructions issued
+  uint32_t hold;        // ring bytes before this linear position are free
   uint32_t head, tail;  // queue indices (popped / pushed)
   uint32_t ring_base;
   const uint8_t *ring;
@@ -382,13 +390,12 @@ struct Pipe {
   int lane;
 
   __device__ __forceinline__ void pump() {
-    while (has_pend && tail - head < (uint32_t)kQueue &&
-           pend.lin + item_bytes(pend.kind(), pend.lv(), pend.last()) - hold <= (uint32_t)kRing) {
+    while (has_pend && tail - head < (uint32_t)kQueue && pend.end - hold <= (uint32_t)kRing) {
       issue(prod, pend, ring_base, lane);
       issued = pend.cnt_end;
       if (lane == 0) {
         uint32_t *q = queue + 8 * (tail % kQueue);
-        *(uint4 *)q = make_uint4(pend.lin, pend.cnt_end, pend.meta, 0u);
+        *(uint4 *)q = make_uint4(pend.lin, pend.end, pend.cnt_end, pend.meta);
         *(uint2 *)(q + 4) = make_uint2((uint32_t)prod.valid, (uint32_t)(prod.valid >> 32));
       }
       ++tail;
@@ -403,17 +410,16 @@ struct Pipe {
     const uint4 e = *(const uint4 *)q;
     const uint2 vv = *(const uint2 *)(q + 4);
     it.lin = uni(e.x);
-    it.cnt_end = uni(e.y);
-    it.meta = uni(e.z);
+    it.end = uni(e.y);
+    it.cnt_end = uni(e.z);
+    it.meta = uni(e.w);
     valid = ((uint64_t)(uint32_t)uni(vv.y) << 32) | (uint32_t)uni(vv.x);
     ++head;
     wait_loads(issued - it.cnt_end);
-    ip = ring + it.lin % kRing;
+    ip = ring + (it.lin & (kRing - 1));
     return true;
   }
-  __device__ __forceinline__ void release(const Item &it) {
-    hold = it.lin + item_bytes(it.kind(), it.lv(), it.last());
-  }
+  __device__ __forceinline__ void release(const Item &it) { hold = it.end; }
 };
 
 // ---------------------------------------------------------------- per-wave state
@@ -557,13 +563,14 @@ __device__ __forceinline__ void int_header(IntBlock &ib, const uint8_t *qs, cons
   ib.pb = f4{0, 0, 0, 0};
 }
 
+// One 16-token tile of an int block: key codes at kt, value codes at vt (LDS).
 template <int BITS>
-__device__ __forceinline__ void int_tile(const AttnParams &p, State &st, IntBlock &ib, const uint8_t *ip,
-                                         uint32_t tvalid, bool last, int lane) {
+__device__ __forceinline__ void int_tile(const AttnParams &p, State &st, IntBlock &ib, const uint8_t *kt,
+                                         const uint8_t *vt, uint32_t tvalid, int lane) {
   constexpr int NW = Unpack<BITS>::kWords;
   const int kg = lane >> 4;
-  const uint8_t *kc = ip + lane * (4 * BITS);
-  const uint8_t *vc = ip + 256 * BITS + lane * (4 * BITS);
+  const uint8_t *kc = kt + lane * (4 * BITS);
+  const uint8_t *vc = vt + lane * (4 * BITS);
   uint32_t kw[NW];
   if (NW >= 4) {
 #pragma unroll
@@ -608,32 +615,34 @@ __device__ __forceinline__ void int_tile(const AttnParams &p, State &st, IntBloc
 #pragma unroll
   for (int j = 0; j < 8; ++j)
     ib.acc[j] = mfma16(as_h4(Unpack<BITS>::pair(vw, 2 * j), Unpack<BITS>::pair(vw, 2 * j + 1)), P4, ib.acc[j]);
-  if (last) {
-    // O[d][h] += s_d * (acc - off * sum p) + z_d * sum p,  d = 16j + 4kg + r;
-    // the value scale/zero follow the last tile's codes in LDS
-    const uint8_t *sz = ip + 512 * BITS + kg * 64;
+}
+
+// End of an int block: O[d][h] += s_d * (acc - off * sum p) + z_d * sum p,
+// d = 16j + 4kg + r, with the value scale/zero at vsz (LDS).
+template <int BITS>
+__device__ __forceinline__ void int_epilogue(State &st, IntBlock &ib, const uint8_t *vsz, int lane) {
+  const uint8_t *sz = vsz + (lane >> 4) * 64;
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {  // two halves keep fewer scale/zero registers live
-      U8 sV[2], zV[2];
+  for (int hh = 0; hh < 2; ++hh) {  // two halves keep fewer scale/zero registers live
+    U8 sV[2], zV[2];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        sV[i].v = lds16(sz + 32 * hh + 16 * i);
-        zV[i].v = lds16(sz + 256 + 32 * hh + 16 * i);
-      }
+    for (int i = 0; i < 2; ++i) {
+      sV[i].v = lds16(sz + 32 * hh + 16 * i);
+      zV[i].v = lds16(sz + 256 + 32 * hh + 16 * i);
+    }
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        const int j = 4 * hh + jj;
-        const float off = v_off<BITS>(j);
+    for (int jj = 0; jj < 4; ++jj) {
+      const int j = 4 * hh + jj;
+      const float off = v_off<BITS>(j);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int n = 4 * jj + r;
-          const float x = fmaf(-off, ib.pb[r], ib.acc[j][r]);
-          st.O[j][r] = fmaf((float)sV[n >> 3].h[n & 7], x, fmaf((float)zV[n >> 3].h[n & 7], ib.pb[r], st.O[j][r]));
-        }
+      for (int r = 0; r < 4; ++r) {
+        const int n = 4 * jj + r;
+        const float x = fmaf(-off, ib.pb[r], ib.acc[j][r]);
+        st.O[j][r] = fmaf((float)sV[n >> 3].h[n & 7], x, fmaf((float)zV[n >> 3].h[n & 7], ib.pb[r], st.O[j][r]));
       }
     }
-    st.l += ib.pb[0];
   }
+  st.l += ib.pb[0];
 }
 
 // Centroid block: one item with both records.
@@ -711,8 +720,22 @@ __device__ __forceinline__ bool int_run(const AttnParams &p, State &st, const ui
                                         Item &it, uint64_t &valid, const uint8_t *&ip, int lane) {
   IntBlock ib;
   do {
-    if (it.kind() == kHeader) int_header<BITS>(ib, qs, ip, lane);
-    else int_tile<BITS>(p, st, ib, ip, it.tvalid(), it.last(), lane);
+    const uint8_t *kq = ip;
+    if (it.first()) {
+      int_header<BITS>(ib, qs, kq, lane);
+      kq += kSZBytes;
+    }
+    const int n = it.ntiles();
+    const uint8_t *vq = kq + n * 256 * BITS;
+    uint32_t tl = it.tiles();
+#pragma unroll 1
+    for (int j = 0; j < n; ++j) {
+      const int t = __builtin_ctz(tl);
+      tl &= tl - 1;
+      int_tile<BITS>(p, st, ib, kq + j * 256 * BITS, vq + j * 256 * BITS, (uint32_t)(valid >> (16 * t)) & 0xFFFFu,
+                     lane);
+    }
+    if (it.last()) int_epilogue<BITS>(st, ib, vq + n * 256 * BITS, lane);
     pp.release(it);
     if (!pp.pop(it, valid, ip)) return false;
   } while (it.lv() == BITS);
@@ -767,7 +790,7 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   pp.prod.lin = 0;
   pp.prod.cnt = 0;
   pp.prod.in_visit = false;
-  pp.prod.need_header = false;
+  pp.prod.first = false;
   pp.prod.tiles = 0;
   pp.prod.lv = 0;
   pp.prod.valid = 0;
@@ -833,32 +856,47 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
       out[g * (D + 2) + 1] = L;
     }
   }
-  // ---------------- the last workgroup of this (b, KV head) merges all partials
-  int *last = (int *)(sl + kWaves * 16);  // after the merge buffers, inside the ring space
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) *last = atomicAdd(p.arrive + u, 1u) == (uint32_t)(p.nsplit - 1);
-  __syncthreads();
-  if (!*last) return;
-  __threadfence();
-  const float *base = p.part + u * p.nsplit * (int64_t)p.G * (D + 2);
-  const int64_t stride = (int64_t)p.G * (D + 2);
-  for (int i = threadIdx.x; i < p.G * D; i += kThreads) {
-    const int g = i >> 7, d = i & 127;
-    const float *pgp = base + g * (D + 2);
-    float M = kNegInf;
-    for (int s = 0; s < p.nsplit; ++s) M = fmaxf(M, __builtin_nontemporal_load(pgp + s * stride));
-    float L = 0.f, o = 0.f;
-    for (int s = 0; s < p.nsplit; ++s) {
-      const float ms = __builtin_nontemporal_load(pgp + s * stride);
-      if (ms == kNegInf) continue;
-      const float a = __builtin_amdgcn_exp2f(ms - M);
-      L = fmaf(__builtin_nontemporal_load(pgp + s * stride + 1), a, L);
-      o = fmaf(__builtin_nontemporal_load(pgp + s * stride + 2 + d), a, o);
-    }
-    p.out[(u * p.G + g) * D + d] = o / L;
+}
+
+// ---------------------------------------------------------------- merge
+// One workgroup per (head, (b, KV head)), one thread per channel: the partials
+// (m_s, l_s, o_s) of the nsplit workgroups combine to o = sum_s a_s o_s / sum_s a_s l_s
+// with a_s = 2^(m_s - max_s m_s).
+__global__ void __launch_bounds__(D) merge_kernel(const float *part, float *out, int nsplit, int G) {
+  __shared__ float sa[kMaxWaves / kWaves], sl[kMaxWaves / kWaves];
+  __shared__ float sinv;
+  const int g = blockIdx.x, d = threadIdx.x;
+  const int64_t u = blockIdx.y;
+  const int64_t stride = (int64_t)G * (D + 2);
+  const float *base = part + u * nsplit * stride + g * (D + 2);
+  for (int s2 = d; s2 < nsplit; s2 += D) {
+    sa[s2] = base[s2 * stride];
+    sl[s2] = base[s2 * stride + 1];
   }
-  if (threadIdx.x == 0) p.arrive[u] = 0;  // leave the counter ready for the next call
+  __syncthreads();
+  if (d == 0) {
+    float M = kNegInf;
+    for (int s2 = 0; s2 < nsplit; ++s2) M = fmaxf(M, sa[s2]);
+    float L = 0.f;
+    for (int s2 = 0; s2 < nsplit; ++s2) {
+      const float a = sa[s2] == kNegInf ? 0.f : __builtin_amdgcn_exp2f(sa[s2] - M);
+      sa[s2] = a;
+      L = fmaf(a, sl[s2], L);
+    }
+    sinv = 1.0f / L;
+  }
+  __syncthreads();
+  float o = 0.f;
+  int s2 = 0;
+  for (; s2 + 8 <= nsplit; s2 += 8) {
+    float v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = base[(s2 + k) * stride + 2 + d];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) o = fmaf(sa[s2 + k], v[k], o);
+  }
+  for (; s2 < nsplit; ++s2) o = fmaf(sa[s2], base[s2 * stride + 2 + d], o);
+  out[(u * G + g) * D + d] = o * sinv;
 }
 
 // ---------------------------------------------------------------- plan
@@ -867,15 +905,37 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
 // a fixed cost per pipeline item (visit v goes to the wavefront that owns the
 // midpoint of its cost interval).
 constexpr int kPlanThreads = 1024;
-constexpr uint32_t kItemCost = 48;  // per-item pipeline cost, in 16-byte units
+// Balance cost of a visit in 16-byte units: the bytes copied, a per-item pipeline
+// cost and the per-tile compute (dequantisation makes an int tile dearer than an
+// exact one), each converted at one wavefront's share of the bandwidth.
+constexpr uint32_t kItemCost = 12, kExactTileCost = 17, kIntTileCost = 45, kCentroidCost = 25;
 
 __device__ __forceinline__ uint32_t balance_cost(int lv, uint64_t va) {
-  uint32_t tiles = 0;
-  for (int t = 0; t < 4; ++t) tiles += ((va >> (16 * t)) & 0xFFFFull) != 0;
+  uint32_t tiles = 0, mask = 0;
+  for (int t = 0; t < 4; ++t)
+    if ((va >> (16 * t)) & 0xFFFFull) {
+      ++tiles;
+      mask |= 1u << t;
+    }
   if (!tiles) return 0;
-  if (lv == GKV_CENTROID) return 2 * kCentBytes / 16 + kItemCost;
-  if (lv == GKV_EXACT) return tiles * (2 * 4096 / 16 + kItemCost);
-  return 2 * (kSZBytes / 16) + kItemCost + tiles * (32 * lv + kItemCost);
+  if (lv == GKV_CENTROID) return 2 * kCentBytes / 16 + kCentroidCost + kItemCost;
+  if (lv == GKV_EXACT) return tiles * (2 * 4096 / 16 + kExactTileCost + kItemCost);
+  // int: items are runs of up to group_tiles(lv) consecutive read tiles
+  uint32_t items = 0;
+  const int tg = group_tiles(lv);
+  for (int t = 0; t < 4;) {
+    if (!((mask >> t) & 1u)) {
+      ++t;
+      continue;
+    }
+    int n = 0;
+    while (t < 4 && ((mask >> t) & 1u) && n < tg) {
+      ++t;
+      ++n;
+    }
+    ++items;
+  }
+  return 2 * (kSZBytes / 16) + items * kItemCost + tiles * (32 * lv + kIntTileCost);
 }
 
 __device__ __forceinline__ uint64_t token_mask(int64_t left) {  // tokens of a block below `left`
@@ -919,9 +979,13 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
   const int64_t *ko = p.koff + u * p.nblk_cap, *vo = p.voff + u * p.nblk_cap;
   int64_t nvis;
   if (!p.pages) {
-    // dense: blocks 0..nblk-1, then the residual rows as exact pseudo-blocks
+    // dense: blocks 0..nblk-1, then the residual rows as exact pseudo-blocks; each
+    // thread describes a contiguous run of visits
     nvis = nblk + (p.nres + P - 1) / P;
-    for (int64_t v = threadIdx.x; v < nvis; v += kPlanThreads) {
+    const int64_t per = (nvis + kPlanThreads - 1) / kPlanThreads;
+    const int64_t v0 = threadIdx.x * per, v1 = v0 + per < nvis ? v0 + per : nvis;
+#pragma unroll 4
+    for (int64_t v = v0; v < v1; ++v) {
       VisitDesc d;
       if (v < nblk) {
         d.level = lvl[v];
@@ -986,40 +1050,39 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
     nvis = (int64_t)vbase;
   }
   __syncthreads();
-  // total cost, then the owner of every visit
-  uint64_t total = 0;
-  for (int64_t base = 0; base < nvis; base += kPlanThreads) {
-    const int64_t v = base + threadIdx.x;
-    uint64_t tot;
-    block_scan(v < nvis ? desc[v].cost : 0u, sh, tot);
-    total += tot;
+  if (nvis == 0) {
+    for (int ww = threadIdx.x; ww <= W; ww += kPlanThreads) split[ww] = 0;
+    return;
   }
-  auto owner = [&](uint64_t excl, uint32_t c) -> int {
+  // prefix cost of each thread's run of visits, then the owner of every visit
+  const int64_t per = (nvis + kPlanThreads - 1) / kPlanThreads;
+  const int64_t v0 = threadIdx.x * per, v1 = v0 + per < nvis ? v0 + per : nvis;
+  uint64_t mine = 0;
+#pragma unroll 4
+  for (int64_t v = v0; v < v1; ++v) mine += desc[v].cost;
+  uint64_t total;
+  uint64_t excl = block_scan(mine, sh, total) - mine;
+  auto owner = [&](uint64_t e, uint32_t c) -> int {
     if (!total) return 0;
-    const uint64_t o = ((uint64_t)W * (2 * excl + c)) / (2 * total);
+    const uint64_t o = ((uint64_t)W * (2 * e + c)) / (2 * total);
     return o < (uint64_t)W ? (int)o : W - 1;
   };
-  uint64_t carry = 0;
-  for (int64_t base = 0; base < nvis; base += kPlanThreads) {
-    const int64_t v = base + threadIdx.x;
-    const uint32_t c = v < nvis ? desc[v].cost : 0u;
-    uint64_t tot;
-    const uint64_t excl = carry + block_scan(c, sh, tot) - c;
-    if (v < nvis) {
+  if (v0 < v1) {
+    int prev = -1;
+    if (v0 > 0) {
+      const uint32_t cp = desc[v0 - 1].cost;
+      prev = owner(excl - cp, cp);
+    }
+    for (int64_t v = v0; v < v1; ++v) {
+      const uint32_t c = desc[v].cost;
       const int own = owner(excl, c);
-      int prev = -1;
-      if (v > 0) {
-        const uint32_t cp = desc[v - 1].cost;
-        prev = owner(excl - cp, cp);
-      }
       for (int ww = prev + 1; ww <= own; ++ww) split[ww] = (int32_t)v;
       if (v == nvis - 1)
         for (int ww = own + 1; ww <= W; ++ww) split[ww] = (int32_t)nvis;
+      prev = own;
+      excl += c;
     }
-    carry += tot;
   }
-  if (nvis == 0)
-    for (int ww = threadIdx.x; ww <= W; ww += kPlanThreads) split[ww] = 0;
 }
 
 }  // namespace
@@ -1038,15 +1101,15 @@ static int attn_nsplit(const gkv_cache *c, int32_t topk, int64_t T) {
     if (waves > nvis) waves = nvis;
   }
   if (waves < 1) waves = 1;
-  if (waves > 4096) waves = 4096;
+  if (waves > kMaxWaves) waves = kMaxWaves;
   return (int)((waves + kWaves - 1) / kWaves);
 }
 
 // Workspace layout, sized by the cache capacity so that it does not move as T grows:
-// partials | arrival counters | wavefront splits | visit descriptors (+1 KB: the
-// descriptor copies read whole 1 KB chunks).
+// partials | wavefront splits | visit descriptors (+1 KB: the descriptor copies
+// read whole 1 KB chunks).
 struct AttnLayout {
-  int64_t arrive, split, plan, total, vcap;
+  int64_t split, plan, total, vcap;
   int ncap;
 };
 static int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
@@ -1056,8 +1119,7 @@ static AttnLayout attn_layout(const gkv_cache *c, int32_t topk) {
   const int G = c->Hq / c->Hkv;
   L.ncap = attn_nsplit(c, topk, (int64_t)c->nblk_cap * P);
   L.vcap = topk > 0 ? (int64_t)topk + 1 : (int64_t)c->nblk_cap + (c->nres_cap + P - 1) / P;
-  L.arrive = align256(units * L.ncap * G * (D + 2) * 4);
-  L.split = L.arrive + align256(units * 4);
+  L.split = align256(units * L.ncap * G * (D + 2) * 4);
   L.plan = L.split + align256(units * ((int64_t)L.ncap * kWaves + 1) * 4);
   L.total = L.plan + units * L.vcap * (int64_t)sizeof(VisitDesc) + 1024;
   return L;
@@ -1090,11 +1152,9 @@ extern "C" gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache 
   p.res_rows = c->res_rows;
   p.pages = pages;
   p.part = (float *)ws;
-  p.arrive = (uint32_t *)((uint8_t *)ws + L.arrive);
   p.split = (int32_t *)((uint8_t *)ws + L.split);
   p.plan = (uint8_t *)ws + L.plan;
   p.vcap = L.vcap;
-  p.out = out;
   p.T = c->T;
   p.nblk_cap = c->nblk_cap;
   p.Hkv = c->Hkv;
@@ -1107,5 +1167,7 @@ extern "C" gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache 
   hipLaunchKernelGGL(plan_kernel, dim3(c->B * c->Hkv), dim3(kPlanThreads), 0, (hipStream_t)stream, p);
   const size_t lds = (size_t)kWaves * kWaveLds + 16 * kQRow;  // rings also hold the merge buffers
   hipLaunchKernelGGL(attn_kernel, dim3(p.nsplit, c->Hkv, c->B), dim3(kThreads), lds, (hipStream_t)stream, p);
+  hipLaunchKernelGGL(merge_kernel, dim3(p.G, c->Hkv * c->B), dim3(D), 0, (hipStream_t)stream, (const float *)p.part,
+                     out, p.nsplit, p.G);
   return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP;
 }
