@@ -75,6 +75,13 @@ __device__ __forceinline__ f4 mfma16(half4 a, half4 b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x16f16(a, b, c, 0, 0, 0);
 }
 __device__ __forceinline__ uint32_t andor(uint32_t x, uint32_t m, uint32_t c) { return (x & m) | c; }
+// max(a, b) for non-NaN operands as one v_max_f32: fmaxf adds NaN-quieting copies of
+// its operands.
+__device__ __forceinline__ float vmax(float a, float b) {
+  float r;
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
 __device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel) {
   return __builtin_amdgcn_perm(hi, lo, sel);
 }
@@ -84,43 +91,49 @@ __device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel)
 constexpr uint32_t M1024 = 0x64646464u;  // byte-wise exponent for perm (1024 + byte)
 constexpr uint32_t E64 = 0x54005400u, E16 = 0x4C004C00u, E4 = 0x44004400u;
 
+// The fp16 exponent words sit in registers (see Mag) so that each pair is one
+// v_and_or_b32: that instruction cannot take two literal constants.
+struct Mag {
+  uint32_t e64, e16, e4;
+};
+
 template <int BITS>
 struct Unpack;
 
 template <>
 struct Unpack<8> {
   static constexpr int kWords = 8;
-  __device__ static uint32_t pair(const uint32_t *w, int q) {  // pair q (0..15) = codes 2q, 2q+1
+  __device__ static uint32_t pair(const uint32_t *w, int q, const Mag &) {  // codes 2q, 2q+1
     return perm(M1024, w[q >> 1], (q & 1) ? 0x04030402u : 0x04010400u);
   }
 };
 template <>
 struct Unpack<4> {
   static constexpr int kWords = 4;
-  __device__ static uint32_t pair(const uint32_t *w, int q) {
+  __device__ static uint32_t pair(const uint32_t *w, int q, const Mag &mg) {
     const uint32_t x = w[q >> 2];
     switch (q & 3) {
-      case 0: return andor(x, 0x00F000F0u, E64);
-      case 1: return andor(x >> 8, 0x00F000F0u, E64);
-      case 2: return andor(x << 6, 0x03C003C0u, E16);
-      default: return andor(x >> 2, 0x03C003C0u, E16);
+      case 0: return andor(x, 0x00F000F0u, mg.e64);
+      case 1: return andor(x >> 8, 0x00F000F0u, mg.e64);
+      case 2: return andor(x << 6, 0x03C003C0u, mg.e16);
+      default: return andor(x >> 2, 0x03C003C0u, mg.e16);
     }
   }
 };
 template <>
 struct Unpack<2> {
   static constexpr int kWords = 2;
-  __device__ static uint32_t pair(const uint32_t *w, int q) {
+  __device__ static uint32_t pair(const uint32_t *w, int q, const Mag &mg) {
     const uint32_t x = w[q >> 3];
     switch (q & 7) {
-      case 0: return andor(x, 0x03000300u, E4);
-      case 1: return andor(x >> 6, 0x03000300u, E4);
-      case 2: return andor(x, 0x00C000C0u, E16);
-      case 3: return andor(x >> 6, 0x00C000C0u, E16);
-      case 4: return andor(x, 0x00300030u, E64);
-      case 5: return andor(x >> 6, 0x00300030u, E64);
-      case 6: return andor(x << 8, 0x03000300u, E4);
-      default: return andor(x << 6, 0x03000300u, E4);
+      case 0: return andor(x, 0x03000300u, mg.e4);
+      case 1: return andor(x >> 6, 0x03000300u, mg.e4);
+      case 2: return andor(x, 0x00C000C0u, mg.e16);
+      case 3: return andor(x >> 6, 0x00C000C0u, mg.e16);
+      case 4: return andor(x, 0x00300030u, mg.e64);
+      case 5: return andor(x >> 6, 0x00300030u, mg.e64);
+      case 6: return andor(x << 8, 0x03000300u, mg.e4);
+      default: return andor(x << 6, 0x03000300u, mg.e4);
     }
   }
 };
@@ -177,6 +190,8 @@ constexpr int kMaxWaves = 1024;   // wavefronts per (b, KV head)
 
 
 // ---------------------------------------------------------------- async copies
+// lds_wave_base is wave-uniform (it goes to M0; lane l writes 16 bytes at +16 l); the
+// readfirstlane folds away when the compiler already holds it in a scalar register.
 __device__ __forceinline__ void dma16(const void *g, uint32_t lds_wave_base) {
   const uint32_t m0v = __builtin_amdgcn_readfirstlane(lds_wave_base);
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(m0v) : "memory", "m0");
@@ -351,11 +366,16 @@ struct Walker {
   }
 };
 
-// Copy `units` 16-byte units from `src` to LDS address `dst` (1 KB per instruction).
+// Copy `units` 16-byte units from `src` to LDS address `dst` (1 KB per instruction;
+// only a last partial instruction is lane-predicated).
 __device__ __forceinline__ void copy_segment(const uint8_t *src, uint32_t units, uint32_t dst, int lane) {
+  const uint8_t *s = src + 16 * lane;
+  const uint32_t full = units >> 6;
 #pragma unroll 1
-  for (uint32_t i = 0; i * 64 < units; ++i)
-    if (i * 64 + lane < units) dma16(src + 16 * (i * 64 + lane), dst + 1024 * i);
+  for (uint32_t i = 0; i < full; ++i) dma16(s + 1024 * i, dst + 1024 * i);
+  if (units & 63u) {
+    if ((uint32_t)lane < (units & 63u)) dma16(s + 1024 * full, dst + 1024 * full);
+  }
 }
 
 // Issue the copies of the producer's current item.
@@ -428,10 +448,13 @@ struct State {
   float m, l;
 };
 
-__device__ __forceinline__ float wave_max16(float x) {  // max over the 4 lanes of a head (kg)
-  x = fmaxf(x, __shfl_xor(x, 16));
-  x = fmaxf(x, __shfl_xor(x, 32));
-  return x;
+// Maximum over the 4 lanes of a head (lanes m16 + 16 kg): the row-swap permutes
+// pair lane l with l ^ 32 and l ^ 16.
+__device__ __forceinline__ float wave_max16(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = vmax(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return vmax(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
 __device__ __forceinline__ half4 as_h4(uint32_t a, uint32_t b) {
@@ -457,29 +480,36 @@ __device__ __forceinline__ float rescale_factor(State &st, float bm) {
   return alpha;
 }
 
-// Tile maximum (scaled to log2 units) over the valid tokens, shared by the 4 lanes
-// of each head.
-__device__ __forceinline__ float tile_max(const AttnParams &p, f4 S, bool full, uint32_t mine) {
-  float bm;
-  if (full) {
-    bm = fmaxf(fmaxf(S[0], S[1]), fmaxf(S[2], S[3]));
-  } else {
-    bm = kNegInf;
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-      if (mine & (1u << r)) bm = fmaxf(bm, S[r]);
-  }
-  return wave_max16(bm) * p.sl2;
-}
-
-__device__ __forceinline__ half4 tile_probs(const AttnParams &p, const State &st, f4 S, bool full, uint32_t mine) {
-  float pv[4];
+// Probabilities of one tile (this lane's 4 token rows of its head) against the
+// running maximum.  Only when some logit lies more than kRescale above it (always on
+// the first tile, with m = -inf) does the wavefront take the tile maximum over the
+// head's lanes and rescale.  Returns true when it rescaled (alpha holds the factor).
+__device__ __forceinline__ bool tile_softmax(const AttnParams &p, State &st, f4 S, bool full, uint32_t mine,
+                                             half4 &P4, float &alpha) {
+  float x[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
-    const float e = __builtin_amdgcn_exp2f(fmaf(S[r], p.sl2, -st.m));
-    pv[r] = (full || (mine & (1u << r))) ? e : 0.0f;
+    x[r] = fmaf(S[r], p.sl2, -st.m);
+    if (!full && !(mine & (1u << r))) x[r] = kNegInf;
   }
-  return half4{(_Float16)pv[0], (_Float16)pv[1], (_Float16)pv[2], (_Float16)pv[3]};
+  const bool big = vmax(vmax(x[0], x[1]), vmax(x[2], x[3])) > kRescale;
+  const bool resc = __any(big);
+  alpha = 1.0f;
+  if (resc) {
+    float bm = kNegInf;
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (full || (mine & (1u << r))) bm = vmax(bm, S[r]);
+    alpha = rescale_factor(st, wave_max16(bm) * p.sl2);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      x[r] = fmaf(S[r], p.sl2, -st.m);
+      if (!full && !(mine & (1u << r))) x[r] = kNegInf;
+    }
+  }
+  P4 = half4{(_Float16)__builtin_amdgcn_exp2f(x[0]), (_Float16)__builtin_amdgcn_exp2f(x[1]),
+             (_Float16)__builtin_amdgcn_exp2f(x[2]), (_Float16)__builtin_amdgcn_exp2f(x[3])};
+  return resc;
 }
 
 __device__ __forceinline__ uint4 lds16(const uint8_t *a) { return *(const uint4 *)a; }
@@ -508,8 +538,9 @@ __device__ __forceinline__ void exact_tile(const AttnParams &p, State &st, const
   for (int i = 0; i < 4; ++i) S = mfma32(a[i].h, qchunk(qs, lane, i), S);
   const bool full = tvalid == 0xFFFFu;
   const uint32_t mine = (tvalid >> (4 * kg)) & 0xFu;
-  rescale_factor(st, tile_max(p, S, full, mine));
-  const half4 P4 = tile_probs(p, st, S, full, mine);
+  half4 P4;
+  float alpha;
+  tile_softmax(p, st, S, full, mine, P4, alpha);
   const f4 pb = mfma16(kOnes, P4, f4{0, 0, 0, 0});
 #pragma unroll
   for (int i = 0; i < 4; ++i) a[i].v = lds16(ip + 4096 + lane * 64 + 16 * i);
@@ -571,6 +602,12 @@ __device__ __forceinline__ void int_tile(const AttnParams &p, State &st, IntBloc
   const int kg = lane >> 4;
   const uint8_t *kc = kt + lane * (4 * BITS);
   const uint8_t *vc = vt + lane * (4 * BITS);
+  Mag mg;
+  if (BITS != 8) {
+    mg.e64 = opaque(E64);
+    mg.e16 = opaque(E16);
+    mg.e4 = opaque(E4);
+  }
   uint32_t kw[NW];
   if (NW >= 4) {
 #pragma unroll
@@ -582,26 +619,7 @@ __device__ __forceinline__ void int_tile(const AttnParams &p, State &st, IntBloc
     const uint2 a = *(const uint2 *)kc;
     kw[0] = a.x; kw[1] = a.y;
   }
-  f4 S = ib.c0;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    U8 a;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) a.u[e] = Unpack<BITS>::pair(kw, 4 * i + e);
-    S = mfma32(a.h, ib.qh[i], S);
-    S = mfma32(a.h, ib.ql[i], S);
-  }
-  const bool full = tvalid == 0xFFFFu;
-  const uint32_t mine = (tvalid >> (4 * kg)) & 0xFu;
-  const float alpha = rescale_factor(st, tile_max(p, S, full, mine));
-  if (alpha != 1.0f) {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) ib.acc[j] *= alpha;
-    ib.pb *= alpha;
-  }
-  const half4 P4 = tile_probs(p, st, S, full, mine);
-  ib.pb = mfma16(kOnes, P4, ib.pb);
-  uint32_t vw[NW];
+  uint32_t vw[NW];  // value codes, read now so that the softmax hides the latency
   if (NW >= 4) {
 #pragma unroll
     for (int q = 0; q < NW; q += 4) {
@@ -612,9 +630,30 @@ __device__ __forceinline__ void int_tile(const AttnParams &p, State &st, IntBloc
     const uint2 a = *(const uint2 *)vc;
     vw[0] = a.x; vw[1] = a.y;
   }
+  // two independent MFMA chains (q*s high and low terms)
+  f4 S = ib.c0, S2 = {0, 0, 0, 0};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    U8 a;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) a.u[e] = Unpack<BITS>::pair(kw, 4 * i + e, mg);
+    S = mfma32(a.h, ib.qh[i], S);
+    S2 = mfma32(a.h, ib.ql[i], S2);
+  }
+  S += S2;
+  const bool full = tvalid == 0xFFFFu;
+  const uint32_t mine = (tvalid >> (4 * kg)) & 0xFu;
+  half4 P4;
+  float alpha;
+  if (tile_softmax(p, st, S, full, mine, P4, alpha)) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) ib.acc[j] *= alpha;
+    ib.pb *= alpha;
+  }
+  ib.pb = mfma16(kOnes, P4, ib.pb);
 #pragma unroll
   for (int j = 0; j < 8; ++j)
-    ib.acc[j] = mfma16(as_h4(Unpack<BITS>::pair(vw, 2 * j), Unpack<BITS>::pair(vw, 2 * j + 1)), P4, ib.acc[j]);
+    ib.acc[j] = mfma16(as_h4(Unpack<BITS>::pair(vw, 2 * j, mg), Unpack<BITS>::pair(vw, 2 * j + 1, mg)), P4, ib.acc[j]);
 }
 
 // End of an int block: O[d][h] += s_d * (acc - off * sum p) + z_d * sum p,
@@ -679,7 +718,7 @@ __device__ __forceinline__ void centroid_item(const AttnParams &p, State &st, co
   float bm = kNegInf;
 #pragma unroll
   for (int a = 0; a < 4; ++a)
-    if (used[a] > 0.f) bm = fmaxf(bm, sc[a]);
+    if (used[a] > 0.f) bm = vmax(bm, sc[a]);
   rescale_factor(st, bm * p.sl2);
   float pk[4];
 #pragma unroll
@@ -783,7 +822,7 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   Pipe pp;
   pp.prod.dsrc = p.plan + (u * p.vcap + vstart) * (int64_t)sizeof(VisitDesc);
   pp.prod.dring = smem + wave * kWaveLds + kRing + kQueueBytes;
-  pp.prod.dlds = (uint32_t)(uintptr_t)pp.prod.dring;
+  pp.prod.dlds = (uint32_t)uni((int32_t)(uintptr_t)pp.prod.dring);
   pp.prod.dcnt0 = pp.prod.dcnt1 = 0;
   pp.prod.v = 0;
   pp.prod.nv = vend - vstart;
@@ -797,7 +836,7 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   pp.prod.kp = pp.prod.vp = nullptr;
   pp.ring = smem + wave * kWaveLds;
   pp.queue = (uint32_t *)(smem + wave * kWaveLds + kRing);
-  pp.ring_base = (uint32_t)(uintptr_t)pp.ring;
+  pp.ring_base = (uint32_t)uni((int32_t)(uintptr_t)pp.ring);
   pp.lane = lane;
   pp.issued = 0;
   pp.hold = 0;
@@ -905,37 +944,21 @@ __global__ void __launch_bounds__(D) merge_kernel(const float *part, float *out,
 // a fixed cost per pipeline item (visit v goes to the wavefront that owns the
 // midpoint of its cost interval).
 constexpr int kPlanThreads = 1024;
-// Balance cost of a visit in 16-byte units: the bytes copied, a per-item pipeline
-// cost and the per-tile compute (dequantisation makes an int tile dearer than an
-// exact one), each converted at one wavefront's share of the bandwidth.
-constexpr uint32_t kItemCost = 12, kExactTileCost = 17, kIntTileCost = 45, kCentroidCost = 25;
+// Balance cost of a visit: the measured time of its parts on one wavefront sharing
+// its SIMD (about 8 cycles per unit).  Exact tiles are bound by the wavefront's
+// share of the bandwidth (8 KB each), int tiles by the dequantisation and softmax
+// work rather than by their bytes.
+constexpr uint32_t kCostExactTile = 625, kCostInt8Tile = 450, kCostInt4Tile = 300, kCostInt2Tile = 210,
+                   kCostCentroid = 550, kCostIntBlock = 240;
 
 __device__ __forceinline__ uint32_t balance_cost(int lv, uint64_t va) {
-  uint32_t tiles = 0, mask = 0;
-  for (int t = 0; t < 4; ++t)
-    if ((va >> (16 * t)) & 0xFFFFull) {
-      ++tiles;
-      mask |= 1u << t;
-    }
+  uint32_t tiles = 0;
+  for (int t = 0; t < 4; ++t) tiles += ((va >> (16 * t)) & 0xFFFFull) != 0;
   if (!tiles) return 0;
-  if (lv == GKV_CENTROID) return 2 * kCentBytes / 16 + kCentroidCost + kItemCost;
-  if (lv == GKV_EXACT) return tiles * (2 * 4096 / 16 + kExactTileCost + kItemCost);
-  // int: items are runs of up to group_tiles(lv) consecutive read tiles
-  uint32_t items = 0;
-  const int tg = group_tiles(lv);
-  for (int t = 0; t < 4;) {
-    if (!((mask >> t) & 1u)) {
-      ++t;
-      continue;
-    }
-    int n = 0;
-    while (t < 4 && ((mask >> t) & 1u) && n < tg) {
-      ++t;
-      ++n;
-    }
-    ++items;
-  }
-  return 2 * (kSZBytes / 16) + items * kItemCost + tiles * (32 * lv + kIntTileCost);
+  if (lv == GKV_CENTROID) return kCostCentroid;
+  if (lv == GKV_EXACT) return tiles * kCostExactTile;
+  const uint32_t per = lv == 8 ? kCostInt8Tile : (lv == 4 ? kCostInt4Tile : kCostInt2Tile);
+  return kCostIntBlock + tiles * per;
 }
 
 __device__ __forceinline__ uint64_t token_mask(int64_t left) {  // tokens of a block below `left`
