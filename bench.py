@@ -83,6 +83,59 @@ def step_loop(caches, qs, outs, steps, warmup, pages=None):
     return per, total_ms
 
 
+def staged_loop(caches, qs, outs, steps, warmup):
+    """The same decode step as its three stages (plan, partials, merge) with an event
+    pair around each, on the stream the library launches on: the attention kernel's
+    own launch durations (us) and the plan and merge durations."""
+    import numpy as np
+    import torch
+    nc = len(caches)
+
+    def stage(i, ev=None):
+        c = caches[i % nc]
+        if ev:
+            ev[0].record()
+        c.attn_plan()
+        if ev:
+            ev[1].record()
+        c.attn_partials(qs[i % len(qs)])
+        if ev:
+            ev[2].record()
+        c.attn_merge(outs[i % nc])
+        if ev:
+            ev[3].record()
+
+    for i in range(warmup):
+        stage(i)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    for i in range(steps):
+        stage(i, evs[i])
+    torch.cuda.synchronize()
+    plan = np.array([e[0].elapsed_time(e[1]) for e in evs]) * 1e3
+    attn = np.array([e[1].elapsed_time(e[2]) for e in evs]) * 1e3
+    merge = np.array([e[2].elapsed_time(e[3]) for e in evs]) * 1e3
+    return plan, attn, merge
+
+
+def committed_traffic(kernel_src):
+    """HBM bytes per attention launch from the committed counter summary, if it was
+    taken on the current kernel source (else None)."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "attn_kernel_rd128k_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    sha = hashlib.sha256(open(kernel_src, "rb").read()).hexdigest()
+    if kv.get("source_sha256") != sha or "bytes_per_launch" not in kv:
+        return None
+    return float(kv["bytes_per_launch"])
+
+
 def cpu_oracle_sample(ks_unit, vs_unit, lv, mass, nres, q_group, out_gpu):
     """Time the plain oracle on one (b, KV head) unit of the workload (dequantize
     every block, apply the residual, attend) and check the GPU output of that unit."""
@@ -164,6 +217,12 @@ def main():
     mean_us = float(per.mean())
     gbps = alg_bytes / (mean_us * 1e-6) / 1e9
     log(f"[bench] median {med:.1f} us, p90 {p90:.1f} us, mean {mean_us:.1f} us, {gbps:.0f} GB/s")
+    plan_us, attn_us, merge_us = staged_loop(caches, qs, outs, args.steps, args.warmup)
+    attn_mean = float(attn_us.mean())
+    attn_gbps = alg_bytes / (attn_mean * 1e-6) / 1e9
+    traffic = committed_traffic(os.path.join(ROOT, "paper_2608_23599_amd", "csrc", "attn.hip"))
+    log(f"[bench] attention kernel {attn_mean:.1f} us ({attn_gbps:.0f} GB/s), plan {np.median(plan_us):.1f} us, "
+        f"merge {np.median(merge_us):.1f} us")
 
     if args.profile:
         # reference for hardware byte counters: one device-to-device copy of 512 MiB
@@ -264,9 +323,14 @@ def main():
         "read_bpv": round(rates["read_bpv"], 4),
         "resident_bpv": round(rates["resident_bpv"], 4),
         "algorithmic_bytes_per_step": int(alg_bytes),
-        "roofline": {"bound": "hbm", "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(gbps / HBM_PEAK_GBPS, 4), "traffic": None,
-                     "kernel": "attn_kernel (one launch per step)"},
+        "roofline": {"bound": "hbm", "achieved": round(attn_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
+                     "traffic": None if traffic is None else int(traffic),
+                     "kernel": "attn_kernel", "kernel_us_mean": round(attn_mean, 2),
+                     "algorithmic_bytes_per_launch": int(alg_bytes)},
+        "stages_us": {"plan_median": round(float(np.median(plan_us)), 2),
+                      "attn_kernel_median": round(float(np.median(attn_us)), 2),
+                      "merge_median": round(float(np.median(merge_us)), 2)},
         "cpu_baseline": cpu,
         "phases": phases,
         "quest_128k": quest,

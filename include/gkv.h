@@ -238,6 +238,20 @@ gkv_status gkv_quest_select(const uint16_t *q, const gkv_cache *c, int32_t topk,
 gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache *c, const int32_t *pages, int32_t topk,
                                   float *out, void *ws, int64_t ws_bytes, void *stream);
 
+/* The three stages of gkv_graded_decode_attn, for callers that time or schedule them
+ * apart; called in this order on one stream with the same cache, pages, topk and
+ * workspace they compute the same result.  gkv_attn_plan writes the per-(b,h) visit
+ * plan (block records, read tokens, wavefront split) into ws; gkv_attn_partials runs
+ * the attention over the plan and leaves one partial (max, sum, output) per
+ * workgroup in ws; gkv_attn_merge combines the partials into out.  Arguments and
+ * errors as for gkv_graded_decode_attn. */
+gkv_status gkv_attn_plan(const gkv_cache *c, const int32_t *pages, int32_t topk, void *ws, int64_t ws_bytes,
+                         void *stream);
+gkv_status gkv_attn_partials(const uint16_t *q, const gkv_cache *c, const int32_t *pages, int32_t topk, void *ws,
+                             int64_t ws_bytes, void *stream);
+gkv_status gkv_attn_merge(const gkv_cache *c, const int32_t *pages, int32_t topk, float *out, void *ws,
+                          int64_t ws_bytes, void *stream);
+
 /* Rate-distortion exact residual (section 3.4, Eq. rdscore): score every token
  * s_j = a_j * sum_d (v_jd - v_hat_jd)^2 (fp64, channel order, no fused multiply-add)
  * with v_hat its value at its block's level, keep the first nkeep of the order

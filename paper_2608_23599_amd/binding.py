@@ -72,6 +72,9 @@ _page_boxes = _sig("gkv_page_boxes", _i32, [_P(CacheStruct), _vp, _i64, _i64, _i
 _append = _sig("gkv_append", _i32, [_P(CacheStruct), _vp, _vp, _vp, _vp, _vp])
 _quest_select = _sig("gkv_quest_select", _i32, [_vp, _P(CacheStruct), _i32, _vp, _vp, _i64, _vp])
 _attn = _sig("gkv_graded_decode_attn", _i32, [_vp, _P(CacheStruct), _vp, _i32, _vp, _vp, _i64, _vp])
+_attn_plan = _sig("gkv_attn_plan", _i32, [_P(CacheStruct), _vp, _i32, _vp, _i64, _vp])
+_attn_partials = _sig("gkv_attn_partials", _i32, [_vp, _P(CacheStruct), _vp, _i32, _vp, _i64, _vp])
+_attn_merge = _sig("gkv_attn_merge", _i32, [_P(CacheStruct), _vp, _i32, _vp, _vp, _i64, _vp])
 _rd = _sig("gkv_rd_residual_select", _i32, [_P(CacheStruct), _vp, _vp, _vp, _i32, _vp, _i64, _vp])
 
 EXPORTED = [
@@ -79,6 +82,7 @@ EXPORTED = [
     "gkv_pool_bytes", "gkv_pool_alloc", "gkv_pool_free", "gkv_pool_used", "gkv_pool_destroy", "gkv_account",
     "gkv_decode_record", "gkv_f64_to_f16", "gkv_workspace_bytes", "gkv_quantize_block", "gkv_demote",
     "gkv_page_boxes", "gkv_append", "gkv_quest_select", "gkv_graded_decode_attn", "gkv_rd_residual_select",
+    "gkv_attn_plan", "gkv_attn_partials", "gkv_attn_merge",
 ]
 
 
@@ -402,6 +406,25 @@ class GradedCache:
         return out
 
     decode = graded_decode_attn
+
+    # the three stages of graded_decode_attn (same result when called in order)
+    def attn_plan(self, pages=None):
+        topk = int(pages.shape[-1]) if pages is not None else 0
+        ws = self.workspace(1, topk)
+        _check(_attn_plan(ctypes.byref(self.c), _dptr(pages), topk, _dptr(ws), ws.numel(), _stream()), "attn_plan")
+
+    def attn_partials(self, q, pages=None):
+        q = _as_bits(q, self.device)
+        topk = int(pages.shape[-1]) if pages is not None else 0
+        ws = self.workspace(1, topk)
+        _check(_attn_partials(_dptr(q), ctypes.byref(self.c), _dptr(pages), topk, _dptr(ws), ws.numel(), _stream()),
+               "attn_partials")
+
+    def attn_merge(self, out, pages=None):
+        topk = int(pages.shape[-1]) if pages is not None else 0
+        ws = self.workspace(1, topk)
+        _check(_attn_merge(ctypes.byref(self.c), _dptr(pages), topk, _dptr(out), _dptr(ws), ws.numel(), _stream()),
+               "attn_merge")
 
     def rd_residual_select(self, k_src, v_src, mass, nkeep):
         kd = _as_bits(k_src, self.device)

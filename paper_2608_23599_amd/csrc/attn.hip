@@ -1150,11 +1150,13 @@ static AttnLayout attn_layout(const gkv_cache *c, int32_t topk) {
 
 int64_t gkv_attn_workspace(const gkv_cache *c, int32_t topk) { return attn_layout(c, topk).total; }
 
-extern "C" gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache *c, const int32_t *pages,
-                                             int32_t topk, float *out, void *ws, int64_t ws_bytes, void *stream) {
+// Checks the call and fills the kernel parameters (q and out may be null for the
+// stages that do not use them).
+static gkv_status attn_setup(const uint16_t *q, const gkv_cache *c, const int32_t *pages, int32_t topk, void *ws,
+                             int64_t ws_bytes, AttnParams &p) {
   gkv_status st = gkv_validate_cache(c);
   if (st) return st;
-  if (!q || !out || !ws) return GKV_E_ARG;
+  if (!ws) return GKV_E_ARG;
   if (c->T <= 0) return GKV_E_SHAPE;
   if (pages) {
     if (topk <= 0) return GKV_E_ARG;
@@ -1165,7 +1167,6 @@ extern "C" gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache 
   }
   const AttnLayout L = attn_layout(c, topk);
   if (ws_bytes < L.total) return GKV_E_WORKSPACE;
-  AttnParams p;
   p.q = q;
   p.level = c->level;
   p.koff = c->koff;
@@ -1187,10 +1188,59 @@ extern "C" gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache 
   p.topk = topk;
   p.nsplit = attn_nsplit(c, topk, c->T);
   p.sl2 = 1.4426950408889634f / sqrtf((float)D);
-  hipLaunchKernelGGL(plan_kernel, dim3(c->B * c->Hkv), dim3(kPlanThreads), 0, (hipStream_t)stream, p);
+  return GKV_OK;
+}
+
+static void launch_plan(const AttnParams &p, const gkv_cache *c, hipStream_t s) {
+  hipLaunchKernelGGL(plan_kernel, dim3(c->B * c->Hkv), dim3(kPlanThreads), 0, s, p);
+}
+static void launch_partials(const AttnParams &p, const gkv_cache *c, hipStream_t s) {
   const size_t lds = (size_t)kWaves * kWaveLds + 16 * kQRow;  // rings also hold the merge buffers
-  hipLaunchKernelGGL(attn_kernel, dim3(p.nsplit, c->Hkv, c->B), dim3(kThreads), lds, (hipStream_t)stream, p);
-  hipLaunchKernelGGL(merge_kernel, dim3(p.G, c->Hkv * c->B), dim3(D), 0, (hipStream_t)stream, (const float *)p.part,
-                     out, p.nsplit, p.G);
+  hipLaunchKernelGGL(attn_kernel, dim3(p.nsplit, c->Hkv, c->B), dim3(kThreads), lds, s, p);
+}
+static void launch_merge(const AttnParams &p, const gkv_cache *c, float *out, hipStream_t s) {
+  hipLaunchKernelGGL(merge_kernel, dim3(p.G, c->Hkv * c->B), dim3(D), 0, s, (const float *)p.part, out, p.nsplit,
+                     p.G);
+}
+
+extern "C" gkv_status gkv_attn_plan(const gkv_cache *c, const int32_t *pages, int32_t topk, void *ws, int64_t ws_bytes,
+                                    void *stream) {
+  AttnParams p;
+  const gkv_status st = attn_setup(nullptr, c, pages, topk, ws, ws_bytes, p);
+  if (st) return st;
+  launch_plan(p, c, (hipStream_t)stream);
+  return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP;
+}
+
+extern "C" gkv_status gkv_attn_partials(const uint16_t *q, const gkv_cache *c, const int32_t *pages, int32_t topk,
+                                        void *ws, int64_t ws_bytes, void *stream) {
+  if (!q) return GKV_E_ARG;
+  AttnParams p;
+  const gkv_status st = attn_setup(q, c, pages, topk, ws, ws_bytes, p);
+  if (st) return st;
+  launch_partials(p, c, (hipStream_t)stream);
+  return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP;
+}
+
+extern "C" gkv_status gkv_attn_merge(const gkv_cache *c, const int32_t *pages, int32_t topk, float *out, void *ws,
+                                     int64_t ws_bytes, void *stream) {
+  if (!out) return GKV_E_ARG;
+  AttnParams p;
+  const gkv_status st = attn_setup(nullptr, c, pages, topk, ws, ws_bytes, p);
+  if (st) return st;
+  launch_merge(p, c, out, (hipStream_t)stream);
+  return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP;
+}
+
+extern "C" gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache *c, const int32_t *pages,
+                                             int32_t topk, float *out, void *ws, int64_t ws_bytes, void *stream) {
+  if (!q || !out) return GKV_E_ARG;
+  AttnParams p;
+  const gkv_status st = attn_setup(q, c, pages, topk, ws, ws_bytes, p);
+  if (st) return st;
+  const hipStream_t s = (hipStream_t)stream;
+  launch_plan(p, c, s);
+  launch_partials(p, c, s);
+  launch_merge(p, c, out, s);
   return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP;
 }

@@ -246,3 +246,33 @@ def test_constant_channel_and_equal_rows(gpu):
         compare_record(cache, uc, 0, 0, blk, 1)
     q = synth.queries(61, 1, Hq)
     assert max_err(cache.decode(q).cpu().numpy()[0], uc.decode_dense(q[0])) <= TOL
+
+
+def test_staged_attention_equals_one_call(gpu):
+    """plan -> partials -> merge on one stream gives the one-call result bit for bit,
+    for a dense read with residual rows and for a Compressed-Quest read."""
+    torch = _torch()
+    T, Hq, Hkv = 3000, 8, 2
+    ks, vs = kv_all(4, 1, Hkv, T)
+    lv = olad.ladder("graded", T)
+    nres = ores.n_keep(T, 2)
+    cache = _build(gpu, ks, vs, Hq, lv, nres_cap=nres, page=16)
+    mass = np.stack([synth.mass_unit(4, 0, h, T) for h in range(Hkv)])[None]
+    q = synth.queries(4, 1, Hq)
+    qd = torch.from_numpy(q.view(np.int16)).cuda()
+    # Compressed-Quest read (before the residual exists: it requires nres = 0)
+    pages = cache.quest_select(q, 24)
+    one = cache.decode(qd, pages=pages).clone()
+    out = torch.full_like(one, float("nan"))
+    cache.attn_plan(pages)
+    cache.attn_partials(qd, pages)
+    cache.attn_merge(out, pages)
+    assert torch.equal(one, out)
+    # dense read with residual rows
+    cache.rd_residual_select(ks, vs, mass, nres)
+    one = cache.decode(qd).clone()
+    out = torch.full_like(one, float("nan"))
+    cache.attn_plan()
+    cache.attn_partials(qd)
+    cache.attn_merge(out)
+    assert torch.equal(one, out)
