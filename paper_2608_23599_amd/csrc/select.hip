@@ -27,10 +27,10 @@ __device__ __forceinline__ uint64_t order_key(double x) {
 // UB_g(p) = sum_d q_gd * (q_gd >= 0 ? kmax_pd : kmin_pd), channel-ascending in fp64
 // (each product of two fp16 values is exact, so the fused multiply-add rounds once,
 // like a separate add); page score = max_g UB_g.  grid (ceil(npages/256), Hkv, B).
+template <int G>
 __global__ void __launch_bounds__(256) quest_score_kernel(const uint16_t *__restrict__ q,
                                                           const uint16_t *__restrict__ boxes, int64_t npage_cap,
-                                                          int64_t npages, int Hkv, int G,
-                                                          uint64_t *__restrict__ keys) {
+                                                          int64_t npages, int Hkv, uint64_t *__restrict__ keys) {
   __shared__ double qs[16 * D];
   const int h = blockIdx.y, b = blockIdx.z;
   const int64_t u = (int64_t)b * Hkv + h;
@@ -39,16 +39,22 @@ __global__ void __launch_bounds__(256) quest_score_kernel(const uint16_t *__rest
   const int64_t pg = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (pg >= npages) return;
   const uint32_t *bx = (const uint32_t *)(boxes + u * npage_cap * 2 * D);
-  double acc[16];
+  double acc[G];
 #pragma unroll
-  for (int g = 0; g < 16; ++g) acc[g] = 0.0;
-  for (int d = 0; d < D; ++d) {
-    const uint32_t pr = bx[box_index(pg, d) >> 1];
-    const double lo = (double)__builtin_bit_cast(_Float16, (uint16_t)(pr & 0xFFFFu));
-    const double hi = (double)__builtin_bit_cast(_Float16, (uint16_t)(pr >> 16));
+  for (int g = 0; g < G; ++g) acc[g] = 0.0;
+  // 64 channels' box words are loaded before they are used (independent loads in
+  // flight); the accumulation stays channel-ascending
+  for (int d0 = 0; d0 < D; d0 += 64) {
+    uint32_t pr[64];
 #pragma unroll
-    for (int g = 0; g < 16; ++g) {
-      if (g < G) {
+    for (int e = 0; e < 64; ++e) pr[e] = bx[box_index(pg, d0 + e) >> 1];
+#pragma unroll
+    for (int e = 0; e < 64; ++e) {
+      const int d = d0 + e;
+      const double lo = (double)__builtin_bit_cast(_Float16, (uint16_t)(pr[e] & 0xFFFFu));
+      const double hi = (double)__builtin_bit_cast(_Float16, (uint16_t)(pr[e] >> 16));
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
         const double qd = qs[g * D + d];
         acc[g] = __builtin_fma(qd, qd >= 0.0 ? hi : lo, acc[g]);
       }
@@ -56,25 +62,70 @@ __global__ void __launch_bounds__(256) quest_score_kernel(const uint16_t *__rest
   }
   double best = acc[0];
 #pragma unroll
-  for (int g = 1; g < 16; ++g)
-    if (g < G) best = acc[g] > best ? acc[g] : best;
+  for (int g = 1; g < G; ++g) best = acc[g] > best ? acc[g] : best;
   keys[u * npage_cap + pg] = order_key(best);
 }
 
 // Select the first k of the order (key desc, index asc) among keys[0..n) of one
 // unit and write their indices ascending to out[0..k) (-1 padded).  Optionally
 // sets the selected tokens' bits in a per-64 mask.  One workgroup per unit.
+//
+// Radix select of the threshold key (the need-th largest), 8 bits per pass, with
+// one histogram per wavefront (so that LDS atomics contend only inside a
+// wavefront); then an ordered compaction: selected = key > threshold, or key ==
+// threshold among the first `eq_take` such keys by index.  With KPT > 0 (n <= KPT *
+// threads) thread t holds keys t * KPT + j (j < KPT) in registers; with KPT == 0
+// keys are streamed from memory in 1024-key chunks.
 constexpr int kSelThreads = 1024;
+constexpr int kSelWaves = kSelThreads / 64;
 
+constexpr int kSelKPT = 8;  // keys per thread held in registers (n <= 8192)
+
+struct SelShared {
+  uint32_t hist[kSelWaves][256];
+  uint64_t prefix, pmask;
+  int64_t remaining;
+  int64_t wsum[kSelWaves][2];
+  int64_t base[2];
+};
+
+// Exclusive scan of (a, b) over the workgroup in thread order; returns the totals.
+__device__ __forceinline__ void scan2(SelShared &sh, int64_t &a, int64_t &b, int64_t &ta, int64_t &tb) {
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  int64_t x = a, y = b;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int64_t px = __shfl_up(x, o), py = __shfl_up(y, o);
+    if (lane >= o) {
+      x += px;
+      y += py;
+    }
+  }
+  if (lane == 63) {
+    sh.wsum[wv][0] = x;
+    sh.wsum[wv][1] = y;
+  }
+  __syncthreads();
+  int64_t bx = 0, by = 0;
+  ta = tb = 0;
+  for (int q = 0; q < kSelWaves; ++q) {
+    if (q < wv) {
+      bx += sh.wsum[q][0];
+      by += sh.wsum[q][1];
+    }
+    ta += sh.wsum[q][0];
+    tb += sh.wsum[q][1];
+  }
+  a = bx + x - a;
+  b = by + y - b;
+  __syncthreads();
+}
+
+template <int KPT>
 __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__restrict__ keys, int64_t key_stride,
                                                              int64_t n, int k, int32_t *__restrict__ out,
                                                              int64_t out_stride, uint64_t *mask, int64_t mask_stride,
                                                              int64_t mask_words) {
-  __shared__ uint32_t hist[256];
-  __shared__ uint64_t sh_prefix, sh_pmask;
-  __shared__ int64_t sh_remaining;
-  __shared__ int64_t wsum[kSelThreads / 64][2];
-  __shared__ int64_t sh_base[2];
+  __shared__ SelShared sh;
   const int64_t u = blockIdx.x;
   const uint64_t *key = keys + u * key_stride;
   int32_t *o = out + u * out_stride;
@@ -85,74 +136,176 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
   const int64_t need = n < k ? n : k;
   for (int64_t i = need + tid; i < k; i += kSelThreads) o[i] = -1;
   if (need == 0) return;
-  // radix select of the threshold key (the need-th largest), 8 bits at a time
-  if (tid == 0) {
-    sh_prefix = 0;
-    sh_pmask = 0;
-    sh_remaining = need;
+  uint64_t kr[KPT > 0 ? KPT : 1];
+  if (KPT > 0) {
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) {
+      const int64_t i = (int64_t)tid * KPT + j;
+      kr[j] = i < n ? key[i] : 0;
+    }
   }
-  __syncthreads();
-  for (int pass = 0; pass < 8; ++pass) {
-    const int shift = 56 - 8 * pass;
-    for (int i = tid; i < 256; i += kSelThreads) hist[i] = 0;
-    __syncthreads();
-    const uint64_t pre = sh_prefix, pm = sh_pmask;
+  // bits that differ between keys: bytes above the highest differing byte are the
+  // same in every key, so their digits are known without a pass
+  uint64_t kand = ~0ull, kor = 0;
+  if (KPT > 0) {
+#pragma unroll
+    for (int j = 0; j < KPT; ++j)
+      if ((int64_t)tid * KPT + j < n) {
+        kand &= kr[j];
+        kor |= kr[j];
+      }
+  } else {
     for (int64_t i = tid; i < n; i += kSelThreads) {
       const uint64_t kv = key[i];
-      if ((kv & pm) == pre) atomicAdd(&hist[(kv >> shift) & 255u], 1u);
+      kand &= kv;
+      kor |= kv;
     }
-    __syncthreads();
-    if (tid == 0) {
-      int64_t rem = sh_remaining;
-      int dig = 255;
-      for (; dig > 0; --dig) {
-        if ((int64_t)hist[dig] >= rem) break;
-        rem -= hist[dig];
-      }
-      sh_remaining = rem;
-      sh_prefix = pre | ((uint64_t)dig << shift);
-      sh_pmask = pm | (0xFFull << shift);
-    }
-    __syncthreads();
   }
-  const uint64_t thr = sh_prefix;
-  const int64_t eq_take = sh_remaining;  // keys equal to thr to take, lowest index first
-  // ordered compaction: selected = key > thr, or key == thr among the first eq_take
-  if (tid == 0) {
-    sh_base[0] = 0;  // selected so far
-    sh_base[1] = 0;  // keys equal to thr so far
+  for (int o2 = 32; o2 > 0; o2 >>= 1) {
+    kand &= __shfl_xor(kand, o2);
+    kor |= __shfl_xor(kor, o2);
+  }
+  if (lane == 0) {
+    sh.wsum[wv][0] = (int64_t)kand;
+    sh.wsum[wv][1] = (int64_t)kor;
   }
   __syncthreads();
-  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  if (tid == 0) {
+    uint64_t a = ~0ull, b = 0;
+    for (int q = 0; q < kSelWaves; ++q) {
+      a &= (uint64_t)sh.wsum[q][0];
+      b |= (uint64_t)sh.wsum[q][1];
+    }
+    const uint64_t diff = a ^ b;
+    const int top = diff ? (63 - __builtin_clzll(diff)) / 8 : -1;  // highest differing byte
+    const uint64_t known = top >= 7 ? 0ull : (~0ull << (8 * (top + 1)));
+    sh.prefix = a & known;
+    sh.pmask = known;
+    sh.remaining = need;
+    sh.base[0] = top;
+  }
+  __syncthreads();
+  const int first_pass = 7 - (int)sh.base[0];
+  for (int i = tid; i < kSelWaves * 256; i += kSelThreads) (&sh.hist[0][0])[i] = 0;
+  __syncthreads();
+  for (int pass = first_pass; pass < 8; ++pass) {
+    const int shift = 56 - 8 * pass;
+    const uint64_t pre = sh.prefix, pm = sh.pmask;
+    if (KPT > 0) {
+#pragma unroll
+      for (int j = 0; j < KPT; ++j) {
+        const int64_t i = (int64_t)tid * KPT + j;
+        if (i < n && (kr[j] & pm) == pre) atomicAdd(&sh.hist[wv][(kr[j] >> shift) & 255u], 1u);
+      }
+    } else {
+      for (int64_t i = tid; i < n; i += kSelThreads) {
+        const uint64_t kv = key[i];
+        if ((kv & pm) == pre) atomicAdd(&sh.hist[wv][(kv >> shift) & 255u], 1u);
+      }
+    }
+    __syncthreads();
+    // wavefront 0: suffix sums over digits (digit d counts keys with digit >= d;
+    // lane l holds digits 4l..4l+3), then the digit whose suffix first reaches the
+    // remaining count
+    if (wv == 0) {
+      uint32_t c[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        c[e] = 0;
+        for (int q = 0; q < kSelWaves; ++q) {
+          c[e] += sh.hist[q][4 * lane + e];
+          sh.hist[q][4 * lane + e] = 0;  // cleared for the next pass
+        }
+      }
+      const uint32_t mine = c[0] + c[1] + c[2] + c[3];
+      uint32_t incl = mine;  // sum over lanes >= this lane
+      for (int o2 = 1; o2 < 64; o2 <<= 1) {
+        const uint32_t y = __shfl_down(incl, o2);
+        if (lane + o2 < 64) incl += y;
+      }
+      const int64_t rem = sh.remaining;
+      uint32_t suf[5];  // suffix at digits 4l .. 4l+4
+      suf[4] = incl - mine;
+#pragma unroll
+      for (int e = 3; e >= 0; --e) suf[e] = suf[e + 1] + c[e];
+      int hit = -1;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if ((int64_t)suf[e] >= rem && (int64_t)suf[e + 1] < rem) hit = e;
+      if (hit >= 0) {
+        const int dig = 4 * lane + hit;
+        sh.remaining = rem - suf[hit + 1];
+        sh.prefix = pre | ((uint64_t)dig << shift);
+        sh.pmask = pm | (0xFFull << shift);
+      }
+    }
+    __syncthreads();
+  }
+  const uint64_t thr = sh.prefix;
+  const int64_t eq_take = sh.remaining;  // keys equal to thr to take, lowest index first
+  if (KPT > 0) {
+    int64_t gt = 0, eq = 0;
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) {
+      if ((int64_t)tid * KPT + j < n) {
+        gt += kr[j] > thr;
+        eq += kr[j] == thr;
+      }
+    }
+    int64_t tg, te;
+    scan2(sh, gt, eq, tg, te);  // gt, eq: counts in the threads before this one
+    int64_t pos = gt + (eq < eq_take ? eq : eq_take);
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) {
+      const int64_t i = (int64_t)tid * KPT + j;
+      if (i < n) {
+        const bool sel = kr[j] > thr || (kr[j] == thr && eq++ < eq_take);
+        if (sel) {
+          o[pos++] = (int32_t)i;
+          if (mk) atomicOr((unsigned long long *)&mk[i >> 6], 1ull << (i & 63));
+        }
+      }
+    }
+    return;
+  }
+  // streamed: chunks of kSelThreads keys, one key per thread
+  if (tid == 0) {
+    sh.base[0] = 0;  // selected so far
+    sh.base[1] = 0;  // keys equal to thr so far
+  }
+  __syncthreads();
   for (int64_t c0 = 0; c0 < n; c0 += kSelThreads) {
     const int64_t i = c0 + tid;
     const bool in = i < n;
     const uint64_t kv = in ? key[i] : 0;
-    const bool gt = in && kv > thr, eq = in && kv == thr;
-    const uint64_t be = __ballot(eq);
-    if (lane == 0) wsum[wv][0] = __popcll(be);
-    __syncthreads();
-    int64_t eq_rank = sh_base[1] + __popcll(be & below);
-    for (int q = 0; q < wv; ++q) eq_rank += wsum[q][0];
-    const bool sel = gt || (eq && eq_rank < eq_take);
-    const uint64_t bs = __ballot(sel);
-    if (lane == 0) wsum[wv][1] = __popcll(bs);
-    __syncthreads();
-    int64_t pos = sh_base[0] + __popcll(bs & below);
-    for (int q = 0; q < wv; ++q) pos += wsum[q][1];
+    int64_t g = in && kv > thr, e = in && kv == thr;
+    const int64_t b0 = sh.base[0], b1 = sh.base[1];
+    int64_t tg, te;
+    const int64_t g0 = g, e0 = e;
+    scan2(sh, g, e, tg, te);
+    const int64_t eq_rank = b1 + e;
+    const bool sel = g0 || (e0 && eq_rank < eq_take);
+    const int64_t pos = b0 + g + (e < eq_take - b1 ? e : (eq_take - b1 > 0 ? eq_take - b1 : 0));
     if (sel) {
       o[pos] = (int32_t)i;
       if (mk) atomicOr((unsigned long long *)&mk[i >> 6], 1ull << (i & 63));
     }
-    __syncthreads();
     if (tid == 0) {
-      for (int q = 0; q < kSelThreads / 64; ++q) {
-        sh_base[0] += wsum[q][1];
-        sh_base[1] += wsum[q][0];
-      }
+      sh.base[0] = b0 + tg + (te < eq_take - b1 ? te : (eq_take - b1 > 0 ? eq_take - b1 : 0));
+      sh.base[1] = b1 + te;
     }
     __syncthreads();
   }
+}
+
+void launch_select(const uint64_t *keys, int64_t key_stride, int64_t n, int k, int32_t *out, int64_t out_stride,
+                   uint64_t *mask, int64_t mask_stride, int64_t mask_words, int units, hipStream_t s) {
+  if (n <= (int64_t)kSelKPT * kSelThreads)
+    hipLaunchKernelGGL(select_kernel<kSelKPT>, dim3(units), dim3(kSelThreads), 0, s, keys, key_stride, n, k, out,
+                       out_stride, mask, mask_stride, mask_words);
+  else
+    hipLaunchKernelGGL(select_kernel<0>, dim3(units), dim3(kSelThreads), 0, s, keys, key_stride, n, k, out,
+                       out_stride, mask, mask_stride, mask_words);
 }
 
 // Copy the exact key/value rows of the selected residual tokens into exact-format
@@ -215,10 +368,20 @@ extern "C" gkv_status gkv_quest_select(const uint16_t *q, const gkv_cache *c, in
   uint64_t *keys = (uint64_t *)ws;
   if (ncur > 0) {
     dim3 grid((unsigned)((ncur + 255) / 256), c->Hkv, c->B);
-    hipLaunchKernelGGL(quest_score_kernel, grid, dim3(256), 0, s, q, c->boxes, c->npage_cap, ncur, c->Hkv, G, keys);
+    switch (G) {
+#define GKV_SCORE(g)                                                                                          \
+  case g:                                                                                                     \
+    hipLaunchKernelGGL(quest_score_kernel<g>, grid, dim3(256), 0, s, q, c->boxes, c->npage_cap, ncur, c->Hkv, \
+                       keys);                                                                                 \
+    break;
+      GKV_SCORE(1) GKV_SCORE(2) GKV_SCORE(3) GKV_SCORE(4) GKV_SCORE(5) GKV_SCORE(6) GKV_SCORE(7) GKV_SCORE(8)
+      GKV_SCORE(9) GKV_SCORE(10) GKV_SCORE(11) GKV_SCORE(12) GKV_SCORE(13) GKV_SCORE(14) GKV_SCORE(15)
+      GKV_SCORE(16)
+#undef GKV_SCORE
+      default: return GKV_E_SHAPE;
+    }
   }
-  hipLaunchKernelGGL(select_kernel, dim3(c->B * c->Hkv), dim3(kSelThreads), 0, s, (const uint64_t *)keys, c->npage_cap,
-                     ncur, topk, pages, (int64_t)topk, (uint64_t *)nullptr, (int64_t)0, (int64_t)0);
+  launch_select((const uint64_t *)keys, c->npage_cap, ncur, topk, pages, (int64_t)topk, nullptr, 0, 0, c->B * c->Hkv, s);
   return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP;
 }
 
@@ -234,9 +397,8 @@ extern "C" gkv_status gkv_rd_residual_select(gkv_cache *c, const uint16_t *k_src
   hipStream_t s = (hipStream_t)stream;
   uint64_t *keys = (uint64_t *)ws;
   if (nkeep > 0) gkv_launch_rd_score(c, v_src, mass, keys, s);
-  hipLaunchKernelGGL(select_kernel, dim3(c->B * c->Hkv), dim3(kSelThreads), 0, s, (const uint64_t *)keys, c->T, c->T,
-                     nkeep, c->res_idx, (int64_t)c->nres_cap, c->res_mask, (int64_t)c->nblk_cap,
-                     (int64_t)c->nblk_cap);
+  launch_select((const uint64_t *)keys, c->T, c->T, nkeep, c->res_idx, (int64_t)c->nres_cap, c->res_mask,
+                (int64_t)c->nblk_cap, (int64_t)c->nblk_cap, c->B * c->Hkv, s);
   if (nkeep > 0) {
     dim3 g2((unsigned)((nkeep + P - 1) / P), c->Hkv, c->B);
     hipLaunchKernelGGL(res_gather_kernel, g2, dim3(256), 0, s, k_src, v_src, c->T, (const int32_t *)c->res_idx,

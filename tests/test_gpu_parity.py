@@ -111,10 +111,11 @@ def test_quest_ties_go_to_lower_page(gpu):
         np.testing.assert_array_equal(got, oquest.select_top(s, k))
 
 
-@pytest.mark.parametrize("T,Bn", [(8192, 2), (3000, 1)])
+@pytest.mark.parametrize("T,Bn", [(8192, 2), (3000, 1), (9001, 1)])
 def test_rd_residual_selection_and_attention(gpu, T, Bn):
     """Workload 4 shapes at reduced length: 28 query / 4 KV heads, 2% residual by
-    attention mass x squared value error."""
+    attention mass x squared value error.  T = 9001 exceeds the register-resident
+    selection (8192 keys) and takes the streamed one."""
     Hq, Hkv = 28, 4
     ks, vs = kv_all(4, Bn, Hkv, T)
     lv = olad.ladder("graded", T)
@@ -276,3 +277,17 @@ def test_staged_attention_equals_one_call(gpu):
     cache.attn_partials(qd)
     cache.attn_merge(out)
     assert torch.equal(one, out)
+
+
+def test_quest_selection_beyond_register_keys(gpu):
+    """More than 8192 ranked pages (T = 16 * 8300): the streamed selection path
+    must give the oracle's page set (selection only: the page order is index work)."""
+    T, Hq, Hkv, page, topk = 16 * 8300 + 5, 4, 1, 16, 200
+    ks, vs = kv_all(3, 1, Hkv, T)
+    lv = olad.ladder("graded", T)
+    cache = _build(gpu, ks, vs, Hq, lv, page=page)
+    q = synth.queries(3, 1, Hq, step=7)
+    pages = cache.quest_select(q, topk).cpu().numpy()
+    kmin, kmax = oquest.page_boxes(ks[0, 0])
+    want = oquest.quest_select(q_group(q, 0, 0, Hq), kmin, kmax, T, topk)
+    np.testing.assert_array_equal(pages[0, 0], want)
