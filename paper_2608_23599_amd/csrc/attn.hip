@@ -172,20 +172,19 @@ struct AttnParams {
   const uint64_t *res_mask;
   const uint8_t *res_rows;
   const int32_t *pages;
-  uint8_t *plan;   // visit descriptors, vcap per (b, KV head)
-  int32_t *split;  // first visit of each wavefront, W + 1 per (b, KV head)
+  uint8_t *visits;  // visit descriptors (plan kernel scratch), vcap per (b, KV head)
+  uint8_t *plan;    // item descriptors, icap per (b, KV head)
+  int32_t *split;   // first item of each wavefront, W + 1 per (b, KV head)
   float *part;
   int64_t T;
   int nblk_cap, Hkv, G, nres, nrb_cap, topk, nsplit;
-  int64_t vcap;
+  int64_t vcap, icap;
   float sl2;  // log2(e) / sqrt(D)
 };
 
 constexpr int kRing = 16384;    // staging ring per wavefront (bytes, a power of two)
-constexpr int kQueue = 16;      // item descriptors in flight per wavefront
-constexpr int kQueueBytes = 32 * kQueue;
-constexpr int kDescBytes = 2048;  // visit-descriptor ring: two 1 KB chunks
-constexpr int kWaveLds = kRing + kQueueBytes + kDescBytes;  // LDS per wavefront
+constexpr int kDescBytes = 2048;  // item-descriptor ring: two 1 KB chunks
+constexpr int kWaveLds = kRing + kDescBytes;  // LDS per wavefront
 constexpr int kMaxWaves = 1024;   // wavefronts per (b, KV head)
 
 
@@ -232,16 +231,25 @@ __device__ __forceinline__ int64_t uni64(int64_t x) {
 //   int group:    [K scale/zero if first][K codes of n tiles][V codes of n tiles]
 //                 [V scale/zero if last]   (n consecutive read tiles of one block)
 //   centroid:     [K record][V record]
+// The plan kernel expands every visit into its items and writes one 32-byte
+// descriptor per item; the attention kernel only follows the list.
 enum ItemKind { kExactTile = 0, kIntGroup = 1, kCentroid = 2 };
 
-// meta: kind (2 bits) | level (5) | first (1) | last (1) | tile mask (4) | tile
-// count (3) | exact tile's valid-token bits (16)
-struct Item {
-  uint32_t lin;      // linear ring position of the item (bytes)
-  uint32_t end;      // linear ring position after it
-  uint32_t cnt_end;  // load instructions issued through this item
+// Item descriptor.  meta: kind (2 bits) | level (5) | first (1) | last (1) | tile
+// mask (4) | tile count (3) | exact tile's valid-token bits (16).  geo: size in
+// 16-byte units (10 bits) | load instructions (6) | 16-byte units per code segment (10).
+struct ItemDesc {
+  uint64_t kp, vp;  // K and V record addresses
+  uint64_t valid;   // tokens of the block that are read
+  uint32_t meta, geo;
+};
+static_assert(sizeof(ItemDesc) == 32, "descriptor size");
+constexpr int kDescChunk = 1024 / sizeof(ItemDesc);  // descriptors per copy (one 1 KB copy)
+constexpr uint32_t kMaxAhead = kDescChunk / 2;          // producer lead over the consumer, in items
+
+struct Item {  // the consumer's view of an item
+  uint32_t lin, end;  // linear ring positions of the item and after it
   uint32_t meta;
-  uint32_t koff, kun, voff, vun;  // producer only: code segments (offset in record, 16-byte units)
   __device__ int kind() const { return meta & 3u; }
   __device__ int lv() const { return (meta >> 2) & 31u; }
   __device__ bool first() const { return (meta >> 7) & 1u; }
@@ -251,120 +259,12 @@ struct Item {
   __device__ uint32_t tvalid() const { return meta >> 16; }
 };
 
+__device__ __forceinline__ uint32_t geo_size(uint32_t g) { return (g & 1023u) * 16u; }
+__device__ __forceinline__ uint32_t geo_ninstr(uint32_t g) { return (g >> 10) & 63u; }
+__device__ __forceinline__ uint32_t geo_units(uint32_t g) { return g >> 16; }
+
 // Consecutive read tiles per int item: about 4 KB of codes (K + V).
 __device__ __forceinline__ int group_tiles(int lv) { return lv == 2 ? 4 : (lv == 4 ? 2 : 1); }
-
-// A visit: one block of one (b, KV head) and the tokens of it that are read.  The
-// plan kernel writes one 32-byte descriptor per visit, in visit order, and the
-// split of the visits over the wavefronts.
-struct VisitDesc {
-  uint64_t kp, vp;  // addresses of the K and V records
-  uint64_t valid;   // tokens of the block that are read (bit t = token t)
-  int32_t level;    // storage level of both records
-  uint32_t cost;    // balance cost (plan kernel only)
-};
-static_assert(sizeof(VisitDesc) == 32, "descriptor size");
-constexpr int kDescChunk = 1024 / sizeof(VisitDesc);  // descriptors per copy (one 1 KB copy)
-
-// Walks the visits of one wavefront and the items of each visit.  The wavefront's
-// descriptors stream through a two-slot LDS ring, one 1 KB chunk per copy, each
-// chunk requested one chunk ahead of its first use.
-struct Walker {
-  const uint8_t *dsrc;   // descriptors of this wavefront's visits
-  const uint8_t *dring;  // the descriptor ring (2 x 1 KB of LDS)
-  uint32_t dlds;         // its LDS address
-  uint32_t dcnt0, dcnt1;  // load count through the copy of each slot's chunk
-  uint32_t v, nv;         // next visit (relative), number of visits
-  const uint8_t *kp, *vp;
-  uint64_t valid;
-  uint32_t lin, cnt;  // ring position and loads issued, both through the last item
-  int lv;
-  uint32_t tiles;  // read tiles not yet emitted
-  bool in_visit, first;
-
-  __device__ __forceinline__ void fetch_chunk(uint32_t c, int lane) {  // copy descriptor chunk c
-    dma16(dsrc + (size_t)c * 1024 + 16 * lane, dlds + (c & 1) * 1024);
-    ++cnt;
-    if (c & 1) dcnt1 = cnt;
-    else dcnt0 = cnt;
-  }
-
-  // `cnt` equals the number of loads issued whenever the walker runs: the producer
-  // issues every item before asking for the next one.
-  __device__ bool open_visit(int lane) {
-    while (v < nv) {
-      const uint32_t r = v++;
-      const uint32_t c = r / kDescChunk;
-      if (r % kDescChunk == 0) {
-        wait_loads(cnt - ((c & 1) ? dcnt1 : dcnt0));
-        if ((c + 1) * kDescChunk < nv) fetch_chunk(c + 1, lane);  // the other slot is done with
-      }
-      const uint8_t *e = dring + (c & 1) * 1024 + (r % kDescChunk) * 32;
-      const uint4 d0 = *(const uint4 *)e, d1 = *(const uint4 *)(e + 16);
-      kp = (const uint8_t *)(uintptr_t)uni64((int64_t)(((uint64_t)d0.y << 32) | d0.x));
-      vp = (const uint8_t *)(uintptr_t)uni64((int64_t)(((uint64_t)d0.w << 32) | d0.z));
-      valid = (uint64_t)uni64((int64_t)(((uint64_t)d1.y << 32) | d1.x));
-      lv = uni((int32_t)d1.z);
-      tiles = 0;
-      for (int t = 0; t < 4; ++t)
-        if ((valid >> (16 * t)) & 0xFFFFull) tiles |= 1u << t;
-      if (!tiles) continue;
-      first = true;
-      in_visit = true;
-      return true;
-    }
-    return false;
-  }
-
-  __device__ bool next(Item &it, int lane) {
-    if (!in_visit && !open_visit(lane)) return false;
-    uint32_t kind, taken, n = 1, tv = 0, size, ninstr;
-    bool f = false, l = true;
-    if (lv == GKV_CENTROID) {
-      kind = kCentroid;
-      taken = tiles;
-      it.koff = it.voff = 0;
-      it.kun = it.vun = kCentBytes / 16;
-      size = 2 * kCentBytes;
-      ninstr = 2 * ((kCentBytes / 16 + 63) / 64);
-    } else if (lv == GKV_EXACT) {
-      kind = kExactTile;
-      const uint32_t t = __builtin_ctz(tiles);
-      taken = 1u << t;
-      tv = (uint32_t)((valid >> (16 * t)) & 0xFFFFull);
-      it.koff = it.voff = t * 4096;
-      it.kun = it.vun = 256;
-      size = 2 * 4096;
-      ninstr = 8;
-    } else {
-      kind = kIntGroup;
-      const uint32_t t = __builtin_ctz(tiles);
-      const int tg = group_tiles(lv);
-      while ((int)n < tg && ((tiles >> (t + n)) & 1u)) ++n;
-      taken = ((1u << n) - 1) << t;
-      f = first;
-      it.koff = it.voff = kSZBytes + t * 256 * lv;
-      it.kun = it.vun = n * 16 * lv;
-      const uint32_t cu = n * 16 * lv;  // units per code segment (a multiple of 32)
-      l = (tiles & ~taken) == 0;
-      size = 2 * 16 * cu + (f ? kSZBytes : 0) + (l ? kSZBytes : 0);
-      ninstr = 2 * ((cu + 63) / 64) + (f ? 1 : 0) + (l ? 1 : 0);
-    }
-    tiles &= ~taken;
-    first = false;
-    if (!tiles) in_visit = false;
-    const uint32_t off = lin & (kRing - 1);
-    if (off + size > kRing) lin += kRing - off;  // an item never wraps around the ring end
-    it.lin = lin;
-    lin += size;
-    it.end = lin;
-    cnt += ninstr;
-    it.cnt_end = cnt;
-    it.meta = kind | ((uint32_t)lv << 2) | ((uint32_t)f << 7) | ((uint32_t)l << 8) | (taken << 9) | (n << 13) |
-              (tv << 16);
-    return true;
-  }
-};
 
 // Copy `units` 16-byte units from `src` to LDS address `dst` (1 KB per instruction;
 // only a last partial instruction is lane-predicated).
@@ -378,64 +278,97 @@ __device__ __forceinline__ void copy_segment(const uint8_t *src, uint32_t units,
   }
 }
 
-// Issue the copies of the producer's current item.
-__device__ __forceinline__ void issue(const Walker &w, const Item &it, uint32_t ring_base, int lane) {
-  uint32_t dst = ring_base + (it.lin & (kRing - 1));
-  const bool sz = it.kind() == kIntGroup;
-  if (sz && it.first()) {
-    copy_segment(w.kp, kSZBytes / 16, dst, lane);
-    dst += kSZBytes;
-  }
-  copy_segment(w.kp + it.koff, it.kun, dst, lane);
-  dst += 16 * it.kun;
-  copy_segment(w.vp + it.voff, it.vun, dst, lane);
-  dst += 16 * it.vun;
-  if (sz && it.last()) copy_segment(w.vp, kSZBytes / 16, dst, lane);
-}
-
 // ---------------------------------------------------------------- pipeline
-// Producer side of a wavefront's pipeline: the walker, its next item, the ring and
-// a queue of issued item descriptors (lin, end, cnt_end, meta, valid lo, valid hi)
-// that the consumer pops in order.
+// One wavefront's pipeline over its item list.  The producer copies items ahead
+// into the LDS ring; the consumer pops them in order.  Both read the item
+// descriptors from a two-slot LDS ring of 32-descriptor chunks, and both derive
+// the same sequence of ring positions and load counts from the descriptors, so
+// nothing else passes between them.  The producer copies chunk c + 1 just before
+// item 32c + 16 and stays at most kMaxAhead items ahead of the consumer, so the
+// slot it overwrites (chunk c - 1) is no longer read.
 struct Pipe {
-  Walker prod;
-  Item pend;
-  bool has_pend;
-  uint32_t issued;      // load instructions issued
-  uint32_t hold;        // ring bytes before this linear position are free
-  uint32_t head, tail;  // queue indices (popped / pushed)
-  uint32_t ring_base;
-  const uint8_t *ring;
-  uint32_t *queue;
+  const uint8_t *ring;   // staging ring (LDS)
+  const uint8_t *dring;  // descriptor ring (LDS, 2 x 1 KB)
+  const uint8_t *dsrc;   // this wavefront's descriptors (global)
+  uint32_t ring_base, dlds;  // LDS addresses of the two rings (wave-uniform)
+  uint32_t nitems;
+  uint32_t issued;  // load instructions issued
+  // producer
+  uint32_t pk, plin, pchunk;  // next item, its ring position, load count through the last chunk copy
+  bool pend;                  // descriptor of item pk already read
+  uint64_t pkp, pvp;
+  uint32_t pmeta, pgeo;
+  // consumer
+  uint32_t ck, clin, ccnt, hold;
   int lane;
 
+  __device__ __forceinline__ void fetch_chunk(uint32_t c) {
+    dma16(dsrc + (size_t)c * 1024 + 16 * lane, dlds + (c & 1) * 1024);
+    pchunk = ++issued;
+  }
+  __device__ __forceinline__ const uint8_t *desc(uint32_t k) const {
+    return dring + ((k / kDescChunk) & 1) * 1024 + (k % kDescChunk) * sizeof(ItemDesc);
+  }
+  __device__ __forceinline__ bool chunk_copy_before(uint32_t k) const {  // a chunk copy precedes item k
+    return k % kDescChunk == kDescChunk / 2 && (k / kDescChunk + 1) * kDescChunk < nitems;
+  }
+  __device__ __forceinline__ static uint32_t place(uint32_t lin, uint32_t size) {  // no wrap inside an item
+    const uint32_t off = lin & (kRing - 1);
+    return off + size > kRing ? lin + (kRing - off) : lin;
+  }
+
   __device__ __forceinline__ void pump() {
-    while (has_pend && tail - head < (uint32_t)kQueue && pend.end - hold <= (uint32_t)kRing) {
-      issue(prod, pend, ring_base, lane);
-      issued = pend.cnt_end;
-      if (lane == 0) {
-        uint32_t *q = queue + 8 * (tail % kQueue);
-        *(uint4 *)q = make_uint4(pend.lin, pend.end, pend.cnt_end, pend.meta);
-        *(uint2 *)(q + 4) = make_uint2((uint32_t)prod.valid, (uint32_t)(prod.valid >> 32));
+    while (pk < nitems && pk - ck < kMaxAhead) {
+      if (!pend) {
+        if (pk % kDescChunk == 0) wait_loads(issued - pchunk);  // chunk pk / 32 has landed
+        const uint8_t *e = desc(pk);
+        const uint4 d0 = *(const uint4 *)e, d1 = *(const uint4 *)(e + 16);
+        pkp = (uint64_t)uni64((int64_t)(((uint64_t)d0.y << 32) | d0.x));
+        pvp = (uint64_t)uni64((int64_t)(((uint64_t)d0.w << 32) | d0.z));
+        pmeta = uni((int32_t)d1.z);
+        pgeo = uni((int32_t)d1.w);
+        pend = true;
       }
-      ++tail;
-      has_pend = prod.next(pend, lane);
+      const uint32_t size = geo_size(pgeo), lin = place(plin, size);
+      if (lin + size - hold > (uint32_t)kRing) break;  // ring full
+      if (chunk_copy_before(pk)) fetch_chunk(pk / kDescChunk + 1);
+      // the copy segments of the item
+      const uint8_t *kp = (const uint8_t *)(uintptr_t)pkp, *vp = (const uint8_t *)(uintptr_t)pvp;
+      const int kind = pmeta & 3u, lv = (pmeta >> 2) & 31u;
+      const uint32_t t0 = __builtin_ctz((pmeta >> 9) & 15u), un = geo_units(pgeo);
+      const uint32_t koff = kind == kIntGroup ? kSZBytes + t0 * 256 * lv : (kind == kExactTile ? t0 * 4096 : 0);
+      uint32_t dst = ring_base + (lin & (kRing - 1));
+      if (kind == kIntGroup && ((pmeta >> 7) & 1u)) {
+        copy_segment(kp, kSZBytes / 16, dst, lane);
+        dst += kSZBytes;
+      }
+      copy_segment(kp + koff, un, dst, lane);
+      dst += 16 * un;
+      copy_segment(vp + koff, un, dst, lane);
+      dst += 16 * un;
+      if (kind == kIntGroup && ((pmeta >> 8) & 1u)) copy_segment(vp, kSZBytes / 16, dst, lane);
+      issued += geo_ninstr(pgeo);
+      plin = lin + size;
+      ++pk;
+      pend = false;
     }
   }
-  // Pop the next item (false when the sequence is exhausted), wait for its copies.
+  // Pop the next item (false when the list is exhausted), wait for its copies.
   __device__ __forceinline__ bool pop(Item &it, uint64_t &valid, const uint8_t *&ip) {
     pump();
-    if (head == tail) return false;
-    const uint32_t *q = queue + 8 * (head % kQueue);
-    const uint4 e = *(const uint4 *)q;
-    const uint2 vv = *(const uint2 *)(q + 4);
-    it.lin = uni(e.x);
-    it.end = uni(e.y);
-    it.cnt_end = uni(e.z);
-    it.meta = uni(e.w);
-    valid = ((uint64_t)(uint32_t)uni(vv.y) << 32) | (uint32_t)uni(vv.x);
-    ++head;
-    wait_loads(issued - it.cnt_end);
+    if (ck == nitems) return false;
+    const uint8_t *e = desc(ck);
+    const uint4 d1 = *(const uint4 *)(e + 16);
+    valid = (uint64_t)uni64((int64_t)(((uint64_t)d1.y << 32) | d1.x));
+    it.meta = uni((int32_t)d1.z);
+    const uint32_t geo = uni((int32_t)d1.w), size = geo_size(geo);
+    it.lin = place(clin, size);
+    it.end = it.lin + size;
+    clin = it.end;
+    if (chunk_copy_before(ck)) ++ccnt;
+    ccnt += geo_ninstr(geo);
+    ++ck;
+    wait_loads(issued - ccnt);
     ip = ring + (it.lin & (kRing - 1));
     return true;
   }
@@ -814,35 +747,27 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   st.m = kNegInf;
   st.l = 0.f;
 
-  // this wavefront's visits, from the plan
+  // this wavefront's items, from the plan
   const int32_t *sp = p.split + u * (int64_t)(W + 1);
-  const uint32_t vstart = (uint32_t)uni(sp[w]), vend = (uint32_t)uni(sp[w + 1]);
+  const uint32_t istart = (uint32_t)uni(sp[w]), iend = (uint32_t)uni(sp[w + 1]);
 
   // ---------------- pipelined item loop
   Pipe pp;
-  pp.prod.dsrc = p.plan + (u * p.vcap + vstart) * (int64_t)sizeof(VisitDesc);
-  pp.prod.dring = smem + wave * kWaveLds + kRing + kQueueBytes;
-  pp.prod.dlds = (uint32_t)uni((int32_t)(uintptr_t)pp.prod.dring);
-  pp.prod.dcnt0 = pp.prod.dcnt1 = 0;
-  pp.prod.v = 0;
-  pp.prod.nv = vend - vstart;
-  pp.prod.lin = 0;
-  pp.prod.cnt = 0;
-  pp.prod.in_visit = false;
-  pp.prod.first = false;
-  pp.prod.tiles = 0;
-  pp.prod.lv = 0;
-  pp.prod.valid = 0;
-  pp.prod.kp = pp.prod.vp = nullptr;
   pp.ring = smem + wave * kWaveLds;
-  pp.queue = (uint32_t *)(smem + wave * kWaveLds + kRing);
+  pp.dring = smem + wave * kWaveLds + kRing;
   pp.ring_base = (uint32_t)uni((int32_t)(uintptr_t)pp.ring);
+  pp.dlds = (uint32_t)uni((int32_t)(uintptr_t)pp.dring);
+  pp.dsrc = p.plan + (u * p.icap + istart) * (int64_t)sizeof(ItemDesc);
+  pp.nitems = iend - istart;
   pp.lane = lane;
   pp.issued = 0;
-  pp.hold = 0;
-  pp.head = pp.tail = 0;
-  if (pp.prod.nv) pp.prod.fetch_chunk(0, lane);
-  pp.has_pend = pp.prod.next(pp.pend, lane);
+  pp.pk = pp.plin = pp.pchunk = 0;
+  pp.pend = false;
+  pp.pkp = pp.pvp = 0;
+  pp.pmeta = pp.pgeo = 0;
+  pp.ck = pp.clin = pp.hold = 0;
+  if (pp.nitems) pp.fetch_chunk(0);
+  pp.ccnt = pp.issued;
   // Items are processed in runs of one level, each run in a loop specialised for
   // that level (the constants of one level's path are then live only in its loop).
   Item it;
@@ -939,17 +864,28 @@ __global__ void __launch_bounds__(D) merge_kernel(const float *part, float *out,
 }
 
 // ---------------------------------------------------------------- plan
-// One workgroup per (b, KV head): writes the visit descriptors in visit order and
-// splits the visits over the W wavefronts by a cost that counts the bytes read and
-// a fixed cost per pipeline item (visit v goes to the wavefront that owns the
-// midpoint of its cost interval).
+// One workgroup per (b, KV head).  A visit is one block and the tokens of it that
+// are read: all valid tokens of a dense read minus the residual rows, or the
+// selected pages of a Compressed-Quest read.  The plan kernel describes the visits,
+// splits them over the W wavefronts by a balance cost (visit v goes to the
+// wavefront that owns the midpoint of its cost interval), and expands every visit
+// into its pipeline items, written in order; each wavefront's items are the items
+// of its visits.
 constexpr int kPlanThreads = 1024;
+
+struct VisitDesc {
+  uint64_t kp, vp;  // addresses of the K and V records
+  uint64_t valid;   // tokens of the block that are read (bit t = token t)
+  int32_t level;    // storage level of both records
+  uint32_t cost;    // balance cost (bits 0..23) | number of items (bits 24..31)
+};
+static_assert(sizeof(VisitDesc) == 32, "descriptor size");
 // Balance cost of a visit: the measured time of its parts on one wavefront sharing
 // its SIMD (about 8 cycles per unit).  Exact tiles are bound by the wavefront's
 // share of the bandwidth (8 KB each), int tiles by the dequantisation and softmax
 // work rather than by their bytes.
-constexpr uint32_t kCostExactTile = 625, kCostInt8Tile = 450, kCostInt4Tile = 300, kCostInt2Tile = 210,
-                   kCostCentroid = 550, kCostIntBlock = 240;
+constexpr uint32_t kCostExactTile = 500, kCostInt8Tile = 450, kCostInt4Tile = 300, kCostInt2Tile = 210,
+                   kCostCentroid = 565, kCostIntBlock = 240;
 
 __device__ __forceinline__ uint32_t balance_cost(int lv, uint64_t va) {
   uint32_t tiles = 0;
@@ -990,12 +926,151 @@ __device__ __forceinline__ uint64_t block_scan(uint64_t x, uint64_t *sh, uint64_
   return x + before;
 }
 
+// Number of items of a visit (as visit_items writes them).
+__device__ __forceinline__ uint32_t visit_item_count(int lv, uint64_t valid) {
+  uint32_t tiles = 0;
+  for (int t = 0; t < 4; ++t)
+    if ((valid >> (16 * t)) & 0xFFFFull) tiles |= 1u << t;
+  if (!tiles) return 0;
+  if (lv == GKV_CENTROID) return 1;
+  if (lv == GKV_EXACT) return __builtin_popcount(tiles);
+  const int tg = group_tiles(lv);
+  uint32_t k = 0;
+  while (tiles) {
+    const uint32_t t = __builtin_ctz(tiles);
+    uint32_t n = 1;
+    while ((int)n < tg && ((tiles >> (t + n)) & 1u)) ++n;
+    tiles &= ~(((1u << n) - 1) << t);
+    ++k;
+  }
+  return k;
+}
+
+// Writes the items of a visit (at most 4), in order, to out[]; returns their number.
+__device__ __forceinline__ int visit_items(const VisitDesc &v, ItemDesc *out) {
+  uint32_t tiles = 0;
+  for (int t = 0; t < 4; ++t)
+    if ((v.valid >> (16 * t)) & 0xFFFFull) tiles |= 1u << t;
+  if (!tiles) return 0;
+  const uint32_t lv = (uint32_t)v.level;
+  auto put = [&](int i, uint32_t kind, bool first, bool last, uint32_t taken, uint32_t n, uint32_t tv,
+                 uint32_t size, uint32_t ninstr, uint32_t units) {
+    out[i].kp = v.kp;
+    out[i].vp = v.vp;
+    out[i].valid = v.valid;
+    out[i].meta = kind | (lv << 2) | ((uint32_t)first << 7) | ((uint32_t)last << 8) | (taken << 9) | (n << 13) |
+                  (tv << 16);
+    out[i].geo = (size / 16) | (ninstr << 10) | (units << 16);
+  };
+  if (lv == GKV_CENTROID) {
+    put(0, kCentroid, true, true, tiles, 1, 0, 2 * kCentBytes, 2 * ((kCentBytes / 16 + 63) / 64), kCentBytes / 16);
+    return 1;
+  }
+  int k = 0;
+  if (lv == GKV_EXACT) {
+    for (int t = 0; t < 4; ++t)
+      if ((tiles >> t) & 1u)
+        put(k++, kExactTile, true, true, 1u << t, 1, (uint32_t)((v.valid >> (16 * t)) & 0xFFFFull), 2 * 4096, 8, 256);
+    return k;
+  }
+  const int tg = group_tiles((int)lv);
+  uint32_t left = tiles;
+  bool first = true;
+  while (left) {
+    const uint32_t t = __builtin_ctz(left);
+    uint32_t n = 1;
+    while ((int)n < tg && ((left >> (t + n)) & 1u)) ++n;
+    const uint32_t taken = ((1u << n) - 1) << t;
+    left &= ~taken;
+    const bool last = left == 0;
+    const uint32_t cu = n * 16 * lv;  // units per code segment (a multiple of 32)
+    put(k++, kIntGroup, first, last, taken, n, 0, 2 * 16 * cu + (first ? kSZBytes : 0) + (last ? kSZBytes : 0),
+        2 * ((cu + 63) / 64) + (first ? 1 : 0) + (last ? 1 : 0), cu);
+    first = false;
+  }
+  return k;
+}
+
+// Visit v of a dense read: block v (v < nblk), else residual pseudo-block v - nblk.
+__device__ __forceinline__ VisitDesc dense_visit(const AttnParams &p, int64_t u, int64_t nblk, int64_t v) {
+  VisitDesc d;
+  if (v < nblk) {
+    d.level = p.level[u * p.nblk_cap + v];
+    d.kp = (uint64_t)(uintptr_t)(p.arena + p.koff[u * p.nblk_cap + v]);
+    d.vp = (uint64_t)(uintptr_t)(p.arena + p.voff[u * p.nblk_cap + v]);
+    d.valid = token_mask(p.T - v * P);
+    if (p.nres) d.valid &= ~p.res_mask[u * p.nblk_cap + v];
+  } else {
+    const int64_t rb = v - nblk;
+    const uint8_t *kp = p.res_rows + (u * p.nrb_cap + rb) * (2 * kExactBytes);
+    d.level = GKV_EXACT;
+    d.kp = (uint64_t)(uintptr_t)kp;
+    d.vp = (uint64_t)(uintptr_t)(kp + kExactBytes);
+    d.valid = token_mask(p.nres - rb * P);
+  }
+  d.cost = balance_cost(d.level, d.valid) | (visit_item_count(d.level, d.valid) << 24);
+  return d;
+}
+
+// Wavefront owning the midpoint of cost interval [e, e + c) of a total, in fp64
+// (every operand is an integer below 2^53, and the floor of a monotone quotient
+// keeps the owners non-decreasing along the visits).
+__device__ __forceinline__ int midpoint_owner(int W, uint64_t e, uint32_t c, uint64_t total) {
+  if (!total) return 0;
+  const double o = __builtin_floor(((double)W * (double)(2 * e + c)) / (2.0 * (double)total));
+  return o < (double)W ? (int)o : W - 1;
+}
+
+// Dense plan when every thread holds at most kPlanRegs visits: the visits stay in
+// registers through the cost scan and the item expansion.
+constexpr int kPlanRegs = 4;
+__device__ __forceinline__ void plan_dense_regs(const AttnParams &p, int64_t u, int64_t nblk, int64_t nvis, int W,
+                                                ItemDesc *items, int32_t *split, uint64_t *sh, uint32_t *lastc) {
+  const int64_t per = (nvis + kPlanThreads - 1) / kPlanThreads;
+  const int64_t v0 = threadIdx.x * per, v1 = v0 + per < nvis ? v0 + per : nvis;
+  VisitDesc dv[kPlanRegs];
+  uint64_t mine = 0;
+  uint32_t last = 0;
+#pragma unroll
+  for (int j = 0; j < kPlanRegs; ++j)
+    if (v0 + j < v1) {
+      dv[j] = dense_visit(p, u, nblk, v0 + j);
+      const uint32_t c = dv[j].cost;
+      mine += ((uint64_t)(c & 0xFFFFFFu) << 24) | (c >> 24);
+      last = c & 0xFFFFFFu;
+    }
+  lastc[threadIdx.x] = last;  // read by the next thread after the scan's barriers
+  uint64_t tot;
+  const uint64_t excl = block_scan(mine, sh, tot) - mine;
+  const uint64_t total = tot >> 24;
+  const uint32_t nitems = (uint32_t)(tot & 0xFFFFFFu);
+  if (v0 >= v1) return;
+  uint64_t ecost = excl >> 24;
+  uint32_t eitem = (uint32_t)(excl & 0xFFFFFFu);
+  int prev = -1;
+  if (v0 > 0) prev = midpoint_owner(W, ecost - lastc[threadIdx.x - 1], lastc[threadIdx.x - 1], total);
+#pragma unroll
+  for (int j = 0; j < kPlanRegs; ++j)
+    if (v0 + j < v1) {
+      const uint32_t c = dv[j].cost & 0xFFFFFFu;
+      const int own = midpoint_owner(W, ecost, c, total);
+      for (int ww = prev + 1; ww <= own; ++ww) split[ww] = (int32_t)eitem;
+      eitem += visit_items(dv[j], items + eitem);
+      if (v0 + j == nvis - 1)
+        for (int ww = own + 1; ww <= W; ++ww) split[ww] = (int32_t)nitems;
+      prev = own;
+      ecost += c;
+    }
+}
+
 __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
   __shared__ uint64_t sh[2 * kPlanThreads / 64];
+  __shared__ uint32_t lastc[kPlanThreads];
   __shared__ int s_cnt;
   const int64_t u = blockIdx.x;
   const int W = p.nsplit * kWaves;
-  VisitDesc *desc = (VisitDesc *)p.plan + u * p.vcap;
+  VisitDesc *desc = (VisitDesc *)p.visits + u * p.vcap;
+  ItemDesc *items = (ItemDesc *)p.plan + u * p.icap;
   int32_t *split = p.split + u * (int64_t)(W + 1);
   const int64_t nblk = (p.T + P - 1) / P;
   const int8_t *lvl = p.level + u * p.nblk_cap;
@@ -1006,27 +1081,13 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
     // thread describes a contiguous run of visits
     nvis = nblk + (p.nres + P - 1) / P;
     const int64_t per = (nvis + kPlanThreads - 1) / kPlanThreads;
+    if (nvis > 0 && per <= kPlanRegs) {
+      plan_dense_regs(p, u, nblk, nvis, W, items, split, sh, lastc);
+      return;
+    }
     const int64_t v0 = threadIdx.x * per, v1 = v0 + per < nvis ? v0 + per : nvis;
 #pragma unroll 4
-    for (int64_t v = v0; v < v1; ++v) {
-      VisitDesc d;
-      if (v < nblk) {
-        d.level = lvl[v];
-        d.kp = (uint64_t)(uintptr_t)(p.arena + ko[v]);
-        d.vp = (uint64_t)(uintptr_t)(p.arena + vo[v]);
-        d.valid = token_mask(p.T - v * P);
-        if (p.nres) d.valid &= ~p.res_mask[u * p.nblk_cap + v];
-      } else {
-        const int64_t rb = v - nblk;
-        const uint8_t *kp = p.res_rows + (u * p.nrb_cap + rb) * (2 * kExactBytes);
-        d.level = GKV_EXACT;
-        d.kp = (uint64_t)(uintptr_t)kp;
-        d.vp = (uint64_t)(uintptr_t)(kp + kExactBytes);
-        d.valid = token_mask(p.nres - rb * P);
-      }
-      d.cost = balance_cost(d.level, d.valid);
-      desc[v] = d;
-    }
+    for (int64_t v = v0; v < v1; ++v) desc[v] = dense_visit(p, u, nblk, v);
   } else {
     // Compressed-Quest: the leading valid ranked pages (ascending) and the current
     // page; consecutive pages of one block form one visit
@@ -1065,7 +1126,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
         for (int t = 0; t < 4; ++t)
           if (tl & (1u << t)) va |= 0xFFFFull << (16 * t);
         d.valid = va & token_mask(p.T - blk * P);
-        d.cost = balance_cost(d.level, d.valid);
+        d.cost = balance_cost(d.level, d.valid) | (visit_item_count(d.level, d.valid) << 24);
         desc[vbase + incl - 1] = d;
       }
       vbase += tot;
@@ -1077,33 +1138,39 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
     for (int ww = threadIdx.x; ww <= W; ww += kPlanThreads) split[ww] = 0;
     return;
   }
-  // prefix cost of each thread's run of visits, then the owner of every visit
+  // prefix cost and item count of each thread's run of visits (packed: cost in the
+  // high bits, items in the low 24), then the owner and first item of every visit
   const int64_t per = (nvis + kPlanThreads - 1) / kPlanThreads;
   const int64_t v0 = threadIdx.x * per, v1 = v0 + per < nvis ? v0 + per : nvis;
   uint64_t mine = 0;
 #pragma unroll 4
-  for (int64_t v = v0; v < v1; ++v) mine += desc[v].cost;
-  uint64_t total;
-  uint64_t excl = block_scan(mine, sh, total) - mine;
-  auto owner = [&](uint64_t e, uint32_t c) -> int {
-    if (!total) return 0;
-    const uint64_t o = ((uint64_t)W * (2 * e + c)) / (2 * total);
-    return o < (uint64_t)W ? (int)o : W - 1;
-  };
+  for (int64_t v = v0; v < v1; ++v) {
+    const uint32_t c = desc[v].cost;
+    mine += ((uint64_t)(c & 0xFFFFFFu) << 24) | (c >> 24);
+  }
+  uint64_t tot;
+  const uint64_t excl = block_scan(mine, sh, tot) - mine;
+  const uint64_t total = tot >> 24;
+  const uint32_t nitems = (uint32_t)(tot & 0xFFFFFFu);
+  auto owner = [&](uint64_t e, uint32_t c) -> int { return midpoint_owner(W, e, c, total); };
   if (v0 < v1) {
+    uint64_t ecost = excl >> 24;
+    uint32_t eitem = (uint32_t)(excl & 0xFFFFFFu);
     int prev = -1;
     if (v0 > 0) {
-      const uint32_t cp = desc[v0 - 1].cost;
-      prev = owner(excl - cp, cp);
+      const uint32_t cp = desc[v0 - 1].cost & 0xFFFFFFu;
+      prev = owner(ecost - cp, cp);
     }
     for (int64_t v = v0; v < v1; ++v) {
-      const uint32_t c = desc[v].cost;
-      const int own = owner(excl, c);
-      for (int ww = prev + 1; ww <= own; ++ww) split[ww] = (int32_t)v;
+      const VisitDesc d = desc[v];
+      const uint32_t c = d.cost & 0xFFFFFFu;
+      const int own = owner(ecost, c);
+      for (int ww = prev + 1; ww <= own; ++ww) split[ww] = (int32_t)eitem;
+      eitem += visit_items(d, items + eitem);
       if (v == nvis - 1)
-        for (int ww = own + 1; ww <= W; ++ww) split[ww] = (int32_t)nvis;
+        for (int ww = own + 1; ww <= W; ++ww) split[ww] = (int32_t)nitems;
       prev = own;
-      excl += c;
+      ecost += c;
     }
   }
 }
@@ -1129,10 +1196,10 @@ static int attn_nsplit(const gkv_cache *c, int32_t topk, int64_t T) {
 }
 
 // Workspace layout, sized by the cache capacity so that it does not move as T grows:
-// partials | wavefront splits | visit descriptors (+1 KB: the descriptor copies
-// read whole 1 KB chunks).
+// partials | wavefront splits | visit descriptors | item descriptors (at most 4
+// items per visit; +1 KB: the descriptor copies read whole 1 KB chunks).
 struct AttnLayout {
-  int64_t split, plan, total, vcap;
+  int64_t split, visits, plan, total, vcap, icap;
   int ncap;
 };
 static int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
@@ -1142,9 +1209,11 @@ static AttnLayout attn_layout(const gkv_cache *c, int32_t topk) {
   const int G = c->Hq / c->Hkv;
   L.ncap = attn_nsplit(c, topk, (int64_t)c->nblk_cap * P);
   L.vcap = topk > 0 ? (int64_t)topk + 1 : (int64_t)c->nblk_cap + (c->nres_cap + P - 1) / P;
+  L.icap = 4 * L.vcap;
   L.split = align256(units * L.ncap * G * (D + 2) * 4);
-  L.plan = L.split + align256(units * ((int64_t)L.ncap * kWaves + 1) * 4);
-  L.total = L.plan + units * L.vcap * (int64_t)sizeof(VisitDesc) + 1024;
+  L.visits = L.split + align256(units * ((int64_t)L.ncap * kWaves + 1) * 4);
+  L.plan = L.visits + align256(units * L.vcap * (int64_t)sizeof(VisitDesc));
+  L.total = L.plan + units * L.icap * (int64_t)sizeof(ItemDesc) + 1024;
   return L;
 }
 
@@ -1177,8 +1246,10 @@ static gkv_status attn_setup(const uint16_t *q, const gkv_cache *c, const int32_
   p.pages = pages;
   p.part = (float *)ws;
   p.split = (int32_t *)((uint8_t *)ws + L.split);
+  p.visits = (uint8_t *)ws + L.visits;
   p.plan = (uint8_t *)ws + L.plan;
   p.vcap = L.vcap;
+  p.icap = L.icap;
   p.T = c->T;
   p.nblk_cap = c->nblk_cap;
   p.Hkv = c->Hkv;
