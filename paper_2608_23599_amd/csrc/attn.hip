@@ -450,16 +450,31 @@ __device__ __forceinline__ uint4 lds16(const uint8_t *a) { return *(const uint4 
 // The group's queries live in LDS, one 272-byte row per head (padded against bank
 // conflicts); lane (head m, kg) reads its B-operand chunk of MFMA i.
 constexpr int kQRow = 272;
+// With PACK (group of at most 8 heads) MFMA columns 8..15 repeat heads 0..7, so
+// that an int block can carry the high and low query terms in one MFMA.
+template <bool PACK>
+__device__ __forceinline__ int qrow(int lane) { return PACK ? (lane & 7) : (lane & 15); }
+template <bool PACK>
 __device__ __forceinline__ half8 qchunk(const uint8_t *qs, int lane, int i) {
   U8 t;
-  t.v = lds16(qs + (lane & 15) * kQRow + (32 * i + 8 * (lane >> 4)) * 2);
+  t.v = lds16(qs + qrow<PACK>(lane) * kQRow + (32 * i + 8 * (lane >> 4)) * 2);
   return t.h;
+}
+
+// x[lane] + x[lane ^ 8] within each 16-lane row (DPP row rotate by 8).
+__device__ __forceinline__ f4 add_row_half(f4 x) {
+  f4 r;
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+    r[k] = x[k] + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x[k]), 0x128, 0xF, 0xF, false));
+  return r;
 }
 
 constexpr half4 kOnes = half4{(_Float16)1, (_Float16)1, (_Float16)1, (_Float16)1};
 
 // ---------------------------------------------------------------- items
 // Exact block tile: 16 tokens of fp16 K and V.
+template <bool PACK>
 __device__ __forceinline__ void exact_tile(const AttnParams &p, State &st, const uint8_t *qs, const uint8_t *ip,
                                            uint32_t tvalid, int lane) {
   const int kg = lane >> 4;
@@ -468,7 +483,7 @@ __device__ __forceinline__ void exact_tile(const AttnParams &p, State &st, const
   for (int i = 0; i < 4; ++i) a[i].v = lds16(ip + lane * 64 + 16 * i);
   f4 S = {0, 0, 0, 0};
 #pragma unroll
-  for (int i = 0; i < 4; ++i) S = mfma32(a[i].h, qchunk(qs, lane, i), S);
+  for (int i = 0; i < 4; ++i) S = mfma32(a[i].h, qchunk<PACK>(qs, lane, i), S);
   const bool full = tvalid == 0xFFFFu;
   const uint32_t mine = (tvalid >> (4 * kg)) & 0xFu;
   half4 P4;
@@ -490,12 +505,14 @@ struct IntBlock {
   f4 acc[8], pb;       // block-local P.V on codes and sum of P
 };
 
-template <int BITS>
+// PACK: lanes of columns 0..7 keep the high term of q * s of their head in qh,
+// lanes of columns 8..15 the low term (ql is unused); one MFMA chain then holds both.
+template <int BITS, bool PACK>
 __device__ __forceinline__ void int_header(IntBlock &ib, const uint8_t *qs, const uint8_t *ip, int lane) {
   const int kg = lane >> 4;
   half8 qB[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) qB[i] = qchunk(qs, lane, i);
+  for (int i = 0; i < 4; ++i) qB[i] = qchunk<PACK>(qs, lane, i);
   U8 sK[4], zK[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -511,15 +528,32 @@ __device__ __forceinline__ void int_header(IntBlock &ib, const uint8_t *qs, cons
       ib.ql[i][e] = (_Float16)__builtin_fmaf((float)qB[i][e], (float)sK[i].h[e], -(float)ib.qh[i][e]);
   }
   f4 c0 = {0, 0, 0, 0};
+  if (PACK) {
+    const bool lo = (lane & 8) != 0;
+    const half8 zero8 = half8{0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
-  for (int i = 0; i < 4; ++i) c0 = mfma32(zK[i].h, qB[i], c0);
+    for (int i = 0; i < 4; ++i) {
+      ib.qh[i] = lo ? ib.ql[i] : ib.qh[i];
+      c0 = mfma32(zK[i].h, lo ? zero8 : qB[i], c0);  // the zero-point term once per head
+    }
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    U8 o;
+    for (int i = 0; i < 4; ++i) {
+      U8 o;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) o.u[e] = opaque(neg_off_pair<BITS>(4 * i + e));
-    c0 = mfma32(o.h, ib.qh[i], c0);
-    c0 = mfma32(o.h, ib.ql[i], c0);
+      for (int e = 0; e < 4; ++e) o.u[e] = opaque(neg_off_pair<BITS>(4 * i + e));
+      c0 = mfma32(o.h, ib.qh[i], c0);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) c0 = mfma32(zK[i].h, qB[i], c0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      U8 o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o.u[e] = opaque(neg_off_pair<BITS>(4 * i + e));
+      c0 = mfma32(o.h, ib.qh[i], c0);
+      c0 = mfma32(o.h, ib.ql[i], c0);
+    }
   }
   ib.c0 = c0;
 #pragma unroll
@@ -528,7 +562,7 @@ __device__ __forceinline__ void int_header(IntBlock &ib, const uint8_t *qs, cons
 }
 
 // One 16-token tile of an int block: key codes at kt, value codes at vt (LDS).
-template <int BITS>
+template <int BITS, bool PACK>
 __device__ __forceinline__ void int_tile(const AttnParams &p, State &st, IntBlock &ib, const uint8_t *kt,
                                          const uint8_t *vt, uint32_t tvalid, int lane) {
   constexpr int NW = Unpack<BITS>::kWords;
@@ -563,17 +597,28 @@ __device__ __forceinline__ void int_tile(const AttnParams &p, State &st, IntBloc
     const uint2 a = *(const uint2 *)vc;
     vw[0] = a.x; vw[1] = a.y;
   }
-  // two independent MFMA chains (q*s high and low terms)
-  f4 S = ib.c0, S2 = {0, 0, 0, 0};
+  f4 S = ib.c0;
+  if (PACK) {  // one chain: high terms in columns 0..7, low terms in 8..15
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    U8 a;
+    for (int i = 0; i < 4; ++i) {
+      U8 a;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) a.u[e] = Unpack<BITS>::pair(kw, 4 * i + e, mg);
-    S = mfma32(a.h, ib.qh[i], S);
-    S2 = mfma32(a.h, ib.ql[i], S2);
+      for (int e = 0; e < 4; ++e) a.u[e] = Unpack<BITS>::pair(kw, 4 * i + e, mg);
+      S = mfma32(a.h, ib.qh[i], S);
+    }
+    S = add_row_half(S);
+  } else {  // two independent chains (q*s high and low terms)
+    f4 S2 = {0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      U8 a;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) a.u[e] = Unpack<BITS>::pair(kw, 4 * i + e, mg);
+      S = mfma32(a.h, ib.qh[i], S);
+      S2 = mfma32(a.h, ib.ql[i], S2);
+    }
+    S += S2;
   }
-  S += S2;
   const bool full = tvalid == 0xFFFFu;
   const uint32_t mine = (tvalid >> (4 * kg)) & 0xFu;
   half4 P4;
@@ -618,6 +663,7 @@ __device__ __forceinline__ void int_epilogue(State &st, IntBlock &ib, const uint
 }
 
 // Centroid block: one item with both records.
+template <bool PACK>
 __device__ __forceinline__ void centroid_item(const AttnParams &p, State &st, const uint8_t *qs, const uint8_t *ip,
                                               uint64_t valid, int lane) {
   const int kg = lane >> 4, m16 = lane & 15;
@@ -627,7 +673,7 @@ __device__ __forceinline__ void centroid_item(const AttnParams &p, State &st, co
   for (int i = 0; i < 4; ++i) {
     U8 a;
     a.v = lds16(ip + ((m16 & 3) * D + 8 * kg + 32 * i) * 2);
-    sc = mfma32(a.h, qchunk(qs, lane, i), sc);
+    sc = mfma32(a.h, qchunk<PACK>(qs, lane, i), sc);
   }
   const uint32_t *kid = (const uint32_t *)(ip + KC * D * 2);
   const uint32_t *vid = (const uint32_t *)(ip + kCentBytes + KC * D * 2);
@@ -677,24 +723,25 @@ __device__ __forceinline__ void centroid_item(const AttnParams &p, State &st, co
 
 // Runs: process items of one level until the next item has another level (left in
 // `it`, already popped) or the sequence ends (returns false).
+template <bool PACK>
 __device__ __forceinline__ bool exact_run(const AttnParams &p, State &st, const uint8_t *qs, Pipe &pp,
                                           Item &it, uint64_t &valid, const uint8_t *&ip, int lane) {
   do {
-    exact_tile(p, st, qs, ip, it.tvalid(), lane);
+    exact_tile<PACK>(p, st, qs, ip, it.tvalid(), lane);
     pp.release(it);
     if (!pp.pop(it, valid, ip)) return false;
   } while (it.lv() == GKV_EXACT);
   return true;
 }
 
-template <int BITS>
+template <int BITS, bool PACK>
 __device__ __forceinline__ bool int_run(const AttnParams &p, State &st, const uint8_t *qs, Pipe &pp,
                                         Item &it, uint64_t &valid, const uint8_t *&ip, int lane) {
   IntBlock ib;
   do {
     const uint8_t *kq = ip;
     if (it.first()) {
-      int_header<BITS>(ib, qs, kq, lane);
+      int_header<BITS, PACK>(ib, qs, kq, lane);
       kq += kSZBytes;
     }
     const int n = it.ntiles();
@@ -704,7 +751,7 @@ __device__ __forceinline__ bool int_run(const AttnParams &p, State &st, const ui
     for (int j = 0; j < n; ++j) {
       const int t = __builtin_ctz(tl);
       tl &= tl - 1;
-      int_tile<BITS>(p, st, ib, kq + j * 256 * BITS, vq + j * 256 * BITS, (uint32_t)(valid >> (16 * t)) & 0xFFFFu,
+      int_tile<BITS, PACK>(p, st, ib, kq + j * 256 * BITS, vq + j * 256 * BITS, (uint32_t)(valid >> (16 * t)) & 0xFFFFu,
                      lane);
     }
     if (it.last()) int_epilogue<BITS>(st, ib, vq + n * 256 * BITS, lane);
@@ -714,17 +761,19 @@ __device__ __forceinline__ bool int_run(const AttnParams &p, State &st, const ui
   return true;
 }
 
+template <bool PACK>
 __device__ __forceinline__ bool centroid_run(const AttnParams &p, State &st, const uint8_t *qs, Pipe &pp,
                                              Item &it, uint64_t &valid, const uint8_t *&ip,
                                              int lane) {
   do {
-    centroid_item(p, st, qs, ip, valid, lane);
+    centroid_item<PACK>(p, st, qs, ip, valid, lane);
     pp.release(it);
     if (!pp.pop(it, valid, ip)) return false;
   } while (it.lv() == GKV_CENTROID);
   return true;
 }
 
+template <bool PACK>
 __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   extern __shared__ __align__(16) uint8_t smem[];
   const int sidx = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
@@ -776,11 +825,11 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   bool more = pp.pop(it, valid, ip);
   while (more) {
     switch (it.lv()) {
-      case GKV_EXACT: more = exact_run(p, st, qs, pp, it, valid, ip, lane); break;
-      case GKV_INT8: more = int_run<8>(p, st, qs, pp, it, valid, ip, lane); break;
-      case GKV_INT4: more = int_run<4>(p, st, qs, pp, it, valid, ip, lane); break;
-      case GKV_INT2: more = int_run<2>(p, st, qs, pp, it, valid, ip, lane); break;
-      default: more = centroid_run(p, st, qs, pp, it, valid, ip, lane); break;
+      case GKV_EXACT: more = exact_run<PACK>(p, st, qs, pp, it, valid, ip, lane); break;
+      case GKV_INT8: more = int_run<8, PACK>(p, st, qs, pp, it, valid, ip, lane); break;
+      case GKV_INT4: more = int_run<4, PACK>(p, st, qs, pp, it, valid, ip, lane); break;
+      case GKV_INT2: more = int_run<2, PACK>(p, st, qs, pp, it, valid, ip, lane); break;
+      default: more = centroid_run<PACK>(p, st, qs, pp, it, valid, ip, lane); break;
     }
   }
   vm_wait<0>();
@@ -1267,7 +1316,10 @@ static void launch_plan(const AttnParams &p, const gkv_cache *c, hipStream_t s) 
 }
 static void launch_partials(const AttnParams &p, const gkv_cache *c, hipStream_t s) {
   const size_t lds = (size_t)kWaves * kWaveLds + 16 * kQRow;  // rings also hold the merge buffers
-  hipLaunchKernelGGL(attn_kernel, dim3(p.nsplit, c->Hkv, c->B), dim3(kThreads), lds, s, p);
+  if (p.G <= 8)
+    hipLaunchKernelGGL(attn_kernel<true>, dim3(p.nsplit, c->Hkv, c->B), dim3(kThreads), lds, s, p);
+  else
+    hipLaunchKernelGGL(attn_kernel<false>, dim3(p.nsplit, c->Hkv, c->B), dim3(kThreads), lds, s, p);
 }
 static void launch_merge(const AttnParams &p, const gkv_cache *c, float *out, hipStream_t s) {
   hipLaunchKernelGGL(merge_kernel, dim3(p.G, c->Hkv * c->B), dim3(D), 0, s, (const float *)p.part, out, p.nsplit,
