@@ -11,15 +11,16 @@
 // workgroup are merged in LDS into one partial (m, l, o) per head, and a merge
 // kernel combines the partials of each (b, KV head).
 //
-// Memory pipeline: a visit is a sequence of "items" (an int block's key
-// scale/zero, a 16-token K+V tile, a centroid block).  A producer cursor walks the
-// wavefront's visits and copies items ahead into a private LDS ring with
-// asynchronous global -> LDS loads (global_load_lds_dwordx4: every lane moves 16 B,
-// so one instruction moves 1 KB); the visit descriptors arrive the same way, one
-// 1 KB chunk (32 visits) ahead.  Issued items go through a small LDS queue to the
-// consumer, which waits on the load counter for its item and computes from LDS.
-// The copies are issued from inline assembly so that the compiler does not add a
-// full load-counter wait in front of every LDS read; the waits are explicit, and
+// Memory pipeline: the plan kernel turns every visit into compute "items" (an
+// exact 16-token tile, a group of int tiles, a centroid block) and copy "units": a
+// unit fills one 4 KB slot of a wavefront's LDS ring with exactly four asynchronous
+// global -> LDS loads (global_load_lds_dwordx4: every lane moves 16 B, so one
+// instruction moves up to 1 KB).  The producer keeps every free slot filled; since
+// every unit is four instructions and the producer's lead is fixed by the slots the
+// consumer holds, the wait for a unit is a constant load count at each place the
+// consumer pops one.  The descriptors arrive the same way, in 512-byte chunks
+// copied half a chunk ahead.  The copies are issued from inline assembly so that
+// the compiler does not add a full load-counter wait in front of every LDS read;
 // no other vector-memory instruction runs inside the loop (the load counter
 // retires in order, so any would wait for every copy in flight).
 //
@@ -89,12 +90,13 @@ __device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel)
 // ---------------------------------------------------------------- code unpacking
 // fp16 magic exponents: code bits at mantissa [p, p+b) of exponent e give 2^(10-p) + c.
 constexpr uint32_t M1024 = 0x64646464u;  // byte-wise exponent for perm (1024 + byte)
-constexpr uint32_t E64 = 0x54005400u, E16 = 0x4C004C00u, E4 = 0x44004400u;
+constexpr uint32_t E1024 = 0x64006400u, E256 = 0x5C005C00u, E64 = 0x54005400u, E16 = 0x4C004C00u,
+                   E4 = 0x44004400u;
 
 // The fp16 exponent words sit in registers (see Mag) so that each pair is one
 // v_and_or_b32: that instruction cannot take two literal constants.
 struct Mag {
-  uint32_t e64, e16, e4;
+  uint32_t e1024, e256, e64, e16, e4;
 };
 
 template <int BITS>
@@ -106,10 +108,23 @@ struct Unpack<8> {
   __device__ static uint32_t pair(const uint32_t *w, int q, const Mag &) {  // codes 2q, 2q+1
     return perm(M1024, w[q >> 1], (q & 1) ? 0x04030402u : 0x04010400u);
   }
+  __device__ static uint32_t kpair(const uint32_t *w, int q, const Mag &mg) { return pair(w, q, mg); }
 };
 template <>
 struct Unpack<4> {
   static constexpr int kWords = 4;
+  // Keys: nibbles 1, 5 | 3, 7 at 64 + c, nibbles 0, 4 | 2, 6 at 1024 + c (one shift
+  // per word; the offsets fold into the per-block constant).
+  __device__ static uint32_t kpair(const uint32_t *w, int q, const Mag &mg) {
+    const uint32_t x = w[q >> 2];
+    switch (q & 3) {
+      case 0: return andor(x, 0x00F000F0u, mg.e64);
+      case 1: return andor(x >> 8, 0x00F000F0u, mg.e64);
+      case 2: return andor(x, 0x000F000Fu, mg.e1024);
+      default: return andor(x >> 8, 0x000F000Fu, mg.e1024);
+    }
+  }
+  // Values: small offsets (64 and 16), which the block epilogue subtracts in fp32.
   __device__ static uint32_t pair(const uint32_t *w, int q, const Mag &mg) {
     const uint32_t x = w[q >> 2];
     switch (q & 3) {
@@ -123,6 +138,22 @@ struct Unpack<4> {
 template <>
 struct Unpack<2> {
   static constexpr int kWords = 2;
+  // Keys: every position keeps its own offset (they are folded into the per-block
+  // constant), so only the high six bits need a shift.
+  __device__ static uint32_t kpair(const uint32_t *w, int q, const Mag &mg) {
+    const uint32_t x = w[q >> 3];
+    switch (q & 7) {
+      case 0: return andor(x, 0x03000300u, mg.e4);
+      case 1: return andor(x >> 6, 0x03000300u, mg.e4);
+      case 2: return andor(x, 0x00C000C0u, mg.e16);
+      case 3: return andor(x >> 6, 0x00C000C0u, mg.e16);
+      case 4: return andor(x, 0x00300030u, mg.e64);
+      case 5: return andor(x >> 6, 0x00300030u, mg.e64);
+      case 6: return andor(x, 0x00030003u, mg.e1024);
+      default: return andor(x, 0x000C000Cu, mg.e256);
+    }
+  }
+  // Values: the two pairs of one MFMA share an offset.
   __device__ static uint32_t pair(const uint32_t *w, int q, const Mag &mg) {
     const uint32_t x = w[q >> 3];
     switch (q & 7) {
@@ -147,12 +178,14 @@ __device__ __forceinline__ uint32_t opaque(uint32_t c) {
 }
 
 // Offset (as fp16 pair, negated) of code pair q.
+// Offset (as fp16 pair, negated) of key code pair q.
 template <int BITS>
 __device__ __forceinline__ uint32_t neg_off_pair(int q) {
   if (BITS == 8) return 0xE400E400u;  // -1024
-  if (BITS == 4) return (q & 3) < 2 ? 0xD400D400u : 0xCC00CC00u;  // -64 / -16
+  if (BITS == 4) return (q & 3) < 2 ? 0xD400D400u : 0xE400E400u;  // -64 / -1024
   const int r = q & 7;
-  return (r < 2 || r >= 6) ? 0xC400C400u : (r < 4 ? 0xCC00CC00u : 0xD400D400u);  // -4 / -16 / -64
+  if (r < 6) return r < 2 ? 0xC400C400u : (r < 4 ? 0xCC00CC00u : 0xD400D400u);  // -4 / -16 / -64
+  return r == 6 ? 0xE400E400u : 0xDC00DC00u;  // -1024 / -256
 }
 // Value offset of the codes of value MFMA j (uniform per j by construction).
 template <int BITS>
@@ -174,17 +207,22 @@ struct AttnParams {
   const int32_t *pages;
   uint8_t *visits;  // visit descriptors (plan kernel scratch), vcap per (b, KV head)
   uint8_t *plan;    // item descriptors, icap per (b, KV head)
-  int32_t *split;   // first item of each wavefront, W + 1 per (b, KV head)
+  uint8_t *units;   // unit descriptors, ucap per (b, KV head)
+  int32_t *split;   // first item and first unit of each wavefront, 2 (W + 1) per (b, KV head)
   float *part;
   int64_t T;
   int nblk_cap, Hkv, G, nres, nrb_cap, topk, nsplit;
-  int64_t vcap, icap;
+  int64_t vcap, icap, ucap;
   float sl2;  // log2(e) / sqrt(D)
 };
 
-constexpr int kRing = 16384;    // staging ring per wavefront (bytes, a power of two)
-constexpr int kDescBytes = 2048;  // item-descriptor ring: two 1 KB chunks
-constexpr int kWaveLds = kRing + kDescBytes;  // LDS per wavefront
+constexpr int kSlotBytes = 4096;  // one copy unit
+constexpr int kSlots = 4;         // ring slots per wavefront
+constexpr int kRing = kSlots * kSlotBytes;
+constexpr int kChunk = 32;        // descriptors per 512-byte chunk
+// per wavefront: ring | unit-descriptor chunks (2 x 512) | item-descriptor chunks
+// (2 x 512) | value scale/zero of the current int block (512)
+constexpr int kWaveLds = kRing + 4 * 512 + 512;
 constexpr int kMaxWaves = 1024;   // wavefronts per (b, KV head)
 
 
@@ -194,6 +232,19 @@ constexpr int kMaxWaves = 1024;   // wavefronts per (b, KV head)
 __device__ __forceinline__ void dma16(const void *g, uint32_t lds_wave_base) {
   const uint32_t m0v = __builtin_amdgcn_readfirstlane(lds_wave_base);
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(m0v) : "memory", "m0");
+}
+// Four 1 KB copies into one ring slot with one M0: a -> slot [0, 2K), b -> slot [2K, 4K)
+// (the instruction offset moves the global and the LDS address together).
+__device__ __forceinline__ void dma4(const uint8_t *a, const uint8_t *b, uint32_t slot) {
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane(slot);
+  asm volatile(
+      "s_mov_b32 m0, %2\n\t"
+      "global_load_lds_dwordx4 %0, off\n\t"
+      "global_load_lds_dwordx4 %0, off offset:1024\n\t"
+      "global_load_lds_dwordx4 %1, off offset:2048\n\t"
+      "global_load_lds_dwordx4 %1, off offset:3072" ::"v"(a),
+      "v"(b - 2048), "s"(m0v)
+      : "memory", "m0");
 }
 template <int N>
 __device__ __forceinline__ void vm_wait() {
@@ -224,155 +275,145 @@ __device__ __forceinline__ int64_t uni64(int64_t x) {
   return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
-// ---------------------------------------------------------------- item sequence
-// An item is one unit of the pipeline: a contiguous span of the ring filled by up
-// to four copy segments, and one step of the consumer.
-//   exact tile:   [K tile 4 KB][V tile 4 KB]
-//   int group:    [K scale/zero if first][K codes of n tiles][V codes of n tiles]
-//                 [V scale/zero if last]   (n consecutive read tiles of one block)
-//   centroid:     [K record][V record]
-// The plan kernel expands every visit into its items and writes one 32-byte
-// descriptor per item; the attention kernel only follows the list.
+// ---------------------------------------------------------------- items and units
+// Items, in the order the consumer computes them, and the copy units they read:
+//   exact tile:   unit [K tile 4 KB], unit [V tile 4 KB]
+//   int group:    (first of a block: unit [K scale/zero | V scale/zero]), unit
+//                 [K codes of n tiles | V codes of n tiles]  (n consecutive read
+//                 tiles of one block, at most 2 KB of codes per record)
+//   centroid:     unit [K record | V record]
 enum ItemKind { kExactTile = 0, kIntGroup = 1, kCentroid = 2 };
 
 // Item descriptor.  meta: kind (2 bits) | level (5) | first (1) | last (1) | tile
-// mask (4) | tile count (3) | exact tile's valid-token bits (16).  geo: size in
-// 16-byte units (10 bits) | load instructions (6) | 16-byte units per code segment (10).
+// mask (4) | tile count (3) | exact tile's valid-token bits (16).
 struct ItemDesc {
-  uint64_t kp, vp;  // K and V record addresses
-  uint64_t valid;   // tokens of the block that are read
-  uint32_t meta, geo;
+  uint32_t meta, pad;
+  uint64_t valid;  // tokens of the block that are read
 };
-static_assert(sizeof(ItemDesc) == 32, "descriptor size");
-constexpr int kDescChunk = 1024 / sizeof(ItemDesc);  // descriptors per copy (one 1 KB copy)
-constexpr uint32_t kMaxAhead = kDescChunk / 2;          // producer lead over the consumer, in items
+static_assert(sizeof(ItemDesc) == 16, "descriptor size");
 
-struct Item {  // the consumer's view of an item
-  uint32_t lin, end;  // linear ring positions of the item and after it
-  uint32_t meta;
-  __device__ int kind() const { return meta & 3u; }
-  __device__ int lv() const { return (meta >> 2) & 31u; }
-  __device__ bool first() const { return (meta >> 7) & 1u; }
-  __device__ bool last() const { return (meta >> 8) & 1u; }
-  __device__ uint32_t tiles() const { return (meta >> 9) & 15u; }
-  __device__ int ntiles() const { return (meta >> 13) & 7u; }
-  __device__ uint32_t tvalid() const { return meta >> 16; }
+// Copy unit: part A (slot bytes [0, 2K)) from address a, part B ([2K, 4K)) from b.
+// In each part the first load moves n0 16-byte lanes from the part's address and
+// the second n1 lanes from the address + 1 KB; n1 = 0 stands for one lane that
+// re-reads the part's first 16 bytes, so that every unit is four loads.
+struct UnitDesc {
+  uint64_t a;  // address (bits 0..47) | n0 (bits 48..55) | n1 (bits 56..63)
+  uint64_t b;  // address
 };
+static_assert(sizeof(UnitDesc) == 16, "descriptor size");
 
-__device__ __forceinline__ uint32_t geo_size(uint32_t g) { return (g & 1023u) * 16u; }
-__device__ __forceinline__ uint32_t geo_ninstr(uint32_t g) { return (g >> 10) & 63u; }
-__device__ __forceinline__ uint32_t geo_units(uint32_t g) { return g >> 16; }
+__device__ __forceinline__ int meta_kind(uint32_t m) { return m & 3u; }
+__device__ __forceinline__ int meta_lv(uint32_t m) { return (m >> 2) & 31u; }
+__device__ __forceinline__ bool meta_first(uint32_t m) { return (m >> 7) & 1u; }
+__device__ __forceinline__ bool meta_last(uint32_t m) { return (m >> 8) & 1u; }
+__device__ __forceinline__ uint32_t meta_tiles(uint32_t m) { return (m >> 9) & 15u; }
+__device__ __forceinline__ int meta_ntiles(uint32_t m) { return (m >> 13) & 7u; }
+__device__ __forceinline__ uint32_t meta_tvalid(uint32_t m) { return m >> 16; }
 
-// Consecutive read tiles per int item: about 4 KB of codes (K + V).
+// Consecutive read tiles per int item: 2 KB of codes per record.
 __device__ __forceinline__ int group_tiles(int lv) { return lv == 2 ? 4 : (lv == 4 ? 2 : 1); }
 
-// Copy `units` 16-byte units from `src` to LDS address `dst` (1 KB per instruction;
-// only a last partial instruction is lane-predicated).
-__device__ __forceinline__ void copy_segment(const uint8_t *src, uint32_t units, uint32_t dst, int lane) {
-  const uint8_t *s = src + 16 * lane;
-  const uint32_t full = units >> 6;
-#pragma unroll 1
-  for (uint32_t i = 0; i < full; ++i) dma16(s + 1024 * i, dst + 1024 * i);
-  if (units & 63u) {
-    if ((uint32_t)lane < (units & 63u)) dma16(s + 1024 * full, dst + 1024 * full);
+// Issues the four loads of a unit into the slot at LDS address `slot`.
+__device__ __forceinline__ void issue_unit(uint64_t a, uint64_t b, uint32_t slot, int lane) {
+  const uint32_t n0 = (uint32_t)(a >> 48) & 255u, n1 = (uint32_t)(a >> 56);
+  const uint8_t *pa = (const uint8_t *)(uintptr_t)(a & 0xFFFFFFFFFFFFull) + 16 * lane;
+  const uint8_t *pb = (const uint8_t *)(uintptr_t)b + 16 * lane;
+  if (n0 == 64 && n1 == 64) {
+    dma4(pa, pb, slot);
+    return;
+  }
+  if ((uint32_t)lane < n0) {
+    dma16(pa, slot);
+    dma16(pb, slot + 2048);
+  }
+  const uint32_t m1 = n1 ? n1 : 1u, o1 = n1 ? 1024u : 0u;
+  if ((uint32_t)lane < m1) {
+    dma16(pa + o1, slot + 1024);
+    dma16(pb + o1, slot + 3072);
   }
 }
 
 // ---------------------------------------------------------------- pipeline
-// One wavefront's pipeline over its item list.  The producer copies items ahead
-// into the LDS ring; the consumer pops them in order.  Both read the item
-// descriptors from a two-slot LDS ring of 32-descriptor chunks, and both derive
-// the same sequence of ring positions and load counts from the descriptors, so
-// nothing else passes between them.  The producer copies chunk c + 1 just before
-// item 32c + 16 and stays at most kMaxAhead items ahead of the consumer, so the
-// slot it overwrites (chunk c - 1) is no longer read.
+// One wavefront's pipeline over its units and items.  The producer issues unit k
+// into slot k % kSlots as soon as the consumer has released unit k - kSlots; the
+// consumer pops the units of each item in order.  When the consumer pops unit k
+// while holding H units, every unit up to min(n, released + kSlots) has been
+// issued, so at least 4 (kSlots - 1 - H) loads follow unit k's unless the list ends
+// first (then it waits for all).  Descriptor chunk c + 1 is copied when the cursor
+// of its list reaches 32 c + 16 and waited for when it reaches 32 (c + 1).
 struct Pipe {
-  const uint8_t *ring;   // staging ring (LDS)
-  const uint8_t *dring;  // descriptor ring (LDS, 2 x 1 KB)
-  const uint8_t *dsrc;   // this wavefront's descriptors (global)
-  uint32_t ring_base, dlds;  // LDS addresses of the two rings (wave-uniform)
-  uint32_t nitems;
+  const uint8_t *ring;           // ring (LDS)
+  const uint8_t *uchunk, *ichunk;  // descriptor chunks (LDS, 2 x 512 B each)
+  const uint8_t *usrc, *isrc;    // this wavefront's unit and item descriptors (global)
+  uint32_t ring_base, ulds, ilds;  // LDS addresses (wave-uniform)
+  uint32_t nunits, nitems;
   uint32_t issued;  // load instructions issued
-  // producer
-  uint32_t pk, plin, pchunk;  // next item, its ring position, load count through the last chunk copy
-  bool pend;                  // descriptor of item pk already read
-  uint64_t pkp, pvp;
-  uint32_t pmeta, pgeo;
-  // consumer
-  uint32_t ck, clin, ccnt, hold;
+  uint32_t pk;      // units issued
+  uint32_t ufetch;  // load count through the last unit-chunk copy
+  uint32_t ck, rel; // units popped, released
+  uint32_t ik;      // items read
+  uint32_t ifetch;  // load count through the last item-chunk copy
+  uint8_t *ebuf;    // value scale/zero of the current int block (LDS, 512 B)
   int lane;
 
-  __device__ __forceinline__ void fetch_chunk(uint32_t c) {
-    dma16(dsrc + (size_t)c * 1024 + 16 * lane, dlds + (c & 1) * 1024);
-    pchunk = ++issued;
+  __device__ __forceinline__ void fetch(const uint8_t *src, uint32_t lds, uint32_t c) {
+    if (lane < 32) dma16(src + (size_t)c * 512 + 16 * lane, lds + (c & 1) * 512);
   }
-  __device__ __forceinline__ const uint8_t *desc(uint32_t k) const {
-    return dring + ((k / kDescChunk) & 1) * 1024 + (k % kDescChunk) * sizeof(ItemDesc);
+  __device__ __forceinline__ void start(int ln) {
+    lane = ln;
+    issued = pk = ck = rel = ik = 0;
+    ufetch = ifetch = 0;
+    if (nunits) {
+      fetch(usrc, ulds, 0);
+      ufetch = ++issued;
+    }
+    if (nitems) {
+      fetch(isrc, ilds, 0);
+      ifetch = ++issued;
+    }
+    vm_wait<0>();
   }
-  __device__ __forceinline__ bool chunk_copy_before(uint32_t k) const {  // a chunk copy precedes item k
-    return k % kDescChunk == kDescChunk / 2 && (k / kDescChunk + 1) * kDescChunk < nitems;
-  }
-  __device__ __forceinline__ static uint32_t place(uint32_t lin, uint32_t size) {  // no wrap inside an item
-    const uint32_t off = lin & (kRing - 1);
-    return off + size > kRing ? lin + (kRing - off) : lin;
-  }
-
   __device__ __forceinline__ void pump() {
-    while (pk < nitems && pk - ck < kMaxAhead) {
-      if (!pend) {
-        if (pk % kDescChunk == 0) wait_loads(issued - pchunk);  // chunk pk / 32 has landed
-        const uint8_t *e = desc(pk);
-        const uint4 d0 = *(const uint4 *)e, d1 = *(const uint4 *)(e + 16);
-        pkp = (uint64_t)uni64((int64_t)(((uint64_t)d0.y << 32) | d0.x));
-        pvp = (uint64_t)uni64((int64_t)(((uint64_t)d0.w << 32) | d0.z));
-        pmeta = uni((int32_t)d1.z);
-        pgeo = uni((int32_t)d1.w);
-        pend = true;
+    while (pk < nunits && pk < rel + kSlots) {
+      const uint32_t r = pk % kChunk;
+      if (r == 0 && pk) wait_loads(issued - ufetch);  // chunk pk / 32 has landed
+      if (r == kChunk / 2 && (pk / kChunk + 1) * kChunk < nunits) {
+        fetch(usrc, ulds, pk / kChunk + 1);
+        ufetch = ++issued;
       }
-      const uint32_t size = geo_size(pgeo), lin = place(plin, size);
-      if (lin + size - hold > (uint32_t)kRing) break;  // ring full
-      if (chunk_copy_before(pk)) fetch_chunk(pk / kDescChunk + 1);
-      // the copy segments of the item
-      const uint8_t *kp = (const uint8_t *)(uintptr_t)pkp, *vp = (const uint8_t *)(uintptr_t)pvp;
-      const int kind = pmeta & 3u, lv = (pmeta >> 2) & 31u;
-      const uint32_t t0 = __builtin_ctz((pmeta >> 9) & 15u), un = geo_units(pgeo);
-      const uint32_t koff = kind == kIntGroup ? kSZBytes + t0 * 256 * lv : (kind == kExactTile ? t0 * 4096 : 0);
-      uint32_t dst = ring_base + (lin & (kRing - 1));
-      if (kind == kIntGroup && ((pmeta >> 7) & 1u)) {
-        copy_segment(kp, kSZBytes / 16, dst, lane);
-        dst += kSZBytes;
-      }
-      copy_segment(kp + koff, un, dst, lane);
-      dst += 16 * un;
-      copy_segment(vp + koff, un, dst, lane);
-      dst += 16 * un;
-      if (kind == kIntGroup && ((pmeta >> 8) & 1u)) copy_segment(vp, kSZBytes / 16, dst, lane);
-      issued += geo_ninstr(pgeo);
-      plin = lin + size;
+      const uint4 d = *(const uint4 *)(uchunk + ((pk / kChunk) & 1) * 512 + r * sizeof(UnitDesc));
+      const uint64_t a = (uint64_t)uni64((int64_t)(((uint64_t)d.y << 32) | d.x));
+      const uint64_t b = (uint64_t)uni64((int64_t)(((uint64_t)d.w << 32) | d.z));
+      issue_unit(a, b, ring_base + (pk % kSlots) * kSlotBytes, lane);
+      issued += 4;
       ++pk;
-      pend = false;
     }
   }
-  // Pop the next item (false when the list is exhausted), wait for its copies.
-  __device__ __forceinline__ bool pop(Item &it, uint64_t &valid, const uint8_t *&ip) {
-    pump();
-    if (ck == nitems) return false;
-    const uint8_t *e = desc(ck);
-    const uint4 d1 = *(const uint4 *)(e + 16);
-    valid = (uint64_t)uni64((int64_t)(((uint64_t)d1.y << 32) | d1.x));
-    it.meta = uni((int32_t)d1.z);
-    const uint32_t geo = uni((int32_t)d1.w), size = geo_size(geo);
-    it.lin = place(clin, size);
-    it.end = it.lin + size;
-    clin = it.end;
-    if (chunk_copy_before(ck)) ++ccnt;
-    ccnt += geo_ninstr(geo);
-    ++ck;
-    wait_loads(issued - ccnt);
-    ip = ring + (it.lin & (kRing - 1));
+  // The next item's descriptor (false when the wavefront's items are done).
+  __device__ __forceinline__ bool next_item(uint32_t &meta, uint64_t &valid) {
+    if (ik == nitems) return false;
+    const uint32_t r = ik % kChunk;
+    if (r == 0 && ik) wait_loads(issued - ifetch);
+    if (r == kChunk / 2 && (ik / kChunk + 1) * kChunk < nitems) {
+      fetch(isrc, ilds, ik / kChunk + 1);
+      ifetch = ++issued;
+    }
+    const uint4 d = *(const uint4 *)(ichunk + ((ik / kChunk) & 1) * 512 + r * sizeof(ItemDesc));
+    meta = (uint32_t)uni((int32_t)d.x);
+    valid = (uint64_t)uni64((int64_t)(((uint64_t)d.w << 32) | d.z));
+    ++ik;
     return true;
   }
-  __device__ __forceinline__ void release(const Item &it) { hold = it.end; }
+  // Pop the next unit while holding H units; returns its slot once it has landed.
+  template <int H>
+  __device__ __forceinline__ const uint8_t *pop() {
+    pump();
+    const uint32_t k = ck++;
+    if (k + kSlots - H > nunits) vm_wait<0>();
+    else vm_wait<4 * (kSlots - 1 - H)>();
+    return ring + (k % kSlots) * kSlotBytes;
+  }
+  __device__ __forceinline__ void release(uint32_t n) { rel += n; }
 };
 
 // ---------------------------------------------------------------- per-wave state
@@ -421,9 +462,11 @@ __device__ __forceinline__ bool tile_softmax(const AttnParams &p, State &st, f4 
                                              half4 &P4, float &alpha) {
   float x[4];
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    x[r] = fmaf(S[r], p.sl2, -st.m);
-    if (!full && !(mine & (1u << r))) x[r] = kNegInf;
+  for (int r = 0; r < 4; ++r) x[r] = fmaf(S[r], p.sl2, -st.m);
+  if (!full) {  // tokens that are not read (a uniform branch: most tiles are full)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (!(mine & (1u << r))) x[r] = kNegInf;
   }
   const bool big = vmax(vmax(x[0], x[1]), vmax(x[2], x[3])) > kRescale;
   const bool resc = __any(big);
@@ -475,12 +518,13 @@ constexpr half4 kOnes = half4{(_Float16)1, (_Float16)1, (_Float16)1, (_Float16)1
 // ---------------------------------------------------------------- items
 // Exact block tile: 16 tokens of fp16 K and V.
 template <bool PACK>
-__device__ __forceinline__ void exact_tile(const AttnParams &p, State &st, const uint8_t *qs, const uint8_t *ip,
+__device__ __forceinline__ void exact_tile(const AttnParams &p, State &st, const uint8_t *qs, Pipe &pp,
                                            uint32_t tvalid, int lane) {
   const int kg = lane >> 4;
+  const uint8_t *kt = pp.template pop<0>();
   U8 a[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) a[i].v = lds16(ip + lane * 64 + 16 * i);
+  for (int i = 0; i < 4; ++i) a[i].v = lds16(kt + lane * 64 + 16 * i);
   f4 S = {0, 0, 0, 0};
 #pragma unroll
   for (int i = 0; i < 4; ++i) S = mfma32(a[i].h, qchunk<PACK>(qs, lane, i), S);
@@ -490,12 +534,14 @@ __device__ __forceinline__ void exact_tile(const AttnParams &p, State &st, const
   float alpha;
   tile_softmax(p, st, S, full, mine, P4, alpha);
   const f4 pb = mfma16(kOnes, P4, f4{0, 0, 0, 0});
+  const uint8_t *vt = pp.template pop<1>();
 #pragma unroll
-  for (int i = 0; i < 4; ++i) a[i].v = lds16(ip + 4096 + lane * 64 + 16 * i);
+  for (int i = 0; i < 4; ++i) a[i].v = lds16(vt + lane * 64 + 16 * i);
 #pragma unroll
   for (int j = 0; j < 8; ++j)
     st.O[j] = mfma16(as_h4(a[j >> 1].u[2 * (j & 1)], a[j >> 1].u[2 * (j & 1) + 1]), P4, st.O[j]);
   st.l += pb[0];
+  pp.release(2);
 }
 
 // State of the scalar-code block being read.
@@ -564,17 +610,11 @@ __device__ __forceinline__ void int_header(IntBlock &ib, const uint8_t *qs, cons
 // One 16-token tile of an int block: key codes at kt, value codes at vt (LDS).
 template <int BITS, bool PACK>
 __device__ __forceinline__ void int_tile(const AttnParams &p, State &st, IntBlock &ib, const uint8_t *kt,
-                                         const uint8_t *vt, uint32_t tvalid, int lane) {
+                                         const uint8_t *vt, uint32_t tvalid, const Mag &mg, int lane) {
   constexpr int NW = Unpack<BITS>::kWords;
   const int kg = lane >> 4;
   const uint8_t *kc = kt + lane * (4 * BITS);
   const uint8_t *vc = vt + lane * (4 * BITS);
-  Mag mg;
-  if (BITS != 8) {
-    mg.e64 = opaque(E64);
-    mg.e16 = opaque(E16);
-    mg.e4 = opaque(E4);
-  }
   uint32_t kw[NW];
   if (NW >= 4) {
 #pragma unroll
@@ -603,7 +643,7 @@ __device__ __forceinline__ void int_tile(const AttnParams &p, State &st, IntBloc
     for (int i = 0; i < 4; ++i) {
       U8 a;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) a.u[e] = Unpack<BITS>::pair(kw, 4 * i + e, mg);
+      for (int e = 0; e < 4; ++e) a.u[e] = Unpack<BITS>::kpair(kw, 4 * i + e, mg);
       S = mfma32(a.h, ib.qh[i], S);
     }
     S = add_row_half(S);
@@ -613,7 +653,7 @@ __device__ __forceinline__ void int_tile(const AttnParams &p, State &st, IntBloc
     for (int i = 0; i < 4; ++i) {
       U8 a;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) a.u[e] = Unpack<BITS>::pair(kw, 4 * i + e, mg);
+      for (int e = 0; e < 4; ++e) a.u[e] = Unpack<BITS>::kpair(kw, 4 * i + e, mg);
       S = mfma32(a.h, ib.qh[i], S);
       S2 = mfma32(a.h, ib.ql[i], S2);
     }
@@ -662,7 +702,7 @@ __device__ __forceinline__ void int_epilogue(State &st, IntBlock &ib, const uint
   st.l += ib.pb[0];
 }
 
-// Centroid block: one item with both records.
+// Centroid block: one unit with both records (K at +0, V at +2 KB).
 template <bool PACK>
 __device__ __forceinline__ void centroid_item(const AttnParams &p, State &st, const uint8_t *qs, const uint8_t *ip,
                                               uint64_t valid, int lane) {
@@ -676,12 +716,12 @@ __device__ __forceinline__ void centroid_item(const AttnParams &p, State &st, co
     sc = mfma32(a.h, qchunk<PACK>(qs, lane, i), sc);
   }
   const uint32_t *kid = (const uint32_t *)(ip + KC * D * 2);
-  const uint32_t *vid = (const uint32_t *)(ip + kCentBytes + KC * D * 2);
+  const uint32_t *vid = (const uint32_t *)(ip + 2048 + KC * D * 2);
   const uint32_t ki = (kid[lane >> 4] >> (2 * (lane & 15))) & 3u;
   const uint32_t vi = (vid[lane >> 4] >> (2 * (lane & 15))) & 3u;
   U8 vc[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) vc[i].v = kg == 0 ? lds16(ip + kCentBytes + m16 * 64 + 16 * i) : make_uint4(0, 0, 0, 0);
+  for (int i = 0; i < 4; ++i) vc[i].v = kg == 0 ? lds16(ip + 2048 + m16 * 64 + 16 * i) : make_uint4(0, 0, 0, 0);
   const bool on = (valid >> lane) & 1ull;
   float cnt[4][4], used[4];
 #pragma unroll
@@ -721,55 +761,63 @@ __device__ __forceinline__ void centroid_item(const AttnParams &p, State &st, co
   st.l += lsum;
 }
 
-// Runs: process items of one level until the next item has another level (left in
-// `it`, already popped) or the sequence ends (returns false).
+// Runs: process items of one level until the next item has another level (its
+// descriptor left in meta/valid) or the items end (returns false).
 template <bool PACK>
 __device__ __forceinline__ bool exact_run(const AttnParams &p, State &st, const uint8_t *qs, Pipe &pp,
-                                          Item &it, uint64_t &valid, const uint8_t *&ip, int lane) {
+                                          uint32_t &meta, uint64_t &valid, int lane) {
   do {
-    exact_tile<PACK>(p, st, qs, ip, it.tvalid(), lane);
-    pp.release(it);
-    if (!pp.pop(it, valid, ip)) return false;
-  } while (it.lv() == GKV_EXACT);
+    exact_tile<PACK>(p, st, qs, pp, meta_tvalid(meta), lane);
+    if (!pp.next_item(meta, valid)) return false;
+  } while (meta_lv(meta) == GKV_EXACT);
   return true;
 }
 
 template <int BITS, bool PACK>
 __device__ __forceinline__ bool int_run(const AttnParams &p, State &st, const uint8_t *qs, Pipe &pp,
-                                        Item &it, uint64_t &valid, const uint8_t *&ip, int lane) {
+                                        uint32_t &meta, uint64_t &valid, int lane) {
   IntBlock ib;
+  Mag mg;  // the exponent words, once per run
+  if (BITS != 8) {
+    mg.e1024 = opaque(E1024);
+    mg.e256 = opaque(E256);
+    mg.e64 = opaque(E64);
+    mg.e16 = opaque(E16);
+    mg.e4 = opaque(E4);
+  }
   do {
-    const uint8_t *kq = ip;
-    if (it.first()) {
-      int_header<BITS, PACK>(ib, qs, kq, lane);
-      kq += kSZBytes;
+    if (meta_first(meta)) {
+      const uint8_t *sz = pp.template pop<0>();
+      int_header<BITS, PACK>(ib, qs, sz, lane);
+      *(uint2 *)(pp.ebuf + 8 * lane) = *(const uint2 *)(sz + 2048 + 8 * lane);  // V scale/zero, kept
+      pp.release(1);
     }
-    const int n = it.ntiles();
-    const uint8_t *vq = kq + n * 256 * BITS;
-    uint32_t tl = it.tiles();
+    const uint8_t *kq = pp.template pop<0>();
+    const uint8_t *vq = kq + 2048;
+    const int n = meta_ntiles(meta);
+    uint32_t tl = meta_tiles(meta);
 #pragma unroll 1
     for (int j = 0; j < n; ++j) {
       const int t = __builtin_ctz(tl);
       tl &= tl - 1;
-      int_tile<BITS, PACK>(p, st, ib, kq + j * 256 * BITS, vq + j * 256 * BITS, (uint32_t)(valid >> (16 * t)) & 0xFFFFu,
-                     lane);
+      int_tile<BITS, PACK>(p, st, ib, kq + j * 256 * BITS, vq + j * 256 * BITS,
+                           (uint32_t)(valid >> (16 * t)) & 0xFFFFu, mg, lane);
     }
-    if (it.last()) int_epilogue<BITS>(st, ib, vq + n * 256 * BITS, lane);
-    pp.release(it);
-    if (!pp.pop(it, valid, ip)) return false;
-  } while (it.lv() == BITS);
+    if (meta_last(meta)) int_epilogue<BITS>(st, ib, pp.ebuf, lane);
+    pp.release(1);
+    if (!pp.next_item(meta, valid)) return false;
+  } while (meta_lv(meta) == BITS);
   return true;
 }
 
 template <bool PACK>
 __device__ __forceinline__ bool centroid_run(const AttnParams &p, State &st, const uint8_t *qs, Pipe &pp,
-                                             Item &it, uint64_t &valid, const uint8_t *&ip,
-                                             int lane) {
+                                             uint32_t &meta, uint64_t &valid, int lane) {
   do {
-    centroid_item<PACK>(p, st, qs, ip, valid, lane);
-    pp.release(it);
-    if (!pp.pop(it, valid, ip)) return false;
-  } while (it.lv() == GKV_CENTROID);
+    centroid_item<PACK>(p, st, qs, pp.template pop<0>(), valid, lane);
+    pp.release(1);
+    if (!pp.next_item(meta, valid)) return false;
+  } while (meta_lv(meta) == GKV_CENTROID);
   return true;
 }
 
@@ -796,40 +844,38 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   st.m = kNegInf;
   st.l = 0.f;
 
-  // this wavefront's items, from the plan
-  const int32_t *sp = p.split + u * (int64_t)(W + 1);
-  const uint32_t istart = (uint32_t)uni(sp[w]), iend = (uint32_t)uni(sp[w + 1]);
+  // this wavefront's items and units, from the plan
+  const int32_t *isp = p.split + u * (int64_t)(2 * (W + 1)), *usp = isp + (W + 1);
+  const uint32_t i0 = (uint32_t)uni(isp[w]), i1 = (uint32_t)uni(isp[w + 1]);
+  const uint32_t u0 = (uint32_t)uni(usp[w]), u1 = (uint32_t)uni(usp[w + 1]);
 
   // ---------------- pipelined item loop
   Pipe pp;
-  pp.ring = smem + wave * kWaveLds;
-  pp.dring = smem + wave * kWaveLds + kRing;
+  uint8_t *wl = smem + wave * kWaveLds;
+  pp.ring = wl;
+  pp.uchunk = wl + kRing;
+  pp.ichunk = wl + kRing + 1024;
+  pp.ebuf = wl + kRing + 2048;
   pp.ring_base = (uint32_t)uni((int32_t)(uintptr_t)pp.ring);
-  pp.dlds = (uint32_t)uni((int32_t)(uintptr_t)pp.dring);
-  pp.dsrc = p.plan + (u * p.icap + istart) * (int64_t)sizeof(ItemDesc);
-  pp.nitems = iend - istart;
-  pp.lane = lane;
-  pp.issued = 0;
-  pp.pk = pp.plin = pp.pchunk = 0;
-  pp.pend = false;
-  pp.pkp = pp.pvp = 0;
-  pp.pmeta = pp.pgeo = 0;
-  pp.ck = pp.clin = pp.hold = 0;
-  if (pp.nitems) pp.fetch_chunk(0);
-  pp.ccnt = pp.issued;
+  pp.ulds = (uint32_t)uni((int32_t)(uintptr_t)pp.uchunk);
+  pp.ilds = (uint32_t)uni((int32_t)(uintptr_t)pp.ichunk);
+  pp.isrc = p.plan + (u * p.icap + i0) * (int64_t)sizeof(ItemDesc);
+  pp.usrc = p.units + (u * p.ucap + u0) * (int64_t)sizeof(UnitDesc);
+  pp.nitems = i1 - i0;
+  pp.nunits = u1 - u0;
+  pp.start(lane);
   // Items are processed in runs of one level, each run in a loop specialised for
   // that level (the constants of one level's path are then live only in its loop).
-  Item it;
+  uint32_t meta;
   uint64_t valid;
-  const uint8_t *ip;
-  bool more = pp.pop(it, valid, ip);
+  bool more = pp.next_item(meta, valid);
   while (more) {
-    switch (it.lv()) {
-      case GKV_EXACT: more = exact_run<PACK>(p, st, qs, pp, it, valid, ip, lane); break;
-      case GKV_INT8: more = int_run<8, PACK>(p, st, qs, pp, it, valid, ip, lane); break;
-      case GKV_INT4: more = int_run<4, PACK>(p, st, qs, pp, it, valid, ip, lane); break;
-      case GKV_INT2: more = int_run<2, PACK>(p, st, qs, pp, it, valid, ip, lane); break;
-      default: more = centroid_run<PACK>(p, st, qs, pp, it, valid, ip, lane); break;
+    switch (meta_lv(meta)) {
+      case GKV_EXACT: more = exact_run<PACK>(p, st, qs, pp, meta, valid, lane); break;
+      case GKV_INT8: more = int_run<8, PACK>(p, st, qs, pp, meta, valid, lane); break;
+      case GKV_INT4: more = int_run<4, PACK>(p, st, qs, pp, meta, valid, lane); break;
+      case GKV_INT2: more = int_run<2, PACK>(p, st, qs, pp, meta, valid, lane); break;
+      default: more = centroid_run<PACK>(p, st, qs, pp, meta, valid, lane); break;
     }
   }
   vm_wait<0>();
@@ -926,7 +972,7 @@ struct VisitDesc {
   uint64_t kp, vp;  // addresses of the K and V records
   uint64_t valid;   // tokens of the block that are read (bit t = token t)
   int32_t level;    // storage level of both records
-  uint32_t cost;    // balance cost (bits 0..23) | number of items (bits 24..31)
+  uint32_t cost;    // balance cost (bits 0..23) | items (bits 24..26) | units (bits 27..30)
 };
 static_assert(sizeof(VisitDesc) == 32, "descriptor size");
 // Balance cost of a visit: the measured time of its parts on one wavefront sharing
@@ -975,14 +1021,14 @@ __device__ __forceinline__ uint64_t block_scan(uint64_t x, uint64_t *sh, uint64_
   return x + before;
 }
 
-// Number of items of a visit (as visit_items writes them).
-__device__ __forceinline__ uint32_t visit_item_count(int lv, uint64_t valid) {
+// Items and units of a visit (as visit_items writes them): items | units << 3.
+__device__ __forceinline__ uint32_t visit_counts(int lv, uint64_t valid) {
   uint32_t tiles = 0;
   for (int t = 0; t < 4; ++t)
     if ((valid >> (16 * t)) & 0xFFFFull) tiles |= 1u << t;
   if (!tiles) return 0;
-  if (lv == GKV_CENTROID) return 1;
-  if (lv == GKV_EXACT) return __builtin_popcount(tiles);
+  if (lv == GKV_CENTROID) return 1u | (1u << 3);
+  if (lv == GKV_EXACT) return (uint32_t)__builtin_popcount(tiles) * (1u | (2u << 3));
   const int tg = group_tiles(lv);
   uint32_t k = 0;
   while (tiles) {
@@ -992,36 +1038,46 @@ __device__ __forceinline__ uint32_t visit_item_count(int lv, uint64_t valid) {
     tiles &= ~(((1u << n) - 1) << t);
     ++k;
   }
-  return k;
+  return k | ((k + 1) << 3);  // one unit per item and the scale/zero unit
 }
 
-// Writes the items of a visit (at most 4), in order, to out[]; returns their number.
-__device__ __forceinline__ int visit_items(const VisitDesc &v, ItemDesc *out) {
+__device__ __forceinline__ UnitDesc unit_desc(uint64_t a, uint64_t b, uint32_t bytes) {  // parts of `bytes` <= 2 KB
+  const uint32_t n0 = (bytes < 1024 ? bytes : 1024) / 16, n1 = (bytes > 1024 ? bytes - 1024 : 0) / 16;
+  UnitDesc d;
+  d.a = a | ((uint64_t)n0 << 48) | ((uint64_t)n1 << 56);
+  d.b = b;
+  return d;
+}
+
+// Writes the items and units of a visit, in order.
+__device__ __forceinline__ void visit_items(const VisitDesc &v, ItemDesc *items, UnitDesc *units) {
   uint32_t tiles = 0;
   for (int t = 0; t < 4; ++t)
     if ((v.valid >> (16 * t)) & 0xFFFFull) tiles |= 1u << t;
-  if (!tiles) return 0;
+  if (!tiles) return;
   const uint32_t lv = (uint32_t)v.level;
-  auto put = [&](int i, uint32_t kind, bool first, bool last, uint32_t taken, uint32_t n, uint32_t tv,
-                 uint32_t size, uint32_t ninstr, uint32_t units) {
-    out[i].kp = v.kp;
-    out[i].vp = v.vp;
-    out[i].valid = v.valid;
-    out[i].meta = kind | (lv << 2) | ((uint32_t)first << 7) | ((uint32_t)last << 8) | (taken << 9) | (n << 13) |
-                  (tv << 16);
-    out[i].geo = (size / 16) | (ninstr << 10) | (units << 16);
+  auto put = [&](int i, uint32_t kind, bool first, bool last, uint32_t taken, uint32_t n, uint32_t tv) {
+    items[i].meta = kind | (lv << 2) | ((uint32_t)first << 7) | ((uint32_t)last << 8) | (taken << 9) | (n << 13) |
+                    (tv << 16);
+    items[i].pad = 0;
+    items[i].valid = v.valid;
   };
   if (lv == GKV_CENTROID) {
-    put(0, kCentroid, true, true, tiles, 1, 0, 2 * kCentBytes, 2 * ((kCentBytes / 16 + 63) / 64), kCentBytes / 16);
-    return 1;
+    put(0, kCentroid, true, true, tiles, 1, 0);
+    units[0] = unit_desc(v.kp, v.vp, kCentBytes);
+    return;
   }
-  int k = 0;
+  int k = 0, m = 0;
   if (lv == GKV_EXACT) {
     for (int t = 0; t < 4; ++t)
-      if ((tiles >> t) & 1u)
-        put(k++, kExactTile, true, true, 1u << t, 1, (uint32_t)((v.valid >> (16 * t)) & 0xFFFFull), 2 * 4096, 8, 256);
-    return k;
+      if ((tiles >> t) & 1u) {
+        put(k++, kExactTile, true, true, 1u << t, 1, (uint32_t)((v.valid >> (16 * t)) & 0xFFFFull));
+        units[m++] = unit_desc(v.kp + 4096 * t, v.kp + 4096 * t + 2048, 2048);
+        units[m++] = unit_desc(v.vp + 4096 * t, v.vp + 4096 * t + 2048, 2048);
+      }
+    return;
   }
+  units[m++] = unit_desc(v.kp, v.vp, kSZBytes);
   const int tg = group_tiles((int)lv);
   uint32_t left = tiles;
   bool first = true;
@@ -1031,13 +1087,11 @@ __device__ __forceinline__ int visit_items(const VisitDesc &v, ItemDesc *out) {
     while ((int)n < tg && ((left >> (t + n)) & 1u)) ++n;
     const uint32_t taken = ((1u << n) - 1) << t;
     left &= ~taken;
-    const bool last = left == 0;
-    const uint32_t cu = n * 16 * lv;  // units per code segment (a multiple of 32)
-    put(k++, kIntGroup, first, last, taken, n, 0, 2 * 16 * cu + (first ? kSZBytes : 0) + (last ? kSZBytes : 0),
-        2 * ((cu + 63) / 64) + (first ? 1 : 0) + (last ? 1 : 0), cu);
+    put(k++, kIntGroup, first, left == 0, taken, n, 0);
+    const uint32_t off = kSZBytes + t * 256 * lv;
+    units[m++] = unit_desc(v.kp + off, v.vp + off, n * 256 * lv);
     first = false;
   }
-  return k;
 }
 
 // Visit v of a dense read: block v (v < nblk), else residual pseudo-block v - nblk.
@@ -1057,7 +1111,7 @@ __device__ __forceinline__ VisitDesc dense_visit(const AttnParams &p, int64_t u,
     d.vp = (uint64_t)(uintptr_t)(kp + kExactBytes);
     d.valid = token_mask(p.nres - rb * P);
   }
-  d.cost = balance_cost(d.level, d.valid) | (visit_item_count(d.level, d.valid) << 24);
+  d.cost = balance_cost(d.level, d.valid) | (visit_counts(d.level, d.valid) << 24);
   return d;
 }
 
@@ -1070,46 +1124,73 @@ __device__ __forceinline__ int midpoint_owner(int W, uint64_t e, uint32_t c, uin
   return o < (double)W ? (int)o : W - 1;
 }
 
+// Visit counts packed for the prefix scan: units in the high half, items in the low.
+__device__ __forceinline__ uint64_t count_key(uint32_t cost) {
+  const uint32_t c = cost >> 24;
+  return ((uint64_t)(c >> 3) << 32) | (c & 7u);
+}
+
+// Owner of every visit of a thread's run [v0, v1) and its items and units: the splits
+// of the wavefronts whose first visit lies in the run, and the descriptors.
+struct PlanOut {
+  ItemDesc *items;
+  UnitDesc *units;
+  int32_t *isplit, *usplit;
+  int W;
+  uint64_t total;           // total cost
+  uint32_t nitems, nunits;  // totals
+};
+
+__device__ __forceinline__ void place_visit(const PlanOut &o, const VisitDesc &d, int64_t v, int64_t nvis,
+                                            uint64_t &ecost, uint64_t &ecnt, int &prev) {
+  const uint32_t c = d.cost & 0xFFFFFFu;
+  const int own = midpoint_owner(o.W, ecost, c, o.total);
+  const uint32_t ei = (uint32_t)ecnt, eu = (uint32_t)(ecnt >> 32);
+  for (int ww = prev + 1; ww <= own; ++ww) {
+    o.isplit[ww] = (int32_t)ei;
+    o.usplit[ww] = (int32_t)eu;
+  }
+  visit_items(d, o.items + ei, o.units + eu);
+  if (v == nvis - 1)
+    for (int ww = own + 1; ww <= o.W; ++ww) {
+      o.isplit[ww] = (int32_t)o.nitems;
+      o.usplit[ww] = (int32_t)o.nunits;
+    }
+  prev = own;
+  ecost += c;
+  ecnt += count_key(d.cost);
+}
+
 // Dense plan when every thread holds at most kPlanRegs visits: the visits stay in
-// registers through the cost scan and the item expansion.
+// registers through the scans and the expansion.
 constexpr int kPlanRegs = 4;
-__device__ __forceinline__ void plan_dense_regs(const AttnParams &p, int64_t u, int64_t nblk, int64_t nvis, int W,
-                                                ItemDesc *items, int32_t *split, uint64_t *sh, uint32_t *lastc) {
+__device__ __forceinline__ void plan_dense_regs(const AttnParams &p, int64_t u, int64_t nblk, int64_t nvis,
+                                                PlanOut o, uint64_t *sh, uint32_t *lastc) {
   const int64_t per = (nvis + kPlanThreads - 1) / kPlanThreads;
   const int64_t v0 = threadIdx.x * per, v1 = v0 + per < nvis ? v0 + per : nvis;
   VisitDesc dv[kPlanRegs];
-  uint64_t mine = 0;
+  uint64_t mcost = 0, mcnt = 0;
   uint32_t last = 0;
 #pragma unroll
   for (int j = 0; j < kPlanRegs; ++j)
     if (v0 + j < v1) {
       dv[j] = dense_visit(p, u, nblk, v0 + j);
-      const uint32_t c = dv[j].cost;
-      mine += ((uint64_t)(c & 0xFFFFFFu) << 24) | (c >> 24);
-      last = c & 0xFFFFFFu;
+      mcost += dv[j].cost & 0xFFFFFFu;
+      mcnt += count_key(dv[j].cost);
+      last = dv[j].cost & 0xFFFFFFu;
     }
-  lastc[threadIdx.x] = last;  // read by the next thread after the scan's barriers
-  uint64_t tot;
-  const uint64_t excl = block_scan(mine, sh, tot) - mine;
-  const uint64_t total = tot >> 24;
-  const uint32_t nitems = (uint32_t)(tot & 0xFFFFFFu);
+  lastc[threadIdx.x] = last;  // read by the next thread after the scans' barriers
+  uint64_t tcnt;
+  uint64_t ecost = block_scan(mcost, sh, o.total) - mcost;
+  uint64_t ecnt = block_scan(mcnt, sh, tcnt) - mcnt;
+  o.nitems = (uint32_t)tcnt;
+  o.nunits = (uint32_t)(tcnt >> 32);
   if (v0 >= v1) return;
-  uint64_t ecost = excl >> 24;
-  uint32_t eitem = (uint32_t)(excl & 0xFFFFFFu);
   int prev = -1;
-  if (v0 > 0) prev = midpoint_owner(W, ecost - lastc[threadIdx.x - 1], lastc[threadIdx.x - 1], total);
+  if (v0 > 0) prev = midpoint_owner(o.W, ecost - lastc[threadIdx.x - 1], lastc[threadIdx.x - 1], o.total);
 #pragma unroll
   for (int j = 0; j < kPlanRegs; ++j)
-    if (v0 + j < v1) {
-      const uint32_t c = dv[j].cost & 0xFFFFFFu;
-      const int own = midpoint_owner(W, ecost, c, total);
-      for (int ww = prev + 1; ww <= own; ++ww) split[ww] = (int32_t)eitem;
-      eitem += visit_items(dv[j], items + eitem);
-      if (v0 + j == nvis - 1)
-        for (int ww = own + 1; ww <= W; ++ww) split[ww] = (int32_t)nitems;
-      prev = own;
-      ecost += c;
-    }
+    if (v0 + j < v1) place_visit(o, dv[j], v0 + j, nvis, ecost, ecnt, prev);
 }
 
 __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
@@ -1119,8 +1200,12 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
   const int64_t u = blockIdx.x;
   const int W = p.nsplit * kWaves;
   VisitDesc *desc = (VisitDesc *)p.visits + u * p.vcap;
-  ItemDesc *items = (ItemDesc *)p.plan + u * p.icap;
-  int32_t *split = p.split + u * (int64_t)(W + 1);
+  PlanOut o;
+  o.items = (ItemDesc *)p.plan + u * p.icap;
+  o.units = (UnitDesc *)p.units + u * p.ucap;
+  o.isplit = p.split + u * (int64_t)(2 * (W + 1));
+  o.usplit = o.isplit + (W + 1);
+  o.W = W;
   const int64_t nblk = (p.T + P - 1) / P;
   const int8_t *lvl = p.level + u * p.nblk_cap;
   const int64_t *ko = p.koff + u * p.nblk_cap, *vo = p.voff + u * p.nblk_cap;
@@ -1131,7 +1216,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
     nvis = nblk + (p.nres + P - 1) / P;
     const int64_t per = (nvis + kPlanThreads - 1) / kPlanThreads;
     if (nvis > 0 && per <= kPlanRegs) {
-      plan_dense_regs(p, u, nblk, nvis, W, items, split, sh, lastc);
+      plan_dense_regs(p, u, nblk, nvis, o, sh, lastc);
       return;
     }
     const int64_t v0 = threadIdx.x * per, v1 = v0 + per < nvis ? v0 + per : nvis;
@@ -1175,7 +1260,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
         for (int t = 0; t < 4; ++t)
           if (tl & (1u << t)) va |= 0xFFFFull << (16 * t);
         d.valid = va & token_mask(p.T - blk * P);
-        d.cost = balance_cost(d.level, d.valid) | (visit_item_count(d.level, d.valid) << 24);
+        d.cost = balance_cost(d.level, d.valid) | (visit_counts(d.level, d.valid) << 24);
         desc[vbase + incl - 1] = d;
       }
       vbase += tot;
@@ -1184,43 +1269,32 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
   }
   __syncthreads();
   if (nvis == 0) {
-    for (int ww = threadIdx.x; ww <= W; ww += kPlanThreads) split[ww] = 0;
+    for (int ww = threadIdx.x; ww <= W; ww += kPlanThreads) o.isplit[ww] = o.usplit[ww] = 0;
     return;
   }
-  // prefix cost and item count of each thread's run of visits (packed: cost in the
-  // high bits, items in the low 24), then the owner and first item of every visit
+  // prefix cost and counts of each thread's run of visits, then the owner and the
+  // first item and unit of every visit
   const int64_t per = (nvis + kPlanThreads - 1) / kPlanThreads;
   const int64_t v0 = threadIdx.x * per, v1 = v0 + per < nvis ? v0 + per : nvis;
-  uint64_t mine = 0;
+  uint64_t mcost = 0, mcnt = 0;
 #pragma unroll 4
   for (int64_t v = v0; v < v1; ++v) {
     const uint32_t c = desc[v].cost;
-    mine += ((uint64_t)(c & 0xFFFFFFu) << 24) | (c >> 24);
+    mcost += c & 0xFFFFFFu;
+    mcnt += count_key(c);
   }
-  uint64_t tot;
-  const uint64_t excl = block_scan(mine, sh, tot) - mine;
-  const uint64_t total = tot >> 24;
-  const uint32_t nitems = (uint32_t)(tot & 0xFFFFFFu);
-  auto owner = [&](uint64_t e, uint32_t c) -> int { return midpoint_owner(W, e, c, total); };
+  uint64_t tcnt;
+  uint64_t ecost = block_scan(mcost, sh, o.total) - mcost;
+  uint64_t ecnt = block_scan(mcnt, sh, tcnt) - mcnt;
+  o.nitems = (uint32_t)tcnt;
+  o.nunits = (uint32_t)(tcnt >> 32);
   if (v0 < v1) {
-    uint64_t ecost = excl >> 24;
-    uint32_t eitem = (uint32_t)(excl & 0xFFFFFFu);
     int prev = -1;
     if (v0 > 0) {
       const uint32_t cp = desc[v0 - 1].cost & 0xFFFFFFu;
-      prev = owner(ecost - cp, cp);
+      prev = midpoint_owner(W, ecost - cp, cp, o.total);
     }
-    for (int64_t v = v0; v < v1; ++v) {
-      const VisitDesc d = desc[v];
-      const uint32_t c = d.cost & 0xFFFFFFu;
-      const int own = owner(ecost, c);
-      for (int ww = prev + 1; ww <= own; ++ww) split[ww] = (int32_t)eitem;
-      eitem += visit_items(d, items + eitem);
-      if (v == nvis - 1)
-        for (int ww = own + 1; ww <= W; ++ww) split[ww] = (int32_t)nitems;
-      prev = own;
-      ecost += c;
-    }
+    for (int64_t v = v0; v < v1; ++v) place_visit(o, desc[v], v, nvis, ecost, ecnt, prev);
   }
 }
 
@@ -1245,10 +1319,10 @@ static int attn_nsplit(const gkv_cache *c, int32_t topk, int64_t T) {
 }
 
 // Workspace layout, sized by the cache capacity so that it does not move as T grows:
-// partials | wavefront splits | visit descriptors | item descriptors (at most 4
-// items per visit; +1 KB: the descriptor copies read whole 1 KB chunks).
+// partials | wavefront splits (items, units) | visit descriptors | item descriptors |
+// unit descriptors (+512 B: the descriptor copies read whole 512-byte chunks).
 struct AttnLayout {
-  int64_t split, visits, plan, total, vcap, icap;
+  int64_t split, visits, plan, units, total, vcap, icap, ucap;
   int ncap;
 };
 static int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
@@ -1258,11 +1332,13 @@ static AttnLayout attn_layout(const gkv_cache *c, int32_t topk) {
   const int G = c->Hq / c->Hkv;
   L.ncap = attn_nsplit(c, topk, (int64_t)c->nblk_cap * P);
   L.vcap = topk > 0 ? (int64_t)topk + 1 : (int64_t)c->nblk_cap + (c->nres_cap + P - 1) / P;
-  L.icap = 4 * L.vcap;
+  L.icap = 4 * L.vcap;  // at most 4 items per visit
+  L.ucap = 8 * L.vcap;  // at most 8 units per visit (an exact block)
   L.split = align256(units * L.ncap * G * (D + 2) * 4);
-  L.visits = L.split + align256(units * ((int64_t)L.ncap * kWaves + 1) * 4);
+  L.visits = L.split + align256(units * 2 * ((int64_t)L.ncap * kWaves + 1) * 4);
   L.plan = L.visits + align256(units * L.vcap * (int64_t)sizeof(VisitDesc));
-  L.total = L.plan + units * L.icap * (int64_t)sizeof(ItemDesc) + 1024;
+  L.units = L.plan + align256(units * L.icap * (int64_t)sizeof(ItemDesc));
+  L.total = L.units + units * L.ucap * (int64_t)sizeof(UnitDesc) + 512;
   return L;
 }
 
@@ -1297,8 +1373,10 @@ static gkv_status attn_setup(const uint16_t *q, const gkv_cache *c, const int32_
   p.split = (int32_t *)((uint8_t *)ws + L.split);
   p.visits = (uint8_t *)ws + L.visits;
   p.plan = (uint8_t *)ws + L.plan;
+  p.units = (uint8_t *)ws + L.units;
   p.vcap = L.vcap;
   p.icap = L.icap;
+  p.ucap = L.ucap;
   p.T = c->T;
   p.nblk_cap = c->nblk_cap;
   p.Hkv = c->Hkv;
