@@ -1161,6 +1161,12 @@ __device__ __forceinline__ void place_visit(const PlanOut &o, const VisitDesc &d
   ecnt += count_key(d.cost);
 }
 
+// A dense plan runs gridDim.y workgroups per (b, KV head): each scans the costs and
+// counts of all visits (cheap) and expands only the visits of its slice of threads.
+__device__ __forceinline__ bool own_slice() {
+  return (int)((threadIdx.x * gridDim.y) / kPlanThreads) == (int)blockIdx.y;
+}
+
 // Dense plan when every thread holds at most kPlanRegs visits: the visits stay in
 // registers through the scans and the expansion.
 constexpr int kPlanRegs = 4;
@@ -1185,7 +1191,7 @@ __device__ __forceinline__ void plan_dense_regs(const AttnParams &p, int64_t u, 
   uint64_t ecnt = block_scan(mcnt, sh, tcnt) - mcnt;
   o.nitems = (uint32_t)tcnt;
   o.nunits = (uint32_t)(tcnt >> 32);
-  if (v0 >= v1) return;
+  if (v0 >= v1 || !own_slice()) return;
   int prev = -1;
   if (v0 > 0) prev = midpoint_owner(o.W, ecost - lastc[threadIdx.x - 1], lastc[threadIdx.x - 1], o.total);
 #pragma unroll
@@ -1220,9 +1226,27 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
       return;
     }
     const int64_t v0 = threadIdx.x * per, v1 = v0 + per < nvis ? v0 + per : nvis;
-#pragma unroll 4
-    for (int64_t v = v0; v < v1; ++v) desc[v] = dense_visit(p, u, nblk, v);
+    uint64_t mcost = 0, mcnt = 0;
+    for (int64_t v = v0; v < v1; ++v) {
+      const uint32_t c = dense_visit(p, u, nblk, v).cost;
+      mcost += c & 0xFFFFFFu;
+      mcnt += count_key(c);
+    }
+    uint64_t tcnt;
+    uint64_t ecost = block_scan(mcost, sh, o.total) - mcost;
+    uint64_t ecnt = block_scan(mcnt, sh, tcnt) - mcnt;
+    o.nitems = (uint32_t)tcnt;
+    o.nunits = (uint32_t)(tcnt >> 32);
+    if (v0 >= v1 || !own_slice()) return;
+    int prev = -1;
+    if (v0 > 0) {
+      const uint32_t cp = dense_visit(p, u, nblk, v0 - 1).cost & 0xFFFFFFu;
+      prev = midpoint_owner(W, ecost - cp, cp, o.total);
+    }
+    for (int64_t v = v0; v < v1; ++v) place_visit(o, dense_visit(p, u, nblk, v), v, nvis, ecost, ecnt, prev);
+    return;
   } else {
+    if (blockIdx.y) return;  // one workgroup per (b, KV head)
     // Compressed-Quest: the leading valid ranked pages (ascending) and the current
     // page; consecutive pages of one block form one visit
     const int32_t *pg = p.pages + u * p.topk;
@@ -1390,7 +1414,13 @@ static gkv_status attn_setup(const uint16_t *q, const gkv_cache *c, const int32_
 }
 
 static void launch_plan(const AttnParams &p, const gkv_cache *c, hipStream_t s) {
-  hipLaunchKernelGGL(plan_kernel, dim3(c->B * c->Hkv), dim3(kPlanThreads), 0, s, p);
+  // dense reads: one workgroup per 256 visits of a (b, KV head), at most 8
+  int slices = 1;
+  if (!p.pages) {
+    const int64_t nvis = (p.T + P - 1) / P + (p.nres + P - 1) / P;
+    slices = (int)(nvis / 256 < 1 ? 1 : (nvis / 256 > 8 ? 8 : nvis / 256));
+  }
+  hipLaunchKernelGGL(plan_kernel, dim3(c->B * c->Hkv, slices), dim3(kPlanThreads), 0, s, p);
 }
 static void launch_partials(const AttnParams &p, const gkv_cache *c, hipStream_t s) {
   const size_t lds = (size_t)kWaves * kWaveLds + 16 * kQRow;  // rings also hold the merge buffers
