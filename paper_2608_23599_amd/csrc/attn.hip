@@ -1,15 +1,15 @@
 // Fused dequant + online-softmax GQA decode attention over a graded cache
 // (sections 3.1, 3.5 and 3.7), and the split-context reduction.
 //
-// Three kernels per call.  The plan kernel (one workgroup per (b, KV head)) writes a
-// 32-byte descriptor per "visit" (a block and the tokens of it that are read: all
-// valid tokens of a dense read minus the residual rows, or the selected pages of a
-// Compressed-Quest read) and splits the visits over the wavefronts by a cost that
-// counts bytes and pipeline items.  The attention kernel runs grid (nsplit, Hkv, B)
-// x 4 wavefronts; each wavefront keeps an online-softmax state for the up-to-16
-// query heads of the group in MFMA accumulator layout; the four wavefronts of a
-// workgroup are merged in LDS into one partial (m, l, o) per head, and a merge
-// kernel combines the partials of each (b, KV head).
+// Three kernels per call.  The plan kernel describes every "visit" (a block and the
+// tokens of it that are read: all valid tokens of a dense read minus the residual
+// rows, or the selected pages of a Compressed-Quest read), splits the visits over the
+// wavefronts by a balance cost, and writes the wavefronts' work lists.  The attention
+// kernel runs nsplit workgroups of 4 wavefronts per (b, KV head); each wavefront keeps
+// an online-softmax state for the up-to-16 query heads of the group in MFMA
+// accumulator layout; the four wavefronts of a workgroup are merged in LDS into one
+// partial (m, l, o) per head, and a merge kernel combines the partials of each
+// (b, KV head).
 //
 // Memory pipeline: the plan kernel turns every visit into compute "items" (an
 // exact 16-token tile, a group of int tiles, a centroid block) and copy "units": a
@@ -212,6 +212,7 @@ struct AttnParams {
   float *part;
   int64_t T;
   int nblk_cap, Hkv, G, nres, nrb_cap, topk, nsplit;
+  int fast;  // workgroups of each (b, KV head) dispatched first (see attn_grid)
   int64_t vcap, icap, ucap;
   float sl2;  // log2(e) / sqrt(D)
 };
@@ -824,7 +825,10 @@ __device__ __forceinline__ bool centroid_run(const AttnParams &p, State &st, con
 template <bool PACK>
 __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   extern __shared__ __align__(16) uint8_t smem[];
-  const int sidx = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  // Workgroup L of the one-dimensional grid serves (b, KV head) L % units as its
+  // workgroup L / units, so that the workgroups dispatched first cover every (b, KV head).
+  const int units = (int)gridDim.x / p.nsplit;
+  const int sidx = (int)blockIdx.x / units, h = (int)blockIdx.x % units % p.Hkv, b = (int)blockIdx.x % units / p.Hkv;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int kg = lane >> 4, m16 = lane & 15;
   const int64_t u = (int64_t)b * p.Hkv + h;
@@ -979,8 +983,8 @@ static_assert(sizeof(VisitDesc) == 32, "descriptor size");
 // its SIMD (about 8 cycles per unit).  Exact tiles are bound by the wavefront's
 // share of the bandwidth (8 KB each), int tiles by the dequantisation and softmax
 // work rather than by their bytes.
-constexpr uint32_t kCostExactTile = 500, kCostInt8Tile = 450, kCostInt4Tile = 300, kCostInt2Tile = 210,
-                   kCostCentroid = 565, kCostIntBlock = 240;
+constexpr uint32_t kCostExactTile = 510, kCostInt8Tile = 450, kCostInt4Tile = 305, kCostInt2Tile = 232,
+                   kCostCentroid = 590, kCostIntBlock = 248;
 
 __device__ __forceinline__ uint32_t balance_cost(int lv, uint64_t va) {
   uint32_t tiles = 0;
@@ -1118,9 +1122,14 @@ __device__ __forceinline__ VisitDesc dense_visit(const AttnParams &p, int64_t u,
 // Wavefront owning the midpoint of cost interval [e, e + c) of a total, in fp64
 // (every operand is an integer below 2^53, and the floor of a monotone quotient
 // keeps the owners non-decreasing along the visits).
-__device__ __forceinline__ int midpoint_owner(int W, uint64_t e, uint32_t c, uint64_t total) {
+// The first W1 wavefronts (those of the workgroups dispatched first, which win the
+// issue arbitration against the later ones on their SIMDs) get 6 capacity units,
+// the others 5.
+__device__ __forceinline__ int midpoint_owner(int W, int W1, uint64_t e, uint32_t c, uint64_t total) {
   if (!total) return 0;
-  const double o = __builtin_floor(((double)W * (double)(2 * e + c)) / (2.0 * (double)total));
+  const double cap = 6.0 * W1 + 5.0 * (W - W1);
+  const double x = ((double)(2 * e + c) * cap) / (2.0 * (double)total);
+  const double o = x < 6.0 * W1 ? __builtin_floor(x / 6.0) : W1 + __builtin_floor((x - 6.0 * W1) / 5.0);
   return o < (double)W ? (int)o : W - 1;
 }
 
@@ -1136,7 +1145,7 @@ struct PlanOut {
   ItemDesc *items;
   UnitDesc *units;
   int32_t *isplit, *usplit;
-  int W;
+  int W, W1;                // wavefronts, wavefronts of the workgroups dispatched first
   uint64_t total;           // total cost
   uint32_t nitems, nunits;  // totals
 };
@@ -1144,7 +1153,7 @@ struct PlanOut {
 __device__ __forceinline__ void place_visit(const PlanOut &o, const VisitDesc &d, int64_t v, int64_t nvis,
                                             uint64_t &ecost, uint64_t &ecnt, int &prev) {
   const uint32_t c = d.cost & 0xFFFFFFu;
-  const int own = midpoint_owner(o.W, ecost, c, o.total);
+  const int own = midpoint_owner(o.W, o.W1, ecost, c, o.total);
   const uint32_t ei = (uint32_t)ecnt, eu = (uint32_t)(ecnt >> 32);
   for (int ww = prev + 1; ww <= own; ++ww) {
     o.isplit[ww] = (int32_t)ei;
@@ -1193,7 +1202,7 @@ __device__ __forceinline__ void plan_dense_regs(const AttnParams &p, int64_t u, 
   o.nunits = (uint32_t)(tcnt >> 32);
   if (v0 >= v1 || !own_slice()) return;
   int prev = -1;
-  if (v0 > 0) prev = midpoint_owner(o.W, ecost - lastc[threadIdx.x - 1], lastc[threadIdx.x - 1], o.total);
+  if (v0 > 0) prev = midpoint_owner(o.W, o.W1, ecost - lastc[threadIdx.x - 1], lastc[threadIdx.x - 1], o.total);
 #pragma unroll
   for (int j = 0; j < kPlanRegs; ++j)
     if (v0 + j < v1) place_visit(o, dv[j], v0 + j, nvis, ecost, ecnt, prev);
@@ -1212,6 +1221,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
   o.isplit = p.split + u * (int64_t)(2 * (W + 1));
   o.usplit = o.isplit + (W + 1);
   o.W = W;
+  o.W1 = p.fast * kWaves;
   const int64_t nblk = (p.T + P - 1) / P;
   const int8_t *lvl = p.level + u * p.nblk_cap;
   const int64_t *ko = p.koff + u * p.nblk_cap, *vo = p.voff + u * p.nblk_cap;
@@ -1241,7 +1251,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
     int prev = -1;
     if (v0 > 0) {
       const uint32_t cp = dense_visit(p, u, nblk, v0 - 1).cost & 0xFFFFFFu;
-      prev = midpoint_owner(W, ecost - cp, cp, o.total);
+      prev = midpoint_owner(W, o.W1, ecost - cp, cp, o.total);
     }
     for (int64_t v = v0; v < v1; ++v) place_visit(o, dense_visit(p, u, nblk, v), v, nvis, ecost, ecnt, prev);
     return;
@@ -1316,7 +1326,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
     int prev = -1;
     if (v0 > 0) {
       const uint32_t cp = desc[v0 - 1].cost & 0xFFFFFFu;
-      prev = midpoint_owner(W, ecost - cp, cp, o.total);
+      prev = midpoint_owner(W, o.W1, ecost - cp, cp, o.total);
     }
     for (int64_t v = v0; v < v1; ++v) place_visit(o, desc[v], v, nvis, ecost, ecnt, prev);
   }
@@ -1340,6 +1350,30 @@ static int attn_nsplit(const gkv_cache *c, int32_t topk, int64_t T) {
   if (waves < 1) waves = 1;
   if (waves > kMaxWaves) waves = kMaxWaves;
   return (int)((waves + kWaves - 1) / kWaves);
+}
+
+// Compute units of the current device (cached per device).
+static int device_cus() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1;
+  static int cache[64];
+  if (!cache[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 1;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
+// Workgroups of each (b, KV head) that are dispatched first.  With two attention
+// workgroups per CU and the whole grid resident at once, workgroups 0 .. CUs-1 of the
+// one-dimensional grid take the first slot of every CU; their wavefronts win the
+// issue arbitration on their SIMDs (the older wavefront goes first) and run about a
+// fifth faster, so the split gives them more work.  Otherwise all count the same.
+static int attn_fast(int nsplit, int64_t units) {
+  const int64_t cus = device_cus(), nb = (int64_t)nsplit * units;
+  if (nb <= cus || nb > 2 * cus) return nsplit;
+  return (int)(cus / units);
 }
 
 // Workspace layout, sized by the cache capacity so that it does not move as T grows:
@@ -1409,6 +1443,7 @@ static gkv_status attn_setup(const uint16_t *q, const gkv_cache *c, const int32_
   p.nrb_cap = (c->nres_cap + P - 1) / P;
   p.topk = topk;
   p.nsplit = attn_nsplit(c, topk, c->T);
+  p.fast = attn_fast(p.nsplit, (int64_t)c->B * c->Hkv);
   p.sl2 = 1.4426950408889634f / sqrtf((float)D);
   return GKV_OK;
 }
@@ -1425,9 +1460,9 @@ static void launch_plan(const AttnParams &p, const gkv_cache *c, hipStream_t s) 
 static void launch_partials(const AttnParams &p, const gkv_cache *c, hipStream_t s) {
   const size_t lds = (size_t)kWaves * kWaveLds + 16 * kQRow;  // rings also hold the merge buffers
   if (p.G <= 8)
-    hipLaunchKernelGGL(attn_kernel<true>, dim3(p.nsplit, c->Hkv, c->B), dim3(kThreads), lds, s, p);
+    hipLaunchKernelGGL(attn_kernel<true>, dim3(p.nsplit * c->Hkv * c->B), dim3(kThreads), lds, s, p);
   else
-    hipLaunchKernelGGL(attn_kernel<false>, dim3(p.nsplit, c->Hkv, c->B), dim3(kThreads), lds, s, p);
+    hipLaunchKernelGGL(attn_kernel<false>, dim3(p.nsplit * c->Hkv * c->B), dim3(kThreads), lds, s, p);
 }
 static void launch_merge(const AttnParams &p, const gkv_cache *c, float *out, hipStream_t s) {
   hipLaunchKernelGGL(merge_kernel, dim3(p.G, c->Hkv * c->B), dim3(D), 0, s, (const float *)p.part, out, p.nsplit,
