@@ -26,44 +26,59 @@ __device__ __forceinline__ uint64_t order_key(double x) {
 // Box upper bound of every ranked page for the G query heads of a KV head:
 // UB_g(p) = sum_d q_gd * (q_gd >= 0 ? kmax_pd : kmin_pd), channel-ascending in fp64
 // (each product of two fp16 values is exact, so the fused multiply-add rounds once,
-// like a separate add); page score = max_g UB_g.  grid (ceil(npages/256), Hkv, B).
+// like a separate add); page score = max_g UB_g.  A workgroup covers 64 pages with one
+// wavefront per query head (lane = page); the bound of one head is one chain of 128
+// multiply-adds.  Which half of a box word a head reads depends only on the sign of
+// q_gd, so it is a shift chosen per (head, channel); for q_gd = +-0 either half gives
+// the same sum (the product is a zero and the running sum is never -0).  The heads'
+// bounds meet in LDS and the first wavefront writes the keys.  grid (ceil(npages/64),
+// Hkv, B) x 64 G threads.
+struct QCoef {
+  double q;
+  uint32_t shift, pad;
+};
 template <int G>
-__global__ void __launch_bounds__(256) quest_score_kernel(const uint16_t *__restrict__ q,
-                                                          const uint16_t *__restrict__ boxes, int64_t npage_cap,
-                                                          int64_t npages, int Hkv, uint64_t *__restrict__ keys) {
-  __shared__ double qs[16 * D];
+__global__ void __launch_bounds__(64 * G) quest_score_kernel(const uint16_t *__restrict__ q,
+                                                             const uint16_t *__restrict__ boxes, int64_t npage_cap,
+                                                             int64_t npages, int Hkv, uint64_t *__restrict__ keys) {
+  __shared__ QCoef qc[G * D];
+  __shared__ double ub[G][64];
   const int h = blockIdx.y, b = blockIdx.z;
   const int64_t u = (int64_t)b * Hkv + h;
-  for (int i = threadIdx.x; i < G * D; i += 256) qs[i] = (double)__builtin_bit_cast(_Float16, q[u * G * D + i]);
+  for (int i = threadIdx.x; i < G * D; i += 64 * G) {
+    const uint16_t bits = q[u * G * D + i];
+    qc[i].q = (double)__builtin_bit_cast(_Float16, bits);
+    qc[i].shift = (bits & 0x8000u) ? 0u : 16u;  // kmin in the low half, kmax in the high
+  }
   __syncthreads();
-  const int64_t pg = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (pg >= npages) return;
-  const uint32_t *bx = (const uint32_t *)(boxes + u * npage_cap * 2 * D);
-  double acc[G];
-#pragma unroll
-  for (int g = 0; g < G; ++g) acc[g] = 0.0;
+  const int g = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t pg = (int64_t)blockIdx.x * 64 + lane;
+  const bool on = pg < npages;
+  const uint32_t *bx = (const uint32_t *)(boxes + u * npage_cap * 2 * D) + (on ? box_index(pg, 0) >> 1 : 0);
+  const QCoef *qg = qc + g * D;
+  double acc = 0.0;
   // 64 channels' box words are loaded before they are used (independent loads in
-  // flight); the accumulation stays channel-ascending
+  // flight; two batches keep the registers low enough for every wavefront of the
+  // grid to be resident); the accumulation stays channel-ascending
   for (int d0 = 0; d0 < D; d0 += 64) {
     uint32_t pr[64];
 #pragma unroll
-    for (int e = 0; e < 64; ++e) pr[e] = bx[box_index(pg, d0 + e) >> 1];
+    for (int e = 0; e < 64; ++e) pr[e] = on ? bx[(d0 + e) * 64] : 0u;
 #pragma unroll
     for (int e = 0; e < 64; ++e) {
-      const int d = d0 + e;
-      const double lo = (double)__builtin_bit_cast(_Float16, (uint16_t)(pr[e] & 0xFFFFu));
-      const double hi = (double)__builtin_bit_cast(_Float16, (uint16_t)(pr[e] >> 16));
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        const double qd = qs[g * D + d];
-        acc[g] = __builtin_fma(qd, qd >= 0.0 ? hi : lo, acc[g]);
-      }
+      const QCoef c = qg[d0 + e];
+      const double x = (double)__builtin_bit_cast(_Float16, (uint16_t)(pr[e] >> c.shift));
+      acc = __builtin_fma(c.q, x, acc);
     }
   }
-  double best = acc[0];
+  ub[g][lane] = acc;
+  __syncthreads();
+  if (g == 0 && on) {
+    double best = ub[0][lane];
 #pragma unroll
-  for (int g = 1; g < G; ++g) best = acc[g] > best ? acc[g] : best;
-  keys[u * npage_cap + pg] = order_key(best);
+    for (int j = 1; j < G; ++j) best = ub[j][lane] > best ? ub[j][lane] : best;
+    keys[u * npage_cap + pg] = order_key(best);
+  }
 }
 
 // Select the first k of the order (key desc, index asc) among keys[0..n) of one
@@ -367,12 +382,12 @@ extern "C" gkv_status gkv_quest_select(const uint16_t *q, const gkv_cache *c, in
   hipStream_t s = (hipStream_t)stream;
   uint64_t *keys = (uint64_t *)ws;
   if (ncur > 0) {
-    dim3 grid((unsigned)((ncur + 255) / 256), c->Hkv, c->B);
+    dim3 grid((unsigned)((ncur + 63) / 64), c->Hkv, c->B);
     switch (G) {
-#define GKV_SCORE(g)                                                                                          \
-  case g:                                                                                                     \
-    hipLaunchKernelGGL(quest_score_kernel<g>, grid, dim3(256), 0, s, q, c->boxes, c->npage_cap, ncur, c->Hkv, \
-                       keys);                                                                                 \
+#define GKV_SCORE(g)                                                                                           \
+  case g:                                                                                                      \
+    hipLaunchKernelGGL(quest_score_kernel<g>, grid, dim3(64 * g), 0, s, q, c->boxes, c->npage_cap, ncur, c->Hkv, \
+                       keys);                                                                                  \
     break;
       GKV_SCORE(1) GKV_SCORE(2) GKV_SCORE(3) GKV_SCORE(4) GKV_SCORE(5) GKV_SCORE(6) GKV_SCORE(7) GKV_SCORE(8)
       GKV_SCORE(9) GKV_SCORE(10) GKV_SCORE(11) GKV_SCORE(12) GKV_SCORE(13) GKV_SCORE(14) GKV_SCORE(15)
