@@ -135,6 +135,64 @@ __device__ __forceinline__ void scan2(SelShared &sh, int64_t &a, int64_t &b, int
   __syncthreads();
 }
 
+// The keys that match the current prefix (at most 64) are gathered into LDS and
+// ranked exactly by (key descending, index ascending) in one wavefront; the key of
+// rank remaining - 1 becomes the threshold and `remaining` the number of keys equal
+// to it still to take.  Leaves the workgroup synchronised.
+template <int KPT>
+__device__ __forceinline__ void small_candidates(SelShared &sh, const uint64_t *kr, const uint64_t *key, int64_t n) {
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  uint64_t *ckey = (uint64_t *)&sh.hist[0][0];
+  int32_t *cidx = (int32_t *)(ckey + 64);
+  uint32_t *cnt = (uint32_t *)(cidx + 64);
+  const uint64_t pre = sh.prefix, pm = sh.pmask;
+  const int64_t rem = sh.remaining;
+  if (tid == 0) *cnt = 0;
+  __syncthreads();
+  if (KPT > 0) {
+#pragma unroll
+    for (int j = 0; j < (KPT > 0 ? KPT : 1); ++j) {
+      const int64_t i = (int64_t)tid * KPT + j;
+      if (i < n && (kr[j] & pm) == pre) {
+        const uint32_t at = atomicAdd(cnt, 1u);
+        ckey[at] = kr[j];
+        cidx[at] = (int32_t)i;
+      }
+    }
+  } else {
+    for (int64_t i = tid; i < n; i += kSelThreads) {
+      const uint64_t kv = key[i];
+      if ((kv & pm) == pre) {
+        const uint32_t at = atomicAdd(cnt, 1u);
+        ckey[at] = kv;
+        cidx[at] = (int32_t)i;
+      }
+    }
+  }
+  __syncthreads();
+  if (wv == 0) {
+    const int nc = (int)*cnt;
+    const bool in = lane < nc;
+    const uint64_t mk = in ? ckey[lane] : 0;
+    const int32_t mi = in ? cidx[lane] : 0;
+    int rank = 0;
+    for (int j = 0; j < nc; ++j) {
+      const uint64_t kj = __shfl(mk, j);
+      const int32_t ij = __shfl(mi, j);
+      rank += kj > mk || (kj == mk && ij < mi);
+    }
+    const bool thr_lane = in && rank == (int)rem - 1;
+    const uint64_t thr = __shfl(mk, __builtin_ctzll(__ballot(thr_lane)));
+    const int above = __popcll(__ballot(in && mk > thr));
+    if (lane == 0) {
+      sh.prefix = thr;
+      sh.pmask = ~0ull;
+      sh.remaining = rem - above;
+    }
+  }
+  __syncthreads();
+}
+
 template <int KPT>
 __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__restrict__ keys, int64_t key_stride,
                                                              int64_t n, int k, int32_t *__restrict__ out,
@@ -252,9 +310,14 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
         sh.remaining = rem - suf[hit + 1];
         sh.prefix = pre | ((uint64_t)dig << shift);
         sh.pmask = pm | (0xFFull << shift);
+        sh.base[1] = c[hit];  // keys in the chosen digit's bucket
       }
     }
     __syncthreads();
+    if (pass < 7 && sh.base[1] <= 64) {  // few candidates left: rank them in one wavefront
+      small_candidates<KPT>(sh, kr, key, n);
+      break;
+    }
   }
   const uint64_t thr = sh.prefix;
   const int64_t eq_take = sh.remaining;  // keys equal to thr to take, lowest index first
