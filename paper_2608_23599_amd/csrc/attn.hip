@@ -1133,41 +1133,50 @@ __device__ __forceinline__ int midpoint_owner(int W, int W1, uint64_t e, uint32_
   return o < (double)W ? (int)o : W - 1;
 }
 
-// Visit counts packed for the prefix scan: units in the high half, items in the low.
-__device__ __forceinline__ uint64_t count_key(uint32_t cost) {
-  const uint32_t c = cost >> 24;
-  return ((uint64_t)(c >> 3) << 32) | (c & 7u);
+// Cost, units and items of a visit packed for one prefix scan: cost (bits 35..63) |
+// units (17..34) | items (0..16); the totals fit while a (b, KV head) has at most
+// 32767 visits (checked on the host).
+__device__ __forceinline__ uint64_t scan_key(uint32_t cost) {
+  return ((uint64_t)(cost & 0xFFFFFFu) << 35) | ((uint64_t)((cost >> 27) & 15u) << 17) | ((cost >> 24) & 7u);
 }
+__device__ __forceinline__ uint64_t key_cost(uint64_t k) { return k >> 35; }
+__device__ __forceinline__ uint32_t key_units(uint64_t k) { return (uint32_t)(k >> 17) & 0x3FFFFu; }
+__device__ __forceinline__ uint32_t key_items(uint64_t k) { return (uint32_t)k & 0x1FFFFu; }
 
-// Owner of every visit of a thread's run [v0, v1) and its items and units: the splits
-// of the wavefronts whose first visit lies in the run, and the descriptors.
+// Where a plan writes: the wavefronts' splits and the item and unit lists.
 struct PlanOut {
   ItemDesc *items;
   UnitDesc *units;
   int32_t *isplit, *usplit;
-  int W, W1;                // wavefronts, wavefronts of the workgroups dispatched first
-  uint64_t total;           // total cost
-  uint32_t nitems, nunits;  // totals
+  int W, W1;       // wavefronts, wavefronts of the workgroups dispatched first
+  uint64_t total;  // scan key of all visits
 };
 
+// Visit v, whose scan key interval starts at e: the splits of the wavefronts whose
+// first visit it is, and its items and units.
 __device__ __forceinline__ void place_visit(const PlanOut &o, const VisitDesc &d, int64_t v, int64_t nvis,
-                                            uint64_t &ecost, uint64_t &ecnt, int &prev) {
+                                            uint64_t &e, int &prev) {
   const uint32_t c = d.cost & 0xFFFFFFu;
-  const int own = midpoint_owner(o.W, o.W1, ecost, c, o.total);
-  const uint32_t ei = (uint32_t)ecnt, eu = (uint32_t)(ecnt >> 32);
+  const int own = midpoint_owner(o.W, o.W1, key_cost(e), c, key_cost(o.total));
   for (int ww = prev + 1; ww <= own; ++ww) {
-    o.isplit[ww] = (int32_t)ei;
-    o.usplit[ww] = (int32_t)eu;
+    o.isplit[ww] = (int32_t)key_items(e);
+    o.usplit[ww] = (int32_t)key_units(e);
   }
-  visit_items(d, o.items + ei, o.units + eu);
+  visit_items(d, o.items + key_items(e), o.units + key_units(e));
   if (v == nvis - 1)
     for (int ww = own + 1; ww <= o.W; ++ww) {
-      o.isplit[ww] = (int32_t)o.nitems;
-      o.usplit[ww] = (int32_t)o.nunits;
+      o.isplit[ww] = (int32_t)key_items(o.total);
+      o.usplit[ww] = (int32_t)key_units(o.total);
     }
   prev = own;
-  ecost += c;
-  ecnt += count_key(d.cost);
+  e += scan_key(d.cost);
+}
+
+// Owner of the visit before v0 (cost interval ending at e), -1 for v0 == 0.
+__device__ __forceinline__ int prev_owner(const PlanOut &o, int64_t v0, uint64_t e, uint32_t prev_cost) {
+  if (v0 == 0) return -1;
+  const uint32_t c = prev_cost & 0xFFFFFFu;
+  return midpoint_owner(o.W, o.W1, key_cost(e) - c, c, key_cost(o.total));
 }
 
 // A dense plan runs gridDim.y workgroups per (b, KV head): each scans the costs and
@@ -1177,44 +1186,40 @@ __device__ __forceinline__ bool own_slice() {
 }
 
 // Dense plan when every thread holds at most kPlanRegs visits: the visits stay in
-// registers through the scans and the expansion.
+// registers through the scan and the expansion.
 constexpr int kPlanRegs = 4;
 __device__ __forceinline__ void plan_dense_regs(const AttnParams &p, int64_t u, int64_t nblk, int64_t nvis,
                                                 PlanOut o, uint64_t *sh, uint32_t *lastc) {
   const int64_t per = (nvis + kPlanThreads - 1) / kPlanThreads;
   const int64_t v0 = threadIdx.x * per, v1 = v0 + per < nvis ? v0 + per : nvis;
   VisitDesc dv[kPlanRegs];
-  uint64_t mcost = 0, mcnt = 0;
+  uint64_t mine = 0;
   uint32_t last = 0;
 #pragma unroll
   for (int j = 0; j < kPlanRegs; ++j)
     if (v0 + j < v1) {
       dv[j] = dense_visit(p, u, nblk, v0 + j);
-      mcost += dv[j].cost & 0xFFFFFFu;
-      mcnt += count_key(dv[j].cost);
-      last = dv[j].cost & 0xFFFFFFu;
+      mine += scan_key(dv[j].cost);
+      last = dv[j].cost;
     }
-  lastc[threadIdx.x] = last;  // read by the next thread after the scans' barriers
-  uint64_t tcnt;
-  uint64_t ecost = block_scan(mcost, sh, o.total) - mcost;
-  uint64_t ecnt = block_scan(mcnt, sh, tcnt) - mcnt;
-  o.nitems = (uint32_t)tcnt;
-  o.nunits = (uint32_t)(tcnt >> 32);
+  lastc[threadIdx.x] = last;  // read by the next thread after the scan's barriers
+  uint64_t e = block_scan(mine, sh, o.total) - mine;
   if (v0 >= v1 || !own_slice()) return;
-  int prev = -1;
-  if (v0 > 0) prev = midpoint_owner(o.W, o.W1, ecost - lastc[threadIdx.x - 1], lastc[threadIdx.x - 1], o.total);
+  int prev = prev_owner(o, v0, e, v0 > 0 ? lastc[threadIdx.x - 1] : 0u);
 #pragma unroll
   for (int j = 0; j < kPlanRegs; ++j)
-    if (v0 + j < v1) place_visit(o, dv[j], v0 + j, nvis, ecost, ecnt, prev);
+    if (v0 + j < v1) place_visit(o, dv[j], v0 + j, nvis, e, prev);
 }
+
+constexpr int kPlanLdsVisits = kPlanThreads;  // Compressed-Quest visits kept in LDS
 
 __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
   __shared__ uint64_t sh[2 * kPlanThreads / 64];
   __shared__ uint32_t lastc[kPlanThreads];
+  __shared__ VisitDesc lds_desc[kPlanLdsVisits];
   __shared__ int s_cnt;
   const int64_t u = blockIdx.x;
   const int W = p.nsplit * kWaves;
-  VisitDesc *desc = (VisitDesc *)p.visits + u * p.vcap;
   PlanOut o;
   o.items = (ItemDesc *)p.plan + u * p.icap;
   o.units = (UnitDesc *)p.units + u * p.ucap;
@@ -1223,52 +1228,76 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
   o.W = W;
   o.W1 = p.fast * kWaves;
   const int64_t nblk = (p.T + P - 1) / P;
-  const int8_t *lvl = p.level + u * p.nblk_cap;
-  const int64_t *ko = p.koff + u * p.nblk_cap, *vo = p.voff + u * p.nblk_cap;
-  int64_t nvis;
   if (!p.pages) {
     // dense: blocks 0..nblk-1, then the residual rows as exact pseudo-blocks; each
     // thread describes a contiguous run of visits
-    nvis = nblk + (p.nres + P - 1) / P;
+    const int64_t nvis = nblk + (p.nres + P - 1) / P;
     const int64_t per = (nvis + kPlanThreads - 1) / kPlanThreads;
-    if (nvis > 0 && per <= kPlanRegs) {
+    if (per <= kPlanRegs) {
       plan_dense_regs(p, u, nblk, nvis, o, sh, lastc);
       return;
     }
     const int64_t v0 = threadIdx.x * per, v1 = v0 + per < nvis ? v0 + per : nvis;
-    uint64_t mcost = 0, mcnt = 0;
-    for (int64_t v = v0; v < v1; ++v) {
-      const uint32_t c = dense_visit(p, u, nblk, v).cost;
-      mcost += c & 0xFFFFFFu;
-      mcnt += count_key(c);
-    }
-    uint64_t tcnt;
-    uint64_t ecost = block_scan(mcost, sh, o.total) - mcost;
-    uint64_t ecnt = block_scan(mcnt, sh, tcnt) - mcnt;
-    o.nitems = (uint32_t)tcnt;
-    o.nunits = (uint32_t)(tcnt >> 32);
+    uint64_t mine = 0;
+    for (int64_t v = v0; v < v1; ++v) mine += scan_key(dense_visit(p, u, nblk, v).cost);
+    uint64_t e = block_scan(mine, sh, o.total) - mine;
     if (v0 >= v1 || !own_slice()) return;
-    int prev = -1;
-    if (v0 > 0) {
-      const uint32_t cp = dense_visit(p, u, nblk, v0 - 1).cost & 0xFFFFFFu;
-      prev = midpoint_owner(W, o.W1, ecost - cp, cp, o.total);
-    }
-    for (int64_t v = v0; v < v1; ++v) place_visit(o, dense_visit(p, u, nblk, v), v, nvis, ecost, ecnt, prev);
+    int prev = prev_owner(o, v0, e, v0 > 0 ? dense_visit(p, u, nblk, v0 - 1).cost : 0u);
+    for (int64_t v = v0; v < v1; ++v) place_visit(o, dense_visit(p, u, nblk, v), v, nvis, e, prev);
     return;
-  } else {
-    if (blockIdx.y) return;  // one workgroup per (b, KV head)
-    // Compressed-Quest: the leading valid ranked pages (ascending) and the current
-    // page; consecutive pages of one block form one visit
-    const int32_t *pg = p.pages + u * p.topk;
-    const int64_t cur = (p.T - 1) / 16;
-    if (threadIdx.x == 0) s_cnt = p.topk;
+  }
+  if (blockIdx.y) return;  // one workgroup per (b, KV head)
+  // Compressed-Quest: the leading valid ranked pages (ascending) and the current
+  // page; consecutive pages of one block form one visit
+  const int8_t *lvl = p.level + u * p.nblk_cap;
+  const int64_t *ko = p.koff + u * p.nblk_cap, *vo = p.voff + u * p.nblk_cap;
+  VisitDesc *desc = p.topk + 1 <= kPlanLdsVisits ? lds_desc : (VisitDesc *)p.visits + u * p.vcap;
+  const int32_t *pg = p.pages + u * p.topk;
+  const int64_t cur = (p.T - 1) / 16;
+  auto make_visit = [&](int64_t blk, uint32_t tl) {
+    VisitDesc d;
+    d.level = lvl[blk];
+    d.kp = (uint64_t)(uintptr_t)(p.arena + ko[blk]);
+    d.vp = (uint64_t)(uintptr_t)(p.arena + vo[blk]);
+    uint64_t va = 0;
+    for (int t = 0; t < 4; ++t)
+      if (tl & (1u << t)) va |= 0xFFFFull << (16 * t);
+    d.valid = va & token_mask(p.T - blk * P);
+    d.cost = balance_cost(d.level, d.valid) | (visit_counts(d.level, d.valid) << 24);
+    return d;
+  };
+  if (threadIdx.x == 0) s_cnt = p.topk;
+  __syncthreads();
+  uint64_t vbase = 0;
+  if (p.topk + 1 <= kPlanThreads) {
+    // the pages go to LDS once (lastc holds them); page i is thread i's
+    int32_t *spg = (int32_t *)lastc;
+    const int i = threadIdx.x;
+    if (i < p.topk) {
+      const int32_t v = pg[i];
+      spg[i] = v;
+      if (v < 0 || v >= cur) atomicMin(&s_cnt, i);
+    }
     __syncthreads();
+    const int cnt = s_cnt, n = cnt + 1;
+    if (i == 0) spg[cnt] = (int32_t)cur;  // the current page is always read
+    __syncthreads();
+    const int64_t blk = i < n ? spg[i] >> 2 : -1;
+    const bool start = i < n && (i == 0 || (spg[i - 1] >> 2) != blk);
+    uint64_t tot;
+    const uint64_t incl = block_scan(start ? 1 : 0, sh, tot);
+    if (start) {
+      uint32_t tl = 0;
+      for (int j = i; j < n && (spg[j] >> 2) == blk; ++j) tl |= 1u << (spg[j] & 3);
+      desc[incl - 1] = make_visit(blk, tl);
+    }
+    vbase = tot;
+  } else {
     for (int i = threadIdx.x; i < p.topk; i += kPlanThreads)
       if (pg[i] < 0 || pg[i] >= cur) atomicMin(&s_cnt, i);
     __syncthreads();
     const int cnt = s_cnt;
     const int n = cnt + 1;
-    uint64_t vbase = 0;
     for (int base = 0; base < n; base += kPlanThreads) {
       const int i = base + threadIdx.x;
       int64_t blk = -1;
@@ -1286,49 +1315,27 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
           if ((pj >> 2) != blk) break;
           tl |= 1u << (pj & 3);
         }
-        VisitDesc d;
-        d.level = lvl[blk];
-        d.kp = (uint64_t)(uintptr_t)(p.arena + ko[blk]);
-        d.vp = (uint64_t)(uintptr_t)(p.arena + vo[blk]);
-        uint64_t va = 0;
-        for (int t = 0; t < 4; ++t)
-          if (tl & (1u << t)) va |= 0xFFFFull << (16 * t);
-        d.valid = va & token_mask(p.T - blk * P);
-        d.cost = balance_cost(d.level, d.valid) | (visit_counts(d.level, d.valid) << 24);
-        desc[vbase + incl - 1] = d;
+        desc[vbase + incl - 1] = make_visit(blk, tl);
       }
       vbase += tot;
     }
-    nvis = (int64_t)vbase;
   }
+  const int64_t nvis = (int64_t)vbase;
   __syncthreads();
   if (nvis == 0) {
     for (int ww = threadIdx.x; ww <= W; ww += kPlanThreads) o.isplit[ww] = o.usplit[ww] = 0;
     return;
   }
-  // prefix cost and counts of each thread's run of visits, then the owner and the
-  // first item and unit of every visit
+  // prefix keys of each thread's run of visits, then the owner, first item and
+  // first unit of every visit
   const int64_t per = (nvis + kPlanThreads - 1) / kPlanThreads;
   const int64_t v0 = threadIdx.x * per, v1 = v0 + per < nvis ? v0 + per : nvis;
-  uint64_t mcost = 0, mcnt = 0;
-#pragma unroll 4
-  for (int64_t v = v0; v < v1; ++v) {
-    const uint32_t c = desc[v].cost;
-    mcost += c & 0xFFFFFFu;
-    mcnt += count_key(c);
-  }
-  uint64_t tcnt;
-  uint64_t ecost = block_scan(mcost, sh, o.total) - mcost;
-  uint64_t ecnt = block_scan(mcnt, sh, tcnt) - mcnt;
-  o.nitems = (uint32_t)tcnt;
-  o.nunits = (uint32_t)(tcnt >> 32);
+  uint64_t mine = 0;
+  for (int64_t v = v0; v < v1; ++v) mine += scan_key(desc[v].cost);
+  uint64_t e = block_scan(mine, sh, o.total) - mine;
   if (v0 < v1) {
-    int prev = -1;
-    if (v0 > 0) {
-      const uint32_t cp = desc[v0 - 1].cost & 0xFFFFFFu;
-      prev = midpoint_owner(W, o.W1, ecost - cp, cp, o.total);
-    }
-    for (int64_t v = v0; v < v1; ++v) place_visit(o, desc[v], v, nvis, ecost, ecnt, prev);
+    int prev = prev_owner(o, v0, e, v0 > 0 ? desc[v0 - 1].cost : 0u);
+    for (int64_t v = v0; v < v1; ++v) place_visit(o, desc[v], v, nvis, e, prev);
   }
 }
 
@@ -1418,6 +1425,7 @@ static gkv_status attn_setup(const uint16_t *q, const gkv_cache *c, const int32_
     topk = 0;
   }
   const AttnLayout L = attn_layout(c, topk);
+  if (L.vcap > 32767) return GKV_E_UNSUPPORTED;  // the plan's packed prefix sums
   if (ws_bytes < L.total) return GKV_E_WORKSPACE;
   p.q = q;
   p.level = c->level;
