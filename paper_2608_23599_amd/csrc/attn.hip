@@ -279,9 +279,10 @@ __device__ __forceinline__ int64_t uni64(int64_t x) {
 // ---------------------------------------------------------------- items and units
 // Items, in the order the consumer computes them, and the copy units they read:
 //   exact tile:   unit [K tile 4 KB], unit [V tile 4 KB]
-//   int group:    (first of a block: unit [K scale/zero | V scale/zero]), unit
-//                 [K codes of n tiles | V codes of n tiles]  (n consecutive read
-//                 tiles of one block, at most 2 KB of codes per record)
+//   int group:    (first of a block: unit [K scale/zero | V scale/zero]), then for
+//                 int2 unit [K codes of n tiles | V codes of n tiles], for int4 and
+//                 int8 unit [K codes of n tiles], unit [V codes of n tiles]  (n
+//                 consecutive read tiles of one block, at most 4 KB of codes per record)
 //   centroid:     unit [K record | V record]
 enum ItemKind { kExactTile = 0, kIntGroup = 1, kCentroid = 2 };
 
@@ -296,10 +297,11 @@ static_assert(sizeof(ItemDesc) == 16, "descriptor size");
 // Copy unit: part A (slot bytes [0, 2K)) from address a, part B ([2K, 4K)) from b.
 // In each part the first load moves n0 16-byte lanes from the part's address and
 // the second n1 lanes from the address + 1 KB; n1 = 0 stands for one lane that
-// re-reads the part's first 16 bytes, so that every unit is four loads.
+// re-reads the part's first 16 bytes, so that every unit is four loads (an empty
+// part B is one such lane at part A's address).
 struct UnitDesc {
-  uint64_t a;  // address (bits 0..47) | n0 (bits 48..55) | n1 (bits 56..63)
-  uint64_t b;  // address
+  uint64_t a;  // address (bits 0..47) | n0 (bits 48..55) | n1 (bits 56..63), part A
+  uint64_t b;  // the same for part B
 };
 static_assert(sizeof(UnitDesc) == 16, "descriptor size");
 
@@ -311,27 +313,27 @@ __device__ __forceinline__ uint32_t meta_tiles(uint32_t m) { return (m >> 9) & 1
 __device__ __forceinline__ int meta_ntiles(uint32_t m) { return (m >> 13) & 7u; }
 __device__ __forceinline__ uint32_t meta_tvalid(uint32_t m) { return m >> 16; }
 
-// Consecutive read tiles per int item: 2 KB of codes per record.
-__device__ __forceinline__ int group_tiles(int lv) { return lv == 2 ? 4 : (lv == 4 ? 2 : 1); }
+// Consecutive read tiles per int item: up to 4 KB of codes per record (int8: 2 tiles,
+// int4 and int2: a whole block).  int2 items read one unit (K codes | V codes, 2 KB
+// each); int4 and int8 items read a K unit and a V unit.
+__device__ __forceinline__ int group_tiles(int lv) { return lv == 8 ? 2 : 4; }
 
 // Issues the four loads of a unit into the slot at LDS address `slot`.
-__device__ __forceinline__ void issue_unit(uint64_t a, uint64_t b, uint32_t slot, int lane) {
+__device__ __forceinline__ void issue_part(uint64_t a, uint32_t dst, int lane) {
   const uint32_t n0 = (uint32_t)(a >> 48) & 255u, n1 = (uint32_t)(a >> 56);
   const uint8_t *pa = (const uint8_t *)(uintptr_t)(a & 0xFFFFFFFFFFFFull) + 16 * lane;
-  const uint8_t *pb = (const uint8_t *)(uintptr_t)b + 16 * lane;
-  if (n0 == 64 && n1 == 64) {
-    dma4(pa, pb, slot);
+  if ((uint32_t)lane < n0) dma16(pa, dst);
+  const uint32_t m1 = n1 ? n1 : 1u, o1 = n1 ? 1024u : 0u;
+  if ((uint32_t)lane < m1) dma16(pa + o1, dst + 1024);
+}
+__device__ __forceinline__ void issue_unit(uint64_t a, uint64_t b, uint32_t slot, int lane) {
+  if ((a >> 48) == 0x4040u && (b >> 48) == 0x4040u) {  // both parts full: 4 x 1 KB, one M0
+    dma4((const uint8_t *)(uintptr_t)(a & 0xFFFFFFFFFFFFull) + 16 * lane,
+         (const uint8_t *)(uintptr_t)(b & 0xFFFFFFFFFFFFull) + 16 * lane, slot);
     return;
   }
-  if ((uint32_t)lane < n0) {
-    dma16(pa, slot);
-    dma16(pb, slot + 2048);
-  }
-  const uint32_t m1 = n1 ? n1 : 1u, o1 = n1 ? 1024u : 0u;
-  if ((uint32_t)lane < m1) {
-    dma16(pa + o1, slot + 1024);
-    dma16(pb + o1, slot + 3072);
-  }
+  issue_part(a, slot, lane);
+  issue_part(b, slot + 2048, lane);
 }
 
 // ---------------------------------------------------------------- pipeline
@@ -459,12 +461,17 @@ __device__ __forceinline__ float rescale_factor(State &st, float bm) {
 // running maximum.  Only when some logit lies more than kRescale above it (always on
 // the first tile, with m = -inf) does the wavefront take the tile maximum over the
 // head's lanes and rescale.  Returns true when it rescaled (alpha holds the factor).
-__device__ __forceinline__ bool tile_softmax(const AttnParams &p, State &st, f4 S, bool full, uint32_t mine,
+__device__ __forceinline__ bool tile_softmax(const AttnParams &p, State &st, f4 S, uint32_t tvalid, int kg,
                                              half4 &P4, float &alpha) {
+  const bool full = tvalid == 0xFFFFu;
   float x[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) x[r] = fmaf(S[r], p.sl2, -st.m);
+  uint32_t mine = 15u;
   if (!full) {  // tokens that are not read (a uniform branch: most tiles are full)
+    uint32_t t = tvalid;
+    asm volatile("" : "+s"(t));  // keeps the mask work inside the branch
+    mine = (t >> (4 * kg)) & 15u;
 #pragma unroll
     for (int r = 0; r < 4; ++r)
       if (!(mine & (1u << r))) x[r] = kNegInf;
@@ -476,12 +483,12 @@ __device__ __forceinline__ bool tile_softmax(const AttnParams &p, State &st, f4 
     float bm = kNegInf;
 #pragma unroll
     for (int r = 0; r < 4; ++r)
-      if (full || (mine & (1u << r))) bm = vmax(bm, S[r]);
+      if (mine & (1u << r)) bm = vmax(bm, S[r]);
     alpha = rescale_factor(st, wave_max16(bm) * p.sl2);
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       x[r] = fmaf(S[r], p.sl2, -st.m);
-      if (!full && !(mine & (1u << r))) x[r] = kNegInf;
+      if (!(mine & (1u << r))) x[r] = kNegInf;
     }
   }
   P4 = half4{(_Float16)__builtin_amdgcn_exp2f(x[0]), (_Float16)__builtin_amdgcn_exp2f(x[1]),
@@ -529,11 +536,9 @@ __device__ __forceinline__ void exact_tile(const AttnParams &p, State &st, const
   f4 S = {0, 0, 0, 0};
 #pragma unroll
   for (int i = 0; i < 4; ++i) S = mfma32(a[i].h, qchunk<PACK>(qs, lane, i), S);
-  const bool full = tvalid == 0xFFFFu;
-  const uint32_t mine = (tvalid >> (4 * kg)) & 0xFu;
   half4 P4;
   float alpha;
-  tile_softmax(p, st, S, full, mine, P4, alpha);
+  tile_softmax(p, st, S, tvalid, kg, P4, alpha);
   const f4 pb = mfma16(kOnes, P4, f4{0, 0, 0, 0});
   const uint8_t *vt = pp.template pop<1>();
 #pragma unroll
@@ -660,11 +665,9 @@ __device__ __forceinline__ void int_tile(const AttnParams &p, State &st, IntBloc
     }
     S += S2;
   }
-  const bool full = tvalid == 0xFFFFu;
-  const uint32_t mine = (tvalid >> (4 * kg)) & 0xFu;
   half4 P4;
   float alpha;
-  if (tile_softmax(p, st, S, full, mine, P4, alpha)) {
+  if (tile_softmax(p, st, S, tvalid, kg, P4, alpha)) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) ib.acc[j] *= alpha;
     ib.pb *= alpha;
@@ -794,7 +797,7 @@ __device__ __forceinline__ bool int_run(const AttnParams &p, State &st, const ui
       pp.release(1);
     }
     const uint8_t *kq = pp.template pop<0>();
-    const uint8_t *vq = kq + 2048;
+    const uint8_t *vq = BITS == 2 ? kq + 2048 : pp.template pop<1>();
     const int n = meta_ntiles(meta);
     uint32_t tl = meta_tiles(meta);
 #pragma unroll 1
@@ -805,7 +808,7 @@ __device__ __forceinline__ bool int_run(const AttnParams &p, State &st, const ui
                            (uint32_t)(valid >> (16 * t)) & 0xFFFFu, mg, lane);
     }
     if (meta_last(meta)) int_epilogue<BITS>(st, ib, pp.ebuf, lane);
-    pp.release(1);
+    pp.release(BITS == 2 ? 1 : 2);
     if (!pp.next_item(meta, valid)) return false;
   } while (meta_lv(meta) == BITS);
   return true;
@@ -1042,14 +1045,19 @@ __device__ __forceinline__ uint32_t visit_counts(int lv, uint64_t valid) {
     tiles &= ~(((1u << n) - 1) << t);
     ++k;
   }
-  return k | ((k + 1) << 3);  // one unit per item and the scale/zero unit
+  return k | ((k * (lv == 2 ? 1u : 2u) + 1) << 3);  // the items' units and the scale/zero unit
 }
 
-__device__ __forceinline__ UnitDesc unit_desc(uint64_t a, uint64_t b, uint32_t bytes) {  // parts of `bytes` <= 2 KB
+// A unit of part A (ba bytes from a) and part B (bb bytes from b); each part at most
+// 2 KB, part A at least 16 bytes.
+__device__ __forceinline__ uint64_t unit_part(uint64_t a, uint32_t bytes) {
   const uint32_t n0 = (bytes < 1024 ? bytes : 1024) / 16, n1 = (bytes > 1024 ? bytes - 1024 : 0) / 16;
+  return a | ((uint64_t)n0 << 48) | ((uint64_t)n1 << 56);
+}
+__device__ __forceinline__ UnitDesc unit_desc(uint64_t a, uint32_t ba, uint64_t b, uint32_t bb) {
   UnitDesc d;
-  d.a = a | ((uint64_t)n0 << 48) | ((uint64_t)n1 << 56);
-  d.b = b;
+  d.a = unit_part(a, ba);
+  d.b = bb ? unit_part(b, bb) : unit_part(a, 16);
   return d;
 }
 
@@ -1068,7 +1076,7 @@ __device__ __forceinline__ void visit_items(const VisitDesc &v, ItemDesc *items,
   };
   if (lv == GKV_CENTROID) {
     put(0, kCentroid, true, true, tiles, 1, 0);
-    units[0] = unit_desc(v.kp, v.vp, kCentBytes);
+    units[0] = unit_desc(v.kp, kCentBytes, v.vp, kCentBytes);
     return;
   }
   int k = 0, m = 0;
@@ -1076,12 +1084,12 @@ __device__ __forceinline__ void visit_items(const VisitDesc &v, ItemDesc *items,
     for (int t = 0; t < 4; ++t)
       if ((tiles >> t) & 1u) {
         put(k++, kExactTile, true, true, 1u << t, 1, (uint32_t)((v.valid >> (16 * t)) & 0xFFFFull));
-        units[m++] = unit_desc(v.kp + 4096 * t, v.kp + 4096 * t + 2048, 2048);
-        units[m++] = unit_desc(v.vp + 4096 * t, v.vp + 4096 * t + 2048, 2048);
+        units[m++] = unit_desc(v.kp + 4096 * t, 2048, v.kp + 4096 * t + 2048, 2048);
+        units[m++] = unit_desc(v.vp + 4096 * t, 2048, v.vp + 4096 * t + 2048, 2048);
       }
     return;
   }
-  units[m++] = unit_desc(v.kp, v.vp, kSZBytes);
+  units[m++] = unit_desc(v.kp, kSZBytes, v.vp, kSZBytes);
   const int tg = group_tiles((int)lv);
   uint32_t left = tiles;
   bool first = true;
@@ -1092,8 +1100,14 @@ __device__ __forceinline__ void visit_items(const VisitDesc &v, ItemDesc *items,
     const uint32_t taken = ((1u << n) - 1) << t;
     left &= ~taken;
     put(k++, kIntGroup, first, left == 0, taken, n, 0);
-    const uint32_t off = kSZBytes + t * 256 * lv;
-    units[m++] = unit_desc(v.kp + off, v.vp + off, n * 256 * lv);
+    const uint32_t off = kSZBytes + t * 256 * lv, span = n * 256 * lv;
+    if (lv == 2) {
+      units[m++] = unit_desc(v.kp + off, span, v.vp + off, span);
+    } else {
+      const uint32_t pa = span < 2048 ? span : 2048, pb = span - pa;
+      units[m++] = unit_desc(v.kp + off, pa, v.kp + off + 2048, pb);
+      units[m++] = unit_desc(v.vp + off, pa, v.vp + off + 2048, pb);
+    }
     first = false;
   }
 }
