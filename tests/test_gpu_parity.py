@@ -291,3 +291,56 @@ def test_quest_selection_beyond_register_keys(gpu):
     kmin, kmax = oquest.page_boxes(ks[0, 0])
     want = oquest.quest_select(q_group(q, 0, 0, Hq), kmin, kmax, T, topk)
     np.testing.assert_array_equal(pages[0, 0], want)
+
+
+def test_quest_1m_sampled(gpu):
+    """Workload 5 length (T = 2^20, 65,535 ranked pages, top-256) with one KV head of
+    the workload's group size (4 query heads):
+    boxes, box-bound selection (bit-exact), attention over the selected pages
+    (against the oracle, which encodes only the blocks the read set touches), then
+    one append that opens a block and the demotions it triggers (bit-exact
+    records)."""
+    import types
+    from oracle import attention as oattn
+    T, Hq, Hkv, page, topk = 1 << 20, 4, 1, 16, 256
+    G = Hq // Hkv
+    ks, vs = kv_all(5, 1, Hkv, T + 1)
+    lv = olad.ladder("graded", T)
+    cache = _build(gpu, ks[:, :, :T], vs[:, :, :T], Hq, lv, page=page, extra_blocks=2,
+                   slack={16: 2, 8: 8, 4: 8, 2: 8, 1: 8})
+    q = synth.queries(5, 1, Hq, step=0)
+    pages = cache.quest_select(q, topk)
+    out = cache.decode(q, pages=pages).cpu().numpy()
+    pages = pages.cpu().numpy()
+    for h in range(Hkv):
+        kmin, kmax = oquest.page_boxes(ks[0, h, :T])
+        gmin, gmax = cache.boxes_host(0, h, T // page)
+        np.testing.assert_array_equal(gmin, kmin)
+        np.testing.assert_array_equal(gmax, kmax)
+        want = oquest.quest_select(q_group(q, 0, h, G), kmin, kmax, T, topk)
+        np.testing.assert_array_equal(pages[0, h], want)
+        idx = oquest.read_tokens(want, T)
+        kh = np.empty((len(idx), 128))
+        vh = np.empty((len(idx), 128))
+        for blk in np.unique(idx // 64):
+            rows = slice(blk * 64, (blk + 1) * 64)
+            sel = (idx // 64) == blk
+            kh[sel] = oquant.decode(oquant.encode_fp16(int(lv[blk]), ks[0, h, rows]))[idx[sel] - blk * 64]
+            vh[sel] = oquant.decode(oquant.encode_fp16(int(lv[blk]), vs[0, h, rows]))[idx[sel] - blk * 64]
+        ref = oattn.unit_decode(q_group(q, 0, h, G), kh, vh)
+        assert max_err(out[0, h * G:(h + 1) * G], ref) <= TOL
+    # the next token opens block 2^14: every block whose level the ladder lowers is
+    # re-encoded from its record
+    moves = cache.append(ks[:, :, T], vs[:, :, T], profile="graded")
+    lv1 = olad.ladder("graded", T + 1)
+    want_moves = sorted((h, int(i), int(lv[i]), int(lv1[i])) for h in range(Hkv)
+                        for i in range(len(lv)) if lv1[i] != lv[i])
+    assert sorted((h, blk, o, n) for b, h, blk, o, n in moves) == want_moves
+    assert moves
+    for b, h, blk, old, new in moves:
+        rows = slice(blk * 64, (blk + 1) * 64)
+        ko = oquant.demote(oquant.encode_fp16(old, ks[0, h, rows]), new)
+        vo = oquant.demote(oquant.encode_fp16(old, vs[0, h, rows]), new)
+        uc = types.SimpleNamespace(k_recs={blk: ko}, v_recs={blk: vo})
+        compare_record(cache, uc, 0, h, blk, 0)
+        compare_record(cache, uc, 0, h, blk, 1)
