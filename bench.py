@@ -160,6 +160,7 @@ def main():
     ap.add_argument("--no-phases", action="store_true", help="skip the one-off timings of the other rows")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-quest", action="store_true", help="skip the Compressed-Quest 128k point")
+    ap.add_argument("--no-1m", action="store_true", help="skip the 1M-token Compressed-Quest + demotion steps")
     ap.add_argument("--profile", action="store_true",
                     help="decode loop only, then a plain 512 MiB device copy as a counter reference")
     args = ap.parse_args()
@@ -173,7 +174,6 @@ def main():
     import numpy as np
     import torch
     from paper_2608_23599_amd import binding as gkv, synth, workloads
-    from oracle import ladder as olad, residual as ores
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -183,8 +183,8 @@ def main():
     log(f"[bench] generating {wl.name}")
     t0 = time.time()
     k, v = gen_inputs(wl.id, B, Hkv, T, dev)
-    lv = olad.ladder("graded", T)
-    nres = ores.n_keep(T, wl.rd_percent)
+    lv = gkv.ladder_levels("graded", T)
+    nres = (int(wl.rd_percent) * T) // 100  # the workload's residual fraction
     mass = np.stack([np.stack([synth.mass_unit(wl.id, b, h, T) for h in range(Hkv)]) for b in range(B)])
     mass_d = torch.from_numpy(mass).to(dev)
     log(f"[bench] inputs ready in {time.time() - t0:.1f}s; building caches")
@@ -231,7 +231,7 @@ def main():
         for _ in range(3):
             dst.copy_(src)
         torch.cuda.synchronize()
-        args.no_cpu = args.no_phases = args.no_quest = True
+        args.no_cpu = args.no_phases = args.no_quest = args.no_1m = True
 
     # parity of the benchmarked launch on one sampled unit, and the CPU baseline
     cpu = None
@@ -274,7 +274,7 @@ def main():
         del k, v
         torch.cuda.empty_cache()
         kq, vq = gen_inputs(wq.id, wq.B, wq.Hkv, wq.T, dev)
-        lvq = olad.ladder("graded", wq.T)
+        lvq = gkv.ladder_levels("graded", wq.T)
         qc = gkv.GradedCache.build(kq, vq, Hq=wq.Hq, levels=lvq, page=wq.page, device=dev)
         bms = timed(lambda: qc.page_boxes(kq, 0, wq.T // wq.page))
         qq = torch.from_numpy(synth.queries(wq.id, wq.B, wq.Hq).view(np.int16)).to(dev)
@@ -298,6 +298,50 @@ def main():
                  "achieved_GBps": round(qbytes / (ev_ms * 1e-3) / 1e9, 1),
                  "page_boxes_all_ms": round(bms, 3), "cache_copies_rotated": n}
         log(f"[bench] quest 128k: {quest['us_per_step']} us/step")
+
+    quest1m = None
+    if not args.no_1m:
+        w5 = workloads.QUEST1M
+        log(f"[bench] {w5.name}")
+        if quest is not None:
+            del copies, pages, qouts, qc, kq, vq
+        torch.cuda.empty_cache()
+        k5, v5 = gen_inputs(w5.id, w5.B, w5.Hkv, w5.T, dev)
+        c5 = gkv.GradedCache.build(k5, v5, Hq=w5.Hq, levels=gkv.ladder_levels("graded", w5.T), page=w5.page, device=dev,
+                                   extra_blocks=4, slack={L: 2 * w5.B * w5.Hkv for L in gkv.LEVELS})
+        del k5, v5
+        torch.cuda.empty_cache()
+        p5 = torch.empty((w5.B, w5.Hkv, w5.topk), dtype=torch.int32, device=dev)
+        o5 = torch.empty((w5.B, w5.Hq, 128), dtype=torch.float32, device=dev)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * w5.dynamic_steps)]
+        warm5 = 8
+        nmoves = []
+        for st in range(warm5 + w5.dynamic_steps):
+            kn, vn = synth.append_tokens(w5.id, st, w5.B, w5.Hkv)
+            qq5 = torch.from_numpy(synth.queries(w5.id, w5.B, w5.Hq, step=st).view(np.int16)).to(dev)
+            i = st - warm5
+            if i >= 0:
+                ev[2 * i].record()
+            moves = c5.append(kn, vn, profile="graded")
+            c5.quest_select(qq5, w5.topk, out=p5)
+            c5.decode(qq5, pages=p5, out=o5)
+            if i >= 0:
+                ev[2 * i + 1].record()
+                nmoves.append(len(moves))
+        torch.cuda.synchronize()
+        per5 = np.array([ev[2 * i].elapsed_time(ev[2 * i + 1]) * 1e3 for i in range(w5.dynamic_steps)])
+        r5 = c5.account(p5)
+        quest1m = {"workload": w5.name, "steps": w5.dynamic_steps, "us_per_step_median": round(float(np.median(per5)), 2),
+                   "us_per_step_mean": round(float(per5.mean()), 2), "us_per_step_max": round(float(per5.max()), 2),
+                   "demotions_in_steps": int(sum(nmoves)), "steps_with_demotion": int(sum(1 for m in nmoves if m)),
+                   "read_bpv": round(r5["read_bpv"], 4), "resident_bpv": round(r5["resident_bpv"], 4),
+                   "algorithmic_bytes": int(r5["read_bits"] / 8.0),
+                   "note": "each step: append one token per KV head (new exact block every 64 steps, boxes of "
+                           "completed pages, demotion of the blocks the ladder lowers), page selection, attention; "
+                           "event-timed including the host-side bookkeeping of the step"}
+        log(f"[bench] quest 1M: {quest1m['us_per_step_median']} us/step median")
+        del c5
+        torch.cuda.empty_cache()
 
     res = {
         "metric": METRIC,
@@ -334,6 +378,7 @@ def main():
         "cpu_baseline": cpu,
         "phases": phases,
         "quest_128k": quest,
+        "quest_1m": quest1m,
     }
     print(json.dumps(res), flush=True)
 

@@ -367,7 +367,6 @@ class GradedCache:
                        _np_ptr(nv) if nv is not None else None, _stream()), "append")
         moves = []
         if profile is not None:
-            maxj = self.units * self.nblk_cap
             jobs = np.empty(3 * 64, dtype=np.int32)
             to = np.empty(64, dtype=np.int8)
             n = _ladder_crossings(ctypes.byref(self.c), PROFILES.get(profile, profile), self.T, _np_ptr(jobs),
@@ -379,7 +378,6 @@ class GradedCache:
                 to = np.empty(n, dtype=np.int8)
                 n = _ladder_crossings(ctypes.byref(self.c), PROFILES.get(profile, profile), self.T, _np_ptr(jobs),
                                       _np_ptr(to), n)
-            del maxj
             J = jobs[: 3 * n].reshape(n, 3)
             olds = [int(self.level_host[b, h, i]) for b, h, i in J]
             self.demote([tuple(x) for x in J], to[:n])
