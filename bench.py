@@ -316,9 +316,16 @@ def main():
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * w5.dynamic_steps)]
         warm5 = 8
         nmoves = []
+        # the appended rows and the queries are device-resident before the timed steps,
+        # as a model's projections would leave them
+        steps5 = []
         for st in range(warm5 + w5.dynamic_steps):
             kn, vn = synth.append_tokens(w5.id, st, w5.B, w5.Hkv)
-            qq5 = torch.from_numpy(synth.queries(w5.id, w5.B, w5.Hq, step=st).view(np.int16)).to(dev)
+            steps5.append(tuple(torch.from_numpy(a.view(np.int16)).to(dev) for a in
+                                (kn, vn, synth.queries(w5.id, w5.B, w5.Hq, step=st))))
+        torch.cuda.synchronize()
+        for st in range(warm5 + w5.dynamic_steps):
+            kn, vn, qq5 = steps5[st]
             i = st - warm5
             if i >= 0:
                 ev[2 * i].record()

@@ -38,19 +38,22 @@ extern "C" gkv_status gkv_ladder_levels(int32_t profile, int64_t T, int8_t *lv, 
     return GKV_OK;
   }
   if (profile == 1) {
+    // block i has age r = nblk - 1 - i; each level is a contiguous range of i, and
+    // the ranges are written in increasing precedence (int2 < int4 < int8 <
+    // centroid < exact) so that a later one overrides an earlier one
     const int64_t E = 16;
     const int64_t R = nblk > E ? nblk - E : 0;
     const int64_t b8 = E + (25 * R) / 100, b4 = E + (60 * R) / 100, nc = (10 * (int64_t)nblk) / 100;
-    for (int32_t i = 0; i < nblk; ++i) {
-      const int64_t r = nblk - 1 - i;
-      int8_t v;
-      if (r < E) v = GKV_EXACT;
-      else if (i < nc) v = GKV_CENTROID;
-      else if (r < b8) v = GKV_INT8;
-      else if (r < b4) v = GKV_INT4;
-      else v = GKV_INT2;
-      lv[i] = v;
-    }
+    auto fill = [&](int64_t lo, int64_t hi, int8_t v) {
+      lo = lo < 0 ? 0 : lo;
+      hi = hi > nblk ? nblk : hi;
+      if (hi > lo) memset(lv + lo, v, (size_t)(hi - lo));
+    };
+    fill(0, nblk, GKV_INT2);
+    fill(nblk - b4, nblk, GKV_INT4);   // r < b4
+    fill(nblk - b8, nblk, GKV_INT8);   // r < b8
+    fill(0, nc, GKV_CENTROID);         // i < nc
+    fill(nblk - E, nblk, GKV_EXACT);   // r < E
     return GKV_OK;
   }
   if (profile == 2) {
@@ -73,9 +76,15 @@ extern "C" int32_t gkv_ladder_crossings(const gkv_cache *c, int32_t profile, int
   const int64_t nb_old = (c->T + P - 1) / P;
   int32_t n = 0;
   for (int b = 0; b < c->B; ++b)
-    for (int h = 0; h < c->Hkv; ++h)
+    for (int h = 0; h < c->Hkv; ++h) {
+      const int8_t *cl = c->level_host + ((int64_t)b * c->Hkv + h) * c->nblk_cap;
+      if (memcmp(cl, lv.data(), (size_t)nb_old) == 0) continue;  // the common case: nothing crosses
       for (int64_t i = 0; i < nb_old; ++i) {
-        const int cur = c->level_host[((int64_t)b * c->Hkv + h) * c->nblk_cap + i];
+        if ((i & 63) == 0 && i + 64 <= nb_old && memcmp(cl + i, lv.data() + i, 64) == 0) {
+          i += 63;  // 64 equal levels
+          continue;
+        }
+        const int cur = cl[i];
         if (lv[i] == cur) continue;
         if (level_rank(lv[i]) > level_rank(cur)) return GKV_E_NOT_MONOTONE;
         if (n < max_jobs) {
@@ -86,6 +95,7 @@ extern "C" int32_t gkv_ladder_crossings(const gkv_cache *c, int32_t profile, int
         }
         ++n;
       }
+    }
   return n;
 }
 

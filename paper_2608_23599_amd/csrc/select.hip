@@ -85,6 +85,15 @@ __global__ void __launch_bounds__(64 * G) quest_score_kernel(const uint16_t *__r
 // unit and write their indices ascending to out[0..k) (-1 padded).  Optionally
 // sets the selected tokens' bits in a per-64 mask.  One workgroup per unit.
 //
+// Long inputs are reduced in stages: the first k of the whole order all lie among
+// the first k of their own slice, so a stage splits the candidates into slices of
+// kSelKPT * kSelThreads, keeps the first k of each slice (one workgroup per slice,
+// blockIdx.x) and writes their indices slice after slice, ascending in each; the
+// candidates' order by position is then still their order by index, which is the
+// tie order.  A stage reads its keys through the previous stage's index list
+// (`idx`, null for the first), and the last stage, a single slice, writes the
+// result.
+//
 // Radix select of the threshold key (the need-th largest), 8 bits per pass, with
 // one histogram per wavefront (so that LDS atomics contend only inside a
 // wavefront); then an ordered compaction: selected = key > threshold, or key ==
@@ -195,26 +204,31 @@ __device__ __forceinline__ void small_candidates(SelShared &sh, const uint64_t *
 
 template <int KPT>
 __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__restrict__ keys, int64_t key_stride,
-                                                             int64_t n, int k, int32_t *__restrict__ out,
-                                                             int64_t out_stride, uint64_t *mask, int64_t mask_stride,
+                                                             const int32_t *__restrict__ idx, int64_t idx_stride,
+                                                             int64_t n_all, int64_t slice, int k,
+                                                             int32_t *__restrict__ out, int64_t out_stride,
+                                                             uint64_t *mask, int64_t mask_stride,
                                                              int64_t mask_words) {
   __shared__ SelShared sh;
-  const int64_t u = blockIdx.x;
+  const int64_t u = blockIdx.y, base = (int64_t)blockIdx.x * slice;
+  const int64_t n = n_all - base < slice ? n_all - base : slice;
   const uint64_t *key = keys + u * key_stride;
-  int32_t *o = out + u * out_stride;
+  const int32_t *ix = idx ? idx + u * idx_stride + base : nullptr;  // KPT > 0 only
+  int32_t *o = out + u * out_stride + (int64_t)blockIdx.x * k;
   uint64_t *mk = mask ? mask + u * mask_stride : nullptr;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   if (mk)
     for (int64_t i = tid; i < mask_words; i += kSelThreads) mk[i] = 0;
   const int64_t need = n < k ? n : k;
-  for (int64_t i = need + tid; i < k; i += kSelThreads) o[i] = -1;
+  if (gridDim.x == 1)
+    for (int64_t i = need + tid; i < k; i += kSelThreads) o[i] = -1;
   if (need == 0) return;
   uint64_t kr[KPT > 0 ? KPT : 1];
   if (KPT > 0) {
 #pragma unroll
     for (int j = 0; j < KPT; ++j) {
       const int64_t i = (int64_t)tid * KPT + j;
-      kr[j] = i < n ? key[i] : 0;
+      kr[j] = i < n ? key[ix ? (int64_t)ix[i] : base + i] : 0;
     }
   }
   // bits that differ between keys: bytes above the highest differing byte are the
@@ -339,8 +353,9 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
       if (i < n) {
         const bool sel = kr[j] > thr || (kr[j] == thr && eq++ < eq_take);
         if (sel) {
-          o[pos++] = (int32_t)i;
-          if (mk) atomicOr((unsigned long long *)&mk[i >> 6], 1ull << (i & 63));
+          const int64_t t = ix ? (int64_t)ix[i] : base + i;
+          o[pos++] = (int32_t)t;
+          if (mk) atomicOr((unsigned long long *)&mk[t >> 6], 1ull << (t & 63));
         }
       }
     }
@@ -376,14 +391,31 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
   }
 }
 
+constexpr int64_t kSelSlice = (int64_t)kSelKPT * kSelThreads;
+
+// idx_ws: two index lists of `key_stride` entries per unit (the stages' candidates).
 void launch_select(const uint64_t *keys, int64_t key_stride, int64_t n, int k, int32_t *out, int64_t out_stride,
-                   uint64_t *mask, int64_t mask_stride, int64_t mask_words, int units, hipStream_t s) {
-  if (n <= (int64_t)kSelKPT * kSelThreads)
-    hipLaunchKernelGGL(select_kernel<kSelKPT>, dim3(units), dim3(kSelThreads), 0, s, keys, key_stride, n, k, out,
-                       out_stride, mask, mask_stride, mask_words);
-  else
-    hipLaunchKernelGGL(select_kernel<0>, dim3(units), dim3(kSelThreads), 0, s, keys, key_stride, n, k, out,
-                       out_stride, mask, mask_stride, mask_words);
+                   uint64_t *mask, int64_t mask_stride, int64_t mask_words, int units, int32_t *idx_ws,
+                   hipStream_t s) {
+  if (n > kSelSlice && 2 * (int64_t)k > kSelSlice) {  // too few candidates dropped per stage: one streamed pass
+    hipLaunchKernelGGL(select_kernel<0>, dim3(1, units), dim3(kSelThreads), 0, s, keys, key_stride,
+                       (const int32_t *)nullptr, (int64_t)0, n, n, k, out, out_stride, mask, mask_stride, mask_words);
+    return;
+  }
+  const int32_t *idx = nullptr;
+  int64_t cur = n;
+  for (int buf = 0; cur > kSelSlice; buf ^= 1) {
+    const int64_t S = (cur + kSelSlice - 1) / kSelSlice;
+    int32_t *dst = idx_ws + (int64_t)buf * units * key_stride;
+    hipLaunchKernelGGL(select_kernel<kSelKPT>, dim3((unsigned)S, units), dim3(kSelThreads), 0, s, keys, key_stride,
+                       idx, key_stride, cur, kSelSlice, k, dst, key_stride, (uint64_t *)nullptr, (int64_t)0,
+                       (int64_t)0);
+    const int64_t last = cur - (S - 1) * kSelSlice;
+    cur = (S - 1) * k + (last < k ? last : k);
+    idx = dst;
+  }
+  hipLaunchKernelGGL(select_kernel<kSelKPT>, dim3(1, units), dim3(kSelThreads), 0, s, keys, key_stride, idx,
+                     key_stride, cur, cur, k, out, out_stride, mask, mask_stride, mask_words);
 }
 
 // Copy the exact key/value rows of the selected residual tokens into exact-format
@@ -420,8 +452,9 @@ __global__ void __launch_bounds__(256) res_gather_kernel(const uint16_t *__restr
 }  // namespace
 
 // ---------------------------------------------------------------- C ABI
-static int64_t quest_ws(const gkv_cache *c) { return (int64_t)c->B * c->Hkv * c->npage_cap * 8; }
-static int64_t rd_ws(const gkv_cache *c) { return (int64_t)c->B * c->Hkv * (c->T > 0 ? c->T : 1) * 8; }
+// keys (8 bytes) and two candidate index lists (4 bytes each) per ranked item
+static int64_t quest_ws(const gkv_cache *c) { return (int64_t)c->B * c->Hkv * c->npage_cap * 16; }
+static int64_t rd_ws(const gkv_cache *c) { return (int64_t)c->B * c->Hkv * (c->T > 0 ? c->T : 1) * 16; }
 
 extern "C" int64_t gkv_workspace_bytes(const gkv_cache *c, int32_t op, int32_t topk) {
   if (gkv_validate_cache(c)) return -1;
@@ -459,7 +492,9 @@ extern "C" gkv_status gkv_quest_select(const uint16_t *q, const gkv_cache *c, in
       default: return GKV_E_SHAPE;
     }
   }
-  launch_select((const uint64_t *)keys, c->npage_cap, ncur, topk, pages, (int64_t)topk, nullptr, 0, 0, c->B * c->Hkv, s);
+  int32_t *idx_ws = (int32_t *)(keys + (int64_t)c->B * c->Hkv * c->npage_cap);
+  launch_select((const uint64_t *)keys, c->npage_cap, ncur, topk, pages, (int64_t)topk, nullptr, 0, 0, c->B * c->Hkv,
+                idx_ws, s);
   return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP;
 }
 
@@ -475,8 +510,9 @@ extern "C" gkv_status gkv_rd_residual_select(gkv_cache *c, const uint16_t *k_src
   hipStream_t s = (hipStream_t)stream;
   uint64_t *keys = (uint64_t *)ws;
   if (nkeep > 0) gkv_launch_rd_score(c, v_src, mass, keys, s);
+  int32_t *idx_ws = (int32_t *)(keys + (int64_t)c->B * c->Hkv * c->T);
   launch_select((const uint64_t *)keys, c->T, c->T, nkeep, c->res_idx, (int64_t)c->nres_cap, c->res_mask,
-                (int64_t)c->nblk_cap, (int64_t)c->nblk_cap, c->B * c->Hkv, s);
+                (int64_t)c->nblk_cap, (int64_t)c->nblk_cap, c->B * c->Hkv, idx_ws, s);
   if (nkeep > 0) {
     dim3 g2((unsigned)((nkeep + P - 1) / P), c->Hkv, c->B);
     hipLaunchKernelGGL(res_gather_kernel, g2, dim3(256), 0, s, k_src, v_src, c->T, (const int32_t *)c->res_idx,

@@ -114,8 +114,8 @@ def test_quest_ties_go_to_lower_page(gpu):
 @pytest.mark.parametrize("T,Bn", [(8192, 2), (3000, 1), (9001, 1)])
 def test_rd_residual_selection_and_attention(gpu, T, Bn):
     """Workload 4 shapes at reduced length: 28 query / 4 KV heads, 2% residual by
-    attention mass x squared value error.  T = 9001 exceeds the register-resident
-    selection (8192 keys) and takes the streamed one."""
+    attention mass x squared value error.  T = 9001 exceeds one 8192-key slice and
+    is selected in two slices and a final pass."""
     Hq, Hkv = 28, 4
     ks, vs = kv_all(4, Bn, Hkv, T)
     lv = olad.ladder("graded", T)
@@ -280,8 +280,8 @@ def test_staged_attention_equals_one_call(gpu):
 
 
 def test_quest_selection_beyond_register_keys(gpu):
-    """More than 8192 ranked pages (T = 16 * 8300): the streamed selection path
-    must give the oracle's page set (selection only: the page order is index work)."""
+    """More than 8192 ranked pages (T = 16 * 8300): the selection in two slices and a
+    final pass must give the oracle's page set."""
     T, Hq, Hkv, page, topk = 16 * 8300 + 5, 4, 1, 16, 200
     ks, vs = kv_all(3, 1, Hkv, T)
     lv = olad.ladder("graded", T)
@@ -291,6 +291,45 @@ def test_quest_selection_beyond_register_keys(gpu):
     kmin, kmax = oquest.page_boxes(ks[0, 0])
     want = oquest.quest_select(q_group(q, 0, 0, Hq), kmin, kmax, T, topk)
     np.testing.assert_array_equal(pages[0, 0], want)
+
+
+@pytest.mark.parametrize("k", [1, 100, 4096, 5000])
+def test_quest_select_ties_across_slices(gpu, k):
+    """16500 ranked pages built from three page contents, so every score is shared by
+    thousands of pages and the k-th falls inside a tie: the winners must be the oracle's
+    (ties to the lower page) whether the selection runs in 8192-page slices and a final
+    pass (k <= 4096) or in one streamed pass (k = 5000)."""
+    T, Hq, Hkv, page = 16 * 16500 + 3, 4, 1, 16
+    r = np.random.default_rng(77)
+    pat = r.standard_normal((3, page, 128)).astype(np.float16).view(np.uint16)
+    which = r.integers(0, 3, size=(T + page - 1) // page)
+    ks = np.ascontiguousarray(pat[which].reshape(-1, 128)[:T])[None, None]
+    vs = np.zeros_like(ks)
+    cache = _build(gpu, ks, vs, Hq, olad.ladder("exact", T), page=page)
+    q = synth.queries(3, 1, Hq, step=3)
+    kmin, kmax = oquest.page_boxes(ks[0, 0])
+    n = (T - 1) // page
+    s = oquest.page_scores(q[0], kmin[:n], kmax[:n])
+    assert len(np.unique(s)) == 3
+    got = cache.quest_select(q, k).cpu().numpy()[0, 0]
+    np.testing.assert_array_equal(got, oquest.select_top(s, k))
+
+
+def test_rd_residual_streamed_selection(gpu):
+    """A residual of 5000 rows out of 9001 tokens (more than half of a 8192-key slice)
+    takes the single streamed selection pass; residual set and mask bit-exact."""
+    T, Hq, Hkv, n = 9001, 8, 1, 5000
+    ks, vs = kv_all(4, 1, Hkv, T)
+    lv = olad.ladder("graded", T)
+    cache = _build(gpu, ks, vs, Hq, lv, nres_cap=n)
+    mass = synth.mass_unit(4, 0, 0, T)[None, None]
+    cache.rd_residual_select(ks, vs, mass, n)
+    uc = ocache.UnitCache(ks[0, 0], vs[0, 0], lv)
+    want, _ = uc.select_residual(ks[0, 0], vs[0, 0], mass[0, 0], n)
+    np.testing.assert_array_equal(cache.res_idx.cpu().numpy()[0, 0, :n], want)
+    q = synth.queries(4, 1, Hq)
+    out = cache.decode(q).cpu().numpy()
+    assert max_err(out[0], uc.decode_dense(q_group(q, 0, 0, Hq))) <= TOL
 
 
 def test_quest_1m_sampled(gpu):
