@@ -1373,8 +1373,7 @@ static int attn_nsplit(const gkv_cache *c, int32_t topk, int64_t T) {
   return (int)((waves + kWaves - 1) / kWaves);
 }
 
-// Compute units of the current device (cached per device).
-static int device_cus() {
+int gkv_device_cus() {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1;
   static int cache[64];
@@ -1392,7 +1391,7 @@ static int device_cus() {
 // issue arbitration on their SIMDs (the older wavefront goes first) and run about a
 // fifth faster, so the split gives them more work.  Otherwise all count the same.
 static int attn_fast(int nsplit, int64_t units) {
-  const int64_t cus = device_cus(), nb = (int64_t)nsplit * units;
+  const int64_t cus = gkv_device_cus(), nb = (int64_t)nsplit * units;
   if (nb <= cus || nb > 2 * cus) return nsplit;
   return (int)(cus / units);
 }

@@ -138,3 +138,6 @@ GKV_HD double f16_to_f64(uint16_t h) {
 
 // Host-side validation shared by the call wrappers (host.cpp).
 gkv_status gkv_validate_cache(const gkv_cache *c);
+
+// Compute units of the current device (cached per device; attn.hip).
+int gkv_device_cus();

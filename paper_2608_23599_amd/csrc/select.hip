@@ -23,62 +23,82 @@ __device__ __forceinline__ uint64_t order_key(double x) {
   return (bits >> 63) ? ~bits : (bits | 0x8000000000000000ull);
 }
 
+// Query coefficients of the box bound for one (sequence, KV head) as fp64, laid out
+// [HG][D][G / HG] (head g = hg * (G / HG) + j), so that the coefficients one
+// wavefront of the score kernel reads are contiguous.  grid (Hkv, B) x 256 threads.
+__global__ void __launch_bounds__(256) quest_qtab_kernel(const uint16_t *__restrict__ q, int G, int HG, int Hkv,
+                                                         double *__restrict__ qt) {
+  const int64_t u = (int64_t)blockIdx.y * Hkv + blockIdx.x;
+  const int hpw = G / HG;
+  for (int i = threadIdx.x; i < G * D; i += 256) {
+    const int g = i / D, d = i % D;
+    const int hg = g / hpw, j = g % hpw;
+    qt[u * G * D + ((int64_t)hg * D + d) * hpw + j] = (double)__builtin_bit_cast(_Float16, q[u * G * D + i]);
+  }
+}
+
 // Box upper bound of every ranked page for the G query heads of a KV head:
 // UB_g(p) = sum_d q_gd * (q_gd >= 0 ? kmax_pd : kmin_pd), channel-ascending in fp64
 // (each product of two fp16 values is exact, so the fused multiply-add rounds once,
-// like a separate add); page score = max_g UB_g.  A workgroup covers 64 pages with one
-// wavefront per query head (lane = page); the bound of one head is one chain of 128
-// multiply-adds.  Which half of a box word a head reads depends only on the sign of
-// q_gd, so it is a shift chosen per (head, channel); for q_gd = +-0 either half gives
-// the same sum (the product is a zero and the running sum is never -0).  The heads'
-// bounds meet in LDS and the first wavefront writes the keys.  grid (ceil(npages/64),
-// Hkv, B) x 64 G threads.
-struct QCoef {
-  double q;
-  uint32_t shift, pad;
-};
-template <int G>
-__global__ void __launch_bounds__(64 * G) quest_score_kernel(const uint16_t *__restrict__ q,
-                                                             const uint16_t *__restrict__ boxes, int64_t npage_cap,
-                                                             int64_t npages, int Hkv, uint64_t *__restrict__ keys) {
-  __shared__ QCoef qc[G * D];
-  __shared__ double ub[G][64];
+// like a separate add); page score = max_g UB_g.
+//
+// One wavefront covers 64 pages (lane = page) and G / HG of the heads; a workgroup is
+// four wavefronts: 4 / HG page groups times HG head groups, whose bounds meet in LDS.
+// Both halves of a box word are widened once per wavefront and each head picks one
+// by the sign of its coefficient.  The coefficients are wavefront-uniform and come
+// from the table through the scalar cache (contiguous per wavefront, so a few wide
+// scalar loads cover many channels).  grid (ceil(npages / (64 * 4 / HG)), Hkv, B) x
+// 256 threads.
+constexpr int kScoreBatch = 32;  // box words in flight per lane
+template <int G, int HG>
+__global__ void __launch_bounds__(256) quest_score_kernel(const double *__restrict__ qt,
+                                                          const uint16_t *__restrict__ boxes, int64_t npage_cap,
+                                                          int64_t npages, int Hkv, uint64_t *__restrict__ keys) {
+  constexpr int HPW = G / HG;
+  __shared__ double ub[4][64];
   const int h = blockIdx.y, b = blockIdx.z;
   const int64_t u = (int64_t)b * Hkv + h;
-  for (int i = threadIdx.x; i < G * D; i += 64 * G) {
-    const uint16_t bits = q[u * G * D + i];
-    qc[i].q = (double)__builtin_bit_cast(_Float16, bits);
-    qc[i].shift = (bits & 0x8000u) ? 0u : 16u;  // kmin in the low half, kmax in the high
-  }
-  __syncthreads();
-  const int g = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t pg = (int64_t)blockIdx.x * 64 + lane;
+  const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)), lane = threadIdx.x & 63;
+  const int hg = w % HG;
+  const int64_t pg0 = ((int64_t)blockIdx.x * (4 / HG) + w / HG) * 64;
+  const int64_t pg = pg0 + lane;
   const bool on = pg < npages;
-  const uint32_t *bx = (const uint32_t *)(boxes + u * npage_cap * 2 * D) + (on ? box_index(pg, 0) >> 1 : 0);
-  const QCoef *qg = qc + g * D;
-  double acc = 0.0;
-  // 64 channels' box words are loaded before they are used (independent loads in
-  // flight; two batches keep the registers low enough for every wavefront of the
-  // grid to be resident); the accumulation stays channel-ascending
-  for (int d0 = 0; d0 < D; d0 += 64) {
-    uint32_t pr[64];
+  double best = 0.0;
+  if (pg0 < npages) {
+    // the whole 64-page group lies inside the box capacity (a multiple of 64 pages),
+    // so every lane loads; lanes past the ranked pages drop their result
+    const uint32_t *bx = (const uint32_t *)(boxes + u * npage_cap * 2 * D) + (box_index(pg0, 0) >> 1) + lane;
+    const double *qu = qt + u * G * D + (int64_t)hg * D * HPW;
+    double acc[HPW];
 #pragma unroll
-    for (int e = 0; e < 64; ++e) pr[e] = on ? bx[(d0 + e) * 64] : 0u;
+    for (int j = 0; j < HPW; ++j) acc[j] = 0.0;
+    for (int d0 = 0; d0 < D; d0 += kScoreBatch) {
+      uint32_t pr[kScoreBatch];
 #pragma unroll
-    for (int e = 0; e < 64; ++e) {
-      const QCoef c = qg[d0 + e];
-      const double x = (double)__builtin_bit_cast(_Float16, (uint16_t)(pr[e] >> c.shift));
-      acc = __builtin_fma(c.q, x, acc);
+      for (int e = 0; e < kScoreBatch; ++e) pr[e] = bx[(d0 + e) * 64];
+#pragma unroll
+      for (int e = 0; e < kScoreBatch; ++e) {
+        const double lo = (double)(float)__builtin_bit_cast(_Float16, (uint16_t)pr[e]);          // kmin
+        const double hi = (double)(float)__builtin_bit_cast(_Float16, (uint16_t)(pr[e] >> 16));  // kmax
+#pragma unroll
+        for (int j = 0; j < HPW; ++j) {
+          const double qq = qu[(d0 + e) * HPW + j];
+          acc[j] = __builtin_fma(qq, qq >= 0.0 ? hi : lo, acc[j]);
+        }
+      }
     }
-  }
-  ub[g][lane] = acc;
-  __syncthreads();
-  if (g == 0 && on) {
-    double best = ub[0][lane];
+    best = acc[0];
 #pragma unroll
-    for (int j = 1; j < G; ++j) best = ub[j][lane] > best ? ub[j][lane] : best;
-    keys[u * npage_cap + pg] = order_key(best);
+    for (int j = 1; j < HPW; ++j) best = acc[j] > best ? acc[j] : best;
   }
+  if (HG > 1) {
+    ub[w][lane] = best;
+    __syncthreads();
+    if (hg != 0) return;
+#pragma unroll
+    for (int j = 1; j < HG; ++j) best = ub[w + j][lane] > best ? ub[w + j][lane] : best;
+  }
+  if (on) keys[u * npage_cap + pg] = order_key(best);
 }
 
 // Select the first k of the order (key desc, index asc) among keys[0..n) of one
@@ -452,8 +472,11 @@ __global__ void __launch_bounds__(256) res_gather_kernel(const uint16_t *__restr
 }  // namespace
 
 // ---------------------------------------------------------------- C ABI
-// keys (8 bytes) and two candidate index lists (4 bytes each) per ranked item
-static int64_t quest_ws(const gkv_cache *c) { return (int64_t)c->B * c->Hkv * c->npage_cap * 16; }
+// keys (8 bytes) and two candidate index lists (4 bytes each) per ranked item; Quest
+// adds the fp64 query-coefficient table, G x D per (b,h)
+static int64_t quest_ws(const gkv_cache *c) {
+  return (int64_t)c->B * c->Hkv * (c->npage_cap * 16 + (int64_t)D * (c->Hq / c->Hkv) * 8);
+}
 static int64_t rd_ws(const gkv_cache *c) { return (int64_t)c->B * c->Hkv * (c->T > 0 ? c->T : 1) * 16; }
 
 extern "C" int64_t gkv_workspace_bytes(const gkv_cache *c, int32_t op, int32_t topk) {
@@ -477,17 +500,28 @@ extern "C" gkv_status gkv_quest_select(const uint16_t *q, const gkv_cache *c, in
   if (ncur > c->npage_cap) return GKV_E_SHAPE;
   hipStream_t s = (hipStream_t)stream;
   uint64_t *keys = (uint64_t *)ws;
+  const int64_t units = (int64_t)c->B * c->Hkv;
+  double *qt = (double *)((int32_t *)(keys + units * c->npage_cap) + 2 * units * c->npage_cap);
   if (ncur > 0) {
-    dim3 grid((unsigned)((ncur + 63) / 64), c->Hkv, c->B);
-    switch (G) {
-#define GKV_SCORE(g)                                                                                           \
-  case g:                                                                                                      \
-    hipLaunchKernelGGL(quest_score_kernel<g>, grid, dim3(64 * g), 0, s, q, c->boxes, c->npage_cap, ncur, c->Hkv, \
-                       keys);                                                                                  \
+    // head groups per page group: two where the head count allows, four when that
+    // still leaves fewer than 16 wavefronts per compute unit
+    const int64_t groups = units * ((ncur + 63) / 64);
+    int HG = 1;
+    while (HG < 4 && G % (2 * HG) == 0 && (HG == 1 || groups * HG < 16 * (int64_t)gkv_device_cus())) HG *= 2;
+    const int per = 4 / HG;  // page groups per workgroup
+    dim3 grid((unsigned)(((ncur + 63) / 64 + per - 1) / per), c->Hkv, c->B);
+    hipLaunchKernelGGL(quest_qtab_kernel, dim3(c->Hkv, c->B), dim3(256), 0, s, q, G, HG, c->Hkv, qt);
+    switch (G * 4 + HG - 1) {
+#define GKV_SCORE(g, hg)                                                                                   \
+  case g * 4 + hg - 1:                                                                                     \
+    hipLaunchKernelGGL((quest_score_kernel<g, hg>), grid, dim3(256), 0, s, (const double *)qt, c->boxes,  \
+                       c->npage_cap, ncur, c->Hkv, keys);                                                  \
     break;
-      GKV_SCORE(1) GKV_SCORE(2) GKV_SCORE(3) GKV_SCORE(4) GKV_SCORE(5) GKV_SCORE(6) GKV_SCORE(7) GKV_SCORE(8)
-      GKV_SCORE(9) GKV_SCORE(10) GKV_SCORE(11) GKV_SCORE(12) GKV_SCORE(13) GKV_SCORE(14) GKV_SCORE(15)
-      GKV_SCORE(16)
+      GKV_SCORE(1, 1) GKV_SCORE(3, 1) GKV_SCORE(5, 1) GKV_SCORE(7, 1) GKV_SCORE(9, 1) GKV_SCORE(11, 1)
+      GKV_SCORE(13, 1) GKV_SCORE(15, 1)
+      GKV_SCORE(2, 2) GKV_SCORE(4, 2) GKV_SCORE(6, 2) GKV_SCORE(8, 2) GKV_SCORE(10, 2) GKV_SCORE(12, 2)
+      GKV_SCORE(14, 2) GKV_SCORE(16, 2)
+      GKV_SCORE(4, 4) GKV_SCORE(8, 4) GKV_SCORE(12, 4) GKV_SCORE(16, 4)
 #undef GKV_SCORE
       default: return GKV_E_SHAPE;
     }

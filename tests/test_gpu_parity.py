@@ -293,6 +293,23 @@ def test_quest_selection_beyond_register_keys(gpu):
     np.testing.assert_array_equal(pages[0, 0], want)
 
 
+@pytest.mark.parametrize("G", [1, 2, 3, 6, 8, 16])
+def test_quest_selection_per_group_size(gpu, G):
+    """Page sets for GQA group sizes 1..16: the scoring splits a group's heads over one,
+    two or four wavefronts depending on the size, and each split must give the oracle's
+    pages (ties to the lower page)."""
+    T, Hkv, page, topk = 4001, 2, 16, 40
+    Hq = G * Hkv
+    ks, vs = kv_all(3, 1, Hkv, T)
+    cache = _build(gpu, ks, vs, Hq, olad.ladder("graded", T), page=page)
+    q = synth.queries(3, 1, Hq, step=G)
+    pages = cache.quest_select(q, topk).cpu().numpy()
+    for h in range(Hkv):
+        kmin, kmax = oquest.page_boxes(ks[0, h])
+        want = oquest.quest_select(q_group(q, 0, h, G), kmin, kmax, T, topk)
+        np.testing.assert_array_equal(pages[0, h], want)
+
+
 @pytest.mark.parametrize("k", [1, 100, 4096, 5000])
 def test_quest_select_ties_across_slices(gpu, k):
     """16500 ranked pages built from three page contents, so every score is shared by
