@@ -496,6 +496,52 @@ __device__ __forceinline__ bool tile_softmax(const AttnParams &p, State &st, f4 
   return resc;
 }
 
+// Probabilities of two tiles of one block at once (this lane's 4 token rows of its
+// head in each), with one rescale decision for the pair: P8 holds tile A's rows in
+// elements 0..3 and tile B's in 4..7.
+__device__ __forceinline__ bool pair_softmax(const AttnParams &p, State &st, f4 SA, f4 SB, uint32_t tvA,
+                                             uint32_t tvB, int kg, half8 &P8, float &alpha) {
+  const bool full = (tvA & tvB) == 0xFFFFu;
+  float x[8];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    x[r] = fmaf(SA[r], p.sl2, -st.m);
+    x[4 + r] = fmaf(SB[r], p.sl2, -st.m);
+  }
+  uint32_t mine = 0xFFu;
+  if (!full) {  // tokens that are not read (a uniform branch: most pairs are full)
+    uint32_t a = tvA, b = tvB;
+    asm volatile("" : "+s"(a), "+s"(b));  // keeps the mask work inside the branch
+    mine = ((a >> (4 * kg)) & 15u) | (((b >> (4 * kg)) & 15u) << 4);
+#pragma unroll
+    for (int r = 0; r < 8; ++r)
+      if (!(mine & (1u << r))) x[r] = kNegInf;
+  }
+  const bool big = vmax(vmax(vmax(x[0], x[1]), vmax(x[2], x[3])), vmax(vmax(x[4], x[5]), vmax(x[6], x[7]))) > kRescale;
+  const bool resc = __any(big);
+  alpha = 1.0f;
+  if (resc) {
+    float bm = kNegInf;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      if (mine & (1u << r)) bm = vmax(bm, SA[r]);
+      if (mine & (1u << (4 + r))) bm = vmax(bm, SB[r]);
+    }
+    alpha = rescale_factor(st, wave_max16(bm) * p.sl2);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      x[r] = fmaf(SA[r], p.sl2, -st.m);
+      x[4 + r] = fmaf(SB[r], p.sl2, -st.m);
+    }
+#pragma unroll
+    for (int r = 0; r < 8; ++r)
+      if (!(mine & (1u << r))) x[r] = kNegInf;
+  }
+#pragma unroll
+  for (int r = 0; r < 8; ++r) P8[r] = (_Float16)__builtin_amdgcn_exp2f(x[r]);
+  return resc;
+}
+
 __device__ __forceinline__ uint4 lds16(const uint8_t *a) { return *(const uint4 *)a; }
 
 // The group's queries live in LDS, one 272-byte row per head (padded against bank
@@ -522,6 +568,8 @@ __device__ __forceinline__ f4 add_row_half(f4 x) {
 }
 
 constexpr half4 kOnes = half4{(_Float16)1, (_Float16)1, (_Float16)1, (_Float16)1};
+constexpr half8 kOnes8 = half8{(_Float16)1, (_Float16)1, (_Float16)1, (_Float16)1,
+                               (_Float16)1, (_Float16)1, (_Float16)1, (_Float16)1};
 
 // ---------------------------------------------------------------- items
 // Exact block tile: 16 tokens of fp16 K and V.
@@ -571,13 +619,13 @@ __device__ __forceinline__ void int_header(IntBlock &ib, const uint8_t *qs, cons
     sK[i].v = lds16(ip + kg * 64 + 16 * i);
     zK[i].v = lds16(ip + 256 + kg * 64 + 16 * i);
   }
-  // q * s as two fp16 terms hi + lo (q * s and q * s - hi are exact in fp32)
+  // q * s as two fp16 terms hi + lo: hi = fp16(q * s), lo = fp16(q * s - hi).  The
+  // fused fp16 multiply-add rounds the exact q * s - hi once, so two packed
+  // instructions give both terms of two channels
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     ib.qh[i] = qB[i] * sK[i].h;
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      ib.ql[i][e] = (_Float16)__builtin_fmaf((float)qB[i][e], (float)sK[i].h[e], -(float)ib.qh[i][e]);
+    ib.ql[i] = __builtin_elementwise_fma(qB[i], sK[i].h, -ib.qh[i]);
   }
   f4 c0 = {0, 0, 0, 0};
   if (PACK) {
@@ -613,36 +661,25 @@ __device__ __forceinline__ void int_header(IntBlock &ib, const uint8_t *qs, cons
   ib.pb = f4{0, 0, 0, 0};
 }
 
-// One 16-token tile of an int block: key codes at kt, value codes at vt (LDS).
-template <int BITS, bool PACK>
-__device__ __forceinline__ void int_tile(const AttnParams &p, State &st, IntBlock &ib, const uint8_t *kt,
-                                         const uint8_t *vt, uint32_t tvalid, const Mag &mg, int lane) {
+// This lane's code words of one tile (LDS).
+template <int BITS>
+__device__ __forceinline__ void tile_words(const uint8_t *c, uint32_t *w) {
   constexpr int NW = Unpack<BITS>::kWords;
-  const int kg = lane >> 4;
-  const uint8_t *kc = kt + lane * (4 * BITS);
-  const uint8_t *vc = vt + lane * (4 * BITS);
-  uint32_t kw[NW];
   if (NW >= 4) {
 #pragma unroll
     for (int q = 0; q < NW; q += 4) {
-      const uint4 a = lds16(kc + 4 * q);
-      kw[q] = a.x; kw[q + 1] = a.y; kw[q + 2] = a.z; kw[q + 3] = a.w;
+      const uint4 a = lds16(c + 4 * q);
+      w[q] = a.x; w[q + 1] = a.y; w[q + 2] = a.z; w[q + 3] = a.w;
     }
   } else {
-    const uint2 a = *(const uint2 *)kc;
-    kw[0] = a.x; kw[1] = a.y;
+    const uint2 a = *(const uint2 *)c;
+    w[0] = a.x; w[1] = a.y;
   }
-  uint32_t vw[NW];  // value codes, read now so that the softmax hides the latency
-  if (NW >= 4) {
-#pragma unroll
-    for (int q = 0; q < NW; q += 4) {
-      const uint4 a = lds16(vc + 4 * q);
-      vw[q] = a.x; vw[q + 1] = a.y; vw[q + 2] = a.z; vw[q + 3] = a.w;
-    }
-  } else {
-    const uint2 a = *(const uint2 *)vc;
-    vw[0] = a.x; vw[1] = a.y;
-  }
+}
+
+// Logits of one tile of an int block from its key code words.
+template <int BITS, bool PACK>
+__device__ __forceinline__ f4 int_logits(const IntBlock &ib, const uint32_t *kw, const Mag &mg) {
   f4 S = ib.c0;
   if (PACK) {  // one chain: high terms in columns 0..7, low terms in 8..15
 #pragma unroll
@@ -665,6 +702,19 @@ __device__ __forceinline__ void int_tile(const AttnParams &p, State &st, IntBloc
     }
     S += S2;
   }
+  return S;
+}
+
+// One 16-token tile of an int block: key codes at kt, value codes at vt (LDS).
+template <int BITS, bool PACK>
+__device__ __forceinline__ void int_tile(const AttnParams &p, State &st, IntBlock &ib, const uint8_t *kt,
+                                         const uint8_t *vt, uint32_t tvalid, const Mag &mg, int lane) {
+  constexpr int NW = Unpack<BITS>::kWords;
+  const int kg = lane >> 4;
+  uint32_t kw[NW], vw[NW];  // value codes read now so that the softmax hides the latency
+  tile_words<BITS>(kt + lane * (4 * BITS), kw);
+  tile_words<BITS>(vt + lane * (4 * BITS), vw);
+  const f4 S = int_logits<BITS, PACK>(ib, kw, mg);
   half4 P4;
   float alpha;
   if (tile_softmax(p, st, S, tvalid, kg, P4, alpha)) {
@@ -676,6 +726,42 @@ __device__ __forceinline__ void int_tile(const AttnParams &p, State &st, IntBloc
 #pragma unroll
   for (int j = 0; j < 8; ++j)
     ib.acc[j] = mfma16(as_h4(Unpack<BITS>::pair(vw, 2 * j, mg), Unpack<BITS>::pair(vw, 2 * j + 1, mg)), P4, ib.acc[j]);
+}
+
+// Two consecutive tiles of an int block (tile B's codes follow tile A's).  P.V runs
+// as one 32-deep MFMA per channel group: the contraction index k = 8 kg + e takes
+// tile A's token 4 kg + e for e < 4 and tile B's token 4 kg + e - 4 for e >= 4, in
+// both operands, so each lane's operands are its own registers of the two tiles.
+template <int BITS, bool PACK>
+__device__ __forceinline__ void int_tile2(const AttnParams &p, State &st, IntBlock &ib, const uint8_t *kt,
+                                          const uint8_t *vt, uint32_t tvA, uint32_t tvB, const Mag &mg, int lane) {
+  constexpr int NW = Unpack<BITS>::kWords;
+  constexpr int TB = 256 * BITS;  // code bytes of one tile and tensor
+  const int kg = lane >> 4;
+  uint32_t kwA[NW], kwB[NW], vwA[NW], vwB[NW];
+  tile_words<BITS>(kt + lane * (4 * BITS), kwA);
+  tile_words<BITS>(kt + TB + lane * (4 * BITS), kwB);
+  tile_words<BITS>(vt + lane * (4 * BITS), vwA);
+  tile_words<BITS>(vt + TB + lane * (4 * BITS), vwB);
+  const f4 SA = int_logits<BITS, PACK>(ib, kwA, mg);
+  const f4 SB = int_logits<BITS, PACK>(ib, kwB, mg);
+  half8 P8;
+  float alpha;
+  if (pair_softmax(p, st, SA, SB, tvA, tvB, kg, P8, alpha)) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) ib.acc[j] *= alpha;
+    ib.pb *= alpha;
+  }
+  ib.pb = mfma32(kOnes8, P8, ib.pb);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    U8 a;
+    a.u[0] = Unpack<BITS>::pair(vwA, 2 * j, mg);
+    a.u[1] = Unpack<BITS>::pair(vwA, 2 * j + 1, mg);
+    a.u[2] = Unpack<BITS>::pair(vwB, 2 * j, mg);
+    a.u[3] = Unpack<BITS>::pair(vwB, 2 * j + 1, mg);
+    ib.acc[j] = mfma32(a.h, P8, ib.acc[j]);
+  }
 }
 
 // End of an int block: O[d][h] += s_d * (acc - off * sum p) + z_d * sum p,
@@ -800,13 +886,20 @@ __device__ __forceinline__ bool int_run(const AttnParams &p, State &st, const ui
     const uint8_t *vq = BITS == 2 ? kq + 2048 : pp.template pop<1>();
     const int n = meta_ntiles(meta);
     uint32_t tl = meta_tiles(meta);
+    int j = 0;
 #pragma unroll 1
-    for (int j = 0; j < n; ++j) {
-      const int t = __builtin_ctz(tl);
+    for (; j + 1 < n; j += 2) {  // tiles in pairs
+      const int ta = __builtin_ctz(tl);
       tl &= tl - 1;
-      int_tile<BITS, PACK>(p, st, ib, kq + j * 256 * BITS, vq + j * 256 * BITS,
-                           (uint32_t)(valid >> (16 * t)) & 0xFFFFu, mg, lane);
+      const int tb = __builtin_ctz(tl);
+      tl &= tl - 1;
+      int_tile2<BITS, PACK>(p, st, ib, kq + j * 256 * BITS, vq + j * 256 * BITS,
+                            (uint32_t)(valid >> (16 * ta)) & 0xFFFFu, (uint32_t)(valid >> (16 * tb)) & 0xFFFFu, mg,
+                            lane);
     }
+    if (j < n)
+      int_tile<BITS, PACK>(p, st, ib, kq + j * 256 * BITS, vq + j * 256 * BITS,
+                           (uint32_t)(valid >> (16 * __builtin_ctz(tl))) & 0xFFFFu, mg, lane);
     if (meta_last(meta)) int_epilogue<BITS>(st, ib, pp.ebuf, lane);
     pp.release(BITS == 2 ? 1 : 2);
     if (!pp.next_item(meta, valid)) return false;
@@ -986,8 +1079,8 @@ static_assert(sizeof(VisitDesc) == 32, "descriptor size");
 // its SIMD (about 8 cycles per unit).  Exact tiles are bound by the wavefront's
 // share of the bandwidth (8 KB each), int tiles by the dequantisation and softmax
 // work rather than by their bytes.
-constexpr uint32_t kCostExactTile = 510, kCostInt8Tile = 450, kCostInt4Tile = 305, kCostInt2Tile = 232,
-                   kCostCentroid = 590, kCostIntBlock = 248;
+constexpr uint32_t kCostExactTile = 523, kCostInt8Tile = 426, kCostInt4Tile = 305, kCostInt2Tile = 260,
+                   kCostCentroid = 711, kCostIntBlock = 248;
 
 __device__ __forceinline__ uint32_t balance_cost(int lv, uint64_t va) {
   uint32_t tiles = 0;
@@ -1137,13 +1230,15 @@ __device__ __forceinline__ VisitDesc dense_visit(const AttnParams &p, int64_t u,
 // (every operand is an integer below 2^53, and the floor of a monotone quotient
 // keeps the owners non-decreasing along the visits).
 // The first W1 wavefronts (those of the workgroups dispatched first, which win the
-// issue arbitration against the later ones on their SIMDs) get 6 capacity units,
-// the others 5.
+// issue arbitration against the later ones on their SIMDs) get kFastCap capacity
+// units, the others kSlowCap (measured: 1.28 times the work in the same time).
+constexpr double kFastCap = 23.0, kSlowCap = 18.0;
 __device__ __forceinline__ int midpoint_owner(int W, int W1, uint64_t e, uint32_t c, uint64_t total) {
   if (!total) return 0;
-  const double cap = 6.0 * W1 + 5.0 * (W - W1);
+  const double cap = kFastCap * W1 + kSlowCap * (W - W1);
   const double x = ((double)(2 * e + c) * cap) / (2.0 * (double)total);
-  const double o = x < 6.0 * W1 ? __builtin_floor(x / 6.0) : W1 + __builtin_floor((x - 6.0 * W1) / 5.0);
+  const double o = x < kFastCap * W1 ? __builtin_floor(x / kFastCap)
+                                     : W1 + __builtin_floor((x - kFastCap * W1) / kSlowCap);
   return o < (double)W ? (int)o : W - 1;
 }
 
