@@ -124,6 +124,7 @@ constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
 
 constexpr int kSelKPT = 8;  // keys per thread held in registers (n <= 8192)
+constexpr int kSelRank = 16;  // candidates ranked directly instead of another radix pass (<= 64)
 
 struct SelShared {
   uint32_t hist[kSelWaves][256];
@@ -133,17 +134,53 @@ struct SelShared {
   int64_t base[2];
 };
 
+// Wavefront scans and reductions of 32-bit values by DPP row shifts within each row
+// of 16 lanes and row broadcasts between rows (lane 63 ends with the total).
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t dpp_add(uint32_t x) {
+  return x + (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, ROWS, 0xF, true);
+}
+__device__ __forceinline__ uint32_t wave_scan(uint32_t x) {  // inclusive, lane order
+  x = dpp_add<0x111, 0xF>(x);  // row_shr:1
+  x = dpp_add<0x112, 0xF>(x);  // row_shr:2
+  x = dpp_add<0x114, 0xF>(x);  // row_shr:4
+  x = dpp_add<0x118, 0xF>(x);  // row_shr:8
+  x = dpp_add<0x142, 0xA>(x);  // row_bcast:15 into rows 1, 3
+  x = dpp_add<0x143, 0xC>(x);  // row_bcast:31 into rows 2, 3
+  return x;
+}
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t dpp_or(uint32_t x) {
+  return x | (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, ROWS, 0xF, true);
+}
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t dpp_and(uint32_t x) {  // lanes without a source keep all ones
+  return x & (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)x, CTRL, ROWS, 0xF, false);
+}
+__device__ __forceinline__ uint32_t wave_or(uint32_t x) {
+  x = dpp_or<0x111, 0xF>(x);
+  x = dpp_or<0x112, 0xF>(x);
+  x = dpp_or<0x114, 0xF>(x);
+  x = dpp_or<0x118, 0xF>(x);
+  x = dpp_or<0x142, 0xA>(x);
+  x = dpp_or<0x143, 0xC>(x);
+  return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
+}
+__device__ __forceinline__ uint32_t wave_and(uint32_t x) {
+  x = dpp_and<0x111, 0xF>(x);
+  x = dpp_and<0x112, 0xF>(x);
+  x = dpp_and<0x114, 0xF>(x);
+  x = dpp_and<0x118, 0xF>(x);
+  x = dpp_and<0x142, 0xA>(x);
+  x = dpp_and<0x143, 0xC>(x);
+  return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
+}
+
 // Exclusive scan of (a, b) over the workgroup in thread order; returns the totals.
+// Counts of one pass fit in 32 bits (at most 8192 keys per workgroup pass).
 __device__ __forceinline__ void scan2(SelShared &sh, int64_t &a, int64_t &b, int64_t &ta, int64_t &tb) {
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  int64_t x = a, y = b;
-  for (int o = 1; o < 64; o <<= 1) {
-    const int64_t px = __shfl_up(x, o), py = __shfl_up(y, o);
-    if (lane >= o) {
-      x += px;
-      y += py;
-    }
-  }
+  const int64_t x = wave_scan((uint32_t)a), y = wave_scan((uint32_t)b);
   if (lane == 63) {
     sh.wsum[wv][0] = x;
     sh.wsum[wv][1] = y;
@@ -164,7 +201,7 @@ __device__ __forceinline__ void scan2(SelShared &sh, int64_t &a, int64_t &b, int
   __syncthreads();
 }
 
-// The keys that match the current prefix (at most 64) are gathered into LDS and
+// The keys that match the current prefix (at most kSelRank) are gathered into LDS and
 // ranked exactly by (key descending, index ascending) in one wavefront; the key of
 // rank remaining - 1 becomes the threshold and `remaining` the number of keys equal
 // to it still to take.  Leaves the workgroup synchronised.
@@ -205,9 +242,10 @@ __device__ __forceinline__ void small_candidates(SelShared &sh, const uint64_t *
     const uint64_t mk = in ? ckey[lane] : 0;
     const int32_t mi = in ? cidx[lane] : 0;
     int rank = 0;
-    for (int j = 0; j < nc; ++j) {
-      const uint64_t kj = __shfl(mk, j);
-      const int32_t ij = __shfl(mi, j);
+    for (int j = 0; j < nc; ++j) {  // j is uniform: lane reads, not shuffles
+      const uint64_t kj = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(mk >> 32), j) << 32) |
+                          (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)mk, j);
+      const int32_t ij = __builtin_amdgcn_readlane(mi, j);
       rank += kj > mk || (kj == mk && ij < mi);
     }
     const bool thr_lane = in && rank == (int)rem - 1;
@@ -268,10 +306,8 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
       kor |= kv;
     }
   }
-  for (int o2 = 32; o2 > 0; o2 >>= 1) {
-    kand &= __shfl_xor(kand, o2);
-    kor |= __shfl_xor(kor, o2);
-  }
+  kand = ((uint64_t)wave_and((uint32_t)(kand >> 32)) << 32) | wave_and((uint32_t)kand);
+  kor = ((uint64_t)wave_or((uint32_t)(kor >> 32)) << 32) | wave_or((uint32_t)kor);
   if (lane == 0) {
     sh.wsum[wv][0] = (int64_t)kand;
     sh.wsum[wv][1] = (int64_t)kor;
@@ -284,30 +320,31 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
       b |= (uint64_t)sh.wsum[q][1];
     }
     const uint64_t diff = a ^ b;
-    const int top = diff ? (63 - __builtin_clzll(diff)) / 8 : -1;  // highest differing byte
-    const uint64_t known = top >= 7 ? 0ull : (~0ull << (8 * (top + 1)));
+    const int hb = diff ? 63 - __builtin_clzll(diff) : -1;  // highest differing bit
+    const uint64_t known = hb >= 63 ? 0ull : (~0ull << (hb + 1));
     sh.prefix = a & known;
     sh.pmask = known;
     sh.remaining = need;
-    sh.base[0] = top;
+    sh.base[0] = hb;
   }
-  __syncthreads();
-  const int first_pass = 7 - (int)sh.base[0];
   for (int i = tid; i < kSelWaves * 256; i += kSelThreads) (&sh.hist[0][0])[i] = 0;
   __syncthreads();
-  for (int pass = first_pass; pass < 8; ++pass) {
-    const int shift = 56 - 8 * pass;
+  // digits of up to 8 bits from the highest differing bit down (the first digit
+  // spreads the keys over all its buckets)
+  for (int top = (int)sh.base[0]; top >= 0; top -= 8) {
+    const int shift = top >= 7 ? top - 7 : 0;
+    const uint64_t dmask = (2ull << (top - shift)) - 1;
     const uint64_t pre = sh.prefix, pm = sh.pmask;
     if (KPT > 0) {
 #pragma unroll
       for (int j = 0; j < KPT; ++j) {
         const int64_t i = (int64_t)tid * KPT + j;
-        if (i < n && (kr[j] & pm) == pre) atomicAdd(&sh.hist[wv][(kr[j] >> shift) & 255u], 1u);
+        if (i < n && (kr[j] & pm) == pre) atomicAdd(&sh.hist[wv][(kr[j] >> shift) & dmask], 1u);
       }
     } else {
       for (int64_t i = tid; i < n; i += kSelThreads) {
         const uint64_t kv = key[i];
-        if ((kv & pm) == pre) atomicAdd(&sh.hist[wv][(kv >> shift) & 255u], 1u);
+        if ((kv & pm) == pre) atomicAdd(&sh.hist[wv][(kv >> shift) & dmask], 1u);
       }
     }
     __syncthreads();
@@ -325,11 +362,8 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
         }
       }
       const uint32_t mine = c[0] + c[1] + c[2] + c[3];
-      uint32_t incl = mine;  // sum over lanes >= this lane
-      for (int o2 = 1; o2 < 64; o2 <<= 1) {
-        const uint32_t y = __shfl_down(incl, o2);
-        if (lane + o2 < 64) incl += y;
-      }
+      const uint32_t pref = wave_scan(mine);  // sum over lanes <= this lane
+      const uint32_t incl = (uint32_t)__builtin_amdgcn_readlane((int)pref, 63) - pref + mine;  // lanes >= this one
       const int64_t rem = sh.remaining;
       uint32_t suf[5];  // suffix at digits 4l .. 4l+4
       suf[4] = incl - mine;
@@ -343,12 +377,12 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
         const int dig = 4 * lane + hit;
         sh.remaining = rem - suf[hit + 1];
         sh.prefix = pre | ((uint64_t)dig << shift);
-        sh.pmask = pm | (0xFFull << shift);
+        sh.pmask = pm | (dmask << shift);
         sh.base[1] = c[hit];  // keys in the chosen digit's bucket
       }
     }
     __syncthreads();
-    if (pass < 7 && sh.base[1] <= 64) {  // few candidates left: rank them in one wavefront
+    if (shift > 0 && sh.base[1] <= kSelRank) {  // few candidates left: rank them in one wavefront
       small_candidates<KPT>(sh, kr, key, n);
       break;
     }
