@@ -1096,29 +1096,56 @@ __device__ __forceinline__ uint64_t token_mask(int64_t left) {  // tokens of a b
   return left >= P ? ~0ull : ((1ull << left) - 1);
 }
 
-// Inclusive scan over the workgroup; `total` receives the sum over all threads.
+// Wavefront inclusive scan of a 32-bit value in lane order: DPP row shifts within
+// each row of 16 lanes, then row broadcasts between rows.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t dpp_add(uint32_t x) {
+  return x + (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, ROWS, 0xF, true);
+}
+__device__ __forceinline__ uint32_t wave_scan32(uint32_t x) {
+  x = dpp_add<0x111, 0xF>(x);  // row_shr:1
+  x = dpp_add<0x112, 0xF>(x);  // row_shr:2
+  x = dpp_add<0x114, 0xF>(x);  // row_shr:4
+  x = dpp_add<0x118, 0xF>(x);  // row_shr:8
+  x = dpp_add<0x142, 0xA>(x);  // row_bcast:15 into rows 1, 3
+  x = dpp_add<0x143, 0xC>(x);  // row_bcast:31 into rows 2, 3
+  return x;
+}
+
+// Inclusive scan over the workgroup of packed scan keys (cost | units | items, see
+// scan_key); `total` receives the sum over all threads.  The three fields are scanned
+// as 32-bit values, which equals the 64-bit sum since no field overflows.
 __device__ __forceinline__ uint64_t block_scan(uint64_t x, uint64_t *sh, uint64_t &total) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   constexpr int NW = kPlanThreads / 64;
-  for (int o = 1; o < 64; o <<= 1) {
-    const uint64_t y = __shfl_up(x, o);
-    if (lane >= o) x += y;
+  uint32_t c = wave_scan32((uint32_t)(x >> 35)), un = wave_scan32((uint32_t)(x >> 17) & 0x3FFFFu),
+           it = wave_scan32((uint32_t)x & 0x1FFFFu);
+  uint32_t *s32 = (uint32_t *)sh;  // [3][NW] wave totals, then [3][NW] exclusive wave offsets
+  if (lane == 63) {
+    s32[wv] = c;
+    s32[NW + wv] = un;
+    s32[2 * NW + wv] = it;
   }
-  if (lane == 63) sh[wv] = x;
   __syncthreads();
-  if (wv == 0) {
-    uint64_t t = lane < NW ? sh[lane] : 0;
+  if (wv == 0 && lane < 3 * NW) {  // 48 lanes: three 16-wave scans
+    const int f = lane / NW, q = lane % NW;
+    uint32_t t = s32[lane];
     for (int o = 1; o < NW; o <<= 1) {
-      const uint64_t y = __shfl_up(t, o);
-      if (lane >= o) t += y;
+      const uint32_t y = __shfl_up(t, o);
+      if (q >= o) t += y;
     }
-    if (lane < NW) sh[NW + lane] = t;
+    s32[3 * NW + f * NW + q] = t;  // inclusive over waves
   }
   __syncthreads();
-  const uint64_t before = wv ? sh[NW + wv - 1] : 0;
-  total = sh[2 * NW - 1];
+  const uint32_t *inc = s32 + 3 * NW;
+  if (wv) {
+    c += inc[wv - 1];
+    un += inc[NW + wv - 1];
+    it += inc[2 * NW + wv - 1];
+  }
+  total = ((uint64_t)inc[NW - 1] << 35) | ((uint64_t)inc[2 * NW - 1] << 17) | inc[3 * NW - 1];
   __syncthreads();
-  return x + before;
+  return ((uint64_t)c << 35) | ((uint64_t)un << 17) | it;
 }
 
 // Items and units of a visit (as visit_items writes them): items | units << 3.
@@ -1232,13 +1259,16 @@ __device__ __forceinline__ VisitDesc dense_visit(const AttnParams &p, int64_t u,
 // The first W1 wavefronts (those of the workgroups dispatched first, which win the
 // issue arbitration against the later ones on their SIMDs) get kFastCap capacity
 // units, the others kSlowCap (measured: 1.28 times the work in the same time).
+// The position is scaled by cap / (2 total), taken once per plan (a product with a
+// positive constant is monotone, so the owners stay non-decreasing).
 constexpr double kFastCap = 23.0, kSlowCap = 18.0;
-__device__ __forceinline__ int midpoint_owner(int W, int W1, uint64_t e, uint32_t c, uint64_t total) {
-  if (!total) return 0;
-  const double cap = kFastCap * W1 + kSlowCap * (W - W1);
-  const double x = ((double)(2 * e + c) * cap) / (2.0 * (double)total);
-  const double o = x < kFastCap * W1 ? __builtin_floor(x / kFastCap)
-                                     : W1 + __builtin_floor((x - kFastCap * W1) / kSlowCap);
+__device__ __forceinline__ double owner_scale(int W, int W1, uint64_t total) {
+  return total ? (kFastCap * W1 + kSlowCap * (W - W1)) / (2.0 * (double)total) : 0.0;
+}
+__device__ __forceinline__ int midpoint_owner(int W, int W1, uint64_t e, uint32_t c, double scale) {
+  const double x = (double)(2 * e + c) * scale;
+  const double o = x < kFastCap * W1 ? __builtin_floor(x * (1.0 / kFastCap))
+                                     : W1 + __builtin_floor((x - kFastCap * W1) * (1.0 / kSlowCap));
   return o < (double)W ? (int)o : W - 1;
 }
 
@@ -1259,6 +1289,7 @@ struct PlanOut {
   int32_t *isplit, *usplit;
   int W, W1;       // wavefronts, wavefronts of the workgroups dispatched first
   uint64_t total;  // scan key of all visits
+  double scale;    // owner_scale of the total cost
 };
 
 // Visit v, whose scan key interval starts at e: the splits of the wavefronts whose
@@ -1266,7 +1297,7 @@ struct PlanOut {
 __device__ __forceinline__ void place_visit(const PlanOut &o, const VisitDesc &d, int64_t v, int64_t nvis,
                                             uint64_t &e, int &prev) {
   const uint32_t c = d.cost & 0xFFFFFFu;
-  const int own = midpoint_owner(o.W, o.W1, key_cost(e), c, key_cost(o.total));
+  const int own = midpoint_owner(o.W, o.W1, key_cost(e), c, o.scale);
   for (int ww = prev + 1; ww <= own; ++ww) {
     o.isplit[ww] = (int32_t)key_items(e);
     o.usplit[ww] = (int32_t)key_units(e);
@@ -1285,7 +1316,7 @@ __device__ __forceinline__ void place_visit(const PlanOut &o, const VisitDesc &d
 __device__ __forceinline__ int prev_owner(const PlanOut &o, int64_t v0, uint64_t e, uint32_t prev_cost) {
   if (v0 == 0) return -1;
   const uint32_t c = prev_cost & 0xFFFFFFu;
-  return midpoint_owner(o.W, o.W1, key_cost(e) - c, c, key_cost(o.total));
+  return midpoint_owner(o.W, o.W1, key_cost(e) - c, c, o.scale);
 }
 
 // A dense plan runs gridDim.y workgroups per (b, KV head): each scans the costs and
@@ -1313,6 +1344,7 @@ __device__ __forceinline__ void plan_dense_regs(const AttnParams &p, int64_t u, 
     }
   lastc[threadIdx.x] = last;  // read by the next thread after the scan's barriers
   uint64_t e = block_scan(mine, sh, o.total) - mine;
+  o.scale = owner_scale(o.W, o.W1, key_cost(o.total));
   if (v0 >= v1 || !own_slice()) return;
   int prev = prev_owner(o, v0, e, v0 > 0 ? lastc[threadIdx.x - 1] : 0u);
 #pragma unroll
@@ -1323,7 +1355,7 @@ __device__ __forceinline__ void plan_dense_regs(const AttnParams &p, int64_t u, 
 constexpr int kPlanLdsVisits = kPlanThreads;  // Compressed-Quest visits kept in LDS
 
 __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
-  __shared__ uint64_t sh[2 * kPlanThreads / 64];
+  __shared__ uint64_t sh[3 * kPlanThreads / 64];  // block_scan: 6 x 16 32-bit words
   __shared__ uint32_t lastc[kPlanThreads];
   __shared__ VisitDesc lds_desc[kPlanLdsVisits];
   __shared__ int s_cnt;
@@ -1350,6 +1382,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
     uint64_t mine = 0;
     for (int64_t v = v0; v < v1; ++v) mine += scan_key(dense_visit(p, u, nblk, v).cost);
     uint64_t e = block_scan(mine, sh, o.total) - mine;
+    o.scale = owner_scale(o.W, o.W1, key_cost(o.total));
     if (v0 >= v1 || !own_slice()) return;
     int prev = prev_owner(o, v0, e, v0 > 0 ? dense_visit(p, u, nblk, v0 - 1).cost : 0u);
     for (int64_t v = v0; v < v1; ++v) place_visit(o, dense_visit(p, u, nblk, v), v, nvis, e, prev);
@@ -1442,6 +1475,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
   uint64_t mine = 0;
   for (int64_t v = v0; v < v1; ++v) mine += scan_key(desc[v].cost);
   uint64_t e = block_scan(mine, sh, o.total) - mine;
+  o.scale = owner_scale(o.W, o.W1, key_cost(o.total));
   if (v0 < v1) {
     int prev = prev_owner(o, v0, e, v0 > 0 ? desc[v0 - 1].cost : 0u);
     for (int64_t v = v0; v < v1; ++v) place_visit(o, desc[v], v, nvis, e, prev);
