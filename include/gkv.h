@@ -234,9 +234,10 @@ gkv_status gkv_quest_select(const uint16_t *q, const gkv_cache *c, int32_t topk,
  * over the read set -- all tokens < T (pages == NULL) or the selected pages
  * [B][Hkv][topk] plus the current page (section 3.5).  Residual rows override their
  * tokens' graded entries (dense reads only).  q: [B][Hq][128] fp16;
- * out: [B][Hq][128] fp32.  GKV_E_UNSUPPORTED for pages with residual rows, a page
- * size other than 16, or more than 32767 visits per (b,h) (block capacity plus
- * residual pseudo-blocks, or topk + 1). */
+ * out: [B][Hq][128] fp32.  Pages may be 16, 32 or 64 tokens (a selected page reads
+ * its tiles of one block).  GKV_E_UNSUPPORTED for pages with residual rows, or more
+ * than 32767 visits per (b,h) (block capacity plus residual pseudo-blocks, or
+ * topk + 1). */
 gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache *c, const int32_t *pages, int32_t topk,
                                   float *out, void *ws, int64_t ws_bytes, void *stream);
 

@@ -212,6 +212,7 @@ struct AttnParams {
   float *part;
   int64_t T;
   int nblk_cap, Hkv, G, nres, nrb_cap, topk, nsplit;
+  int page;  // Compressed-Quest page tokens (16, 32 or 64)
   int fast;  // workgroups of each (b, KV head) dispatched first (see attn_grid)
   int64_t vcap, icap, ucap;
   float sl2;  // log2(e) / sqrt(D)
@@ -1395,7 +1396,10 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
   const int64_t *ko = p.koff + u * p.nblk_cap, *vo = p.voff + u * p.nblk_cap;
   VisitDesc *desc = p.topk + 1 <= kPlanLdsVisits ? lds_desc : (VisitDesc *)p.visits + u * p.vcap;
   const int32_t *pg = p.pages + u * p.topk;
-  const int64_t cur = (p.T - 1) / 16;
+  // page pg lies in block pg >> pshift and covers tiles page_tiles(pg) of it
+  const int pshift = p.page == 16 ? 2 : (p.page == 32 ? 1 : 0), tpp = p.page / 16;
+  auto page_tiles = [&](int64_t pg) { return ((1u << tpp) - 1) << ((pg & ((1 << pshift) - 1)) * tpp); };
+  const int64_t cur = (p.T - 1) / p.page;
   auto make_visit = [&](int64_t blk, uint32_t tl) {
     VisitDesc d;
     d.level = lvl[blk];
@@ -1424,13 +1428,13 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
     const int cnt = s_cnt, n = cnt + 1;
     if (i == 0) spg[cnt] = (int32_t)cur;  // the current page is always read
     __syncthreads();
-    const int64_t blk = i < n ? spg[i] >> 2 : -1;
-    const bool start = i < n && (i == 0 || (spg[i - 1] >> 2) != blk);
+    const int64_t blk = i < n ? spg[i] >> pshift : -1;
+    const bool start = i < n && (i == 0 || (spg[i - 1] >> pshift) != blk);
     uint64_t tot;
     const uint64_t incl = block_scan(start ? 1 : 0, sh, tot);
     if (start) {
       uint32_t tl = 0;
-      for (int j = i; j < n && (spg[j] >> 2) == blk; ++j) tl |= 1u << (spg[j] & 3);
+      for (int j = i; j < n && (spg[j] >> pshift) == blk; ++j) tl |= page_tiles(spg[j]);
       desc[incl - 1] = make_visit(blk, tl);
     }
     vbase = tot;
@@ -1445,8 +1449,8 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
       int64_t blk = -1;
       bool start = false;
       if (i < n) {
-        blk = (i < cnt ? pg[i] : cur) >> 2;
-        start = i == 0 || ((i - 1 < cnt ? pg[i - 1] : cur) >> 2) != blk;
+        blk = (i < cnt ? pg[i] : cur) >> pshift;
+        start = i == 0 || ((i - 1 < cnt ? pg[i - 1] : cur) >> pshift) != blk;
       }
       uint64_t tot;
       const uint64_t incl = block_scan(start ? 1 : 0, sh, tot);
@@ -1454,8 +1458,8 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
         uint32_t tl = 0;
         for (int j = i; j < n; ++j) {
           const int64_t pj = j < cnt ? pg[j] : cur;
-          if ((pj >> 2) != blk) break;
-          tl |= 1u << (pj & 3);
+          if ((pj >> pshift) != blk) break;
+          tl |= page_tiles(pj);
         }
         desc[vbase + incl - 1] = make_visit(blk, tl);
       }
@@ -1561,7 +1565,7 @@ static gkv_status attn_setup(const uint16_t *q, const gkv_cache *c, const int32_
   if (c->T <= 0) return GKV_E_SHAPE;
   if (pages) {
     if (topk <= 0) return GKV_E_ARG;
-    if (c->page != 16) return GKV_E_UNSUPPORTED;
+    if (c->page != 16 && c->page != 32 && c->page != 64) return GKV_E_UNSUPPORTED;
     if (c->nres) return GKV_E_UNSUPPORTED;
   } else {
     topk = 0;
@@ -1592,6 +1596,7 @@ static gkv_status attn_setup(const uint16_t *q, const gkv_cache *c, const int32_
   p.nres = c->nres;
   p.nrb_cap = (c->nres_cap + P - 1) / P;
   p.topk = topk;
+  p.page = c->page ? c->page : 16;
   p.nsplit = attn_nsplit(c, topk, c->T);
   p.fast = attn_fast(p.nsplit, (int64_t)c->B * c->Hkv);
   p.sl2 = 1.4426950408889634f / sqrtf((float)D);

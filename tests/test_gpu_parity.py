@@ -96,6 +96,34 @@ def test_quest_boxes_selection_and_sparse_attention(gpu, T, topk):
                 assert max_err(out[b, h * G:(h + 1) * G], uc.decode_dense(q_group(q, b, h, G))) <= TOL
 
 
+@pytest.mark.parametrize("page,T,topk", [(32, 6001, 40), (64, 8192, 30), (64, 3000, 50)])
+def test_quest_larger_pages(gpu, page, T, topk):
+    """Compressed-Quest with 32- and 64-token pages (the paper's own box granularity is
+    a 64-token block): boxes, selection and attention over the selected pages plus the
+    current page against the oracle; T = 3000 with top-50 selects every ranked page."""
+    B_, Hq, Hkv = 1, 8, 2
+    ks, vs = kv_all(3, B_, Hkv, T)
+    lv = olad.ladder("graded", T)
+    cache = _build(gpu, ks, vs, Hq, lv, page=page)
+    G = Hq // Hkv
+    q = synth.queries(3, B_, Hq, step=page)
+    pages = cache.quest_select(q, topk)
+    out = cache.decode(q, pages=pages).cpu().numpy()
+    pages = pages.cpu().numpy()
+    for h in range(Hkv):
+        kmin, kmax = oquest.page_boxes(ks[0, h], page)
+        gmin, gmax = cache.boxes_host(0, h, T // page)
+        np.testing.assert_array_equal(gmin, kmin)
+        np.testing.assert_array_equal(gmax, kmax)
+        want = oquest.quest_select(q_group(q, 0, h, G), kmin, kmax, T, topk, page)
+        np.testing.assert_array_equal(pages[0, h], want)
+        uc = ocache.UnitCache(ks[0, h], vs[0, h], lv)
+        ref = uc.decode_quest(q_group(q, 0, h, G), want, page)
+        assert max_err(out[0, h * G:(h + 1) * G], ref) <= TOL
+        if topk >= (T - 1) // page:
+            assert max_err(out[0, h * G:(h + 1) * G], uc.decode_dense(q_group(q, 0, h, G))) <= TOL
+
+
 def test_quest_ties_go_to_lower_page(gpu):
     T, Hq, Hkv = 2048, 4, 1
     ks, vs = kv_all(31, 1, Hkv, T)
