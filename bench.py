@@ -14,6 +14,7 @@ sparse attention at 128k) are timed once each and reported under "phases".
 Prints ONE JSON line.  Only one GPU is supported: --gpus N > 1 exits.
 """
 import argparse
+import dataclasses
 import json
 import os
 import sys
@@ -152,6 +153,40 @@ def cpu_oracle_sample(ks_unit, vs_unit, lv, mass, nres, q_group, out_gpu):
     return dt, err
 
 
+def quest_point(wq, ncopies, dev):
+    """Compressed-Quest decode steps (page selection + sparse graded attention) at
+    workload wq, rotating ncopies identical caches so that the step's working set
+    exceeds the Infinity Cache."""
+    import numpy as np
+    import torch
+    from paper_2608_23599_amd import binding as gkv, synth
+    log(f"[bench] {wq.name} (B={wq.B})")
+    kq, vq = gen_inputs(wq.id, wq.B, wq.Hkv, wq.T, dev)
+    qc = gkv.GradedCache.build(kq, vq, Hq=wq.Hq, levels=gkv.ladder_levels("graded", wq.T), page=wq.page, device=dev)
+    bms = timed(lambda: qc.page_boxes(kq, 0, wq.T // wq.page))
+    del kq, vq
+    qq = torch.from_numpy(synth.queries(wq.id, wq.B, wq.Hq).view(np.int16)).to(dev)
+    copies = [qc] + [qc.clone() for _ in range(ncopies - 1)]
+    pages = [torch.empty((wq.B, wq.Hkv, wq.topk), dtype=torch.int32, device=dev) for _ in copies]
+    qouts = [torch.empty((wq.B, wq.Hq, 128), dtype=torch.float32, device=dev) for _ in copies]
+    n = len(copies)
+    for i in range(10):
+        copies[i % n].quest_select(qq, wq.topk, out=pages[i % n])
+        copies[i % n].decode(qq, pages=pages[i % n], out=qouts[i % n])
+    reps = max(1, 24 // n)
+    sel_ms = timed(lambda: [copies[i].quest_select(qq, wq.topk, out=pages[i]) for i in range(n)], reps) / n
+    att_ms = timed(lambda: [copies[i].decode(qq, pages=pages[i], out=qouts[i]) for i in range(n)], reps) / n
+    ev_ms = timed(lambda: [(copies[i].quest_select(qq, wq.topk, out=pages[i]),
+                            copies[i].decode(qq, pages=pages[i], out=qouts[i])) for i in range(n)], reps) / n
+    r = qc.account(pages[0])
+    qbytes = r["read_bits"] / 8.0
+    return {"workload": wq.name, "B": wq.B, "us_per_step": round(ev_ms * 1e3, 2), "select_us": round(sel_ms * 1e3, 2),
+            "attn_us": round(att_ms * 1e3, 2), "read_bpv": round(r["read_bpv"], 4),
+            "resident_bpv": round(r["resident_bpv"], 4), "algorithmic_bytes": int(qbytes),
+            "achieved_GBps": round(qbytes / (ev_ms * 1e-3) / 1e9, 1),
+            "page_boxes_all_ms": round(bms, 3), "cache_copies_rotated": n}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -266,45 +301,33 @@ def main():
             caches[0].account()
         phases["accounting_host_us"] = round((time.perf_counter() - ta) / 100 * 1e6, 1)
         del small
+        # a second denominator: what a plain library reduction reads per second
+        big = torch.zeros(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB
+        for _ in range(3):
+            big.sum()
+        phases["stream_read_GBps_torch_sum_1GiB"] = round((1 << 30) / (timed(lambda: big.sum(), 10) * 1e-3) / 1e9, 1)
+        del big
 
-    quest = None
+    quest = quest_b8 = quest_p64 = None
     if not args.no_quest:
-        wq = workloads.QUEST128K
-        log(f"[bench] {wq.name}")
         del k, v
         torch.cuda.empty_cache()
-        kq, vq = gen_inputs(wq.id, wq.B, wq.Hkv, wq.T, dev)
-        lvq = gkv.ladder_levels("graded", wq.T)
-        qc = gkv.GradedCache.build(kq, vq, Hq=wq.Hq, levels=lvq, page=wq.page, device=dev)
-        bms = timed(lambda: qc.page_boxes(kq, 0, wq.T // wq.page))
-        qq = torch.from_numpy(synth.queries(wq.id, wq.B, wq.Hq).view(np.int16)).to(dev)
-        # rotate enough identical copies that the step working set exceeds the Infinity Cache
-        copies = [qc] + [qc.clone() for _ in range(11)]
-        pages = [torch.empty((wq.B, wq.Hkv, wq.topk), dtype=torch.int32, device=dev) for _ in copies]
-        qouts = [torch.empty((wq.B, wq.Hq, 128), dtype=torch.float32, device=dev) for _ in copies]
-        n = len(copies)
-        for i in range(10):
-            copies[i % n].quest_select(qq, wq.topk, out=pages[i % n])
-            copies[i % n].decode(qq, pages=pages[i % n], out=qouts[i % n])
-        sel_ms = timed(lambda: [copies[i].quest_select(qq, wq.topk, out=pages[i]) for i in range(n)], 1) / n
-        att_ms = timed(lambda: [copies[i].decode(qq, pages=pages[i], out=qouts[i]) for i in range(n)], 1) / n
-        ev_ms = timed(lambda: [(copies[i].quest_select(qq, wq.topk, out=pages[i]),
-                                copies[i].decode(qq, pages=pages[i], out=qouts[i])) for i in range(n)], 1) / n
-        r = qc.account(pages[0])
-        qbytes = r["read_bits"] / 8.0
-        quest = {"workload": wq.name, "us_per_step": round(ev_ms * 1e3, 2), "select_us": round(sel_ms * 1e3, 2),
-                 "attn_us": round(att_ms * 1e3, 2), "read_bpv": round(r["read_bpv"], 4),
-                 "resident_bpv": round(r["resident_bpv"], 4), "algorithmic_bytes": int(qbytes),
-                 "achieved_GBps": round(qbytes / (ev_ms * 1e-3) / 1e9, 1),
-                 "page_boxes_all_ms": round(bms, 3), "cache_copies_rotated": n}
+        quest = quest_point(workloads.QUEST128K, 12, dev)
         log(f"[bench] quest 128k: {quest['us_per_step']} us/step")
+        w8 = dataclasses.replace(workloads.QUEST128K, B=8, name=workloads.QUEST128K.name.replace("B=1", "") + ", B=8")
+        quest_b8 = quest_point(w8, 2, dev)
+        log(f"[bench] quest 128k B8: {quest_b8['us_per_step']} us/step")
+        # the paper's own box granularity: 64-token pages, the same 2048 tokens read
+        w64 = dataclasses.replace(workloads.QUEST128K, page=64, topk=32,
+                                  name=workloads.QUEST128K.name.replace("page 16, top-128", "page 64, top-32"))
+        quest_p64 = quest_point(w64, 24, dev)
+        log(f"[bench] quest 128k page 64: {quest_p64['us_per_step']} us/step")
+        torch.cuda.empty_cache()
 
     quest1m = None
     if not args.no_1m:
         w5 = workloads.QUEST1M
         log(f"[bench] {w5.name}")
-        if quest is not None:
-            del copies, pages, qouts, qc, kq, vq
         torch.cuda.empty_cache()
         k5, v5 = gen_inputs(w5.id, w5.B, w5.Hkv, w5.T, dev)
         c5 = gkv.GradedCache.build(k5, v5, Hq=w5.Hq, levels=gkv.ladder_levels("graded", w5.T), page=w5.page, device=dev,
@@ -385,6 +408,8 @@ def main():
         "cpu_baseline": cpu,
         "phases": phases,
         "quest_128k": quest,
+        "quest_128k_b8": quest_b8,
+        "quest_128k_page64": quest_p64,
         "quest_1m": quest1m,
     }
     print(json.dumps(res), flush=True)
