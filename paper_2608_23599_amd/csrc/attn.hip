@@ -1495,7 +1495,11 @@ static int attn_nsplit(const gkv_cache *c, int32_t topk, int64_t T) {
   const int64_t units = (int64_t)c->B * c->Hkv;
   int64_t waves;
   if (topk > 0) {
-    waves = (topk + 1 + 3) / 4;
+    // one visit per wavefront while the chip holds them (2048 wavefronts over all
+    // (b, KV head)); at least one per four visits
+    waves = topk + 1;
+    const int64_t room = 2048 / units, least = (topk + 1 + 3) / 4;
+    if (waves > room) waves = room > least ? room : least;
   } else {
     const int64_t nvis = (T + P - 1) / P + (c->nres_cap + P - 1) / P;
     waves = 2048 / units;
