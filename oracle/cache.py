@@ -9,7 +9,7 @@ plus the monotone per-step append-and-demote update (section 3.2).
 """
 import numpy as np
 
-from . import fp16, quant, quest, attention, residual
+from . import fp16, quant, quest, attention, residual, certificate
 from .ladder import EXACT, ORDER, ladder
 
 P = 64
@@ -23,6 +23,8 @@ class UnitCache:
         self.levels = np.array(levels, dtype=np.int8)
         self.k_recs = []
         self.v_recs = []
+        # decode-time certificate numbers per block (see certificate.decode_bound)
+        self.kerr, self.verr, self.vmax = [], [], []
         for b, lv in enumerate(self.levels):
             rows = slice(b * P, min((b + 1) * P, self.T))
             kb = np.zeros((P, self.D), dtype=np.uint16)
@@ -33,6 +35,11 @@ class UnitCache:
                 raise ValueError("only an exact block may be partial")
             self.k_recs.append(quant.encode_fp16(lv, kb))
             self.v_recs.append(quant.encode_fp16(lv, vb))
+            ke, _ = certificate.block_numbers(fp16.to_f64(kb), quant.decode(self.k_recs[-1]))
+            ve, vn = certificate.block_numbers(fp16.to_f64(vb), quant.decode(self.v_recs[-1]))
+            self.kerr.append(ke)
+            self.verr.append(ve)
+            self.vmax.append(vn)
         self.res_idx = np.zeros(0, dtype=np.int32)
         self.res_k = None
         self.res_v = None
@@ -64,6 +71,20 @@ class UnitCache:
         kh, vh = self.khat_vhat()
         return attention.unit_decode(q_bits_group, kh, vh)
 
+    def certificate(self, q_bits_group):
+        """Decode-time certificate of a dense read, per query head of the group."""
+        kh, _ = self.khat_vhat()
+        kerr = np.repeat(np.asarray(self.kerr), P)[: self.T]
+        verr = np.repeat(np.asarray(self.verr), P)[: self.T]
+        if len(self.res_idx):
+            kerr = kerr.copy()
+            verr = verr.copy()
+            kerr[self.res_idx] = 0.0
+            verr[self.res_idx] = 0.0
+        q = fp16.to_f64(q_bits_group)
+        vmax = max(self.vmax)
+        return np.array([certificate.decode_bound(q[g], kh, kerr, verr, vmax) for g in range(q.shape[0])])
+
     def decode_quest(self, q_bits_group, pages, page=quest.PAGE):
         kh, vh = self.khat_vhat()
         idx = quest.read_tokens(pages, self.T, page)
@@ -83,10 +104,14 @@ class UnitCache:
             self.k_recs.append(quant.Record(EXACT, exact=z.copy()))
             self.v_recs.append(quant.Record(EXACT, exact=z.copy()))
             self.levels = np.append(self.levels, np.int8(EXACT))
+            self.kerr.append(0.0)
+            self.verr.append(0.0)
+            self.vmax.append(0.0)
         b = t // P
         assert self.k_recs[b].level == EXACT
         self.k_recs[b].exact[t % P] = k_row_bits
         self.v_recs[b].exact[t % P] = v_row_bits
+        self.vmax[b] = max(self.vmax[b], float(np.sqrt((fp16.to_f64(np.asarray(v_row_bits)) ** 2).sum())))
         self.T = t + 1
         new_lv = ladder(profile, self.T)
         moves = []
@@ -94,8 +119,11 @@ class UnitCache:
             if old != new:
                 if ORDER[int(new)] > ORDER[int(old)]:
                     raise quant.NotMonotone(f"block {i}: {old} -> {new}")
-                self.k_recs[i] = quant.demote(self.k_recs[i], new)
-                self.v_recs[i] = quant.demote(self.v_recs[i], new)
+                kold, vold = self.k_recs[i], self.v_recs[i]
+                self.k_recs[i] = quant.demote(kold, new)
+                self.v_recs[i] = quant.demote(vold, new)
+                self.kerr[i] += certificate.demote_increment(quant.decode(kold), quant.decode(self.k_recs[i]))
+                self.verr[i] += certificate.demote_increment(quant.decode(vold), quant.decode(self.v_recs[i]))
                 moves.append((i, int(old), int(new)))
         self.levels = np.array(new_lv, dtype=np.int8)
         return moves
