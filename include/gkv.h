@@ -115,6 +115,15 @@ typedef struct gkv_cache {
   uint8_t *res_rows;         /* device [B][Hkv][ceil(nres_cap/64)] pseudo-blocks      */
   uint64_t *res_mask;        /* device [B][Hkv][nblk_cap] bit t%64 set = token t is
                                 read from the residual instead of its block           */
+  float *cert;               /* device [B][Hkv][nblk_cap][4] or NULL: per block
+                                {kerr, verr, vmax, 0} for the decode-time attention
+                                error certificate (section 3.6): kerr = max_t
+                                ||k_t - k_hat_t||, verr = max_t ||v_t - v_hat_t||
+                                against the exact rows, vmax = max_t ||v_t||; written
+                                by gkv_quantize_block (keys: kerr; values: verr,
+                                vmax), raised by gkv_demote by the change of the
+                                reconstruction (triangle inequality) and kept by
+                                gkv_append; fp32 rounded upwards                     */
 } gkv_cache;
 
 /* ---------------------------------------------------------------- host helpers */
@@ -240,6 +249,17 @@ gkv_status gkv_quest_select(const uint16_t *q, const gkv_cache *c, int32_t topk,
  * topk + 1). */
 gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache *c, const int32_t *pages, int32_t topk,
                                   float *out, void *ws, int64_t ws_bytes, void *stream);
+
+/* Dense gkv_graded_decode_attn plus the decode-time attention error certificate
+ * (section 3.6, Eq. certificate) of every query head: bound[b][g] bounds
+ * ||o - o_hat|| between attention over the exact rows and out, as
+ *   sum_b a_b verr_b + min(2, M+/M- - M-/M+) * max_b vmax_b,
+ *   M+- = sum_b a_b exp(+-eps_b),  eps_b = ||q_g|| kerr_b / sqrt(128),
+ * with a_b the block's share of out's attention weights and kerr, verr, vmax the
+ * cache's per-block numbers (c->cert, required).  Residual rows count as exact.
+ * bound: [B][Hq] fp32.  GKV_E_ARG when c->cert is NULL. */
+gkv_status gkv_graded_decode_attn_bound(const uint16_t *q, const gkv_cache *c, float *out, float *bound, void *ws,
+                                        int64_t ws_bytes, void *stream);
 
 /* The three stages of gkv_graded_decode_attn, for callers that time or schedule them
  * apart; called in this order on one stream with the same cache, pages, topk and

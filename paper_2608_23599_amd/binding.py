@@ -37,6 +37,7 @@ class CacheStruct(ctypes.Structure):
         ("level_host", _vp),
         ("page", _i32), ("npage_cap", _i64), ("boxes", _vp),
         ("nres", _i32), ("nres_cap", _i32), ("res_idx", _vp), ("res_rows", _vp), ("res_mask", _vp),
+        ("cert", _vp),
     ]
 
 
@@ -72,6 +73,7 @@ _page_boxes = _sig("gkv_page_boxes", _i32, [_P(CacheStruct), _vp, _i64, _i64, _i
 _append = _sig("gkv_append", _i32, [_P(CacheStruct), _vp, _vp, _vp, _vp, _vp])
 _quest_select = _sig("gkv_quest_select", _i32, [_vp, _P(CacheStruct), _i32, _vp, _vp, _i64, _vp])
 _attn = _sig("gkv_graded_decode_attn", _i32, [_vp, _P(CacheStruct), _vp, _i32, _vp, _vp, _i64, _vp])
+_attn_bound = _sig("gkv_graded_decode_attn_bound", _i32, [_vp, _P(CacheStruct), _vp, _vp, _vp, _i64, _vp])
 _attn_plan = _sig("gkv_attn_plan", _i32, [_P(CacheStruct), _vp, _i32, _vp, _i64, _vp])
 _attn_partials = _sig("gkv_attn_partials", _i32, [_vp, _P(CacheStruct), _vp, _i32, _vp, _i64, _vp])
 _attn_merge = _sig("gkv_attn_merge", _i32, [_P(CacheStruct), _vp, _i32, _vp, _vp, _i64, _vp])
@@ -82,7 +84,7 @@ EXPORTED = [
     "gkv_pool_bytes", "gkv_pool_alloc", "gkv_pool_free", "gkv_pool_used", "gkv_pool_destroy", "gkv_account",
     "gkv_decode_record", "gkv_f64_to_f16", "gkv_workspace_bytes", "gkv_quantize_block", "gkv_demote",
     "gkv_page_boxes", "gkv_append", "gkv_quest_select", "gkv_graded_decode_attn", "gkv_rd_residual_select",
-    "gkv_attn_plan", "gkv_attn_partials", "gkv_attn_merge",
+    "gkv_attn_plan", "gkv_attn_partials", "gkv_attn_merge", "gkv_graded_decode_attn_bound",
 ]
 
 
@@ -213,6 +215,8 @@ class GradedCache:
             self.res_mask = torch.zeros((B, Hkv, nblk_cap), dtype=torch.int64, device=self.device)
         else:
             self.res_idx = self.res_rows = self.res_mask = None
+        # per-block certificate numbers {kerr, verr, vmax, 0}
+        self.cert = torch.zeros((B, Hkv, nblk_cap, 4), dtype=torch.float32, device=self.device)
         self.c = CacheStruct()
         self._bind(T, 0)
         self._ws = {}
@@ -236,13 +240,14 @@ class GradedCache:
         c.res_idx = self.res_idx.data_ptr() if self.nres_cap else None
         c.res_rows = self.res_rows.data_ptr() if self.nres_cap else None
         c.res_mask = self.res_mask.data_ptr() if self.nres_cap else None
+        c.cert = self.cert.data_ptr()
 
     def clone(self):
         """A read-only copy in separate device memory (same layout and offsets), for
         benchmarks that rotate identical caches; it cannot append or demote."""
         new = object.__new__(GradedCache)
         new.__dict__.update(self.__dict__)
-        for name in ("arena", "level", "koff", "voff", "boxes", "res_idx", "res_rows", "res_mask"):
+        for name in ("arena", "level", "koff", "voff", "boxes", "res_idx", "res_rows", "res_mask", "cert"):
             t = getattr(self, name)
             setattr(new, name, t.clone() if t is not None else None)
         new.level_host = self.level_host.copy()
@@ -404,6 +409,19 @@ class GradedCache:
         return out
 
     decode = graded_decode_attn
+
+    def decode_bound(self, q, out=None, bound=None):
+        """Dense decode plus the attention error certificate per query head:
+        returns (out [B][Hq][128] fp32, bound [B][Hq] fp32)."""
+        q = _as_bits(q, self.device)
+        if out is None:
+            out = torch.empty((self.B, self.Hq, D), dtype=torch.float32, device=self.device)
+        if bound is None:
+            bound = torch.empty((self.B, self.Hq), dtype=torch.float32, device=self.device)
+        ws = self.workspace(1, 0)
+        _check(_attn_bound(_dptr(q), ctypes.byref(self.c), _dptr(out), _dptr(bound), _dptr(ws), ws.numel(),
+                           _stream()), "graded_decode_attn_bound")
+        return out, bound
 
     # the three stages of graded_decode_attn (same result when called in order)
     def attn_plan(self, pages=None):

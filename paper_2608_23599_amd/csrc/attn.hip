@@ -213,6 +213,8 @@ struct AttnParams {
   int64_t T;
   int nblk_cap, Hkv, G, nres, nrb_cap, topk, nsplit;
   int page;  // Compressed-Quest page tokens (16, 32 or 64)
+  const float *cert;  // per-block certificate numbers {kerr, verr, vmax, 0} (dense reads)
+  float *bound;       // when set: the attention error certificate per query head
   int fast;  // workgroups of each (b, KV head) dispatched first (see attn_grid)
   int64_t vcap, icap, ucap;
   float sl2;  // log2(e) / sqrt(D)
@@ -226,6 +228,8 @@ constexpr int kChunk = 32;        // descriptors per 512-byte chunk
 // (2 x 512) | value scale/zero of the current int block (512)
 constexpr int kWaveLds = kRing + 4 * 512 + 512;
 constexpr int kMaxWaves = 1024;   // wavefronts per (b, KV head)
+// partial per workgroup and head: m, l, o[D], then the certificate sums c1, c2, c3
+constexpr int kPart = D + 5;
 
 
 // ---------------------------------------------------------------- async copies
@@ -359,6 +363,8 @@ struct Pipe {
   uint32_t ifetch;  // load count through the last item-chunk copy
   uint8_t *ebuf;    // value scale/zero of the current int block (LDS, 512 B)
   int lane;
+  uint32_t blk;        // block index of the current item (0xFFFF: no block record)
+  const float *cert;   // this (b, KV head)'s certificate rows, or null
 
   __device__ __forceinline__ void fetch(const uint8_t *src, uint32_t lds, uint32_t c) {
     if (lane < 32) dma16(src + (size_t)c * 512 + 16 * lane, lds + (c & 1) * 512);
@@ -394,6 +400,7 @@ struct Pipe {
     }
   }
   // The next item's descriptor (false when the wavefront's items are done).
+  template <bool CERT>
   __device__ __forceinline__ bool next_item(uint32_t &meta, uint64_t &valid) {
     if (ik == nitems) return false;
     const uint32_t r = ik % kChunk;
@@ -405,6 +412,7 @@ struct Pipe {
     const uint4 d = *(const uint4 *)(ichunk + ((ik / kChunk) & 1) * 512 + r * sizeof(ItemDesc));
     meta = (uint32_t)uni((int32_t)d.x);
     valid = (uint64_t)uni64((int64_t)(((uint64_t)d.w << 32) | d.z));
+    if (CERT) blk = (uint32_t)uni((int32_t)d.y);
     ++ik;
     return true;
   }
@@ -424,7 +432,17 @@ struct Pipe {
 struct State {
   f4 O[8];
   float m, l;
+  float c1, c2, c3;  // certificate sums: sum_b p_b verr_b, sum_b p_b e^eps_b, sum_b p_b e^-eps_b
+  float es;          // eps_b = es * kerr_b in log2 units: ||q|| log2(e) / sqrt(D)
 };
+
+// Adds block mass pb (this lane's head) with certificate numbers kerr, verr.
+__device__ __forceinline__ void cert_add(State &st, float pb, float kerr, float verr) {
+  const float x = st.es * kerr;
+  st.c1 = fmaf(pb, verr, st.c1);
+  st.c2 = fmaf(pb, __builtin_amdgcn_exp2f(x), st.c2);
+  st.c3 = fmaf(pb, __builtin_amdgcn_exp2f(-x), st.c3);
+}
 
 // Maximum over the 4 lanes of a head (lanes m16 + 16 kg): the row-swap permutes
 // pair lane l with l ^ 32 and l ^ 16.
@@ -453,6 +471,9 @@ __device__ __forceinline__ float rescale_factor(State &st, float bm) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) st.O[j] *= alpha;
     st.l *= alpha;
+    st.c1 *= alpha;
+    st.c2 *= alpha;
+    st.c3 *= alpha;
     st.m = mn;
   }
   return alpha;
@@ -574,7 +595,7 @@ constexpr half8 kOnes8 = half8{(_Float16)1, (_Float16)1, (_Float16)1, (_Float16)
 
 // ---------------------------------------------------------------- items
 // Exact block tile: 16 tokens of fp16 K and V.
-template <bool PACK>
+template <bool PACK, bool CERT>
 __device__ __forceinline__ void exact_tile(const AttnParams &p, State &st, const uint8_t *qs, Pipe &pp,
                                            uint32_t tvalid, int lane) {
   const int kg = lane >> 4;
@@ -596,6 +617,10 @@ __device__ __forceinline__ void exact_tile(const AttnParams &p, State &st, const
   for (int j = 0; j < 8; ++j)
     st.O[j] = mfma16(as_h4(a[j >> 1].u[2 * (j & 1)], a[j >> 1].u[2 * (j & 1) + 1]), P4, st.O[j]);
   st.l += pb[0];
+  if (CERT) {  // exact rows: no logit or value error
+    st.c2 += pb[0];
+    st.c3 += pb[0];
+  }
   pp.release(2);
 }
 
@@ -604,6 +629,7 @@ struct IntBlock {
   half8 qh[4], ql[4];  // q * s as two fp16 terms
   f4 c0;               // per-block logit constant
   f4 acc[8], pb;       // block-local P.V on codes and sum of P
+  float kerr, verr;    // certificate numbers of the block
 };
 
 // PACK: lanes of columns 0..7 keep the high term of q * s of their head in qh,
@@ -794,9 +820,9 @@ __device__ __forceinline__ void int_epilogue(State &st, IntBlock &ib, const uint
 }
 
 // Centroid block: one unit with both records (K at +0, V at +2 KB).
-template <bool PACK>
+template <bool PACK, bool CERT>
 __device__ __forceinline__ void centroid_item(const AttnParams &p, State &st, const uint8_t *qs, const uint8_t *ip,
-                                              uint64_t valid, int lane) {
+                                              uint64_t valid, int lane, const float *cb) {
   const int kg = lane >> 4, m16 = lane & 15;
   // logits of the 4 key centroids: rows 4kg + r of A hold centroid r
   f4 sc = {0, 0, 0, 0};
@@ -850,21 +876,22 @@ __device__ __forceinline__ void centroid_item(const AttnParams &p, State &st, co
   for (int j = 0; j < 8; ++j)
     st.O[j] = mfma16(as_h4(vc[j >> 1].u[2 * (j & 1)], vc[j >> 1].u[2 * (j & 1) + 1]), Bw, st.O[j]);
   st.l += lsum;
+  if (CERT) cert_add(st, lsum, cb[0], cb[1]);
 }
 
 // Runs: process items of one level until the next item has another level (its
 // descriptor left in meta/valid) or the items end (returns false).
-template <bool PACK>
+template <bool PACK, bool CERT>
 __device__ __forceinline__ bool exact_run(const AttnParams &p, State &st, const uint8_t *qs, Pipe &pp,
                                           uint32_t &meta, uint64_t &valid, int lane) {
   do {
-    exact_tile<PACK>(p, st, qs, pp, meta_tvalid(meta), lane);
-    if (!pp.next_item(meta, valid)) return false;
+    exact_tile<PACK, CERT>(p, st, qs, pp, meta_tvalid(meta), lane);
+    if (!pp.template next_item<CERT>(meta, valid)) return false;
   } while (meta_lv(meta) == GKV_EXACT);
   return true;
 }
 
-template <int BITS, bool PACK>
+template <int BITS, bool PACK, bool CERT>
 __device__ __forceinline__ bool int_run(const AttnParams &p, State &st, const uint8_t *qs, Pipe &pp,
                                         uint32_t &meta, uint64_t &valid, int lane) {
   IntBlock ib;
@@ -878,6 +905,10 @@ __device__ __forceinline__ bool int_run(const AttnParams &p, State &st, const ui
   }
   do {
     if (meta_first(meta)) {
+      if (CERT) {
+        ib.kerr = pp.cert[pp.blk * 4];
+        ib.verr = pp.cert[pp.blk * 4 + 1];
+      }
       const uint8_t *sz = pp.template pop<0>();
       int_header<BITS, PACK>(ib, qs, sz, lane);
       *(uint2 *)(pp.ebuf + 8 * lane) = *(const uint2 *)(sz + 2048 + 8 * lane);  // V scale/zero, kept
@@ -901,25 +932,28 @@ __device__ __forceinline__ bool int_run(const AttnParams &p, State &st, const ui
     if (j < n)
       int_tile<BITS, PACK>(p, st, ib, kq + j * 256 * BITS, vq + j * 256 * BITS,
                            (uint32_t)(valid >> (16 * __builtin_ctz(tl))) & 0xFFFFu, mg, lane);
-    if (meta_last(meta)) int_epilogue<BITS>(st, ib, pp.ebuf, lane);
+    if (meta_last(meta)) {
+      int_epilogue<BITS>(st, ib, pp.ebuf, lane);
+      if (CERT) cert_add(st, ib.pb[0], ib.kerr, ib.verr);
+    }
     pp.release(BITS == 2 ? 1 : 2);
-    if (!pp.next_item(meta, valid)) return false;
+    if (!pp.template next_item<CERT>(meta, valid)) return false;
   } while (meta_lv(meta) == BITS);
   return true;
 }
 
-template <bool PACK>
+template <bool PACK, bool CERT>
 __device__ __forceinline__ bool centroid_run(const AttnParams &p, State &st, const uint8_t *qs, Pipe &pp,
                                              uint32_t &meta, uint64_t &valid, int lane) {
   do {
-    centroid_item<PACK>(p, st, qs, pp.template pop<0>(), valid, lane);
+    centroid_item<PACK, CERT>(p, st, qs, pp.template pop<0>(), valid, lane, CERT ? pp.cert + pp.blk * 4 : nullptr);
     pp.release(1);
-    if (!pp.next_item(meta, valid)) return false;
+    if (!pp.template next_item<CERT>(meta, valid)) return false;
   } while (meta_lv(meta) == GKV_CENTROID);
   return true;
 }
 
-template <bool PACK>
+template <bool PACK, bool CERT>
 __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   extern __shared__ __align__(16) uint8_t smem[];
   // Workgroup L of the one-dimensional grid serves (b, KV head) L % units as its
@@ -944,6 +978,18 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   for (int j = 0; j < 8; ++j) st.O[j] = f4{0, 0, 0, 0};
   st.m = kNegInf;
   st.l = 0.f;
+  st.c1 = st.c2 = st.c3 = 0.f;
+  st.es = 0.f;
+  if (CERT) {  // ||q|| of this lane's head, for eps_b = ||q|| kerr_b / sqrt(D)
+    float qq = 0.f;
+    for (int c8 = 0; c8 < D; c8 += 8) {
+      U8 t;
+      t.v = lds16(qs + qrow<PACK>(lane) * kQRow + c8 * 2);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qq = fmaf((float)t.h[e], (float)t.h[e], qq);
+    }
+    st.es = __builtin_sqrtf(qq) * p.sl2;  // sl2 = log2(e) / sqrt(D)
+  }
 
   // this wavefront's items and units, from the plan
   const int32_t *isp = p.split + u * (int64_t)(2 * (W + 1)), *usp = isp + (W + 1);
@@ -964,19 +1010,21 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   pp.usrc = p.units + (u * p.ucap + u0) * (int64_t)sizeof(UnitDesc);
   pp.nitems = i1 - i0;
   pp.nunits = u1 - u0;
+  pp.cert = CERT ? p.cert + u * p.nblk_cap * 4 : nullptr;
+  pp.blk = 0xFFFFu;
   pp.start(lane);
   // Items are processed in runs of one level, each run in a loop specialised for
   // that level (the constants of one level's path are then live only in its loop).
   uint32_t meta;
   uint64_t valid;
-  bool more = pp.next_item(meta, valid);
+  bool more = pp.template next_item<CERT>(meta, valid);
   while (more) {
     switch (meta_lv(meta)) {
-      case GKV_EXACT: more = exact_run<PACK>(p, st, qs, pp, meta, valid, lane); break;
-      case GKV_INT8: more = int_run<8, PACK>(p, st, qs, pp, meta, valid, lane); break;
-      case GKV_INT4: more = int_run<4, PACK>(p, st, qs, pp, meta, valid, lane); break;
-      case GKV_INT2: more = int_run<2, PACK>(p, st, qs, pp, meta, valid, lane); break;
-      default: more = centroid_run<PACK>(p, st, qs, pp, meta, valid, lane); break;
+      case GKV_EXACT: more = exact_run<PACK, CERT>(p, st, qs, pp, meta, valid, lane); break;
+      case GKV_INT8: more = int_run<8, PACK, CERT>(p, st, qs, pp, meta, valid, lane); break;
+      case GKV_INT4: more = int_run<4, PACK, CERT>(p, st, qs, pp, meta, valid, lane); break;
+      case GKV_INT2: more = int_run<2, PACK, CERT>(p, st, qs, pp, meta, valid, lane); break;
+      default: more = centroid_run<PACK, CERT>(p, st, qs, pp, meta, valid, lane); break;
     }
   }
   vm_wait<0>();
@@ -986,6 +1034,7 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   float(*so)[16][D + 1] = (float(*)[16][D + 1])smem;
   float *sm = (float *)(smem + kWaves * 16 * (D + 1) * 4);
   float *sl = sm + kWaves * 16;
+  float *scs = sl + kWaves * 16;  // certificate sums [3][kWaves * 16]
 #pragma unroll
   for (int j = 0; j < 8; ++j)
 #pragma unroll
@@ -993,28 +1042,35 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   if (kg == 0) {
     sm[wave * 16 + m16] = st.m;
     sl[wave * 16 + m16] = st.l;
+    if (CERT) {
+      scs[wave * 16 + m16] = st.c1;
+      scs[kWaves * 16 + wave * 16 + m16] = st.c2;
+      scs[2 * kWaves * 16 + wave * 16 + m16] = st.c3;
+    }
   }
   __syncthreads();
-  float *out = p.part + (u * p.nsplit + sidx) * (int64_t)p.G * (D + 2);
+  float *out = p.part + (u * p.nsplit + sidx) * (int64_t)p.G * kPart;
   for (int i = threadIdx.x; i < p.G * D; i += kThreads) {
     const int g = i >> 7, d = i & 127;
     float M = kNegInf;
 #pragma unroll
     for (int q = 0; q < kWaves; ++q) M = fmaxf(M, sm[q * 16 + g]);
-    float L = 0.f, o = 0.f;
+    float L = 0.f, o = 0.f, cc = 0.f;  // cc: certificate sum d (d < 3)
     if (M > kNegInf) {
 #pragma unroll
       for (int q = 0; q < kWaves; ++q) {
         const float a = __builtin_amdgcn_exp2f(sm[q * 16 + g] - M);
         L = fmaf(sl[q * 16 + g], a, L);
         o = fmaf(so[q][g][d], a, o);
+        if (CERT && d < 3) cc = fmaf(scs[d * kWaves * 16 + q * 16 + g], a, cc);
       }
     }
-    out[g * (D + 2) + 2 + d] = o;
+    out[g * kPart + 2 + d] = o;
     if (d == 0) {
-      out[g * (D + 2)] = M;
-      out[g * (D + 2) + 1] = L;
+      out[g * kPart] = M;
+      out[g * kPart + 1] = L;
     }
+    if (CERT && d < 3) out[g * kPart + D + 2 + d] = cc;
   }
 }
 
@@ -1022,16 +1078,22 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
 // One workgroup per (head, (b, KV head)), one thread per channel: the partials
 // (m_s, l_s, o_s) of the nsplit workgroups combine to o = sum_s a_s o_s / sum_s a_s l_s
 // with a_s = 2^(m_s - max_s m_s).
-__global__ void __launch_bounds__(D) merge_kernel(const float *part, float *out, int nsplit, int G) {
+__global__ void __launch_bounds__(D) merge_kernel(const float *part, float *out, int nsplit, int G, float *bound,
+                                                  const float *cert, int nblk_cap, int nblk) {
   __shared__ float sa[kMaxWaves / kWaves], sl[kMaxWaves / kWaves];
-  __shared__ float sinv;
+  __shared__ float sinv, svm[D];
   const int g = blockIdx.x, d = threadIdx.x;
   const int64_t u = blockIdx.y;
-  const int64_t stride = (int64_t)G * (D + 2);
-  const float *base = part + u * nsplit * stride + g * (D + 2);
+  const int64_t stride = (int64_t)G * kPart;
+  const float *base = part + u * nsplit * stride + g * kPart;
   for (int s2 = d; s2 < nsplit; s2 += D) {
     sa[s2] = base[s2 * stride];
     sl[s2] = base[s2 * stride + 1];
+  }
+  if (bound) {  // max_b vmax_b over the blocks of this (b, KV head)
+    float vm = 0.f;
+    for (int b = d; b < nblk; b += D) vm = fmaxf(vm, cert[(u * nblk_cap + b) * 4 + 2]);
+    svm[d] = vm;
   }
   __syncthreads();
   if (d == 0) {
@@ -1044,6 +1106,17 @@ __global__ void __launch_bounds__(D) merge_kernel(const float *part, float *out,
       L = fmaf(a, sl[s2], L);
     }
     sinv = 1.0f / L;
+    if (bound) {  // section 3.6: sum_b a_b verr_b + min(2, M+/M- - M-/M+) max_j ||v_j||
+      float c1 = 0.f, c2 = 0.f, c3 = 0.f, vm = 0.f;
+      for (int s2 = 0; s2 < nsplit; ++s2) {
+        c1 = fmaf(sa[s2], base[s2 * stride + D + 2], c1);
+        c2 = fmaf(sa[s2], base[s2 * stride + D + 3], c2);
+        c3 = fmaf(sa[s2], base[s2 * stride + D + 4], c3);
+      }
+      for (int i = 0; i < D; ++i) vm = fmaxf(vm, svm[i]);
+      const float r = c2 / c3;
+      bound[u * G + g] = c1 / L + fminf(2.f, r - 1.0f / r) * vm;
+    }
   }
   __syncthreads();
   float o = 0.f;
@@ -1072,7 +1145,8 @@ constexpr int kPlanThreads = 1024;
 struct VisitDesc {
   uint64_t kp, vp;  // addresses of the K and V records
   uint64_t valid;   // tokens of the block that are read (bit t = token t)
-  int32_t level;    // storage level of both records
+  int16_t level;    // storage level of both records
+  uint16_t blk;     // block index (0xFFFF: residual rows or a Compressed-Quest visit)
   uint32_t cost;    // balance cost (bits 0..23) | items (bits 24..26) | units (bits 27..30)
 };
 static_assert(sizeof(VisitDesc) == 32, "descriptor size");
@@ -1192,7 +1266,7 @@ __device__ __forceinline__ void visit_items(const VisitDesc &v, ItemDesc *items,
   auto put = [&](int i, uint32_t kind, bool first, bool last, uint32_t taken, uint32_t n, uint32_t tv) {
     items[i].meta = kind | (lv << 2) | ((uint32_t)first << 7) | ((uint32_t)last << 8) | (taken << 9) | (n << 13) |
                     (tv << 16);
-    items[i].pad = 0;
+    items[i].pad = v.blk;
     items[i].valid = v.valid;
   };
   if (lv == GKV_CENTROID) {
@@ -1238,6 +1312,7 @@ __device__ __forceinline__ VisitDesc dense_visit(const AttnParams &p, int64_t u,
   VisitDesc d;
   if (v < nblk) {
     d.level = p.level[u * p.nblk_cap + v];
+    d.blk = (uint16_t)v;
     d.kp = (uint64_t)(uintptr_t)(p.arena + p.koff[u * p.nblk_cap + v]);
     d.vp = (uint64_t)(uintptr_t)(p.arena + p.voff[u * p.nblk_cap + v]);
     d.valid = token_mask(p.T - v * P);
@@ -1246,6 +1321,7 @@ __device__ __forceinline__ VisitDesc dense_visit(const AttnParams &p, int64_t u,
     const int64_t rb = v - nblk;
     const uint8_t *kp = p.res_rows + (u * p.nrb_cap + rb) * (2 * kExactBytes);
     d.level = GKV_EXACT;
+    d.blk = 0xFFFF;
     d.kp = (uint64_t)(uintptr_t)kp;
     d.vp = (uint64_t)(uintptr_t)(kp + kExactBytes);
     d.valid = token_mask(p.nres - rb * P);
@@ -1403,6 +1479,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
   auto make_visit = [&](int64_t blk, uint32_t tl) {
     VisitDesc d;
     d.level = lvl[blk];
+    d.blk = 0xFFFF;
     d.kp = (uint64_t)(uintptr_t)(p.arena + ko[blk]);
     d.vp = (uint64_t)(uintptr_t)(p.arena + vo[blk]);
     uint64_t va = 0;
@@ -1549,7 +1626,7 @@ static AttnLayout attn_layout(const gkv_cache *c, int32_t topk) {
   L.vcap = topk > 0 ? (int64_t)topk + 1 : (int64_t)c->nblk_cap + (c->nres_cap + P - 1) / P;
   L.icap = 4 * L.vcap;  // at most 4 items per visit
   L.ucap = 8 * L.vcap;  // at most 8 units per visit (an exact block)
-  L.split = align256(units * L.ncap * G * (D + 2) * 4);
+  L.split = align256(units * L.ncap * G * kPart * 4);
   L.visits = L.split + align256(units * 2 * ((int64_t)L.ncap * kWaves + 1) * 4);
   L.plan = L.visits + align256(units * L.vcap * (int64_t)sizeof(VisitDesc));
   L.units = L.plan + align256(units * L.icap * (int64_t)sizeof(ItemDesc));
@@ -1601,6 +1678,8 @@ static gkv_status attn_setup(const uint16_t *q, const gkv_cache *c, const int32_
   p.nrb_cap = (c->nres_cap + P - 1) / P;
   p.topk = topk;
   p.page = c->page ? c->page : 16;
+  p.cert = c->cert;
+  p.bound = nullptr;
   p.nsplit = attn_nsplit(c, topk, c->T);
   p.fast = attn_fast(p.nsplit, (int64_t)c->B * c->Hkv);
   p.sl2 = 1.4426950408889634f / sqrtf((float)D);
@@ -1618,14 +1697,18 @@ static void launch_plan(const AttnParams &p, const gkv_cache *c, hipStream_t s) 
 }
 static void launch_partials(const AttnParams &p, const gkv_cache *c, hipStream_t s) {
   const size_t lds = (size_t)kWaves * kWaveLds + 16 * kQRow;  // rings also hold the merge buffers
-  if (p.G <= 8)
-    hipLaunchKernelGGL(attn_kernel<true>, dim3(p.nsplit * c->Hkv * c->B), dim3(kThreads), lds, s, p);
-  else
-    hipLaunchKernelGGL(attn_kernel<false>, dim3(p.nsplit * c->Hkv * c->B), dim3(kThreads), lds, s, p);
+  const dim3 grid(p.nsplit * c->Hkv * c->B);
+  if (p.bound) {  // the certificate sums are a separate instantiation: the plain decode keeps its registers
+    if (p.G <= 8) hipLaunchKernelGGL((attn_kernel<true, true>), grid, dim3(kThreads), lds, s, p);
+    else hipLaunchKernelGGL((attn_kernel<false, true>), grid, dim3(kThreads), lds, s, p);
+  } else {
+    if (p.G <= 8) hipLaunchKernelGGL((attn_kernel<true, false>), grid, dim3(kThreads), lds, s, p);
+    else hipLaunchKernelGGL((attn_kernel<false, false>), grid, dim3(kThreads), lds, s, p);
+  }
 }
 static void launch_merge(const AttnParams &p, const gkv_cache *c, float *out, hipStream_t s) {
   hipLaunchKernelGGL(merge_kernel, dim3(p.G, c->Hkv * c->B), dim3(D), 0, s, (const float *)p.part, out, p.nsplit,
-                     p.G);
+                     p.G, p.bound, p.cert, c->nblk_cap, (int)((c->T + P - 1) / P));
 }
 
 extern "C" gkv_status gkv_attn_plan(const gkv_cache *c, const int32_t *pages, int32_t topk, void *ws, int64_t ws_bytes,
@@ -1654,6 +1737,20 @@ extern "C" gkv_status gkv_attn_merge(const gkv_cache *c, const int32_t *pages, i
   const gkv_status st = attn_setup(nullptr, c, pages, topk, ws, ws_bytes, p);
   if (st) return st;
   launch_merge(p, c, out, (hipStream_t)stream);
+  return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP;
+}
+
+extern "C" gkv_status gkv_graded_decode_attn_bound(const uint16_t *q, const gkv_cache *c, float *out, float *bound,
+                                                   void *ws, int64_t ws_bytes, void *stream) {
+  if (!q || !out || !bound || !c || !c->cert) return GKV_E_ARG;
+  AttnParams p;
+  const gkv_status st = attn_setup(q, c, nullptr, 0, ws, ws_bytes, p);
+  if (st) return st;
+  p.bound = bound;
+  const hipStream_t s = (hipStream_t)stream;
+  launch_plan(p, c, s);
+  launch_partials(p, c, s);
+  launch_merge(p, c, out, s);
   return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP;
 }
 

@@ -31,6 +31,7 @@ struct EncodeShared {
   uint8_t codes[P * D];    // new codes (int levels)
   int32_t assign[P], prev[P];
   int32_t flag;
+  double cert[2];  // block_cert results
 };
 
 // Exact fp64 value of source element (t, d): an fp16 value, or code * scale + zero
@@ -250,11 +251,56 @@ __device__ void encode_to(EncodeShared &S, uint8_t *dst, int level, int tensor) 
   else encode_centroid(S, dst, tensor);
 }
 
+// Non-negative fp64 -> fp32 rounded towards +inf (the certificate keeps upper
+// bounds): one ulp up when the nearest float lies below.
+__device__ __forceinline__ float round_up_f32(double x) {
+  float f = (float)x;
+  if ((double)f < x) f = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, f) + 1u);
+  return f;
+}
+
+// Certificate numbers of the block just encoded at `level` from the source in S:
+// err = max_t ||x_t - x_hat_t|| and nrm = max_t ||x_t|| over the 64 rows (fp64; x is
+// the source, x_hat the new record's reconstruction).  256 threads: 4 per row, 32
+// channels each.  Result in S.cert[0..1].
+__device__ void block_cert(EncodeShared &S, int level) {
+  const int t = threadIdx.x >> 2, j = threadIdx.x & 3;
+  double e = 0.0, n = 0.0;
+  for (int d = 32 * j; d < 32 * j + 32; ++d) {
+    const double x = getx(S, t, d);
+    double xh = x;
+    if (is_int_level(level)) xh = (double)S.codes[t * D + d] * S.s64[d] + S.z64[d];
+    else if (level == GKV_CENTROID) xh = S.c[S.assign[t] * XS + d];
+    e += (x - xh) * (x - xh);
+    n += x * x;
+  }
+  e += __shfl_xor(e, 1);
+  e += __shfl_xor(e, 2);
+  n += __shfl_xor(n, 1);
+  n += __shfl_xor(n, 2);
+  if (j == 0) {
+    S.dist[t * KC] = e;  // scratch: the k-means distances are no longer needed
+    S.dist[t * KC + 1] = n;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double me = 0.0, mn = 0.0;
+    for (int r = 0; r < P; ++r) {
+      me = S.dist[r * KC] > me ? S.dist[r * KC] : me;
+      mn = S.dist[r * KC + 1] > mn ? S.dist[r * KC + 1] : mn;
+    }
+    S.cert[0] = __builtin_sqrt(me);
+    S.cert[1] = __builtin_sqrt(mn);
+  }
+  __syncthreads();
+}
+
 // Prefill encode: one workgroup per (block, h, b) of one tensor.
 __global__ void __launch_bounds__(kThreads) quantize_kernel(const uint16_t *__restrict__ src, int64_t T_src,
                                                             const int8_t *__restrict__ level,
                                                             const int64_t *__restrict__ off, uint8_t *arena,
-                                                            int Hkv, int nblk_cap, int blk0, int tensor) {
+                                                            int Hkv, int nblk_cap, int blk0, int tensor,
+                                                            float *cert) {
   extern __shared__ __align__(16) unsigned char smem[];
   EncodeShared &S = *reinterpret_cast<EncodeShared *>(smem);
   const int blk = blk0 + blockIdx.x, h = blockIdx.y, b = blockIdx.z;
@@ -263,6 +309,20 @@ __global__ void __launch_bounds__(kThreads) quantize_kernel(const uint16_t *__re
   load_rows(S, src + u * T_src * D, T_src, (int64_t)blk * P);
   __syncthreads();
   encode_to(S, arena + off[u * nblk_cap + blk], lv, tensor);
+  if (cert) {  // error against the exact rows; the value tensor also keeps the row norms
+    __syncthreads();
+    block_cert(S, lv);
+    if (threadIdx.x == 0) {
+      float *cb = cert + (u * nblk_cap + blk) * 4;
+      if (tensor == GKV_KEYS) {
+        cb[0] = round_up_f32(S.cert[0]);
+      } else {
+        cb[1] = round_up_f32(S.cert[0]);
+        cb[2] = round_up_f32(S.cert[1]);
+        cb[3] = 0.f;
+      }
+    }
+  }
 }
 
 constexpr int kMaxDemoteJobs = 64;
@@ -276,8 +336,8 @@ struct DemoteJobs {
 // Demotion: grid (jobs, 2 tensors).  Reads the current record through the device
 // tables, writes the new record, then points the tables at it.
 __global__ void __launch_bounds__(kThreads) demote_kernel(DemoteJobs jobs, int8_t *level, int64_t *koff,
-                                                          int64_t *voff, uint8_t *arena, int Hkv,
-                                                          int nblk_cap) {
+                                                          int64_t *voff, uint8_t *arena, int Hkv, int nblk_cap,
+                                                          float *cert) {
   extern __shared__ __align__(16) unsigned char smem[];
   EncodeShared &S = *reinterpret_cast<EncodeShared *>(smem);
   const int j = blockIdx.x, tensor = blockIdx.y;
@@ -289,6 +349,13 @@ __global__ void __launch_bounds__(kThreads) demote_kernel(DemoteJobs jobs, int8_
   __syncthreads();
   encode_to(S, arena + dst, jobs.to[j], tensor);
   __syncthreads();
+  if (cert) {  // the error grows by at most the change of the reconstruction
+    block_cert(S, jobs.to[j]);
+    if (threadIdx.x == 0) {
+      float *ce = cert + idx * 4 + (tensor == GKV_KEYS ? 0 : 1);
+      *ce = round_up_f32((double)*ce + S.cert[0]);
+    }
+  }
   if (threadIdx.x == 0) {
     offt[idx] = dst;
     if (tensor == GKV_KEYS) level[idx] = jobs.to[j];
@@ -304,7 +371,9 @@ __global__ void __launch_bounds__(128) append_kernel(const uint16_t *__restrict_
                                                      const uint16_t *__restrict__ v_new, int8_t *level,
                                                      int64_t *koff, int64_t *voff, uint8_t *arena,
                                                      uint16_t *boxes, int64_t npage_cap, int page, int Hkv,
-                                                     int nblk_cap, int64_t T, int open_block, NewSlots slots) {
+                                                     int nblk_cap, int64_t T, int open_block, NewSlots slots,
+                                                     float *cert) {
+  __shared__ double vsq[D];
   const int h = blockIdx.x, b = blockIdx.y, d = threadIdx.x;
   const int64_t u = (int64_t)b * Hkv + h;
   const int blk = (int)(T / P), tok = (int)(T % P);
@@ -323,6 +392,25 @@ __global__ void __launch_bounds__(128) append_kernel(const uint16_t *__restrict_
     vo = voff[ti];
   }
   const uint16_t kv = k_new[u * D + d], vv = v_new[u * D + d];
+  if (cert) {  // an exact block: no error; the value norms grow by this row
+    const double x = (double)__builtin_bit_cast(_Float16, vv);
+    vsq[d] = x * x;
+    __syncthreads();
+    if (d == 0) {
+      double n = 0.0;
+      for (int i = 0; i < D; ++i) n += vsq[i];
+      float *cb = cert + ti * 4;
+      const float vn = round_up_f32(__builtin_sqrt(n));
+      if (open_block) {
+        cb[0] = 0.f;
+        cb[1] = 0.f;
+        cb[2] = vn;
+        cb[3] = 0.f;
+      } else {
+        cb[2] = vn > cb[2] ? vn : cb[2];
+      }
+    }
+  }
   // key element (tok, d): page tok>>4, lane ((d>>3)&3)*16 + (tok&15), n = ((d>>5)<<3) | (d&7)
   {
     const int pg = tok >> 4, lane = ((d >> 3) & 3) * 16 + (tok & 15), n = ((d >> 5) << 3) | (d & 7);
@@ -452,7 +540,7 @@ extern "C" gkv_status gkv_quantize_block(const gkv_cache *c, int32_t which, cons
   dim3 grid(blk_end - blk_begin, c->Hkv, c->B);
   hipLaunchKernelGGL(quantize_kernel, grid, dim3(kThreads), sizeof(EncodeShared), (hipStream_t)stream, src,
                      T_src, c->level, which == GKV_KEYS ? c->koff : c->voff, c->arena, c->Hkv, c->nblk_cap,
-                     blk_begin, which);
+                     blk_begin, which, c->cert);
   return hip_status();
 }
 
@@ -489,7 +577,7 @@ extern "C" gkv_status gkv_demote(gkv_cache *c, int32_t n, const int32_t *jobs, c
       J.voff[i] = nv[base + i];
     }
     hipLaunchKernelGGL(demote_kernel, dim3(cnt, 2), dim3(kThreads), sizeof(EncodeShared), (hipStream_t)stream, J,
-                       c->level, c->koff, c->voff, c->arena, c->Hkv, c->nblk_cap);
+                       c->level, c->koff, c->voff, c->arena, c->Hkv, c->nblk_cap, c->cert);
     if (hipGetLastError() != hipSuccess) return GKV_E_HIP;
   }
   for (int i = 0; i < n; ++i)
@@ -540,7 +628,7 @@ extern "C" gkv_status gkv_append(gkv_cache *c, const uint16_t *k_new, const uint
   if (c->page && (T + 1) / c->page > c->npage_cap) return GKV_E_SHAPE;
   hipLaunchKernelGGL(append_kernel, dim3(c->Hkv, c->B), dim3(128), 0, (hipStream_t)stream, k_new, v_new, c->level,
                      c->koff, c->voff, c->arena, c->page ? c->boxes : nullptr, c->npage_cap, c->page ? c->page : 1,
-                     c->Hkv, c->nblk_cap, T, open, slots);
+                     c->Hkv, c->nblk_cap, T, open, slots, c->cert);
   if (hipGetLastError() != hipSuccess) return GKV_E_HIP;
   if (open)
     for (int64_t u = 0; u < (int64_t)c->B * c->Hkv; ++u) c->level_host[u * c->nblk_cap + blk] = GKV_EXACT;

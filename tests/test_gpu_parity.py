@@ -428,3 +428,87 @@ def test_quest_1m_sampled(gpu):
         uc = types.SimpleNamespace(k_recs={blk: ko}, v_recs={blk: vo})
         compare_record(cache, uc, 0, h, blk, 0)
         compare_record(cache, uc, 0, h, blk, 1)
+
+
+def _cert_compare(cache, uc, b, h):
+    """The cache's per-block certificate numbers against the oracle's: fp32 rounded
+    upwards from fp64, so never below and within a few ulps above."""
+    nblk = len(uc.levels)
+    got = cache.cert[b, h, :nblk, :3].cpu().numpy().astype(np.float64)
+    want = np.stack([uc.kerr, uc.verr, uc.vmax], 1)
+    assert np.all(got >= want * (1 - 1e-12))
+    assert np.all(got <= want * (1 + 1e-6) + 1e-30)
+
+
+def _bound_close(got, want):
+    assert np.all(np.abs(got - want) <= 2e-3 * want + 1e-6), (got, want)
+
+
+@pytest.mark.parametrize("prof,T,Bn", [("tiny", 2048, 1), ("graded", 5000, 2), ("int8", 2048, 1)])
+def test_certificate_numbers_and_bound(gpu, prof, T, Bn):
+    """Decode-time attention error certificate (section 3.6): per-block numbers written
+    by the encoder and the per-head bound from the attention kernel and merge, against
+    the oracle; the output equals the plain decode bit for bit."""
+    torch = _torch()
+    Hq, Hkv = 8, 2
+    ks, vs = kv_all(6, Bn, Hkv, T)
+    lv = np.full(T // 64, olad.INT8, np.int8) if prof == "int8" else olad.ladder(prof, T)
+    cache = _build(gpu, ks, vs, Hq, lv)
+    q = synth.queries(6, Bn, Hq)
+    out, bnd = cache.decode_bound(q)
+    assert torch.equal(out, cache.decode(q))
+    bnd = bnd.cpu().numpy()
+    G = Hq // Hkv
+    for b in range(Bn):
+        for h in range(Hkv):
+            uc = ocache.UnitCache(ks[b, h], vs[b, h], lv)
+            _cert_compare(cache, uc, b, h)
+            _bound_close(bnd[b, h * G:(h + 1) * G], uc.certificate(q_group(q, b, h, G)))
+    if prof == "int8":  # informative: well below the universal cap of 2 max ||v||
+        assert np.all(bnd < 0.5 * 2 * cache.cert[..., 2].max().item())
+
+
+def test_certificate_with_residual_rows(gpu):
+    """Residual rows count as exact in the bound."""
+    T, Hq, Hkv = 3000, 8, 2
+    ks, vs = kv_all(7, 1, Hkv, T)
+    lv = olad.ladder("graded", T)
+    n = ores.n_keep(T, 2)
+    cache = _build(gpu, ks, vs, Hq, lv, nres_cap=n)
+    mass = np.stack([synth.mass_unit(7, 0, h, T) for h in range(Hkv)])[None]
+    cache.rd_residual_select(ks, vs, mass, n)
+    q = synth.queries(7, 1, Hq)
+    _, bnd = cache.decode_bound(q)
+    bnd = bnd.cpu().numpy()
+    G = Hq // Hkv
+    for h in range(Hkv):
+        uc = ocache.UnitCache(ks[0, h], vs[0, h], lv)
+        uc.select_residual(ks[0, h], vs[0, h], mass[0, h], n)
+        _bound_close(bnd[0, h * G:(h + 1) * G], uc.certificate(q_group(q, 0, h, G)))
+
+
+def test_certificate_through_appends_and_demotions(gpu):
+    """Appends open exact blocks and raise the value norms; demotions raise the
+    errors by the change of the reconstruction; the bound follows the oracle."""
+    Hq, Hkv = 8, 2
+    T0 = 64 * 40 - 3
+    steps = 70
+    ks, vs = kv_all(8, 1, Hkv, T0 + steps)
+    lv = olad.ladder("graded", T0)
+    cache = _build(gpu, ks[:, :, :T0], vs[:, :, :T0], Hq, lv, extra_blocks=4,
+                   slack={16: 8, 8: 8, 4: 8, 2: 8, 1: 8})
+    ucs = [ocache.UnitCache(ks[0, h, :T0], vs[0, h, :T0], lv) for h in range(Hkv)]
+    nmoves = 0
+    for s in range(steps):
+        t = T0 + s
+        nmoves += len(cache.append(ks[:, :, t], vs[:, :, t], profile="graded"))
+        for h in range(Hkv):
+            ucs[h].append(ks[0, h, t], vs[0, h, t], "graded")
+    assert nmoves > 0
+    q = synth.queries(8, 1, Hq)
+    _, bnd = cache.decode_bound(q)
+    bnd = bnd.cpu().numpy()
+    G = Hq // Hkv
+    for h in range(Hkv):
+        _cert_compare(cache, ucs[h], 0, h)
+        _bound_close(bnd[0, h * G:(h + 1) * G], ucs[h].certificate(q_group(q, 0, h, G)))
