@@ -301,6 +301,12 @@ def main():
             caches[0].account()
         phases["accounting_host_us"] = round((time.perf_counter() - ta) / 100 * 1e6, 1)
         del small
+        # the decode step with the attention error certificate (section 3.6)
+        for _ in range(3):
+            caches[0].decode_bound(qs[0])
+        phases["decode_with_certificate_us"] = round(timed(lambda: caches[0].decode_bound(qs[0]), 20) * 1e3, 1)
+        _, bnd = caches[0].decode_bound(qs[0])
+        phases["certificate_bound_mean_max"] = [round(float(bnd.mean()), 4), round(float(bnd.max()), 4)]
         # a second denominator: what a plain library reduction reads per second
         big = torch.zeros(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB
         for _ in range(3):
