@@ -7,6 +7,7 @@ Per tensor block of P = 64 tokens x D = 128 channels:
     exact     P * D * 16
     int b     P * D * b + D * 2 * 16          (fp16 scale and zero per channel)
     centroid  K * D * 16 + P * log2(K)        (K = 4 fp16 centroids, 2-bit ids)
+    mean      D * 16                          (one fp16 centroid, no ids)
 
 Compressed-Quest adds 2 * D * 16 bits of exact box per closed page
 (R_resident = R_graded + sum of boxes) and reads, per query, all stored boxes
@@ -23,7 +24,7 @@ override mask per block while a residual exists.
 Values are normalised by B * Hkv * T * 2 * D (keys and values).  The newest
 block is always fully allocated, so a partial block counts whole.
 """
-from .ladder import EXACT, INT8, INT4, INT2, CENTROID
+from .ladder import EXACT, INT8, INT4, INT2, CENTROID, MEAN
 
 P, D = 64, 128
 KCENT = 4
@@ -38,6 +39,8 @@ def block_bits(level, P=P, D=D):
         return P * D * level + D * 2 * 16
     if level == CENTROID:
         return KCENT * D * 16 + P * IDBITS
+    if level == MEAN:
+        return D * 16
     raise ValueError(level)
 
 
@@ -48,6 +51,8 @@ def block_overhead_bits(level, D=D):
         return D * 2 * 16
     if level == CENTROID:
         return KCENT * D * 16
+    if level == MEAN:
+        return D * 16
     return 0
 
 
@@ -60,6 +65,8 @@ def row_bits(level, D=D):
         return D * level
     if level == CENTROID:
         return IDBITS
+    if level == MEAN:
+        return 0
     raise ValueError(level)
 
 

@@ -1,7 +1,8 @@
 """Monotone precision ladder by block age (Method, section 3.2).
 
 The cache is cut into blocks of P = 64 tokens; each block holds one level of
-{16 (exact fp16), 8, 4, 2 (packed scalar codes), 1 (centroid state)}.  A block
+{16 (exact fp16), 8, 4, 2 (packed scalar codes), 1 (centroid state with 4
+centroids), 0 (one-centroid state: the block mean, no per-token code)}.  A block
 only ever moves down the ladder as it ages: there is no promotion, because once
 demoted its dense data no longer exists.
 
@@ -18,12 +19,12 @@ Levels are returned per block, index 0 = oldest block.
 """
 import numpy as np
 
-EXACT, INT8, INT4, INT2, CENTROID = 16, 8, 4, 2, 1
-LEVELS = (EXACT, INT8, INT4, INT2, CENTROID)
+EXACT, INT8, INT4, INT2, CENTROID, MEAN = 16, 8, 4, 2, 1, 0
+LEVELS = (EXACT, INT8, INT4, INT2, CENTROID, MEAN)
 BLOCK = 64
 
 # rank of a level on the ladder: larger = more precise
-ORDER = {CENTROID: 0, INT2: 1, INT4: 2, INT8: 3, EXACT: 4}
+ORDER = {MEAN: 0, CENTROID: 1, INT2: 2, INT4: 3, INT8: 4, EXACT: 5}
 
 
 def n_blocks(T, P=BLOCK):
@@ -74,12 +75,25 @@ def graded_ladder(nblk, exact_blocks=16, pct8=25, pct84=60, pct_centroid=10):
     return lv
 
 
+def rdv2_ladder(nblk, exact_blocks=16):
+    """Low-rate RD-V2 base (section 3.4, the variation with a nearly centroid-only
+    base): the newest ``exact_blocks`` blocks exact, every older block in the
+    one-centroid state.  The exact residual (about 10.2% of the tokens) is kept on
+    top of it.
+    """
+    lv = np.full(nblk, MEAN, dtype=np.int8)
+    lv[max(nblk - exact_blocks, 0):] = EXACT
+    return lv
+
+
 def ladder(profile, T):
     nblk = n_blocks(T)
     if profile == "tiny":
         return tiny_ladder(nblk)
     if profile == "graded":
         return graded_ladder(nblk)
+    if profile == "rdv2":
+        return rdv2_ladder(nblk)
     if profile == "exact":
         return np.full(nblk, EXACT, dtype=np.int8)
     raise ValueError(profile)

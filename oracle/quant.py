@@ -27,11 +27,16 @@ these are chosen because both sides can reproduce them exactly in fp64):
   stored fp16 centroids (what is stored is what is decoded).
   Parity of the centroid choices themselves is unpinned by the paper (no worked
   example); the invariants in the tests pin the implementation.
+* One-centroid state (level 0): the same iteration with k = 1 (initial centroid
+  row 0).  Every token is assigned to it, so one update gives the ascending-token
+  fp64 mean and the next round repeats the assignment: the state is the fp16 of
+  the block mean, which is the value centroid of Eq. rdscore.  A sum of 64 fp16
+  values is exact in fp64, so this is the correctly rounded mean.
 """
 import numpy as np
 
 from . import fp16
-from .ladder import EXACT, INT8, INT4, INT2, CENTROID, ORDER
+from .ladder import EXACT, INT8, INT4, INT2, CENTROID, MEAN, ORDER
 
 P, D = 64, 128
 KCENT = 4
@@ -40,12 +45,12 @@ KCENT = 4
 class Record:
     """One encoded tensor block.
 
-    level      one of 16, 8, 4, 2, 1
+    level      one of 16, 8, 4, 2, 1, 0
     exact      uint16 [P][D] fp16 bits              (level 16)
     codes      int32  [P][D] in [0, 2^b - 1]        (levels 8/4/2)
     s16, z16   uint16 [D] fp16 bits                 (levels 8/4/2)
-    cent16     uint16 [KCENT][D] fp16 bits          (level 1)
-    ids        int32  [P] in [0, KCENT)             (level 1)
+    cent16     uint16 [KCENT][D] fp16 bits          (level 1; [1][D] at level 0)
+    ids        int32  [P] in [0, KCENT)             (level 1; all 0 at level 0)
     """
 
     def __init__(self, level, **kw):
@@ -142,6 +147,9 @@ def encode(level, x):
     if level == CENTROID:
         cent16, ids = kmeans_centroids(x)
         return Record(CENTROID, cent16=cent16, ids=ids)
+    if level == MEAN:
+        cent16, ids = kmeans_centroids(x, k=1)
+        return Record(MEAN, cent16=cent16, ids=ids)
     raise ValueError(level)
 
 
@@ -159,7 +167,7 @@ def decode(rec):
         return fp16.to_f64(rec.exact)
     if rec.level in (INT8, INT4, INT2):
         return dequant_scalar(rec.codes, rec.s16, rec.z16)
-    if rec.level == CENTROID:
+    if rec.level in (CENTROID, MEAN):
         return dequant_centroid(rec.cent16, rec.ids)
     raise ValueError(rec.level)
 

@@ -13,7 +13,8 @@ Readings (listed in the design notes):
 * e_j = sum over channels, ascending, of fl(fl(v_jd - v_hat_jd)^2) in fp64 with
   separate multiply and add (v - v_hat is exact in fp64);
   s_j = fl(a_j * e_j) with a_j the fp32 mass widened to fp64.
-* n = floor(frac * T) tokens per (sequence, KV head) are kept: the first n of the
+* n = floor(frac * T) tokens per (sequence, KV head) are kept (frac a ratio of
+  integers, floored once): the first n of the
   order (s descending, token index ascending), reported ascending.
 """
 import numpy as np
@@ -36,8 +37,10 @@ def scores(v_exact, v_hat, mass_f32):
     return a * distortion(v_exact, v_hat) + 0.0
 
 
-def n_keep(T, frac_percent=2):
-    return (int(frac_percent) * int(T)) // 100
+def n_keep(T, frac=2, den=100):
+    """Rows kept for an exact fraction frac / den (2% by default; RD-V2 keeps
+    102 / 1000)."""
+    return (int(frac) * int(T)) // int(den)
 
 
 def select(s, n):

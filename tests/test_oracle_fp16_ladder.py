@@ -79,7 +79,7 @@ def test_tiny_ladder_token_bands():
     lv = ladder.ladder("tiny", 2048)
     toks = {L: 64 * int((lv == L).sum()) for L in ladder.LEVELS}
     # newest 256 exact, next 512 int8, next 768 int4, oldest 512 int2
-    assert toks == {16: 256, 8: 512, 4: 768, 2: 512, 1: 0}
+    assert toks == {16: 256, 8: 512, 4: 768, 2: 512, 1: 0, 0: 0}
     assert lv[-1] == 16 and lv[0] == 2
 
 
@@ -104,7 +104,7 @@ def _rank(lv):
     return np.array([ladder.ORDER[int(x)] for x in lv])
 
 
-@pytest.mark.parametrize("profile", ["tiny", "graded"])
+@pytest.mark.parametrize("profile", ["tiny", "graded", "rdv2"])
 def test_ladder_monotone_in_age_and_time(profile):
     prev = None
     for nb in range(1, 2600):

@@ -154,3 +154,42 @@ def test_demote_chain_and_no_promotion():
     d4 = quant.demote(r8, 4)
     c, s, z = quant.quantize_scalar(quant.decode(r8), 4)
     assert np.array_equal(d4.codes, c) and np.array_equal(d4.s16, s) and np.array_equal(d4.z16, z)
+
+
+def test_mean_level_is_correctly_rounded_block_mean():
+    """Level 0 stores the fp16 of the exact block mean (rational arithmetic here,
+    numpy's own fp16 rounding for the reference), and decodes every row to it."""
+    x = _block(9, scale=3.0)
+    rec = quant.encode(0, x)
+    exact_mean = [sum(Fraction(v) for v in x[:, d]) / 64 for d in range(128)]
+    ref = np.array([float(m) for m in exact_mean]).astype(np.float16).view(np.uint16)
+    ref = np.where(ref == 0x8000, 0, ref)  # negative zero is stored as +0
+    assert rec.cent16.shape == (1, 128)
+    assert np.array_equal(rec.cent16[0], ref)
+    assert np.all(rec.ids == 0)
+    dec = quant.decode(rec)
+    assert np.array_equal(dec, np.repeat(fp16.to_f64(ref[None, :]), 64, axis=0))
+
+
+def test_mean_level_demotion_from_centroid_weights_by_count():
+    """Demoting a 4-centroid block to level 0 averages its reconstruction, i.e.
+    the centroids weighted by their token counts."""
+    x = _block(10)
+    c1 = quant.encode(1, x)
+    m = quant.demote(c1, 0)
+    c = fp16.to_f64(c1.cent16)
+    cnt = np.bincount(c1.ids, minlength=4)
+    exact = [sum(Fraction(int(cnt[k])) * Fraction(c[k, d]) for k in range(4)) / 64 for d in range(128)]
+    ref = np.array([float(e) for e in exact]).astype(np.float16).view(np.uint16)
+    ref = np.where(ref == 0x8000, 0, ref)
+    assert np.array_equal(m.cent16[0], ref)
+    # level 0 is the bottom of the ladder: nothing is below it, and no promotion
+    for to in (1, 2, 16):
+        with pytest.raises(quant.NotMonotone):
+            quant.demote(m, to)
+    with pytest.raises(quant.NotMonotone):
+        quant.demote(m, 0)
+    chain = quant.encode_fp16(16, fp16.from_f64(x))
+    for lv in (8, 4, 2, 1, 0):
+        chain = quant.demote(chain, lv)
+    assert chain.level == 0

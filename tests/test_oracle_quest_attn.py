@@ -140,8 +140,66 @@ def test_rd_score_on_centroid_block_is_equation():
 
 
 def test_level_bits_per_value():
-    got = [accounting.block_bits(L) / (64 * 128) for L in (16, 8, 4, 2, 1)]
-    assert got == [16.0, 8.5, 4.5, 2.5, 1.015625]
+    got = [accounting.block_bits(L) / (64 * 128) for L in (16, 8, 4, 2, 1, 0)]
+    assert got == [16.0, 8.5, 4.5, 2.5, 1.015625, 0.25]
+    # the one-centroid state costs one exact row per block and nothing per token
+    assert accounting.block_bits(0) == accounting.row_bits(16)
+    assert accounting.row_bits(0) == 0
+
+
+def test_mean_blocks_attend_as_counted_single_keys():
+    """Closed form: every token of a level-0 block has the same key and value, so
+    the block acts as ONE key whose weight is multiplied by its token count
+    (log-count added to the logit); residual tokens leave their block's count."""
+    T = 64 * 6
+    k, v = synth.kv_unit(211, 0, 0, T)
+    lv = np.array([0, 0, 0, 0, 16, 16], dtype=np.int8)
+    uc = cache.UnitCache(k, v, lv)
+    m = synth.mass_unit(211, 0, 0, T)
+    idx, _ = uc.select_residual(k, v, m, 40)
+    q = synth.queries(211, 1, 3)[0]
+    got = uc.decode_dense(q)
+    kf, vf, qf = fp16.to_f64(k), fp16.to_f64(v), fp16.to_f64(q)
+    res = set(int(j) for j in idx)
+    for g in range(3):
+        logits, vals = [], []
+        for b in range(4):
+            means_k = quant.decode(quant.encode(0, kf[64 * b:64 * b + 64]))[0]
+            means_v = quant.decode(quant.encode(0, vf[64 * b:64 * b + 64]))[0]
+            n = sum(1 for j in range(64 * b, 64 * b + 64) if j not in res)
+            if n:
+                logits.append(float(qf[g] @ means_k) / np.sqrt(128) + np.log(n))
+                vals.append(means_v)
+        # residual rows of the level-0 blocks, then the exact blocks, read exactly
+        for j in sorted(r for r in res if r < 256) + list(range(256, T)):
+            logits.append(float(qf[g] @ kf[j]) / np.sqrt(128))
+            vals.append(vf[j])
+        logits = np.array(logits)
+        w = np.exp(logits - logits.max())
+        ref = (w[:, None] * np.array(vals)).sum(0) / w.sum()
+        np.testing.assert_allclose(got[g], ref, rtol=1e-10, atol=1e-12)
+
+
+def test_rdv2_ladder_and_rates():
+    """RD-V2: newest 16 blocks exact, older blocks one-centroid; growth only
+    demotes exact blocks straight to level 0, once each; with 10.2% exact residual
+    rows the resident rate at 128k tokens is 0.25 bpv of base plus the exact
+    window plus 16 bits, a 32-bit index per row and one mask per block."""
+    lv = ladder("rdv2", 131072)
+    assert (lv == 16).sum() == 16 and (lv == 0).sum() == 2048 - 16 and np.all(lv[-16:] == 16)
+    from oracle import ladder as lad
+    for T0 in (64 * 16, 64 * 16 + 1, 5000):
+        cr = lad.crossings("rdv2", T0, T0 + 64)
+        assert all(o == 16 and n == 0 for _, o, n in cr)
+        assert len(cr) == (1 if lad.n_blocks(T0) >= 16 else 0)
+    n = residual.n_keep(131072, 102, 1000)
+    assert n == 13369
+    r = accounting.unit_rates(lv, 131072, nres=n)
+    vals = 131072 * 2 * 128
+    base = (16 * 64 * 128 * 16 + 2032 * 128 * 16) * 2
+    res = n * (2 * 128 * 16 + 32) + 2048 * 64
+    assert r["resident_bits"] == base + res
+    assert abs(r["resident_bits"] / vals - 2.0217) < 1e-4
 
 
 def test_tiny_and_llama_graded_rates():
