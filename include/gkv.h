@@ -4,8 +4,8 @@
  * Method: Geodesia-KV (arXiv 2608.23599).  One layer's KV cache is cut into
  * blocks of P = 64 tokens per (sequence b, KV head h); every block holds one level
  * of a monotone precision ladder (section 3.2): exact fp16, block-scaled 8/4/2-bit
- * scalar codes with fp16 per-channel scale and zero, or 4 fp16 centroids with
- * per-token ids.  Single-query (Q = 1) GQA decode attention reads the graded
+ * scalar codes with fp16 per-channel scale and zero, 4 fp16 centroids with
+ * per-token ids, or one fp16 centroid (the block mean).  Single-query (Q = 1) GQA decode attention reads the graded
  * blocks, dequantizing inside an online-softmax loop (section 3.7); optional
  * exact per-page key boxes rank pages for a sparse read (Compressed-Quest,
  * section 3.5); an optional exact residual keeps the tokens with the largest
@@ -45,8 +45,11 @@ typedef enum gkv_status {
   GKV_E_UNSUPPORTED = -6   /* valid but not implemented combination            */
 } gkv_status;
 
-/* Ladder levels; the numeric value is the bits of a code (1 = centroid state). */
+/* Ladder levels; the numeric value is the bits of a code (1 = centroid state with
+ * 4 centroids, 0 = one-centroid state: the block mean, no per-token code).  The
+ * numeric order is the ladder order. */
 typedef enum gkv_level {
+  GKV_MEAN = 0,
   GKV_CENTROID = 1,
   GKV_INT2 = 2,
   GKV_INT4 = 4,
@@ -86,6 +89,8 @@ typedef enum gkv_tensor { GKV_KEYS = 0, GKV_VALUES = 1 } gkv_tensor;
  * GKV_CENTROID (1040 B): 4 x 128 fp16 centroids, then 64 two-bit ids (16 B; the
  *   id of token t is bits 2t..2t+1).  Key centroids are stored [centroid][channel];
  *   value centroids [channel & 15][channel >> 4][centroid].
+ * GKV_MEAN (256 B): 128 fp16 values in channel order (keys and values alike); every
+ *   token of the block reads this row.
  *
  * Residual rows (section 3.4) are stored as exact-format pseudo-blocks: row r of
  * (b,h) is "token" r & 63 of pseudo-block r >> 6, whose K record is followed by
@@ -138,7 +143,9 @@ int64_t gkv_block_bytes(int32_t level);
  *   1 "graded": newest 16 exact; int8 / int4 boundaries at 16 + floor(25R/100) and
  *               16 + floor(60R/100), R = nblk - 16; oldest floor(10*nblk/100) blocks
  *               centroid (the exact window takes precedence); rest int2;
- *   2 "exact":  all exact.
+ *   2 "exact":  all exact;
+ *   3 "rdv2":   newest 16 exact, every older block one-centroid (the low-rate RD-V2
+ *               base of section 3.4, used with an exact residual of about 10.2%).
  * Writes levels for blocks 0..nblk-1 (0 = oldest) of a context of T tokens. */
 gkv_status gkv_ladder_levels(int32_t profile, int64_t T, int8_t *levels_host, int32_t nblk);
 
@@ -152,10 +159,10 @@ int32_t gkv_ladder_crossings(const gkv_cache *c, int32_t profile, int64_t T_new,
                              int8_t *to_host, int32_t max_jobs);
 
 /* Slab arena: per-level pools of fixed-size slots inside one device buffer.
- * cap[i] = slots for level {16,8,4,2,1}[i].  Offsets are byte offsets into the
+ * cap[i] = slots for level {16,8,4,2,1,0}[i].  Offsets are byte offsets into the
  * arena; the pool is host-only bookkeeping (single-threaded). */
 typedef struct gkv_pool gkv_pool;
-gkv_pool *gkv_pool_create(const int64_t cap_host[5]);
+gkv_pool *gkv_pool_create(const int64_t cap_host[6]);
 int64_t gkv_pool_bytes(const gkv_pool *p);
 int64_t gkv_pool_alloc(gkv_pool *p, int32_t level); /* -1 when the pool is full */
 gkv_status gkv_pool_free(gkv_pool *p, int32_t level, int64_t offset);
@@ -174,8 +181,8 @@ gkv_status gkv_account(const gkv_cache *c, const int32_t *pages_host, int32_t to
 /* Decode one record (host copy) to codes / values, for inspection and tests.
  * values_host: [64][128] fp64 reconstruction (token-major); codes_host (optional,
  * int levels): [64][128]; scale_host, zero_host (optional, int levels): [128] fp16
- * in channel order; ids_host (optional, centroid): [64]; cent_host (optional,
- * centroid): [4][128] fp16. */
+ * in channel order; ids_host (optional, centroid or mean): [64]; cent_host
+ * (optional): [4][128] fp16 for a centroid record, [128] for a mean record. */
 gkv_status gkv_decode_record(int32_t level, int32_t tensor, const uint8_t *rec_host, double *values_host,
                              int32_t *codes_host, uint16_t *scale_host, uint16_t *zero_host,
                              int32_t *ids_host, uint16_t *cent_host);
@@ -200,7 +207,8 @@ int64_t gkv_workspace_bytes(const gkv_cache *c, int32_t op, int32_t topk);
  * the per-channel asymmetric quantizer z = f16(min), s = f16((max-min)/(2^b-1)),
  * code = rint((x-z)/s) clamped, in fp64; centroid blocks run 4-means Lloyd in fp64
  * (rows 0,16,32,48 initial, at most 10 rounds, fp16 centroids, ids re-assigned
- * against the stored centroids). */
+ * against the stored centroids); mean blocks store the fp16 of the block mean (the
+ * same iteration with one centroid; the fp64 token-ascending sum is exact). */
 gkv_status gkv_quantize_block(const gkv_cache *c, int32_t which, const uint16_t *src, int64_t T_src,
                               int32_t blk_begin, int32_t blk_end, void *stream);
 

@@ -20,10 +20,10 @@ if not os.path.exists(_LIB_PATH):
     raise ImportError(f"{_LIB_PATH} is not built; run __graft_entry__.build()")
 lib = ctypes.CDLL(_LIB_PATH)
 
-EXACT, INT8, INT4, INT2, CENTROID = 16, 8, 4, 2, 1
-LEVELS = (EXACT, INT8, INT4, INT2, CENTROID)
+EXACT, INT8, INT4, INT2, CENTROID, MEAN = 16, 8, 4, 2, 1, 0
+LEVELS = (EXACT, INT8, INT4, INT2, CENTROID, MEAN)
 KEYS, VALUES = 0, 1
-PROFILES = {"tiny": 0, "graded": 1, "exact": 2}
+PROFILES = {"tiny": 0, "graded": 1, "exact": 2, "rdv2": 3}
 P, D = 64, 128
 
 _vp, _i32, _i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
@@ -142,6 +142,8 @@ def decode_record(level, tensor, rec):
         out.update(codes=codes, s16=s, z16=z)
     if level == CENTROID:
         out.update(ids=ids, cent16=cent)
+    if level == MEAN:
+        out.update(ids=ids, cent16=cent[:1].copy())
     return out
 
 

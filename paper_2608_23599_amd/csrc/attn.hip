@@ -289,7 +289,8 @@ __device__ __forceinline__ int64_t uni64(int64_t x) {
 //                 int8 unit [K codes of n tiles], unit [V codes of n tiles]  (n
 //                 consecutive read tiles of one block, at most 4 KB of codes per record)
 //   centroid:     unit [K record | V record]
-enum ItemKind { kExactTile = 0, kIntGroup = 1, kCentroid = 2 };
+//   mean:         unit [K row | V row]
+enum ItemKind { kExactTile = 0, kIntGroup = 1, kCentroid = 2, kMean = 3 };
 
 // Item descriptor.  meta: kind (2 bits) | level (5) | first (1) | last (1) | tile
 // mask (4) | tile count (3) | exact tile's valid-token bits (16).
@@ -879,6 +880,35 @@ __device__ __forceinline__ void centroid_item(const AttnParams &p, State &st, co
   if (CERT) cert_add(st, lsum, cb[0], cb[1]);
 }
 
+// One-centroid block: one unit with the key row at +0 and the value row at +2 KB.
+// All read tokens share one key and one value, so the block adds one logit per head
+// with weight (tokens read) x exp, and that weight times the value row.
+template <bool PACK, bool CERT>
+__device__ __forceinline__ void mean_item(const AttnParams &p, State &st, const uint8_t *qs, const uint8_t *ip,
+                                          uint64_t valid, int lane, const float *cb) {
+  const int kg = lane >> 4;
+  // every row of A is the key row, so each output row holds the logit of the column's head
+  f4 sc = {0, 0, 0, 0};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    U8 a;
+    a.v = lds16(ip + (8 * kg + 32 * i) * 2);
+    sc = mfma32(a.h, qchunk<PACK>(qs, lane, i), sc);
+  }
+  rescale_factor(st, sc[0] * p.sl2);
+  const float w = (float)__popcll(valid) * __builtin_amdgcn_exp2f(fmaf(sc[0], p.sl2, -st.m));
+  // O[channel 16j + 4kg + r][head] += w * v[channel]
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    U4 v;
+    *(uint2 *)v.u = *(const uint2 *)(ip + 2048 + (16 * j + 4 * kg) * 2);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) st.O[j][r] = fmaf(w, (float)v.h[r], st.O[j][r]);
+  }
+  st.l += w;
+  if (CERT) cert_add(st, w, cb[0], cb[1]);
+}
+
 // Runs: process items of one level until the next item has another level (its
 // descriptor left in meta/valid) or the items end (returns false).
 template <bool PACK, bool CERT>
@@ -954,6 +984,17 @@ __device__ __forceinline__ bool centroid_run(const AttnParams &p, State &st, con
 }
 
 template <bool PACK, bool CERT>
+__device__ __forceinline__ bool mean_run(const AttnParams &p, State &st, const uint8_t *qs, Pipe &pp,
+                                         uint32_t &meta, uint64_t &valid, int lane) {
+  do {
+    mean_item<PACK, CERT>(p, st, qs, pp.template pop<0>(), valid, lane, CERT ? pp.cert + pp.blk * 4 : nullptr);
+    pp.release(1);
+    if (!pp.template next_item<CERT>(meta, valid)) return false;
+  } while (meta_lv(meta) == GKV_MEAN);
+  return true;
+}
+
+template <bool PACK, bool CERT>
 __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   extern __shared__ __align__(16) uint8_t smem[];
   // Workgroup L of the one-dimensional grid serves (b, KV head) L % units as its
@@ -1024,7 +1065,8 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
       case GKV_INT8: more = int_run<8, PACK, CERT>(p, st, qs, pp, meta, valid, lane); break;
       case GKV_INT4: more = int_run<4, PACK, CERT>(p, st, qs, pp, meta, valid, lane); break;
       case GKV_INT2: more = int_run<2, PACK, CERT>(p, st, qs, pp, meta, valid, lane); break;
-      default: more = centroid_run<PACK, CERT>(p, st, qs, pp, meta, valid, lane); break;
+      case GKV_CENTROID: more = centroid_run<PACK, CERT>(p, st, qs, pp, meta, valid, lane); break;
+      default: more = mean_run<PACK, CERT>(p, st, qs, pp, meta, valid, lane); break;
     }
   }
   vm_wait<0>();
@@ -1155,13 +1197,14 @@ static_assert(sizeof(VisitDesc) == 32, "descriptor size");
 // share of the bandwidth (8 KB each), int tiles by the dequantisation and softmax
 // work rather than by their bytes.
 constexpr uint32_t kCostExactTile = 523, kCostInt8Tile = 426, kCostInt4Tile = 305, kCostInt2Tile = 260,
-                   kCostCentroid = 711, kCostIntBlock = 248;
+                   kCostCentroid = 711, kCostIntBlock = 248, kCostMean = 300;
 
 __device__ __forceinline__ uint32_t balance_cost(int lv, uint64_t va) {
   uint32_t tiles = 0;
   for (int t = 0; t < 4; ++t) tiles += ((va >> (16 * t)) & 0xFFFFull) != 0;
   if (!tiles) return 0;
   if (lv == GKV_CENTROID) return kCostCentroid;
+  if (lv == GKV_MEAN) return kCostMean;
   if (lv == GKV_EXACT) return tiles * kCostExactTile;
   const uint32_t per = lv == 8 ? kCostInt8Tile : (lv == 4 ? kCostInt4Tile : kCostInt2Tile);
   return kCostIntBlock + tiles * per;
@@ -1229,7 +1272,7 @@ __device__ __forceinline__ uint32_t visit_counts(int lv, uint64_t valid) {
   for (int t = 0; t < 4; ++t)
     if ((valid >> (16 * t)) & 0xFFFFull) tiles |= 1u << t;
   if (!tiles) return 0;
-  if (lv == GKV_CENTROID) return 1u | (1u << 3);
+  if (lv == GKV_CENTROID || lv == GKV_MEAN) return 1u | (1u << 3);
   if (lv == GKV_EXACT) return (uint32_t)__builtin_popcount(tiles) * (1u | (2u << 3));
   const int tg = group_tiles(lv);
   uint32_t k = 0;
@@ -1272,6 +1315,11 @@ __device__ __forceinline__ void visit_items(const VisitDesc &v, ItemDesc *items,
   if (lv == GKV_CENTROID) {
     put(0, kCentroid, true, true, tiles, 1, 0);
     units[0] = unit_desc(v.kp, kCentBytes, v.vp, kCentBytes);
+    return;
+  }
+  if (lv == GKV_MEAN) {
+    put(0, kMean, true, true, tiles, 1, 0);
+    units[0] = unit_desc(v.kp, kMeanBytes, v.vp, kMeanBytes);
     return;
   }
   int k = 0, m = 0;

@@ -72,6 +72,13 @@ __device__ void load_record(EncodeShared &S, const uint8_t *rec, int level, int 
     }
     return;
   }
+  if (level == GKV_MEAN) {  // one centroid: every token reads it
+    if (threadIdx.x == 0) S.src_int = 2;
+    const uint16_t *cc = (const uint16_t *)rec;
+    for (int d = threadIdx.x; d < D; d += kThreads) S.sc[d] = (double)__builtin_bit_cast(_Float16, cc[d]);
+    for (int t = threadIdx.x; t < P; t += kThreads) S.xc[t * D] = 0;
+    return;
+  }
   if (level == GKV_CENTROID) {
     if (threadIdx.x == 0) S.src_int = 2;
     const uint16_t *cc = (const uint16_t *)rec;
@@ -245,9 +252,25 @@ __device__ void encode_centroid(EncodeShared &S, uint8_t *dst, int tensor) {
   }
 }
 
+// One-centroid state: the Lloyd iteration with one centroid converges in one
+// update to the block mean; the fp64 token-ascending sum of 64 fp16 values (or of
+// decoded values) is the same sum the iteration takes, then one fp16 rounding.
+__device__ void encode_mean(EncodeShared &S, uint8_t *dst) {
+  const int tid = threadIdx.x;
+  if (tid < D) {
+    double acc = 0.0;
+    for (int t = 0; t < P; ++t) acc = acc + getx(S, t, tid);
+    const uint16_t h = canon_zero(f64_to_f16(acc / (double)P));
+    S.c[tid] = f16_to_f64(h);  // centroid 0, for the certificate
+    ((uint16_t *)dst)[tid] = h;
+  }
+  if (tid < P) S.assign[tid] = 0;
+}
+
 __device__ void encode_to(EncodeShared &S, uint8_t *dst, int level, int tensor) {
   if (level == GKV_EXACT) write_exact(S, dst, tensor);
   else if (is_int_level(level)) encode_int(S, dst, level, tensor);
+  else if (level == GKV_MEAN) encode_mean(S, dst);
   else encode_centroid(S, dst, tensor);
 }
 
@@ -270,7 +293,7 @@ __device__ void block_cert(EncodeShared &S, int level) {
     const double x = getx(S, t, d);
     double xh = x;
     if (is_int_level(level)) xh = (double)S.codes[t * D + d] * S.s64[d] + S.z64[d];
-    else if (level == GKV_CENTROID) xh = S.c[S.assign[t] * XS + d];
+    else if (level == GKV_CENTROID || level == GKV_MEAN) xh = S.c[S.assign[t] * XS + d];
     e += (x - xh) * (x - xh);
     n += x * x;
   }

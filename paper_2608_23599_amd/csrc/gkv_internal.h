@@ -16,6 +16,7 @@ constexpr int KC = 4;
 constexpr int kExactBytes = P * D * 2;  // 16384
 constexpr int kSZBytes = 2 * D * 2;     // scale + zero, 512
 constexpr int kCentBytes = KC * D * 2 + P * 2 / 8;  // 1040
+constexpr int kMeanBytes = D * 2;                   // 256
 
 GKV_HD int64_t block_bytes(int level) {
   switch (level) {
@@ -24,6 +25,7 @@ GKV_HD int64_t block_bytes(int level) {
     case GKV_INT4: return kSZBytes + P * D / 2;
     case GKV_INT2: return kSZBytes + P * D / 4;
     case GKV_CENTROID: return kCentBytes;
+    case GKV_MEAN: return kMeanBytes;
     default: return 0;
   }
 }
@@ -33,11 +35,12 @@ GKV_HD bool is_int_level(int level) { return level == GKV_INT8 || level == GKV_I
 // Ladder order: larger = more precise.
 GKV_HD int level_rank(int level) {
   switch (level) {
-    case GKV_CENTROID: return 0;
-    case GKV_INT2: return 1;
-    case GKV_INT4: return 2;
-    case GKV_INT8: return 3;
-    case GKV_EXACT: return 4;
+    case GKV_MEAN: return 0;
+    case GKV_CENTROID: return 1;
+    case GKV_INT2: return 2;
+    case GKV_INT4: return 3;
+    case GKV_INT8: return 4;
+    case GKV_EXACT: return 5;
     default: return -1;
   }
 }

@@ -60,6 +60,10 @@ extern "C" gkv_status gkv_ladder_levels(int32_t profile, int64_t T, int8_t *lv, 
     for (int32_t i = 0; i < nblk; ++i) lv[i] = GKV_EXACT;
     return GKV_OK;
   }
+  if (profile == 3) {  // RD-V2 base: newest 16 exact, the rest one-centroid
+    for (int32_t i = 0; i < nblk; ++i) lv[i] = nblk - 1 - i < 16 ? GKV_EXACT : GKV_MEAN;
+    return GKV_OK;
+  }
   return GKV_E_ARG;
 }
 
@@ -100,25 +104,26 @@ extern "C" int32_t gkv_ladder_crossings(const gkv_cache *c, int32_t profile, int
 }
 
 // ---------------------------------------------------------------- slab pool
-static const int kLevels[5] = {GKV_EXACT, GKV_INT8, GKV_INT4, GKV_INT2, GKV_CENTROID};
+constexpr int kNLevels = 6;
+static const int kLevels[kNLevels] = {GKV_EXACT, GKV_INT8, GKV_INT4, GKV_INT2, GKV_CENTROID, GKV_MEAN};
 static int level_slot(int level) {
-  for (int i = 0; i < 5; ++i)
+  for (int i = 0; i < kNLevels; ++i)
     if (kLevels[i] == level) return i;
   return -1;
 }
 
 struct gkv_pool {
-  int64_t base[5], cap[5], bytes;
-  std::vector<int64_t> free_list[5];  // slot indices, popped from the back
-  std::vector<uint8_t> used[5];
-  int64_t nused[5];
+  int64_t base[kNLevels], cap[kNLevels], bytes;
+  std::vector<int64_t> free_list[kNLevels];  // slot indices, popped from the back
+  std::vector<uint8_t> used[kNLevels];
+  int64_t nused[kNLevels];
 };
 
-extern "C" gkv_pool *gkv_pool_create(const int64_t cap[5]) {
+extern "C" gkv_pool *gkv_pool_create(const int64_t cap[kNLevels]) {
   if (!cap) return nullptr;
   gkv_pool *p = new gkv_pool();
   int64_t off = 0;
-  for (int i = 0; i < 5; ++i) {
+  for (int i = 0; i < kNLevels; ++i) {
     if (cap[i] < 0) {
       delete p;
       return nullptr;
@@ -200,6 +205,7 @@ static int64_t row_bits(int level) {
 static int64_t overhead_bits(int level) {
   if (is_int_level(level)) return D * 2 * 16;
   if (level == GKV_CENTROID) return KC * D * 16;
+  if (level == GKV_MEAN) return D * 16;
   return 0;
 }
 
@@ -302,6 +308,15 @@ extern "C" gkv_status gkv_decode_record(int32_t level, int32_t tensor, const uin
       for (int d = 0; d < D; ++d) vals[t * D + d] = f16_to_f64(cen[id][d]);
     }
     if (cent) memcpy(cent, cen, sizeof cen);
+    return GKV_OK;
+  }
+  if (level == GKV_MEAN) {
+    const uint16_t *cc = (const uint16_t *)rec;
+    for (int t = 0; t < P; ++t) {
+      if (ids) ids[t] = 0;
+      for (int d = 0; d < D; ++d) vals[t * D + d] = f16_to_f64(cc[d]);
+    }
+    if (cent) memcpy(cent, cc, D * sizeof(uint16_t));
     return GKV_OK;
   }
   return GKV_E_ARG;

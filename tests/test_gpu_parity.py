@@ -512,3 +512,107 @@ def test_certificate_through_appends_and_demotions(gpu):
     for h in range(Hkv):
         _cert_compare(cache, ucs[h], 0, h)
         _bound_close(bnd[0, h * G:(h + 1) * G], ucs[h].certificate(q_group(q, 0, h, G)))
+
+
+# ---------------------------------------------------------------- one-centroid state, RD-V2
+
+
+@pytest.mark.parametrize("T,Bn", [(8192, 2), (3001, 1)])
+def test_rdv2_codes_residual_attention_and_bound(gpu, T, Bn):
+    """RD-V2 (section 3.4): newest 16 blocks exact, older blocks one-centroid, and
+    10.2% exact residual rows by Eq. rdscore against the block mean; 28 query / 4 KV
+    heads.  Records, residual sets and masks bit-exact; attention and certificate
+    against the oracle."""
+    torch = _torch()
+    Hq, Hkv = 28, 4
+    ks, vs = kv_all(9, Bn, Hkv, T)
+    lv = olad.ladder("rdv2", T)
+    n = ores.n_keep(T, 102, 1000)
+    cache = _build(gpu, ks, vs, Hq, lv, nres_cap=n)
+    mass = np.stack([np.stack([synth.mass_unit(9, b, h, T) for h in range(Hkv)]) for b in range(Bn)])
+    cache.rd_residual_select(ks, vs, mass, n)
+    q = synth.queries(9, Bn, Hq)
+    out, bnd = cache.decode_bound(q)
+    assert torch.equal(out, cache.decode(q))
+    out, bnd = out.cpu().numpy(), bnd.cpu().numpy()
+    idx = cache.res_idx.cpu().numpy()
+    G = Hq // Hkv
+    for b in range(Bn):
+        for h in range(Hkv):
+            uc = ocache.UnitCache(ks[b, h], vs[b, h], lv)
+            for blk in (0, 1, len(lv) // 2, len(lv) - 17, len(lv) - 16, len(lv) - 1):
+                compare_record(cache, uc, b, h, blk, 0)
+                compare_record(cache, uc, b, h, blk, 1)
+            want, _ = uc.select_residual(ks[b, h], vs[b, h], mass[b, h], n)
+            np.testing.assert_array_equal(idx[b, h, :n], want)
+            ref = uc.decode_dense(q_group(q, b, h, G))
+            assert max_err(out[b, h * G:(h + 1) * G], ref) <= TOL
+            _cert_compare(cache, uc, b, h)
+            _bound_close(bnd[b, h * G:(h + 1) * G], uc.certificate(q_group(q, b, h, G)))
+
+
+def test_demote_every_level_to_mean(gpu):
+    """gkv_demote to the one-centroid state from every other level, bit-exact, and
+    attention over the result."""
+    T, Hq, Hkv = 512, 4, 2
+    ks, vs = kv_all(52, 1, Hkv, T)
+    lv = np.array([16, 8, 4, 2, 1, 16, 16, 16], dtype=np.int8)
+    cache = _build(gpu, ks, vs, Hq, lv, slack={0: 16})
+    ucs = oracle_units(ks, vs, lv)
+    jobs = [(0, h, blk) for h in range(Hkv) for blk in range(5)]
+    cache.demote(jobs, [0] * len(jobs))
+    for (b, h), uc in ucs.items():
+        for blk in range(5):
+            uc.k_recs[blk] = oquant.demote(uc.k_recs[blk], 0)
+            uc.v_recs[blk] = oquant.demote(uc.v_recs[blk], 0)
+            uc.levels[blk] = 0
+            compare_record(cache, uc, b, h, blk, 0)
+            compare_record(cache, uc, b, h, blk, 1)
+    with pytest.raises(Exception):
+        cache.demote([(0, 0, 1)], [1])
+    q = synth.queries(52, 1, Hq)
+    out = cache.decode(q).cpu().numpy()
+    for (b, h), uc in ucs.items():
+        assert max_err(out[b, 2 * h:2 * h + 2], uc.decode_dense(q_group(q, b, h, 2))) <= TOL
+
+
+def test_rdv2_append_steps_with_quest_pages(gpu):
+    """Decode steps on an RD-V2 ladder: appends open exact blocks and demote the
+    block leaving the exact window straight to the one-centroid state; Compressed-
+    Quest selects pages by their exact boxes and reads one-centroid pages as counted
+    single keys; dense and sparse reads against the oracle at every step."""
+    Hq, Hkv, page, topk = 8, 2, 16, 20
+    T0 = 64 * 24 - 5
+    steps = 70
+    ks, vs = kv_all(53, 1, Hkv, T0 + steps)
+    lv = olad.ladder("rdv2", T0)
+    cache = _build(gpu, ks[:, :, :T0], vs[:, :, :T0], Hq, lv, page=page, extra_blocks=4, slack={16: 8, 0: 8})
+    ucs = {(0, h): ocache.UnitCache(ks[0, h, :T0], vs[0, h, :T0], lv) for h in range(Hkv)}
+    G = Hq // Hkv
+    nmoves = 0
+    for s in range(steps):
+        t = T0 + s
+        moves = cache.append(ks[:, :, t], vs[:, :, t], profile="rdv2")
+        nmoves += len(moves)
+        for h in range(Hkv):
+            omoves = ucs[(0, h)].append(ks[0, h, t], vs[0, h, t], "rdv2")
+        assert sorted((blk, o, n) for b, h, blk, o, n in moves if h == 0) == sorted(omoves)
+        assert all(o == 16 and n == 0 for b, h, blk, o, n in moves)
+        q = synth.queries(53, 1, Hq, step=s)
+        pages = cache.quest_select(q, topk)
+        out = cache.decode(q, pages=pages).cpu().numpy()
+        dense = cache.decode(q).cpu().numpy()
+        pages = pages.cpu().numpy()
+        T = t + 1
+        for h in range(Hkv):
+            uc = ucs[(0, h)]
+            kmin, kmax = oquest.page_boxes(ks[0, h, :T])
+            want = oquest.quest_select(q_group(q, 0, h, G), kmin, kmax, T, topk)
+            np.testing.assert_array_equal(pages[0, h], want)
+            assert max_err(out[0, h * G:(h + 1) * G], uc.decode_quest(q_group(q, 0, h, G), want)) <= TOL
+            assert max_err(dense[0, h * G:(h + 1) * G], uc.decode_dense(q_group(q, 0, h, G))) <= TOL
+            for b_, h_, blk, o, n in moves:
+                if h_ == h:
+                    compare_record(cache, uc, 0, h, blk, 0)
+                    compare_record(cache, uc, 0, h, blk, 1)
+    assert nmoves == 2 * Hkv  # two blocks leave the exact window per KV head in 70 steps

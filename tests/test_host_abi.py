@@ -45,7 +45,8 @@ def test_f64_to_f16_matches_single_rounding(B):
 
 
 @pytest.mark.parametrize("profile,T", [("tiny", 2048), ("tiny", 1000), ("graded", 16384), ("graded", 131072),
-                                       ("graded", 1048576 + 64), ("graded", 5000), ("exact", 300)])
+                                       ("graded", 1048576 + 64), ("graded", 5000), ("exact", 300),
+                                       ("rdv2", 131072), ("rdv2", 700)])
 def test_ladder_matches_oracle(B, profile, T):
     assert np.array_equal(B.ladder_levels(profile, T), olad.ladder(profile, T))
 
@@ -170,7 +171,7 @@ def test_call_validation_errors(B):
 
 
 def test_pool_slots(B):
-    p = B.Pool({16: 2, 8: 3, 1: 1})
+    p = B.Pool({16: 2, 8: 3, 1: 1, 0: 2})
     offs = [p.alloc(8) for _ in range(3)]
     assert len(set(offs)) == 3 and all(o % 16 == 0 for o in offs)
     with pytest.raises(B.GkvError):
@@ -182,7 +183,10 @@ def test_pool_slots(B):
     assert p.used(8) == 3 and p.used(16) == 0
     e = [p.alloc(16), p.alloc(16)]
     c = p.alloc(1)
-    spans = sorted([(o, o + B.block_bytes(8)) for o in offs] + [(o, o + 16384) for o in e] + [(c, c + 1040)])
+    mm = [p.alloc(0), p.alloc(0)]
+    assert p.used(0) == 2 and all(o % 16 == 0 for o in mm)
+    spans = sorted([(o, o + B.block_bytes(8)) for o in offs] + [(o, o + 16384) for o in e] + [(c, c + 1040)]
+                   + [(o, o + 256) for o in mm])
     assert all(a[1] <= b[0] for a, b in zip(spans, spans[1:]))
     assert p.bytes >= spans[-1][1]
 
@@ -231,6 +235,8 @@ def _pack(level, tensor, rec):
                         w, p = n >> 4, pos2[n & 15]
                     words[(pg * 64 + l) * bits + w] |= np.uint32(c << p)
         return sz.tobytes() + words.tobytes()
+    if level == 0:  # one row of 128 fp16 values in channel order
+        return np.asarray(rec.cent16[0], dtype=np.uint16).tobytes()
     cen = np.zeros(512, dtype=np.uint16)
     for k in range(4):
         for d in range(128):
@@ -246,7 +252,7 @@ def B_bytes(level):
     return oacc.block_bits(level) // 8
 
 
-@pytest.mark.parametrize("level", [16, 8, 4, 2, 1])
+@pytest.mark.parametrize("level", [16, 8, 4, 2, 1, 0])
 @pytest.mark.parametrize("tensor", [0, 1])
 def test_decode_record_reads_documented_layout(B, level, tensor):
     k, v = synth.kv_unit(300 + level, 0, 0, 64)
@@ -259,6 +265,6 @@ def test_decode_record_reads_documented_layout(B, level, tensor):
         np.testing.assert_array_equal(d["codes"], rec.codes)
         np.testing.assert_array_equal(d["s16"], rec.s16)
         np.testing.assert_array_equal(d["z16"], rec.z16)
-    if level == 1:
+    if level in (1, 0):
         np.testing.assert_array_equal(d["ids"], rec.ids)
         np.testing.assert_array_equal(d["cent16"], rec.cent16)
