@@ -196,6 +196,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-quest", action="store_true", help="skip the Compressed-Quest 128k point")
     ap.add_argument("--no-1m", action="store_true", help="skip the 1M-token Compressed-Quest + demotion steps")
+    ap.add_argument("--no-rdv2", action="store_true", help="skip the RD-V2 (one-centroid base) point")
     ap.add_argument("--profile", action="store_true",
                     help="decode loop only, then a plain 512 MiB device copy as a counter reference")
     args = ap.parse_args()
@@ -224,8 +225,8 @@ def main():
     mass_d = torch.from_numpy(mass).to(dev)
     log(f"[bench] inputs ready in {time.time() - t0:.1f}s; building caches")
     phases = {}
-    caches = []
-    for c in range(2):
+
+    def build_cache(lv, nres):
         cache = gkv.GradedCache(B, Hkv, Hq, T, len(lv), {L: 2 * B * Hkv * int((lv == L).sum()) for L in gkv.LEVELS},
                                 nres_cap=nres, device=dev)
         for b in range(B):
@@ -238,6 +239,11 @@ def main():
         qms = timed(lambda: (cache.quantize_block(gkv.KEYS, k, 0, len(lv)),
                              cache.quantize_block(gkv.VALUES, v, 0, len(lv))))
         rms = timed(lambda: cache.rd_residual_select(k, v, mass_d, nres))
+        return cache, qms, rms
+
+    caches = []
+    for c in range(2):
+        cache, qms, rms = build_cache(lv, nres)
         if c == 1:
             phases["quantize_all_blocks_ms"] = round(qms, 3)
             phases["rd_residual_select_ms"] = round(rms, 3)
@@ -266,7 +272,7 @@ def main():
         for _ in range(3):
             dst.copy_(src)
         torch.cuda.synchronize()
-        args.no_cpu = args.no_phases = args.no_quest = args.no_1m = True
+        args.no_cpu = args.no_phases = args.no_quest = args.no_1m = args.no_rdv2 = True
 
     # parity of the benchmarked launch on one sampled unit, and the CPU baseline
     cpu = None
@@ -313,6 +319,33 @@ def main():
             big.sum()
         phases["stream_read_GBps_torch_sum_1GiB"] = round((1 << 30) / (timed(lambda: big.sum(), 10) * 1e-3) / 1e9, 1)
         del big
+
+    rdv2 = None
+    if not args.no_rdv2:
+        # RD-V2 (section 3.4 low-rate variation): one-centroid base outside the 16-block
+        # exact window, 10.2% exact residual rows; same shape, inputs and queries
+        del caches
+        torch.cuda.empty_cache()
+        lv2 = gkv.ladder_levels("rdv2", T)
+        nres2 = (102 * T) // 1000
+        log(f"[bench] RD-V2: one-centroid base + {nres2} residual rows per (sequence, KV head)")
+        c2 = [build_cache(lv2, nres2)[0] for _ in range(2)]
+        r2 = c2[0].account()
+        b2 = r2["read_bits"] / 8.0
+        n2 = max(args.steps // 2, 10)
+        per2, _ = step_loop(c2, qs, outs, n2, args.warmup)
+        _, attn2, _ = staged_loop(c2, qs, outs, n2, args.warmup)
+        rdv2 = {"workload": wl.name.split(",")[0] + f", B={B}, T={T}, RD-V2: 16 exact blocks + one-centroid base, "
+                                                    f"10.2% exact residual",
+                "us_per_step_median": round(float(np.median(per2)), 2),
+                "attn_kernel_us_mean": round(float(attn2.mean()), 2),
+                "attn_GBps": round(b2 / (float(attn2.mean()) * 1e-6) / 1e9, 1),
+                "read_bpv": round(r2["read_bpv"], 4), "resident_bpv": round(r2["resident_bpv"], 4),
+                "algorithmic_bytes": int(b2)}
+        log(f"[bench] RD-V2: {rdv2['us_per_step_median']} us/step, attention {rdv2['attn_kernel_us_mean']} us, "
+            f"{rdv2['read_bpv']} bpv read")
+        del c2
+        torch.cuda.empty_cache()
 
     quest = quest_b8 = quest_p64 = None
     if not args.no_quest:
@@ -413,6 +446,7 @@ def main():
                       "merge_median": round(float(np.median(merge_us)), 2)},
         "cpu_baseline": cpu,
         "phases": phases,
+        "rd_v2": rdv2,
         "quest_128k": quest,
         "quest_128k_b8": quest_b8,
         "quest_128k_page64": quest_p64,

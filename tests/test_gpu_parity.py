@@ -616,3 +616,42 @@ def test_rdv2_append_steps_with_quest_pages(gpu):
                     compare_record(cache, uc, 0, h, blk, 0)
                     compare_record(cache, uc, 0, h, blk, 1)
     assert nmoves == 2 * Hkv  # two blocks leave the exact window per KV head in 70 steps
+
+
+@pytest.mark.parametrize("prof,frac", [("graded", (2, 100)), ("rdv2", (102, 1000))])
+def test_rd128k_full_size_sampled(gpu, prof, frac):
+    """The 128k decode step at its full size and launch configuration (B = 8, 28
+    query / 4 KV heads, T = 131072): graded ladder with 2% residual rows, and RD-V2
+    with 10.2%.  Units (0, 0) and (7, 3) hold their own seeded data and are checked
+    against the oracle (sampled records, residual set, attention); the other 30
+    units repeat those two, so that the launch covers the whole grid."""
+    from paper_2608_23599_amd import workloads
+    wl = workloads.RD128K
+    B, Hq, Hkv, T = wl.B, wl.Hq, wl.Hkv, wl.T
+    samp = [(0, 0), (B - 1, Hkv - 1)]
+    data = {u: synth.kv_unit(wl.id, *u, T) for u in samp}
+    masses = {u: synth.mass_unit(wl.id, *u, T) for u in samp}
+    ks = np.empty((B, Hkv, T, 128), np.uint16)
+    vs = np.empty((B, Hkv, T, 128), np.uint16)
+    mass = np.empty((B, Hkv, T), np.float32)
+    for b in range(B):
+        for h in range(Hkv):
+            u = samp[(b * Hkv + h) % 2]
+            ks[b, h], vs[b, h] = data[u]
+            mass[b, h] = masses[u]
+    lv = olad.ladder(prof, T)
+    n = ores.n_keep(T, *frac)
+    cache = _build(gpu, ks, vs, Hq, lv, nres_cap=n)
+    cache.rd_residual_select(ks, vs, mass, n)
+    q = synth.queries(wl.id, B, Hq)
+    out = cache.decode(q).cpu().numpy()
+    idx = cache.res_idx.cpu().numpy()
+    G = Hq // Hkv
+    for b, h in samp:
+        uc = ocache.UnitCache(ks[b, h], vs[b, h], lv)
+        for blk in (0, 1, 700, 1500, len(lv) - 17, len(lv) - 1):
+            compare_record(cache, uc, b, h, blk, 0)
+            compare_record(cache, uc, b, h, blk, 1)
+        want, _ = uc.select_residual(ks[b, h], vs[b, h], mass[b, h], n)
+        np.testing.assert_array_equal(idx[b, h, :n], want)
+        assert max_err(out[b, h * G:(h + 1) * G], uc.decode_dense(q_group(q, b, h, G))) <= TOL
