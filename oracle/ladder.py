@@ -76,8 +76,8 @@ def graded_ladder(nblk, exact_blocks=16, pct8=25, pct84=60, pct_centroid=10):
 
 
 def rdv2_ladder(nblk, exact_blocks=16):
-    """Low-rate RD-V2 base (section 3.4, the variation with a nearly centroid-only
-    base): the newest ``exact_blocks`` blocks exact, every older block in the
+    """Low-rate RD-V2 base (section 3.4; its base is almost all centroid state):
+    the newest ``exact_blocks`` blocks exact, every older block in the
     one-centroid state.  The exact residual (about 10.2% of the tokens) is kept on
     top of it.
     """
