@@ -313,6 +313,23 @@ def main():
         phases["decode_with_certificate_us"] = round(timed(lambda: caches[0].decode_bound(qs[0]), 20) * 1e3, 1)
         _, bnd = caches[0].decode_bound(qs[0])
         phases["certificate_bound_mean_max"] = [round(float(bnd.mean()), 4), round(float(bnd.max()), 4)]
+        # causal mass observer (Eq. 1-2) over the last 64 prompt positions, and the
+        # closed-form level allocation, at this workload's shape
+        n_obs = 64
+        q_obs = torch.from_numpy(np.stack([synth.queries(wl.id, B, Hq, step=100 + i) for i in range(n_obs)], 1)
+                                 .view(np.int16)).to(dev)
+        ows = torch.empty(gkv.observe_ws_bytes(B, Hkv, Hq, T, n_obs), dtype=torch.uint8, device=dev)
+        mass_o = torch.empty((B, Hkv, len(lv)), dtype=torch.float32, device=dev)
+        for _ in range(2):
+            gkv.observe_mass(q_obs, k, mass=mass_o, ws=ows)
+        obs_ms = timed(lambda: gkv.observe_mass(q_obs, k, mass=mass_o, ws=ows), 5)
+        flops = 2.0 * B * Hq * n_obs * T * 128  # the logits' multiply-adds
+        phases["observe_mass_n64_us"] = round(obs_ms * 1e3, 1)
+        phases["observe_mass_logit_TFLOPs"] = round(flops / (obs_ms * 1e-3) / 1e12, 1)
+        qn_o = gkv.query_norms(q_obs, Hkv)
+        phases["allocate_levels_us"] = round(timed(lambda: gkv.allocate_levels(k, mass_o, qn_o, 1.0, 1e-3, 16), 5)
+                                             * 1e3, 1)
+        del q_obs, ows, mass_o
         # a second denominator: what a plain library reduction reads per second
         big = torch.zeros(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB
         for _ in range(3):

@@ -293,6 +293,47 @@ gkv_status gkv_rd_residual_select(gkv_cache *c, const uint16_t *k_src, const uin
                                   const float *mass, int32_t nkeep, void *ws, int64_t ws_bytes,
                                   void *stream);
 
+/* ---------------------------------------------------------------- observer and allocation */
+
+/* Workspace bytes of gkv_observe_mass for these shapes, or -1 when they are invalid. */
+int64_t gkv_observe_ws_bytes(int32_t B, int32_t Hkv, int32_t Hq, int64_t T, int32_t n_obs);
+
+/* Causal attention-mass observer (section 3.1, Eq. 1-2, GQA aggregation and EMA).
+ * For every (b, KV head h) the observed queries are the group's G = Hq/Hkv heads at
+ * the last n_obs prompt positions T - n_obs .. T - 1; query i sees keys
+ * 0 .. T - n_obs + i.  With w = softmax(q . k / sqrt(128)) over the visible keys,
+ *   m_new[blk] = mean over the G * n_obs (query, head) rows of sum_{j in blk} w_j,
+ * so the masses of one (b, h) sum to 1, and
+ *   mass = (1 - alpha) * mass + alpha * m_new   (0 < alpha <= 1; alpha = 1 writes
+ *                                                m_new without reading mass).
+ * q_obs: [B][n_obs][Hq][128] fp16; k_src: [B][Hkv][T][128] fp16 exact keys;
+ * mass: [B][Hkv][ceil(T/64)] fp32.  Logits are fp32 sums of fp16 products (MFMA);
+ * the softmax runs in fp32.  GKV_E_UNSUPPORTED when n_obs * G > 512. */
+gkv_status gkv_observe_mass(const uint16_t *q_obs, int32_t n_obs, const uint16_t *k_src, int32_t B, int32_t Hkv,
+                            int32_t Hq, int64_t T, float alpha, float *mass, void *ws, int64_t ws_bytes,
+                            void *stream);
+
+/* qn[b][h] = the largest ||q|| over the group's observed queries q_obs
+ * [B][n_obs][Hq][128] fp16 (fp64: channel-ascending sum of squares, then sqrt);
+ * the query norm of the bit-depth formula (section 3.3).  qn: [B][Hkv] fp64. */
+gkv_status gkv_query_norms(const uint16_t *q_obs, int32_t n_obs, int32_t B, int32_t Hkv, int32_t Hq, double *qn,
+                           void *stream);
+
+/* Closed-form level allocation (section 3.3, Eq. allocation solved per block by
+ * the analytic bit depth): for every block of every (b, h),
+ *   e_b = max over channels of (max - min) of the block's exact keys k_src
+ *         [B][Hkv][T][128] fp16,
+ *   x   = c * qn[b][h] * e_b * N_b * mass[b][h][blk] / (2 tau)  (fp64, left to right;
+ *         N_b = ceil(T/64); this is c ||q|| e_b / (2 eps_t) with eps_t = tau/(N_b m_b)),
+ *   b*  = ceil(log2(x + 1)), and the level is the smallest of {1, 2, 4, 8} that is
+ *         >= b* (tested as x <= 2^L - 1), else 16.
+ * The newest `window` blocks and a partial last block are exact.  levels: device
+ * [B][Hkv][ceil(T/64)] int8 gkv_level.  c > 0 and tau > 0 (the paper leaves both
+ * open). */
+gkv_status gkv_allocate_levels(const uint16_t *k_src, const float *mass, const double *qn, int32_t B,
+                               int32_t Hkv, int64_t T, double c, double tau, int32_t window, int8_t *levels,
+                               void *stream);
+
 #ifdef __cplusplus
 }
 #endif

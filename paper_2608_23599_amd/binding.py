@@ -78,6 +78,12 @@ _attn_plan = _sig("gkv_attn_plan", _i32, [_P(CacheStruct), _vp, _i32, _vp, _i64,
 _attn_partials = _sig("gkv_attn_partials", _i32, [_vp, _P(CacheStruct), _vp, _i32, _vp, _i64, _vp])
 _attn_merge = _sig("gkv_attn_merge", _i32, [_P(CacheStruct), _vp, _i32, _vp, _vp, _i64, _vp])
 _rd = _sig("gkv_rd_residual_select", _i32, [_P(CacheStruct), _vp, _vp, _vp, _i32, _vp, _i64, _vp])
+_observe_ws = _sig("gkv_observe_ws_bytes", _i64, [_i32, _i32, _i32, _i64, _i32])
+_observe = _sig("gkv_observe_mass", _i32,
+                [_vp, _i32, _vp, _i32, _i32, _i32, _i64, ctypes.c_float, _vp, _vp, _i64, _vp])
+_query_norms = _sig("gkv_query_norms", _i32, [_vp, _i32, _i32, _i32, _i32, _vp, _vp])
+_allocate = _sig("gkv_allocate_levels", _i32,
+                 [_vp, _vp, _vp, _i32, _i32, _i64, ctypes.c_double, ctypes.c_double, _i32, _vp, _vp])
 
 EXPORTED = [
     "gkv_strerror", "gkv_block_bytes", "gkv_ladder_levels", "gkv_ladder_crossings", "gkv_pool_create",
@@ -85,6 +91,7 @@ EXPORTED = [
     "gkv_decode_record", "gkv_f64_to_f16", "gkv_workspace_bytes", "gkv_quantize_block", "gkv_demote",
     "gkv_page_boxes", "gkv_append", "gkv_quest_select", "gkv_graded_decode_attn", "gkv_rd_residual_select",
     "gkv_attn_plan", "gkv_attn_partials", "gkv_attn_merge", "gkv_graded_decode_attn_bound",
+    "gkv_observe_ws_bytes", "gkv_observe_mass", "gkv_query_norms", "gkv_allocate_levels",
 ]
 
 
@@ -113,6 +120,60 @@ def _stream():
 
 def block_bytes(level):
     return int(_block_bytes(level))
+
+
+def _fp16_dev(x, device="cuda"):
+    """fp16 bit patterns (numpy uint16 or a 16-bit tensor) as a contiguous device tensor."""
+    if isinstance(x, np.ndarray):
+        x = torch.from_numpy(np.ascontiguousarray(x).view(np.int16))
+    return x.to(device).contiguous()
+
+
+def observe_ws_bytes(B, Hkv, Hq, T, n_obs):
+    nb = int(_observe_ws(B, Hkv, Hq, T, n_obs))
+    if nb < 0:
+        raise GkvError(-2, "observe_ws_bytes")
+    return nb
+
+
+def observe_mass(q_obs, k, alpha=1.0, mass=None, ws=None):
+    """gkv_observe_mass: q_obs [B][n_obs][Hq][128], k [B][Hkv][T][128] fp16 bits.
+    Returns the fp32 mass [B][Hkv][ceil(T/64)] (updated in place when given)."""
+    q_obs, k = _fp16_dev(q_obs), _fp16_dev(k)
+    B, n_obs, Hq, _ = q_obs.shape
+    Hkv, T = k.shape[1], k.shape[2]
+    nblk = (T + P - 1) // P
+    if mass is None:
+        mass = torch.empty((B, Hkv, nblk), dtype=torch.float32, device=k.device)
+    nb = int(_observe_ws(B, Hkv, Hq, T, n_obs))
+    if nb < 0:
+        raise GkvError(-2, "observe_ws_bytes")
+    if ws is None or ws.numel() < nb:
+        ws = torch.empty(nb, dtype=torch.uint8, device=k.device)
+    _check(_observe(_dptr(q_obs), n_obs, _dptr(k), B, Hkv, Hq, T, float(alpha), _dptr(mass), _dptr(ws), ws.numel(),
+                    _stream()), "observe_mass")
+    return mass
+
+
+def query_norms(q_obs, Hkv):
+    """gkv_query_norms: the largest query norm of each group, fp64 [B][Hkv]."""
+    q_obs = _fp16_dev(q_obs)
+    B, n_obs, Hq, _ = q_obs.shape
+    qn = torch.empty((B, Hkv), dtype=torch.float64, device=q_obs.device)
+    _check(_query_norms(_dptr(q_obs), n_obs, B, Hkv, Hq, _dptr(qn), _stream()), "query_norms")
+    return qn
+
+
+def allocate_levels(k, mass, qn, c, tau, window):
+    """gkv_allocate_levels: int8 levels [B][Hkv][ceil(T/64)] on the device."""
+    k = _fp16_dev(k)
+    B, Hkv, T = k.shape[0], k.shape[1], k.shape[2]
+    mass = mass.to(k.device, torch.float32).contiguous()
+    qn = qn.to(k.device, torch.float64).contiguous()
+    lv = torch.empty((B, Hkv, (T + P - 1) // P), dtype=torch.int8, device=k.device)
+    _check(_allocate(_dptr(k), _dptr(mass), _dptr(qn), B, Hkv, T, float(c), float(tau), int(window), _dptr(lv),
+                     _stream()), "allocate_levels")
+    return lv
 
 
 def f64_to_f16(x):

@@ -1,0 +1,338 @@
+// Causal attention-mass observer (section 3.1, Eq. 1-2, GQA aggregation, EMA) and
+// the closed-form level allocation (section 3.3, Eq. allocation and b*).
+//
+// Observer, per (sequence b, KV head h), with R = n_obs * G query rows (row
+// r = i * G + g is query head h * G + g at prompt position T - n_obs + i):
+//   obs_logit_kernel  MFMA logits of every row against every key, one log-sum-exp
+//                     per (block, row) over the block's visible keys (log2 units);
+//   obs_slice_kernel  per (row, slice of blocks) running max and sum;
+//   obs_row_kernel    per row the log-sum-exp over all blocks;
+//   obs_mass_kernel   per block the mean over rows of exp2(lse_block - lse_row),
+//                     blended into the mass with the EMA weight.
+// Allocation: query_norm_kernel (largest query norm of each group, fp64) and
+// alloc_kernel (key range of each block, then the threshold form of b*).
+#include <hip/hip_runtime.h>
+
+#include "gkv_internal.h"
+
+#pragma clang fp contract(off)
+
+using namespace gkv;
+
+namespace {
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+union H8 {
+  half8 h;
+  uint4 v;
+};
+
+constexpr int kObsThreads = 512;  // 8 wavefronts
+constexpr int kObsBlocksPerWave = 4;
+constexpr int kObsChunk = 8 * kObsBlocksPerWave;  // blocks per workgroup
+constexpr int kMaxRows = 512;
+constexpr int kSlice = 128;  // blocks per slice of obs_slice_kernel
+constexpr float kNegInf = -__builtin_huge_valf();
+
+__device__ __forceinline__ f4 mfma32(half8 a, half8 b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+// Query rows in LDS: row r holds 16 chunks of 8 channels; chunk c sits at position
+// c ^ (r & 15), so that the 16 rows read by one MFMA operand fall in distinct banks.
+__device__ __forceinline__ uint32_t qpos(int r, int c) { return (uint32_t)(r * 16 + (c ^ (r & 15))) * 16u; }
+
+__global__ void __launch_bounds__(kObsThreads) obs_logit_kernel(const uint16_t *__restrict__ q_obs,
+                                                                const uint16_t *__restrict__ k_src, int n_obs,
+                                                                int G, int Hkv, int64_t T, int nblk, int Rpad,
+                                                                float sl2, float *__restrict__ lse) {
+  extern __shared__ __align__(16) uint8_t qs[];
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int64_t u = (int64_t)b * Hkv + h;
+  const int R = n_obs * G, Hq = Hkv * G;
+  // stage the group's query rows (zero rows beyond R)
+  for (int i = threadIdx.x; i < Rpad * 16; i += kObsThreads) {
+    const int r = i >> 4, c = i & 15;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (r < R) {
+      const int qi = r / G, g = r - qi * G;
+      v = *(const uint4 *)(q_obs + (((int64_t)b * n_obs + qi) * Hq + h * G + g) * D + 8 * c);
+    }
+    *(uint4 *)(qs + qpos(r, c)) = v;
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, kg = lane >> 4, m16 = lane & 15;
+  const uint16_t *kb = k_src + u * T * D;
+  const int64_t first_masked = T - n_obs + 1;  // keys at or beyond this are hidden from some row
+  for (int k = 0; k < kObsBlocksPerWave; ++k) {
+    const int blk = blockIdx.x * kObsChunk + wv * kObsBlocksPerWave + k;
+    if (blk >= nblk) break;
+    // this lane's key operands: key 64 blk + 16 t + m16, channels 32 i + 8 kg .. + 7
+    H8 a[4][4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int64_t key = (int64_t)blk * P + 16 * t + m16;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        a[t][i].v = key < T ? *(const uint4 *)(kb + key * D + 32 * i + 8 * kg) : make_uint4(0, 0, 0, 0);
+    }
+    const bool masked = (int64_t)blk * P + P > first_masked;  // uniform: the block has hidden keys
+    for (int rt = 0; rt < Rpad / 16; ++rt) {
+      const int row = 16 * rt + m16;
+      H8 qb[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) qb[i].v = *(const uint4 *)(qs + qpos(row, 4 * i + kg));
+      f4 s[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        s[t] = f4{0, 0, 0, 0};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) s[t] = mfma32(a[t][i].h, qb[i].h, s[t]);
+      }
+      // s[t][e]: key 64 blk + 16 t + 4 kg + e, query row `row`
+      float x[16];
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[4 * t + e] = s[t][e] * sl2;
+      if (masked) {
+        const int64_t last = T - n_obs + row / G;  // the last key this row sees
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int64_t key = (int64_t)blk * P + 16 * t + 4 * kg + e;
+            if (key > last || key >= T) x[4 * t + e] = kNegInf;
+          }
+      }
+      float bm = x[0];
+#pragma unroll
+      for (int j = 1; j < 16; ++j) bm = fmaxf(bm, x[j]);
+      bm = fmaxf(bm, __shfl_xor(bm, 16));
+      bm = fmaxf(bm, __shfl_xor(bm, 32));
+      float sum = 0.f;
+      if (bm != kNegInf) {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) sum += __builtin_amdgcn_exp2f(x[j] - bm);
+      }
+      sum += __shfl_xor(sum, 16);
+      sum += __shfl_xor(sum, 32);
+      if (kg == 0 && row < R)
+        lse[(u * nblk + blk) * Rpad + row] = bm == kNegInf ? kNegInf : bm + __builtin_amdgcn_logf(sum);
+    }
+  }
+}
+
+// Running (max, sum) of exp2 over one slice of blocks, per row.
+__global__ void __launch_bounds__(256) obs_slice_kernel(const float *__restrict__ lse, int R, int Rpad, int nblk,
+                                                        int nslice, int Hkv, float2 *__restrict__ part) {
+  const int sl = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int64_t u = (int64_t)b * Hkv + h;
+  const int b0 = sl * kSlice, b1 = b0 + kSlice < nblk ? b0 + kSlice : nblk;
+  for (int r = threadIdx.x; r < R; r += 256) {
+    float m = kNegInf, s = 0.f;
+    for (int blk = b0; blk < b1; ++blk) {
+      const float v = lse[(u * nblk + blk) * Rpad + r];
+      if (v == kNegInf) continue;
+      if (v > m) {
+        s = s * __builtin_amdgcn_exp2f(m - v) + 1.f;
+        m = v;
+      } else {
+        s += __builtin_amdgcn_exp2f(v - m);
+      }
+    }
+    part[(u * nslice + sl) * Rpad + r] = make_float2(m, s);
+  }
+}
+
+__global__ void __launch_bounds__(256) obs_row_kernel(const float2 *__restrict__ part, int R, int Rpad, int nslice,
+                                                      int Hkv, float *__restrict__ row_lse) {
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int64_t u = (int64_t)b * Hkv + h;
+  for (int r = threadIdx.x; r < R; r += 256) {
+    float m = kNegInf;
+    for (int sl = 0; sl < nslice; ++sl) m = fmaxf(m, part[(u * nslice + sl) * Rpad + r].x);
+    float s = 0.f;
+    for (int sl = 0; sl < nslice; ++sl) {
+      const float2 p = part[(u * nslice + sl) * Rpad + r];
+      if (p.x != kNegInf) s += p.y * __builtin_amdgcn_exp2f(p.x - m);
+    }
+    row_lse[u * Rpad + r] = m + __builtin_amdgcn_logf(s);  // every row sees key 0
+  }
+}
+
+// One wavefront per block: mean over rows of the block's share of each row.
+__global__ void __launch_bounds__(256) obs_mass_kernel(const float *__restrict__ lse,
+                                                       const float *__restrict__ row_lse, int R, int Rpad,
+                                                       int nblk, int Hkv, float alpha, float *__restrict__ mass) {
+  const int lane = threadIdx.x & 63;
+  const int blk = blockIdx.x * 4 + (threadIdx.x >> 6), h = blockIdx.y, b = blockIdx.z;
+  if (blk >= nblk) return;
+  const int64_t u = (int64_t)b * Hkv + h;
+  float acc = 0.f;
+  for (int r = lane; r < R; r += 64) {
+    const float v = lse[(u * nblk + blk) * Rpad + r];
+    if (v != kNegInf) acc += __builtin_amdgcn_exp2f(v - row_lse[u * Rpad + r]);
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) acc += __shfl_xor(acc, o);
+  if (lane == 0) {
+    const float m = acc / (float)R;
+    float *dst = mass + u * nblk + blk;
+    *dst = alpha == 1.f ? m : (1.f - alpha) * *dst + alpha * m;
+  }
+}
+
+// Largest ||q|| over the group's observed queries, fp64, channel-ascending sums.
+__global__ void __launch_bounds__(256) query_norm_kernel(const uint16_t *__restrict__ q_obs, int n_obs, int G,
+                                                         int Hkv, double *__restrict__ qn) {
+  __shared__ double best[256];
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int R = n_obs * G, Hq = Hkv * G;
+  double mx = 0.0;
+  for (int r = threadIdx.x; r < R; r += 256) {
+    const int qi = r / G, g = r - qi * G;
+    const uint16_t *q = q_obs + (((int64_t)b * n_obs + qi) * Hq + h * G + g) * D;
+    double acc = 0.0;
+    for (int d = 0; d < D; ++d) {
+      const double x = (double)__builtin_bit_cast(_Float16, q[d]);
+      acc = acc + x * x;
+    }
+    const double n = __builtin_sqrt(acc);
+    mx = n > mx ? n : mx;
+  }
+  best[threadIdx.x] = mx;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double m = 0.0;
+    for (int i = 0; i < 256; ++i) m = best[i] > m ? best[i] : m;
+    qn[(int64_t)b * Hkv + h] = m;
+  }
+}
+
+// Level of one block: key range, then x = c ||q|| e N m / (2 tau) against 2^L - 1.
+__global__ void __launch_bounds__(D) alloc_kernel(const uint16_t *__restrict__ k_src, const float *__restrict__ mass,
+                                                  const double *__restrict__ qn, int Hkv, int64_t T, int nblk,
+                                                  double c, double tau, int window, int8_t *__restrict__ levels) {
+  __shared__ double rng[D];
+  const int blk = blockIdx.x, h = blockIdx.y, b = blockIdx.z, d = threadIdx.x;
+  const int64_t u = (int64_t)b * Hkv + h;
+  const bool exact = blk >= nblk - window || (int64_t)(blk + 1) * P > T;
+  if (exact) {
+    if (d == 0) levels[u * nblk + blk] = GKV_EXACT;
+    return;
+  }
+  const uint16_t *kb = k_src + (u * T + (int64_t)blk * P) * D + d;
+  double mn = (double)__builtin_bit_cast(_Float16, kb[0]), mx = mn;
+  for (int t = 1; t < P; ++t) {
+    const double x = (double)__builtin_bit_cast(_Float16, kb[(int64_t)t * D]);
+    mn = x < mn ? x : mn;
+    mx = x > mx ? x : mx;
+  }
+  rng[d] = mx - mn;  // exact in fp64
+  __syncthreads();
+  if (d == 0) {
+    double e = rng[0];
+    for (int i = 1; i < D; ++i) e = rng[i] > e ? rng[i] : e;
+    double x = c * qn[u];
+    x = x * e;
+    x = x * (double)nblk;
+    x = x * (double)mass[u * nblk + blk];
+    x = x / (2.0 * tau);
+    int8_t lv = GKV_EXACT;
+    if (x <= 1.0) lv = GKV_CENTROID;
+    else if (x <= 3.0) lv = GKV_INT2;
+    else if (x <= 15.0) lv = GKV_INT4;
+    else if (x <= 255.0) lv = GKV_INT8;
+    levels[u * nblk + blk] = lv;
+  }
+}
+
+int rows_padded(int R) { return (R + 15) / 16 * 16; }
+int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
+
+struct ObsLayout {
+  int nblk, R, Rpad, nslice;
+  int64_t lse, part, rows, total;
+};
+
+ObsLayout obs_layout(int B, int Hkv, int Hq, int64_t T, int n_obs) {
+  ObsLayout L;
+  const int64_t units = (int64_t)B * Hkv;
+  L.nblk = (int)((T + P - 1) / P);
+  L.R = n_obs * (Hq / Hkv);
+  L.Rpad = rows_padded(L.R);
+  L.nslice = (L.nblk + kSlice - 1) / kSlice;
+  L.lse = 0;
+  L.part = align256(units * L.nblk * L.Rpad * 4);
+  L.rows = L.part + align256(units * L.nslice * L.Rpad * 8);
+  L.total = L.rows + align256(units * L.Rpad * 4);
+  return L;
+}
+
+gkv_status obs_check(int B, int Hkv, int Hq, int64_t T, int n_obs) {
+  if (B <= 0 || Hkv <= 0 || Hq <= 0 || Hq % Hkv) return GKV_E_SHAPE;
+  const int G = Hq / Hkv;
+  if (G < 1 || G > 16) return GKV_E_SHAPE;
+  if (T <= 0 || n_obs < 1 || n_obs > T) return GKV_E_SHAPE;
+  if ((int64_t)n_obs * G > kMaxRows) return GKV_E_UNSUPPORTED;
+  if ((T + P - 1) / P > (1ll << 24)) return GKV_E_UNSUPPORTED;
+  return GKV_OK;
+}
+
+}  // namespace
+
+extern "C" int64_t gkv_observe_ws_bytes(int32_t B, int32_t Hkv, int32_t Hq, int64_t T, int32_t n_obs) {
+  if (obs_check(B, Hkv, Hq, T, n_obs)) return -1;
+  return obs_layout(B, Hkv, Hq, T, n_obs).total;
+}
+
+extern "C" gkv_status gkv_observe_mass(const uint16_t *q_obs, int32_t n_obs, const uint16_t *k_src, int32_t B,
+                                       int32_t Hkv, int32_t Hq, int64_t T, float alpha, float *mass, void *ws,
+                                       int64_t ws_bytes, void *stream) {
+  gkv_status st = obs_check(B, Hkv, Hq, T, n_obs);
+  if (st) return st;
+  if (!q_obs || !k_src || !mass || !ws) return GKV_E_ARG;
+  if (!(alpha > 0.f && alpha <= 1.f)) return GKV_E_ARG;
+  const ObsLayout L = obs_layout(B, Hkv, Hq, T, n_obs);
+  if (ws_bytes < L.total) return GKV_E_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t *w = (uint8_t *)ws;
+  float *lse = (float *)(w + L.lse);
+  float2 *part = (float2 *)(w + L.part);
+  float *rows = (float *)(w + L.rows);
+  const int G = Hq / Hkv;
+  const float sl2 = 1.4426950408889634f / sqrtf((float)D);
+  hipLaunchKernelGGL(obs_logit_kernel, dim3((L.nblk + kObsChunk - 1) / kObsChunk, Hkv, B), dim3(kObsThreads),
+                     L.Rpad * 256, s, q_obs, k_src, n_obs, G, Hkv, T, L.nblk, L.Rpad, sl2, lse);
+  hipLaunchKernelGGL(obs_slice_kernel, dim3(L.nslice, Hkv, B), dim3(256), 0, s, lse, L.R, L.Rpad, L.nblk, L.nslice,
+                     Hkv, part);
+  hipLaunchKernelGGL(obs_row_kernel, dim3(Hkv, B), dim3(256), 0, s, part, L.R, L.Rpad, L.nslice, Hkv, rows);
+  hipLaunchKernelGGL(obs_mass_kernel, dim3((L.nblk + 3) / 4, Hkv, B), dim3(256), 0, s, lse, rows, L.R, L.Rpad,
+                     L.nblk, Hkv, alpha, mass);
+  return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP;
+}
+
+extern "C" gkv_status gkv_query_norms(const uint16_t *q_obs, int32_t n_obs, int32_t B, int32_t Hkv, int32_t Hq,
+                                      double *qn, void *stream) {
+  if (B <= 0 || Hkv <= 0 || Hq <= 0 || Hq % Hkv || Hq / Hkv > 16 || n_obs < 1) return GKV_E_SHAPE;
+  if (!q_obs || !qn) return GKV_E_ARG;
+  hipLaunchKernelGGL(query_norm_kernel, dim3(Hkv, B), dim3(256), 0, (hipStream_t)stream, q_obs, n_obs, Hq / Hkv,
+                     Hkv, qn);
+  return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP;
+}
+
+extern "C" gkv_status gkv_allocate_levels(const uint16_t *k_src, const float *mass, const double *qn, int32_t B,
+                                          int32_t Hkv, int64_t T, double c, double tau, int32_t window,
+                                          int8_t *levels, void *stream) {
+  if (B <= 0 || Hkv <= 0 || T <= 0) return GKV_E_SHAPE;
+  if (!k_src || !mass || !qn || !levels) return GKV_E_ARG;
+  if (!(c > 0.0) || !(tau > 0.0) || window < 0) return GKV_E_ARG;
+  const int64_t nblk = (T + P - 1) / P;
+  if (nblk > (1ll << 24)) return GKV_E_UNSUPPORTED;
+  hipLaunchKernelGGL(alloc_kernel, dim3((unsigned)nblk, Hkv, B), dim3(D), 0, (hipStream_t)stream, k_src, mass, qn,
+                     Hkv, T, (int)nblk, c, tau, window, levels);
+  return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP;
+}
