@@ -4,9 +4,9 @@
 // Observer, per (sequence b, KV head h), with R = n_obs * G query rows (row
 // r = i * G + g is query head h * G + g at prompt position T - n_obs + i):
 //   obs_logit_kernel  MFMA logits of every row against every key, one log-sum-exp
-//                     per (block, row) over the block's visible keys (log2 units);
-//   obs_slice_kernel  per (row, slice of blocks) running max and sum;
-//   obs_row_kernel    per row the log-sum-exp over all blocks;
+//                     per (block, row) over the block's visible keys (log2 units),
+//                     and per (row, workgroup chunk of blocks) a running max and sum;
+//   obs_row_kernel    per row the log-sum-exp over all chunks;
 //   obs_mass_kernel   per block the mean over rows of exp2(lse_block - lse_row),
 //                     blended into the mass with the EMA weight.
 // Allocation: query_norm_kernel (largest query norm of each group, fp64) and
@@ -33,7 +33,6 @@ constexpr int kObsThreads = 512;  // 8 wavefronts
 constexpr int kObsBlocksPerWave = 4;
 constexpr int kObsChunk = 8 * kObsBlocksPerWave;  // blocks per workgroup
 constexpr int kMaxRows = 512;
-constexpr int kSlice = 128;  // blocks per slice of obs_slice_kernel
 constexpr float kNegInf = -__builtin_huge_valf();
 
 __device__ __forceinline__ f4 mfma32(half8 a, half8 b, f4 c) {
@@ -44,15 +43,104 @@ __device__ __forceinline__ f4 mfma32(half8 a, half8 b, f4 c) {
 // c ^ (r & 15), so that the 16 rows read by one MFMA operand fall in distinct banks.
 __device__ __forceinline__ uint32_t qpos(int r, int c) { return (uint32_t)(r * 16 + (c ^ (r & 15))) * 16u; }
 
+// This lane's key operands of one block: key 64 blk + 16 t + m16, channels
+// 32 i + 8 kg .. + 7 (zero beyond T).
+__device__ __forceinline__ void load_keys(H8 (&a)[4][4], const uint16_t *kb, int64_t T, int blk, int kg, int m16) {
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int64_t key = (int64_t)blk * P + 16 * t + m16;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      a[t][i].v = key < T ? *(const uint4 *)(kb + key * D + 32 * i + 8 * kg) : make_uint4(0, 0, 0, 0);
+  }
+}
+
+// Sum and maximum over the 4 lanes of a row (lanes m16 + 16 kg): the row swaps pair
+// lane l with l ^ 32, then with l ^ 16.
+__device__ __forceinline__ float row_sum4(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+__device__ __forceinline__ float row_max4(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+// Sum over the tile of exp2(s * sl2 - ref) across the 4 lanes of each row; with
+// MASKED only the keys <= last (and < T) count.  key0 is the key of s[0][0] for kg = 0.
+template <bool MASKED>
+__device__ __forceinline__ float tile_sum(const f4 (&s)[4], float sl2, float ref, int64_t key0, int kg,
+                                          int64_t last, int64_t T) {
+  float x[16];
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[4 * t + e] = __builtin_amdgcn_exp2f(fmaf(s[t][e], sl2, -ref));
+      if (MASKED) {
+        const int64_t key = key0 + 16 * t + 4 * kg + e;
+        x[4 * t + e] = key <= last && key < T ? x[4 * t + e] : 0.f;
+      }
+    }
+#pragma unroll
+  for (int w = 8; w >= 1; w >>= 1)  // pairwise: a chain of depth 4
+#pragma unroll
+    for (int j = 0; j < w; ++j) x[j] += x[j + w];
+  return row_sum4(x[0]);
+}
+
+template <bool MASKED>
+__device__ __forceinline__ float tile_max(const f4 (&s)[4], float sl2, int64_t key0, int kg, int64_t last,
+                                          int64_t T) {
+  float bm = kNegInf;
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int64_t key = key0 + 16 * t + 4 * kg + e;
+      if (!MASKED || (key <= last && key < T)) bm = fmaxf(bm, s[t][e] * sl2);
+    }
+  return row_max4(bm);
+}
+
+// Log-sum-exp (log2 units) of one (block, 16-row tile): sum_j exp2(x_j - ref) with
+// ref the row's running maximum, redone against the tile's own maximum when that
+// sum overflows (always on a row's first block, where ref = -inf).
+template <bool MASKED>
+__device__ __forceinline__ float tile_lse(const f4 (&s)[4], float sl2, float ref, int64_t key0, int kg, int64_t last,
+                                          int64_t T) {
+  // a row's first block (ref = -inf) goes straight to the tile maximum
+  float sum = __any(ref == kNegInf) ? __builtin_inff() : tile_sum<MASKED>(s, sl2, ref, key0, kg, last, T);
+  if (__any(!(sum <= 0x1p100f))) {
+    ref = tile_max<MASKED>(s, sl2, key0, kg, last, T);
+    sum = ref == kNegInf ? 0.f : tile_sum<MASKED>(s, sl2, ref, key0, kg, last, T);
+  }
+  return sum > 0.f ? ref + __builtin_amdgcn_logf(sum) : kNegInf;
+}
+
+// Logits and per-block log-sum-exp.  Each wavefront takes kObsBlocksPerWave blocks
+// and, per block, every 16-row tile of the group's queries: 16 MFMAs give the 64 x 16
+// logits, then sum_j exp2(x_j - ref) over the block's visible keys with ref the row's
+// running maximum of block log-sum-exps (kept in LDS per wavefront and row).  The
+// block's log-sum-exp is ref + log2(sum), whatever ref is, as long as the sum neither
+// overflows (then the tile is redone against the block's own maximum) nor loses all
+// its terms (a block 2^-126 below an earlier one, whose share is below fp32
+// resolution).  The running (max, sum) over the wavefront's blocks are merged over
+// the workgroup into one (max, sum) per (row, workgroup chunk).
 __global__ void __launch_bounds__(kObsThreads) obs_logit_kernel(const uint16_t *__restrict__ q_obs,
                                                                 const uint16_t *__restrict__ k_src, int n_obs,
                                                                 int G, int Hkv, int64_t T, int nblk, int Rpad,
-                                                                float sl2, float *__restrict__ lse) {
+                                                                float sl2, float *__restrict__ lse,
+                                                                float2 *__restrict__ part) {
   extern __shared__ __align__(16) uint8_t qs[];
+  float2 *stats = (float2 *)(qs + Rpad * 256);  // [8 wavefronts][Rpad] running (max, sum)
   const int h = blockIdx.y, b = blockIdx.z;
   const int64_t u = (int64_t)b * Hkv + h;
   const int R = n_obs * G, Hq = Hkv * G;
-  // stage the group's query rows (zero rows beyond R)
   for (int i = threadIdx.x; i < Rpad * 16; i += kObsThreads) {
     const int r = i >> 4, c = i & 15;
     uint4 v = make_uint4(0, 0, 0, 0);
@@ -62,88 +150,74 @@ __global__ void __launch_bounds__(kObsThreads) obs_logit_kernel(const uint16_t *
     }
     *(uint4 *)(qs + qpos(r, c)) = v;
   }
+  for (int i = threadIdx.x; i < 8 * Rpad; i += kObsThreads) stats[i] = make_float2(kNegInf, 0.f);
   __syncthreads();
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, kg = lane >> 4, m16 = lane & 15;
+  float2 *wst = stats + wv * Rpad;
   const uint16_t *kb = k_src + u * T * D;
   const int64_t first_masked = T - n_obs + 1;  // keys at or beyond this are hidden from some row
-  for (int k = 0; k < kObsBlocksPerWave; ++k) {
-    const int blk = blockIdx.x * kObsChunk + wv * kObsBlocksPerWave + k;
-    if (blk >= nblk) break;
-    // this lane's key operands: key 64 blk + 16 t + m16, channels 32 i + 8 kg .. + 7
-    H8 a[4][4];
+  const int blk0 = blockIdx.x * kObsChunk + wv * kObsBlocksPerWave;
+  const int nb = blk0 >= nblk ? 0 : (nblk - blk0 < kObsBlocksPerWave ? nblk - blk0 : kObsBlocksPerWave);
+  H8 a[4][4];
+  for (int k = 0; k < nb; ++k) {
+    const int blk = blk0 + k;
+    load_keys(a, kb, T, blk, kg, m16);
+    const int64_t key0 = (int64_t)blk * P;
+    const bool masked = key0 + P > first_masked;  // uniform: the block has hidden keys
+    for (int rt = 0; rt < Rpad / 16; rt += 2) {  // two row tiles at a time (Rpad is a multiple of 32)
+      int row[2];
+      H8 qb[2][4];
+      float2 run[2];
+      f4 s[2][4];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int64_t key = (int64_t)blk * P + 16 * t + m16;
+      for (int p = 0; p < 2; ++p) {
+        row[p] = 16 * (rt + p) + m16;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        a[t][i].v = key < T ? *(const uint4 *)(kb + key * D + 32 * i + 8 * kg) : make_uint4(0, 0, 0, 0);
-    }
-    const bool masked = (int64_t)blk * P + P > first_masked;  // uniform: the block has hidden keys
-    for (int rt = 0; rt < Rpad / 16; ++rt) {
-      const int row = 16 * rt + m16;
-      H8 qb[4];
+        for (int i = 0; i < 4; ++i) qb[p][i].v = *(const uint4 *)(qs + qpos(row[p], 4 * i + kg));
+        run[p] = wst[row[p]];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) qb[i].v = *(const uint4 *)(qs + qpos(row, 4 * i + kg));
-      f4 s[4];
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        s[t] = f4{0, 0, 0, 0};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) s[t] = mfma32(a[t][i].h, qb[i].h, s[t]);
+        for (int t = 0; t < 4; ++t) s[p][t] = f4{0, 0, 0, 0};
       }
-      // s[t][e]: key 64 blk + 16 t + 4 kg + e, query row `row`
-      float x[16];
 #pragma unroll
-      for (int t = 0; t < 4; ++t)
+      for (int i = 0; i < 4; ++i)  // eight independent accumulation chains
 #pragma unroll
-        for (int e = 0; e < 4; ++e) x[4 * t + e] = s[t][e] * sl2;
-      if (masked) {
-        const int64_t last = T - n_obs + row / G;  // the last key this row sees
+        for (int p = 0; p < 2; ++p)
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
+          for (int t = 0; t < 4; ++t) s[p][t] = mfma32(a[t][i].h, qb[p][i].h, s[p][t]);
+      // s[p][t][e]: key 64 blk + 16 t + 4 kg + e, query row row[p]
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int64_t key = (int64_t)blk * P + 16 * t + 4 * kg + e;
-            if (key > last || key >= T) x[4 * t + e] = kNegInf;
+      for (int p = 0; p < 2; ++p) {
+        const int64_t last = T - n_obs + row[p] / G;  // the last key this row sees
+        const float v = masked ? tile_lse<true>(s[p], sl2, run[p].x, key0, kg, last, T)
+                               : tile_lse<false>(s[p], sl2, run[p].x, key0, kg, last, T);
+        if (kg == 0 && row[p] < R) {
+          lse[(u * nblk + blk) * Rpad + row[p]] = v;
+          if (v != kNegInf) {  // the wavefront's running (max, sum) of this row
+            float2 r2 = run[p];
+            if (v > r2.x) {
+              r2.y = r2.y * __builtin_amdgcn_exp2f(r2.x - v) + 1.f;
+              r2.x = v;
+            } else {
+              r2.y += __builtin_amdgcn_exp2f(v - r2.x);
+            }
+            wst[row[p]] = r2;
           }
+        }
       }
-      float bm = x[0];
-#pragma unroll
-      for (int j = 1; j < 16; ++j) bm = fmaxf(bm, x[j]);
-      bm = fmaxf(bm, __shfl_xor(bm, 16));
-      bm = fmaxf(bm, __shfl_xor(bm, 32));
-      float sum = 0.f;
-      if (bm != kNegInf) {
-#pragma unroll
-        for (int j = 0; j < 16; ++j) sum += __builtin_amdgcn_exp2f(x[j] - bm);
-      }
-      sum += __shfl_xor(sum, 16);
-      sum += __shfl_xor(sum, 32);
-      if (kg == 0 && row < R)
-        lse[(u * nblk + blk) * Rpad + row] = bm == kNegInf ? kNegInf : bm + __builtin_amdgcn_logf(sum);
     }
   }
-}
-
-// Running (max, sum) of exp2 over one slice of blocks, per row.
-__global__ void __launch_bounds__(256) obs_slice_kernel(const float *__restrict__ lse, int R, int Rpad, int nblk,
-                                                        int nslice, int Hkv, float2 *__restrict__ part) {
-  const int sl = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int64_t u = (int64_t)b * Hkv + h;
-  const int b0 = sl * kSlice, b1 = b0 + kSlice < nblk ? b0 + kSlice : nblk;
-  for (int r = threadIdx.x; r < R; r += 256) {
-    float m = kNegInf, s = 0.f;
-    for (int blk = b0; blk < b1; ++blk) {
-      const float v = lse[(u * nblk + blk) * Rpad + r];
-      if (v == kNegInf) continue;
-      if (v > m) {
-        s = s * __builtin_amdgcn_exp2f(m - v) + 1.f;
-        m = v;
-      } else {
-        s += __builtin_amdgcn_exp2f(v - m);
+  __syncthreads();
+  // merge the wavefronts' running sums: one (max, sum) per (row, chunk)
+  for (int r = threadIdx.x; r < R; r += kObsThreads) {
+    float m = kNegInf;
+    for (int w = 0; w < 8; ++w) m = fmaxf(m, stats[w * Rpad + r].x);
+    float sm = 0.f;
+    if (m != kNegInf)
+      for (int w = 0; w < 8; ++w) {
+        const float2 p = stats[w * Rpad + r];
+        if (p.x != kNegInf) sm += p.y * __builtin_amdgcn_exp2f(p.x - m);
       }
-    }
-    part[(u * nslice + sl) * Rpad + r] = make_float2(m, s);
+    part[(u * gridDim.x + blockIdx.x) * Rpad + r] = make_float2(m, sm);
   }
 }
 
@@ -154,7 +228,7 @@ __global__ void __launch_bounds__(256) obs_row_kernel(const float2 *__restrict__
   for (int r = threadIdx.x; r < R; r += 256) {
     float m = kNegInf;
     for (int sl = 0; sl < nslice; ++sl) m = fmaxf(m, part[(u * nslice + sl) * Rpad + r].x);
-    float s = 0.f;
+    float s = 0.f;  // every row sees key 0, so m is finite
     for (int sl = 0; sl < nslice; ++sl) {
       const float2 p = part[(u * nslice + sl) * Rpad + r];
       if (p.x != kNegInf) s += p.y * __builtin_amdgcn_exp2f(p.x - m);
@@ -250,7 +324,7 @@ __global__ void __launch_bounds__(D) alloc_kernel(const uint16_t *__restrict__ k
   }
 }
 
-int rows_padded(int R) { return (R + 15) / 16 * 16; }
+int rows_padded(int R) { return (R + 31) / 32 * 32; }
 int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
 
 struct ObsLayout {
@@ -264,7 +338,7 @@ ObsLayout obs_layout(int B, int Hkv, int Hq, int64_t T, int n_obs) {
   L.nblk = (int)((T + P - 1) / P);
   L.R = n_obs * (Hq / Hkv);
   L.Rpad = rows_padded(L.R);
-  L.nslice = (L.nblk + kSlice - 1) / kSlice;
+  L.nslice = (L.nblk + kObsChunk - 1) / kObsChunk;
   L.lse = 0;
   L.part = align256(units * L.nblk * L.Rpad * 4);
   L.rows = L.part + align256(units * L.nslice * L.Rpad * 8);
@@ -305,10 +379,8 @@ extern "C" gkv_status gkv_observe_mass(const uint16_t *q_obs, int32_t n_obs, con
   float *rows = (float *)(w + L.rows);
   const int G = Hq / Hkv;
   const float sl2 = 1.4426950408889634f / sqrtf((float)D);
-  hipLaunchKernelGGL(obs_logit_kernel, dim3((L.nblk + kObsChunk - 1) / kObsChunk, Hkv, B), dim3(kObsThreads),
-                     L.Rpad * 256, s, q_obs, k_src, n_obs, G, Hkv, T, L.nblk, L.Rpad, sl2, lse);
-  hipLaunchKernelGGL(obs_slice_kernel, dim3(L.nslice, Hkv, B), dim3(256), 0, s, lse, L.R, L.Rpad, L.nblk, L.nslice,
-                     Hkv, part);
+  hipLaunchKernelGGL(obs_logit_kernel, dim3(L.nslice, Hkv, B), dim3(kObsThreads), L.Rpad * (256 + 8 * 8), s, q_obs,
+                     k_src, n_obs, G, Hkv, T, L.nblk, L.Rpad, sl2, lse, part);
   hipLaunchKernelGGL(obs_row_kernel, dim3(Hkv, B), dim3(256), 0, s, part, L.R, L.Rpad, L.nslice, Hkv, rows);
   hipLaunchKernelGGL(obs_mass_kernel, dim3((L.nblk + 3) / 4, Hkv, B), dim3(256), 0, s, lse, rows, L.R, L.Rpad,
                      L.nblk, Hkv, alpha, mass);
