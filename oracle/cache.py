@@ -16,11 +16,13 @@ P = 64
 
 
 class UnitCache:
-    def __init__(self, k_bits, v_bits, levels):
-        """k_bits, v_bits: uint16 [T][D] exact fp16; levels per block (oldest first)."""
+    def __init__(self, k_bits, v_bits, levels, v_per_token=False):
+        """k_bits, v_bits: uint16 [T][D] exact fp16; levels per block (oldest first);
+        v_per_token groups the values' scalar levels per token (section 3.2 text)."""
         self.T = k_bits.shape[0]
         self.D = k_bits.shape[1]
         self.levels = np.array(levels, dtype=np.int8)
+        self.v_per_token = bool(v_per_token)
         self.k_recs = []
         self.v_recs = []
         # decode-time certificate numbers per block (see certificate.decode_bound)
@@ -34,7 +36,7 @@ class UnitCache:
             if rows.stop - rows.start < P and lv != EXACT:
                 raise ValueError("only an exact block may be partial")
             self.k_recs.append(quant.encode_fp16(lv, kb))
-            self.v_recs.append(quant.encode_fp16(lv, vb))
+            self.v_recs.append(quant.encode_fp16(lv, vb, v_per_token))
             ke, _ = certificate.block_numbers(fp16.to_f64(kb), quant.decode(self.k_recs[-1]))
             ve, vn = certificate.block_numbers(fp16.to_f64(vb), quant.decode(self.v_recs[-1]))
             self.kerr.append(ke)
@@ -102,7 +104,7 @@ class UnitCache:
         if t % P == 0:
             z = np.zeros((P, self.D), dtype=np.uint16)
             self.k_recs.append(quant.Record(EXACT, exact=z.copy()))
-            self.v_recs.append(quant.Record(EXACT, exact=z.copy()))
+            self.v_recs.append(quant.Record(EXACT, exact=z.copy(), per_token=self.v_per_token))
             self.levels = np.append(self.levels, np.int8(EXACT))
             self.kerr.append(0.0)
             self.verr.append(0.0)

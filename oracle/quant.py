@@ -11,7 +11,10 @@ Readings (the paper gives no rounding mode, scale precision or degenerate case;
 these are chosen because both sides can reproduce them exactly in fp64):
 
 * Scalar level b, asymmetric, one group per channel over the block's 64 tokens,
-  for keys AND values (the workloads fix per-block-per-channel groups):
+  for keys AND values (the workloads fix per-block-per-channel groups); the
+  paper's own text groups values per token instead (one group per token over its
+  128 channels), which `per_token=True` selects for a value block, with the same
+  formulas along the other axis:
       z16 = f16(min),  s16 = f16((max - min) / (2^b - 1)),
       code = 0 if s16 == 0 else clamp(rint((x - z16) / s16), 0, 2^b - 1),
   with fp64 arithmetic, IEEE division, rint = round-half-even, and one RNE
@@ -51,6 +54,7 @@ class Record:
     s16, z16   uint16 [D] fp16 bits                 (levels 8/4/2)
     cent16     uint16 [KCENT][D] fp16 bits          (level 1; [1][D] at level 0)
     ids        int32  [P] in [0, KCENT)             (level 1; all 0 at level 0)
+    per_token  s16, z16 are [P] (one group per token) instead of [D]
     """
 
     def __init__(self, level, **kw):
@@ -61,6 +65,7 @@ class Record:
         self.z16 = kw.get("z16")
         self.cent16 = kw.get("cent16")
         self.ids = kw.get("ids")
+        self.per_token = bool(kw.get("per_token", False))
 
 
 # ---------------------------------------------------------------- scalar levels
@@ -86,6 +91,16 @@ def quantize_scalar(x, bits):
 def dequant_scalar(codes, s16, z16):
     """Exact fp64 decode code * s16 + z16."""
     return codes.astype(np.float64) * fp16.to_f64(s16)[None, :] + fp16.to_f64(z16)[None, :]
+
+
+def quantize_scalar_per_token(x, bits):
+    """One group per token (row): the per-channel quantizer of the transpose."""
+    codes, s16, z16 = quantize_scalar(np.asarray(x, dtype=np.float64).T, bits)
+    return codes.T.copy(), s16, z16
+
+
+def dequant_scalar_per_token(codes, s16, z16):
+    return codes.astype(np.float64) * fp16.to_f64(s16)[:, None] + fp16.to_f64(z16)[:, None]
 
 
 # ---------------------------------------------------------------- centroid level
@@ -133,15 +148,19 @@ def dequant_centroid(cent16, ids):
 
 
 # ---------------------------------------------------------------- records
-def encode(level, x):
+def encode(level, x, per_token=False):
     """Encode float64 block x [P][D] at ``level``.  For level 16 x must be
-    fp16-representable (it is stored as-is)."""
+    fp16-representable (it is stored as-is).  per_token groups a scalar level per
+    token (value blocks read the paper's way); other levels ignore it."""
     level = int(level)
     if level == EXACT:
         bits = fp16.from_f64(x)
         assert np.array_equal(fp16.to_f64(bits), np.asarray(x, np.float64)), "exact level needs fp16 values"
         return Record(EXACT, exact=bits)
     if level in (INT8, INT4, INT2):
+        if per_token:
+            codes, s16, z16 = quantize_scalar_per_token(x, level)
+            return Record(level, codes=codes, s16=s16, z16=z16, per_token=True)
         codes, s16, z16 = quantize_scalar(x, level)
         return Record(level, codes=codes, s16=s16, z16=z16)
     if level == CENTROID:
@@ -153,12 +172,12 @@ def encode(level, x):
     raise ValueError(level)
 
 
-def encode_fp16(level, bits):
+def encode_fp16(level, bits, per_token=False):
     """Encode a block given as fp16 bit patterns [P][D]."""
     bits = np.asarray(bits, dtype=np.uint16)
     if int(level) == EXACT:
-        return Record(EXACT, exact=bits.copy())
-    return encode(level, fp16.to_f64(bits))
+        return Record(EXACT, exact=bits.copy(), per_token=per_token)
+    return encode(level, fp16.to_f64(bits), per_token)
 
 
 def decode(rec):
@@ -166,6 +185,8 @@ def decode(rec):
     if rec.level == EXACT:
         return fp16.to_f64(rec.exact)
     if rec.level in (INT8, INT4, INT2):
+        if rec.per_token:
+            return dequant_scalar_per_token(rec.codes, rec.s16, rec.z16)
         return dequant_scalar(rec.codes, rec.s16, rec.z16)
     if rec.level in (CENTROID, MEAN):
         return dequant_centroid(rec.cent16, rec.ids)
@@ -181,4 +202,6 @@ def demote(rec, to_level):
     representation (section 3.2: demotion only, never promotion)."""
     if ORDER[int(to_level)] >= ORDER[rec.level]:
         raise NotMonotone(f"demote {rec.level} -> {to_level} is not a demotion")
-    return encode(to_level, decode(rec))
+    out = encode(to_level, decode(rec), rec.per_token)
+    out.per_token = rec.per_token  # the grouping is a property of the tensor, kept down the ladder
+    return out

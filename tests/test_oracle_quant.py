@@ -193,3 +193,43 @@ def test_mean_level_demotion_from_centroid_weights_by_count():
     for lv in (8, 4, 2, 1, 0):
         chain = quant.demote(chain, lv)
     assert chain.level == 0
+
+
+@pytest.mark.parametrize("bits", [8, 4, 2])
+def test_per_token_codes_are_nearest_levels(bits):
+    """Per-token grouping (values read the paper's way): each token's codes are the
+    nearest of its own 2^b levels c*s_t + z_t, with exact rationals, and every
+    decoded value is within half a step of the input."""
+    x = _block(12, scale=2.0)[:8]  # 8 tokens x 128 channels
+    codes, s16, z16 = quant.quantize_scalar_per_token(x, bits)
+    assert codes.shape == x.shape and s16.shape == (8,) and z16.shape == (8,)
+    s, z = fp16.to_f64(s16), fp16.to_f64(z16)
+    qmax = (1 << bits) - 1
+    for t in range(8):
+        assert z[t] == float(np.float16(x[t].min())) or z[t] == 0.0
+        lv = [Fraction(c) * Fraction(s[t]) + Fraction(z[t]) for c in range(qmax + 1)]
+        for d in range(0, 128, 7):
+            fx = Fraction(x[t, d])
+            errs = [abs(fx - v) for v in lv]
+            assert errs[codes[t, d]] == min(errs)
+    rec = quant.encode(bits, np.vstack([x] * 8), per_token=True)
+    dec = quant.decode(rec)
+    step = np.repeat(fp16.to_f64(rec.s16)[:, None], 128, axis=1)
+    rng_lo = np.repeat(fp16.to_f64(rec.z16)[:, None], 128, axis=1)
+    inside = np.vstack([x] * 8) >= rng_lo
+    assert np.all(np.abs(dec - np.vstack([x] * 8))[inside] <= step[inside] / 2 + 1e-12)
+
+
+def test_per_token_grouping_is_kept_down_the_ladder():
+    x = _block(13)
+    r8 = quant.encode(8, x, per_token=True)
+    r4 = quant.demote(r8, 4)
+    assert r4.per_token and r4.s16.shape == (64,)
+    c, s, z = quant.quantize_scalar_per_token(quant.decode(r8), 4)
+    assert np.array_equal(r4.codes, c) and np.array_equal(r4.s16, s) and np.array_equal(r4.z16, z)
+    r1 = quant.demote(r4, 1)  # centroid state: no grouping, the flag only rides along
+    assert r1.level == 1 and r1.per_token
+    # per-token and per-channel differ on a block whose channels have different spreads
+    xc = x * np.linspace(0.1, 3.0, 128)[None, :]
+    xc = fp16.to_f64(fp16.from_f64(xc))
+    assert not np.array_equal(quant.decode(quant.encode(4, xc)), quant.decode(quant.encode(4, xc, per_token=True)))
