@@ -57,7 +57,9 @@ typedef enum gkv_level {
   GKV_EXACT = 16
 } gkv_level;
 
-typedef enum gkv_tensor { GKV_KEYS = 0, GKV_VALUES = 1 } gkv_tensor;
+/* GKV_VALUES_PER_TOKEN names a value record of a cache with v_per_token set; it is
+ * accepted by gkv_decode_record only. */
+typedef enum gkv_tensor { GKV_KEYS = 0, GKV_VALUES = 1, GKV_VALUES_PER_TOKEN = 2 } gkv_tensor;
 
 #define GKV_D 128
 #define GKV_P 64
@@ -86,6 +88,10 @@ typedef enum gkv_tensor { GKV_KEYS = 0, GKV_VALUES = 1 } gkv_tensor;
  *     int2: {8,24,14,30,6,22,12,28,4,20,10,26,0,16,2,18}[n&15]
  *   Decoded value = code * scale + zero, exact in fp64 (section 3.2 packed scalar
  *   quantizers; one group per channel over the block's 64 tokens).
+ *   Value records of a cache with v_per_token (one group per token over its 128
+ *   channels, the grouping of the section 3.2 text) keep the same size and code
+ *   layout, with scale[64] and zero[64] fp16 in token order, then 256 unused bytes
+ *   (written as zero): decoded value = code * scale[token] + zero[token].
  * GKV_CENTROID (1040 B): 4 x 128 fp16 centroids, then 64 two-bit ids (16 B; the
  *   id of token t is bits 2t..2t+1).  Key centroids are stored [centroid][channel];
  *   value centroids [channel & 15][channel >> 4][centroid].
@@ -129,6 +135,8 @@ typedef struct gkv_cache {
                                 vmax), raised by gkv_demote by the change of the
                                 reconstruction (triangle inequality) and kept by
                                 gkv_append; fp32 rounded upwards                     */
+  int32_t v_per_token;       /* 1: the values' int levels are grouped per token (see
+                                the record layout); 0: per channel, like the keys     */
 } gkv_cache;
 
 /* ---------------------------------------------------------------- host helpers */
@@ -181,7 +189,7 @@ gkv_status gkv_account(const gkv_cache *c, const int32_t *pages_host, int32_t to
 /* Decode one record (host copy) to codes / values, for inspection and tests.
  * values_host: [64][128] fp64 reconstruction (token-major); codes_host (optional,
  * int levels): [64][128]; scale_host, zero_host (optional, int levels): [128] fp16
- * in channel order; ids_host (optional, centroid or mean): [64]; cent_host
+ * in channel order ([64] in token order for tensor GKV_VALUES_PER_TOKEN); ids_host (optional, centroid or mean): [64]; cent_host
  * (optional): [4][128] fp16 for a centroid record, [128] for a mean record. */
 gkv_status gkv_decode_record(int32_t level, int32_t tensor, const uint8_t *rec_host, double *values_host,
                              int32_t *codes_host, uint16_t *scale_host, uint16_t *zero_host,

@@ -22,7 +22,7 @@ lib = ctypes.CDLL(_LIB_PATH)
 
 EXACT, INT8, INT4, INT2, CENTROID, MEAN = 16, 8, 4, 2, 1, 0
 LEVELS = (EXACT, INT8, INT4, INT2, CENTROID, MEAN)
-KEYS, VALUES = 0, 1
+KEYS, VALUES, VALUES_PER_TOKEN = 0, 1, 2
 PROFILES = {"tiny": 0, "graded": 1, "exact": 2, "rdv2": 3}
 P, D = 64, 128
 
@@ -38,6 +38,7 @@ class CacheStruct(ctypes.Structure):
         ("page", _i32), ("npage_cap", _i64), ("boxes", _vp),
         ("nres", _i32), ("nres_cap", _i32), ("res_idx", _vp), ("res_rows", _vp), ("res_mask", _vp),
         ("cert", _vp),
+        ("v_per_token", _i32),
     ]
 
 
@@ -200,7 +201,8 @@ def decode_record(level, tensor, rec):
                           _np_ptr(ids), _np_ptr(cent)), "decode_record")
     out = {"values": vals}
     if level in (INT8, INT4, INT2):
-        out.update(codes=codes, s16=s, z16=z)
+        g = P if tensor == VALUES_PER_TOKEN else D  # groups: tokens or channels
+        out.update(codes=codes, s16=s[:g].copy(), z16=z[:g].copy())
     if level == CENTROID:
         out.update(ids=ids, cent16=cent)
     if level == MEAN:
@@ -253,8 +255,10 @@ class GradedCache:
     """One layer's graded KV cache in device memory (section 3.2 ladder, optional
     Compressed-Quest boxes and exact residual)."""
 
-    def __init__(self, B, Hkv, Hq, T, nblk_cap, caps, page=0, npage_cap=0, nres_cap=0, device="cuda"):
+    def __init__(self, B, Hkv, Hq, T, nblk_cap, caps, page=0, npage_cap=0, nres_cap=0, device="cuda",
+                 v_per_token=False):
         self.device = torch.device(device)
+        self.v_per_token = bool(v_per_token)
         self.B, self.Hkv, self.Hq = B, Hkv, Hq
         self.units = B * Hkv
         self.nblk_cap = nblk_cap
@@ -304,6 +308,7 @@ class GradedCache:
         c.res_rows = self.res_rows.data_ptr() if self.nres_cap else None
         c.res_mask = self.res_mask.data_ptr() if self.nres_cap else None
         c.cert = self.cert.data_ptr()
+        c.v_per_token = int(self.v_per_token)
 
     def clone(self):
         """A read-only copy in separate device memory (same layout and offsets), for
@@ -324,7 +329,8 @@ class GradedCache:
 
     # ------------------------------------------------------------ construction
     @classmethod
-    def build(cls, k, v, Hq, levels, page=0, nres_cap=0, device="cuda", extra_blocks=0, slack=None):
+    def build(cls, k, v, Hq, levels, page=0, nres_cap=0, device="cuda", extra_blocks=0, slack=None,
+              v_per_token=False):
         """k, v: fp16 bits [B][Hkv][T][128] (numpy uint16 or torch int16/float16).
         levels: per-block levels, [nblk] (shared) or [B][Hkv][nblk].  Encodes every
         block at its level (gkv_quantize_block) and, with page > 0, writes the page
@@ -347,7 +353,8 @@ class GradedCache:
         npage_cap = 0
         if page:
             npage_cap = (((T + extra_blocks * P) // page) + 63) // 64 * 64
-        self = cls(B, Hkv, Hq, T, nblk_cap, caps, page=page, npage_cap=npage_cap, nres_cap=nres_cap, device=device)
+        self = cls(B, Hkv, Hq, T, nblk_cap, caps, page=page, npage_cap=npage_cap, nres_cap=nres_cap, device=device,
+                   v_per_token=v_per_token)
         for b in range(B):
             for h in range(Hkv):
                 for i in range(nblk):
@@ -534,7 +541,7 @@ class GradedCache:
 
     def record(self, b, h, blk, tensor):
         L, raw = self.record_bytes(b, h, blk, tensor)
-        d = decode_record(L, tensor, raw)
+        d = decode_record(L, VALUES_PER_TOKEN if tensor == VALUES and self.v_per_token else tensor, raw)
         d["level"] = L
         return d
 

@@ -630,6 +630,7 @@ struct IntBlock {
   half8 qh[4], ql[4];  // q * s as two fp16 terms
   f4 c0;               // per-block logit constant
   f4 acc[8], pb;       // block-local P.V on codes and sum of P
+  f4 ps, pz;           // values grouped per token: sum of P * scale and of P * zero
   float kerr, verr;    // certificate numbers of the block
 };
 
@@ -733,10 +734,20 @@ __device__ __forceinline__ f4 int_logits(const IntBlock &ib, const uint32_t *kw,
   return S;
 }
 
-// One 16-token tile of an int block: key codes at kt, value codes at vt (LDS).
-template <int BITS, bool PACK>
+// Per-token value scale and zero of this lane's 4 tokens of block tile ti (VTOK: the
+// block's value header, scale[64] then zero[64] in token order, at ebuf).
+__device__ __forceinline__ void tok_sz(const uint8_t *ebuf, int ti, int kg, U4 &sv, U4 &zv) {
+  *(uint2 *)sv.u = *(const uint2 *)(ebuf + 2 * (16 * ti + 4 * kg));
+  *(uint2 *)zv.u = *(const uint2 *)(ebuf + 128 + 2 * (16 * ti + 4 * kg));
+}
+
+// One 16-token tile of an int block: key codes at kt, value codes at vt (LDS).  With
+// VTOK (values grouped per token) P is scaled by each token's value scale before the
+// P.V product, and sum P * scale and sum P * zero are kept for the block epilogue.
+template <int BITS, bool PACK, bool VTOK>
 __device__ __forceinline__ void int_tile(const AttnParams &p, State &st, IntBlock &ib, const uint8_t *kt,
-                                         const uint8_t *vt, uint32_t tvalid, const Mag &mg, int lane) {
+                                         const uint8_t *vt, uint32_t tvalid, const Mag &mg, int lane, int ti,
+                                         const uint8_t *ebuf) {
   constexpr int NW = Unpack<BITS>::kWords;
   const int kg = lane >> 4;
   uint32_t kw[NW], vw[NW];  // value codes read now so that the softmax hides the latency
@@ -749,20 +760,33 @@ __device__ __forceinline__ void int_tile(const AttnParams &p, State &st, IntBloc
 #pragma unroll
     for (int j = 0; j < 8; ++j) ib.acc[j] *= alpha;
     ib.pb *= alpha;
+    if (VTOK) {
+      ib.ps *= alpha;
+      ib.pz *= alpha;
+    }
   }
   ib.pb = mfma16(kOnes, P4, ib.pb);
+  half4 PV = P4;
+  if (VTOK) {
+    U4 sv, zv;
+    tok_sz(ebuf, ti, kg, sv, zv);
+    PV = P4 * sv.h;  // one rounding of the exact fp16 product
+    ib.ps = mfma16(kOnes, PV, ib.ps);
+    ib.pz = mfma16(zv.h, P4, ib.pz);  // every row of A holds the 4 tokens' zeros
+  }
 #pragma unroll
   for (int j = 0; j < 8; ++j)
-    ib.acc[j] = mfma16(as_h4(Unpack<BITS>::pair(vw, 2 * j, mg), Unpack<BITS>::pair(vw, 2 * j + 1, mg)), P4, ib.acc[j]);
+    ib.acc[j] = mfma16(as_h4(Unpack<BITS>::pair(vw, 2 * j, mg), Unpack<BITS>::pair(vw, 2 * j + 1, mg)), PV, ib.acc[j]);
 }
 
 // Two consecutive tiles of an int block (tile B's codes follow tile A's).  P.V runs
 // as one 32-deep MFMA per channel group: the contraction index k = 8 kg + e takes
 // tile A's token 4 kg + e for e < 4 and tile B's token 4 kg + e - 4 for e >= 4, in
 // both operands, so each lane's operands are its own registers of the two tiles.
-template <int BITS, bool PACK>
+template <int BITS, bool PACK, bool VTOK>
 __device__ __forceinline__ void int_tile2(const AttnParams &p, State &st, IntBlock &ib, const uint8_t *kt,
-                                          const uint8_t *vt, uint32_t tvA, uint32_t tvB, const Mag &mg, int lane) {
+                                          const uint8_t *vt, uint32_t tvA, uint32_t tvB, const Mag &mg, int lane,
+                                          int ta, int tb, const uint8_t *ebuf) {
   constexpr int NW = Unpack<BITS>::kWords;
   constexpr int TB = 256 * BITS;  // code bytes of one tile and tensor
   const int kg = lane >> 4;
@@ -779,8 +803,24 @@ __device__ __forceinline__ void int_tile2(const AttnParams &p, State &st, IntBlo
 #pragma unroll
     for (int j = 0; j < 8; ++j) ib.acc[j] *= alpha;
     ib.pb *= alpha;
+    if (VTOK) {
+      ib.ps *= alpha;
+      ib.pz *= alpha;
+    }
   }
   ib.pb = mfma32(kOnes8, P8, ib.pb);
+  half8 PV = P8;
+  if (VTOK) {
+    U4 sA, zA, sB, zB;
+    tok_sz(ebuf, ta, kg, sA, zA);
+    tok_sz(ebuf, tb, kg, sB, zB);
+    U8 s8, z8;
+    s8.u[0] = sA.u[0]; s8.u[1] = sA.u[1]; s8.u[2] = sB.u[0]; s8.u[3] = sB.u[1];
+    z8.u[0] = zA.u[0]; z8.u[1] = zA.u[1]; z8.u[2] = zB.u[0]; z8.u[3] = zB.u[1];
+    PV = P8 * s8.h;
+    ib.ps = mfma32(kOnes8, PV, ib.ps);
+    ib.pz = mfma32(z8.h, P8, ib.pz);
+  }
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     U8 a;
@@ -788,14 +828,25 @@ __device__ __forceinline__ void int_tile2(const AttnParams &p, State &st, IntBlo
     a.u[1] = Unpack<BITS>::pair(vwA, 2 * j + 1, mg);
     a.u[2] = Unpack<BITS>::pair(vwB, 2 * j, mg);
     a.u[3] = Unpack<BITS>::pair(vwB, 2 * j + 1, mg);
-    ib.acc[j] = mfma32(a.h, P8, ib.acc[j]);
+    ib.acc[j] = mfma32(a.h, PV, ib.acc[j]);
   }
 }
 
 // End of an int block: O[d][h] += s_d * (acc - off * sum p) + z_d * sum p,
-// d = 16j + 4kg + r, with the value scale/zero at vsz (LDS).
-template <int BITS>
+// d = 16j + 4kg + r, with the value scale/zero at vsz (LDS).  With VTOK the scales
+// are already inside acc: O[d][h] += acc - off * sum p s + sum p z.
+template <int BITS, bool VTOK>
 __device__ __forceinline__ void int_epilogue(State &st, IntBlock &ib, const uint8_t *vsz, int lane) {
+  if (VTOK) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float off = v_off<BITS>(j);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) st.O[j][r] += fmaf(-off, ib.ps[r], ib.acc[j][r]) + ib.pz[r];
+    }
+    st.l += ib.pb[0];
+    return;
+  }
   const uint8_t *sz = vsz + (lane >> 4) * 64;
 #pragma unroll
   for (int hh = 0; hh < 2; ++hh) {  // two halves keep fewer scale/zero registers live
@@ -921,7 +972,7 @@ __device__ __forceinline__ bool exact_run(const AttnParams &p, State &st, const 
   return true;
 }
 
-template <int BITS, bool PACK, bool CERT>
+template <int BITS, bool PACK, bool CERT, bool VTOK>
 __device__ __forceinline__ bool int_run(const AttnParams &p, State &st, const uint8_t *qs, Pipe &pp,
                                         uint32_t &meta, uint64_t &valid, int lane) {
   IntBlock ib;
@@ -941,6 +992,10 @@ __device__ __forceinline__ bool int_run(const AttnParams &p, State &st, const ui
       }
       const uint8_t *sz = pp.template pop<0>();
       int_header<BITS, PACK>(ib, qs, sz, lane);
+      if (VTOK) {
+        ib.ps = f4{0, 0, 0, 0};
+        ib.pz = f4{0, 0, 0, 0};
+      }
       *(uint2 *)(pp.ebuf + 8 * lane) = *(const uint2 *)(sz + 2048 + 8 * lane);  // V scale/zero, kept
       pp.release(1);
     }
@@ -955,15 +1010,17 @@ __device__ __forceinline__ bool int_run(const AttnParams &p, State &st, const ui
       tl &= tl - 1;
       const int tb = __builtin_ctz(tl);
       tl &= tl - 1;
-      int_tile2<BITS, PACK>(p, st, ib, kq + j * 256 * BITS, vq + j * 256 * BITS,
-                            (uint32_t)(valid >> (16 * ta)) & 0xFFFFu, (uint32_t)(valid >> (16 * tb)) & 0xFFFFu, mg,
-                            lane);
+      int_tile2<BITS, PACK, VTOK>(p, st, ib, kq + j * 256 * BITS, vq + j * 256 * BITS,
+                                  (uint32_t)(valid >> (16 * ta)) & 0xFFFFu, (uint32_t)(valid >> (16 * tb)) & 0xFFFFu,
+                                  mg, lane, ta, tb, pp.ebuf);
     }
-    if (j < n)
-      int_tile<BITS, PACK>(p, st, ib, kq + j * 256 * BITS, vq + j * 256 * BITS,
-                           (uint32_t)(valid >> (16 * __builtin_ctz(tl))) & 0xFFFFu, mg, lane);
+    if (j < n) {
+      const int ta = __builtin_ctz(tl);
+      int_tile<BITS, PACK, VTOK>(p, st, ib, kq + j * 256 * BITS, vq + j * 256 * BITS,
+                                 (uint32_t)(valid >> (16 * ta)) & 0xFFFFu, mg, lane, ta, pp.ebuf);
+    }
     if (meta_last(meta)) {
-      int_epilogue<BITS>(st, ib, pp.ebuf, lane);
+      int_epilogue<BITS, VTOK>(st, ib, pp.ebuf, lane);
       if (CERT) cert_add(st, ib.pb[0], ib.kerr, ib.verr);
     }
     pp.release(BITS == 2 ? 1 : 2);
@@ -994,7 +1051,7 @@ __device__ __forceinline__ bool mean_run(const AttnParams &p, State &st, const u
   return true;
 }
 
-template <bool PACK, bool CERT>
+template <bool PACK, bool CERT, bool VTOK>
 __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   extern __shared__ __align__(16) uint8_t smem[];
   // Workgroup L of the one-dimensional grid serves (b, KV head) L % units as its
@@ -1062,9 +1119,9 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   while (more) {
     switch (meta_lv(meta)) {
       case GKV_EXACT: more = exact_run<PACK, CERT>(p, st, qs, pp, meta, valid, lane); break;
-      case GKV_INT8: more = int_run<8, PACK, CERT>(p, st, qs, pp, meta, valid, lane); break;
-      case GKV_INT4: more = int_run<4, PACK, CERT>(p, st, qs, pp, meta, valid, lane); break;
-      case GKV_INT2: more = int_run<2, PACK, CERT>(p, st, qs, pp, meta, valid, lane); break;
+      case GKV_INT8: more = int_run<8, PACK, CERT, VTOK>(p, st, qs, pp, meta, valid, lane); break;
+      case GKV_INT4: more = int_run<4, PACK, CERT, VTOK>(p, st, qs, pp, meta, valid, lane); break;
+      case GKV_INT2: more = int_run<2, PACK, CERT, VTOK>(p, st, qs, pp, meta, valid, lane); break;
       case GKV_CENTROID: more = centroid_run<PACK, CERT>(p, st, qs, pp, meta, valid, lane); break;
       default: more = mean_run<PACK, CERT>(p, st, qs, pp, meta, valid, lane); break;
     }
@@ -1746,12 +1803,26 @@ static void launch_plan(const AttnParams &p, const gkv_cache *c, hipStream_t s) 
 static void launch_partials(const AttnParams &p, const gkv_cache *c, hipStream_t s) {
   const size_t lds = (size_t)kWaves * kWaveLds + 16 * kQRow;  // rings also hold the merge buffers
   const dim3 grid(p.nsplit * c->Hkv * c->B);
-  if (p.bound) {  // the certificate sums are a separate instantiation: the plain decode keeps its registers
-    if (p.G <= 8) hipLaunchKernelGGL((attn_kernel<true, true>), grid, dim3(kThreads), lds, s, p);
-    else hipLaunchKernelGGL((attn_kernel<false, true>), grid, dim3(kThreads), lds, s, p);
+  // the certificate sums and per-token value groups are separate instantiations: the
+  // plain decode keeps its registers
+  const bool pack = p.G <= 8, cert = p.bound != nullptr, vtok = c->v_per_token != 0;
+  const dim3 blk(kThreads);
+  if (vtok) {
+    if (cert) {
+      if (pack) hipLaunchKernelGGL((attn_kernel<true, true, true>), grid, blk, lds, s, p);
+      else hipLaunchKernelGGL((attn_kernel<false, true, true>), grid, blk, lds, s, p);
+    } else {
+      if (pack) hipLaunchKernelGGL((attn_kernel<true, false, true>), grid, blk, lds, s, p);
+      else hipLaunchKernelGGL((attn_kernel<false, false, true>), grid, blk, lds, s, p);
+    }
   } else {
-    if (p.G <= 8) hipLaunchKernelGGL((attn_kernel<true, false>), grid, dim3(kThreads), lds, s, p);
-    else hipLaunchKernelGGL((attn_kernel<false, false>), grid, dim3(kThreads), lds, s, p);
+    if (cert) {
+      if (pack) hipLaunchKernelGGL((attn_kernel<true, true, false>), grid, blk, lds, s, p);
+      else hipLaunchKernelGGL((attn_kernel<false, true, false>), grid, blk, lds, s, p);
+    } else {
+      if (pack) hipLaunchKernelGGL((attn_kernel<true, false, false>), grid, blk, lds, s, p);
+      else hipLaunchKernelGGL((attn_kernel<false, false, false>), grid, blk, lds, s, p);
+    }
   }
 }
 static void launch_merge(const AttnParams &p, const gkv_cache *c, float *out, hipStream_t s) {

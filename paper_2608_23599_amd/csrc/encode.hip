@@ -23,6 +23,7 @@ struct EncodeShared {
   uint8_t xc[P * D];       // source as codes (int-level record being demoted)
   double xs[D], xz[D];     // source scale / zero for xc
   int32_t src_int;         // 1: x = xc * xs + xz, 0: x = xh, 2: x = centroid[xc]
+  int32_t src_tok;         // with src_int == 1: xs, xz are per token (index t), else per channel
   double sc[KC * D];       // source centroids (fp64) when src_int == 2
   double c[KC * XS];       // centroids (fp64)
   double dist[P * KC];     // token x centroid distances
@@ -39,8 +40,9 @@ struct EncodeShared {
 __device__ __forceinline__ double getx(const EncodeShared &S, int t, int d) {
   if (S.src_int == 2) return S.sc[S.xc[t * D] * D + d];
   if (S.src_int) {
-    const double prod = (double)S.xc[t * D + d] * S.xs[d];
-    return prod + S.xz[d];
+    const int g = S.src_tok ? t : d;
+    const double prod = (double)S.xc[t * D + d] * S.xs[g];
+    return prod + S.xz[g];
   }
   return (double)__builtin_bit_cast(_Float16, S.xh[t * D + d]);
 }
@@ -48,7 +50,10 @@ __device__ __forceinline__ double getx(const EncodeShared &S, int t, int d) {
 // Load the 64 x 128 block starting at row0 of one (b,h) from token-major fp16 rows;
 // rows at or beyond T_src read as zero.
 __device__ void load_rows(EncodeShared &S, const uint16_t *src, int64_t T_src, int64_t row0) {
-  if (threadIdx.x == 0) S.src_int = 0;
+  if (threadIdx.x == 0) {
+    S.src_int = 0;
+    S.src_tok = 0;
+  }
   for (int i = threadIdx.x; i < P * (D / 8); i += kThreads) {
     const int t = i / (D / 8), c8 = (i % (D / 8)) * 8;
     uint4 v = make_uint4(0, 0, 0, 0);
@@ -57,8 +62,9 @@ __device__ void load_rows(EncodeShared &S, const uint16_t *src, int64_t T_src, i
   }
 }
 
-// Load a record (exact or int level) as the source.
-__device__ void load_record(EncodeShared &S, const uint8_t *rec, int level, int tensor) {
+// Load a record as the source (per_token: an int-level value record grouped per token).
+__device__ void load_record(EncodeShared &S, const uint8_t *rec, int level, int tensor, bool per_token) {
+  if (threadIdx.x == 0) S.src_tok = per_token && is_int_level(level);
   if (level == GKV_EXACT) {
     if (threadIdx.x == 0) S.src_int = 0;
     const uint16_t *hh = (const uint16_t *)rec;
@@ -92,10 +98,17 @@ __device__ void load_record(EncodeShared &S, const uint8_t *rec, int level, int 
   }
   if (threadIdx.x == 0) S.src_int = 1;
   const uint16_t *sz = (const uint16_t *)rec;
-  for (int e = threadIdx.x; e < D; e += kThreads) {
-    const int ch = sz_channel(tensor, e);
-    S.xs[ch] = (double)__builtin_bit_cast(_Float16, sz[e]);
-    S.xz[ch] = (double)__builtin_bit_cast(_Float16, sz[D + e]);
+  if (per_token) {
+    for (int t = threadIdx.x; t < P; t += kThreads) {
+      S.xs[t] = (double)__builtin_bit_cast(_Float16, sz[t]);
+      S.xz[t] = (double)__builtin_bit_cast(_Float16, sz[P + t]);
+    }
+  } else {
+    for (int e = threadIdx.x; e < D; e += kThreads) {
+      const int ch = sz_channel(tensor, e);
+      S.xs[ch] = (double)__builtin_bit_cast(_Float16, sz[e]);
+      S.xz[ch] = (double)__builtin_bit_cast(_Float16, sz[D + e]);
+    }
   }
   const int bits = level;
   const uint32_t *w = (const uint32_t *)(rec + kSZBytes);
@@ -127,14 +140,15 @@ __device__ void write_exact(EncodeShared &S, uint8_t *dst, int tensor) {
   }
 }
 
-// Scalar quantizer, one group per channel (section 3.2).
-__device__ void encode_int(EncodeShared &S, uint8_t *dst, int bits, int tensor) {
+// Scalar quantizer, one group per channel, or per token for a value block of a
+// cache that groups values per token (section 3.2).
+__device__ void encode_int(EncodeShared &S, uint8_t *dst, int bits, int tensor, bool per_token) {
   const double qmax = (double)((1 << bits) - 1);
   const int tid = threadIdx.x;
-  if (tid < D) {
-    double mn = getx(S, 0, tid), mx = mn;
-    for (int t = 1; t < P; ++t) {
-      const double v = getx(S, t, tid);
+  if (tid < (per_token ? P : D)) {
+    double mn = per_token ? getx(S, tid, 0) : getx(S, 0, tid), mx = mn;
+    for (int i = 1; i < (per_token ? D : P); ++i) {
+      const double v = per_token ? getx(S, tid, i) : getx(S, i, tid);
       mn = v < mn ? v : mn;
       mx = v > mx ? v : mx;
     }
@@ -148,11 +162,11 @@ __device__ void encode_int(EncodeShared &S, uint8_t *dst, int bits, int tensor) 
   }
   __syncthreads();
   for (int i = tid; i < P * D; i += kThreads) {
-    const int t = i >> 7, d = i & 127;
-    const double s = S.s64[d];
+    const int t = i >> 7, d = i & 127, g = per_token ? t : d;
+    const double s = S.s64[g];
     uint8_t code = 0;
     if (s != 0.0) {
-      const double diff = getx(S, t, d) - S.z64[d];
+      const double diff = getx(S, t, d) - S.z64[g];
       double r = __builtin_rint(diff / s);
       r = r < 0.0 ? 0.0 : r;
       r = r > qmax ? qmax : r;
@@ -162,10 +176,14 @@ __device__ void encode_int(EncodeShared &S, uint8_t *dst, int bits, int tensor) 
   }
   __syncthreads();
   uint16_t *sz = (uint16_t *)dst;
-  for (int e = tid; e < D; e += kThreads) {
-    const int ch = sz_channel(tensor, e);
-    sz[e] = S.s16[ch];
-    sz[D + e] = S.z16[ch];
+  if (per_token) {  // scale[64], zero[64] in token order, then zeros
+    for (int e = tid; e < 2 * D; e += kThreads) sz[e] = e < P ? S.s16[e] : (e < 2 * P ? S.z16[e - P] : 0);
+  } else {
+    for (int e = tid; e < D; e += kThreads) {
+      const int ch = sz_channel(tensor, e);
+      sz[e] = S.s16[ch];
+      sz[D + e] = S.z16[ch];
+    }
   }
   uint32_t *w = (uint32_t *)(dst + kSZBytes);
   for (int ck = tid; ck < 4 * 64; ck += kThreads) {
@@ -267,9 +285,9 @@ __device__ void encode_mean(EncodeShared &S, uint8_t *dst) {
   if (tid < P) S.assign[tid] = 0;
 }
 
-__device__ void encode_to(EncodeShared &S, uint8_t *dst, int level, int tensor) {
+__device__ void encode_to(EncodeShared &S, uint8_t *dst, int level, int tensor, bool per_token) {
   if (level == GKV_EXACT) write_exact(S, dst, tensor);
-  else if (is_int_level(level)) encode_int(S, dst, level, tensor);
+  else if (is_int_level(level)) encode_int(S, dst, level, tensor, per_token);
   else if (level == GKV_MEAN) encode_mean(S, dst);
   else encode_centroid(S, dst, tensor);
 }
@@ -286,13 +304,16 @@ __device__ __forceinline__ float round_up_f32(double x) {
 // err = max_t ||x_t - x_hat_t|| and nrm = max_t ||x_t|| over the 64 rows (fp64; x is
 // the source, x_hat the new record's reconstruction).  256 threads: 4 per row, 32
 // channels each.  Result in S.cert[0..1].
-__device__ void block_cert(EncodeShared &S, int level) {
+__device__ void block_cert(EncodeShared &S, int level, bool per_token) {
   const int t = threadIdx.x >> 2, j = threadIdx.x & 3;
   double e = 0.0, n = 0.0;
   for (int d = 32 * j; d < 32 * j + 32; ++d) {
     const double x = getx(S, t, d);
     double xh = x;
-    if (is_int_level(level)) xh = (double)S.codes[t * D + d] * S.s64[d] + S.z64[d];
+    if (is_int_level(level)) {
+      const int g = per_token ? t : d;
+      xh = (double)S.codes[t * D + d] * S.s64[g] + S.z64[g];
+    }
     else if (level == GKV_CENTROID || level == GKV_MEAN) xh = S.c[S.assign[t] * XS + d];
     e += (x - xh) * (x - xh);
     n += x * x;
@@ -323,18 +344,19 @@ __global__ void __launch_bounds__(kThreads) quantize_kernel(const uint16_t *__re
                                                             const int8_t *__restrict__ level,
                                                             const int64_t *__restrict__ off, uint8_t *arena,
                                                             int Hkv, int nblk_cap, int blk0, int tensor,
-                                                            float *cert) {
+                                                            float *cert, int vtok) {
   extern __shared__ __align__(16) unsigned char smem[];
   EncodeShared &S = *reinterpret_cast<EncodeShared *>(smem);
   const int blk = blk0 + blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int64_t u = (int64_t)b * Hkv + h;
   const int lv = level[u * nblk_cap + blk];
+  const bool per_token = tensor == GKV_VALUES && vtok;
   load_rows(S, src + u * T_src * D, T_src, (int64_t)blk * P);
   __syncthreads();
-  encode_to(S, arena + off[u * nblk_cap + blk], lv, tensor);
+  encode_to(S, arena + off[u * nblk_cap + blk], lv, tensor, per_token);
   if (cert) {  // error against the exact rows; the value tensor also keeps the row norms
     __syncthreads();
-    block_cert(S, lv);
+    block_cert(S, lv, per_token);
     if (threadIdx.x == 0) {
       float *cb = cert + (u * nblk_cap + blk) * 4;
       if (tensor == GKV_KEYS) {
@@ -360,7 +382,7 @@ struct DemoteJobs {
 // tables, writes the new record, then points the tables at it.
 __global__ void __launch_bounds__(kThreads) demote_kernel(DemoteJobs jobs, int8_t *level, int64_t *koff,
                                                           int64_t *voff, uint8_t *arena, int Hkv, int nblk_cap,
-                                                          float *cert) {
+                                                          float *cert, int vtok) {
   extern __shared__ __align__(16) unsigned char smem[];
   EncodeShared &S = *reinterpret_cast<EncodeShared *>(smem);
   const int j = blockIdx.x, tensor = blockIdx.y;
@@ -368,12 +390,13 @@ __global__ void __launch_bounds__(kThreads) demote_kernel(DemoteJobs jobs, int8_
   const int cur = jobs.cur[j];
   int64_t *offt = tensor == GKV_KEYS ? koff : voff;
   const int64_t dst = tensor == GKV_KEYS ? jobs.koff[j] : jobs.voff[j];
-  load_record(S, arena + offt[idx], cur, tensor);
+  const bool per_token = tensor == GKV_VALUES && vtok;
+  load_record(S, arena + offt[idx], cur, tensor, per_token);
   __syncthreads();
-  encode_to(S, arena + dst, jobs.to[j], tensor);
+  encode_to(S, arena + dst, jobs.to[j], tensor, per_token);
   __syncthreads();
   if (cert) {  // the error grows by at most the change of the reconstruction
-    block_cert(S, jobs.to[j]);
+    block_cert(S, jobs.to[j], per_token);
     if (threadIdx.x == 0) {
       float *ce = cert + idx * 4 + (tensor == GKV_KEYS ? 0 : 1);
       *ce = round_up_f32((double)*ce + S.cert[0]);
@@ -505,13 +528,13 @@ __global__ void __launch_bounds__(kThreads) rd_score_kernel(const uint16_t *__re
                                                             const int8_t *__restrict__ level,
                                                             const int64_t *__restrict__ voff,
                                                             const uint8_t *__restrict__ arena, int Hkv,
-                                                            int nblk_cap, uint64_t *__restrict__ keys) {
+                                                            int nblk_cap, uint64_t *__restrict__ keys, int vtok) {
   extern __shared__ __align__(16) unsigned char smem[];
   EncodeShared &S = *reinterpret_cast<EncodeShared *>(smem);
   const int blk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int64_t u = (int64_t)b * Hkv + h;
   const int64_t ti = u * nblk_cap + blk;
-  load_record(S, arena + voff[ti], level[ti], GKV_VALUES);
+  load_record(S, arena + voff[ti], level[ti], GKV_VALUES, vtok != 0);
   __syncthreads();
   const int t = threadIdx.x;
   const int64_t tok = (int64_t)blk * P + t;
@@ -537,7 +560,7 @@ void gkv_launch_rd_score(const gkv_cache *c, const uint16_t *v_src, const float 
                          hipStream_t stream) {
   const int nblk = (int)((c->T + P - 1) / P);
   hipLaunchKernelGGL(rd_score_kernel, dim3(nblk, c->Hkv, c->B), dim3(kThreads), sizeof(EncodeShared), stream, v_src,
-                     mass, c->T, c->level, c->voff, c->arena, c->Hkv, c->nblk_cap, keys);
+                     mass, c->T, c->level, c->voff, c->arena, c->Hkv, c->nblk_cap, keys, c->v_per_token);
 }
 
 // ---------------------------------------------------------------- C ABI
@@ -563,7 +586,7 @@ extern "C" gkv_status gkv_quantize_block(const gkv_cache *c, int32_t which, cons
   dim3 grid(blk_end - blk_begin, c->Hkv, c->B);
   hipLaunchKernelGGL(quantize_kernel, grid, dim3(kThreads), sizeof(EncodeShared), (hipStream_t)stream, src,
                      T_src, c->level, which == GKV_KEYS ? c->koff : c->voff, c->arena, c->Hkv, c->nblk_cap,
-                     blk_begin, which, c->cert);
+                     blk_begin, which, c->cert, c->v_per_token);
   return hip_status();
 }
 
@@ -600,7 +623,7 @@ extern "C" gkv_status gkv_demote(gkv_cache *c, int32_t n, const int32_t *jobs, c
       J.voff[i] = nv[base + i];
     }
     hipLaunchKernelGGL(demote_kernel, dim3(cnt, 2), dim3(kThreads), sizeof(EncodeShared), (hipStream_t)stream, J,
-                       c->level, c->koff, c->voff, c->arena, c->Hkv, c->nblk_cap, c->cert);
+                       c->level, c->koff, c->voff, c->arena, c->Hkv, c->nblk_cap, c->cert, c->v_per_token);
     if (hipGetLastError() != hipSuccess) return GKV_E_HIP;
   }
   for (int i = 0; i < n; ++i)

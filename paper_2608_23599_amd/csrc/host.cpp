@@ -192,6 +192,7 @@ gkv_status gkv_validate_cache(const gkv_cache *c) {
   }
   if (c->nres < 0 || c->nres > c->nres_cap) return GKV_E_SHAPE;
   if (c->nres_cap > 0 && (!c->res_idx || !c->res_rows || !c->res_mask)) return GKV_E_ARG;
+  if (c->v_per_token != 0 && c->v_per_token != 1) return GKV_E_ARG;
   return GKV_OK;
 }
 
@@ -259,7 +260,27 @@ extern "C" gkv_status gkv_account(const gkv_cache *c, const int32_t *pages, int3
 extern "C" gkv_status gkv_decode_record(int32_t level, int32_t tensor, const uint8_t *rec, double *vals,
                                        int32_t *codes, uint16_t *scale, uint16_t *zero, int32_t *ids,
                                        uint16_t *cent) {
-  if (!rec || !vals || (tensor != GKV_KEYS && tensor != GKV_VALUES)) return GKV_E_ARG;
+  if (!rec || !vals || (tensor != GKV_KEYS && tensor != GKV_VALUES && tensor != GKV_VALUES_PER_TOKEN))
+    return GKV_E_ARG;
+  if (tensor == GKV_VALUES_PER_TOKEN && is_int_level(level)) {  // scale/zero per token
+    const int bits = level;
+    const uint16_t *sz = (const uint16_t *)rec;
+    const uint32_t *w = (const uint32_t *)(rec + kSZBytes);
+    for (int pg = 0; pg < 4; ++pg)
+      for (int l = 0; l < 64; ++l)
+        for (int n = 0; n < 32; ++n) {
+          int t, ch;
+          chunk_coord(GKV_VALUES, pg, l, n, t, ch);
+          const uint32_t word = w[(pg * 64 + l) * bits + code_word(bits, n)];
+          const int c = (int)((word >> code_pos(bits, n)) & ((1u << bits) - 1));
+          if (codes) codes[t * D + ch] = c;
+          vals[t * D + ch] = (double)c * f16_to_f64(sz[t]) + f16_to_f64(sz[P + t]);
+        }
+    if (scale) memcpy(scale, sz, P * sizeof(uint16_t));
+    if (zero) memcpy(zero, sz + P, P * sizeof(uint16_t));
+    return GKV_OK;
+  }
+  if (tensor == GKV_VALUES_PER_TOKEN) tensor = GKV_VALUES;
   if (level == GKV_EXACT) {
     const uint16_t *h = (const uint16_t *)rec;
     for (int pg = 0; pg < 4; ++pg)

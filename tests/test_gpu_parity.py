@@ -655,3 +655,89 @@ def test_rd128k_full_size_sampled(gpu, prof, frac):
         want, _ = uc.select_residual(ks[b, h], vs[b, h], mass[b, h], n)
         np.testing.assert_array_equal(idx[b, h, :n], want)
         assert max_err(out[b, h * G:(h + 1) * G], uc.decode_dense(q_group(q, b, h, G))) <= TOL
+
+
+# ---------------------------------------------------------------- values grouped per token
+
+
+def _units_per_token(ks, vs, lv):
+    B, Hkv = ks.shape[:2]
+    return {(b, h): ocache.UnitCache(ks[b, h], vs[b, h], lv, v_per_token=True) for b in range(B) for h in range(Hkv)}
+
+
+@pytest.mark.parametrize("prof,T,Bn,Hq,Hkv", [("tiny", 2048, 1, 8, 2), ("graded", 5000, 2, 28, 4),
+                                              ("tiny", 1000, 1, 32, 2)])
+def test_per_token_values_codes_attention_and_bound(gpu, prof, T, Bn, Hq, Hkv):
+    """Values quantised per token (one scale and zero per token over its channels):
+    records bit-exact (keys stay per channel), attention and certificate against the
+    oracle; G = 16 runs the kernel without packed query columns."""
+    torch = _torch()
+    ks, vs = kv_all(10, Bn, Hkv, T)
+    lv = olad.ladder(prof, T)
+    cache = _build(gpu, ks, vs, Hq, lv, v_per_token=True)
+    ucs = _units_per_token(ks, vs, lv)
+    for (b, h), uc in ucs.items():
+        for blk in sorted(set(range(0, len(lv), 3)) | {len(lv) - 1}):
+            compare_record(cache, uc, b, h, blk, 0)
+            compare_record(cache, uc, b, h, blk, 1)
+    q = synth.queries(10, Bn, Hq)
+    out, bnd = cache.decode_bound(q)
+    assert torch.equal(out, cache.decode(q))
+    out, bnd = out.cpu().numpy(), bnd.cpu().numpy()
+    G = Hq // Hkv
+    for (b, h), uc in ucs.items():
+        assert max_err(out[b, h * G:(h + 1) * G], uc.decode_dense(q_group(q, b, h, G))) <= TOL
+        _cert_compare(cache, uc, b, h)
+        _bound_close(bnd[b, h * G:(h + 1) * G], uc.certificate(q_group(q, b, h, G)))
+
+
+def test_per_token_values_demotion_and_residual(gpu):
+    """Demotion re-encodes per-token value records (8 -> 4 -> 2 -> centroid), and the
+    residual scores values against their per-token reconstruction."""
+    T, Hq, Hkv = 64 * 12, 8, 2
+    ks, vs = kv_all(11, 1, Hkv, T)
+    lv = olad.ladder("exact", T)
+    n = ores.n_keep(T, 5)
+    cache = _build(gpu, ks, vs, Hq, lv, nres_cap=n, slack={8: 16, 4: 16, 2: 16, 1: 16}, v_per_token=True)
+    ucs = _units_per_token(ks, vs, lv)
+    for to in (8, 4, 2, 1):
+        jobs = [(0, h, blk) for h in range(Hkv) for blk in (0, 2, 5)]
+        cache.demote(jobs, [to] * len(jobs))
+        for (b, h), uc in ucs.items():
+            for blk in (0, 2, 5):
+                uc.k_recs[blk] = oquant.demote(uc.k_recs[blk], to)
+                uc.v_recs[blk] = oquant.demote(uc.v_recs[blk], to)
+                uc.levels[blk] = to
+                compare_record(cache, uc, b, h, blk, 0)
+                compare_record(cache, uc, b, h, blk, 1)
+        if to == 4:  # residual selection over a mix of exact and per-token int4 blocks
+            mass = np.stack([synth.mass_unit(11, 0, h, T) for h in range(Hkv)])[None]
+            cache.rd_residual_select(ks, vs, mass, n)
+            idx = cache.res_idx.cpu().numpy()
+            for (b, h), uc in ucs.items():
+                import copy
+                want, _ = copy.deepcopy(uc).select_residual(ks[b, h], vs[b, h], mass[b, h], n)
+                np.testing.assert_array_equal(idx[b, h, :n], want)
+    q = synth.queries(11, 1, Hq)
+    mass = np.stack([synth.mass_unit(11, 0, h, T) for h in range(Hkv)])[None]
+    out = cache.decode(q).cpu().numpy()
+    for (b, h), uc in ucs.items():
+        # the residual chosen at int4 time, read over the demoted blocks
+        sel = cache.res_idx.cpu().numpy()[b, h, :n]
+        uc.res_idx = sel.astype(np.int32)
+        uc.res_k = ks[b, h][sel]
+        uc.res_v = vs[b, h][sel]
+        assert max_err(out[b, 4 * h:4 * h + 4], uc.decode_dense(q_group(q, b, h, 4))) <= TOL
+
+
+def test_per_token_values_quest_pages(gpu):
+    T, Hq, Hkv, page, topk = 6000, 8, 2, 16, 40
+    ks, vs = kv_all(12, 1, Hkv, T)
+    lv = olad.ladder("graded", T)
+    cache = _build(gpu, ks, vs, Hq, lv, page=page, v_per_token=True)
+    q = synth.queries(12, 1, Hq)
+    pages = cache.quest_select(q, topk)
+    out = cache.decode(q, pages=pages).cpu().numpy()
+    pages = pages.cpu().numpy()
+    for (b, h), uc in _units_per_token(ks, vs, lv).items():
+        assert max_err(out[b, 4 * h:4 * h + 4], uc.decode_quest(q_group(q, b, h, 4), pages[b, h])) <= TOL

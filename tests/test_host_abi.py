@@ -213,10 +213,14 @@ def _pack(level, tensor, rec):
         return a.tobytes()
     if level in (8, 4, 2):
         bits = level
+        per_token = getattr(rec, "per_token", False)
         pos4 = [4, 20, 12, 28, 0, 16, 8, 24]
         pos2 = [8, 24, 14, 30, 6, 22, 12, 28, 4, 20, 10, 26, 0, 16, 2, 18]
         sz = np.zeros(256, dtype=np.uint16)
-        for e in range(128):
+        if per_token:  # scale[64], zero[64] in token order, then 256 zero bytes
+            sz[:64] = rec.s16
+            sz[64:128] = rec.z16
+        for e in range(128 if not per_token else 0):
             kg, n = e >> 5, e & 31
             ch = 32 * (n >> 3) + 8 * kg + (n & 7) if tensor == 0 else 16 * (n >> 2) + 4 * kg + (n & 3)
             sz[e] = rec.s16[ch]
@@ -268,3 +272,17 @@ def test_decode_record_reads_documented_layout(B, level, tensor):
     if level in (1, 0):
         np.testing.assert_array_equal(d["ids"], rec.ids)
         np.testing.assert_array_equal(d["cent16"], rec.cent16)
+
+
+@pytest.mark.parametrize("level", [8, 4, 2])
+def test_decode_per_token_value_record(B, level):
+    """A value record grouped per token (scale and zero per token, token order)."""
+    _, v = synth.kv_unit(310 + level, 0, 0, 64)
+    rec = oquant.encode_fp16(level, v, per_token=True)
+    raw = _pack(level, 1, rec)
+    assert len(raw) == B.block_bytes(level)
+    d = B.decode_record(level, B.VALUES_PER_TOKEN, raw)
+    np.testing.assert_array_equal(d["values"], oquant.decode(rec))
+    np.testing.assert_array_equal(d["codes"], rec.codes)
+    np.testing.assert_array_equal(d["s16"], rec.s16)
+    np.testing.assert_array_equal(d["z16"], rec.z16)
