@@ -226,9 +226,9 @@ def main():
     log(f"[bench] inputs ready in {time.time() - t0:.1f}s; building caches")
     phases = {}
 
-    def build_cache(lv, nres):
+    def build_cache(lv, nres, v_per_token=False):
         cache = gkv.GradedCache(B, Hkv, Hq, T, len(lv), {L: 2 * B * Hkv * int((lv == L).sum()) for L in gkv.LEVELS},
-                                nres_cap=nres, device=dev)
+                                nres_cap=nres, device=dev, v_per_token=v_per_token)
         for b in range(B):
             for h in range(Hkv):
                 for i in range(len(lv)):
@@ -337,7 +337,7 @@ def main():
         phases["stream_read_GBps_torch_sum_1GiB"] = round((1 << 30) / (timed(lambda: big.sum(), 10) * 1e-3) / 1e9, 1)
         del big
 
-    rdv2 = None
+    rdv2 = vtok = None
     if not args.no_rdv2:
         # RD-V2 (section 3.4 low-rate variation): one-centroid base outside the 16-block
         # exact window, 10.2% exact residual rows; same shape, inputs and queries
@@ -362,6 +362,21 @@ def main():
         log(f"[bench] RD-V2: {rdv2['us_per_step_median']} us/step, attention {rdv2['attn_kernel_us_mean']} us, "
             f"{rdv2['read_bpv']} bpv read")
         del c2
+        torch.cuda.empty_cache()
+        # the same graded + 2% residual step with values quantised per token (the
+        # grouping of the method text) instead of per channel
+        c3 = [build_cache(lv, nres, v_per_token=True)[0] for _ in range(2)]
+        r3 = c3[0].account()
+        b3 = r3["read_bits"] / 8.0
+        per3, _ = step_loop(c3, qs, outs, n2, args.warmup)
+        _, attn3, _ = staged_loop(c3, qs, outs, n2, args.warmup)
+        vtok = {"workload": wl.name + ", values quantised per token",
+                "us_per_step_median": round(float(np.median(per3)), 2),
+                "attn_kernel_us_mean": round(float(attn3.mean()), 2),
+                "attn_GBps": round(b3 / (float(attn3.mean()) * 1e-6) / 1e9, 1),
+                "read_bpv": round(r3["read_bpv"], 4), "algorithmic_bytes": int(b3)}
+        log(f"[bench] per-token values: {vtok['us_per_step_median']} us/step, attention {vtok['attn_kernel_us_mean']} us")
+        del c3
         torch.cuda.empty_cache()
 
     quest = quest_b8 = quest_p64 = None
@@ -464,6 +479,7 @@ def main():
         "cpu_baseline": cpu,
         "phases": phases,
         "rd_v2": rdv2,
+        "values_per_token": vtok,
         "quest_128k": quest,
         "quest_128k_b8": quest_b8,
         "quest_128k_page64": quest_p64,
