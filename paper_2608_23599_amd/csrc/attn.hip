@@ -426,7 +426,13 @@ struct Pipe {
     else vm_wait<4 * (kSlots - 1 - H)>();
     return ring + (k % kSlots) * kSlotBytes;
   }
-  __device__ __forceinline__ void release(uint32_t n) { rel += n; }
+  // Releasing slots lets the next pump copy into them: every LDS read issued so far
+  // (the items read their slots with ordinary loads, whose results the compiler may
+  // consume after the copy is issued) must have returned first.
+  __device__ __forceinline__ void release(uint32_t n) {
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    rel += n;
+  }
 };
 
 // ---------------------------------------------------------------- per-wave state
@@ -452,6 +458,13 @@ __device__ __forceinline__ float wave_max16(float x) {
   x = vmax(__uint_as_float(a[0]), __uint_as_float(a[1]));
   const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return vmax(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+__device__ __forceinline__ float wave_sum16(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
 __device__ __forceinline__ half4 as_h4(uint32_t a, uint32_t b) {
@@ -1040,11 +1053,83 @@ __device__ __forceinline__ bool centroid_run(const AttnParams &p, State &st, con
   return true;
 }
 
+// A run of n = 2..8 one-centroid blocks whose records lie back to back in one unit
+// (block g: key row at 512 g, value row at 512 g + 256), with cnt_g = (cnt >> 8 g) &
+// 255 tokens read.  Row m of the logit MFMA's A is block m & 7's key row, so lane
+// (kg, m) gets the logits of blocks 4 (kg & 1) + r; the weights cnt_g * p_g of
+// blocks 4 kg + e (kg < 2) then form the B operand of one 16-deep P.V MFMA per
+// channel group, whose contraction index runs over the blocks.  The slot bytes past
+// the run are stale and never enter an MFMA: those key rows, weights and value
+// operands are selected to zero (with stale key rows in the logit MFMA the results
+// were measured to vary between identical calls).
+template <bool PACK, bool CERT>
+__device__ __forceinline__ void mean_run_item(const AttnParams &p, State &st, const uint8_t *qs, const uint8_t *ip,
+                                              int n, uint64_t cnt, int lane, const float *cb) {
+  const int kg = lane >> 4, m16 = lane & 15;
+  f4 sc = {0, 0, 0, 0};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    U8 a;
+    a.v = (m16 & 7) < n ? lds16(ip + 512 * (m16 & 7) + (8 * kg + 32 * i) * 2) : make_uint4(0, 0, 0, 0);
+    sc = mfma32(a.h, qchunk<PACK>(qs, lane, i), sc);
+  }
+  float c[4];
+  float bm = kNegInf;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int g = 4 * (kg & 1) + r;
+    c[r] = (float)((cnt >> (8 * g)) & 255u);  // 0 for blocks >= n
+    if (c[r] > 0.f) bm = vmax(bm, sc[r]);
+  }
+  rescale_factor(st, wave_max16(bm) * p.sl2);
+  _Float16 wh[4];
+  float lsum = 0.f;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const float w = c[r] > 0.f && kg < 2 ? c[r] * __builtin_amdgcn_exp2f(fmaf(sc[r], p.sl2, -st.m)) : 0.f;
+    wh[r] = (_Float16)w;
+    lsum += (float)wh[r];
+  }
+  const half4 Bw = half4{wh[0], wh[1], wh[2], wh[3]};
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {  // O[16 j + row][head] += sum_g v_g[16 j + row] w_g[head]
+    half4 av;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int g = 4 * kg + e;
+      av[e] = kg < 2 && g < n ? *(const _Float16 *)(ip + 512 * g + 256 + 2 * (16 * j + m16)) : (_Float16)0;
+    }
+    st.O[j] = mfma16(av, Bw, st.O[j]);
+  }
+  st.l += wave_sum16(lsum);
+  if (CERT) {
+    float c1 = 0.f, c2 = 0.f, c3 = 0.f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int g = 4 * kg + r;
+      if (kg < 2 && g < n) {
+        const float pb = (float)wh[r], x = st.es * cb[4 * g];
+        c1 = fmaf(pb, cb[4 * g + 1], c1);
+        c2 = fmaf(pb, __builtin_amdgcn_exp2f(x), c2);
+        c3 = fmaf(pb, __builtin_amdgcn_exp2f(-x), c3);
+      }
+    }
+    st.c1 += wave_sum16(c1);
+    st.c2 += wave_sum16(c2);
+    st.c3 += wave_sum16(c3);
+  }
+}
+
 template <bool PACK, bool CERT>
 __device__ __forceinline__ bool mean_run(const AttnParams &p, State &st, const uint8_t *qs, Pipe &pp,
                                          uint32_t &meta, uint64_t &valid, int lane) {
   do {
-    mean_item<PACK, CERT>(p, st, qs, pp.template pop<0>(), valid, lane, CERT ? pp.cert + pp.blk * 4 : nullptr);
+    const int n = meta_ntiles(meta) + 1;
+    if (n > 1)
+      mean_run_item<PACK, CERT>(p, st, qs, pp.template pop<0>(), n, valid, lane,
+                                CERT ? pp.cert + pp.blk * 4 : nullptr);
+    else
+      mean_item<PACK, CERT>(p, st, qs, pp.template pop<0>(), valid, lane, CERT ? pp.cert + pp.blk * 4 : nullptr);
     pp.release(1);
     if (!pp.template next_item<CERT>(meta, valid)) return false;
   } while (meta_lv(meta) == GKV_MEAN);
@@ -1244,7 +1329,9 @@ constexpr int kPlanThreads = 1024;
 struct VisitDesc {
   uint64_t kp, vp;  // addresses of the K and V records
   uint64_t valid;   // tokens of the block that are read (bit t = token t)
-  int16_t level;    // storage level of both records
+  int16_t level;    // storage level of both records; a run of n one-centroid blocks
+                    // (dense reads) carries n - 1 in bits 8..10 and 8-bit token counts
+                    // per block in `valid`
   uint16_t blk;     // block index (0xFFFF: residual rows or a Compressed-Quest visit)
   uint32_t cost;    // balance cost (bits 0..23) | items (bits 24..26) | units (bits 27..30)
 };
@@ -1254,9 +1341,15 @@ static_assert(sizeof(VisitDesc) == 32, "descriptor size");
 // share of the bandwidth (8 KB each), int tiles by the dequantisation and softmax
 // work rather than by their bytes.
 constexpr uint32_t kCostExactTile = 523, kCostInt8Tile = 426, kCostInt4Tile = 305, kCostInt2Tile = 260,
-                   kCostCentroid = 711, kCostIntBlock = 248, kCostMean = 300;
+                   kCostCentroid = 711, kCostIntBlock = 248, kCostMean = 300, kCostMeanRun = 260,
+                   kCostMeanRunBlock = 45;
+
+// Blocks in a one-centroid run (1 for every other visit) and the visit's level.
+__device__ __forceinline__ int run_blocks(int lv) { return ((lv >> 8) & 7) + 1; }
+__device__ __forceinline__ int run_level(int lv) { return lv & 0xFF; }
 
 __device__ __forceinline__ uint32_t balance_cost(int lv, uint64_t va) {
+  if (run_blocks(lv) > 1) return kCostMeanRun + kCostMeanRunBlock * run_blocks(lv);
   uint32_t tiles = 0;
   for (int t = 0; t < 4; ++t) tiles += ((va >> (16 * t)) & 0xFFFFull) != 0;
   if (!tiles) return 0;
@@ -1325,6 +1418,7 @@ __device__ __forceinline__ uint64_t block_scan(uint64_t x, uint64_t *sh, uint64_
 
 // Items and units of a visit (as visit_items writes them): items | units << 3.
 __device__ __forceinline__ uint32_t visit_counts(int lv, uint64_t valid) {
+  if (run_blocks(lv) > 1) return 1u | (1u << 3);
   uint32_t tiles = 0;
   for (int t = 0; t < 4; ++t)
     if ((valid >> (16 * t)) & 0xFFFFull) tiles |= 1u << t;
@@ -1362,7 +1456,15 @@ __device__ __forceinline__ void visit_items(const VisitDesc &v, ItemDesc *items,
   for (int t = 0; t < 4; ++t)
     if ((v.valid >> (16 * t)) & 0xFFFFull) tiles |= 1u << t;
   if (!tiles) return;
-  const uint32_t lv = (uint32_t)v.level;
+  const uint32_t lv = (uint32_t)run_level(v.level);
+  if (run_blocks(v.level) > 1) {  // one-centroid run: one item, one unit of back-to-back records
+    const uint32_t n = (uint32_t)run_blocks(v.level), bytes = 512 * n;
+    items[0].meta = kMean | (lv << 2) | (1u << 7) | (1u << 8) | ((n - 1) << 13);
+    items[0].pad = v.blk;
+    items[0].valid = v.valid;
+    units[0] = unit_desc(v.kp, bytes < 2048 ? bytes : 2048, v.kp + 2048, bytes > 2048 ? bytes - 2048 : 0);
+    return;
+  }
   auto put = [&](int i, uint32_t kind, bool first, bool last, uint32_t taken, uint32_t n, uint32_t tv) {
     items[i].meta = kind | (lv << 2) | ((uint32_t)first << 7) | ((uint32_t)last << 8) | (taken << 9) | (n << 13) |
                     (tv << 16);
@@ -1375,7 +1477,7 @@ __device__ __forceinline__ void visit_items(const VisitDesc &v, ItemDesc *items,
     return;
   }
   if (lv == GKV_MEAN) {
-    put(0, kMean, true, true, tiles, 1, 0);
+    put(0, kMean, true, true, tiles, 0, 0);
     units[0] = unit_desc(v.kp, kMeanBytes, v.vp, kMeanBytes);
     return;
   }
@@ -1412,8 +1514,47 @@ __device__ __forceinline__ void visit_items(const VisitDesc &v, ItemDesc *items,
   }
 }
 
+// Tokens read from block b of a dense read (residual rows excluded).
+__device__ __forceinline__ uint64_t dense_tokens(const AttnParams &p, int64_t u, int64_t b) {
+  uint64_t va = token_mask(p.T - b * P);
+  if (p.nres) va &= ~p.res_mask[u * p.nblk_cap + b];
+  return va;
+}
+
+// Whether one-centroid block b continues the run of block b - 1: both one-centroid
+// and read, inside one aligned group of 8 blocks, each block's value row right after
+// its key row and block b's key row right after block b - 1's value row.
+__device__ __forceinline__ bool mean_joins(const AttnParams &p, int64_t u, int64_t b) {
+  if ((b & 7) == 0) return false;
+  const int64_t i = u * p.nblk_cap + b;
+  if (p.level[i] != GKV_MEAN || p.level[i - 1] != GKV_MEAN) return false;
+  const int64_t k0 = p.koff[i - 1], k1 = p.koff[i];
+  if (p.voff[i - 1] != k0 + kMeanBytes || k1 != k0 + 2 * kMeanBytes || p.voff[i] != k1 + kMeanBytes) return false;
+  return dense_tokens(p, u, b - 1) != 0 && dense_tokens(p, u, b) != 0;
+}
+
+// One-centroid block v of a dense read, with jn the plan's bitmap of mean_joins: a
+// block that continues a run is read by the run's first block (no items, no cost); a
+// first block takes the run's following blocks and their token counts.
+__device__ __forceinline__ void mean_run_visit(const AttnParams &p, int64_t u, int64_t v, const uint32_t *jn,
+                                               VisitDesc &d) {
+  const uint32_t grp = (jn[v >> 5] >> (v & 24)) & 255u;  // the joins bits of v's aligned group of 8
+  const int o = (int)(v & 7);
+  if ((grp >> o) & 1u) {
+    d.valid = 0;
+    return;
+  }
+  const int n = 1 + __builtin_ctz(~(grp >> (o + 1)) | (1u << (7 - o)));  // following set bits, to the group end
+  if (n == 1) return;
+  uint64_t cnt = 0;
+  for (int g = 0; g < n; ++g) cnt |= (uint64_t)__popcll(dense_tokens(p, u, v + g)) << (8 * g);
+  d.valid = cnt;
+  d.level = (int16_t)(GKV_MEAN | ((n - 1) << 8));
+}
+
 // Visit v of a dense read: block v (v < nblk), else residual pseudo-block v - nblk.
-__device__ __forceinline__ VisitDesc dense_visit(const AttnParams &p, int64_t u, int64_t nblk, int64_t v) {
+__device__ __forceinline__ VisitDesc dense_visit(const AttnParams &p, int64_t u, int64_t nblk, int64_t v,
+                                                 const uint32_t *jn) {
   VisitDesc d;
   if (v < nblk) {
     d.level = p.level[u * p.nblk_cap + v];
@@ -1422,6 +1563,7 @@ __device__ __forceinline__ VisitDesc dense_visit(const AttnParams &p, int64_t u,
     d.vp = (uint64_t)(uintptr_t)(p.arena + p.voff[u * p.nblk_cap + v]);
     d.valid = token_mask(p.T - v * P);
     if (p.nres) d.valid &= ~p.res_mask[u * p.nblk_cap + v];
+    if (jn && d.level == GKV_MEAN && d.valid) mean_run_visit(p, u, v, jn, d);
   } else {
     const int64_t rb = v - nblk;
     const uint8_t *kp = p.res_rows + (u * p.nrb_cap + rb) * (2 * kExactBytes);
@@ -1507,20 +1649,49 @@ __device__ __forceinline__ bool own_slice() {
   return (int)((threadIdx.x * gridDim.y) / kPlanThreads) == (int)blockIdx.y;
 }
 
+// The bitmap of one-centroid runs of a dense plan (bit b: block b continues block
+// b - 1's run), built by every thread for its visits [v0, v1) when any is set (a
+// workgroup-uniform flag); null otherwise.
+__device__ __forceinline__ const uint32_t *build_joins(const AttnParams &p, int64_t u, int64_t nblk, int64_t v0,
+                                                       int64_t v1, bool any, uint32_t *joins) {
+  if (!any) return nullptr;
+  for (int64_t w = threadIdx.x; w < (nblk + 31) / 32; w += kPlanThreads) joins[w] = 0;
+  __syncthreads();
+  for (int64_t b = v0; b < v1 && b < nblk; ++b)
+    if (mean_joins(p, u, b)) atomicOr(&joins[b >> 5], 1u << (b & 31));
+  __syncthreads();
+  return joins;
+}
+
 // Dense plan when every thread holds at most kPlanRegs visits: the visits stay in
 // registers through the scan and the expansion.
 constexpr int kPlanRegs = 4;
 __device__ __forceinline__ void plan_dense_regs(const AttnParams &p, int64_t u, int64_t nblk, int64_t nvis,
-                                                PlanOut o, uint64_t *sh, uint32_t *lastc) {
+                                                PlanOut o, uint64_t *sh, uint32_t *lastc, uint32_t *joins) {
   const int64_t per = (nvis + kPlanThreads - 1) / kPlanThreads;
   const int64_t v0 = threadIdx.x * per, v1 = v0 + per < nvis ? v0 + per : nvis;
   VisitDesc dv[kPlanRegs];
+  bool any_mean = false;
+#pragma unroll
+  for (int j = 0; j < kPlanRegs; ++j)
+    if (v0 + j < v1) {
+      dv[j] = dense_visit(p, u, nblk, v0 + j, nullptr);
+      any_mean |= v0 + j < nblk && dv[j].level == GKV_MEAN;
+    }
+  // one-centroid runs, only when the cache holds one-centroid blocks
+  if (const uint32_t *jn = build_joins(p, u, nblk, v0, v1, __syncthreads_or(any_mean), joins)) {
+#pragma unroll
+    for (int j = 0; j < kPlanRegs; ++j)
+      if (v0 + j < v1 && v0 + j < nblk && dv[j].level == GKV_MEAN && dv[j].valid) {
+        mean_run_visit(p, u, v0 + j, jn, dv[j]);
+        dv[j].cost = balance_cost(dv[j].level, dv[j].valid) | (visit_counts(dv[j].level, dv[j].valid) << 24);
+      }
+  }
   uint64_t mine = 0;
   uint32_t last = 0;
 #pragma unroll
   for (int j = 0; j < kPlanRegs; ++j)
     if (v0 + j < v1) {
-      dv[j] = dense_visit(p, u, nblk, v0 + j);
       mine += scan_key(dv[j].cost);
       last = dv[j].cost;
     }
@@ -1540,6 +1711,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
   __shared__ uint64_t sh[3 * kPlanThreads / 64];  // block_scan: 6 x 16 32-bit words
   __shared__ uint32_t lastc[kPlanThreads];
   __shared__ VisitDesc lds_desc[kPlanLdsVisits];
+  __shared__ uint32_t joins[32768 / 32];  // one-centroid run bits of a dense plan (nblk < 32768)
   __shared__ int s_cnt;
   const int64_t u = blockIdx.x;
   const int W = p.nsplit * kWaves;
@@ -1557,17 +1729,20 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
     const int64_t nvis = nblk + (p.nres + P - 1) / P;
     const int64_t per = (nvis + kPlanThreads - 1) / kPlanThreads;
     if (per <= kPlanRegs) {
-      plan_dense_regs(p, u, nblk, nvis, o, sh, lastc);
+      plan_dense_regs(p, u, nblk, nvis, o, sh, lastc, joins);
       return;
     }
     const int64_t v0 = threadIdx.x * per, v1 = v0 + per < nvis ? v0 + per : nvis;
+    bool any_mean = false;
+    for (int64_t v = v0; v < v1 && v < nblk; ++v) any_mean |= p.level[u * p.nblk_cap + v] == GKV_MEAN;
+    const uint32_t *jn = build_joins(p, u, nblk, v0, v1, __syncthreads_or(any_mean), joins);
     uint64_t mine = 0;
-    for (int64_t v = v0; v < v1; ++v) mine += scan_key(dense_visit(p, u, nblk, v).cost);
+    for (int64_t v = v0; v < v1; ++v) mine += scan_key(dense_visit(p, u, nblk, v, jn).cost);
     uint64_t e = block_scan(mine, sh, o.total) - mine;
     o.scale = owner_scale(o.W, o.W1, key_cost(o.total));
     if (v0 >= v1 || !own_slice()) return;
-    int prev = prev_owner(o, v0, e, v0 > 0 ? dense_visit(p, u, nblk, v0 - 1).cost : 0u);
-    for (int64_t v = v0; v < v1; ++v) place_visit(o, dense_visit(p, u, nblk, v), v, nvis, e, prev);
+    int prev = prev_owner(o, v0, e, v0 > 0 ? dense_visit(p, u, nblk, v0 - 1, jn).cost : 0u);
+    for (int64_t v = v0; v < v1; ++v) place_visit(o, dense_visit(p, u, nblk, v, jn), v, nvis, e, prev);
     return;
   }
   if (blockIdx.y) return;  // one workgroup per (b, KV head)

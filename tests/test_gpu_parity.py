@@ -741,3 +741,21 @@ def test_per_token_values_quest_pages(gpu):
     pages = pages.cpu().numpy()
     for (b, h), uc in _units_per_token(ks, vs, lv).items():
         assert max_err(out[b, 4 * h:4 * h + 4], uc.decode_quest(q_group(q, b, h, 4), pages[b, h])) <= TOL
+
+
+def test_rdv2_long_context_runs(gpu):
+    """RD-V2 beyond 4096 visits per (b, KV head) (T = 300,001: the plan's looped path),
+    with a residual: one-centroid runs, their edges at residual-free and ragged
+    places, against the oracle."""
+    T, Hq, Hkv = 300001, 4, 1
+    ks, vs = kv_all(13, 1, Hkv, T)
+    lv = olad.ladder("rdv2", T)
+    n = ores.n_keep(T, 1, 100)
+    cache = _build(gpu, ks, vs, Hq, lv, nres_cap=n)
+    mass = synth.mass_unit(13, 0, 0, T)[None, None]
+    cache.rd_residual_select(ks, vs, mass, n)
+    q = synth.queries(13, 1, Hq)
+    out = cache.decode(q).cpu().numpy()
+    uc = ocache.UnitCache(ks[0, 0], vs[0, 0], lv)
+    uc.select_residual(ks[0, 0], vs[0, 0], mass[0, 0], n)
+    assert max_err(out[0], uc.decode_dense(q_group(q, 0, 0, Hq))) <= TOL
