@@ -221,20 +221,31 @@ __global__ void __launch_bounds__(kObsThreads) obs_logit_kernel(const uint16_t *
   }
 }
 
+// One wavefront per row: the row's log-sum-exp over the chunks' (max, sum) pairs.
 __global__ void __launch_bounds__(256) obs_row_kernel(const float2 *__restrict__ part, int R, int Rpad, int nslice,
                                                       int Hkv, float *__restrict__ row_lse) {
-  const int h = blockIdx.x, b = blockIdx.y;
+  const int lane = threadIdx.x & 63, r = blockIdx.x * 4 + (threadIdx.x >> 6), h = blockIdx.y, b = blockIdx.z;
+  if (r >= R) return;
   const int64_t u = (int64_t)b * Hkv + h;
-  for (int r = threadIdx.x; r < R; r += 256) {
-    float m = kNegInf;
-    for (int sl = 0; sl < nslice; ++sl) m = fmaxf(m, part[(u * nslice + sl) * Rpad + r].x);
-    float s = 0.f;  // every row sees key 0, so m is finite
-    for (int sl = 0; sl < nslice; ++sl) {
-      const float2 p = part[(u * nslice + sl) * Rpad + r];
-      if (p.x != kNegInf) s += p.y * __builtin_amdgcn_exp2f(p.x - m);
+  float m = kNegInf, s = 0.f;
+  for (int sl = lane; sl < nslice; sl += 64) {
+    const float2 p = part[(u * nslice + sl) * Rpad + r];
+    if (p.x == kNegInf) continue;
+    if (p.x > m) {
+      s = s * __builtin_amdgcn_exp2f(m - p.x) + p.y;
+      m = p.x;
+    } else {
+      s += p.y * __builtin_amdgcn_exp2f(p.x - m);
     }
-    row_lse[u * Rpad + r] = m + __builtin_amdgcn_logf(s);  // every row sees key 0
   }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const float m2 = __shfl_xor(m, o), s2 = __shfl_xor(s, o);
+    const float mm = fmaxf(m, m2);
+    s = (m == kNegInf ? 0.f : s * __builtin_amdgcn_exp2f(m - mm)) + (m2 == kNegInf ? 0.f : s2 * __builtin_amdgcn_exp2f(m2 - mm));
+    m = mm;
+  }
+  if (lane == 0) row_lse[u * Rpad + r] = m + __builtin_amdgcn_logf(s);  // every row sees key 0
 }
 
 // One wavefront per block: mean over rows of the block's share of each row.
@@ -381,7 +392,8 @@ extern "C" gkv_status gkv_observe_mass(const uint16_t *q_obs, int32_t n_obs, con
   const float sl2 = 1.4426950408889634f / sqrtf((float)D);
   hipLaunchKernelGGL(obs_logit_kernel, dim3(L.nslice, Hkv, B), dim3(kObsThreads), L.Rpad * (256 + 8 * 8), s, q_obs,
                      k_src, n_obs, G, Hkv, T, L.nblk, L.Rpad, sl2, lse, part);
-  hipLaunchKernelGGL(obs_row_kernel, dim3(Hkv, B), dim3(256), 0, s, part, L.R, L.Rpad, L.nslice, Hkv, rows);
+  hipLaunchKernelGGL(obs_row_kernel, dim3((L.R + 3) / 4, Hkv, B), dim3(256), 0, s, part, L.R, L.Rpad, L.nslice, Hkv,
+                     rows);
   hipLaunchKernelGGL(obs_mass_kernel, dim3((L.nblk + 3) / 4, Hkv, B), dim3(256), 0, s, lse, rows, L.R, L.Rpad,
                      L.nblk, Hkv, alpha, mass);
   return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP;
