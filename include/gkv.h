@@ -42,7 +42,8 @@ typedef enum gkv_status {
   GKV_E_NOT_MONOTONE = -3, /* a demotion that is not strictly downwards        */
   GKV_E_WORKSPACE = -4,    /* workspace smaller than gkv_workspace_bytes()     */
   GKV_E_HIP = -5,          /* the HIP runtime reported an error                */
-  GKV_E_UNSUPPORTED = -6   /* valid but not implemented combination            */
+  GKV_E_UNSUPPORTED = -6,  /* valid but not implemented combination            */
+  GKV_E_POOL = -7          /* a slab pool has no free slot of a needed level    */
 } gkv_status;
 
 /* Ladder levels; the numeric value is the bits of a code (1 = centroid state with
@@ -238,8 +239,8 @@ gkv_status gkv_page_boxes(const gkv_cache *c, const uint16_t *k_src, int64_t T_s
 /* Append one token per (b,h) (decode step): k_new, v_new [B][Hkv][128] fp16 are
  * written into the newest block, which must be exact.  When T is a multiple of 64
  * a new exact block is opened for every (b,h) u at byte offsets new_koff_host[u] /
- * new_voff_host[u] (arrays of B*Hkv <= 128 entries; ignored otherwise, may be NULL).
- * When the token completes a page and boxes are kept, that page's box is written
+ * new_voff_host[u] (arrays of B*Hkv <= 128 entries; ignored otherwise, may be NULL);
+ * its other 63 rows are written as zero.  When the token completes a page and boxes are kept, that page's box is written
  * from the exact keys.  c->T is incremented. */
 #define GKV_MAX_APPEND_UNITS 128
 gkv_status gkv_append(gkv_cache *c, const uint16_t *k_new, const uint16_t *v_new, const int64_t *new_koff_host,
@@ -300,6 +301,25 @@ gkv_status gkv_attn_merge(const gkv_cache *c, const int32_t *pages, int32_t topk
 gkv_status gkv_rd_residual_select(gkv_cache *c, const uint16_t *k_src, const uint16_t *v_src,
                                   const float *mass, int32_t nkeep, void *ws, int64_t ws_bytes,
                                   void *stream);
+
+/* ---------------------------------------------------------------- multi-layer service */
+
+/* One decode step of cache maintenance for L layers (section 3.2: incremental append
+ * and monotone demotion; the block-paged serving manager of the paper's plug-in, run
+ * natively): for every layer l, append the token k_new[l], v_new[l] (device
+ * [L][B][Hkv][128] fp16) as gkv_append does, then demote every block whose level
+ * the ladder profile lowers at T + 1, as gkv_demote does.  New exact blocks and the
+ * demotion targets take slots from pools[l]; the demoted blocks' old slots are freed
+ * to pools[l] (reusable by later work on the same stream).  koff_host[l] and
+ * voff_host[l] are host mirrors [B][Hkv][nblk_cap] of layer l's offset tables, kept
+ * in sync here.  The layers must share B, Hkv, T, nblk_cap and their levels (as
+ * layers built and stepped together do): the crossings are computed once, from
+ * layer 0.  Every slot is taken before anything is enqueued: GKV_E_POOL (or any
+ * argument error) leaves every cache, pool and mirror unchanged.  Returns the number
+ * of blocks demoted per layer (>= 0) or a negative gkv_status. */
+int32_t gkv_layers_step(gkv_cache *const *caches, gkv_pool *const *pools, int64_t *const *koff_host,
+                        int64_t *const *voff_host, int32_t L, int32_t profile, const uint16_t *k_new,
+                        const uint16_t *v_new, void *stream);
 
 /* ---------------------------------------------------------------- observer and allocation */
 

@@ -79,6 +79,7 @@ _attn_plan = _sig("gkv_attn_plan", _i32, [_P(CacheStruct), _vp, _i32, _vp, _i64,
 _attn_partials = _sig("gkv_attn_partials", _i32, [_vp, _P(CacheStruct), _vp, _i32, _vp, _i64, _vp])
 _attn_merge = _sig("gkv_attn_merge", _i32, [_P(CacheStruct), _vp, _i32, _vp, _vp, _i64, _vp])
 _rd = _sig("gkv_rd_residual_select", _i32, [_P(CacheStruct), _vp, _vp, _vp, _i32, _vp, _i64, _vp])
+_layers_step = _sig("gkv_layers_step", _i32, [_vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _vp])
 _observe_ws = _sig("gkv_observe_ws_bytes", _i64, [_i32, _i32, _i32, _i64, _i32])
 _observe = _sig("gkv_observe_mass", _i32,
                 [_vp, _i32, _vp, _i32, _i32, _i32, _i64, ctypes.c_float, _vp, _vp, _i64, _vp])
@@ -92,7 +93,7 @@ EXPORTED = [
     "gkv_decode_record", "gkv_f64_to_f16", "gkv_workspace_bytes", "gkv_quantize_block", "gkv_demote",
     "gkv_page_boxes", "gkv_append", "gkv_quest_select", "gkv_graded_decode_attn", "gkv_rd_residual_select",
     "gkv_attn_plan", "gkv_attn_partials", "gkv_attn_merge", "gkv_graded_decode_attn_bound",
-    "gkv_observe_ws_bytes", "gkv_observe_mass", "gkv_query_norms", "gkv_allocate_levels",
+    "gkv_observe_ws_bytes", "gkv_observe_mass", "gkv_query_norms", "gkv_allocate_levels", "gkv_layers_step",
 ]
 
 
@@ -410,8 +411,10 @@ class GradedCache:
         to = np.ascontiguousarray(np.array(to_levels, dtype=np.int8))
         old = [(int(self.level_host[b, h, i]), int(self.koff_host[b, h, i]), int(self.voff_host[b, h, i]))
                for b, h, i in J]
-        nk = np.array([self.pool.alloc(int(t)) for t in to], dtype=np.int64)
-        nv = np.array([self.pool.alloc(int(t)) for t in to], dtype=np.int64)
+        # K and V slots of one block side by side, so that demoted one-centroid blocks
+        # keep forming runs of back-to-back records
+        kv = np.array([self.pool.alloc(int(t)) for t in np.repeat(to, 2)], dtype=np.int64)
+        nk, nv = kv[0::2].copy(), kv[1::2].copy()
         st = _demote(ctypes.byref(self.c), n, _np_ptr(J), _np_ptr(to), _np_ptr(nk), _np_ptr(nv), _stream())
         if st != 0:
             for t, a, bb in zip(to, nk, nv):
@@ -434,8 +437,9 @@ class GradedCache:
         nk = nv = None
         if T % P == 0:
             blk = T // P
-            nk = np.array([self.pool.alloc(EXACT) for _ in range(self.units)], dtype=np.int64)
-            nv = np.array([self.pool.alloc(EXACT) for _ in range(self.units)], dtype=np.int64)
+            # K and V slots of one block side by side (the order gkv_layers_step takes them)
+            kv = np.array([self.pool.alloc(EXACT) for _ in range(2 * self.units)], dtype=np.int64)
+            nk, nv = kv[0::2].copy(), kv[1::2].copy()
             self.koff_host[:, :, blk] = nk.reshape(self.B, self.Hkv)
             self.voff_host[:, :, blk] = nv.reshape(self.B, self.Hkv)
         _check(_append(ctypes.byref(self.c), _dptr(kd), _dptr(vd), _np_ptr(nk) if nk is not None else None,
@@ -552,3 +556,29 @@ class GradedCache:
         kmin = g[..., 0].transpose(0, 2, 1).reshape(-1, D)[:npages]
         kmax = g[..., 1].transpose(0, 2, 1).reshape(-1, D)[:npages]
         return kmin, kmax
+
+
+class LayerCaches:
+    """The graded caches of L layers stepped together (gkv_layers_step): one call per
+    decode step appends every layer's token and demotes what the ladder lowers."""
+
+    def __init__(self, caches, profile):
+        self.caches = list(caches)
+        self.profile = PROFILES.get(profile, profile)
+        L = len(self.caches)
+        ptr = lambda xs: (ctypes.c_void_p * L)(*xs)
+        self._c = ptr([ctypes.addressof(c.c) for c in self.caches])
+        self._p = ptr([c.pool.h for c in self.caches])
+        self._ko = ptr([c.koff_host.ctypes.data for c in self.caches])
+        self._vo = ptr([c.voff_host.ctypes.data for c in self.caches])
+
+    def step(self, k_new, v_new):
+        """k_new, v_new: [L][B][Hkv][128] fp16 bits (device tensors or numpy).
+        Returns the number of blocks demoted per layer."""
+        k_new = _fp16_dev(k_new, self.caches[0].device)
+        v_new = _fp16_dev(v_new, self.caches[0].device)
+        n = int(_layers_step(self._c, self._p, self._ko, self._vo, len(self.caches), self.profile, _dptr(k_new),
+                             _dptr(v_new), _stream()))
+        if n < 0:
+            raise GkvError(n, "layers_step")
+        return n

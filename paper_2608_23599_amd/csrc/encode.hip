@@ -437,6 +437,14 @@ __global__ void __launch_bounds__(128) append_kernel(const uint16_t *__restrict_
     ko = koff[ti];
     vo = voff[ti];
   }
+  if (open_block) {  // a new block's other rows are defined (zero): reads mask them, but 0 * NaN is NaN
+    uint4 *kz = (uint4 *)(arena + ko), *vz = (uint4 *)(arena + vo);
+    for (int i = d; i < kExactBytes / 16; i += D) {
+      kz[i] = make_uint4(0, 0, 0, 0);
+      vz[i] = make_uint4(0, 0, 0, 0);
+    }
+    __syncthreads();
+  }
   const uint16_t kv = k_new[u * D + d], vv = v_new[u * D + d];
   if (cert) {  // an exact block: no error; the value norms grow by this row
     const double x = (double)__builtin_bit_cast(_Float16, vv);

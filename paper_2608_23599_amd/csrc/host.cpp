@@ -18,6 +18,7 @@ extern "C" const char *gkv_strerror(gkv_status s) {
     case GKV_E_WORKSPACE: return "workspace too small";
     case GKV_E_HIP: return "HIP runtime error";
     case GKV_E_UNSUPPORTED: return "unsupported combination";
+    case GKV_E_POOL: return "a slab pool has no free slot";
   }
   return "unknown status";
 }

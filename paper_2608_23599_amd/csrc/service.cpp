@@ -1,0 +1,115 @@
+// Multi-layer decode-step maintenance: the paged append service around the cache
+// calls (section 3.2 incremental append and monotone demotion, run for every layer
+// of a model by one host call, as a serving block manager does).
+//
+// The layers share B, Hkv, T and the ladder profile, so they hold the same levels and
+// cross the ladder at the same blocks: the crossings are computed once.  Every slot
+// the step needs (new exact blocks, demotion targets) is taken from the layers' pools
+// before anything is enqueued, so a full pool fails the call without side effects.
+#include <string.h>
+
+#include <vector>
+
+#include "gkv_internal.h"
+
+using namespace gkv;
+
+namespace {
+
+struct Taken {  // slots taken for one layer, released again on failure
+  gkv_pool *pool;
+  std::vector<std::pair<int32_t, int64_t>> slots;
+  bool take(int32_t level, int64_t &off) {
+    off = gkv_pool_alloc(pool, level);
+    if (off < 0) return false;
+    slots.emplace_back(level, off);
+    return true;
+  }
+  void give_back() {
+    for (auto &s : slots) gkv_pool_free(pool, s.first, s.second);
+    slots.clear();
+  }
+};
+
+}  // namespace
+
+extern "C" int32_t gkv_layers_step(gkv_cache *const *caches, gkv_pool *const *pools, int64_t *const *koff_host,
+                                   int64_t *const *voff_host, int32_t L, int32_t profile, const uint16_t *k_new,
+                                   const uint16_t *v_new, void *stream) {
+  if (!caches || !pools || !koff_host || !voff_host || L < 1 || !k_new || !v_new) return GKV_E_ARG;
+  for (int l = 0; l < L; ++l) {
+    if (!caches[l] || !pools[l] || !koff_host[l] || !voff_host[l]) return GKV_E_ARG;
+    const gkv_status st = gkv_validate_cache(caches[l]);
+    if (st) return st;
+    const gkv_cache *c0 = caches[0], *c = caches[l];
+    if (c->B != c0->B || c->Hkv != c0->Hkv || c->T != c0->T || c->nblk_cap != c0->nblk_cap) return GKV_E_SHAPE;
+  }
+  const gkv_cache *c0 = caches[0];
+  const int64_t T = c0->T, units = (int64_t)c0->B * c0->Hkv, cap = c0->nblk_cap;
+  const bool open = T % P == 0;
+  if (T / P >= cap) return GKV_E_SHAPE;
+  // the crossings of T + 1 (the block the token opens never crosses)
+  int32_t none_j[3];
+  int8_t none_t[1];
+  int32_t n = gkv_ladder_crossings(c0, profile, T + 1, none_j, none_t, 0);  // the count only
+  if (n < 0) return n;
+  std::vector<int32_t> jobs(3 * (size_t)n + 3);
+  std::vector<int8_t> to((size_t)n + 1);
+  if (n) {
+    const int32_t m = gkv_ladder_crossings(c0, profile, T + 1, jobs.data(), to.data(), n);
+    if (m != n) return m < 0 ? m : GKV_E_ARG;
+  }
+  // every slot of the step, before anything is enqueued
+  std::vector<Taken> taken(L);
+  std::vector<std::vector<int64_t>> nk(L), nv(L), dk(L), dv(L);
+  for (int l = 0; l < L; ++l) {
+    taken[l].pool = pools[l];
+    bool ok = true;
+    if (open) {
+      nk[l].resize(units);
+      nv[l].resize(units);
+      for (int64_t u = 0; u < units && ok; ++u)
+        ok = taken[l].take(GKV_EXACT, nk[l][u]) && taken[l].take(GKV_EXACT, nv[l][u]);
+    }
+    dk[l].resize(n);
+    dv[l].resize(n);
+    for (int32_t i = 0; i < n && ok; ++i) ok = taken[l].take(to[i], dk[l][i]) && taken[l].take(to[i], dv[l][i]);
+    if (!ok) {
+      for (int j = 0; j <= l; ++j) taken[j].give_back();
+      return GKV_E_POOL;
+    }
+  }
+  for (int l = 0; l < L; ++l) {
+    gkv_cache *c = caches[l];
+    const size_t row = (size_t)units * D;
+    gkv_status st = gkv_append(c, k_new + l * row, v_new + l * row, open ? nk[l].data() : nullptr,
+                               open ? nv[l].data() : nullptr, stream);
+    if (st) return st;
+    if (open)
+      for (int64_t u = 0; u < units; ++u) {
+        koff_host[l][u * cap + T / P] = nk[l][u];
+        voff_host[l][u * cap + T / P] = nv[l][u];
+      }
+    if (!n) continue;
+    // the current slots of the crossing blocks are free once the stream has passed
+    // the demotion (later work on this stream that reuses them is ordered after it)
+    std::vector<int8_t> from(n);
+    std::vector<int64_t> ok_(n), ov_(n);
+    for (int32_t i = 0; i < n; ++i) {
+      const int64_t idx = ((int64_t)jobs[3 * i] * c->Hkv + jobs[3 * i + 1]) * cap + jobs[3 * i + 2];
+      from[i] = c->level_host[idx];
+      ok_[i] = koff_host[l][idx];
+      ov_[i] = voff_host[l][idx];
+    }
+    st = gkv_demote(c, n, jobs.data(), to.data(), dk[l].data(), dv[l].data(), stream);
+    if (st) return st;
+    for (int32_t i = 0; i < n; ++i) {
+      const int64_t idx = ((int64_t)jobs[3 * i] * c->Hkv + jobs[3 * i + 1]) * cap + jobs[3 * i + 2];
+      koff_host[l][idx] = dk[l][i];
+      voff_host[l][idx] = dv[l][i];
+      gkv_pool_free(pools[l], from[i], ok_[i]);
+      gkv_pool_free(pools[l], from[i], ov_[i]);
+    }
+  }
+  return n;
+}

@@ -759,3 +759,75 @@ def test_rdv2_long_context_runs(gpu):
     uc = ocache.UnitCache(ks[0, 0], vs[0, 0], lv)
     uc.select_residual(ks[0, 0], vs[0, 0], mass[0, 0], n)
     assert max_err(out[0], uc.decode_dense(q_group(q, 0, 0, Hq))) <= TOL
+
+
+# ---------------------------------------------------------------- multi-layer service
+
+
+def test_layers_step_matches_per_layer_appends(gpu):
+    """gkv_layers_step on 3 layers (one call per decode step: appends, one crossings
+    computation, demotions, slot recycling) against the same layers stepped one by
+    one with gkv_append / gkv_demote: identical levels, offsets, records, pool use
+    and decode outputs at every step, and each layer against the oracle at the end."""
+    torch = _torch()
+    L, Hq, Hkv, page = 3, 8, 2, 16
+    T0 = 64 * 40 - 3
+    steps = 70
+    data = [kv_all(70 + l, 1, Hkv, T0 + steps) for l in range(L)]
+    lv = olad.ladder("graded", T0)
+    slack = {16: 8, 8: 8, 4: 8, 2: 8, 1: 8}
+    mk = lambda ks, vs: _build(gpu, ks[:, :, :T0], vs[:, :, :T0], Hq, lv, page=page, extra_blocks=4, slack=slack)
+    svc = gpu.LayerCaches([mk(*d) for d in data], "graded")
+    ref = [mk(*d) for d in data]
+    G = Hq // Hkv
+    total = 0
+    for s in range(steps):
+        t = T0 + s
+        kn = np.stack([d[0][:, :, t] for d in data])
+        vn = np.stack([d[1][:, :, t] for d in data])
+        n = svc.step(kn, vn)
+        moves = [r.append(kn[l], vn[l], profile="graded") for l, r in enumerate(ref)]
+        assert all(len(m) == n for m in moves)
+        total += n
+        q = synth.queries(71, 1, Hq, step=s)
+        for l in range(L):
+            a, b = svc.caches[l], ref[l]
+            assert a.T == b.T == t + 1
+            np.testing.assert_array_equal(a.level_host, b.level_host)
+            np.testing.assert_array_equal(a.koff_host, b.koff_host)
+            np.testing.assert_array_equal(a.voff_host, b.voff_host)
+            assert all(a.pool.used(x) == b.pool.used(x) for x in gpu.LEVELS)
+            assert torch.equal(a.decode(q), b.decode(q))
+    assert total > 0
+    for l, (ks, vs) in enumerate(data):
+        T = T0 + steps
+        uc = ocache.UnitCache(ks[0, 0, :T0], vs[0, 0, :T0], lv)
+        for t in range(T0, T):
+            uc.append(ks[0, 0, t], vs[0, 0, t], "graded")
+        for blk in range(T // 64):  # complete blocks (rows past T of the newest are not defined)
+            compare_record(svc.caches[l], uc, 0, 0, blk, 0)
+            compare_record(svc.caches[l], uc, 0, 0, blk, 1)
+        q = synth.queries(71, 1, Hq, step=steps)
+        out = svc.caches[l].decode(q).cpu().numpy()
+        assert max_err(out[0, 0:G], uc.decode_dense(q_group(q, 0, 0, G))) <= TOL
+
+
+def test_opened_block_rows_are_defined(gpu):
+    """A block opened by an append gets zero rows past the token: free slots filled
+    with NaN bit patterns (as recycled records can hold) must not reach the output
+    (masked rows meet P = 0 in the P.V product, and 0 * NaN is NaN)."""
+    T0, Hq, Hkv = 64 * 8, 4, 1
+    ks, vs = kv_all(14, 1, Hkv, T0 + 3)
+    lv = olad.ladder("tiny", T0)
+    cache = _build(gpu, ks[:, :, :T0], vs[:, :, :T0], Hq, lv, extra_blocks=2, slack={16: 4, 8: 4, 4: 4, 2: 4})
+    off = cache.pool.alloc(16)
+    cache.pool.free(16, off)
+    cache.arena[off:off + 4 * 16384] = 0xFF  # every free exact slot: fp16 NaN patterns
+    uc = ocache.UnitCache(ks[0, 0, :T0], vs[0, 0, :T0], lv)
+    for t in range(T0, T0 + 3):
+        cache.append(ks[:, :, t], vs[:, :, t], profile="tiny")
+        uc.append(ks[0, 0, t], vs[0, 0, t], "tiny")
+        q = synth.queries(14, 1, Hq, step=t)
+        out = cache.decode(q).cpu().numpy()
+        assert np.all(np.isfinite(out))
+        assert max_err(out[0], uc.decode_dense(q_group(q, 0, 0, Hq))) <= TOL

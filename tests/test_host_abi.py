@@ -286,3 +286,32 @@ def test_decode_per_token_value_record(B, level):
     np.testing.assert_array_equal(d["codes"], rec.codes)
     np.testing.assert_array_equal(d["s16"], rec.s16)
     np.testing.assert_array_equal(d["z16"], rec.z16)
+
+
+def test_layers_step_full_pool_changes_nothing(B):
+    """gkv_layers_step takes every slot before enqueueing: with a pool that cannot
+    hold the step's new exact blocks, it fails with GKV_E_POOL and leaves the caches,
+    pools and offset mirrors as they were (host-only: nothing reaches the GPU)."""
+    import ctypes
+    T = 64 * 30  # the next token opens block 30 of every (b, h)
+    lv = olad.ladder("graded", T)
+    caches, keeps, pools, kos, vos = [], [], [], [], []
+    for layer in range(2):
+        c, keep = _host_cache(B, 1, 2, 8, T, lv)
+        caches.append(c)
+        keeps.append(keep)
+        pools.append(B.Pool({16: 1 if layer else 8, 8: 8, 4: 8, 2: 8, 1: 8}))  # layer 1: one exact slot
+        kos.append(np.arange(2 * 34, dtype=np.int64).reshape(1, 2, 34))
+        vos.append(kos[-1] + 1000)
+    before = [(k.copy(), v.copy(), kp["lv"].copy()) for k, v, kp in zip(kos, vos, keeps)]
+    used = [[p.used(L) for L in B.LEVELS] for p in pools]
+    arr = lambda xs: (ctypes.c_void_p * 2)(*xs)
+    kn = np.zeros((2, 1, 2, 128), dtype=np.uint16)
+    st = B._layers_step(arr([ctypes.addressof(c) for c in caches]), arr([p.h for p in pools]),
+                        arr([k.ctypes.data for k in kos]), arr([v.ctypes.data for v in vos]), 2,
+                        B.PROFILES["graded"], kn.ctypes.data, kn.ctypes.data, None)
+    assert st == -7  # GKV_E_POOL
+    for (k0, v0, l0), k, v, kp, c in zip(before, kos, vos, keeps, caches):
+        assert np.array_equal(k0, k) and np.array_equal(v0, v) and np.array_equal(l0, kp["lv"])
+        assert c.T == T
+    assert used == [[p.used(L) for L in B.LEVELS] for p in pools]
