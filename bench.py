@@ -330,6 +330,40 @@ def main():
         phases["allocate_levels_us"] = round(timed(lambda: gkv.allocate_levels(k, mass_o, qn_o, 1.0, 1e-3, 16), 5)
                                              * 1e3, 1)
         del q_obs, ows, mass_o
+        # the multi-layer step service: 8 layers of this workload, 64 decode steps of
+        # appends + demotions (one new block per (b, KV head) and the demotions it
+        # triggers), one gkv_layers_step call per step against one append call per layer
+        nl, nsteps = 8, 64
+        lvg = gkv.ladder_levels("graded", T)
+        sl = {L: 4 * B * Hkv for L in gkv.LEVELS}
+        tok = [torch.from_numpy(np.stack([synth.append_tokens(wl.id, st, B, Hkv)[0]] * nl).view(np.int16)).to(dev)
+               for st in range(nsteps)]
+        tov = [torch.from_numpy(np.stack([synth.append_tokens(wl.id, st, B, Hkv)[1]] * nl).view(np.int16)).to(dev)
+               for st in range(nsteps)]
+
+        def layer_set():
+            return [gkv.GradedCache.build(k, v, Hq=Hq, levels=lvg, device=dev, extra_blocks=2, slack=sl)
+                    for _ in range(nl)]
+
+        svc = gkv.LayerCaches(layer_set(), "graded")
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for st in range(nsteps):
+            svc.step(tok[st], tov[st])
+        torch.cuda.synchronize()
+        phases["layers_step_8x128k_us"] = round((time.perf_counter() - t0) / nsteps * 1e6, 1)
+        del svc
+        torch.cuda.empty_cache()
+        ref = layer_set()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for st in range(nsteps):
+            for li, c in enumerate(ref):
+                c.append(tok[st][li], tov[st][li], profile="graded")
+        torch.cuda.synchronize()
+        phases["per_layer_appends_8x128k_us"] = round((time.perf_counter() - t0) / nsteps * 1e6, 1)
+        del ref, tok, tov
+        torch.cuda.empty_cache()
         # a second denominator: what a plain library reduction reads per second
         big = torch.zeros(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB
         for _ in range(3):
