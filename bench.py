@@ -203,7 +203,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU only: the decode path runs per (sequence, KV head) on a single "
-              "MI355X and this build has no multi-GPU path (see DESIGN.md, 'How it would shard').",
+              "MI355X; the path shards by (sequence, KV head) or by context range, which is not built here.",
               file=sys.stderr)
         sys.exit(2)
 
