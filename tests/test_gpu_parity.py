@@ -831,3 +831,37 @@ def test_opened_block_rows_are_defined(gpu):
         out = cache.decode(q).cpu().numpy()
         assert np.all(np.isfinite(out))
         assert max_err(out[0], uc.decode_dense(q_group(q, 0, 0, Hq))) <= TOL
+
+
+def test_graph_replays_match_eager(gpu):
+    """A Compressed-Quest step and a dense step captured in one HIP graph: every
+    replay, with eager work and synchronisations between replays, equals the eager
+    result bit for bit (the calls allocate nothing and clear nothing on the device)."""
+    torch = _torch()
+    T, Hq, Hkv, page, topk = 5000, 8, 2, 16, 40
+    ks, vs = kv_all(15, 1, Hkv, T)
+    lv = olad.ladder("graded", T)
+    cache = _build(gpu, ks, vs, Hq, lv, page=page)
+    q = torch.from_numpy(synth.queries(15, 1, Hq).view(np.int16)).cuda()
+    pages = torch.empty((1, Hkv, topk), dtype=torch.int32, device="cuda")
+    out_q = torch.empty((1, Hq, 128), dtype=torch.float32, device="cuda")
+    out_d = torch.empty_like(out_q)
+    cache.quest_select(q, topk, out=pages)
+    cache.decode(q, pages=pages, out=out_q)
+    cache.decode(q, out=out_d)
+    torch.cuda.synchronize()
+    want = (pages.clone(), out_q.clone(), out_d.clone())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        cache.quest_select(q, topk, out=pages)
+        cache.decode(q, pages=pages, out=out_q)
+        cache.decode(q, out=out_d)
+    for rep in range(3):
+        pages.fill_(-7)
+        out_q.zero_()
+        out_d.zero_()
+        cache.decode(q, out=torch.empty_like(out_d))  # eager work on the same workspace between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(pages, want[0]) and torch.equal(out_q, want[1]) and torch.equal(out_d, want[2]), rep
