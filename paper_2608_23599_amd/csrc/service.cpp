@@ -48,6 +48,15 @@ extern "C" int32_t gkv_layers_step(gkv_cache *const *caches, gkv_pool *const *po
   const int64_t T = c0->T, units = (int64_t)c0->B * c0->Hkv, cap = c0->nblk_cap;
   const bool open = T % P == 0;
   if (T / P >= cap) return GKV_E_SHAPE;
+  // what gkv_append would reject, rejected here before any slot is taken
+  if (open && units > GKV_MAX_APPEND_UNITS) return GKV_E_UNSUPPORTED;
+  for (int l = 0; l < L; ++l) {
+    const gkv_cache *c = caches[l];
+    if (c->page && (T + 1) / c->page > c->npage_cap) return GKV_E_SHAPE;
+    if (!open)
+      for (int64_t u = 0; u < units; ++u)
+        if (c->level_host[u * cap + T / P] != GKV_EXACT) return GKV_E_ARG;
+  }
   // the crossings of T + 1 (the block the token opens never crosses)
   int32_t none_j[3];
   int8_t none_t[1];
