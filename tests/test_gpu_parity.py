@@ -618,11 +618,13 @@ def test_rdv2_append_steps_with_quest_pages(gpu):
     assert nmoves == 2 * Hkv  # two blocks leave the exact window per KV head in 70 steps
 
 
-@pytest.mark.parametrize("prof,frac", [("graded", (2, 100)), ("rdv2", (102, 1000))])
-def test_rd128k_full_size_sampled(gpu, prof, frac):
+@pytest.mark.parametrize("prof,frac,vtok", [("graded", (2, 100), False), ("rdv2", (102, 1000), False),
+                                           ("graded", (2, 100), True)])
+def test_rd128k_full_size_sampled(gpu, prof, frac, vtok):
     """The 128k decode step at its full size and launch configuration (B = 8, 28
     query / 4 KV heads, T = 131072): graded ladder with 2% residual rows, and RD-V2
-    with 10.2%.  Units (0, 0) and (7, 3) hold their own seeded data and are checked
+    with 10.2%, and the graded ladder with values quantised per token.  Units (0, 0)
+    and (7, 3) hold their own seeded data and are checked
     against the oracle (sampled records, residual set, attention); the other 30
     units repeat those two, so that the launch covers the whole grid."""
     from paper_2608_23599_amd import workloads
@@ -641,14 +643,14 @@ def test_rd128k_full_size_sampled(gpu, prof, frac):
             mass[b, h] = masses[u]
     lv = olad.ladder(prof, T)
     n = ores.n_keep(T, *frac)
-    cache = _build(gpu, ks, vs, Hq, lv, nres_cap=n)
+    cache = _build(gpu, ks, vs, Hq, lv, nres_cap=n, v_per_token=vtok)
     cache.rd_residual_select(ks, vs, mass, n)
     q = synth.queries(wl.id, B, Hq)
     out = cache.decode(q).cpu().numpy()
     idx = cache.res_idx.cpu().numpy()
     G = Hq // Hkv
     for b, h in samp:
-        uc = ocache.UnitCache(ks[b, h], vs[b, h], lv)
+        uc = ocache.UnitCache(ks[b, h], vs[b, h], lv, v_per_token=vtok)
         for blk in (0, 1, 700, 1500, len(lv) - 17, len(lv) - 1):
             compare_record(cache, uc, b, h, blk, 0)
             compare_record(cache, uc, b, h, blk, 1)
