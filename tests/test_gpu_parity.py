@@ -867,3 +867,39 @@ def test_graph_replays_match_eager(gpu):
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(pages, want[0]) and torch.equal(out_q, want[1]) and torch.equal(out_d, want[2]), rep
+
+
+def test_quest128k_b8_full_size_sampled(gpu):
+    """The Compressed-Quest 128k point at its full launch configuration (B = 8, 32
+    query / 8 KV heads, T = 131072, 16-token pages, top-128): units (0, 0) and (7, 7)
+    hold their own seeded data (the others repeat them) and their boxes, page sets
+    (bit-exact) and sparse attention are checked against the oracle."""
+    from oracle import attention as oattn
+    B, Hq, Hkv, T, page, topk = 8, 32, 8, 131072, 16, 128
+    G = Hq // Hkv
+    samp = [(0, 0), (B - 1, Hkv - 1)]
+    data = {u: synth.kv_unit(3, *u, T) for u in samp}
+    ks = np.empty((B, Hkv, T, 128), np.uint16)
+    vs = np.empty((B, Hkv, T, 128), np.uint16)
+    for b in range(B):
+        for h in range(Hkv):
+            ks[b, h], vs[b, h] = data[samp[(b * Hkv + h) % 2]]
+    lv = olad.ladder("graded", T)
+    cache = _build(gpu, ks, vs, Hq, lv, page=page)
+    q = synth.queries(3, B, Hq)
+    pages = cache.quest_select(q, topk)
+    out = cache.decode(q, pages=pages).cpu().numpy()
+    pages = pages.cpu().numpy()
+    for b, h in samp:
+        kmin, kmax = oquest.page_boxes(ks[b, h])
+        want = oquest.quest_select(q_group(q, b, h, G), kmin, kmax, T, topk)
+        np.testing.assert_array_equal(pages[b, h], want)
+        idx = oquest.read_tokens(want, T)
+        kh = np.empty((len(idx), 128))
+        vh = np.empty((len(idx), 128))
+        for blk in np.unique(idx // 64):
+            rows = slice(blk * 64, (blk + 1) * 64)
+            sel = (idx // 64) == blk
+            kh[sel] = oquant.decode(oquant.encode_fp16(int(lv[blk]), ks[b, h, rows]))[idx[sel] - blk * 64]
+            vh[sel] = oquant.decode(oquant.encode_fp16(int(lv[blk]), vs[b, h, rows]))[idx[sel] - blk * 64]
+        assert max_err(out[b, h * G:(h + 1) * G], oattn.unit_decode(q_group(q, b, h, G), kh, vh)) <= TOL
