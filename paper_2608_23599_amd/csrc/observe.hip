@@ -30,7 +30,7 @@ union H8 {
 };
 
 constexpr int kObsThreads = 512;  // 8 wavefronts
-constexpr int kObsBlocksPerWave = 4;
+constexpr int kObsBlocksPerWave = 16;
 constexpr int kObsChunk = 8 * kObsBlocksPerWave;  // blocks per workgroup
 constexpr int kMaxRows = 512;
 constexpr float kNegInf = -__builtin_huge_valf();
