@@ -266,8 +266,9 @@ def main():
     per, total_ms = step_loop(caches, qs, outs, args.steps, args.warmup)
     med, p90 = float(np.median(per)), float(np.percentile(per, 90))
     mean_us = float(per.mean())
-    gbps = alg_bytes / (mean_us * 1e-6) / 1e9
-    log(f"[bench] median {med:.1f} us, p90 {p90:.1f} us, mean {mean_us:.1f} us, {gbps:.0f} GB/s")
+    # the headline time, rate and fraction of peak all come from the median step
+    gbps = alg_bytes / (med * 1e-6) / 1e9
+    log(f"[bench] median {med:.1f} us, p90 {p90:.1f} us, mean {mean_us:.1f} us, {gbps:.0f} GB/s at the median")
     plan_us, attn_us, merge_us = staged_loop(caches, qs, outs, args.steps, args.warmup)
     attn_mean = float(attn_us.mean())
     attn_gbps = alg_bytes / (attn_mean * 1e-6) / 1e9
@@ -509,6 +510,7 @@ def main():
         "mean_us": round(mean_us, 2),
         "achieved_GBps": round(gbps, 1),
         "pct_hbm_peak": round(100 * gbps / HBM_PEAK_GBPS, 2),
+        "achieved_GBps_at_mean": round(alg_bytes / (mean_us * 1e-6) / 1e9, 1),
         "read_bpv": round(rates["read_bpv"], 4),
         "resident_bpv": round(rates["resident_bpv"], 4),
         "algorithmic_bytes_per_step": int(alg_bytes),

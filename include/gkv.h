@@ -312,11 +312,16 @@ gkv_status gkv_rd_residual_select(gkv_cache *c, const uint16_t *k_src, const uin
  * demotion targets take slots from pools[l]; the demoted blocks' old slots are freed
  * to pools[l] (reusable by later work on the same stream).  koff_host[l] and
  * voff_host[l] are host mirrors [B][Hkv][nblk_cap] of layer l's offset tables, kept
- * in sync here.  The layers must share B, Hkv, T, nblk_cap and their levels (as
- * layers built and stepped together do): the crossings are computed once, from
- * layer 0.  Every slot is taken before anything is enqueued: GKV_E_POOL (or any
- * argument error) leaves every cache, pool and mirror unchanged.  Returns the number
- * of blocks demoted per layer (>= 0) or a negative gkv_status. */
+ * in sync here.  The layers must share B, Hkv, T and nblk_cap; each layer's
+ * crossings are computed from its own levels (layers may hold different levels, as
+ * the section 3.3 allocator lays them out).  Before anything is enqueued, every
+ * layer's crossings are checked (GKV_E_NOT_MONOTONE when the profile would raise a
+ * level of any layer), every slot is taken and checked against its layer's arena:
+ * GKV_E_POOL, GKV_E_ARG (a slot past arena_bytes) or any other argument error leaves
+ * every cache, pool and mirror unchanged.  Should the HIP runtime fail part-way, the
+ * layers before the failing one stay stepped and every slot not yet in use goes back
+ * to its pool.  Returns the number of blocks demoted over all layers (>= 0) or a
+ * negative gkv_status. */
 int32_t gkv_layers_step(gkv_cache *const *caches, gkv_pool *const *pools, int64_t *const *koff_host,
                         int64_t *const *voff_host, int32_t L, int32_t profile, const uint16_t *k_new,
                         const uint16_t *v_new, void *stream);
@@ -349,17 +354,25 @@ gkv_status gkv_query_norms(const uint16_t *q_obs, int32_t n_obs, int32_t B, int3
 
 /* Closed-form level allocation (section 3.3, Eq. allocation solved per block by
  * the analytic bit depth): for every block of every (b, h),
- *   e_b = max over channels of (max - min) of the block's exact keys k_src
- *         [B][Hkv][T][128] fp16,
+ *   e_b = max over channels of (max - min) of the block's rows of src
+ *         [B][Hkv][T][128] fp16: the exact keys (the reading that matches the ||q||
+ *         factor) or the exact values (Fig. 1's value error radius) -- the call
+ *         takes the range of whichever tensor is passed,
  *   x   = c * qn[b][h] * e_b * N_b * mass[b][h][blk] / (2 tau)  (fp64, left to right;
  *         N_b = ceil(T/64); this is c ||q|| e_b / (2 eps_t) with eps_t = tau/(N_b m_b)),
- *   b*  = ceil(log2(x + 1)), and the level is the smallest of {1, 2, 4, 8} that is
- *         >= b* (tested as x <= 2^L - 1), else 16.
+ *   b*  = ceil(log2(x + 1)), mapped to a level by `rounding`:
+ *         GKV_ROUND_UP: the smallest of {1, 2, 4, 8} that is >= b*, else 16 (the
+ *           level whose step meets the tolerance; tested as x <= 2^L - 1);
+ *         GKV_ROUND_NEAREST: the level of {1, 2, 4, 8, 16} nearest to b*, ties to
+ *           the larger ("thresholded to the nearest available discrete level";
+ *           x <= 1, 3, 31, 2047 give 1, 2, 4, 8, larger x 16).
  * The newest `window` blocks and a partial last block are exact.  levels: device
  * [B][Hkv][ceil(T/64)] int8 gkv_level.  c > 0 and tau > 0 (the paper leaves both
- * open). */
-gkv_status gkv_allocate_levels(const uint16_t *k_src, const float *mass, const double *qn, int32_t B,
-                               int32_t Hkv, int64_t T, double c, double tau, int32_t window, int8_t *levels,
+ * open); GKV_E_ARG for another rounding. */
+#define GKV_ROUND_UP 0
+#define GKV_ROUND_NEAREST 1
+gkv_status gkv_allocate_levels(const uint16_t *src, const float *mass, const double *qn, int32_t B, int32_t Hkv,
+                               int64_t T, double c, double tau, int32_t window, int32_t rounding, int8_t *levels,
                                void *stream);
 
 #ifdef __cplusplus

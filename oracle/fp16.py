@@ -4,7 +4,7 @@ The quantizer stores its scale, zero and centroids as fp16 (Method, section 3.2:
 packed scalar quantizers with exact scale overhead).  A value computed in fp64 is
 stored with ONE round-to-nearest-even to fp16; it never passes through fp32 on
 the way (that would round twice).  numpy's float64 -> float16 cast rounds
-directly; ``tests/test_oracle_fp16.py`` pins that with vectors where a detour
+directly; ``tests/test_oracle_fp16_ladder.py`` pins that with vectors where a detour
 through fp32 gives a different answer.
 
 Zero is canonicalised to +0 wherever the oracle stores a value that is compared

@@ -22,10 +22,20 @@ others in the design notes):
   ascending sum of squares, then the square root).
 * N_b: the number of blocks of the prefix, ceil(T / 64).
 * b* = ceil(log2(x + 1)) with x = c * ||q|| * e_b * N_b * m_b / (2 * tau)
-  (eps_t = tau / (N_b m_b) substituted).  The level is the smallest ladder level
-  L in {1, 2, 4, 8} with b* <= L, else 16; b* <= L is evaluated as the exactly
-  equivalent x <= 2^L - 1, with x formed left to right in fp64 from the fp32
-  mass.  m_b = 0 gives b* = 0 and the centroid level (the clamp).
+  (eps_t = tau / (N_b m_b) substituted), x formed left to right in fp64 from
+  the fp32 mass.  b* (an integer) maps to a ladder level in one of two ways:
+  - "up" (the default): the smallest level L in {1, 2, 4, 8} with b* <= L, else
+    16, so that the level's step meets the tolerance eps_t;
+  - "nearest": the level of {1, 2, 4, 8, 16} nearest to b*, ties to the larger
+    level (the literal "nearest available discrete level" of section 3.3; b*
+    = 3, 6 and 12 are the ties).
+  Both are evaluated on x without a logarithm: b* <= n is exactly x <= 2^n - 1,
+  so "up" has thresholds 1, 3, 15, 255 and "nearest" 1, 3, 31, 2047 (b* <= 5
+  gives 4, b* <= 11 gives 8).  m_b = 0 gives b* = 0 and the centroid level
+  (the clamp).
+* e_b is the range of whatever fp16 tensor is passed: the keys (the default,
+  matching the ||q|| factor, which bounds a logit error by ||q|| ||k - k_hat||)
+  or the values (Fig. 1 labels e_b(L) a value error radius).
 * The newest `window` blocks, and a partial last block, stay exact (the recent
   window of section 3.2).
 
@@ -80,8 +90,9 @@ def ema(m_old, m_new, alpha=0.1):
 
 
 def key_range(k_bits):
-    """e_b for every block: max over channels of the key range over the block's
-    tokens (a partial last block over the tokens it has).  Exact in fp64."""
+    """e_b for every block: max over channels of the range over the block's tokens
+    (a partial last block over the tokens it has) of the fp16 tensor given, keys
+    or values.  Exact in fp64."""
     k = fp16.to_f64(np.asarray(k_bits, dtype=np.uint16))
     T = k.shape[0]
     nblk = (T + P - 1) // P
@@ -104,20 +115,24 @@ def query_norm(q_bits):
     return best
 
 
-_THRESH = ((CENTROID, 1.0), (INT2, 3.0), (INT4, 15.0), (INT8, 255.0))
+# x <= 2^n - 1 is b* <= n: "up" takes n = L (the level itself); "nearest" takes the
+# largest b* that is still nearer to L than to the next level (ties go up): 1, 2, 5, 11
+_THRESH = {"up": ((CENTROID, 1.0), (INT2, 3.0), (INT4, 15.0), (INT8, 255.0)),
+           "nearest": ((CENTROID, 1.0), (INT2, 3.0), (INT4, 31.0), (INT8, 2047.0))}
 
 
-def bit_level(x):
-    """Ladder level of one block from x = c ||q|| e N m / (2 tau): the smallest L with
-    ceil(log2(x + 1)) <= L, i.e. x <= 2^L - 1; 16 above 255."""
-    for lv, t in _THRESH:
+def bit_level(x, rounding="up"):
+    """Ladder level of one block from x = c ||q|| e N m / (2 tau), b* = ceil(log2(x + 1)):
+    "up" is the smallest L with b* <= L (x <= 2^L - 1), 16 above 255; "nearest" the
+    level nearest to b*, ties up (thresholds 1, 3, 31, 2047)."""
+    for lv, t in _THRESH[rounding]:
         if x <= t:
             return lv
     return EXACT
 
 
-def allocate(m_f32, e, qn, T, c, tau, window):
-    """Levels per block (index 0 oldest) from the fp32 masses m_f32, the key
+def allocate(m_f32, e, qn, T, c, tau, window, rounding="up"):
+    """Levels per block (index 0 oldest) from the fp32 masses m_f32, the block
     ranges e and the query norm qn (section 3.3 closed form, read as above)."""
     m = np.asarray(m_f32, dtype=np.float32).astype(np.float64)
     nblk = (int(T) + P - 1) // P
@@ -131,5 +146,5 @@ def allocate(m_f32, e, qn, T, c, tau, window):
         x = x * float(nblk)
         x = x * float(m[b])
         x = x / (2.0 * float(tau))
-        lv[b] = bit_level(x)
+        lv[b] = bit_level(x, rounding)
     return lv

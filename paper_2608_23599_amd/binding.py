@@ -85,7 +85,8 @@ _observe = _sig("gkv_observe_mass", _i32,
                 [_vp, _i32, _vp, _i32, _i32, _i32, _i64, ctypes.c_float, _vp, _vp, _i64, _vp])
 _query_norms = _sig("gkv_query_norms", _i32, [_vp, _i32, _i32, _i32, _i32, _vp, _vp])
 _allocate = _sig("gkv_allocate_levels", _i32,
-                 [_vp, _vp, _vp, _i32, _i32, _i64, ctypes.c_double, ctypes.c_double, _i32, _vp, _vp])
+                 [_vp, _vp, _vp, _i32, _i32, _i64, ctypes.c_double, ctypes.c_double, _i32, _i32, _vp, _vp])
+ROUNDING = {"up": 0, "nearest": 1}
 
 EXPORTED = [
     "gkv_strerror", "gkv_block_bytes", "gkv_ladder_levels", "gkv_ladder_crossings", "gkv_pool_create",
@@ -166,15 +167,17 @@ def query_norms(q_obs, Hkv):
     return qn
 
 
-def allocate_levels(k, mass, qn, c, tau, window):
-    """gkv_allocate_levels: int8 levels [B][Hkv][ceil(T/64)] on the device."""
+def allocate_levels(k, mass, qn, c, tau, window, rounding="up"):
+    """gkv_allocate_levels: int8 levels [B][Hkv][ceil(T/64)] on the device.  e_b is
+    the block range of the tensor passed as k (keys, or values for the value-range
+    reading); rounding is "up" or "nearest"."""
     k = _fp16_dev(k)
     B, Hkv, T = k.shape[0], k.shape[1], k.shape[2]
     mass = mass.to(k.device, torch.float32).contiguous()
     qn = qn.to(k.device, torch.float64).contiguous()
     lv = torch.empty((B, Hkv, (T + P - 1) // P), dtype=torch.int8, device=k.device)
-    _check(_allocate(_dptr(k), _dptr(mass), _dptr(qn), B, Hkv, T, float(c), float(tau), int(window), _dptr(lv),
-                     _stream()), "allocate_levels")
+    _check(_allocate(_dptr(k), _dptr(mass), _dptr(qn), B, Hkv, T, float(c), float(tau), int(window),
+                     ROUNDING[rounding], _dptr(lv), _stream()), "allocate_levels")
     return lv
 
 
@@ -401,6 +404,19 @@ class GradedCache:
         _check(_page_boxes(ctypes.byref(self.c), _dptr(k_src), k_src.shape[2], page_begin, page_end, _stream()),
                "page_boxes")
 
+    def _take(self, levels):
+        """Slots of the given levels from the pool, all or none (a full pool gives back
+        what was taken and raises)."""
+        got = []
+        try:
+            for L in levels:
+                got.append((L, self.pool.alloc(L)))
+        except GkvError:
+            for L, off in got:
+                self.pool.free(L, off)
+            raise
+        return np.array([off for _, off in got], dtype=np.int64)
+
     def demote(self, jobs, to_levels):
         """jobs: [(b, h, blk)], to_levels: levels; allocates the new slots, demotes,
         and frees the old ones (stream-ordered reuse)."""
@@ -413,7 +429,7 @@ class GradedCache:
                for b, h, i in J]
         # K and V slots of one block side by side, so that demoted one-centroid blocks
         # keep forming runs of back-to-back records
-        kv = np.array([self.pool.alloc(int(t)) for t in np.repeat(to, 2)], dtype=np.int64)
+        kv = self._take([int(t) for t in np.repeat(to, 2)])
         nk, nv = kv[0::2].copy(), kv[1::2].copy()
         st = _demote(ctypes.byref(self.c), n, _np_ptr(J), _np_ptr(to), _np_ptr(nk), _np_ptr(nv), _stream())
         if st != 0:
@@ -436,14 +452,19 @@ class GradedCache:
         T = self.T
         nk = nv = None
         if T % P == 0:
-            blk = T // P
             # K and V slots of one block side by side (the order gkv_layers_step takes them)
-            kv = np.array([self.pool.alloc(EXACT) for _ in range(2 * self.units)], dtype=np.int64)
+            kv = self._take([EXACT] * (2 * self.units))
             nk, nv = kv[0::2].copy(), kv[1::2].copy()
-            self.koff_host[:, :, blk] = nk.reshape(self.B, self.Hkv)
-            self.voff_host[:, :, blk] = nv.reshape(self.B, self.Hkv)
-        _check(_append(ctypes.byref(self.c), _dptr(kd), _dptr(vd), _np_ptr(nk) if nk is not None else None,
-                       _np_ptr(nv) if nv is not None else None, _stream()), "append")
+        st = _append(ctypes.byref(self.c), _dptr(kd), _dptr(vd), _np_ptr(nk) if nk is not None else None,
+                     _np_ptr(nv) if nv is not None else None, _stream())
+        if st != 0:
+            if nk is not None:
+                for off in kv:
+                    self.pool.free(EXACT, int(off))
+            raise GkvError(st, "append")
+        if nk is not None:  # the mirrors follow the library only once the call succeeded
+            self.koff_host[:, :, T // P] = nk.reshape(self.B, self.Hkv)
+            self.voff_host[:, :, T // P] = nv.reshape(self.B, self.Hkv)
         moves = []
         if profile is not None:
             jobs = np.empty(3 * 64, dtype=np.int32)
@@ -574,7 +595,7 @@ class LayerCaches:
 
     def step(self, k_new, v_new):
         """k_new, v_new: [L][B][Hkv][128] fp16 bits (device tensors or numpy).
-        Returns the number of blocks demoted per layer."""
+        Returns the number of blocks demoted over all layers."""
         k_new = _fp16_dev(k_new, self.caches[0].device)
         v_new = _fp16_dev(v_new, self.caches[0].device)
         n = int(_layers_step(self._c, self._p, self._ko, self._vo, len(self.caches), self.profile, _dptr(k_new),

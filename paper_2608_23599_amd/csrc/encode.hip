@@ -536,7 +536,8 @@ __global__ void __launch_bounds__(kThreads) rd_score_kernel(const uint16_t *__re
                                                             const int8_t *__restrict__ level,
                                                             const int64_t *__restrict__ voff,
                                                             const uint8_t *__restrict__ arena, int Hkv,
-                                                            int nblk_cap, uint64_t *__restrict__ keys, int vtok) {
+                                                            int nblk_cap, uint64_t *__restrict__ keys,
+                                                            int64_t key_stride, int vtok) {
   extern __shared__ __align__(16) unsigned char smem[];
   EncodeShared &S = *reinterpret_cast<EncodeShared *>(smem);
   const int blk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
@@ -558,17 +559,17 @@ __global__ void __launch_bounds__(kThreads) rd_score_kernel(const uint16_t *__re
     sc = sc + 0.0;  // -0 -> +0
     uint64_t bits;
     __builtin_memcpy(&bits, &sc, 8);
-    keys[u * T + tok] = (bits >> 63) ? ~bits : (bits | 0x8000000000000000ull);
+    keys[u * key_stride + tok] = (bits >> 63) ? ~bits : (bits | 0x8000000000000000ull);
   }
 }
 
 }  // namespace
 
 void gkv_launch_rd_score(const gkv_cache *c, const uint16_t *v_src, const float *mass, uint64_t *keys,
-                         hipStream_t stream) {
+                         int64_t key_stride, hipStream_t stream) {
   const int nblk = (int)((c->T + P - 1) / P);
   hipLaunchKernelGGL(rd_score_kernel, dim3(nblk, c->Hkv, c->B), dim3(kThreads), sizeof(EncodeShared), stream, v_src,
-                     mass, c->T, c->level, c->voff, c->arena, c->Hkv, c->nblk_cap, keys, c->v_per_token);
+                     mass, c->T, c->level, c->voff, c->arena, c->Hkv, c->nblk_cap, keys, key_stride, c->v_per_token);
 }
 
 // ---------------------------------------------------------------- C ABI

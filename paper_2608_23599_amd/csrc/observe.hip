@@ -300,7 +300,8 @@ __global__ void __launch_bounds__(256) query_norm_kernel(const uint16_t *__restr
 // Level of one block: key range, then x = c ||q|| e N m / (2 tau) against 2^L - 1.
 __global__ void __launch_bounds__(D) alloc_kernel(const uint16_t *__restrict__ k_src, const float *__restrict__ mass,
                                                   const double *__restrict__ qn, int Hkv, int64_t T, int nblk,
-                                                  double c, double tau, int window, int8_t *__restrict__ levels) {
+                                                  double c, double tau, int window, int rounding,
+                                                  int8_t *__restrict__ levels) {
   __shared__ double rng[D];
   const int blk = blockIdx.x, h = blockIdx.y, b = blockIdx.z, d = threadIdx.x;
   const int64_t u = (int64_t)b * Hkv + h;
@@ -326,11 +327,14 @@ __global__ void __launch_bounds__(D) alloc_kernel(const uint16_t *__restrict__ k
     x = x * (double)nblk;
     x = x * (double)mass[u * nblk + blk];
     x = x / (2.0 * tau);
+    // b* <= n is x <= 2^n - 1: rounded up, level L takes b* <= L; rounded to the
+    // nearest level (ties up), int4 takes b* <= 5 and int8 b* <= 11
+    const double t4 = rounding ? 31.0 : 15.0, t8 = rounding ? 2047.0 : 255.0;
     int8_t lv = GKV_EXACT;
     if (x <= 1.0) lv = GKV_CENTROID;
     else if (x <= 3.0) lv = GKV_INT2;
-    else if (x <= 15.0) lv = GKV_INT4;
-    else if (x <= 255.0) lv = GKV_INT8;
+    else if (x <= t4) lv = GKV_INT4;
+    else if (x <= t8) lv = GKV_INT8;
     levels[u * nblk + blk] = lv;
   }
 }
@@ -410,13 +414,14 @@ extern "C" gkv_status gkv_query_norms(const uint16_t *q_obs, int32_t n_obs, int3
 
 extern "C" gkv_status gkv_allocate_levels(const uint16_t *k_src, const float *mass, const double *qn, int32_t B,
                                           int32_t Hkv, int64_t T, double c, double tau, int32_t window,
-                                          int8_t *levels, void *stream) {
+                                          int32_t rounding, int8_t *levels, void *stream) {
   if (B <= 0 || Hkv <= 0 || T <= 0) return GKV_E_SHAPE;
   if (!k_src || !mass || !qn || !levels) return GKV_E_ARG;
   if (!(c > 0.0) || !(tau > 0.0) || window < 0) return GKV_E_ARG;
+  if (rounding != GKV_ROUND_UP && rounding != GKV_ROUND_NEAREST) return GKV_E_ARG;
   const int64_t nblk = (T + P - 1) / P;
   if (nblk > (1ll << 24)) return GKV_E_UNSUPPORTED;
   hipLaunchKernelGGL(alloc_kernel, dim3((unsigned)nblk, Hkv, B), dim3(D), 0, (hipStream_t)stream, k_src, mass, qn,
-                     Hkv, T, (int)nblk, c, tau, window, levels);
+                     Hkv, T, (int)nblk, c, tau, window, (int)rounding, levels);
   return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP;
 }

@@ -11,7 +11,7 @@
 using namespace gkv;
 
 void gkv_launch_rd_score(const gkv_cache *c, const uint16_t *v_src, const float *mass, uint64_t *keys,
-                         hipStream_t stream);
+                         int64_t key_stride, hipStream_t stream);
 int64_t gkv_attn_workspace(const gkv_cache *c, int32_t topk);
 
 namespace {
@@ -511,7 +511,10 @@ __global__ void __launch_bounds__(256) res_gather_kernel(const uint16_t *__restr
 static int64_t quest_ws(const gkv_cache *c) {
   return (int64_t)c->B * c->Hkv * (c->npage_cap * 16 + (int64_t)D * (c->Hq / c->Hkv) * 8);
 }
-static int64_t rd_ws(const gkv_cache *c) { return (int64_t)c->B * c->Hkv * (c->T > 0 ? c->T : 1) * 16; }
+// the residual selection's keys and lists are strided by the block capacity in tokens,
+// so that one workspace serves the cache at any length
+static int64_t rd_stride(const gkv_cache *c) { return (int64_t)c->nblk_cap * P; }
+static int64_t rd_ws(const gkv_cache *c) { return (int64_t)c->B * c->Hkv * rd_stride(c) * 16; }
 
 extern "C" int64_t gkv_workspace_bytes(const gkv_cache *c, int32_t op, int32_t topk) {
   if (gkv_validate_cache(c)) return -1;
@@ -577,9 +580,10 @@ extern "C" gkv_status gkv_rd_residual_select(gkv_cache *c, const uint16_t *k_src
   if (ws_bytes < rd_ws(c)) return GKV_E_WORKSPACE;
   hipStream_t s = (hipStream_t)stream;
   uint64_t *keys = (uint64_t *)ws;
-  if (nkeep > 0) gkv_launch_rd_score(c, v_src, mass, keys, s);
-  int32_t *idx_ws = (int32_t *)(keys + (int64_t)c->B * c->Hkv * c->T);
-  launch_select((const uint64_t *)keys, c->T, c->T, nkeep, c->res_idx, (int64_t)c->nres_cap, c->res_mask,
+  const int64_t stride = rd_stride(c);
+  if (nkeep > 0) gkv_launch_rd_score(c, v_src, mass, keys, stride, s);
+  int32_t *idx_ws = (int32_t *)(keys + (int64_t)c->B * c->Hkv * stride);
+  launch_select((const uint64_t *)keys, stride, c->T, nkeep, c->res_idx, (int64_t)c->nres_cap, c->res_mask,
                 (int64_t)c->nblk_cap, (int64_t)c->nblk_cap, c->B * c->Hkv, idx_ws, s);
   if (nkeep > 0) {
     dim3 g2((unsigned)((nkeep + P - 1) / P), c->Hkv, c->B);

@@ -2,10 +2,11 @@
 // calls (section 3.2 incremental append and monotone demotion, run for every layer
 // of a model by one host call, as a serving block manager does).
 //
-// The layers share B, Hkv, T and the ladder profile, so they hold the same levels and
-// cross the ladder at the same blocks: the crossings are computed once.  Every slot
-// the step needs (new exact blocks, demotion targets) is taken from the layers' pools
-// before anything is enqueued, so a full pool fails the call without side effects.
+// The layers share B, Hkv and T; each layer's ladder crossings are computed from its
+// own levels (layers laid out by the section 3.3 allocator hold different levels).
+// Every slot the step needs (new exact blocks, demotion targets) is taken from the
+// layers' pools, and checked against each layer's arena, before anything is
+// enqueued, so a full pool or a bad arena fails the call without side effects.
 #include <string.h>
 
 #include <vector>
@@ -29,6 +30,18 @@ struct Taken {  // slots taken for one layer, released again on failure
     for (auto &s : slots) gkv_pool_free(pool, s.first, s.second);
     slots.clear();
   }
+  // every slot lies inside an arena of `bytes`
+  bool fits(int64_t bytes) const {
+    for (auto &s : slots)
+      if (s.second < 0 || s.second + block_bytes(s.first) > bytes) return false;
+    return true;
+  }
+};
+
+struct Crossings {  // one layer's demotions at T + 1
+  std::vector<int32_t> jobs;
+  std::vector<int8_t> to;
+  int32_t n = 0;
 };
 
 }  // namespace
@@ -57,20 +70,28 @@ extern "C" int32_t gkv_layers_step(gkv_cache *const *caches, gkv_pool *const *po
       for (int64_t u = 0; u < units; ++u)
         if (c->level_host[u * cap + T / P] != GKV_EXACT) return GKV_E_ARG;
   }
-  // the crossings of T + 1 (the block the token opens never crosses)
-  int32_t none_j[3];
-  int8_t none_t[1];
-  int32_t n = gkv_ladder_crossings(c0, profile, T + 1, none_j, none_t, 0);  // the count only
-  if (n < 0) return n;
-  std::vector<int32_t> jobs(3 * (size_t)n + 3);
-  std::vector<int8_t> to((size_t)n + 1);
-  if (n) {
-    const int32_t m = gkv_ladder_crossings(c0, profile, T + 1, jobs.data(), to.data(), n);
-    if (m != n) return m < 0 ? m : GKV_E_ARG;
+  // every layer's crossings of T + 1 (the block the token opens never crosses); a
+  // layer whose levels the profile would raise fails the call here
+  std::vector<Crossings> cr(L);
+  for (int l = 0; l < L; ++l) {
+    int32_t none_j[3];
+    int8_t none_t[1];
+    const int32_t n = gkv_ladder_crossings(caches[l], profile, T + 1, none_j, none_t, 0);  // the count only
+    if (n < 0) return n;
+    cr[l].n = n;
+    cr[l].jobs.resize(3 * (size_t)n + 3);
+    cr[l].to.resize((size_t)n + 1);
+    if (n) {
+      const int32_t m = gkv_ladder_crossings(caches[l], profile, T + 1, cr[l].jobs.data(), cr[l].to.data(), n);
+      if (m != n) return m < 0 ? m : GKV_E_ARG;
+    }
   }
   // every slot of the step, before anything is enqueued
   std::vector<Taken> taken(L);
   std::vector<std::vector<int64_t>> nk(L), nv(L), dk(L), dv(L);
+  auto give_back_from = [&](int l0) {
+    for (int j = l0; j < L; ++j) taken[j].give_back();
+  };
   for (int l = 0; l < L; ++l) {
     taken[l].pool = pools[l];
     bool ok = true;
@@ -80,25 +101,39 @@ extern "C" int32_t gkv_layers_step(gkv_cache *const *caches, gkv_pool *const *po
       for (int64_t u = 0; u < units && ok; ++u)
         ok = taken[l].take(GKV_EXACT, nk[l][u]) && taken[l].take(GKV_EXACT, nv[l][u]);
     }
+    const int32_t n = cr[l].n;
     dk[l].resize(n);
     dv[l].resize(n);
-    for (int32_t i = 0; i < n && ok; ++i) ok = taken[l].take(to[i], dk[l][i]) && taken[l].take(to[i], dv[l][i]);
+    for (int32_t i = 0; i < n && ok; ++i)
+      ok = taken[l].take(cr[l].to[i], dk[l][i]) && taken[l].take(cr[l].to[i], dv[l][i]);
     if (!ok) {
-      for (int j = 0; j <= l; ++j) taken[j].give_back();
+      give_back_from(0);
       return GKV_E_POOL;
     }
+    if (!taken[l].fits(caches[l]->arena_bytes)) {  // a pool larger than the layer's arena
+      give_back_from(0);
+      return GKV_E_ARG;
+    }
   }
+  int32_t total = 0;
   for (int l = 0; l < L; ++l) {
     gkv_cache *c = caches[l];
     const size_t row = (size_t)units * D;
+    const int32_t n = cr[l].n;
+    const int32_t *jobs = cr[l].jobs.data();
+    const int8_t *to = cr[l].to.data();
     gkv_status st = gkv_append(c, k_new + l * row, v_new + l * row, open ? nk[l].data() : nullptr,
                                open ? nv[l].data() : nullptr, stream);
-    if (st) return st;
+    if (st) {  // layers before l are stepped; nothing of layer l or later is
+      give_back_from(l);
+      return st;
+    }
     if (open)
       for (int64_t u = 0; u < units; ++u) {
         koff_host[l][u * cap + T / P] = nk[l][u];
         voff_host[l][u * cap + T / P] = nv[l][u];
       }
+    total += n;
     if (!n) continue;
     // the current slots of the crossing blocks are free once the stream has passed
     // the demotion (later work on this stream that reuses them is ordered after it)
@@ -110,8 +145,15 @@ extern "C" int32_t gkv_layers_step(gkv_cache *const *caches, gkv_pool *const *po
       ok_[i] = koff_host[l][idx];
       ov_[i] = voff_host[l][idx];
     }
-    st = gkv_demote(c, n, jobs.data(), to.data(), dk[l].data(), dv[l].data(), stream);
-    if (st) return st;
+    st = gkv_demote(c, n, jobs, to, dk[l].data(), dv[l].data(), stream);
+    if (st) {  // layer l is appended but not demoted: its demotion slots go back too
+      for (int32_t i = 0; i < n; ++i) {
+        gkv_pool_free(pools[l], to[i], dk[l][i]);
+        gkv_pool_free(pools[l], to[i], dv[l][i]);
+      }
+      give_back_from(l + 1);
+      return st;
+    }
     for (int32_t i = 0; i < n; ++i) {
       const int64_t idx = ((int64_t)jobs[3 * i] * c->Hkv + jobs[3 * i + 1]) * cap + jobs[3 * i + 2];
       koff_host[l][idx] = dk[l][i];
@@ -120,5 +162,5 @@ extern "C" int32_t gkv_layers_step(gkv_cache *const *caches, gkv_pool *const *po
       gkv_pool_free(pools[l], from[i], ov_[i]);
     }
   }
-  return n;
+  return total;
 }

@@ -64,15 +64,19 @@ def test_query_norms_exact(gpu):
             assert got[b, h] == oobs.query_norm(_group(q_obs, b, h, 4))
 
 
-@pytest.mark.parametrize("T,window", [(64 * 300 + 17, 16), (64 * 40, 0)])
-def test_allocation_levels_exact(gpu, T, window):
-    """Levels from the same fp32 masses and query norms are identical.  The masses
-    are seeded log-uniform over 4.5 decades (observed masses of random keys are too
-    even to reach every level), and tau puts the median block at x = 6, so that the
-    blocks spread over the whole ladder."""
+@pytest.mark.parametrize("T,window,rounding,tensor", [(64 * 300 + 17, 16, "up", 0), (64 * 40, 0, "up", 0),
+                                                     (64 * 300 + 17, 16, "nearest", 0), (64 * 40, 0, "nearest", 1)])
+def test_allocation_levels_exact(gpu, T, window, rounding, tensor):
+    """Levels from the same fp32 masses and query norms are identical, for both
+    roundings of b* and for e_b taken over the keys (tensor 0) or the values (1).
+    The masses are seeded log-uniform over 4.5 decades (observed masses of random
+    keys are too even to reach every level), and tau puts the median block at x = 6,
+    so that the blocks spread over the whole ladder."""
     torch = pytest.importorskip("torch")
     B, Hq, Hkv, n_obs = 1, 8, 2, 8
-    ks, _ = kv_all(65, B, Hkv, T)
+    ks, vs = kv_all(65, B, Hkv, T)
+    if tensor:
+        ks = vs  # e_b from the value ranges
     q_obs = _obs_queries(65, B, n_obs, Hq)
     G = Hq // Hkv
     nb = (T + 63) // 64
@@ -85,17 +89,20 @@ def test_allocation_levels_exact(gpu, T, window):
     e = oobs.key_range(ks[0, 0])
     nblk = len(e)
     c = 1.0
-    tau = float(np.median(c * qn[0, 0] * e * nblk * m[0, 0].astype(np.float64))) / (2.0 * 6.0)
-    got = gpu.allocate_levels(ks, torch.from_numpy(m), torch.from_numpy(qn), c, tau, window).cpu().numpy()
+    xmed = 6.0 if rounding == "up" else 40.0  # nearest: int8 covers x up to 2047
+    tau = float(np.median(c * qn[0, 0] * e * nblk * m[0, 0].astype(np.float64))) / (2.0 * xmed)
+    got = gpu.allocate_levels(ks, torch.from_numpy(m), torch.from_numpy(qn), c, tau, window,
+                              rounding=rounding).cpu().numpy()
     seen = set()
     for b in range(B):
         for h in range(Hkv):
-            want = oobs.allocate(m[b, h], oobs.key_range(ks[b, h]), qn[b, h], T, c, tau, window)
+            want = oobs.allocate(m[b, h], oobs.key_range(ks[b, h]), qn[b, h], T, c, tau, window, rounding=rounding)
             np.testing.assert_array_equal(got[b, h], want)
             seen |= set(int(x) for x in want)
     assert {1, 2, 4, 8, 16} <= seen
     # the GPU's own query norms give the same levels
-    got2 = gpu.allocate_levels(ks, torch.from_numpy(m), gpu.query_norms(q_obs, Hkv), c, tau, window).cpu().numpy()
+    got2 = gpu.allocate_levels(ks, torch.from_numpy(m), gpu.query_norms(q_obs, Hkv), c, tau, window,
+                               rounding=rounding).cpu().numpy()
     np.testing.assert_array_equal(got2, got)
 
 

@@ -315,3 +315,96 @@ def test_layers_step_full_pool_changes_nothing(B):
         assert np.array_equal(k0, k) and np.array_equal(v0, v) and np.array_equal(l0, kp["lv"])
         assert c.T == T
     assert used == [[p.used(L) for L in B.LEVELS] for p in pools]
+
+
+def test_account_graded_quest_by_hand(B):
+    """The library's read accounting on the hand-computed graded Compressed-Quest
+    cases of the oracle's pin (section 3.5, R_read equation)."""
+    from tests.test_oracle_quest_attn import GRADED_QUEST_CASES
+    for case in GRADED_QUEST_CASES:
+        T, lv = case["T"], np.array(case["levels"], dtype=np.int8)
+        c, keep = _host_cache(B, 1, 1, 4, T, lv, page=16)
+        pages = np.array(case["pages"], dtype=np.int32).reshape(1, 1, -1)
+        rates = B.Rates()
+        assert B._account(ctypes.byref(c), B._np_ptr(pages), pages.shape[-1], ctypes.byref(rates)) == 0
+        assert rates.read_bits == case["read_bits"]
+        if case["resident_bits"] is not None:
+            assert rates.resident_bits == case["resident_bits"]
+
+
+def _layers_setup(B, T, levels_per_layer, pool_caps, arena_bytes=None):
+    caches, keeps, pools, kos, vos = [], [], [], [], []
+    for lv, caps in zip(levels_per_layer, pool_caps):
+        c, keep = _host_cache(B, 1, 2, 8, T, lv)
+        if arena_bytes is not None:
+            c.arena_bytes = arena_bytes
+        caches.append(c)
+        keeps.append(keep)
+        pools.append(B.Pool(caps))
+        nb = c.nblk_cap
+        kos.append(np.arange(2 * nb, dtype=np.int64).reshape(1, 2, nb))
+        vos.append(kos[-1] + 1000)
+    return caches, keeps, pools, kos, vos
+
+
+def _layers_call(B, caches, pools, kos, vos):
+    L = len(caches)
+    arr = lambda xs: (ctypes.c_void_p * L)(*xs)
+    kn = np.zeros((L, 1, 2, 128), dtype=np.uint16)
+    return B._layers_step(arr([ctypes.addressof(c) for c in caches]), arr([p.h for p in pools]),
+                          arr([k.ctypes.data for k in kos]), arr([v.ctypes.data for v in vos]), L,
+                          B.PROFILES["graded"], kn.ctypes.data, kn.ctypes.data, None)
+
+
+def _unchanged(B, before, used, caches, keeps, pools, kos, vos, T):
+    for (k0, v0, l0), k, v, kp, c in zip(before, kos, vos, keeps, caches):
+        assert np.array_equal(k0, k) and np.array_equal(v0, v) and np.array_equal(l0, kp["lv"])
+        assert c.T == T
+    assert used == [[p.used(L) for L in B.LEVELS] for p in pools]
+
+
+def test_layers_step_rejects_a_layer_the_ladder_would_raise(B):
+    """Each layer's crossings come from its own levels: a layer holding a block below
+    the level the profile gives it at T + 1 (here one int8-band block at int2) makes
+    the call fail with GKV_E_NOT_MONOTONE before any slot is taken, leaving every
+    cache, pool and mirror as it was; layer 0 alone would step."""
+    T = 64 * 40 + 5
+    lv = olad.ladder("graded", T)
+    lv1 = lv.copy()
+    i8 = int(np.flatnonzero(lv == 8)[0])
+    lv1[i8] = 2
+    caps = {16: 8, 8: 8, 4: 8, 2: 8, 1: 8}
+    caches, keeps, pools, kos, vos = _layers_setup(B, T, [lv, lv1], [caps, caps])
+    before = [(k.copy(), v.copy(), kp["lv"].copy()) for k, v, kp in zip(kos, vos, keeps)]
+    used = [[p.used(L) for L in B.LEVELS] for p in pools]
+    assert _layers_call(B, caches, pools, kos, vos) == -3  # GKV_E_NOT_MONOTONE
+    _unchanged(B, before, used, caches, keeps, pools, kos, vos, T)
+
+
+def test_layers_step_rejects_slots_past_the_arena(B):
+    """A pool whose slots lie past a layer's arena_bytes: the step takes its slots,
+    finds one outside the arena, gives every slot back and returns GKV_E_ARG with
+    nothing changed."""
+    T = 64 * 30  # the next token opens block 30 of every (b, h)
+    lv = olad.ladder("graded", T)
+    caps = {16: 8, 8: 8, 4: 8, 2: 8, 1: 8}
+    caches, keeps, pools, kos, vos = _layers_setup(B, T, [lv, lv], [caps, caps], arena_bytes=4 * 16384)
+    before = [(k.copy(), v.copy(), kp["lv"].copy()) for k, v, kp in zip(kos, vos, keeps)]
+    used = [[p.used(L) for L in B.LEVELS] for p in pools]
+    assert _layers_call(B, caches, pools, kos, vos) == -1  # GKV_E_ARG
+    _unchanged(B, before, used, caches, keeps, pools, kos, vos, T)
+
+
+def test_binding_append_with_full_pool_changes_nothing(B):
+    """GradedCache.append takes the new block's slots all or none: with room for one
+    exact slot where a new block needs two per (b, h), it raises before the library
+    is called, and the pool and the offset mirrors are as they were (host-only: the
+    tables live in host memory and nothing is enqueued)."""
+    c = B.GradedCache(1, 2, 8, 64, 4, {16: 1}, device="cpu")
+    ko, vo = c.koff_host.copy(), c.voff_host.copy()
+    used = [c.pool.used(L) for L in B.LEVELS]
+    with pytest.raises(B.GkvError):
+        c.append(np.zeros((1, 2, 128), np.uint16), np.zeros((1, 2, 128), np.uint16))
+    assert [c.pool.used(L) for L in B.LEVELS] == used
+    assert np.array_equal(c.koff_host, ko) and np.array_equal(c.voff_host, vo)
+    assert c.T == 64

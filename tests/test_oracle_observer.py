@@ -101,6 +101,52 @@ def test_bit_depth_thresholds(x, level):
     assert level == min([L for L in (1, 2, 4, 8, 16) if L >= b] or [16])
 
 
+def _nearest_level(b):
+    """The level of {1, 2, 4, 8, 16} nearest to an integer bit depth b (b >= 0),
+    ties to the larger level; b <= 1 clamps to 1."""
+    best = None
+    for L in (1, 2, 4, 8, 16):
+        if best is None or abs(L - b) < abs(best - b) or (abs(L - b) == abs(best - b) and L > best):
+            best = L
+    return best
+
+
+def test_bit_depth_nearest_level():
+    """The "nearest available discrete level" reading of section 3.3: for every
+    integer b* the level nearest to it (ties up), found by brute force over the
+    ladder, equals bit_level(x, "nearest") both at the smallest x with that b*
+    and at the largest (x = 2^b* - 1)."""
+    import math
+    assert [_nearest_level(b) for b in range(14)] == [1, 1, 2, 4, 4, 4, 8, 8, 8, 8, 8, 8, 16, 16]
+    for b in range(0, 20):
+        hi = 2.0 ** b - 1.0                     # largest x with ceil(log2(x + 1)) == b
+        lo = 2.0 ** (b - 1) - 1.0 if b else 0.0  # x a little above it has b* == b
+        xs = [hi] + ([lo + 2.0 ** (b - 1) * 1e-9] if b else [])
+        for x in xs:
+            assert math.ceil(math.log2(x + 1)) == b
+            assert observer.bit_level(x, "nearest") == _nearest_level(b), (b, x)
+    # the two readings differ exactly at b* = 5 and b* = 9..11
+    for b in range(0, 20):
+        up = observer.bit_level(2.0 ** b - 1.0, "up")
+        near = observer.bit_level(2.0 ** b - 1.0, "nearest")
+        assert (up != near) == (b in (5, 9, 10, 11)), b
+
+
+def test_allocate_nearest_reading():
+    """The formula test's setting under both readings: x = m / 2, so masses 6 (x = 3,
+    b* = 2), 30 (x = 15, b* = 4), 60 (x = 30, b* = 5), 510 (x = 255, b* = 8), 4000
+    (x = 2000, b* = 11) and 5000 (x = 2500, b* = 12) give 2, 4, 4, 8, 8, 16 when
+    rounded to the nearest level and 2, 4, 8, 8, 16, 16 when rounded up."""
+    T = 64 * 10 + 5
+    e = np.full(11, 2.0)
+    qn, c, tau = 4.0, 1.0, 11.0 * 8.0
+    m = np.array([0, 2, 6, 30, 60, 510, 4000, 5000, 1, 1, 1], dtype=np.float32)
+    assert list(observer.allocate(m, e, qn, T, c, tau, window=2, rounding="nearest")) == \
+        [1, 1, 2, 4, 4, 8, 8, 16, 1, 16, 16]
+    assert list(observer.allocate(m, e, qn, T, c, tau, window=2, rounding="up")) == \
+        [1, 1, 2, 4, 8, 8, 16, 16, 1, 16, 16]
+
+
 def test_allocate_formula_window_and_monotone():
     T = 64 * 10 + 5          # 11 blocks, the last partial
     e = np.full(11, 2.0)

@@ -8,7 +8,7 @@ import numpy as np
 import pytest
 
 from oracle import fp16, quant, quest, attention, residual, accounting, certificate, cache
-from oracle.ladder import ladder
+from oracle.ladder import ladder, EXACT, INT8, INT4, INT2, CENTROID
 from paper_2608_23599_amd import synth
 
 GOLD = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_rates.json")))
@@ -233,3 +233,52 @@ def test_paper_per_token_bytes():
     g = GOLD["kv_gib_1m_qwen25_7b"]
     bits = g["tokens"] * g["layers"] * g["kv_heads"] * 2 * accounting.row_bits(16, g["head_dim"])
     assert round(bits / 8 / 2 ** 30, 2) == g["value"]
+
+
+# Graded Compressed-Quest read rate (section 3.5, R_read equation), written out term by
+# term by hand.  Per tensor block of 64 tokens x 128 channels: int b codes 128*b bits
+# per row plus 2 * 128 * 16 bits of scale/zero per block; centroid state 2 bits of id
+# per row plus 4 * 128 * 16 bits of centroids per block; exact 128 * 16 bits per row.
+# Every term is doubled for K and V.  A plausible slip fails one of the two cases:
+# scale/zero charged per page instead of per touched block (case 1 has two pages of
+# one int2 block, case 2 two pages of one int4 block), the current page's block
+# overhead dropped (case 2's current page lies in an int8 block), the current page
+# left out or counted as a full page (case 1's is 8 rows), boxes counted for the
+# ranked pages only instead of every closed page.
+GRADED_QUEST_CASES = [
+    dict(T=248, levels=[CENTROID, INT2, INT8, EXACT], pages=[1, 5, 6, 9, 12],
+         terms=[15 * 2 * 128 * 16,       # boxes of the 15 closed pages (248 // 16)
+                16 * 2 * 2,              # page 1: 16 rows of 2-bit centroid ids, block 0
+                2 * 4 * 128 * 16,        # block 0 centroids, once
+                32 * 2 * 128 * 2,        # pages 5, 6: 32 rows of int2 codes, block 1
+                2 * 2 * 128 * 16,        # block 1 scale/zero, once for both pages
+                16 * 2 * 128 * 8,        # page 9: 16 rows of int8 codes, block 2
+                2 * 2 * 128 * 16,        # block 2 scale/zero
+                16 * 2 * 128 * 16,       # page 12: 16 exact rows, block 3
+                8 * 2 * 128 * 16],       # current page 15: tokens 240..247, 8 exact rows
+         read_bits=241728, resident_bits=520448),
+    dict(T=256, levels=[INT4, INT8, INT2, INT8], pages=[0, 3, 9],
+         terms=[16 * 2 * 128 * 16,       # boxes of the 16 closed pages (256 // 16)
+                32 * 2 * 128 * 4,        # pages 0, 3: 32 rows of int4 codes, block 0
+                2 * 2 * 128 * 16,        # block 0 scale/zero, once for both pages
+                16 * 2 * 128 * 2,        # page 9: 16 rows of int2 codes, block 2
+                2 * 2 * 128 * 16,        # block 2 scale/zero
+                16 * 2 * 128 * 8,        # current page 15 (always read): int8, block 3
+                2 * 2 * 128 * 16],       # block 3 scale/zero, touched by the current page only
+         read_bits=163840, resident_bits=None),
+]
+
+
+@pytest.mark.parametrize("case", GRADED_QUEST_CASES)
+def test_graded_quest_read_rate_by_hand(case):
+    assert sum(case["terms"]) == case["read_bits"]
+    T = case["T"]
+    r = accounting.unit_rates(case["levels"], T, page=16, pages=np.array(case["pages"]))
+    assert r["read_bits"] == case["read_bits"]
+    assert r["values"] == T * 2 * 128
+    if case["resident_bits"] is not None:
+        # 2 x (centroid 8320 + int2 20480 + int8 69632 + exact 131072) + 15 boxes
+        assert r["resident_bits"] == 2 * (8320 + 20480 + 69632 + 131072) + 15 * 4096 == case["resident_bits"]
+    # the same pages listed twice, unsorted, with -1 padding read the same bits
+    padded = np.array(list(reversed(case["pages"])) + case["pages"][:1] + [-1, -1])
+    assert accounting.unit_rates(case["levels"], T, page=16, pages=padded)["read_bits"] == case["read_bits"]
