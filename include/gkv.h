@@ -138,7 +138,18 @@ typedef struct gkv_cache {
                                 gkv_append; fp32 rounded upwards                     */
   int32_t v_per_token;       /* 1: the values' int levels are grouped per token (see
                                 the record layout); 0: per channel, like the keys     */
+  uint64_t version;          /* stamp of the block tables' state: every call that
+                                changes level / koff / voff / res_mask / nres / T sets
+                                a new process-wide unique value; a caller that writes
+                                those tables itself calls gkv_cache_changed.  0 =
+                                unknown (dense attention plans are then never reused) */
 } gkv_cache;
+
+/* Stamps c->version with a new process-wide unique value: a caller that has written
+ * the block tables (level, koff, voff, res_mask) or changed T or nres itself calls
+ * this before the next attention call, so that a dense plan kept in a workspace for
+ * the old tables is not reused.  The library's own calls stamp the cache themselves. */
+void gkv_cache_changed(gkv_cache *c);
 
 /* ---------------------------------------------------------------- host helpers */
 
@@ -266,6 +277,13 @@ gkv_status gkv_quest_select(const uint16_t *q, const gkv_cache *c, int32_t topk,
  * topk + 1). */
 gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache *c, const int32_t *pages, int32_t topk,
                                   float *out, void *ws, int64_t ws_bytes, void *stream);
+/* Plan reuse.  The visit plan of a dense read depends only on the block tables, not
+ * on the query.  A dense call whose cache has a nonzero version leaves a tag of the
+ * planned state (version, T, nres, table addresses, split) in the workspace; the plan
+ * kernel of a later dense call with the same workspace and an identical tag exits at
+ * once and the attention reuses the plan.  The check runs on the device, so a captured
+ * graph replays it correctly.  Compressed-Quest calls always plan (their pages change
+ * with every query) and invalidate the tag. */
 
 /* Dense gkv_graded_decode_attn plus the decode-time attention error certificate
  * (section 3.6, Eq. certificate) of every query head: bound[b][g] bounds

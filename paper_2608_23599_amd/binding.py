@@ -39,6 +39,7 @@ class CacheStruct(ctypes.Structure):
         ("nres", _i32), ("nres_cap", _i32), ("res_idx", _vp), ("res_rows", _vp), ("res_mask", _vp),
         ("cert", _vp),
         ("v_per_token", _i32),
+        ("version", ctypes.c_uint64),
     ]
 
 
@@ -79,6 +80,7 @@ _attn_plan = _sig("gkv_attn_plan", _i32, [_P(CacheStruct), _vp, _i32, _vp, _i64,
 _attn_partials = _sig("gkv_attn_partials", _i32, [_vp, _P(CacheStruct), _vp, _i32, _vp, _i64, _vp])
 _attn_merge = _sig("gkv_attn_merge", _i32, [_P(CacheStruct), _vp, _i32, _vp, _vp, _i64, _vp])
 _rd = _sig("gkv_rd_residual_select", _i32, [_P(CacheStruct), _vp, _vp, _vp, _i32, _vp, _i64, _vp])
+_cache_changed = _sig("gkv_cache_changed", None, [_P(CacheStruct)])
 _layers_step = _sig("gkv_layers_step", _i32, [_vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _vp])
 _observe_ws = _sig("gkv_observe_ws_bytes", _i64, [_i32, _i32, _i32, _i64, _i32])
 _observe = _sig("gkv_observe_mass", _i32,
@@ -95,6 +97,7 @@ EXPORTED = [
     "gkv_page_boxes", "gkv_append", "gkv_quest_select", "gkv_graded_decode_attn", "gkv_rd_residual_select",
     "gkv_attn_plan", "gkv_attn_partials", "gkv_attn_merge", "gkv_graded_decode_attn_bound",
     "gkv_observe_ws_bytes", "gkv_observe_mass", "gkv_query_norms", "gkv_allocate_levels", "gkv_layers_step",
+    "gkv_cache_changed",
 ]
 
 
@@ -313,6 +316,7 @@ class GradedCache:
         c.res_mask = self.res_mask.data_ptr() if self.nres_cap else None
         c.cert = self.cert.data_ptr()
         c.v_per_token = int(self.v_per_token)
+        _cache_changed(ctypes.byref(c))  # new tables: a fresh version stamp
 
     def clone(self):
         """A read-only copy in separate device memory (same layout and offsets), for
@@ -377,6 +381,7 @@ class GradedCache:
         self.level.copy_(torch.from_numpy(self.level_host))
         self.koff.copy_(torch.from_numpy(self.koff_host))
         self.voff.copy_(torch.from_numpy(self.voff_host))
+        _cache_changed(ctypes.byref(self.c))  # the tables were written from here
 
     @property
     def T(self):

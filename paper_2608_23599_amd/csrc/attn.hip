@@ -197,6 +197,9 @@ __device__ __forceinline__ float v_off(int j) {
 }
 
 // ---------------------------------------------------------------- parameters
+constexpr int kTagWords = 12;
+constexpr uint64_t kTagMagic = 0x676b76706c616e31ull;  // marks a tag as written by a dense plan
+
 struct AttnParams {
   const uint16_t *q;
   const int8_t *level;
@@ -218,6 +221,12 @@ struct AttnParams {
   int fast;  // workgroups of each (b, KV head) dispatched first (see attn_grid)
   int64_t vcap, icap, ucap;
   float sl2;  // log2(e) / sqrt(D)
+  // Plan reuse (dense reads of a cache with a version stamp): the workspace's tag holds
+  // the key of the state whose plan it holds; the plan kernel skips when it matches,
+  // the attention kernel writes it once the plan is complete.
+  int cacheable;
+  uint64_t *tag;
+  uint64_t key[kTagWords];
 };
 
 constexpr int kSlotBytes = 4096;  // one copy unit
@@ -1147,6 +1156,12 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   const int kg = lane >> 4, m16 = lane & 15;
   const int64_t u = (int64_t)b * p.Hkv + h;
   const int W = p.nsplit * kWaves, w = sidx * kWaves + wave;
+  if (p.cacheable && blockIdx.x == 0 && threadIdx.x == 0) {
+    // the plan kernel of this call has finished: the workspace now holds the plan of
+    // this key (vector stores; read by later calls' plan kernels)
+#pragma unroll
+    for (int i = 0; i < kTagWords; ++i) p.tag[i] = p.key[i];
+  }
 
   // the group's queries (rows of absent heads are zero)
   uint8_t *qs = smem + kWaves * kWaveLds;
@@ -1712,7 +1727,20 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
   __shared__ uint32_t lastc[kPlanThreads];
   __shared__ VisitDesc lds_desc[kPlanLdsVisits];
   __shared__ uint32_t joins[32768 / 32];  // one-centroid run bits of a dense plan (nblk < 32768)
-  __shared__ int s_cnt;
+  __shared__ int s_cnt, s_same;
+  if (p.cacheable) {  // a dense read whose plan the workspace may already hold
+    if (threadIdx.x == 0) {
+      int same = 1;
+#pragma unroll
+      for (int i = 0; i < kTagWords; ++i) same &= p.tag[i] == p.key[i];
+      s_same = same;
+    }
+    __syncthreads();
+    if (s_same) return;
+  }
+  // the plan is rewritten: the tag is stale until an attention kernel validates it
+  // (no workgroup of this launch can see this launch's key in it)
+  if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) p.tag[0] = 0;
   const int64_t u = blockIdx.x;
   const int W = p.nsplit * kWaves;
   PlanOut o;
@@ -1891,10 +1919,11 @@ static int attn_fast(int nsplit, int64_t units) {
 }
 
 // Workspace layout, sized by the cache capacity so that it does not move as T grows:
-// partials | wavefront splits (items, units) | visit descriptors | item descriptors |
-// unit descriptors (+512 B: the descriptor copies read whole 512-byte chunks).
+// plan tag | partials | wavefront splits (items, units) | visit descriptors | item
+// descriptors | unit descriptors (+512 B: the descriptor copies read whole 512-byte
+// chunks).
 struct AttnLayout {
-  int64_t split, visits, plan, units, total, vcap, icap, ucap;
+  int64_t part, split, visits, plan, units, total, vcap, icap, ucap;
   int ncap;
 };
 static int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
@@ -1906,7 +1935,8 @@ static AttnLayout attn_layout(const gkv_cache *c, int32_t topk) {
   L.vcap = topk > 0 ? (int64_t)topk + 1 : (int64_t)c->nblk_cap + (c->nres_cap + P - 1) / P;
   L.icap = 4 * L.vcap;  // at most 4 items per visit
   L.ucap = 8 * L.vcap;  // at most 8 units per visit (an exact block)
-  L.split = align256(units * L.ncap * G * kPart * 4);
+  L.part = 256;  // the plan tag (kTagWords words) comes first
+  L.split = L.part + align256(units * L.ncap * G * kPart * 4);
   L.visits = L.split + align256(units * 2 * ((int64_t)L.ncap * kWaves + 1) * 4);
   L.plan = L.visits + align256(units * L.vcap * (int64_t)sizeof(VisitDesc));
   L.units = L.plan + align256(units * L.icap * (int64_t)sizeof(ItemDesc));
@@ -1942,7 +1972,8 @@ static gkv_status attn_setup(const uint16_t *q, const gkv_cache *c, const int32_
   p.res_mask = c->res_mask;
   p.res_rows = c->res_rows;
   p.pages = pages;
-  p.part = (float *)ws;
+  p.tag = (uint64_t *)ws;
+  p.part = (float *)((uint8_t *)ws + L.part);
   p.split = (int32_t *)((uint8_t *)ws + L.split);
   p.visits = (uint8_t *)ws + L.visits;
   p.plan = (uint8_t *)ws + L.plan;
@@ -1963,6 +1994,22 @@ static gkv_status attn_setup(const uint16_t *q, const gkv_cache *c, const int32_
   p.nsplit = attn_nsplit(c, topk, c->T);
   p.fast = attn_fast(p.nsplit, (int64_t)c->B * c->Hkv);
   p.sl2 = 1.4426950408889634f / sqrtf((float)D);
+  // the key of the planned state: a dense plan depends on the tables (version stamp
+  // and addresses), T, the residual count and the split
+  p.cacheable = !pages && c->version != 0;
+  const uint64_t key[kTagWords] = {c->version,
+                                   (uint64_t)c->T,
+                                   (uint64_t)(uint32_t)c->nres | ((uint64_t)(uint32_t)p.nsplit << 32),
+                                   (uint64_t)(uint32_t)p.fast | ((uint64_t)(uint32_t)c->nblk_cap << 32),
+                                   (uint64_t)(uintptr_t)c->level,
+                                   (uint64_t)(uintptr_t)c->koff,
+                                   (uint64_t)(uintptr_t)c->voff,
+                                   (uint64_t)(uintptr_t)c->arena,
+                                   (uint64_t)(uintptr_t)c->res_mask,
+                                   (uint64_t)(uintptr_t)c->res_rows,
+                                   (uint64_t)(uint32_t)c->B | ((uint64_t)(uint32_t)c->Hkv << 32),
+                                   kTagMagic};
+  for (int i = 0; i < kTagWords; ++i) p.key[i] = key[i];
   return GKV_OK;
 }
 
@@ -2060,3 +2107,4 @@ extern "C" gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache 
   launch_merge(p, c, out, s);
   return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP;
 }
+

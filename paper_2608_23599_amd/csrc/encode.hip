@@ -637,6 +637,7 @@ extern "C" gkv_status gkv_demote(gkv_cache *c, int32_t n, const int32_t *jobs, c
   }
   for (int i = 0; i < n; ++i)
     c->level_host[((int64_t)jobs[3 * i] * c->Hkv + jobs[3 * i + 1]) * c->nblk_cap + jobs[3 * i + 2]] = to[i];
+  gkv_stamp(c);
   return GKV_OK;
 }
 
@@ -688,5 +689,6 @@ extern "C" gkv_status gkv_append(gkv_cache *c, const uint16_t *k_new, const uint
   if (open)
     for (int64_t u = 0; u < (int64_t)c->B * c->Hkv; ++u) c->level_host[u * c->nblk_cap + blk] = GKV_EXACT;
   c->T = T + 1;
+  gkv_stamp(c);
   return GKV_OK;
 }

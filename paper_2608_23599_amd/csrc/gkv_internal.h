@@ -144,3 +144,7 @@ gkv_status gkv_validate_cache(const gkv_cache *c);
 
 // Compute units of the current device (cached per device; attn.hip).
 int gkv_device_cus();
+
+// Sets c->version to a new process-wide unique stamp (host.cpp); every call that
+// changes the block tables, T or nres calls it on success.
+void gkv_stamp(gkv_cache *c);

@@ -3,6 +3,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <atomic>
 #include <vector>
 
 #include "gkv_internal.h"
@@ -24,6 +25,15 @@ extern "C" const char *gkv_strerror(gkv_status s) {
 }
 
 extern "C" int64_t gkv_block_bytes(int32_t level) { return block_bytes(level); }
+
+// ---------------------------------------------------------------- table versions
+static std::atomic<uint64_t> g_version{0};
+
+void gkv_stamp(gkv_cache *c) { c->version = g_version.fetch_add(1, std::memory_order_relaxed) + 1; }
+
+extern "C" void gkv_cache_changed(gkv_cache *c) {
+  if (c) gkv_stamp(c);
+}
 
 extern "C" uint16_t gkv_f64_to_f16(double x) { return f64_to_f16(x); }
 

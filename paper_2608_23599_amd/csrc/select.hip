@@ -592,5 +592,6 @@ extern "C" gkv_status gkv_rd_residual_select(gkv_cache *c, const uint16_t *k_src
   }
   if (hipGetLastError() != hipSuccess) return GKV_E_HIP;
   c->nres = nkeep;
+  gkv_stamp(c);
   return GKV_OK;
 }

@@ -926,3 +926,60 @@ def test_quest128k_b8_full_size_sampled(gpu):
             kh[sel] = oquant.decode(oquant.encode_fp16(int(lv[blk]), ks[b, h, rows]))[idx[sel] - blk * 64]
             vh[sel] = oquant.decode(oquant.encode_fp16(int(lv[blk]), vs[b, h, rows]))[idx[sel] - blk * 64]
         assert max_err(out[b, h * G:(h + 1) * G], oattn.unit_decode(q_group(q, b, h, G), kh, vh)) <= TOL
+
+
+# ---------------------------------------------------------------- dense plan reuse
+
+
+def test_dense_plan_reuse_follows_the_tables(gpu):
+    """A dense read reuses the visit plan a workspace holds only for the same table
+    state: two caches alternating on one workspace, an append (T grows), a demotion
+    (levels and slots change), a residual selection (rows leave their blocks) and a
+    Compressed-Quest read on the same workspace in between each give the output of a
+    call with a fresh workspace, bit for bit.  The workspace's tag carries the
+    cache's version after a dense call and is cleared by a Compressed-Quest call."""
+    import ctypes
+    torch = _torch()
+    T, Hq, Hkv = 2048, 8, 2
+    (ka, va), (kb, vb) = kv_all(40, 1, Hkv, T + 1), kv_all(41, 1, Hkv, T)
+    lv = olad.ladder("tiny", T)
+    A = _build(gpu, ka[:, :, :T], va[:, :, :T], Hq, lv, page=16, extra_blocks=2, nres_cap=64,
+               slack={16: 4, 8: 4, 4: 4, 2: 4, 1: 4})
+    Bc = _build(gpu, kb, vb, Hq, lv, page=16, extra_blocks=2, nres_cap=64, slack={16: 4, 8: 4, 4: 4, 2: 4, 1: 4})
+    q = synth.queries(40, 1, Hq)
+    nbytes = max(A.workspace(1, 0).numel(), A.workspace(1, 32).numel())
+    shared = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+
+    def dec(c, pages=None):
+        out = torch.empty((1, Hq, 128), dtype=torch.float32, device="cuda")
+        topk = 0 if pages is None else int(pages.shape[-1])
+        st = gpu._attn(gpu._dptr(gpu._as_bits(q, "cuda")), ctypes.byref(c.c), gpu._dptr(pages), topk,
+                       gpu._dptr(out), gpu._dptr(shared), shared.numel(), gpu._stream())
+        assert st == 0
+        return out
+
+    def fresh(c, pages=None):
+        c._ws = {}
+        return c.decode(q, pages=pages)
+
+    def tag():
+        torch.cuda.synchronize()
+        return int(shared[:8].cpu().numpy().view(np.uint64)[0])
+
+    for c in (A, Bc, A, Bc, A):
+        assert torch.equal(dec(c), fresh(c))
+        assert tag() == c.c.version
+    A.append(ka[:, :, T], va[:, :, T], profile="tiny")
+    assert torch.equal(dec(A), fresh(A))
+    Bc.demote([(0, 0, 5), (0, 1, 9)], [1, 2])  # int2 -> centroid, int4 -> int2
+    assert torch.equal(dec(Bc), fresh(Bc))
+    mass = np.stack([synth.mass_unit(41, 0, h, T) for h in range(Hkv)])[None]
+    Bc.rd_residual_select(kb, vb, mass, 64)
+    assert torch.equal(dec(Bc), fresh(Bc))
+    pages = A.quest_select(q, 32)
+    assert torch.equal(dec(A, pages), fresh(A, pages))
+    assert tag() == 0
+    assert torch.equal(dec(Bc), fresh(Bc))
+    assert torch.equal(dec(A), fresh(A))
+    # the reused plan is the same one: the same call twice gives the same bits
+    assert torch.equal(dec(A), dec(A))
