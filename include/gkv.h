@@ -285,6 +285,22 @@ gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache *c, const i
  * graph replays it correctly.  Compressed-Quest calls always plan (their pages change
  * with every query) and invalidate the tag. */
 
+/* gkv_graded_decode_attn for callers that cannot allocate or pass a workspace (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the workspace is a device array inside the library, gkv_noalloc_scratch_bytes()
+ * = 32 MiB per GPU, held by each GPU the library runs on until the process ends.
+ * The caller passes inputs and outputs as for gkv_graded_decode_attn.
+ * GKV_E_WORKSPACE (before anything is enqueued) when the call needs more than the
+ * array, i.e. when gkv_workspace_bytes(c, 1, topk) > 32 MiB (a dense read of
+ * B * Hkv = 32 (sequence, KV head) units at 2048 blocks with 2621 residual rows
+ * each needs about 17 MB).  Every call on one GPU uses that GPU's one array, which
+ * keeps the last call's contents: calls that overlap on one GPU (other streams,
+ * other threads) race and must be ordered by the caller.  The call itself allocates
+ * nothing; its first call on a device looks the array's address up. */
+int64_t gkv_noalloc_scratch_bytes(void);
+gkv_status gkv_graded_decode_attn_noalloc(const uint16_t *q, const gkv_cache *c, const int32_t *pages, int32_t topk,
+                                          float *out, void *stream);
+
 /* Dense gkv_graded_decode_attn plus the decode-time attention error certificate
  * (section 3.6, Eq. certificate) of every query head: bound[b][g] bounds
  * ||o - o_hat|| between attention over the exact rows and out, as

@@ -81,6 +81,8 @@ _attn_partials = _sig("gkv_attn_partials", _i32, [_vp, _P(CacheStruct), _vp, _i3
 _attn_merge = _sig("gkv_attn_merge", _i32, [_P(CacheStruct), _vp, _i32, _vp, _vp, _i64, _vp])
 _rd = _sig("gkv_rd_residual_select", _i32, [_P(CacheStruct), _vp, _vp, _vp, _i32, _vp, _i64, _vp])
 _cache_changed = _sig("gkv_cache_changed", None, [_P(CacheStruct)])
+_attn_noalloc = _sig("gkv_graded_decode_attn_noalloc", _i32, [_vp, _P(CacheStruct), _vp, _i32, _vp, _vp])
+_noalloc_bytes = _sig("gkv_noalloc_scratch_bytes", _i64, [])
 _layers_step = _sig("gkv_layers_step", _i32, [_vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _vp])
 _observe_ws = _sig("gkv_observe_ws_bytes", _i64, [_i32, _i32, _i32, _i64, _i32])
 _observe = _sig("gkv_observe_mass", _i32,
@@ -97,7 +99,7 @@ EXPORTED = [
     "gkv_page_boxes", "gkv_append", "gkv_quest_select", "gkv_graded_decode_attn", "gkv_rd_residual_select",
     "gkv_attn_plan", "gkv_attn_partials", "gkv_attn_merge", "gkv_graded_decode_attn_bound",
     "gkv_observe_ws_bytes", "gkv_observe_mass", "gkv_query_norms", "gkv_allocate_levels", "gkv_layers_step",
-    "gkv_cache_changed",
+    "gkv_cache_changed", "gkv_graded_decode_attn_noalloc", "gkv_noalloc_scratch_bytes",
 ]
 
 
@@ -509,6 +511,18 @@ class GradedCache:
         return out
 
     decode = graded_decode_attn
+
+    def graded_decode_attn_noalloc(self, q, pages=None, out=None):
+        """gkv_graded_decode_attn_noalloc: the same read with the library's own device
+        scratch array as workspace (no workspace argument; out must be given by a
+        caller that cannot allocate)."""
+        q = _as_bits(q, self.device)
+        topk = int(pages.shape[-1]) if pages is not None else 0
+        if out is None:
+            out = torch.empty((self.B, self.Hq, D), dtype=torch.float32, device=self.device)
+        _check(_attn_noalloc(_dptr(q), ctypes.byref(self.c), _dptr(pages), topk, _dptr(out), _stream()),
+               "graded_decode_attn_noalloc")
+        return out
 
     def decode_bound(self, q, out=None, bound=None):
         """Dense decode plus the attention error certificate per query head:

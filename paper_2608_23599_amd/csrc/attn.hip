@@ -41,6 +41,8 @@
 // once per block: O += s_d * (acc - off * sum_t p_t) + z_d * sum_t p_t.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "gkv_internal.h"
 
 // the asynchronous copies set M0 themselves (see dma16)
@@ -2108,3 +2110,42 @@ extern "C" gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache 
   return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP;
 }
 
+// ---------------------------------------------------------------- no-allocation entry point
+// For callers that cannot allocate (graph capture, fixed serving loops): the
+// workspace is a file-scope device array that each GPU holds for the life of the
+// process.  Host code never passes `scratch` itself (in host code its name stands for
+// a host-side symbol, not a device address); the device address comes from
+// hipGetSymbolAddress, taken once per device with that device current.
+constexpr int64_t kScratchBytes = 32ll << 20;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+static std::mutex g_scratch_mu;
+static void *g_scratch_ptr[64];
+
+static gkv_status scratch_address(void **ptr) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return GKV_E_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return GKV_E_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return GKV_OK;
+}
+
+extern "C" int64_t gkv_noalloc_scratch_bytes() { return kScratchBytes; }
+
+extern "C" gkv_status gkv_graded_decode_attn_noalloc(const uint16_t *q, const gkv_cache *c, const int32_t *pages,
+                                                     int32_t topk, float *out, void *stream) {
+  if (!q || !out) return GKV_E_ARG;
+  const gkv_status st = gkv_validate_cache(c);
+  if (st) return st;
+  if (pages && topk <= 0) return GKV_E_ARG;
+  if (attn_layout(c, pages ? topk : 0).total > kScratchBytes) return GKV_E_WORKSPACE;  // before any HIP call
+  void *ws = nullptr;
+  const gkv_status sa = scratch_address(&ws);
+  if (sa) return sa;
+  return gkv_graded_decode_attn(q, c, pages, topk, out, ws, kScratchBytes, stream);
+}
