@@ -381,15 +381,17 @@ struct Pipe {
   __device__ __forceinline__ void fetch(const uint8_t *src, uint32_t lds, uint32_t c) {
     if (lane < 32) dma16(src + (size_t)c * 512 + 16 * lane, lds + (c & 1) * 512);
   }
-  __device__ __forceinline__ void start(int ln) {
+  // local: the lists (at most one chunk each) were written into the chunk buffers by
+  // this wavefront, and nothing is fetched
+  __device__ __forceinline__ void start(int ln, bool local) {
     lane = ln;
     issued = pk = ck = rel = ik = 0;
     ufetch = ifetch = 0;
-    if (nunits) {
+    if (nunits && !local) {
       fetch(usrc, ulds, 0);
       ufetch = ++issued;
     }
-    if (nitems) {
+    if (nitems && !local) {
       fetch(isrc, ilds, 0);
       ifetch = ++issued;
     }
@@ -1147,6 +1149,11 @@ __device__ __forceinline__ bool mean_run(const AttnParams &p, State &st, const u
   return true;
 }
 
+// Compressed-Quest reads take no plan: each wavefront writes its own item and unit
+// lists (defined with the plan code below).
+__device__ __forceinline__ uint2 quest_lists(const AttnParams &p, int64_t u, int w, int W, int lane,
+                                             ItemDesc *items, UnitDesc *units);
+
 template <bool PACK, bool CERT, bool VTOK>
 __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   extern __shared__ __align__(16) uint8_t smem[];
@@ -1191,11 +1198,6 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
     st.es = __builtin_sqrtf(qq) * p.sl2;  // sl2 = log2(e) / sqrt(D)
   }
 
-  // this wavefront's items and units, from the plan
-  const int32_t *isp = p.split + u * (int64_t)(2 * (W + 1)), *usp = isp + (W + 1);
-  const uint32_t i0 = (uint32_t)uni(isp[w]), i1 = (uint32_t)uni(isp[w + 1]);
-  const uint32_t u0 = (uint32_t)uni(usp[w]), u1 = (uint32_t)uni(usp[w + 1]);
-
   // ---------------- pipelined item loop
   Pipe pp;
   uint8_t *wl = smem + wave * kWaveLds;
@@ -1206,13 +1208,26 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   pp.ring_base = (uint32_t)uni((int32_t)(uintptr_t)pp.ring);
   pp.ulds = (uint32_t)uni((int32_t)(uintptr_t)pp.uchunk);
   pp.ilds = (uint32_t)uni((int32_t)(uintptr_t)pp.ichunk);
-  pp.isrc = p.plan + (u * p.icap + i0) * (int64_t)sizeof(ItemDesc);
-  pp.usrc = p.units + (u * p.ucap + u0) * (int64_t)sizeof(UnitDesc);
-  pp.nitems = i1 - i0;
-  pp.nunits = u1 - u0;
   pp.cert = CERT ? p.cert + u * p.nblk_cap * 4 : nullptr;
   pp.blk = 0xFFFFu;
-  pp.start(lane);
+  if (!CERT && p.pages) {
+    // Compressed-Quest: this wavefront's share of the read pages, listed in LDS here
+    const uint2 n = quest_lists(p, u, w, W, lane, (ItemDesc *)pp.ichunk, (UnitDesc *)pp.uchunk);
+    pp.isrc = pp.usrc = nullptr;
+    pp.nitems = (uint32_t)uni((int32_t)n.x);
+    pp.nunits = (uint32_t)uni((int32_t)n.y);
+    pp.start(lane, true);
+  } else {
+    // this wavefront's items and units, from the plan
+    const int32_t *isp = p.split + u * (int64_t)(2 * (W + 1)), *usp = isp + (W + 1);
+    const uint32_t i0 = (uint32_t)uni(isp[w]), i1 = (uint32_t)uni(isp[w + 1]);
+    const uint32_t u0 = (uint32_t)uni(usp[w]), u1 = (uint32_t)uni(usp[w + 1]);
+    pp.isrc = p.plan + (u * p.icap + i0) * (int64_t)sizeof(ItemDesc);
+    pp.usrc = p.units + (u * p.ucap + u0) * (int64_t)sizeof(UnitDesc);
+    pp.nitems = i1 - i0;
+    pp.nunits = u1 - u0;
+    pp.start(lane, false);
+  }
   // Items are processed in runs of one level, each run in a loop specialised for
   // that level (the constants of one level's path are then live only in its loop).
   uint32_t meta;
@@ -1334,13 +1349,13 @@ __global__ void __launch_bounds__(D) merge_kernel(const float *part, float *out,
 }
 
 // ---------------------------------------------------------------- plan
-// One workgroup per (b, KV head).  A visit is one block and the tokens of it that
-// are read: all valid tokens of a dense read minus the residual rows, or the
-// selected pages of a Compressed-Quest read.  The plan kernel describes the visits,
-// splits them over the W wavefronts by a balance cost (visit v goes to the
-// wavefront that owns the midpoint of its cost interval), and expands every visit
-// into its pipeline items, written in order; each wavefront's items are the items
-// of its visits.
+// Dense reads: up to 8 workgroups per (b, KV head).  A visit is one block and the
+// tokens of it that are read: all valid tokens minus the residual rows.  The plan
+// kernel describes the visits, splits them over the W wavefronts by a balance cost
+// (visit v goes to the wavefront that owns the midpoint of its cost interval), and
+// expands every visit into its pipeline items, written in order; each wavefront's
+// items are the items of its visits.  Compressed-Quest reads have no plan kernel:
+// their wavefronts list their own pages (quest_lists).
 constexpr int kPlanThreads = 1024;
 
 struct VisitDesc {
@@ -1529,6 +1544,68 @@ __device__ __forceinline__ void visit_items(const VisitDesc &v, ItemDesc *items,
     }
     first = false;
   }
+}
+
+// Read pages per wavefront of a Compressed-Quest read: at most 8 tiles, so that a
+// wavefront's items and units fit one 32-entry descriptor chunk each (a tile costs at
+// most 3 units: an int8 page alone in its block takes its scale/zero unit and a K and
+// a V unit).
+__host__ __device__ __forceinline__ int quest_pages_per_wave(int page) { return 8 / (page / 16); }
+
+// Wavefront w of W of (b, KV head) u in a Compressed-Quest read: the read pages are
+// the leading valid selected pages (ascending; the list ends at its first -1 or
+// out-of-range entry) and then the current page (T - 1) / page; the wavefront takes
+// pages [w n / W, (w + 1) n / W) of those n, joins consecutive pages of one block
+// into one visit, and writes the visits' items and units (as the dense plan expands
+// its visits) into `items` and `units` (LDS).  Returns (items, units).
+__device__ __forceinline__ uint2 quest_lists(const AttnParams &p, int64_t u, int w, int W, int lane,
+                                             ItemDesc *items, UnitDesc *units) {
+  const int32_t *pg = p.pages + u * p.topk;
+  const int64_t cur = (p.T - 1) / p.page;
+  int cnt = p.topk;
+  for (int base = 0; base < p.topk; base += 64) {
+    const int i = base + lane;
+    const uint64_t bad = __ballot(i < p.topk && (pg[i] < 0 || pg[i] >= cur));
+    if (bad) {
+      cnt = base + __builtin_ctzll(bad);
+      break;
+    }
+  }
+  const int n = cnt + 1;
+  const int i0 = (int)(((int64_t)w * n) / W), i1 = (int)(((int64_t)(w + 1) * n) / W);
+  // page pg lies in block pg >> pshift and covers tiles page_tiles(pg) of it
+  const int pshift = p.page == 16 ? 2 : (p.page == 32 ? 1 : 0), tpp = p.page / 16;
+  auto page_at = [&](int i) { return (int64_t)uni(i < cnt ? pg[i] : (int32_t)cur); };
+  auto page_tiles = [&](int64_t q) { return ((1u << tpp) - 1) << ((q & ((1 << pshift) - 1)) * tpp); };
+  const int8_t *lvl = p.level + u * p.nblk_cap;
+  const int64_t *ko = p.koff + u * p.nblk_cap, *vo = p.voff + u * p.nblk_cap;
+  uint32_t ni = 0, nu = 0;
+  for (int i = i0; i < i1;) {
+    const int64_t q0 = page_at(i), blk = q0 >> pshift;
+    uint32_t tl = page_tiles(q0);
+    int j = i + 1;
+    for (; j < i1; ++j) {
+      const int64_t qj = page_at(j);
+      if ((qj >> pshift) != blk) break;
+      tl |= page_tiles(qj);
+    }
+    VisitDesc d;
+    d.level = (int16_t)uni(lvl[blk]);
+    d.blk = 0xFFFF;
+    d.kp = (uint64_t)(uintptr_t)(p.arena + uni64(ko[blk]));
+    d.vp = (uint64_t)(uintptr_t)(p.arena + uni64(vo[blk]));
+    uint64_t va = 0;
+    for (int t = 0; t < 4; ++t)
+      if (tl & (1u << t)) va |= 0xFFFFull << (16 * t);
+    d.valid = va & token_mask(p.T - blk * P);
+    d.cost = 0;
+    const uint32_t c = visit_counts(d.level, d.valid);
+    if (lane == 0) visit_items(d, items + ni, units + nu);
+    ni += c & 7u;
+    nu += c >> 3;
+    i = j;
+  }
+  return make_uint2(ni, nu);
 }
 
 // Tokens read from block b of a dense read (residual rows excluded).
@@ -1722,15 +1799,12 @@ __device__ __forceinline__ void plan_dense_regs(const AttnParams &p, int64_t u, 
     if (v0 + j < v1) place_visit(o, dv[j], v0 + j, nvis, e, prev);
 }
 
-constexpr int kPlanLdsVisits = kPlanThreads;  // Compressed-Quest visits kept in LDS
-
 __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
   __shared__ uint64_t sh[3 * kPlanThreads / 64];  // block_scan: 6 x 16 32-bit words
   __shared__ uint32_t lastc[kPlanThreads];
-  __shared__ VisitDesc lds_desc[kPlanLdsVisits];
-  __shared__ uint32_t joins[32768 / 32];  // one-centroid run bits of a dense plan (nblk < 32768)
-  __shared__ int s_cnt, s_same;
-  if (p.cacheable) {  // a dense read whose plan the workspace may already hold
+  __shared__ uint32_t joins[32768 / 32];  // one-centroid run bits (nblk < 32768)
+  __shared__ int s_same;
+  if (p.cacheable) {  // the workspace may already hold this plan
     if (threadIdx.x == 0) {
       int same = 1;
 #pragma unroll
@@ -1753,124 +1827,25 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
   o.W = W;
   o.W1 = p.fast * kWaves;
   const int64_t nblk = (p.T + P - 1) / P;
-  if (!p.pages) {
-    // dense: blocks 0..nblk-1, then the residual rows as exact pseudo-blocks; each
-    // thread describes a contiguous run of visits
-    const int64_t nvis = nblk + (p.nres + P - 1) / P;
-    const int64_t per = (nvis + kPlanThreads - 1) / kPlanThreads;
-    if (per <= kPlanRegs) {
-      plan_dense_regs(p, u, nblk, nvis, o, sh, lastc, joins);
-      return;
-    }
-    const int64_t v0 = threadIdx.x * per, v1 = v0 + per < nvis ? v0 + per : nvis;
-    bool any_mean = false;
-    for (int64_t v = v0; v < v1 && v < nblk; ++v) any_mean |= p.level[u * p.nblk_cap + v] == GKV_MEAN;
-    const uint32_t *jn = build_joins(p, u, nblk, v0, v1, __syncthreads_or(any_mean), joins);
-    uint64_t mine = 0;
-    for (int64_t v = v0; v < v1; ++v) mine += scan_key(dense_visit(p, u, nblk, v, jn).cost);
-    uint64_t e = block_scan(mine, sh, o.total) - mine;
-    o.scale = owner_scale(o.W, o.W1, key_cost(o.total));
-    if (v0 >= v1 || !own_slice()) return;
-    int prev = prev_owner(o, v0, e, v0 > 0 ? dense_visit(p, u, nblk, v0 - 1, jn).cost : 0u);
-    for (int64_t v = v0; v < v1; ++v) place_visit(o, dense_visit(p, u, nblk, v, jn), v, nvis, e, prev);
-    return;
-  }
-  if (blockIdx.y) return;  // one workgroup per (b, KV head)
-  // Compressed-Quest: the leading valid ranked pages (ascending) and the current
-  // page; consecutive pages of one block form one visit
-  const int8_t *lvl = p.level + u * p.nblk_cap;
-  const int64_t *ko = p.koff + u * p.nblk_cap, *vo = p.voff + u * p.nblk_cap;
-  VisitDesc *desc = p.topk + 1 <= kPlanLdsVisits ? lds_desc : (VisitDesc *)p.visits + u * p.vcap;
-  const int32_t *pg = p.pages + u * p.topk;
-  // page pg lies in block pg >> pshift and covers tiles page_tiles(pg) of it
-  const int pshift = p.page == 16 ? 2 : (p.page == 32 ? 1 : 0), tpp = p.page / 16;
-  auto page_tiles = [&](int64_t pg) { return ((1u << tpp) - 1) << ((pg & ((1 << pshift) - 1)) * tpp); };
-  const int64_t cur = (p.T - 1) / p.page;
-  auto make_visit = [&](int64_t blk, uint32_t tl) {
-    VisitDesc d;
-    d.level = lvl[blk];
-    d.blk = 0xFFFF;
-    d.kp = (uint64_t)(uintptr_t)(p.arena + ko[blk]);
-    d.vp = (uint64_t)(uintptr_t)(p.arena + vo[blk]);
-    uint64_t va = 0;
-    for (int t = 0; t < 4; ++t)
-      if (tl & (1u << t)) va |= 0xFFFFull << (16 * t);
-    d.valid = va & token_mask(p.T - blk * P);
-    d.cost = balance_cost(d.level, d.valid) | (visit_counts(d.level, d.valid) << 24);
-    return d;
-  };
-  if (threadIdx.x == 0) s_cnt = p.topk;
-  __syncthreads();
-  uint64_t vbase = 0;
-  if (p.topk + 1 <= kPlanThreads) {
-    // the pages go to LDS once (lastc holds them); page i is thread i's
-    int32_t *spg = (int32_t *)lastc;
-    const int i = threadIdx.x;
-    if (i < p.topk) {
-      const int32_t v = pg[i];
-      spg[i] = v;
-      if (v < 0 || v >= cur) atomicMin(&s_cnt, i);
-    }
-    __syncthreads();
-    const int cnt = s_cnt, n = cnt + 1;
-    if (i == 0) spg[cnt] = (int32_t)cur;  // the current page is always read
-    __syncthreads();
-    const int64_t blk = i < n ? spg[i] >> pshift : -1;
-    const bool start = i < n && (i == 0 || (spg[i - 1] >> pshift) != blk);
-    uint64_t tot;
-    const uint64_t incl = block_scan(start ? 1 : 0, sh, tot);
-    if (start) {
-      uint32_t tl = 0;
-      for (int j = i; j < n && (spg[j] >> pshift) == blk; ++j) tl |= page_tiles(spg[j]);
-      desc[incl - 1] = make_visit(blk, tl);
-    }
-    vbase = tot;
-  } else {
-    for (int i = threadIdx.x; i < p.topk; i += kPlanThreads)
-      if (pg[i] < 0 || pg[i] >= cur) atomicMin(&s_cnt, i);
-    __syncthreads();
-    const int cnt = s_cnt;
-    const int n = cnt + 1;
-    for (int base = 0; base < n; base += kPlanThreads) {
-      const int i = base + threadIdx.x;
-      int64_t blk = -1;
-      bool start = false;
-      if (i < n) {
-        blk = (i < cnt ? pg[i] : cur) >> pshift;
-        start = i == 0 || ((i - 1 < cnt ? pg[i - 1] : cur) >> pshift) != blk;
-      }
-      uint64_t tot;
-      const uint64_t incl = block_scan(start ? 1 : 0, sh, tot);
-      if (start) {
-        uint32_t tl = 0;
-        for (int j = i; j < n; ++j) {
-          const int64_t pj = j < cnt ? pg[j] : cur;
-          if ((pj >> pshift) != blk) break;
-          tl |= page_tiles(pj);
-        }
-        desc[vbase + incl - 1] = make_visit(blk, tl);
-      }
-      vbase += tot;
-    }
-  }
-  const int64_t nvis = (int64_t)vbase;
-  __syncthreads();
-  if (nvis == 0) {
-    for (int ww = threadIdx.x; ww <= W; ww += kPlanThreads) o.isplit[ww] = o.usplit[ww] = 0;
-    return;
-  }
-  // prefix keys of each thread's run of visits, then the owner, first item and
-  // first unit of every visit
+  // blocks 0..nblk-1, then the residual rows as exact pseudo-blocks; each thread
+  // describes a contiguous run of visits
+  const int64_t nvis = nblk + (p.nres + P - 1) / P;
   const int64_t per = (nvis + kPlanThreads - 1) / kPlanThreads;
+  if (per <= kPlanRegs) {
+    plan_dense_regs(p, u, nblk, nvis, o, sh, lastc, joins);
+    return;
+  }
   const int64_t v0 = threadIdx.x * per, v1 = v0 + per < nvis ? v0 + per : nvis;
+  bool any_mean = false;
+  for (int64_t v = v0; v < v1 && v < nblk; ++v) any_mean |= p.level[u * p.nblk_cap + v] == GKV_MEAN;
+  const uint32_t *jn = build_joins(p, u, nblk, v0, v1, __syncthreads_or(any_mean), joins);
   uint64_t mine = 0;
-  for (int64_t v = v0; v < v1; ++v) mine += scan_key(desc[v].cost);
+  for (int64_t v = v0; v < v1; ++v) mine += scan_key(dense_visit(p, u, nblk, v, jn).cost);
   uint64_t e = block_scan(mine, sh, o.total) - mine;
   o.scale = owner_scale(o.W, o.W1, key_cost(o.total));
-  if (v0 < v1) {
-    int prev = prev_owner(o, v0, e, v0 > 0 ? desc[v0 - 1].cost : 0u);
-    for (int64_t v = v0; v < v1; ++v) place_visit(o, desc[v], v, nvis, e, prev);
-  }
+  if (v0 >= v1 || !own_slice()) return;
+  int prev = prev_owner(o, v0, e, v0 > 0 ? dense_visit(p, u, nblk, v0 - 1, jn).cost : 0u);
+  for (int64_t v = v0; v < v1; ++v) place_visit(o, dense_visit(p, u, nblk, v, jn), v, nvis, e, prev);
 }
 
 }  // namespace
@@ -1882,11 +1857,14 @@ static int attn_nsplit(const gkv_cache *c, int32_t topk, int64_t T) {
   const int64_t units = (int64_t)c->B * c->Hkv;
   int64_t waves;
   if (topk > 0) {
-    // one visit per wavefront while the chip holds them (2048 wavefronts over all
-    // (b, KV head)); at least one per four visits
+    // one read page per wavefront while the chip holds them (2048 wavefronts over all
+    // (b, KV head)); never more pages per wavefront than its descriptor chunk holds
     waves = topk + 1;
-    const int64_t room = 2048 / units, least = (topk + 1 + 3) / 4;
+    const int ppw = quest_pages_per_wave(c->page ? c->page : 16);
+    const int64_t room = 2048 / units, least = (topk + 1 + ppw - 1) / ppw;
     if (waves > room) waves = room > least ? room : least;
+    if (waves > kMaxWaves) waves = kMaxWaves;  // still >= least (checked on the host)
+    return (int)((waves + kWaves - 1) / kWaves);
   } else {
     const int64_t nvis = (T + P - 1) / P + (c->nres_cap + P - 1) / P;
     waves = 2048 / units;
@@ -1934,7 +1912,8 @@ static AttnLayout attn_layout(const gkv_cache *c, int32_t topk) {
   const int64_t units = (int64_t)c->B * c->Hkv;
   const int G = c->Hq / c->Hkv;
   L.ncap = attn_nsplit(c, topk, (int64_t)c->nblk_cap * P);
-  L.vcap = topk > 0 ? (int64_t)topk + 1 : (int64_t)c->nblk_cap + (c->nres_cap + P - 1) / P;
+  // a dense plan's lists; Compressed-Quest reads keep theirs in LDS
+  L.vcap = topk > 0 ? 0 : (int64_t)c->nblk_cap + (c->nres_cap + P - 1) / P;
   L.icap = 4 * L.vcap;  // at most 4 items per visit
   L.ucap = 8 * L.vcap;  // at most 8 units per visit (an exact block)
   L.part = 256;  // the plan tag (kTagWords words) comes first
@@ -1963,8 +1942,12 @@ static gkv_status attn_setup(const uint16_t *q, const gkv_cache *c, const int32_
   } else {
     topk = 0;
   }
+  if (topk > 0) {  // the wavefronts that share the read pages, at most kMaxWaves
+    const int ppw = quest_pages_per_wave(c->page);
+    if ((topk + 1 + ppw - 1) / ppw > kMaxWaves) return GKV_E_UNSUPPORTED;
+  }
   const AttnLayout L = attn_layout(c, topk);
-  if (L.vcap > 32767) return GKV_E_UNSUPPORTED;  // the plan's packed prefix sums
+  if (L.vcap > 32767) return GKV_E_UNSUPPORTED;  // the dense plan's packed prefix sums
   if (ws_bytes < L.total) return GKV_E_WORKSPACE;
   p.q = q;
   p.level = c->level;
@@ -2016,12 +1999,10 @@ static gkv_status attn_setup(const uint16_t *q, const gkv_cache *c, const int32_
 }
 
 static void launch_plan(const AttnParams &p, const gkv_cache *c, hipStream_t s) {
-  // dense reads: one workgroup per 256 visits of a (b, KV head), at most 8
-  int slices = 1;
-  if (!p.pages) {
-    const int64_t nvis = (p.T + P - 1) / P + (p.nres + P - 1) / P;
-    slices = (int)(nvis / 256 < 1 ? 1 : (nvis / 256 > 8 ? 8 : nvis / 256));
-  }
+  if (p.pages) return;  // Compressed-Quest reads list their pages in the attention kernel
+  // one workgroup per 256 visits of a (b, KV head), at most 8
+  const int64_t nvis = (p.T + P - 1) / P + (p.nres + P - 1) / P;
+  const int slices = (int)(nvis / 256 < 1 ? 1 : (nvis / 256 > 8 ? 8 : nvis / 256));
   hipLaunchKernelGGL(plan_kernel, dim3(c->B * c->Hkv, slices), dim3(kPlanThreads), 0, s, p);
 }
 static void launch_partials(const AttnParams &p, const gkv_cache *c, hipStream_t s) {
