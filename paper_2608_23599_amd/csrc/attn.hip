@@ -1172,33 +1172,15 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
     for (int i = 0; i < kTagWords; ++i) p.tag[i] = p.key[i];
   }
 
-  // the group's queries (rows of absent heads are zero)
+  // the group's queries (rows of absent heads are zero): one 16-byte piece per thread,
+  // loaded here and stored to LDS once the wavefront's lists are set up, so that the
+  // loads of both are in flight together
+  static_assert(16 * (D / 8) == kThreads, "one query piece per thread");
   uint8_t *qs = smem + kWaves * kWaveLds;
-  for (int i = threadIdx.x; i < 16 * (D / 8); i += kThreads) {
-    const int g = i / (D / 8), c8 = (i % (D / 8)) * 8;
-    const uint4 v = g < p.G ? *(const uint4 *)(p.q + (u * p.G + g) * D + c8) : make_uint4(0, 0, 0, 0);
-    *(uint4 *)(qs + g * kQRow + c8 * 2) = v;
-  }
-  __syncthreads();
-  State st;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) st.O[j] = f4{0, 0, 0, 0};
-  st.m = kNegInf;
-  st.l = 0.f;
-  st.c1 = st.c2 = st.c3 = 0.f;
-  st.es = 0.f;
-  if (CERT) {  // ||q|| of this lane's head, for eps_b = ||q|| kerr_b / sqrt(D)
-    float qq = 0.f;
-    for (int c8 = 0; c8 < D; c8 += 8) {
-      U8 t;
-      t.v = lds16(qs + qrow<PACK>(lane) * kQRow + c8 * 2);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) qq = fmaf((float)t.h[e], (float)t.h[e], qq);
-    }
-    st.es = __builtin_sqrtf(qq) * p.sl2;  // sl2 = log2(e) / sqrt(D)
-  }
+  const int qg = threadIdx.x / (D / 8), qc8 = (threadIdx.x % (D / 8)) * 8;
+  const uint4 qv = qg < p.G ? *(const uint4 *)(p.q + (u * p.G + qg) * D + qc8) : make_uint4(0, 0, 0, 0);
 
-  // ---------------- pipelined item loop
+  // ---------------- this wavefront's item and unit lists
   Pipe pp;
   uint8_t *wl = smem + wave * kWaveLds;
   pp.ring = wl;
@@ -1228,6 +1210,27 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
     pp.nunits = u1 - u0;
     pp.start(lane, false);
   }
+  *(uint4 *)(qs + qg * kQRow + qc8 * 2) = qv;
+  __syncthreads();
+  State st;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) st.O[j] = f4{0, 0, 0, 0};
+  st.m = kNegInf;
+  st.l = 0.f;
+  st.c1 = st.c2 = st.c3 = 0.f;
+  st.es = 0.f;
+  if (CERT) {  // ||q|| of this lane's head, for eps_b = ||q|| kerr_b / sqrt(D)
+    float qq = 0.f;
+    for (int c8 = 0; c8 < D; c8 += 8) {
+      U8 t;
+      t.v = lds16(qs + qrow<PACK>(lane) * kQRow + c8 * 2);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qq = fmaf((float)t.h[e], (float)t.h[e], qq);
+    }
+    st.es = __builtin_sqrtf(qq) * p.sl2;  // sl2 = log2(e) / sqrt(D)
+  }
+
+  // ---------------- pipelined item loop
   // Items are processed in runs of one level, each run in a loop specialised for
   // that level (the constants of one level's path are then live only in its loop).
   uint32_t meta;

@@ -114,9 +114,10 @@ __global__ void __launch_bounds__(256) quest_score_kernel(const double *__restri
 // (`idx`, null for the first), and the last stage, a single slice, writes the
 // result.
 //
-// Radix select of the threshold key (the need-th largest), 8 bits per pass, with
-// one histogram per wavefront (so that LDS atomics contend only inside a
-// wavefront); then an ordered compaction: selected = key > threshold, or key ==
+// Radix select of the threshold key (the need-th largest), up to 8 bits per pass,
+// with one LDS histogram that every thread adds to (a wavefront's lanes rarely share
+// a digit, so its atomics seldom serialise, and the bucket counts need no reduction
+// over wavefronts); then an ordered compaction: selected = key > threshold, or key ==
 // threshold among the first `eq_take` such keys by index.  With KPT > 0 (n <= KPT *
 // threads) thread t holds keys t * KPT + j (j < KPT) in registers; with KPT == 0
 // keys are streamed from memory in 1024-key chunks.
@@ -127,7 +128,7 @@ constexpr int kSelKPT = 8;  // keys per thread held in registers (n <= 8192)
 constexpr int kSelRank = 16;  // candidates ranked directly instead of another radix pass (<= 64)
 
 struct SelShared {
-  uint32_t hist[kSelWaves][256];
+  uint32_t hist[256];
   uint64_t prefix, pmask;
   int64_t remaining;
   int64_t wsum[kSelWaves][2];
@@ -208,7 +209,7 @@ __device__ __forceinline__ void scan2(SelShared &sh, int64_t &a, int64_t &b, int
 template <int KPT>
 __device__ __forceinline__ void small_candidates(SelShared &sh, const uint64_t *kr, const uint64_t *key, int64_t n) {
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  uint64_t *ckey = (uint64_t *)&sh.hist[0][0];
+  uint64_t *ckey = (uint64_t *)&sh.hist[0];
   int32_t *cidx = (int32_t *)(ckey + 64);
   uint32_t *cnt = (uint32_t *)(cidx + 64);
   const uint64_t pre = sh.prefix, pm = sh.pmask;
@@ -327,7 +328,7 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
     sh.remaining = need;
     sh.base[0] = hb;
   }
-  for (int i = tid; i < kSelWaves * 256; i += kSelThreads) (&sh.hist[0][0])[i] = 0;
+  for (int i = tid; i < 256; i += kSelThreads) sh.hist[i] = 0;
   __syncthreads();
   // digits of up to 8 bits from the highest differing bit down (the first digit
   // spreads the keys over all its buckets)
@@ -339,12 +340,12 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
 #pragma unroll
       for (int j = 0; j < KPT; ++j) {
         const int64_t i = (int64_t)tid * KPT + j;
-        if (i < n && (kr[j] & pm) == pre) atomicAdd(&sh.hist[wv][(kr[j] >> shift) & dmask], 1u);
+        if (i < n && (kr[j] & pm) == pre) atomicAdd(&sh.hist[(kr[j] >> shift) & dmask], 1u);
       }
     } else {
       for (int64_t i = tid; i < n; i += kSelThreads) {
         const uint64_t kv = key[i];
-        if ((kv & pm) == pre) atomicAdd(&sh.hist[wv][(kv >> shift) & dmask], 1u);
+        if ((kv & pm) == pre) atomicAdd(&sh.hist[(kv >> shift) & dmask], 1u);
       }
     }
     __syncthreads();
@@ -355,11 +356,8 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
       uint32_t c[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        c[e] = 0;
-        for (int q = 0; q < kSelWaves; ++q) {
-          c[e] += sh.hist[q][4 * lane + e];
-          sh.hist[q][4 * lane + e] = 0;  // cleared for the next pass
-        }
+        c[e] = sh.hist[4 * lane + e];
+        sh.hist[4 * lane + e] = 0;  // cleared for the next pass
       }
       const uint32_t mine = c[0] + c[1] + c[2] + c[3];
       const uint32_t pref = wave_scan(mine);  // sum over lanes <= this lane
