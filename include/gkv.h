@@ -127,6 +127,10 @@ typedef struct gkv_cache {
   uint8_t *res_rows;         /* device [B][Hkv][ceil(nres_cap/64)] pseudo-blocks      */
   uint64_t *res_mask;        /* device [B][Hkv][nblk_cap] bit t%64 set = token t is
                                 read from the residual instead of its block           */
+  int32_t *res_off;          /* device [B][Hkv][nblk_cap + 1]: residual rows of the
+                                blocks before each block (written by
+                                gkv_rd_residual_select; row of token t of block blk =
+                                res_off[blk] + popcount of the block's mask below t)  */
   float *cert;               /* device [B][Hkv][nblk_cap][4] or NULL: per block
                                 {kerr, verr, vmax, 0} for the decode-time attention
                                 error certificate (section 3.6): kerr = max_t
@@ -196,7 +200,12 @@ void gkv_pool_destroy(gkv_pool *p);
 typedef struct gkv_rates {
   int64_t resident_bits, read_bits, values;
 } gkv_rates;
-gkv_status gkv_account(const gkv_cache *c, const int32_t *pages_host, int32_t topk, gkv_rates *out);
+/* A Compressed-Quest read of a cache with residual rows also reads the rows of the
+ * residual tokens in its read set (2 * 128 * 16 + 32 bits each) and the 64-bit
+ * override mask of every block it touches; res_idx_host = [B][Hkv][nres_cap] host
+ * copy of the residual tokens (required then, ignored otherwise). */
+gkv_status gkv_account(const gkv_cache *c, const int32_t *pages_host, int32_t topk, const int32_t *res_idx_host,
+                       gkv_rates *out);
 
 /* Decode one record (host copy) to codes / values, for inspection and tests.
  * values_host: [64][128] fp64 reconstruction (token-major); codes_host (optional,
@@ -270,11 +279,11 @@ gkv_status gkv_quest_select(const uint16_t *q, const gkv_cache *c, int32_t topk,
  * query head g of every sequence b, out[b][g][:] = sum_j softmax_j(q.k_j/sqrt(128)) v_j
  * over the read set -- all tokens < T (pages == NULL) or the selected pages
  * [B][Hkv][topk] plus the current page (section 3.5).  Residual rows override their
- * tokens' graded entries (dense reads only).  q: [B][Hq][128] fp16;
+ * tokens' graded entries in both reads (section 3.4).  q: [B][Hq][128] fp16;
  * out: [B][Hq][128] fp32.  Pages may be 16, 32 or 64 tokens (a selected page reads
- * its tiles of one block).  GKV_E_UNSUPPORTED for pages with residual rows, or more
- * than 32767 visits per (b,h) (block capacity plus residual pseudo-blocks, or
- * topk + 1). */
+ * its tiles of one block).  GKV_E_UNSUPPORTED for more than 32767 visits per (b,h)
+ * in a dense read (block capacity plus residual pseudo-blocks) or more than 8192
+ * read tiles per (b,h) in a Compressed-Quest read (4096 with residual rows). */
 gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache *c, const int32_t *pages, int32_t topk,
                                   float *out, void *ws, int64_t ws_bytes, void *stream);
 /* Plan reuse.  The visit plan of a dense read depends only on the block tables, not

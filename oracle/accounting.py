@@ -19,7 +19,11 @@ centroids) once per block touched.
 
 The exact residual (section 3.4) costs, per kept token, 2 * D * 16 bits of
 exact key and value plus a 32-bit token index, and the cache keeps one 64-bit
-override mask per block while a residual exists.
+override mask per block while a residual exists.  A dense read reads all of it.
+A Compressed-Quest read of a cache with a residual (the paper prices the two
+separately; this is the reading used here) reads the residual rows of the tokens
+in its read set (2 * D * 16 + 32 bits each) and the override mask of every block
+it touches; the graded rows of those tokens are still counted with their pages.
 
 Values are normalised by B * Hkv * T * 2 * D (keys and values).  The newest
 block is always fully allocated, so a partial block counts whole.
@@ -75,13 +79,14 @@ RES_ROW_BITS = 2 * D * 16 + 32
 MASK_BITS = 64
 
 
-def unit_rates(levels, T, page=None, nres=0, pages=None, P=P, D=D):
+def unit_rates(levels, T, page=None, nres=0, pages=None, res_idx=None, P=P, D=D):
     """Bits for one (sequence, KV head) unit.
 
-    levels : per-block levels (index 0 oldest)
-    page   : Quest page size in tokens, or None when no boxes are kept
-    nres   : exact residual rows kept
-    pages  : selected page indices for one query (Quest read), or None (dense)
+    levels  : per-block levels (index 0 oldest)
+    page    : Quest page size in tokens, or None when no boxes are kept
+    nres    : exact residual rows kept
+    pages   : selected page indices for one query (Quest read), or None (dense)
+    res_idx : the residual rows' tokens (needed for a Quest read with nres > 0)
     Returns dict(resident_bits, read_bits, values).
     """
     nblk = len(levels)
@@ -99,6 +104,7 @@ def unit_rates(levels, T, page=None, nres=0, pages=None, P=P, D=D):
         cur = (int(T) - 1) // page
         read = boxes  # R_boxes: all stored summaries, as in the resident equation
         touched = set()
+        tokens = set()
         for p in sorted(set(int(x) for x in pages if x >= 0) | {cur}):
             t0 = p * page
             t1 = min(t0 + page, int(T))
@@ -106,9 +112,14 @@ def unit_rates(levels, T, page=None, nres=0, pages=None, P=P, D=D):
                 b = t // P
                 read += 2 * row_bits(levels[b], D)
                 touched.add(b)
+                tokens.add(t)
         for b in touched:
             read += 2 * block_overhead_bits(levels[b], D)
-        read += res
+        if nres:
+            if res_idx is None:
+                raise ValueError("a Compressed-Quest read with a residual needs the residual tokens")
+            read += sum(1 for t in set(int(x) for x in res_idx[:nres]) if t in tokens) * RES_ROW_BITS
+            read += len(touched) * MASK_BITS
     return dict(resident_bits=resident, read_bits=read, values=int(T) * 2 * D)
 
 

@@ -37,6 +37,7 @@ class CacheStruct(ctypes.Structure):
         ("level_host", _vp),
         ("page", _i32), ("npage_cap", _i64), ("boxes", _vp),
         ("nres", _i32), ("nres_cap", _i32), ("res_idx", _vp), ("res_rows", _vp), ("res_mask", _vp),
+        ("res_off", _vp),
         ("cert", _vp),
         ("v_per_token", _i32),
         ("version", ctypes.c_uint64),
@@ -65,7 +66,7 @@ _pool_alloc = _sig("gkv_pool_alloc", _i64, [_vp, _i32])
 _pool_free = _sig("gkv_pool_free", _i32, [_vp, _i32, _i64])
 _pool_used = _sig("gkv_pool_used", _i64, [_vp, _i32])
 _pool_destroy = _sig("gkv_pool_destroy", None, [_vp])
-_account = _sig("gkv_account", _i32, [_P(CacheStruct), _vp, _i32, _P(Rates)])
+_account = _sig("gkv_account", _i32, [_P(CacheStruct), _vp, _i32, _vp, _P(Rates)])
 _decode_record = _sig("gkv_decode_record", _i32, [_i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp])
 _f64_to_f16 = _sig("gkv_f64_to_f16", ctypes.c_uint16, [ctypes.c_double])
 _workspace_bytes = _sig("gkv_workspace_bytes", _i64, [_P(CacheStruct), _i32, _i32])
@@ -289,8 +290,9 @@ class GradedCache:
             self.res_idx = torch.zeros((B, Hkv, nres_cap), dtype=torch.int32, device=self.device)
             self.res_rows = torch.zeros((B, Hkv, nrb * 2 * 16384), dtype=torch.uint8, device=self.device)
             self.res_mask = torch.zeros((B, Hkv, nblk_cap), dtype=torch.int64, device=self.device)
+            self.res_off = torch.zeros((B, Hkv, nblk_cap + 1), dtype=torch.int32, device=self.device)
         else:
-            self.res_idx = self.res_rows = self.res_mask = None
+            self.res_idx = self.res_rows = self.res_mask = self.res_off = None
         # per-block certificate numbers {kerr, verr, vmax, 0}
         self.cert = torch.zeros((B, Hkv, nblk_cap, 4), dtype=torch.float32, device=self.device)
         self.c = CacheStruct()
@@ -316,6 +318,7 @@ class GradedCache:
         c.res_idx = self.res_idx.data_ptr() if self.nres_cap else None
         c.res_rows = self.res_rows.data_ptr() if self.nres_cap else None
         c.res_mask = self.res_mask.data_ptr() if self.nres_cap else None
+        c.res_off = self.res_off.data_ptr() if self.nres_cap else None
         c.cert = self.cert.data_ptr()
         c.v_per_token = int(self.v_per_token)
         _cache_changed(ctypes.byref(c))  # new tables: a fresh version stamp
@@ -325,7 +328,7 @@ class GradedCache:
         benchmarks that rotate identical caches; it cannot append or demote."""
         new = object.__new__(GradedCache)
         new.__dict__.update(self.__dict__)
-        for name in ("arena", "level", "koff", "voff", "boxes", "res_idx", "res_rows", "res_mask", "cert"):
+        for name in ("arena", "level", "koff", "voff", "boxes", "res_idx", "res_rows", "res_mask", "res_off", "cert"):
             t = getattr(self, name)
             setattr(new, name, t.clone() if t is not None else None)
         new.level_host = self.level_host.copy()
@@ -571,9 +574,13 @@ class GradedCache:
         r = Rates()
         if pages is not None:
             ph = np.ascontiguousarray(pages.cpu().numpy() if torch.is_tensor(pages) else pages, dtype=np.int32)
-            _check(_account(ctypes.byref(self.c), _np_ptr(ph), ph.shape[-1], ctypes.byref(r)), "account")
+            ri = None
+            if int(self.c.nres):  # a Compressed-Quest read also reads the residual rows in its read set
+                ri = np.ascontiguousarray(self.res_idx.cpu().numpy(), dtype=np.int32)
+            _check(_account(ctypes.byref(self.c), _np_ptr(ph), ph.shape[-1], _np_ptr(ri) if ri is not None else None,
+                            ctypes.byref(r)), "account")
         else:
-            _check(_account(ctypes.byref(self.c), None, 0, ctypes.byref(r)), "account")
+            _check(_account(ctypes.byref(self.c), None, 0, None, ctypes.byref(r)), "account")
         return dict(resident_bits=r.resident_bits, read_bits=r.read_bits, values=r.values,
                     resident_bpv=r.resident_bits / r.values, read_bpv=r.read_bits / r.values)
 

@@ -208,6 +208,7 @@ struct AttnParams {
   const int64_t *koff, *voff;
   const uint8_t *arena;
   const uint64_t *res_mask;
+  const int32_t *res_off;
   const uint8_t *res_rows;
   const int32_t *pages;
   uint8_t *visits;  // visit descriptors (plan kernel scratch), vcap per (b, KV head)
@@ -1553,7 +1554,12 @@ __device__ __forceinline__ void visit_items(const VisitDesc &v, ItemDesc *items,
 // wavefront's items and units fit one 32-entry descriptor chunk each (a tile costs at
 // most 3 units: an int8 page alone in its block takes its scale/zero unit and a K and
 // a V unit).
-__host__ __device__ __forceinline__ int quest_pages_per_wave(int page) { return 8 / (page / 16); }
+// With residual rows a page also brings the residual tiles holding its tokens' rows
+// (a 16-token page's rows span at most 2 tiles, 4 units), so a wavefront takes half as
+// many pages.
+__host__ __device__ __forceinline__ int quest_pages_per_wave(int page, bool residual) {
+  return (residual ? 4 : 8) / (page / 16);
+}
 
 // Wavefront w of W of (b, KV head) u in a Compressed-Quest read: the read pages are
 // the leading valid selected pages (ascending; the list ends at its first -1 or
@@ -1602,10 +1608,44 @@ __device__ __forceinline__ uint2 quest_lists(const AttnParams &p, int64_t u, int
       if (tl & (1u << t)) va |= 0xFFFFull << (16 * t);
     d.valid = va & token_mask(p.T - blk * P);
     d.cost = 0;
+    // residual rows override their tokens (section 3.4): the graded tiles skip them
+    // and the exact tiles of the residual that hold their rows are read instead
+    uint64_t bm = 0, rm = 0;
+    if (p.nres) {
+      bm = (uint64_t)uni64((int64_t)p.res_mask[u * p.nblk_cap + blk]);
+      rm = bm & d.valid;
+      d.valid &= ~bm;
+    }
     const uint32_t c = visit_counts(d.level, d.valid);
     if (lane == 0) visit_items(d, items + ni, units + nu);
     ni += c & 7u;
     nu += c >> 3;
+    if (rm) {
+      const int32_t r0 = uni(p.res_off[u * (p.nblk_cap + 1) + blk]);
+      auto row_of = [&](uint64_t t) { return r0 + __popcll(bm & ((1ull << t) - 1)); };
+      while (rm) {  // the read tokens' rows, ascending: one exact tile item per 16 rows
+        const int rt = row_of(__builtin_ctzll(rm)) >> 4;
+        uint32_t tv = 0;
+        while (rm) {
+          const int r = row_of(__builtin_ctzll(rm));
+          if ((r >> 4) != rt) break;
+          tv |= 1u << (r & 15);
+          rm &= rm - 1;
+        }
+        const uint64_t kp = (uint64_t)(uintptr_t)(p.res_rows + (u * p.nrb_cap + (rt >> 2)) * (2 * kExactBytes) +
+                                                  4096 * (rt & 3));
+        if (lane == 0) {
+          items[ni].meta = kExactTile | ((uint32_t)GKV_EXACT << 2) | (1u << 7) | (1u << 8) |
+                           ((1u << (rt & 3)) << 9) | (1u << 13) | (tv << 16);
+          items[ni].pad = 0xFFFF;
+          items[ni].valid = 0;
+          units[nu] = unit_desc(kp, 2048, kp + 2048, 2048);
+          units[nu + 1] = unit_desc(kp + kExactBytes, 2048, kp + kExactBytes + 2048, 2048);
+        }
+        ni += 1;
+        nu += 2;
+      }
+    }
     i = j;
   }
   return make_uint2(ni, nu);
@@ -1856,14 +1896,15 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
 // ---------------------------------------------------------------- C ABI
 // Workgroups per (b, KV head) for a call at context length T: enough wavefronts to
 // fill the chip (2048 over all (b, KV head)), at most one per visit.
-static int attn_nsplit(const gkv_cache *c, int32_t topk, int64_t T) {
+static int attn_nsplit(const gkv_cache *c, int32_t topk, int64_t T, bool layout) {
   const int64_t units = (int64_t)c->B * c->Hkv;
   int64_t waves;
   if (topk > 0) {
     // one read page per wavefront while the chip holds them (2048 wavefronts over all
     // (b, KV head)); never more pages per wavefront than its descriptor chunk holds
     waves = topk + 1;
-    const int ppw = quest_pages_per_wave(c->page ? c->page : 16);
+    // the workspace is sized for a cache that may get residual rows (more wavefronts)
+    const int ppw = quest_pages_per_wave(c->page ? c->page : 16, layout ? c->nres_cap > 0 : c->nres > 0);
     const int64_t room = 2048 / units, least = (topk + 1 + ppw - 1) / ppw;
     if (waves > room) waves = room > least ? room : least;
     if (waves > kMaxWaves) waves = kMaxWaves;  // still >= least (checked on the host)
@@ -1914,7 +1955,7 @@ static AttnLayout attn_layout(const gkv_cache *c, int32_t topk) {
   AttnLayout L;
   const int64_t units = (int64_t)c->B * c->Hkv;
   const int G = c->Hq / c->Hkv;
-  L.ncap = attn_nsplit(c, topk, (int64_t)c->nblk_cap * P);
+  L.ncap = attn_nsplit(c, topk, (int64_t)c->nblk_cap * P, true);
   // a dense plan's lists; Compressed-Quest reads keep theirs in LDS
   L.vcap = topk > 0 ? 0 : (int64_t)c->nblk_cap + (c->nres_cap + P - 1) / P;
   L.icap = 4 * L.vcap;  // at most 4 items per visit
@@ -1941,12 +1982,11 @@ static gkv_status attn_setup(const uint16_t *q, const gkv_cache *c, const int32_
   if (pages) {
     if (topk <= 0) return GKV_E_ARG;
     if (c->page != 16 && c->page != 32 && c->page != 64) return GKV_E_UNSUPPORTED;
-    if (c->nres) return GKV_E_UNSUPPORTED;
   } else {
     topk = 0;
   }
   if (topk > 0) {  // the wavefronts that share the read pages, at most kMaxWaves
-    const int ppw = quest_pages_per_wave(c->page);
+    const int ppw = quest_pages_per_wave(c->page, c->nres_cap > 0);
     if ((topk + 1 + ppw - 1) / ppw > kMaxWaves) return GKV_E_UNSUPPORTED;
   }
   const AttnLayout L = attn_layout(c, topk);
@@ -1958,6 +1998,7 @@ static gkv_status attn_setup(const uint16_t *q, const gkv_cache *c, const int32_
   p.voff = c->voff;
   p.arena = c->arena;
   p.res_mask = c->res_mask;
+  p.res_off = c->res_off;
   p.res_rows = c->res_rows;
   p.pages = pages;
   p.tag = (uint64_t *)ws;
@@ -1979,7 +2020,7 @@ static gkv_status attn_setup(const uint16_t *q, const gkv_cache *c, const int32_
   p.page = c->page ? c->page : 16;
   p.cert = c->cert;
   p.bound = nullptr;
-  p.nsplit = attn_nsplit(c, topk, c->T);
+  p.nsplit = attn_nsplit(c, topk, c->T, false);
   p.fast = attn_fast(p.nsplit, (int64_t)c->B * c->Hkv);
   p.sl2 = 1.4426950408889634f / sqrtf((float)D);
   // the key of the planned state: a dense plan depends on the tables (version stamp

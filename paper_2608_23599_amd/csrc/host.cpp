@@ -3,6 +3,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <atomic>
 #include <vector>
 
@@ -202,7 +203,7 @@ gkv_status gkv_validate_cache(const gkv_cache *c) {
     if (c->T / c->page > c->npage_cap) return GKV_E_SHAPE;
   }
   if (c->nres < 0 || c->nres > c->nres_cap) return GKV_E_SHAPE;
-  if (c->nres_cap > 0 && (!c->res_idx || !c->res_rows || !c->res_mask)) return GKV_E_ARG;
+  if (c->nres_cap > 0 && (!c->res_idx || !c->res_rows || !c->res_mask || !c->res_off)) return GKV_E_ARG;
   if (c->v_per_token != 0 && c->v_per_token != 1) return GKV_E_ARG;
   return GKV_OK;
 }
@@ -221,11 +222,13 @@ static int64_t overhead_bits(int level) {
   return 0;
 }
 
-extern "C" gkv_status gkv_account(const gkv_cache *c, const int32_t *pages, int32_t topk, gkv_rates *out) {
+extern "C" gkv_status gkv_account(const gkv_cache *c, const int32_t *pages, int32_t topk, const int32_t *res_idx,
+                                  gkv_rates *out) {
   gkv_status st = gkv_validate_cache(c);
   if (st) return st;
   if (!out) return GKV_E_ARG;
   if (pages && (!c->page || topk <= 0)) return GKV_E_ARG;
+  if (pages && c->nres && !res_idx) return GKV_E_ARG;
   const int64_t nblk = (c->T + P - 1) / P;
   const int64_t box_bits = 2 * D * 16;
   int64_t resident = 0, read = 0;
@@ -243,13 +246,15 @@ extern "C" gkv_status gkv_account(const gkv_cache *c, const int32_t *pages, int3
         continue;
       }
       const int64_t cur = (c->T - 1) / c->page;
-      int64_t r = boxes + res;
+      int64_t r = boxes;
       touched.assign(nblk, 0);
       const int32_t *pg = pages + ((int64_t)b * c->Hkv + h) * topk;
       std::vector<int64_t> list;
       for (int k = 0; k < topk; ++k)
         if (pg[k] >= 0 && pg[k] != cur) list.push_back(pg[k]);
       list.push_back(cur);
+      std::sort(list.begin(), list.end());  // a page listed twice is read once
+      list.erase(std::unique(list.begin(), list.end()), list.end());
       for (int64_t p : list) {
         const int64_t t0 = p * c->page, t1 = t0 + c->page < c->T ? t0 + c->page : c->T;
         for (int64_t t = t0; t < t1; ++t) {
@@ -257,8 +262,23 @@ extern "C" gkv_status gkv_account(const gkv_cache *c, const int32_t *pages, int3
           touched[t / P] = 1;
         }
       }
+      int64_t ntouched = 0;
       for (int64_t i = 0; i < nblk; ++i)
-        if (touched[i]) r += 2 * overhead_bits(lv[i]);
+        if (touched[i]) {
+          r += 2 * overhead_bits(lv[i]);
+          ++ntouched;
+        }
+      if (c->nres) {  // the residual rows of the read tokens and the touched blocks' masks
+        std::vector<uint8_t> in_read((size_t)c->T, 0);
+        for (int64_t p : list) {
+          const int64_t t0 = p * c->page, t1 = t0 + c->page < c->T ? t0 + c->page : c->T;
+          for (int64_t t = t0; t < t1; ++t) in_read[t] = 1;
+        }
+        const int32_t *ri = res_idx + ((int64_t)b * c->Hkv + h) * c->nres_cap;
+        for (int32_t k = 0; k < c->nres; ++k)
+          if (ri[k] >= 0 && ri[k] < c->T && in_read[ri[k]]) r += 2 * D * 16 + 32;
+        r += ntouched * 64;
+      }
       read += r;
     }
   out->resident_bits = resident;

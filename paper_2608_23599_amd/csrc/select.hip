@@ -501,6 +501,39 @@ __global__ void __launch_bounds__(256) res_gather_kernel(const uint16_t *__restr
   }
 }
 
+// Residual rows before every block (res_off[blk] = sum over blocks < blk of the
+// mask's population count), for blocks 0 .. nblk_cap: a read that finds token t of
+// block blk in the mask finds its row at res_off[blk] + popcount(mask below t).
+// One workgroup per (b, KV head).
+__global__ void __launch_bounds__(256) res_off_kernel(const uint64_t *__restrict__ res_mask, int nblk_cap,
+                                                      int32_t *__restrict__ res_off) {
+  __shared__ int32_t part[256];
+  const int64_t u = blockIdx.x;
+  const uint64_t *m = res_mask + u * nblk_cap;
+  int32_t *o = res_off + u * (nblk_cap + 1);
+  const int per = (nblk_cap + 255) / 256;
+  const int b0 = threadIdx.x * per, b1 = b0 + per < nblk_cap ? b0 + per : nblk_cap;
+  int32_t c = 0;
+  for (int b = b0; b < b1; ++b) c += __popcll(m[b]);
+  part[threadIdx.x] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {  // exclusive scan of the 256 partial counts
+    int32_t run = 0;
+    for (int i = 0; i < 256; ++i) {
+      const int32_t x = part[i];
+      part[i] = run;
+      run += x;
+    }
+    o[nblk_cap] = run;
+  }
+  __syncthreads();
+  int32_t run = part[threadIdx.x];
+  for (int b = b0; b < b1; ++b) {
+    o[b] = run;
+    run += __popcll(m[b]);
+  }
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------- C ABI
@@ -588,6 +621,9 @@ extern "C" gkv_status gkv_rd_residual_select(gkv_cache *c, const uint16_t *k_src
     hipLaunchKernelGGL(res_gather_kernel, g2, dim3(256), 0, s, k_src, v_src, c->T, (const int32_t *)c->res_idx,
                        c->nres_cap, nkeep, c->res_rows, c->Hkv);
   }
+  if (c->nres_cap > 0)
+    hipLaunchKernelGGL(res_off_kernel, dim3(c->B * c->Hkv), dim3(256), 0, s, (const uint64_t *)c->res_mask,
+                       c->nblk_cap, c->res_off);
   if (hipGetLastError() != hipSuccess) return GKV_E_HIP;
   c->nres = nkeep;
   gkv_stamp(c);

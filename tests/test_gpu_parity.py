@@ -6,6 +6,7 @@ import numpy as np
 import pytest
 
 from oracle import fp16 as ofp16, ladder as olad, quest as oquest, residual as ores, cache as ocache, quant as oquant
+from oracle import accounting as oacc
 from paper_2608_23599_amd import synth
 from tests._util import TOL, kv_all, oracle_units, compare_record, q_group, max_err
 
@@ -986,3 +987,46 @@ def test_dense_plan_reuse_follows_the_tables(gpu):
     assert torch.equal(dec(A), fresh(A))
     # the reused plan is the same one: the same call twice gives the same bits
     assert torch.equal(dec(A), dec(A))
+
+
+# ---------------------------------------------------------------- Compressed-Quest with a residual
+
+
+@pytest.mark.parametrize("page,T,topk,frac,Bn", [(16, 6001, 64, (2, 100), 2), (16, 4096, 60, (20, 100), 1),
+                                                 (32, 5003, 40, (10, 100), 1), (64, 8192, 20, (10, 100), 1)])
+def test_quest_read_with_residual_rows(gpu, page, T, topk, frac, Bn):
+    """A Compressed-Quest read of a cache with exact residual rows (sections 3.4 and
+    3.5): the rows of residual tokens in the selected pages or the current page
+    override their graded entries (the oracle's decode_quest on the same residual),
+    for 16-, 32- and 64-token pages, 2% to 20% residual rows, a partial current page;
+    the read accounting matches the oracle's."""
+    Hq, Hkv = 8, 2
+    G = Hq // Hkv
+    ks, vs = kv_all(44, Bn, Hkv, T)
+    lv = olad.ladder("graded", T)
+    n = ores.n_keep(T, *frac)
+    cache = _build(gpu, ks, vs, Hq, lv, page=page, nres_cap=n)
+    mass = np.stack([np.stack([synth.mass_unit(44, b, h, T) for h in range(Hkv)]) for b in range(Bn)])
+    cache.rd_residual_select(ks, vs, mass, n)
+    q = synth.queries(44, Bn, Hq)
+    pages_d = cache.quest_select(q, topk)
+    out = cache.decode(q, pages=pages_d).cpu().numpy()
+    pages = pages_d.cpu().numpy()
+    idx = cache.res_idx.cpu().numpy()
+    res_bits = read_bits = 0
+    for b in range(Bn):
+        for h in range(Hkv):
+            kmin, kmax = oquest.page_boxes(ks[b, h], page)
+            want = oquest.quest_select(q_group(q, b, h, G), kmin, kmax, T, topk, page)
+            np.testing.assert_array_equal(pages[b, h], want)
+            uc = ocache.UnitCache(ks[b, h], vs[b, h], lv)
+            ridx, _ = uc.select_residual(ks[b, h], vs[b, h], mass[b, h], n)
+            np.testing.assert_array_equal(idx[b, h, :n], ridx)
+            assert np.isin(ridx, oquest.read_tokens(want, T, page)).any()  # the read set holds residual rows
+            ref = uc.decode_quest(q_group(q, b, h, G), want, page)
+            assert max_err(out[b, h * G:(h + 1) * G], ref) <= TOL
+            o = oacc.unit_rates(lv, T, page=page, nres=n, pages=want, res_idx=ridx)
+            res_bits += o["resident_bits"]
+            read_bits += o["read_bits"]
+    r = cache.account(pages_d)
+    assert r["resident_bits"] == res_bits and r["read_bits"] == read_bits

@@ -78,7 +78,7 @@ def _host_cache(B, Bn, Hkv, Hq, T, levels, page=0, nres=0):
         keep["boxes"] = bx
         c.page, c.npage_cap, c.boxes = page, ((T // page) + 63) // 64 * 64 + 64, bx.ctypes.data
     if nres:
-        for name in ("res_idx", "res_rows", "res_mask"):
+        for name in ("res_idx", "res_rows", "res_mask", "res_off"):
             a = np.zeros(8, dtype=np.int64)
             keep[name] = a
             setattr(c, name, a.ctypes.data)
@@ -101,7 +101,8 @@ def test_account_matches_oracle(B, T, page, nres, sel):
             pick = np.sort(r.choice(cur, size=min(sel, cur), replace=False))
             pages[0, h, :len(pick)] = pick
     rates = B.Rates()
-    st = B._account(ctypes.byref(c), B._np_ptr(pages) if pages is not None else None, sel or 0, ctypes.byref(rates))
+    st = B._account(ctypes.byref(c), B._np_ptr(pages) if pages is not None else None, sel or 0, None,
+                    ctypes.byref(rates))
     assert st == 0
     res, rd = 0, 0
     for h in range(2):
@@ -326,7 +327,7 @@ def test_account_graded_quest_by_hand(B):
         c, keep = _host_cache(B, 1, 1, 4, T, lv, page=16)
         pages = np.array(case["pages"], dtype=np.int32).reshape(1, 1, -1)
         rates = B.Rates()
-        assert B._account(ctypes.byref(c), B._np_ptr(pages), pages.shape[-1], ctypes.byref(rates)) == 0
+        assert B._account(ctypes.byref(c), B._np_ptr(pages), pages.shape[-1], None, ctypes.byref(rates)) == 0
         assert rates.read_bits == case["read_bits"]
         if case["resident_bits"] is not None:
             assert rates.resident_bits == case["resident_bits"]
@@ -408,3 +409,21 @@ def test_binding_append_with_full_pool_changes_nothing(B):
     assert [c.pool.used(L) for L in B.LEVELS] == used
     assert np.array_equal(c.koff_host, ko) and np.array_equal(c.voff_host, vo)
     assert c.T == 64
+
+
+def test_account_quest_with_residual_by_hand(B):
+    """The library's Compressed-Quest read accounting with residual rows equals the
+    oracle's hand-computed pin (rows of residual tokens in the read set plus one mask
+    per touched block); without the residual tokens the call is refused."""
+    from tests.test_oracle_quest_attn import GRADED_QUEST_CASES
+    case = GRADED_QUEST_CASES[1]
+    T, lv = case["T"], np.array(case["levels"], dtype=np.int8)
+    res = np.array([5, 40, 52, 100, 150, 200, 250, 255], dtype=np.int32)
+    c, keep = _host_cache(B, 1, 1, 4, T, lv, page=16, nres=len(res))
+    pages = np.array(case["pages"] + [3], dtype=np.int32).reshape(1, 1, -1)  # page 3 listed twice
+    rates = B.Rates()
+    assert B._account(ctypes.byref(c), B._np_ptr(pages), pages.shape[-1], B._np_ptr(res), ctypes.byref(rates)) == 0
+    assert rates.read_bits == 163840 + 5 * (2 * 128 * 16 + 32) + 3 * 64
+    o = oacc.unit_rates(lv, T, page=16, nres=len(res), pages=pages[0, 0], res_idx=res)
+    assert rates.read_bits == o["read_bits"] and rates.resident_bits == o["resident_bits"]
+    assert B._account(ctypes.byref(c), B._np_ptr(pages), pages.shape[-1], None, ctypes.byref(rates)) == -1

@@ -282,3 +282,21 @@ def test_graded_quest_read_rate_by_hand(case):
     # the same pages listed twice, unsorted, with -1 padding read the same bits
     padded = np.array(list(reversed(case["pages"])) + case["pages"][:1] + [-1, -1])
     assert accounting.unit_rates(case["levels"], T, page=16, pages=padded)["read_bits"] == case["read_bits"]
+
+
+def test_quest_read_rate_with_residual_by_hand():
+    """A Compressed-Quest read of a cache with exact residual rows: on top of the
+    graded read of case 2 (163840 bits), the rows of the residual tokens inside the
+    read set (2 * 128 * 16 + 32 bits each) and one 64-bit override mask per touched
+    block; residual tokens outside the read set cost nothing."""
+    case = GRADED_QUEST_CASES[1]  # pages 0, 3, 9 and current page 15 of T = 256
+    res_idx = np.array([5, 40, 52, 100, 150, 200, 250, 255])
+    # in the read set: 5 (page 0), 52 (page 3), 150 (page 9), 250, 255 (page 15);
+    # outside: 40 (page 2), 100 (page 6), 200 (page 12)
+    touched_blocks = 3  # blocks 0, 2, 3
+    want = case["read_bits"] + 5 * (2 * 128 * 16 + 32) + touched_blocks * 64
+    r = accounting.unit_rates(case["levels"], 256, page=16, nres=len(res_idx), pages=np.array(case["pages"]),
+                              res_idx=res_idx)
+    assert r["read_bits"] == want == 163840 + 20640 + 192
+    with pytest.raises(ValueError):
+        accounting.unit_rates(case["levels"], 256, page=16, nres=len(res_idx), pages=np.array(case["pages"]))
