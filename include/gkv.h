@@ -147,6 +147,14 @@ typedef struct gkv_cache {
                                 a new process-wide unique value; a caller that writes
                                 those tables itself calls gkv_cache_changed.  0 =
                                 unknown (dense attention plans are then never reused) */
+  int64_t *seq_len;          /* device [B] or NULL: sequences of different lengths (the
+                                block manager of a serving batch).  seq_len[b] tokens
+                                of sequence b are present (0 <= seq_len[b] <= T, and
+                                T is the largest), or -1: a retired sequence, which no
+                                call reads and gkv_append skips.  NULL: every sequence
+                                has T tokens.  The calls that change lengths keep both
+                                copies in step.                                         */
+  int64_t *seq_len_host;     /* host mirror of seq_len (both NULL or both set)          */
 } gkv_cache;
 
 /* Stamps c->version with a new process-wide unique value: a caller that has written
@@ -176,7 +184,9 @@ gkv_status gkv_ladder_levels(int32_t profile, int64_t T, int8_t *levels_host, in
 /* Ladder crossings of a context growing to T_new tokens (section 3.2 monotone
  * demotion): compares the profile's levels at T_new with c->level_host for every
  * existing, complete block of every (b,h) and writes up to max_jobs entries
- * jobs_host[3*i..3*i+2] = (b, h, blk), to_host[i] = new level.  Returns the number
+ * jobs_host[3*i..3*i+2] = (b, h, blk), to_host[i] = new level.  With per-sequence
+ * lengths every active sequence grows by T_new - c->T tokens and is compared with the
+ * profile at its own new length (retired sequences are skipped).  Returns the number
  * of crossings (>= 0), or a negative gkv_status; GKV_E_NOT_MONOTONE if the profile
  * would raise any block's level. */
 int32_t gkv_ladder_crossings(const gkv_cache *c, int32_t profile, int64_t T_new, int32_t *jobs_host,
@@ -196,7 +206,8 @@ void gkv_pool_destroy(gkv_pool *p);
 /* Rate accounting (section 3.5 rate equations; section 4.4 metrics), from the
  * host level mirror.  pages_host = selected pages [B][Hkv][topk] (-1 padded) for a
  * Compressed-Quest read, or NULL for a dense read.  Outputs are bit counts and
- * the number of values B*Hkv*T*2*D. */
+ * the number of values Hkv*2*D times the tokens of every sequence (B*T without
+ * per-sequence lengths; retired sequences count nothing). */
 typedef struct gkv_rates {
   int64_t resident_bits, read_bits, values;
 } gkv_rates;
@@ -237,7 +248,9 @@ int64_t gkv_workspace_bytes(const gkv_cache *c, int32_t op, int32_t topk);
  * code = rint((x-z)/s) clamped, in fp64; centroid blocks run 4-means Lloyd in fp64
  * (rows 0,16,32,48 initial, at most 10 rounds, fp16 centroids, ids re-assigned
  * against the stored centroids); mean blocks store the fp16 of the block mean (the
- * same iteration with one centroid; the fp64 token-ascending sum is exact). */
+ * same iteration with one centroid; the fp64 token-ascending sum is exact).  With
+ * per-sequence lengths, blocks at or past a sequence's end are skipped and only an
+ * exact block may extend past its length. */
 gkv_status gkv_quantize_block(const gkv_cache *c, int32_t which, const uint16_t *src, int64_t T_src,
                               int32_t blk_begin, int32_t blk_end, void *stream);
 
@@ -252,16 +265,21 @@ gkv_status gkv_demote(gkv_cache *c, int32_t n, const int32_t *jobs_host, const i
 
 /* Exact per-page key boxes (section 3.5): for pages [page_begin, page_end) of every
  * (b,h), per channel min and max of the exact fp16 keys k_src [B][Hkv][T_src][128]
- * (all tokens of each page must be < T_src). */
+ * (all tokens of each page must be < T_src; with per-sequence lengths, pages past a
+ * sequence's last complete page are left as they are). */
 gkv_status gkv_page_boxes(const gkv_cache *c, const uint16_t *k_src, int64_t T_src, int64_t page_begin,
                           int64_t page_end, void *stream);
 
 /* Append one token per (b,h) (decode step): k_new, v_new [B][Hkv][128] fp16 are
- * written into the newest block, which must be exact.  When T is a multiple of 64
- * a new exact block is opened for every (b,h) u at byte offsets new_koff_host[u] /
- * new_voff_host[u] (arrays of B*Hkv <= 128 entries; ignored otherwise, may be NULL);
- * its other 63 rows are written as zero.  When the token completes a page and boxes are kept, that page's box is written
- * from the exact keys.  c->T is incremented. */
+ * written into the newest block, which must be exact.  When the sequence's length is
+ * a multiple of 64 a new exact block is opened for its (b,h) units u at byte offsets
+ * new_koff_host[u] / new_voff_host[u] (arrays of B*Hkv <= 128 entries; entries of
+ * units that open nothing are ignored; may be NULL when no unit opens a block); its
+ * other 63 rows are written as zero.  When the token completes a page and boxes are
+ * kept, that page's box is written from the exact keys.  c->T is incremented; with
+ * per-sequence lengths every active sequence grows by one token at its own position
+ * (its rows of k_new / v_new are used, a retired sequence's are ignored) and T
+ * becomes the largest length. */
 #define GKV_MAX_APPEND_UNITS 128
 gkv_status gkv_append(gkv_cache *c, const uint16_t *k_new, const uint16_t *v_new, const int64_t *new_koff_host,
                       const int64_t *new_voff_host, void *stream);
@@ -335,12 +353,27 @@ gkv_status gkv_attn_partials(const uint16_t *q, const gkv_cache *c, const int32_
 gkv_status gkv_attn_merge(const gkv_cache *c, const int32_t *pages, int32_t topk, float *out, void *ws,
                           int64_t ws_bytes, void *stream);
 
+/* Sequence lifecycle of a batch with per-sequence lengths (c->seq_len set; the block
+ * manager of the paper's serving plug-in).  gkv_retire_sequence gives every block
+ * slot of sequence b (all its KV heads, at the levels of c->level_host) back to
+ * pool, using the host offset mirrors koff_host / voff_host [B][Hkv][nblk_cap], and
+ * marks the sequence retired (-1; T becomes the largest remaining length); the slots
+ * are reusable by later work on `stream`.  gkv_admit_sequence makes a retired slot b
+ * an empty sequence (length 0), which appends then fill from its first block.  Both
+ * update the device length on `stream`.  GKV_E_ARG without per-sequence lengths, for
+ * an inactive b (retire) or an active b (admit). */
+gkv_status gkv_retire_sequence(gkv_cache *c, gkv_pool *pool, const int64_t *koff_host, const int64_t *voff_host,
+                               int32_t b, void *stream);
+gkv_status gkv_admit_sequence(gkv_cache *c, int32_t b, void *stream);
+
 /* Rate-distortion exact residual (section 3.4, Eq. rdscore): score every token
  * s_j = a_j * sum_d (v_jd - v_hat_jd)^2 (fp64, channel order, no fused multiply-add)
  * with v_hat its value at its block's level, keep the first nkeep of the order
  * (score desc, token asc) per (b,h), and store their exact K and V rows, ascending
  * indices and per-block override masks in the cache.  k_src, v_src:
- * [B][Hkv][T][128] fp16; mass: [B][Hkv][T] fp32.  Sets c->nres = nkeep. */
+ * [B][Hkv][T][128] fp16; mass: [B][Hkv][T] fp32.  Sets c->nres = nkeep.
+ * GKV_E_UNSUPPORTED with per-sequence lengths (the selection runs at prefill, on a
+ * batch of one length). */
 gkv_status gkv_rd_residual_select(gkv_cache *c, const uint16_t *k_src, const uint16_t *v_src,
                                   const float *mass, int32_t nkeep, void *ws, int64_t ws_bytes,
                                   void *stream);

@@ -41,6 +41,7 @@ class CacheStruct(ctypes.Structure):
         ("cert", _vp),
         ("v_per_token", _i32),
         ("version", ctypes.c_uint64),
+        ("seq_len", _vp), ("seq_len_host", _vp),
     ]
 
 
@@ -82,6 +83,8 @@ _attn_partials = _sig("gkv_attn_partials", _i32, [_vp, _P(CacheStruct), _vp, _i3
 _attn_merge = _sig("gkv_attn_merge", _i32, [_P(CacheStruct), _vp, _i32, _vp, _vp, _i64, _vp])
 _rd = _sig("gkv_rd_residual_select", _i32, [_P(CacheStruct), _vp, _vp, _vp, _i32, _vp, _i64, _vp])
 _cache_changed = _sig("gkv_cache_changed", None, [_P(CacheStruct)])
+_retire = _sig("gkv_retire_sequence", _i32, [_P(CacheStruct), _vp, _vp, _vp, _i32, _vp])
+_admit = _sig("gkv_admit_sequence", _i32, [_P(CacheStruct), _i32, _vp])
 _attn_noalloc = _sig("gkv_graded_decode_attn_noalloc", _i32, [_vp, _P(CacheStruct), _vp, _i32, _vp, _vp])
 _noalloc_bytes = _sig("gkv_noalloc_scratch_bytes", _i64, [])
 _layers_step = _sig("gkv_layers_step", _i32, [_vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _vp])
@@ -100,7 +103,8 @@ EXPORTED = [
     "gkv_page_boxes", "gkv_append", "gkv_quest_select", "gkv_graded_decode_attn", "gkv_rd_residual_select",
     "gkv_attn_plan", "gkv_attn_partials", "gkv_attn_merge", "gkv_graded_decode_attn_bound",
     "gkv_observe_ws_bytes", "gkv_observe_mass", "gkv_query_norms", "gkv_allocate_levels", "gkv_layers_step",
-    "gkv_cache_changed", "gkv_graded_decode_attn_noalloc", "gkv_noalloc_scratch_bytes",
+    "gkv_cache_changed", "gkv_graded_decode_attn_noalloc", "gkv_noalloc_scratch_bytes", "gkv_retire_sequence",
+    "gkv_admit_sequence",
 ]
 
 
@@ -266,8 +270,15 @@ class GradedCache:
     Compressed-Quest boxes and exact residual)."""
 
     def __init__(self, B, Hkv, Hq, T, nblk_cap, caps, page=0, npage_cap=0, nres_cap=0, device="cuda",
-                 v_per_token=False):
+                 v_per_token=False, seq_lens=None):
         self.device = torch.device(device)
+        # sequences of different lengths (-1: retired): host and device copies
+        if seq_lens is not None:
+            self.seq_len_host = np.ascontiguousarray(np.array(seq_lens, dtype=np.int64).reshape(B))
+            self.seq_len = torch.from_numpy(self.seq_len_host.copy()).to(self.device)
+            T = int(self.seq_len_host.max(initial=0))
+        else:
+            self.seq_len_host = self.seq_len = None
         self.v_per_token = bool(v_per_token)
         self.B, self.Hkv, self.Hq = B, Hkv, Hq
         self.units = B * Hkv
@@ -321,6 +332,8 @@ class GradedCache:
         c.res_off = self.res_off.data_ptr() if self.nres_cap else None
         c.cert = self.cert.data_ptr()
         c.v_per_token = int(self.v_per_token)
+        c.seq_len = self.seq_len.data_ptr() if self.seq_len is not None else None
+        c.seq_len_host = self.seq_len_host.ctypes.data if self.seq_len_host is not None else None
         _cache_changed(ctypes.byref(c))  # new tables: a fresh version stamp
 
     def clone(self):
@@ -334,6 +347,9 @@ class GradedCache:
         new.level_host = self.level_host.copy()
         new.koff_host = self.koff_host.copy()
         new.voff_host = self.voff_host.copy()
+        if self.seq_len is not None:
+            new.seq_len = self.seq_len.clone()
+            new.seq_len_host = self.seq_len_host.copy()
         new.pool = None
         new.c = CacheStruct()
         new._bind(self.T, int(self.c.nres))
@@ -343,11 +359,12 @@ class GradedCache:
     # ------------------------------------------------------------ construction
     @classmethod
     def build(cls, k, v, Hq, levels, page=0, nres_cap=0, device="cuda", extra_blocks=0, slack=None,
-              v_per_token=False):
+              v_per_token=False, seq_lens=None):
         """k, v: fp16 bits [B][Hkv][T][128] (numpy uint16 or torch int16/float16).
         levels: per-block levels, [nblk] (shared) or [B][Hkv][nblk].  Encodes every
         block at its level (gkv_quantize_block) and, with page > 0, writes the page
-        boxes from the exact keys (gkv_page_boxes)."""
+        boxes from the exact keys (gkv_page_boxes).  seq_lens: per-sequence lengths
+        (<= T; k and v are padded to T), blocks past a sequence's end take no slot."""
         kd = _as_bits(k, device)
         vd = _as_bits(v, device)
         B, Hkv, T, Dd = kd.shape
@@ -358,19 +375,24 @@ class GradedCache:
             lv = np.broadcast_to(lv, (B, Hkv, nblk))
         assert lv.shape == (B, Hkv, nblk)
         nblk_cap = nblk + extra_blocks
+        lens = np.full(B, T, np.int64) if seq_lens is None else np.asarray(seq_lens, np.int64)
+        owned = np.arange(nblk)[None, :] < ((np.maximum(lens, 0) + P - 1) // P)[:, None]  # [B][nblk]
+        owned = np.broadcast_to(owned[:, None, :], (B, Hkv, nblk))
         # one slot per tensor block (keys and values separately), plus slack for
         # demotions and appended blocks
-        caps = {L: 2 * int((lv == L).sum()) for L in LEVELS}
+        caps = {L: 2 * int(((lv == L) & owned).sum()) for L in LEVELS}
         for L, n in (slack or {}).items():
             caps[L] += 2 * n
         npage_cap = 0
         if page:
             npage_cap = (((T + extra_blocks * P) // page) + 63) // 64 * 64
         self = cls(B, Hkv, Hq, T, nblk_cap, caps, page=page, npage_cap=npage_cap, nres_cap=nres_cap, device=device,
-                   v_per_token=v_per_token)
+                   v_per_token=v_per_token, seq_lens=seq_lens)
         for b in range(B):
             for h in range(Hkv):
                 for i in range(nblk):
+                    if not owned[b, h, i]:
+                        continue
                     L = int(lv[b, h, i])
                     self.level_host[b, h, i] = L
                     self.koff_host[b, h, i] = self.pool.alloc(L)
@@ -391,6 +413,21 @@ class GradedCache:
     @property
     def T(self):
         return int(self.c.T)
+
+    def lengths(self):
+        """Tokens of every sequence (-1: retired)."""
+        if self.seq_len_host is not None:
+            return self.seq_len_host.copy()
+        return np.full(self.B, self.T, np.int64)
+
+    def retire(self, b):
+        """gkv_retire_sequence: sequence b's slots go back to the pool."""
+        _check(_retire(ctypes.byref(self.c), self.pool.h, _np_ptr(self.koff_host), _np_ptr(self.voff_host), int(b),
+                       _stream()), "retire_sequence")
+
+    def admit(self, b):
+        """gkv_admit_sequence: retired slot b becomes an empty sequence."""
+        _check(_admit(ctypes.byref(self.c), int(b), _stream()), "admit_sequence")
 
     def workspace(self, op, topk=0):
         n = int(_workspace_bytes(ctypes.byref(self.c), op, topk))
@@ -459,12 +496,20 @@ class GradedCache:
         Returns the demotions [(b, h, blk, old, new)]."""
         kd = _as_bits(k_new, self.device)
         vd = _as_bits(v_new, self.device)
-        T = self.T
+        lens = self.lengths()
+        opens = [b for b in range(self.B) if lens[b] >= 0 and lens[b] % P == 0]
         nk = nv = None
-        if T % P == 0:
-            # K and V slots of one block side by side (the order gkv_layers_step takes them)
-            kv = self._take([EXACT] * (2 * self.units))
-            nk, nv = kv[0::2].copy(), kv[1::2].copy()
+        if opens:
+            # K and V slots of one block side by side (the order gkv_layers_step takes
+            # them), for the units whose sequence opens a block
+            kv = self._take([EXACT] * (2 * self.Hkv * len(opens)))
+            nk = np.full(self.units, -1, np.int64)
+            nv = np.full(self.units, -1, np.int64)
+            i = 0
+            for b in opens:
+                for h in range(self.Hkv):
+                    nk[b * self.Hkv + h], nv[b * self.Hkv + h] = kv[i], kv[i + 1]
+                    i += 2
         st = _append(ctypes.byref(self.c), _dptr(kd), _dptr(vd), _np_ptr(nk) if nk is not None else None,
                      _np_ptr(nv) if nv is not None else None, _stream())
         if st != 0:
@@ -472,9 +517,10 @@ class GradedCache:
                 for off in kv:
                     self.pool.free(EXACT, int(off))
             raise GkvError(st, "append")
-        if nk is not None:  # the mirrors follow the library only once the call succeeded
-            self.koff_host[:, :, T // P] = nk.reshape(self.B, self.Hkv)
-            self.voff_host[:, :, T // P] = nv.reshape(self.B, self.Hkv)
+        for b in opens:  # the mirrors follow the library only once the call succeeded
+            blk = int(lens[b]) // P
+            self.koff_host[b, :, blk] = nk[b * self.Hkv:(b + 1) * self.Hkv]
+            self.voff_host[b, :, blk] = nv[b * self.Hkv:(b + 1) * self.Hkv]
         moves = []
         if profile is not None:
             jobs = np.empty(3 * 64, dtype=np.int32)

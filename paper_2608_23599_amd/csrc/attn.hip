@@ -211,6 +211,7 @@ struct AttnParams {
   const int32_t *res_off;
   const uint8_t *res_rows;
   const int32_t *pages;
+  const int64_t *seq_len;  // tokens per sequence (-1: retired), or null: every sequence has T
   uint8_t *visits;  // visit descriptors (plan kernel scratch), vcap per (b, KV head)
   uint8_t *plan;    // item descriptors, icap per (b, KV head)
   uint8_t *units;   // unit descriptors, ucap per (b, KV head)
@@ -1299,7 +1300,8 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
 // (m_s, l_s, o_s) of the nsplit workgroups combine to o = sum_s a_s o_s / sum_s a_s l_s
 // with a_s = 2^(m_s - max_s m_s).
 __global__ void __launch_bounds__(D) merge_kernel(const float *part, float *out, int nsplit, int G, float *bound,
-                                                  const float *cert, int nblk_cap, int nblk) {
+                                                  const float *cert, int nblk_cap, int nblk,
+                                                  const int64_t *seq_len, int Hkv) {
   __shared__ float sa[kMaxWaves / kWaves], sl[kMaxWaves / kWaves];
   __shared__ float sinv, svm[D];
   const int g = blockIdx.x, d = threadIdx.x;
@@ -1309,6 +1311,10 @@ __global__ void __launch_bounds__(D) merge_kernel(const float *part, float *out,
   for (int s2 = d; s2 < nsplit; s2 += D) {
     sa[s2] = base[s2 * stride];
     sl[s2] = base[s2 * stride + 1];
+  }
+  if (seq_len) {  // this sequence's blocks
+    const int64_t t = seq_len[u / Hkv];
+    nblk = t > 0 ? (int)((t + P - 1) / P) : 0;
   }
   if (bound) {  // max_b vmax_b over the blocks of this (b, KV head)
     float vm = 0.f;
@@ -1325,8 +1331,9 @@ __global__ void __launch_bounds__(D) merge_kernel(const float *part, float *out,
       sa[s2] = a;
       L = fmaf(a, sl[s2], L);
     }
-    sinv = 1.0f / L;
-    if (bound) {  // section 3.6: sum_b a_b verr_b + min(2, M+/M- - M-/M+) max_j ||v_j||
+    sinv = L > 0.f ? 1.0f / L : 0.f;  // an empty sequence reads nothing: its output is zero
+    if (bound && !(L > 0.f)) bound[u * G + g] = 0.f;
+    if (bound && L > 0.f) {  // section 3.6: sum_b a_b verr_b + min(2, M+/M- - M-/M+) max_j ||v_j||
       float c1 = 0.f, c2 = 0.f, c3 = 0.f, vm = 0.f;
       for (int s2 = 0; s2 < nsplit; ++s2) {
         c1 = fmaf(sa[s2], base[s2 * stride + D + 2], c1);
@@ -1397,7 +1404,14 @@ __device__ __forceinline__ uint32_t balance_cost(int lv, uint64_t va) {
 }
 
 __device__ __forceinline__ uint64_t token_mask(int64_t left) {  // tokens of a block below `left`
-  return left >= P ? ~0ull : ((1ull << left) - 1);
+  return left >= P ? ~0ull : (left <= 0 ? 0ull : ((1ull << left) - 1));
+}
+
+// Tokens of (b, KV head) u: its sequence's length, 0 for a retired sequence.
+__device__ __forceinline__ int64_t unit_T(const AttnParams &p, int64_t u) {
+  if (!p.seq_len) return p.T;
+  const int64_t t = p.seq_len[u / p.Hkv];
+  return t > 0 ? t : 0;
 }
 
 // Wavefront inclusive scan of a 32-bit value in lane order: DPP row shifts within
@@ -1570,7 +1584,9 @@ __host__ __device__ __forceinline__ int quest_pages_per_wave(int page, bool resi
 __device__ __forceinline__ uint2 quest_lists(const AttnParams &p, int64_t u, int w, int W, int lane,
                                              ItemDesc *items, UnitDesc *units) {
   const int32_t *pg = p.pages + u * p.topk;
-  const int64_t cur = (p.T - 1) / p.page;
+  const int64_t Tu = unit_T(p, u);
+  if (Tu == 0) return make_uint2(0, 0);  // an empty or retired sequence reads nothing
+  const int64_t cur = (Tu - 1) / p.page;
   int cnt = p.topk;
   for (int base = 0; base < p.topk; base += 64) {
     const int i = base + lane;
@@ -1606,7 +1622,7 @@ __device__ __forceinline__ uint2 quest_lists(const AttnParams &p, int64_t u, int
     uint64_t va = 0;
     for (int t = 0; t < 4; ++t)
       if (tl & (1u << t)) va |= 0xFFFFull << (16 * t);
-    d.valid = va & token_mask(p.T - blk * P);
+    d.valid = va & token_mask(Tu - blk * P);
     d.cost = 0;
     // residual rows override their tokens (section 3.4): the graded tiles skip them
     // and the exact tiles of the residual that hold their rows are read instead
@@ -1653,7 +1669,7 @@ __device__ __forceinline__ uint2 quest_lists(const AttnParams &p, int64_t u, int
 
 // Tokens read from block b of a dense read (residual rows excluded).
 __device__ __forceinline__ uint64_t dense_tokens(const AttnParams &p, int64_t u, int64_t b) {
-  uint64_t va = token_mask(p.T - b * P);
+  uint64_t va = token_mask(unit_T(p, u) - b * P);
   if (p.nres) va &= ~p.res_mask[u * p.nblk_cap + b];
   return va;
 }
@@ -1698,7 +1714,7 @@ __device__ __forceinline__ VisitDesc dense_visit(const AttnParams &p, int64_t u,
     d.blk = (uint16_t)v;
     d.kp = (uint64_t)(uintptr_t)(p.arena + p.koff[u * p.nblk_cap + v]);
     d.vp = (uint64_t)(uintptr_t)(p.arena + p.voff[u * p.nblk_cap + v]);
-    d.valid = token_mask(p.T - v * P);
+    d.valid = token_mask(unit_T(p, u) - v * P);
     if (p.nres) d.valid &= ~p.res_mask[u * p.nblk_cap + v];
     if (jn && d.level == GKV_MEAN && d.valid) mean_run_visit(p, u, v, jn, d);
   } else {
@@ -1869,10 +1885,16 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnParams p) {
   o.usplit = o.isplit + (W + 1);
   o.W = W;
   o.W1 = p.fast * kWaves;
-  const int64_t nblk = (p.T + P - 1) / P;
+  const int64_t Tu = unit_T(p, u);
+  const int64_t nblk = (Tu + P - 1) / P;
   // blocks 0..nblk-1, then the residual rows as exact pseudo-blocks; each thread
   // describes a contiguous run of visits
-  const int64_t nvis = nblk + (p.nres + P - 1) / P;
+  const int64_t nvis = Tu ? nblk + (p.nres + P - 1) / P : 0;
+  if (nvis == 0) {  // an empty or retired sequence: every wavefront's lists are empty
+    if (blockIdx.y == 0)
+      for (int ww = threadIdx.x; ww <= W; ww += kPlanThreads) o.isplit[ww] = o.usplit[ww] = 0;
+    return;
+  }
   const int64_t per = (nvis + kPlanThreads - 1) / kPlanThreads;
   if (per <= kPlanRegs) {
     plan_dense_regs(p, u, nblk, nvis, o, sh, lastc, joins);
@@ -2001,6 +2023,7 @@ static gkv_status attn_setup(const uint16_t *q, const gkv_cache *c, const int32_
   p.res_off = c->res_off;
   p.res_rows = c->res_rows;
   p.pages = pages;
+  p.seq_len = c->seq_len;
   p.tag = (uint64_t *)ws;
   p.part = (float *)((uint8_t *)ws + L.part);
   p.split = (int32_t *)((uint8_t *)ws + L.split);
@@ -2076,7 +2099,8 @@ static void launch_partials(const AttnParams &p, const gkv_cache *c, hipStream_t
 }
 static void launch_merge(const AttnParams &p, const gkv_cache *c, float *out, hipStream_t s) {
   hipLaunchKernelGGL(merge_kernel, dim3(p.G, c->Hkv * c->B), dim3(D), 0, s, (const float *)p.part, out, p.nsplit,
-                     p.G, p.bound, p.cert, c->nblk_cap, (int)((c->T + P - 1) / P));
+                     p.G, p.bound, p.cert, c->nblk_cap, (int)((c->T + P - 1) / P), (const int64_t *)c->seq_len,
+                     c->Hkv);
 }
 
 extern "C" gkv_status gkv_attn_plan(const gkv_cache *c, const int32_t *pages, int32_t topk, void *ws, int64_t ws_bytes,

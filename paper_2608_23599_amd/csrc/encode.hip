@@ -344,14 +344,17 @@ __global__ void __launch_bounds__(kThreads) quantize_kernel(const uint16_t *__re
                                                             const int8_t *__restrict__ level,
                                                             const int64_t *__restrict__ off, uint8_t *arena,
                                                             int Hkv, int nblk_cap, int blk0, int tensor,
-                                                            float *cert, int vtok) {
+                                                            float *cert, int vtok, const int64_t *seq_len) {
   extern __shared__ __align__(16) unsigned char smem[];
   EncodeShared &S = *reinterpret_cast<EncodeShared *>(smem);
   const int blk = blk0 + blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int64_t u = (int64_t)b * Hkv + h;
+  // a sequence's own length bounds its rows; blocks past its end are not encoded
+  const int64_t Tb = seq_len ? (seq_len[b] < T_src ? seq_len[b] : T_src) : T_src;
+  if ((int64_t)blk * P >= Tb) return;
   const int lv = level[u * nblk_cap + blk];
   const bool per_token = tensor == GKV_VALUES && vtok;
-  load_rows(S, src + u * T_src * D, T_src, (int64_t)blk * P);
+  load_rows(S, src + u * T_src * D, Tb, (int64_t)blk * P);
   __syncthreads();
   encode_to(S, arena + off[u * nblk_cap + blk], lv, tensor, per_token);
   if (cert) {  // error against the exact rows; the value tensor also keeps the row norms
@@ -409,19 +412,26 @@ __global__ void __launch_bounds__(kThreads) demote_kernel(DemoteJobs jobs, int8_
 }
 
 // Append one token per (b,h); grid (Hkv, B), 128 threads (one per channel).
+// The new blocks' slots of the units that open one, and with per-sequence lengths the
+// length of every sequence before the token (-1: retired, skipped).
 struct NewSlots {
   int64_t k[GKV_MAX_APPEND_UNITS], v[GKV_MAX_APPEND_UNITS];
+  int64_t len[GKV_MAX_APPEND_UNITS];
 };
 
 __global__ void __launch_bounds__(128) append_kernel(const uint16_t *__restrict__ k_new,
                                                      const uint16_t *__restrict__ v_new, int8_t *level,
                                                      int64_t *koff, int64_t *voff, uint8_t *arena,
                                                      uint16_t *boxes, int64_t npage_cap, int page, int Hkv,
-                                                     int nblk_cap, int64_t T, int open_block, NewSlots slots,
+                                                     int nblk_cap, int64_t T_all, int64_t *seq_len, NewSlots slots,
                                                      float *cert) {
   __shared__ double vsq[D];
   const int h = blockIdx.x, b = blockIdx.y, d = threadIdx.x;
   const int64_t u = (int64_t)b * Hkv + h;
+  const int64_t T = seq_len ? slots.len[b] : T_all;
+  if (T < 0) return;  // a retired sequence
+  if (seq_len && h == 0 && d == 0) seq_len[b] = T + 1;
+  const int open_block = (T % P) == 0;
   const int blk = (int)(T / P), tok = (int)(T % P);
   const int64_t ti = u * nblk_cap + blk;
   int64_t ko, vo;
@@ -497,13 +507,18 @@ __global__ void __launch_bounds__(128) append_kernel(const uint16_t *__restrict_
 // Page boxes from token-major exact keys; one workgroup per 64 pages of one (b,h).
 __global__ void __launch_bounds__(kThreads) boxes_kernel(const uint16_t *__restrict__ k_src, int64_t T_src,
                                                          uint16_t *boxes, int64_t npage_cap, int page, int Hkv,
-                                                         int64_t page_begin, int64_t page_end) {
+                                                         int64_t page_begin, int64_t page_end,
+                                                         const int64_t *seq_len) {
   __shared__ uint32_t stage[64 * D];  // [channel][page&63] (kmin | kmax << 16)
   const int h = blockIdx.y, b = blockIdx.z;
   const int64_t u = (int64_t)b * Hkv + h;
   const int64_t g0 = (page_begin >> 6) + blockIdx.x;  // box group
   const int64_t p_lo = g0 * 64;
   const uint16_t *src = k_src + u * T_src * D;
+  if (seq_len) {  // only the sequence's complete pages
+    const int64_t last = seq_len[b] < 0 ? 0 : seq_len[b] / page;
+    page_end = page_end < last ? page_end : last;
+  }
   for (int i = threadIdx.x; i < 64 * D; i += kThreads) {
     const int pi = i >> 7, d = i & 127;
     const int64_t p = p_lo + pi;
@@ -575,6 +590,15 @@ void gkv_launch_rd_score(const gkv_cache *c, const uint16_t *v_src, const float 
 // ---------------------------------------------------------------- C ABI
 static gkv_status hip_status() { return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP; }
 
+__global__ void set_len_kernel(int64_t *seq_len, int b, int64_t v) {
+  if (threadIdx.x == 0) seq_len[b] = v;
+}
+
+gkv_status gkv_launch_set_len(int64_t *seq_len, int b, int64_t v, hipStream_t stream) {
+  hipLaunchKernelGGL(set_len_kernel, dim3(1), dim3(64), 0, stream, seq_len, b, v);
+  return hip_status();
+}
+
 extern "C" gkv_status gkv_quantize_block(const gkv_cache *c, int32_t which, const uint16_t *src, int64_t T_src,
                                          int32_t blk_begin, int32_t blk_end, void *stream) {
   gkv_status st = gkv_validate_cache(c);
@@ -582,20 +606,23 @@ extern "C" gkv_status gkv_quantize_block(const gkv_cache *c, int32_t which, cons
   if (!src || (which != GKV_KEYS && which != GKV_VALUES) || T_src <= 0) return GKV_E_ARG;
   if (blk_begin < 0 || blk_end > c->nblk_cap || blk_begin > blk_end) return GKV_E_SHAPE;
   if (blk_begin == blk_end) return GKV_OK;
-  const int64_t *offt_dev = which == GKV_KEYS ? c->koff : c->voff;
-  for (int b = 0; b < c->B; ++b)
+  for (int b = 0; b < c->B; ++b) {
+    // with per-sequence lengths the sequence's own length bounds its blocks
+    const int64_t Tb = c->seq_len_host ? c->seq_len_host[b] : T_src;
+    if (Tb > T_src) return GKV_E_SHAPE;
     for (int h = 0; h < c->Hkv; ++h)
       for (int blk = blk_begin; blk < blk_end; ++blk) {
+        if (c->seq_len_host && (int64_t)blk * P >= Tb) continue;  // not encoded
         const int lv = c->level_host[((int64_t)b * c->Hkv + h) * c->nblk_cap + blk];
         if (level_rank(lv) < 0) return GKV_E_ARG;
-        if ((int64_t)(blk + 1) * P > T_src && lv != GKV_EXACT) return GKV_E_SHAPE;
-        if ((int64_t)blk * P >= T_src) return GKV_E_SHAPE;
+        if ((int64_t)(blk + 1) * P > Tb && lv != GKV_EXACT) return GKV_E_SHAPE;
+        if ((int64_t)blk * P >= Tb) return GKV_E_SHAPE;
       }
-  (void)offt_dev;
+  }
   dim3 grid(blk_end - blk_begin, c->Hkv, c->B);
   hipLaunchKernelGGL(quantize_kernel, grid, dim3(kThreads), sizeof(EncodeShared), (hipStream_t)stream, src,
                      T_src, c->level, which == GKV_KEYS ? c->koff : c->voff, c->arena, c->Hkv, c->nblk_cap,
-                     blk_begin, which, c->cert, c->v_per_token);
+                     blk_begin, which, c->cert, c->v_per_token, (const int64_t *)c->seq_len);
   return hip_status();
 }
 
@@ -652,7 +679,7 @@ extern "C" gkv_status gkv_page_boxes(const gkv_cache *c, const uint16_t *k_src, 
   const int64_t g0 = page_begin >> 6, g1 = (page_end + 63) >> 6;
   dim3 grid((unsigned)(g1 - g0), c->Hkv, c->B);
   hipLaunchKernelGGL(boxes_kernel, grid, dim3(kThreads), 0, (hipStream_t)stream, k_src, T_src, c->boxes,
-                     c->npage_cap, c->page, c->Hkv, page_begin, page_end);
+                     c->npage_cap, c->page, c->Hkv, page_begin, page_end, (const int64_t *)c->seq_len);
   return hip_status();
 }
 
@@ -661,34 +688,49 @@ extern "C" gkv_status gkv_append(gkv_cache *c, const uint16_t *k_new, const uint
   gkv_status st = gkv_validate_cache(c);
   if (st) return st;
   if (!k_new || !v_new) return GKV_E_ARG;
-  const int64_t T = c->T;
-  const int blk = (int)(T / P);
-  if (blk >= c->nblk_cap) return GKV_E_SHAPE;
-  const int open = (T % P) == 0;
   const int64_t units = (int64_t)c->B * c->Hkv;
+  if (c->seq_len_host && c->B > GKV_MAX_APPEND_UNITS) return GKV_E_UNSUPPORTED;
   NewSlots slots;
-  if (open) {
-    if (units > GKV_MAX_APPEND_UNITS) return GKV_E_UNSUPPORTED;
-    if (!new_koff || !new_voff) return GKV_E_ARG;
-    for (int64_t u = 0; u < units; ++u) {
-      if (new_koff[u] < 0 || new_voff[u] < 0 || new_koff[u] + kExactBytes > c->arena_bytes ||
-          new_voff[u] + kExactBytes > c->arena_bytes)
+  bool any_open = false;
+  for (int b = 0; b < c->B; ++b) {
+    const int64_t T = seq_tokens(c, b);
+    if (c->seq_len_host) slots.len[b] = T;
+    if (T < 0) continue;  // retired
+    const int blk = (int)(T / P);
+    if (blk >= c->nblk_cap) return GKV_E_SHAPE;
+    if (c->page && (T + 1) / c->page > c->npage_cap) return GKV_E_SHAPE;
+    const bool open = (T % P) == 0;
+    any_open |= open;
+    for (int h = 0; h < c->Hkv; ++h) {
+      const int64_t u = (int64_t)b * c->Hkv + h;
+      if (open) {
+        if (units > GKV_MAX_APPEND_UNITS) return GKV_E_UNSUPPORTED;
+        if (!new_koff || !new_voff) return GKV_E_ARG;
+        if (new_koff[u] < 0 || new_voff[u] < 0 || new_koff[u] + kExactBytes > c->arena_bytes ||
+            new_voff[u] + kExactBytes > c->arena_bytes)
+          return GKV_E_ARG;
+        slots.k[u] = new_koff[u];
+        slots.v[u] = new_voff[u];
+      } else if (c->level_host[u * c->nblk_cap + blk] != GKV_EXACT) {
         return GKV_E_ARG;
-      slots.k[u] = new_koff[u];
-      slots.v[u] = new_voff[u];
+      }
     }
-  } else {
-    for (int64_t u = 0; u < units; ++u)
-      if (c->level_host[u * c->nblk_cap + blk] != GKV_EXACT) return GKV_E_ARG;
   }
-  if (c->page && (T + 1) / c->page > c->npage_cap) return GKV_E_SHAPE;
+  (void)any_open;
   hipLaunchKernelGGL(append_kernel, dim3(c->Hkv, c->B), dim3(128), 0, (hipStream_t)stream, k_new, v_new, c->level,
                      c->koff, c->voff, c->arena, c->page ? c->boxes : nullptr, c->npage_cap, c->page ? c->page : 1,
-                     c->Hkv, c->nblk_cap, T, open, slots, c->cert);
+                     c->Hkv, c->nblk_cap, c->T, c->seq_len, slots, c->cert);
   if (hipGetLastError() != hipSuccess) return GKV_E_HIP;
-  if (open)
-    for (int64_t u = 0; u < (int64_t)c->B * c->Hkv; ++u) c->level_host[u * c->nblk_cap + blk] = GKV_EXACT;
-  c->T = T + 1;
+  int64_t mx = 0;
+  for (int b = 0; b < c->B; ++b) {
+    const int64_t T = seq_tokens(c, b);
+    if (T < 0) continue;
+    if (T % P == 0)
+      for (int h = 0; h < c->Hkv; ++h) c->level_host[((int64_t)b * c->Hkv + h) * c->nblk_cap + T / P] = GKV_EXACT;
+    if (c->seq_len_host) c->seq_len_host[b] = T + 1;
+    mx = T + 1 > mx ? T + 1 : mx;
+  }
+  c->T = c->seq_len_host ? mx : c->T + 1;
   gkv_stamp(c);
   return GKV_OK;
 }

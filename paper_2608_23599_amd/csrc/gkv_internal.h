@@ -142,6 +142,12 @@ GKV_HD double f16_to_f64(uint16_t h) {
 // Host-side validation shared by the call wrappers (host.cpp).
 gkv_status gkv_validate_cache(const gkv_cache *c);
 
+// Writes seq_len[b] = v on the device, ordered on `stream` (encode.hip).
+gkv_status gkv_launch_set_len(int64_t *seq_len, int b, int64_t v, hipStream_t stream);
+
+// Tokens of sequence b (-1: retired), from the host mirror.
+inline int64_t seq_tokens(const gkv_cache *c, int b) { return c->seq_len_host ? c->seq_len_host[b] : c->T; }
+
 // Compute units of the current device (cached per device; attn.hip).
 int gkv_device_cus();
 

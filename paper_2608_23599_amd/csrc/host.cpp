@@ -84,14 +84,23 @@ extern "C" int32_t gkv_ladder_crossings(const gkv_cache *c, int32_t profile, int
   gkv_status st = gkv_validate_cache(c);
   if (st) return st;
   if (!jobs || !to || max_jobs < 0 || T_new < c->T) return GKV_E_ARG;
-  const int32_t nb_new = (int32_t)((T_new + P - 1) / P);
-  if (nb_new > c->nblk_cap) return GKV_E_SHAPE;
-  std::vector<int8_t> lv(nb_new);
-  st = gkv_ladder_levels(profile, T_new, lv.data(), nb_new);
-  if (st) return st;
-  const int64_t nb_old = (c->T + P - 1) / P;
+  const int64_t grow = T_new - c->T;
+  if ((c->T + grow + P - 1) / P > c->nblk_cap) return GKV_E_SHAPE;
+  std::vector<int8_t> lv;
+  int64_t lv_T = -1;  // the length whose ladder lv holds
   int32_t n = 0;
-  for (int b = 0; b < c->B; ++b)
+  for (int b = 0; b < c->B; ++b) {
+    const int64_t Tb = seq_tokens(c, b);
+    if (Tb < 0) continue;  // retired
+    const int64_t Tb_new = Tb + grow;
+    if (Tb_new != lv_T) {
+      const int32_t nb_new = (int32_t)((Tb_new + P - 1) / P);
+      lv.assign((size_t)nb_new + 1, 0);
+      st = gkv_ladder_levels(profile, Tb_new, lv.data(), nb_new);
+      if (st) return st;
+      lv_T = Tb_new;
+    }
+    const int64_t nb_old = (Tb + P - 1) / P;
     for (int h = 0; h < c->Hkv; ++h) {
       const int8_t *cl = c->level_host + ((int64_t)b * c->Hkv + h) * c->nblk_cap;
       if (memcmp(cl, lv.data(), (size_t)nb_old) == 0) continue;  // the common case: nothing crosses
@@ -112,6 +121,7 @@ extern "C" int32_t gkv_ladder_crossings(const gkv_cache *c, int32_t profile, int
         ++n;
       }
     }
+  }
   return n;
 }
 
@@ -187,6 +197,60 @@ extern "C" int64_t gkv_pool_used(const gkv_pool *p, int32_t level) {
 
 extern "C" void gkv_pool_destroy(gkv_pool *p) { delete p; }
 
+// ---------------------------------------------------------------- sequence lifecycle
+extern "C" gkv_status gkv_retire_sequence(gkv_cache *c, gkv_pool *pool, const int64_t *koff_host,
+                                          const int64_t *voff_host, int32_t b, void *stream) {
+  gkv_status st = gkv_validate_cache(c);
+  if (st) return st;
+  if (!c->seq_len_host || !pool || !koff_host || !voff_host) return GKV_E_ARG;
+  if (b < 0 || b >= c->B) return GKV_E_SHAPE;
+  const int64_t Tb = c->seq_len_host[b];
+  if (Tb < 0) return GKV_E_ARG;
+  const int64_t nblk = (Tb + P - 1) / P;
+  // every slot must be a used slot of its level, each listed once: checked before
+  // anything changes
+  std::vector<std::pair<int, int64_t>> slots;  // (level index, slot)
+  for (int h = 0; h < c->Hkv; ++h)
+    for (int64_t i = 0; i < nblk; ++i) {
+      const int64_t e = ((int64_t)b * c->Hkv + h) * c->nblk_cap + i;
+      const int li = level_slot(c->level_host[e]);
+      if (li < 0) return GKV_E_ARG;
+      const int64_t bb = block_bytes(kLevels[li]);
+      for (const int64_t off : {koff_host[e], voff_host[e]}) {
+        const int64_t rel = off - pool->base[li];
+        if (rel < 0 || rel % bb != 0 || rel / bb >= pool->cap[li] || !pool->used[li][rel / bb]) return GKV_E_ARG;
+        slots.emplace_back(li, rel / bb);
+      }
+    }
+  std::vector<std::pair<int, int64_t>> sorted = slots;
+  std::sort(sorted.begin(), sorted.end());
+  if (std::adjacent_find(sorted.begin(), sorted.end()) != sorted.end()) return GKV_E_ARG;
+  if (gkv_launch_set_len(c->seq_len, b, -1, (hipStream_t)stream) != GKV_OK) return GKV_E_HIP;
+  for (const auto &sl : slots) {
+    pool->used[sl.first][sl.second] = 0;
+    pool->nused[sl.first]--;
+    pool->free_list[sl.first].push_back(sl.second);
+  }
+  c->seq_len_host[b] = -1;
+  int64_t mx = 0;
+  for (int i = 0; i < c->B; ++i) mx = c->seq_len_host[i] > mx ? c->seq_len_host[i] : mx;
+  c->T = mx;
+  gkv_stamp(c);
+  return GKV_OK;
+}
+
+extern "C" gkv_status gkv_admit_sequence(gkv_cache *c, int32_t b, void *stream) {
+  gkv_status st = gkv_validate_cache(c);
+  if (st) return st;
+  if (!c->seq_len_host) return GKV_E_ARG;
+  if (b < 0 || b >= c->B) return GKV_E_SHAPE;
+  if (c->seq_len_host[b] != -1) return GKV_E_ARG;
+  if (gkv_launch_set_len(c->seq_len, b, 0, (hipStream_t)stream) != GKV_OK) return GKV_E_HIP;
+  c->seq_len_host[b] = 0;
+  gkv_stamp(c);
+  return GKV_OK;
+}
+
 // ---------------------------------------------------------------- validation
 gkv_status gkv_validate_cache(const gkv_cache *c) {
   if (!c) return GKV_E_ARG;
@@ -201,6 +265,16 @@ gkv_status gkv_validate_cache(const gkv_cache *c) {
     if (c->page != 16 && c->page != 32 && c->page != 64) return GKV_E_SHAPE;
     if (!c->boxes || c->npage_cap <= 0 || c->npage_cap % 64) return GKV_E_ARG;
     if (c->T / c->page > c->npage_cap) return GKV_E_SHAPE;
+  }
+  if (!c->seq_len != !c->seq_len_host) return GKV_E_ARG;
+  if (c->seq_len_host) {  // every length in [-1, T]; T the largest
+    int64_t mx = 0;
+    for (int b = 0; b < c->B; ++b) {
+      const int64_t t = c->seq_len_host[b];
+      if (t < -1 || t > c->T) return GKV_E_SHAPE;
+      mx = t > mx ? t : mx;
+    }
+    if (mx != c->T) return GKV_E_SHAPE;
   }
   if (c->nres < 0 || c->nres > c->nres_cap) return GKV_E_SHAPE;
   if (c->nres_cap > 0 && (!c->res_idx || !c->res_rows || !c->res_mask || !c->res_off)) return GKV_E_ARG;
@@ -229,23 +303,26 @@ extern "C" gkv_status gkv_account(const gkv_cache *c, const int32_t *pages, int3
   if (!out) return GKV_E_ARG;
   if (pages && (!c->page || topk <= 0)) return GKV_E_ARG;
   if (pages && c->nres && !res_idx) return GKV_E_ARG;
-  const int64_t nblk = (c->T + P - 1) / P;
   const int64_t box_bits = 2 * D * 16;
-  int64_t resident = 0, read = 0;
+  int64_t resident = 0, read = 0, values = 0;
   std::vector<uint8_t> touched;
-  for (int b = 0; b < c->B; ++b)
+  for (int b = 0; b < c->B; ++b) {
+    const int64_t T = seq_tokens(c, b);
+    if (T <= 0) continue;  // retired or empty
+    const int64_t nblk = (T + P - 1) / P;
+    values += (int64_t)c->Hkv * T * 2 * D;
     for (int h = 0; h < c->Hkv; ++h) {
       const int8_t *lv = c->level_host + ((int64_t)b * c->Hkv + h) * c->nblk_cap;
       int64_t graded = 0;
       for (int64_t i = 0; i < nblk; ++i) graded += 2 * block_bytes(lv[i]) * 8;
-      const int64_t boxes = c->page ? (c->T / c->page) * box_bits : 0;
+      const int64_t boxes = c->page ? (T / c->page) * box_bits : 0;
       const int64_t res = c->nres ? (int64_t)c->nres * (2 * D * 16 + 32) + nblk * 64 : 0;
       resident += graded + boxes + res;
       if (!pages) {
         read += graded + res;
         continue;
       }
-      const int64_t cur = (c->T - 1) / c->page;
+      const int64_t cur = (T - 1) / c->page;
       int64_t r = boxes;
       touched.assign(nblk, 0);
       const int32_t *pg = pages + ((int64_t)b * c->Hkv + h) * topk;
@@ -256,7 +333,7 @@ extern "C" gkv_status gkv_account(const gkv_cache *c, const int32_t *pages, int3
       std::sort(list.begin(), list.end());  // a page listed twice is read once
       list.erase(std::unique(list.begin(), list.end()), list.end());
       for (int64_t p : list) {
-        const int64_t t0 = p * c->page, t1 = t0 + c->page < c->T ? t0 + c->page : c->T;
+        const int64_t t0 = p * c->page, t1 = t0 + c->page < T ? t0 + c->page : T;
         for (int64_t t = t0; t < t1; ++t) {
           r += 2 * row_bits(lv[t / P]);
           touched[t / P] = 1;
@@ -269,21 +346,22 @@ extern "C" gkv_status gkv_account(const gkv_cache *c, const int32_t *pages, int3
           ++ntouched;
         }
       if (c->nres) {  // the residual rows of the read tokens and the touched blocks' masks
-        std::vector<uint8_t> in_read((size_t)c->T, 0);
+        std::vector<uint8_t> in_read((size_t)T, 0);
         for (int64_t p : list) {
-          const int64_t t0 = p * c->page, t1 = t0 + c->page < c->T ? t0 + c->page : c->T;
+          const int64_t t0 = p * c->page, t1 = t0 + c->page < T ? t0 + c->page : T;
           for (int64_t t = t0; t < t1; ++t) in_read[t] = 1;
         }
         const int32_t *ri = res_idx + ((int64_t)b * c->Hkv + h) * c->nres_cap;
         for (int32_t k = 0; k < c->nres; ++k)
-          if (ri[k] >= 0 && ri[k] < c->T && in_read[ri[k]]) r += 2 * D * 16 + 32;
+          if (ri[k] >= 0 && ri[k] < T && in_read[ri[k]]) r += 2 * D * 16 + 32;
         r += ntouched * 64;
       }
       read += r;
     }
+  }
   out->resident_bits = resident;
   out->read_bits = read;
-  out->values = (int64_t)c->B * c->Hkv * c->T * 2 * D;
+  out->values = values;
   return GKV_OK;
 }
 

@@ -3,6 +3,7 @@
 // radix-select kernel picks the first k of the order (key descending, index
 // ascending) and writes the winners in ascending index order.
 #include <hip/hip_runtime.h>
+#include <stdint.h>
 
 #include "gkv_internal.h"
 
@@ -53,7 +54,8 @@ constexpr int kScoreBatch = 32;  // box words in flight per lane
 template <int G, int HG>
 __global__ void __launch_bounds__(256) quest_score_kernel(const double *__restrict__ qt,
                                                           const uint16_t *__restrict__ boxes, int64_t npage_cap,
-                                                          int64_t npages, int Hkv, uint64_t *__restrict__ keys) {
+                                                          int64_t npages, int Hkv, uint64_t *__restrict__ keys,
+                                                          const int64_t *__restrict__ seq_len, int page) {
   constexpr int HPW = G / HG;
   __shared__ double ub[4][64];
   const int h = blockIdx.y, b = blockIdx.z;
@@ -98,11 +100,18 @@ __global__ void __launch_bounds__(256) quest_score_kernel(const double *__restri
 #pragma unroll
     for (int j = 1; j < HG; ++j) best = ub[w + j][lane] > best ? ub[w + j][lane] : best;
   }
-  if (on) keys[u * npage_cap + pg] = order_key(best);
+  // with per-sequence lengths, pages past a sequence's own ranked pages get the key 0,
+  // below every score: they rank last and the selection turns them into -1
+  int64_t nown = npages;
+  if (seq_len) nown = seq_len[b] > 0 ? (seq_len[b] - 1) / page : 0;
+  if (on) keys[u * npage_cap + pg] = pg < nown ? order_key(best) : 0ull;
 }
 
 // Select the first k of the order (key desc, index asc) among keys[0..n) of one
-// unit and write their indices ascending to out[0..k) (-1 padded).  Optionally
+// unit and write their indices ascending to out[0..k) (-1 padded).  With a
+// per-unit limit (Compressed-Quest pages of sequences of different lengths), the
+// last stage writes -1 for indices at or past the unit's limit (their keys are 0,
+// so they are the last of the selection).  Optionally
 // sets the selected tokens' bits in a per-64 mask.  One workgroup per unit.
 //
 // Long inputs are reduced in stages: the first k of the whole order all lie among
@@ -267,9 +276,15 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
                                                              int64_t n_all, int64_t slice, int k,
                                                              int32_t *__restrict__ out, int64_t out_stride,
                                                              uint64_t *mask, int64_t mask_stride,
-                                                             int64_t mask_words) {
+                                                             int64_t mask_words, const int64_t *seq_len, int Hkv,
+                                                             int page) {
   __shared__ SelShared sh;
   const int64_t u = blockIdx.y, base = (int64_t)blockIdx.x * slice;
+  int64_t limit = INT64_MAX;  // the unit's own ranked pages (last stage only)
+  if (seq_len && gridDim.x == 1) {
+    const int64_t t = seq_len[u / Hkv];
+    limit = t > 0 ? (t - 1) / page : 0;
+  }
   const int64_t n = n_all - base < slice ? n_all - base : slice;
   const uint64_t *key = keys + u * key_stride;
   const int32_t *ix = idx ? idx + u * idx_stride + base : nullptr;  // KPT > 0 only
@@ -406,7 +421,7 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
         const bool sel = kr[j] > thr || (kr[j] == thr && eq++ < eq_take);
         if (sel) {
           const int64_t t = ix ? (int64_t)ix[i] : base + i;
-          o[pos++] = (int32_t)t;
+          o[pos++] = t < limit ? (int32_t)t : -1;
           if (mk) atomicOr((unsigned long long *)&mk[t >> 6], 1ull << (t & 63));
         }
       }
@@ -432,7 +447,7 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
     const bool sel = g0 || (e0 && eq_rank < eq_take);
     const int64_t pos = b0 + g + (e < eq_take - b1 ? e : (eq_take - b1 > 0 ? eq_take - b1 : 0));
     if (sel) {
-      o[pos] = (int32_t)i;
+      o[pos] = i < limit ? (int32_t)i : -1;
       if (mk) atomicOr((unsigned long long *)&mk[i >> 6], 1ull << (i & 63));
     }
     if (tid == 0) {
@@ -446,12 +461,14 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
 constexpr int64_t kSelSlice = (int64_t)kSelKPT * kSelThreads;
 
 // idx_ws: two index lists of `key_stride` entries per unit (the stages' candidates).
+// seq_len, Hkv, page: the per-unit limit of Compressed-Quest pages (seq_len null: none).
 void launch_select(const uint64_t *keys, int64_t key_stride, int64_t n, int k, int32_t *out, int64_t out_stride,
                    uint64_t *mask, int64_t mask_stride, int64_t mask_words, int units, int32_t *idx_ws,
-                   hipStream_t s) {
+                   hipStream_t s, const int64_t *seq_len = nullptr, int Hkv = 1, int page = 1) {
   if (n > kSelSlice && 2 * (int64_t)k > kSelSlice) {  // too few candidates dropped per stage: one streamed pass
     hipLaunchKernelGGL(select_kernel<0>, dim3(1, units), dim3(kSelThreads), 0, s, keys, key_stride,
-                       (const int32_t *)nullptr, (int64_t)0, n, n, k, out, out_stride, mask, mask_stride, mask_words);
+                       (const int32_t *)nullptr, (int64_t)0, n, n, k, out, out_stride, mask, mask_stride, mask_words,
+                       seq_len, Hkv, page);
     return;
   }
   const int32_t *idx = nullptr;
@@ -461,13 +478,13 @@ void launch_select(const uint64_t *keys, int64_t key_stride, int64_t n, int k, i
     int32_t *dst = idx_ws + (int64_t)buf * units * key_stride;
     hipLaunchKernelGGL(select_kernel<kSelKPT>, dim3((unsigned)S, units), dim3(kSelThreads), 0, s, keys, key_stride,
                        idx, key_stride, cur, kSelSlice, k, dst, key_stride, (uint64_t *)nullptr, (int64_t)0,
-                       (int64_t)0);
+                       (int64_t)0, seq_len, Hkv, page);
     const int64_t last = cur - (S - 1) * kSelSlice;
     cur = (S - 1) * k + (last < k ? last : k);
     idx = dst;
   }
   hipLaunchKernelGGL(select_kernel<kSelKPT>, dim3(1, units), dim3(kSelThreads), 0, s, keys, key_stride, idx,
-                     key_stride, cur, cur, k, out, out_stride, mask, mask_stride, mask_words);
+                     key_stride, cur, cur, k, out, out_stride, mask, mask_stride, mask_words, seq_len, Hkv, page);
 }
 
 // Copy the exact key/value rows of the selected residual tokens into exact-format
@@ -583,7 +600,7 @@ extern "C" gkv_status gkv_quest_select(const uint16_t *q, const gkv_cache *c, in
 #define GKV_SCORE(g, hg)                                                                                   \
   case g * 4 + hg - 1:                                                                                     \
     hipLaunchKernelGGL((quest_score_kernel<g, hg>), grid, dim3(256), 0, s, (const double *)qt, c->boxes,  \
-                       c->npage_cap, ncur, c->Hkv, keys);                                                  \
+                       c->npage_cap, ncur, c->Hkv, keys, (const int64_t *)c->seq_len, c->page);            \
     break;
       GKV_SCORE(1, 1) GKV_SCORE(3, 1) GKV_SCORE(5, 1) GKV_SCORE(7, 1) GKV_SCORE(9, 1) GKV_SCORE(11, 1)
       GKV_SCORE(13, 1) GKV_SCORE(15, 1)
@@ -596,7 +613,7 @@ extern "C" gkv_status gkv_quest_select(const uint16_t *q, const gkv_cache *c, in
   }
   int32_t *idx_ws = (int32_t *)(keys + (int64_t)c->B * c->Hkv * c->npage_cap);
   launch_select((const uint64_t *)keys, c->npage_cap, ncur, topk, pages, (int64_t)topk, nullptr, 0, 0, c->B * c->Hkv,
-                idx_ws, s);
+                idx_ws, s, (const int64_t *)c->seq_len, c->Hkv, c->page);
   return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP;
 }
 
@@ -606,6 +623,7 @@ extern "C" gkv_status gkv_rd_residual_select(gkv_cache *c, const uint16_t *k_src
   gkv_status st = gkv_validate_cache(c);
   if (st) return st;
   if (!k_src || !v_src || !mass || !ws || nkeep < 0) return GKV_E_ARG;
+  if (c->seq_len_host) return GKV_E_UNSUPPORTED;  // prefill-time selection on one length
   if (c->T <= 0) return GKV_E_SHAPE;
   if (nkeep > c->nres_cap || nkeep > c->T) return GKV_E_SHAPE;
   if (ws_bytes < rd_ws(c)) return GKV_E_WORKSPACE;

@@ -56,20 +56,40 @@ extern "C" int32_t gkv_layers_step(gkv_cache *const *caches, gkv_pool *const *po
     if (st) return st;
     const gkv_cache *c0 = caches[0], *c = caches[l];
     if (c->B != c0->B || c->Hkv != c0->Hkv || c->T != c0->T || c->nblk_cap != c0->nblk_cap) return GKV_E_SHAPE;
+    if (!c->seq_len_host != !c0->seq_len_host) return GKV_E_SHAPE;
+    if (c->seq_len_host)  // the layers of one batch hold the same sequences
+      for (int b = 0; b < c->B; ++b)
+        if (c->seq_len_host[b] != c0->seq_len_host[b]) return GKV_E_SHAPE;
   }
   const gkv_cache *c0 = caches[0];
-  const int64_t T = c0->T, units = (int64_t)c0->B * c0->Hkv, cap = c0->nblk_cap;
-  const bool open = T % P == 0;
-  if (T / P >= cap) return GKV_E_SHAPE;
+  const int64_t units = (int64_t)c0->B * c0->Hkv, cap = c0->nblk_cap;
+  // the block each unit writes into, and whether the token opens it (per sequence)
+  std::vector<int64_t> ublk(units, -1);
+  std::vector<char> uopen(units, 0);
+  bool any_open = false;
+  for (int b = 0; b < c0->B; ++b) {
+    const int64_t Tb = seq_tokens(c0, b);
+    if (Tb < 0) continue;  // retired
+    if (Tb / P >= cap) return GKV_E_SHAPE;
+    for (int h = 0; h < c0->Hkv; ++h) {
+      ublk[(int64_t)b * c0->Hkv + h] = Tb / P;
+      uopen[(int64_t)b * c0->Hkv + h] = Tb % P == 0;
+    }
+    any_open |= Tb % P == 0;
+  }
   // what gkv_append would reject, rejected here before any slot is taken
-  if (open && units > GKV_MAX_APPEND_UNITS) return GKV_E_UNSUPPORTED;
+  if (any_open && units > GKV_MAX_APPEND_UNITS) return GKV_E_UNSUPPORTED;
+  if (c0->seq_len_host && c0->B > GKV_MAX_APPEND_UNITS) return GKV_E_UNSUPPORTED;
   for (int l = 0; l < L; ++l) {
     const gkv_cache *c = caches[l];
-    if (c->page && (T + 1) / c->page > c->npage_cap) return GKV_E_SHAPE;
-    if (!open)
-      for (int64_t u = 0; u < units; ++u)
-        if (c->level_host[u * cap + T / P] != GKV_EXACT) return GKV_E_ARG;
+    for (int b = 0; b < c->B; ++b) {
+      const int64_t Tb = seq_tokens(c, b);
+      if (Tb >= 0 && c->page && (Tb + 1) / c->page > c->npage_cap) return GKV_E_SHAPE;
+    }
+    for (int64_t u = 0; u < units; ++u)
+      if (ublk[u] >= 0 && !uopen[u] && c->level_host[u * cap + ublk[u]] != GKV_EXACT) return GKV_E_ARG;
   }
+  const int64_t T = c0->T;
   // every layer's crossings of T + 1 (the block the token opens never crosses); a
   // layer whose levels the profile would raise fails the call here
   std::vector<Crossings> cr(L);
@@ -95,11 +115,11 @@ extern "C" int32_t gkv_layers_step(gkv_cache *const *caches, gkv_pool *const *po
   for (int l = 0; l < L; ++l) {
     taken[l].pool = pools[l];
     bool ok = true;
-    if (open) {
-      nk[l].resize(units);
-      nv[l].resize(units);
+    if (any_open) {
+      nk[l].assign(units, -1);
+      nv[l].assign(units, -1);
       for (int64_t u = 0; u < units && ok; ++u)
-        ok = taken[l].take(GKV_EXACT, nk[l][u]) && taken[l].take(GKV_EXACT, nv[l][u]);
+        if (uopen[u]) ok = taken[l].take(GKV_EXACT, nk[l][u]) && taken[l].take(GKV_EXACT, nv[l][u]);
     }
     const int32_t n = cr[l].n;
     dk[l].resize(n);
@@ -122,16 +142,16 @@ extern "C" int32_t gkv_layers_step(gkv_cache *const *caches, gkv_pool *const *po
     const int32_t n = cr[l].n;
     const int32_t *jobs = cr[l].jobs.data();
     const int8_t *to = cr[l].to.data();
-    gkv_status st = gkv_append(c, k_new + l * row, v_new + l * row, open ? nk[l].data() : nullptr,
-                               open ? nv[l].data() : nullptr, stream);
+    gkv_status st = gkv_append(c, k_new + l * row, v_new + l * row, any_open ? nk[l].data() : nullptr,
+                               any_open ? nv[l].data() : nullptr, stream);
     if (st) {  // layers before l are stepped; nothing of layer l or later is
       give_back_from(l);
       return st;
     }
-    if (open)
-      for (int64_t u = 0; u < units; ++u) {
-        koff_host[l][u * cap + T / P] = nk[l][u];
-        voff_host[l][u * cap + T / P] = nv[l][u];
+    for (int64_t u = 0; u < units; ++u)
+      if (uopen[u]) {
+        koff_host[l][u * cap + ublk[u]] = nk[l][u];
+        voff_host[l][u * cap + ublk[u]] = nv[l][u];
       }
     total += n;
     if (!n) continue;

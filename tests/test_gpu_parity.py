@@ -1030,3 +1030,155 @@ def test_quest_read_with_residual_rows(gpu, page, T, topk, frac, Bn):
             read_bits += o["read_bits"]
     r = cache.account(pages_d)
     assert r["resident_bits"] == res_bits and r["read_bits"] == read_bits
+
+
+# ---------------------------------------------------------------- sequences of different lengths
+
+
+def _ragged_levels(lens, Hkv, profile="graded"):
+    nb = (max(lens) + 63) // 64
+    lv = np.full((len(lens), Hkv, nb), 16, np.int8)
+    for b, t in enumerate(lens):
+        lv[b, :, :(t + 63) // 64] = olad.ladder(profile, t)
+    return lv
+
+
+def _check_ragged(cache, ucs, keys, q, lens, G, topk, page, live):
+    """Dense and Compressed-Quest reads of every live sequence against its oracle unit
+    (pages bit-exact; keys[b, h] is the unit's exact key stream), zeros for retired
+    ones."""
+    Hkv = cache.Hkv
+    out = cache.decode(q).cpu().numpy()
+    pages = cache.quest_select(q, topk)
+    outq = cache.decode(q, pages=pages).cpu().numpy()
+    pages = pages.cpu().numpy()
+    for b in range(cache.B):
+        if not live[b]:
+            assert np.all(out[b] == 0) and np.all(outq[b] == 0) and np.all(pages[b] == -1)
+            continue
+        for h in range(Hkv):
+            uc = ucs[b, h]
+            assert uc.T == lens[b]
+            qg = q_group(q, b, h, G)
+            assert max_err(out[b, h * G:(h + 1) * G], uc.decode_dense(qg)) <= TOL
+            kmin, kmax = oquest.page_boxes(keys[b, h][:lens[b]], page)
+            want = oquest.quest_select(qg, kmin, kmax, lens[b], topk, page)
+            np.testing.assert_array_equal(pages[b, h], want)
+            assert max_err(outq[b, h * G:(h + 1) * G], uc.decode_quest(qg, want, page)) <= TOL
+
+
+def test_ragged_batch_appends_retire_and_admit(gpu):
+    """Four sequences of different lengths in one batch (section 3.7 serving: the block
+    manager's incremental appends): each is its own oracle unit.  Dense and
+    Compressed-Quest reads, then 70 decode steps of appends in which every sequence
+    opens blocks and crosses ladder boundaries at its own length (records bit-exact);
+    sequence 2 is retired at step 30 (its slots go back to the pool, its outputs are
+    zero) and admitted again as a new, empty sequence at step 45."""
+    torch = _torch()
+    lens0 = [1000, 64 * 23 + 17, 700, 64 * 30 - 3]
+    Bn, Hq, Hkv, page, topk, steps = 4, 8, 2, 16, 24, 70
+    G = Hq // Hkv
+    Tmax = max(lens0) + steps
+    ks, vs = kv_all(46, Bn, Hkv, Tmax)
+    kn2, vn2 = kv_all(47, 1, Hkv, steps)  # the admitted sequence's tokens
+    lv = _ragged_levels(lens0, Hkv)
+    cache = _build(gpu, ks[:, :, :max(lens0)], vs[:, :, :max(lens0)], Hq, lv, page=page, seq_lens=lens0,
+                   extra_blocks=4, slack={16: 8, 8: 8, 4: 8, 2: 8, 1: 8})
+    ucs, keys = {}, {}
+    for b in range(Bn):
+        for h in range(Hkv):
+            t = lens0[b]
+            ucs[b, h] = ocache.UnitCache(ks[b, h, :t], vs[b, h, :t], lv[b, h, :(t + 63) // 64])
+            keys[b, h] = ks[b, h]
+    lens = list(lens0)
+    live = [True] * Bn
+    q = synth.queries(46, Bn, Hq)
+    _check_ragged(cache, ucs, keys, q, lens, G, topk, page, live)
+    pos = list(lens0)  # next token of each sequence's own stream
+    moves_seen = 0
+    for s in range(steps):
+        if s == 30:
+            used = {L: cache.pool.used(L) for L in gpu.LEVELS}
+            nb2 = (lens[2] + 63) // 64
+            freed = {L: 2 * int((cache.level_host[2, :, :nb2] == L).sum()) for L in gpu.LEVELS}
+            cache.retire(2)
+            assert all(cache.pool.used(L) == used[L] - freed[L] for L in gpu.LEVELS)
+            live[2] = False
+            lens[2] = -1
+            assert list(cache.lengths()) == lens
+        if s == 45:
+            cache.admit(2)
+            live[2] = True
+            lens[2] = 0
+            pos[2] = 0
+            ucs[2, 0] = ocache.UnitCache(kn2[0, 0, :0], vn2[0, 0, :0], [])
+            ucs[2, 1] = ocache.UnitCache(kn2[0, 1, :0], vn2[0, 1, :0], [])
+            keys[2, 0], keys[2, 1] = kn2[0, 0], kn2[0, 1]
+        kn = np.zeros((Bn, Hkv, 128), np.uint16)
+        vn = np.zeros((Bn, Hkv, 128), np.uint16)
+        for b in range(Bn):
+            if not live[b]:
+                continue
+            src_k, src_v = (kn2[0], vn2[0]) if (b == 2 and s >= 45) else (ks[b], vs[b])
+            kn[b], vn[b] = src_k[:, pos[b]], src_v[:, pos[b]]
+        moves = cache.append(kn, vn, profile="graded")
+        want = []
+        for b in range(Bn):
+            if not live[b]:
+                continue
+            for h in range(Hkv):
+                for blk, old, new in ucs[b, h].append(kn[b, h], vn[b, h], "graded"):
+                    want.append((b, h, blk, old, new))
+            pos[b] += 1
+            lens[b] += 1
+        assert sorted(moves) == sorted(want)
+        moves_seen += len(moves)
+        assert list(cache.lengths()) == lens
+        if s % 23 == 22 or s == steps - 1:
+            qs = synth.queries(46, Bn, Hq, step=s + 1)
+            _check_ragged(cache, ucs, keys, qs, lens, G, topk, page, live)
+    assert moves_seen > 0
+    for b in range(Bn):
+        for h in range(Hkv):
+            for blk in range(lens[b] // 64):  # complete blocks
+                compare_record(cache, ucs[b, h], b, h, blk, 0)
+                compare_record(cache, ucs[b, h], b, h, blk, 1)
+    r = cache.account()
+    want_bits = sum(oacc.unit_rates(ucs[b, h].levels, lens[b], page=page)["resident_bits"]
+                    for b in range(Bn) for h in range(Hkv))
+    assert r["resident_bits"] == want_bits
+
+
+def test_layers_step_with_sequences_of_different_lengths(gpu):
+    """gkv_layers_step over two layers of a batch of three sequences of different
+    lengths: every sequence opens blocks and crosses ladder boundaries at its own
+    length; the service equals per-layer appends step by step (levels, offsets, pool
+    use, decode outputs bit for bit)."""
+    torch = _torch()
+    L, Bn, Hq, Hkv, steps = 2, 3, 8, 2, 70
+    lens = [64 * 10 - 1, 64 * 7 + 3, 64 * 12]
+    data = [kv_all(80 + l, Bn, Hkv, max(lens) + steps) for l in range(L)]
+    lv = _ragged_levels(lens, Hkv, "tiny")  # 4 exact, 8 int8, 12 int4 blocks: crossings at these lengths
+    slack = {16: 16, 8: 16, 4: 16, 2: 16, 1: 8}
+    mk = lambda ks, vs: _build(gpu, ks[:, :, :max(lens)], vs[:, :, :max(lens)], Hq, lv, page=16, extra_blocks=4,
+                               slack=slack, seq_lens=lens)
+    svc = gpu.LayerCaches([mk(*d) for d in data], "tiny")
+    ref = [mk(*d) for d in data]
+    total = 0
+    for s in range(steps):
+        kn = np.stack([np.stack([d[0][b, :, lens[b] + s] for b in range(Bn)]) for d in data])
+        vn = np.stack([np.stack([d[1][b, :, lens[b] + s] for b in range(Bn)]) for d in data])
+        n = svc.step(kn, vn)
+        moves = [r.append(kn[l], vn[l], profile="tiny") for l, r in enumerate(ref)]
+        assert sum(len(m) for m in moves) == n
+        total += n
+        q = synth.queries(81, Bn, Hq, step=s)
+        for l in range(L):
+            a, b = svc.caches[l], ref[l]
+            assert list(a.lengths()) == list(b.lengths()) == [t + s + 1 for t in lens]
+            np.testing.assert_array_equal(a.level_host, b.level_host)
+            np.testing.assert_array_equal(a.koff_host, b.koff_host)
+            np.testing.assert_array_equal(a.voff_host, b.voff_host)
+            assert all(a.pool.used(x) == b.pool.used(x) for x in gpu.LEVELS)
+            assert torch.equal(a.decode(q), b.decode(q))
+    assert total > 0

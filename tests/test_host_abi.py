@@ -427,3 +427,81 @@ def test_account_quest_with_residual_by_hand(B):
     o = oacc.unit_rates(lv, T, page=16, nres=len(res), pages=pages[0, 0], res_idx=res)
     assert rates.read_bits == o["read_bits"] and rates.resident_bits == o["resident_bits"]
     assert B._account(ctypes.byref(c), B._np_ptr(pages), pages.shape[-1], None, ctypes.byref(rates)) == -1
+
+
+def _ragged_cache(B, lens, Hkv=2, page=0):
+    """A host-only cache of sequences of different lengths (levels: each sequence's
+    own graded ladder)."""
+    T = int(max(lens))
+    nb = (T + 63) // 64
+    lv = np.zeros((len(lens), Hkv, nb), np.int8)
+    for b, t in enumerate(lens):
+        if t > 0:
+            lv[b, :, :(t + 63) // 64] = olad.ladder("graded", t)
+    c, keep = _host_cache(B, len(lens), Hkv, 4 * Hkv, T, lv, page=page)
+    sl = np.array(lens, np.int64)
+    keep["sl"], keep["sld"] = sl, np.zeros(len(lens), np.int64)
+    c.seq_len_host, c.seq_len = sl.ctypes.data, keep["sld"].ctypes.data
+    return c, keep
+
+
+def test_ragged_lengths_validation_crossings_and_accounting(B):
+    """Per-sequence lengths: T must be the largest length and every length in
+    [-1, T]; the crossings of one more token are each sequence's own (the oracle's
+    ladder at its length + 1, a retired sequence none); the accounting counts every
+    sequence at its own length and a retired one not at all."""
+    lens = [64 * 40, 64 * 25 + 7, -1, 64 * 33]
+    c, keep = _ragged_cache(B, lens)
+    jobs = np.zeros(3 * 256, np.int32)
+    to = np.zeros(256, np.int8)
+    n = B._ladder_crossings(ctypes.byref(c), 1, c.T + 1, B._np_ptr(jobs), B._np_ptr(to), 256)
+    want = []
+    for b, t in enumerate(lens):
+        if t < 0:
+            continue
+        for blk, old, new in olad.crossings("graded", t, t + 1):
+            want += [(b, h, blk, new) for h in range(2)]
+    assert n == len(want) and n > 0
+    got = sorted((int(jobs[3 * i]), int(jobs[3 * i + 1]), int(jobs[3 * i + 2]), int(to[i])) for i in range(n))
+    assert got == sorted(want)
+    rates = B.Rates()
+    assert B._account(ctypes.byref(c), None, 0, None, ctypes.byref(rates)) == 0
+    res = sum(2 * oacc.unit_rates(olad.ladder("graded", t), t)["resident_bits"] for t in lens if t > 0)
+    assert rates.resident_bits == res and rates.read_bits == res
+    assert rates.values == sum(2 * t * 2 * 128 for t in lens if t > 0)
+    keep["sl"][0] = c.T + 1  # longer than T
+    assert B._account(ctypes.byref(c), None, 0, None, ctypes.byref(rates)) == -2
+    keep["sl"][0] = 5  # T no longer the largest length
+    assert B._account(ctypes.byref(c), None, 0, None, ctypes.byref(rates)) == -2
+    keep["sl"][0] = -2
+    assert B._account(ctypes.byref(c), None, 0, None, ctypes.byref(rates)) == -2
+
+
+def test_retire_checks_every_slot_before_anything_changes(B):
+    """gkv_retire_sequence refuses (before any device work) a retired sequence, a
+    cache without per-sequence lengths, and a sequence whose offsets are not used
+    slots of the pool, leaving the pool and the lengths unchanged."""
+    lens = [64 * 3, 64 * 2 + 5]
+    c, keep = _ragged_cache(B, lens, Hkv=1)
+    pool = B.Pool({L: 16 for L in B.LEVELS})
+    nb = c.nblk_cap
+    ko = np.zeros((2, 1, nb), np.int64)
+    vo = np.zeros((2, 1, nb), np.int64)
+    for b, t in enumerate(lens):
+        for i in range((t + 63) // 64):
+            L = int(keep["lv"][b, 0, i])
+            ko[b, 0, i], vo[b, 0, i] = pool.alloc(L), pool.alloc(L)
+    used = [pool.used(L) for L in B.LEVELS]
+    retire = lambda b: B._retire(ctypes.byref(c), pool.h, B._np_ptr(ko), B._np_ptr(vo), b, None)
+    ko[1, 0, 1] += 7  # not a slot boundary
+    assert retire(1) == -1
+    ko[1, 0, 1] -= 7
+    vo[1, 0, 0] = ko[1, 0, 0]  # one slot listed twice
+    assert retire(1) == -1
+    keep["sl"][1] = -1
+    c.T = 64 * 3
+    assert retire(1) == -1  # already retired
+    assert [pool.used(L) for L in B.LEVELS] == used
+    assert list(keep["sl"]) == [64 * 3, -1]
+    c2, _ = _host_cache(B, 1, 1, 4, 128, olad.ladder("exact", 128))
+    assert B._retire(ctypes.byref(c2), pool.h, B._np_ptr(ko), B._np_ptr(vo), 0, None) == -1
