@@ -402,6 +402,14 @@ int32_t gkv_layers_step(gkv_cache *const *caches, gkv_pool *const *pools, int64_
                         int64_t *const *voff_host, int32_t L, int32_t profile, const uint16_t *k_new,
                         const uint16_t *v_new, void *stream);
 
+/* ---------------------------------------------------------------- measurement */
+
+/* Streaming-read probe (measurement only, not part of the method): reads `bytes`
+ * (a multiple of 16, src 16-byte aligned) with nsink workgroups of 16-byte loads and
+ * writes one word per workgroup to sink [nsink], so that a timed call gives the HBM
+ * read rate a plain kernel reaches on this GPU. */
+gkv_status gkv_stream_read_probe(const void *src, int64_t bytes, uint32_t *sink, int32_t nsink, void *stream);
+
 /* ---------------------------------------------------------------- observer and allocation */
 
 /* Workspace bytes of gkv_observe_mass for these shapes, or -1 when they are invalid. */

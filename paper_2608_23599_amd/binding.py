@@ -85,6 +85,7 @@ _rd = _sig("gkv_rd_residual_select", _i32, [_P(CacheStruct), _vp, _vp, _vp, _i32
 _cache_changed = _sig("gkv_cache_changed", None, [_P(CacheStruct)])
 _retire = _sig("gkv_retire_sequence", _i32, [_P(CacheStruct), _vp, _vp, _vp, _i32, _vp])
 _admit = _sig("gkv_admit_sequence", _i32, [_P(CacheStruct), _i32, _vp])
+_stream_probe = _sig("gkv_stream_read_probe", _i32, [_vp, _i64, _vp, _i32, _vp])
 _attn_noalloc = _sig("gkv_graded_decode_attn_noalloc", _i32, [_vp, _P(CacheStruct), _vp, _i32, _vp, _vp])
 _noalloc_bytes = _sig("gkv_noalloc_scratch_bytes", _i64, [])
 _layers_step = _sig("gkv_layers_step", _i32, [_vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _vp])
@@ -104,7 +105,7 @@ EXPORTED = [
     "gkv_attn_plan", "gkv_attn_partials", "gkv_attn_merge", "gkv_graded_decode_attn_bound",
     "gkv_observe_ws_bytes", "gkv_observe_mass", "gkv_query_norms", "gkv_allocate_levels", "gkv_layers_step",
     "gkv_cache_changed", "gkv_graded_decode_attn_noalloc", "gkv_noalloc_scratch_bytes", "gkv_retire_sequence",
-    "gkv_admit_sequence",
+    "gkv_admit_sequence", "gkv_stream_read_probe",
 ]
 
 
@@ -189,6 +190,12 @@ def allocate_levels(k, mass, qn, c, tau, window, rounding="up"):
     _check(_allocate(_dptr(k), _dptr(mass), _dptr(qn), B, Hkv, T, float(c), float(tau), int(window),
                      ROUNDING[rounding], _dptr(lv), _stream()), "allocate_levels")
     return lv
+
+
+def stream_read_probe(buf, sink):
+    """gkv_stream_read_probe: one streaming read of a device buffer (measurement)."""
+    _check(_stream_probe(_dptr(buf), buf.numel() * buf.element_size(), _dptr(sink), sink.numel(), _stream()),
+           "stream_read_probe")
 
 
 def f64_to_f16(x):
@@ -616,6 +623,11 @@ class GradedCache:
                "rd_residual_select")
 
     # ------------------------------------------------------------ inspection
+    def pool_bits(self):
+        """Bits of the arena slots in use (the K and V records of every block), as the
+        slab pool counts them."""
+        return sum(self.pool.used(L) * block_bytes(L) for L in LEVELS) * 8
+
     def account(self, pages=None):
         r = Rates()
         if pages is not None:

@@ -505,3 +505,22 @@ def test_retire_checks_every_slot_before_anything_changes(B):
     assert list(keep["sl"]) == [64 * 3, -1]
     c2, _ = _host_cache(B, 1, 1, 4, 128, olad.ladder("exact", 128))
     assert B._retire(ctypes.byref(c2), pool.h, B._np_ptr(ko), B._np_ptr(vo), 0, None) == -1
+
+
+def test_pool_occupancy_equals_the_accounted_graded_bits(B):
+    """The resident rate measured from the slab pool (slots in use x record sizes)
+    equals the accounting's graded bits exactly: every block holds one K and one V
+    record of its level, and the record sizes are the accounting's block bits (the
+    paper compares a measured packed format with its accounting, section 5.7)."""
+    for prof, T in (("graded", 131072), ("tiny", 2048), ("rdv2", 5000)):
+        lv = olad.ladder(prof, T)
+        c, keep = _host_cache(B, 2, 2, 8, T, lv)
+        pool = B.Pool({L: 2 * 2 * 2 * int((lv == L).sum()) for L in B.LEVELS})
+        for _ in range(2 * 2):
+            for L in lv:
+                pool.alloc(int(L))
+                pool.alloc(int(L))
+        measured = sum(pool.used(L) * B.block_bytes(L) for L in B.LEVELS) * 8
+        rates = B.Rates()
+        assert B._account(ctypes.byref(c), None, 0, None, ctypes.byref(rates)) == 0
+        assert measured == rates.resident_bits
