@@ -405,9 +405,10 @@ int32_t gkv_layers_step(gkv_cache *const *caches, gkv_pool *const *pools, int64_
 /* ---------------------------------------------------------------- measurement */
 
 /* Streaming-read probe (measurement only, not part of the method): reads `bytes`
- * (a multiple of 16, src 16-byte aligned) with nsink workgroups of 16-byte loads and
- * writes one word per workgroup to sink [nsink], so that a timed call gives the HBM
- * read rate a plain kernel reaches on this GPU. */
+ * (a multiple of 16, src 16-byte aligned) with nsink workgroups, each reading one
+ * contiguous share with 16-byte nontemporal loads, and writes one word per workgroup
+ * to sink [nsink], so that a timed call gives the HBM read rate a plain kernel
+ * reaches on this GPU. */
 gkv_status gkv_stream_read_probe(const void *src, int64_t bytes, uint32_t *sink, int32_t nsink, void *stream);
 
 /* ---------------------------------------------------------------- observer and allocation */
