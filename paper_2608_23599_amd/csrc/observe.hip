@@ -22,200 +22,295 @@ using namespace gkv;
 namespace {
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
-typedef float f4 __attribute__((ext_vector_type(4)));
+typedef float f16x __attribute__((ext_vector_type(16)));
 
 union H8 {
   half8 h;
   uint4 v;
 };
 
-constexpr int kObsThreads = 512;  // 8 wavefronts
-constexpr int kObsBlocksPerWave = 16;
-constexpr int kObsChunk = 8 * kObsBlocksPerWave;  // blocks per workgroup
+constexpr int kObsWaves = 8;
+constexpr int kObsThreads = 64 * kObsWaves;
+constexpr int kObsBlocksPerWave = 128 / kObsWaves;
+constexpr int kObsChunk = kObsWaves * kObsBlocksPerWave;  // blocks per workgroup
 constexpr int kMaxRows = 512;
 constexpr float kNegInf = -__builtin_huge_valf();
+// A running sum may grow to this before its reference is moved to the block's maximum.
+constexpr float kSumLimit = 0x1p64f;
 
-__device__ __forceinline__ f4 mfma32(half8 a, half8 b, f4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+__device__ __forceinline__ f16x mfma32x32(half8 a, half8 b, f16x c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
 }
 
-// Query rows in LDS: row r holds 16 chunks of 8 channels; chunk c sits at position
-// c ^ (r & 15), so that the 16 rows read by one MFMA operand fall in distinct banks.
-__device__ __forceinline__ uint32_t qpos(int r, int c) { return (uint32_t)(r * 16 + (c ^ (r & 15))) * 16u; }
+// The logits use 32 x 32 x 16 MFMAs: A = 32 keys x 16 channels, B = 16 channels x
+// 32 query rows.  Lane l = 32 hf + j (j = l & 31, hf = l >> 5) supplies A row j
+// and B column j, channels 16 c + 8 hf .. + 7 of channel chunk c (0..7), and holds
+// accumulator element e of column j = query row j, key 8 (e >> 2) + 4 hf + (e & 3)
+// of the 32-key half kt of the block.
+//
+// Query rows in LDS in operand order: tile rt (32 rows), chunk c, lane l -> 16 bytes
+// at ((rt * 8 + c) * 64 + l) * 16, so that the 64 lanes of one read are contiguous.
+__device__ __forceinline__ uint32_t qoff(int rt, int c, int l) { return (uint32_t)((rt * 8 + c) * 64 + l) * 16u; }
 
-// This lane's key operands of one block: key 64 blk + 16 t + m16, channels
-// 32 i + 8 kg .. + 7 (zero beyond T).
-__device__ __forceinline__ void load_keys(H8 (&a)[4][4], const uint16_t *kb, int64_t T, int blk, int kg, int m16) {
+// This lane's key operands of one block (zero beyond T).  One load instruction takes
+// 32 bytes of each of 32 key rows, so the four loads that share a 128-byte line rely
+// on finding it in the caches: these are plain loads (with the nontemporal hint, lines
+// left the caches early and the bytes fetched from HBM grew by a quarter).
+__device__ __forceinline__ void load_keys(H8 (&a)[2][8], const uint16_t *kb, int64_t T, int blk, int j, int hf) {
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    const int64_t key = (int64_t)blk * P + 16 * t + m16;
+  for (int kt = 0; kt < 2; ++kt) {
+    const int64_t key = (int64_t)blk * P + 32 * kt + j;
+    const int64_t kk = key < T ? key : T - 1;  // in bounds; replaced by zero below
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      a[t][i].v = key < T ? *(const uint4 *)(kb + key * D + 32 * i + 8 * kg) : make_uint4(0, 0, 0, 0);
+    for (int c = 0; c < 8; ++c) {
+      const uint4 v = *(const uint4 *)(kb + kk * D + 16 * c + 8 * hf);
+      a[kt][c].v = key < T ? v : make_uint4(0, 0, 0, 0);
+    }
   }
 }
 
-// Sum and maximum over the 4 lanes of a row (lanes m16 + 16 kg): the row swaps pair
-// lane l with l ^ 32, then with l ^ 16.
-__device__ __forceinline__ float row_sum4(float x) {
-  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
-}
-__device__ __forceinline__ float row_max4(float x) {
-  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
-  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+// Logits of one (block, 32-row tile): acc[kt] = keys of half kt against the tile's rows;
+// qt = this lane's operand of the tile's chunk 0 in LDS.
+__device__ __forceinline__ void tile_logits(f16x (&acc)[2], const H8 (&a)[2][8], const uint8_t *qt) {
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt) acc[kt] = f16x{};
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    H8 qb;
+    qb.v = *(const uint4 *)(qt + c * 1024);
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) acc[kt] = mfma32x32(a[kt][c].h, qb.h, acc[kt]);
+  }
 }
 
-// Sum over the tile of exp2(s * sl2 - ref) across the 4 lanes of each row; with
-// MASKED only the keys <= last (and < T) count.  key0 is the key of s[0][0] for kg = 0.
+// This lane's query operands of one tile (qt = its operand of the tile's chunk 0).
+__device__ __forceinline__ void load_q(H8 (&qb)[8], const uint8_t *qt) {
+#pragma unroll
+  for (int c = 0; c < 8; ++c) qb[c].v = *(const uint4 *)(qt + c * 1024);
+}
+
+// Logits of one (block, 32-row tile) from query operands already in registers.
+__device__ __forceinline__ void tile_logits_q(f16x (&acc)[2], const H8 (&a)[2][8], const H8 (&qb)[8]) {
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt) acc[kt] = f16x{};
+#pragma unroll
+  for (int c = 0; c < 8; ++c)
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) acc[kt] = mfma32x32(a[kt][c].h, qb[c].h, acc[kt]);
+}
+
+// The two lanes of a row (l and l ^ 32) exchange and combine a value.
+__device__ __forceinline__ float row_sum2(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(a[0]) + __uint_as_float(a[1]);
+}
+__device__ __forceinline__ float row_max2(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+}
+
+// Key of accumulator element e of half kt for this lane (relative to the block start).
+__device__ __forceinline__ int elem_key(int kt, int e, int hf) { return 32 * kt + 8 * (e >> 2) + 4 * hf + (e & 3); }
+
+// sum over the row's visible keys of exp2(s * sl2 - ref); with MASKED only the keys
+// key0 + k <= last (and < T) count.
 template <bool MASKED>
-__device__ __forceinline__ float tile_sum(const f4 (&s)[4], float sl2, float ref, int64_t key0, int kg,
+__device__ __forceinline__ float tile_sum(const f16x (&acc)[2], float sl2, float ref, int64_t key0, int hf,
                                           int64_t last, int64_t T) {
-  float x[16];
+  float x[32];
 #pragma unroll
-  for (int t = 0; t < 4; ++t)
+  for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      x[4 * t + e] = __builtin_amdgcn_exp2f(fmaf(s[t][e], sl2, -ref));
+    for (int e = 0; e < 16; ++e) {
+      float v = __builtin_amdgcn_exp2f(fmaf(acc[kt][e], sl2, -ref));
       if (MASKED) {
-        const int64_t key = key0 + 16 * t + 4 * kg + e;
-        x[4 * t + e] = key <= last && key < T ? x[4 * t + e] : 0.f;
+        const int64_t key = key0 + elem_key(kt, e, hf);
+        v = key <= last && key < T ? v : 0.f;
       }
+      x[16 * kt + e] = v;
     }
 #pragma unroll
-  for (int w = 8; w >= 1; w >>= 1)  // pairwise: a chain of depth 4
+  for (int w = 16; w >= 1; w >>= 1)  // pairwise: a chain of depth 5
 #pragma unroll
-    for (int j = 0; j < w; ++j) x[j] += x[j + w];
-  return row_sum4(x[0]);
+    for (int i = 0; i < w; ++i) x[i] += x[i + w];
+  return row_sum2(x[0]);
 }
 
 template <bool MASKED>
-__device__ __forceinline__ float tile_max(const f4 (&s)[4], float sl2, int64_t key0, int kg, int64_t last,
+__device__ __forceinline__ float tile_max(const f16x (&acc)[2], float sl2, int64_t key0, int hf, int64_t last,
                                           int64_t T) {
-  float bm = kNegInf;
+  float m = kNegInf;
 #pragma unroll
-  for (int t = 0; t < 4; ++t)
+  for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int64_t key = key0 + 16 * t + 4 * kg + e;
-      if (!MASKED || (key <= last && key < T)) bm = fmaxf(bm, s[t][e] * sl2);
+    for (int e = 0; e < 16; ++e) {
+      const int64_t key = key0 + elem_key(kt, e, hf);
+      if (!MASKED || (key <= last && key < T)) m = fmaxf(m, acc[kt][e] * sl2);
     }
-  return row_max4(bm);
+  return row_max2(m);
 }
 
-// Log-sum-exp (log2 units) of one (block, 16-row tile): sum_j exp2(x_j - ref) with
-// ref the row's running maximum, redone against the tile's own maximum when that
-// sum overflows (always on a row's first block, where ref = -inf).
+// Merges a block's log-sum-exp v (-inf: no visible key) into the running pair r of its
+// row, moving the reference to the larger of the two; written with selects only.
+__device__ __forceinline__ void merge_lse(float v, float2 &r) {
+  const bool valid = v > kNegInf;
+  const bool first = valid && r.y == 0.f;  // the row's first visible block
+  const bool up = v > r.x;
+  const float e = __builtin_amdgcn_exp2f(-__builtin_fabsf(v - r.x));  // 0 when v = -inf
+  const float y = up ? fmaf(r.y, e, 1.f) : r.y + e;
+  r.y = first ? 1.f : (valid ? y : r.y);
+  r.x = first || (valid && up) ? v : r.x;
+}
+
+// General path for one (block, tile): the block's log-sum-exp against its own maximum
+// (-inf when the row sees none of its keys), merged into the running pair r.
 template <bool MASKED>
-__device__ __forceinline__ float tile_lse(const f4 (&s)[4], float sl2, float ref, int64_t key0, int kg, int64_t last,
-                                          int64_t T) {
-  // a row's first block (ref = -inf) goes straight to the tile maximum
-  float sum = __any(ref == kNegInf) ? __builtin_inff() : tile_sum<MASKED>(s, sl2, ref, key0, kg, last, T);
-  if (__any(!(sum <= 0x1p100f))) {
-    ref = tile_max<MASKED>(s, sl2, key0, kg, last, T);
-    sum = ref == kNegInf ? 0.f : tile_sum<MASKED>(s, sl2, ref, key0, kg, last, T);
+__device__ __forceinline__ float tile_lse_general(const f16x (&acc)[2], float sl2, int64_t key0, int hf,
+                                                  int64_t last, int64_t T, float2 &r) {
+  const float ref = tile_max<MASKED>(acc, sl2, key0, hf, last, T);
+  const float ref0 = ref == kNegInf ? 0.f : ref;  // keeps the sum finite (it is 0 then)
+  const float sum = tile_sum<MASKED>(acc, sl2, ref0, key0, hf, last, T);
+  const float v = ref == kNegInf ? kNegInf : ref + __builtin_amdgcn_logf(sum);
+  merge_lse(v, r);
+  return v;
+}
+
+// One unmasked tile: sum_j exp2(x_j - ref) against the row's running reference
+// ref = r.x, so that the block adds exactly that sum to r.y and its log-sum-exp is
+// ref + log2(sum).  Every row starts at (ref, sum) = (0, 0).  The wavefront takes the
+// general path (uniformly) when some row's sum exceeds kSumLimit, or is below
+// 1 / kSumLimit while the row has no earlier block at or above the reference (so that
+// no block of the row can lose its precision).  The log-sum-exp goes to lse[0] and the
+// running pair to st[0].
+__device__ __forceinline__ void finish_tile(const f16x (&acc)[2], float sl2, int64_t key0, int hf, int64_t T,
+                                            float2 r, float *lse, float2 *st) {
+  const float sum = tile_sum<false>(acc, sl2, r.x, key0, hf, 0, T);
+  const bool ok = (sum <= kSumLimit) & ((sum >= 1.f / kSumLimit) | (r.y >= 1.f));
+  float v;
+  if (__builtin_expect(__builtin_amdgcn_ballot_w64(!ok) != 0, 0)) {
+    v = tile_lse_general<false>(acc, sl2, key0, hf, 0, T, r);
+  } else {
+    r.y += sum;
+    v = r.x + __builtin_amdgcn_logf(sum);  // -inf when every term is below fp32 range
   }
-  return sum > 0.f ? ref + __builtin_amdgcn_logf(sum) : kNegInf;
+  lse[0] = v;
+  st[0] = r;
 }
 
 // Logits and per-block log-sum-exp.  Each wavefront takes kObsBlocksPerWave blocks
-// and, per block, every 16-row tile of the group's queries: 16 MFMAs give the 64 x 16
+// and, per block, every 32-row tile of the group's queries: 16 MFMAs give the 64 x 32
 // logits, then sum_j exp2(x_j - ref) over the block's visible keys with ref the row's
-// running maximum of block log-sum-exps (kept in LDS per wavefront and row).  The
-// block's log-sum-exp is ref + log2(sum), whatever ref is, as long as the sum neither
-// overflows (then the tile is redone against the block's own maximum) nor loses all
-// its terms (a block 2^-126 below an earlier one, whose share is below fp32
-// resolution).  The running (max, sum) over the wavefront's blocks are merged over
-// the workgroup into one (max, sum) per (row, workgroup chunk).
+// running reference (kept in LDS per wavefront and row with the running sum of
+// exp2(lse - ref) over the wavefront's blocks).  While the vector ALUs work on tile
+// rt, the MFMAs of tile rt + 1 are issued in the same basic block, so the matrix cores
+// and the vector ALUs overlap.  The running pairs are merged over the workgroup into
+// one (max, sum) per (row, workgroup chunk).
 __global__ void __launch_bounds__(kObsThreads) obs_logit_kernel(const uint16_t *__restrict__ q_obs,
                                                                 const uint16_t *__restrict__ k_src, int n_obs,
                                                                 int G, int Hkv, int64_t T, int nblk, int Rpad,
                                                                 float sl2, float *__restrict__ lse,
                                                                 float2 *__restrict__ part) {
   extern __shared__ __align__(16) uint8_t qs[];
-  float2 *stats = (float2 *)(qs + Rpad * 256);  // [8 wavefronts][Rpad] running (max, sum)
+  float2 *stats = (float2 *)(qs + Rpad * 256);  // [kObsWaves][Rpad] running (reference, sum)
   const int h = blockIdx.y, b = blockIdx.z;
   const int64_t u = (int64_t)b * Hkv + h;
   const int R = n_obs * G, Hq = Hkv * G;
   for (int i = threadIdx.x; i < Rpad * 16; i += kObsThreads) {
-    const int r = i >> 4, c = i & 15;
+    const int r = i >> 4, cc = i & 15;  // row, 8-channel chunk
     uint4 v = make_uint4(0, 0, 0, 0);
     if (r < R) {
       const int qi = r / G, g = r - qi * G;
-      v = *(const uint4 *)(q_obs + (((int64_t)b * n_obs + qi) * Hq + h * G + g) * D + 8 * c);
+      v = *(const uint4 *)(q_obs + (((int64_t)b * n_obs + qi) * Hq + h * G + g) * D + 8 * cc);
     }
-    *(uint4 *)(qs + qpos(r, c)) = v;
+    *(uint4 *)(qs + qoff(r >> 5, cc >> 1, (r & 31) + 32 * (cc & 1))) = v;
   }
-  for (int i = threadIdx.x; i < 8 * Rpad; i += kObsThreads) stats[i] = make_float2(kNegInf, 0.f);
+  for (int i = threadIdx.x; i < kObsWaves * Rpad; i += kObsThreads) stats[i] = make_float2(0.f, 0.f);
   __syncthreads();
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, kg = lane >> 4, m16 = lane & 15;
-  float2 *wst = stats + wv * Rpad;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, j = lane & 31, hf = lane >> 5;
+  float2 *wst = stats + wv * Rpad + j;
   const uint16_t *kb = k_src + u * T * D;
   const int64_t first_masked = T - n_obs + 1;  // keys at or beyond this are hidden from some row
   const int blk0 = blockIdx.x * kObsChunk + wv * kObsBlocksPerWave;
   const int nb = blk0 >= nblk ? 0 : (nblk - blk0 < kObsBlocksPerWave ? nblk - blk0 : kObsBlocksPerWave);
-  H8 a[4][4];
+  const int nt = Rpad / 32;
+  const uint8_t *qlane = qs + lane * 16;
+  H8 a[2][8];
+  if (nb > 0) load_keys(a, kb, T, blk0, j, hf);
+  uint32_t pf0 = 0, pf1 = 0;
   for (int k = 0; k < nb; ++k) {
     const int blk = blk0 + k;
-    load_keys(a, kb, T, blk, kg, m16);
+    // The keys of block blk are in flight (issued when the previous block's last MFMAs
+    // were out).  Touch every 128-byte line of the next block now, so that its loads
+    // hit the L2 cache; the values only have to arrive before the next iteration.
+    asm volatile("" ::"v"(pf0), "v"(pf1));
+    if (k + 1 < nb) {
+      const int64_t lim = T * D - 2, e0 = (int64_t)(blk + 1) * P * D + lane * 64;
+      pf0 = *(const uint32_t *)(kb + (e0 < lim ? e0 : lim));
+      pf1 = *(const uint32_t *)(kb + (e0 + 4096 < lim ? e0 + 4096 : lim));
+    }
     const int64_t key0 = (int64_t)blk * P;
-    const bool masked = key0 + P > first_masked;  // uniform: the block has hidden keys
-    for (int rt = 0; rt < Rpad / 16; rt += 2) {  // two row tiles at a time (Rpad is a multiple of 32)
-      int row[2];
-      H8 qb[2][4];
-      float2 run[2];
-      f4 s[2][4];
-#pragma unroll
-      for (int p = 0; p < 2; ++p) {
-        row[p] = 16 * (rt + p) + m16;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) qb[p][i].v = *(const uint4 *)(qs + qpos(row[p], 4 * i + kg));
-        run[p] = wst[row[p]];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) s[p][t] = f4{0, 0, 0, 0};
+    float *lse_blk = lse + (u * nblk + blk) * Rpad + j;
+    f16x cur[2];
+    tile_logits(cur, a, qlane);
+    if (key0 + P > first_masked) {  // uniform: some row does not see every key of the block
+      for (int rt = 0; rt < nt; ++rt) {
+        if (rt > 0) tile_logits(cur, a, qlane + rt * 8192);
+        const int row = 32 * rt + j;
+        const int64_t last = T - n_obs + row / G;  // the last key this row sees
+        float2 r = wst[32 * rt];
+        const float v = tile_lse_general<true>(cur, sl2, key0, hf, last, T, r);
+        lse_blk[32 * rt] = v;
+        wst[32 * rt] = r;
       }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)  // eight independent accumulation chains
-#pragma unroll
-        for (int p = 0; p < 2; ++p)
-#pragma unroll
-          for (int t = 0; t < 4; ++t) s[p][t] = mfma32(a[t][i].h, qb[p][i].h, s[p][t]);
-      // s[p][t][e]: key 64 blk + 16 t + 4 kg + e, query row row[p]
-#pragma unroll
-      for (int p = 0; p < 2; ++p) {
-        const int64_t last = T - n_obs + row[p] / G;  // the last key this row sees
-        const float v = masked ? tile_lse<true>(s[p], sl2, run[p].x, key0, kg, last, T)
-                               : tile_lse<false>(s[p], sl2, run[p].x, key0, kg, last, T);
-        if (kg == 0 && row[p] < R) {
-          lse[(u * nblk + blk) * Rpad + row[p]] = v;
-          if (v != kNegInf) {  // the wavefront's running (max, sum) of this row
-            float2 r2 = run[p];
-            if (v > r2.x) {
-              r2.y = r2.y * __builtin_amdgcn_exp2f(r2.x - v) + 1.f;
-              r2.x = v;
-            } else {
-              r2.y += __builtin_amdgcn_exp2f(v - r2.x);
-            }
-            wst[row[p]] = r2;
-          }
-        }
-      }
+      if (k + 1 < nb) load_keys(a, kb, T, blk + 1, j, hf);
+      continue;
+    }
+    // Unmasked: software-pipelined over the row tiles, unrolled by two so that the two
+    // accumulator sets trade roles (tile rt in one set while the MFMAs of tile rt + 1
+    // fill the other) without copies, which would wait for the MFMAs to drain.  The
+    // query operands of a tile are read from LDS one tile ahead of its MFMAs.
+    H8 qb[8];
+    load_q(qb, qlane + (nt > 1 ? 8192 : 0));  // tile 1 (tile 0 is in cur)
+    f16x alt[2];
+    float2 r = wst[0];
+    int rt = 0;
+    for (; rt + 2 < nt; rt += 2) {
+      tile_logits_q(alt, a, qb);
+      load_q(qb, qlane + (rt + 2) * 8192);
+      float2 r_next = wst[32 * (rt + 1)];
+      finish_tile(cur, sl2, key0, hf, T, r, lse_blk + 32 * rt, wst + 32 * rt);
+      r = r_next;
+      tile_logits_q(cur, a, qb);
+      load_q(qb, qlane + (rt + 3 < nt ? rt + 3 : nt - 1) * 8192);
+      r_next = wst[32 * (rt + 2)];
+      finish_tile(alt, sl2, key0, hf, T, r, lse_blk + 32 * (rt + 1), wst + 32 * (rt + 1));
+      r = r_next;
+    }
+    if (rt + 1 < nt) {  // two tiles left: rt in cur, rt + 1 (operands in qb) still to compute
+      tile_logits_q(alt, a, qb);
+      const float2 r_next = wst[32 * (rt + 1)];
+      if (k + 1 < nb) load_keys(a, kb, T, blk + 1, j, hf);  // the block's MFMAs are all issued
+      finish_tile(cur, sl2, key0, hf, T, r, lse_blk + 32 * rt, wst + 32 * rt);
+      r = r_next;
+      finish_tile(alt, sl2, key0, hf, T, r, lse_blk + 32 * (rt + 1), wst + 32 * (rt + 1));
+    } else {  // one tile left, in cur
+      if (k + 1 < nb) load_keys(a, kb, T, blk + 1, j, hf);
+      finish_tile(cur, sl2, key0, hf, T, r, lse_blk + 32 * rt, wst + 32 * rt);
     }
   }
   __syncthreads();
   // merge the wavefronts' running sums: one (max, sum) per (row, chunk)
   for (int r = threadIdx.x; r < R; r += kObsThreads) {
-    float m = kNegInf;
-    for (int w = 0; w < 8; ++w) m = fmaxf(m, stats[w * Rpad + r].x);
+    float m = kNegInf;  // pairs with a zero sum hold no block
+    for (int w = 0; w < kObsWaves; ++w) {
+      const float2 p = stats[w * Rpad + r];
+      if (p.y > 0.f) m = fmaxf(m, p.x);
+    }
     float sm = 0.f;
     if (m != kNegInf)
-      for (int w = 0; w < 8; ++w) {
+      for (int w = 0; w < kObsWaves; ++w) {
         const float2 p = stats[w * Rpad + r];
-        if (p.x != kNegInf) sm += p.y * __builtin_amdgcn_exp2f(p.x - m);
+        if (p.y > 0.f) sm += p.y * __builtin_amdgcn_exp2f(p.x - m);
       }
     part[(u * gridDim.x + blockIdx.x) * Rpad + r] = make_float2(m, sm);
   }
@@ -394,7 +489,7 @@ extern "C" gkv_status gkv_observe_mass(const uint16_t *q_obs, int32_t n_obs, con
   float *rows = (float *)(w + L.rows);
   const int G = Hq / Hkv;
   const float sl2 = 1.4426950408889634f / sqrtf((float)D);
-  hipLaunchKernelGGL(obs_logit_kernel, dim3(L.nslice, Hkv, B), dim3(kObsThreads), L.Rpad * (256 + 8 * 8), s, q_obs,
+  hipLaunchKernelGGL(obs_logit_kernel, dim3(L.nslice, Hkv, B), dim3(kObsThreads), L.Rpad * (256 + 8 * kObsWaves), s, q_obs,
                      k_src, n_obs, G, Hkv, T, L.nblk, L.Rpad, sl2, lse, part);
   hipLaunchKernelGGL(obs_row_kernel, dim3((L.R + 3) / 4, Hkv, B), dim3(256), 0, s, part, L.R, L.Rpad, L.nslice, Hkv,
                      rows);

@@ -41,6 +41,39 @@ def test_observer_mass_matches_oracle(gpu, B, Hq, Hkv, T, n_obs):
             assert abs(got[b, h].sum() - 1.0) < 1e-5
 
 
+def _extreme_inputs(kind, T=64 * 40 + 9, n_obs=8, Hq=4):
+    """fp16 bits of queries [1][n_obs][Hq][128] and keys [1][1][T][128] whose block sums
+    leave [2^-64, 2^64] against a reference of 0, so that the kernel's general path
+    (reference moved to the block maximum) runs: 'scaled' multiplies the queries by 8
+    (block sums up to about 2^134); 'cold' points the first three blocks' keys away
+    from a direction the queries share (their sums near 2^-92 while the row has no
+    earlier block), and the later blocks then lie about 2^100 above that reference."""
+    from oracle import fp16
+    ks, _ = kv_all(66, 1, 1, T)
+    q = _obs_queries(66, 1, n_obs, Hq)
+    qf = fp16.to_f64(np.asarray(q, dtype=np.uint16))
+    kf = fp16.to_f64(np.asarray(ks, dtype=np.uint16))
+    if kind == "scaled":
+        qf = qf * 8.0
+    else:
+        d = np.ones(128) / np.sqrt(128)
+        qf = qf * 0.25 + 4.0 * d
+        kf[0, 0, :192] = -192.0 * d
+    return qf.astype(np.float16).view(np.uint16), kf.astype(np.float16).view(np.uint16)
+
+
+@pytest.mark.parametrize("kind", ["scaled", "cold"])
+def test_observer_mass_extreme_logits(gpu, kind):
+    """Block sums far outside [2^-64, 2^64] of the running reference: fp32 logits of
+    up to about 130 (log2 units) stay within the same tolerance (an fp32 simulation
+    of these inputs lands below a tenth of it)."""
+    q_obs, ks = _extreme_inputs(kind)
+    got = gpu.observe_mass(q_obs, ks).cpu().numpy()
+    want = oobs.observe_mass(q_obs[0], ks[0, 0])
+    _mass_close(got[0, 0], want)
+    assert abs(got[0, 0].sum() - 1.0) < 1e-5
+
+
 def test_observer_ema_update(gpu):
     B, Hq, Hkv, T, n_obs = 1, 8, 2, 1500, 8
     ks, _ = kv_all(62, B, Hkv, T)
