@@ -343,25 +343,56 @@ __global__ void __launch_bounds__(256) obs_row_kernel(const float2 *__restrict__
   if (lane == 0) row_lse[u * Rpad + r] = m + __builtin_amdgcn_logf(s);  // every row sees key 0
 }
 
-// One wavefront per block: mean over rows of the block's share of each row.
+// Per block: the mean over rows of the block's share exp2(lse_block - lse_row) of each
+// row, blended into the mass with the EMA weight.  A workgroup takes 16 consecutive
+// blocks of one (b, h), four per wavefront; lane l holds rows 4 l .. 4 l + 3 and
+// 256 + 4 l .. + 3 (Rpad <= 512), so that one block is two 16-byte loads per lane, and
+// every load of the wavefront is issued before the first is used.
+constexpr int kMassWaveBlocks = 4;
+constexpr int kMassBlocks = 4 * kMassWaveBlocks;  // per workgroup
+
 __global__ void __launch_bounds__(256) obs_mass_kernel(const float *__restrict__ lse,
                                                        const float *__restrict__ row_lse, int R, int Rpad,
                                                        int nblk, int Hkv, float alpha, float *__restrict__ mass) {
-  const int lane = threadIdx.x & 63;
-  const int blk = blockIdx.x * 4 + (threadIdx.x >> 6), h = blockIdx.y, b = blockIdx.z;
-  if (blk >= nblk) return;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int h = blockIdx.y, b = blockIdx.z;
   const int64_t u = (int64_t)b * Hkv + h;
-  float acc = 0.f;
-  for (int r = lane; r < R; r += 64) {
-    const float v = lse[(u * nblk + blk) * Rpad + r];
-    if (v != kNegInf) acc += __builtin_amdgcn_exp2f(v - row_lse[u * Rpad + r]);
-  }
+  const int blk0 = (blockIdx.x * 4 + wv) * kMassWaveBlocks;
+  if (blk0 >= nblk) return;
+  float rl[8];
+  bool row_ok[8];
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) acc += __shfl_xor(acc, o);
-  if (lane == 0) {
-    const float m = acc / (float)R;
-    float *dst = mass + u * nblk + blk;
-    *dst = alpha == 1.f ? m : (1.f - alpha) * *dst + alpha * m;
+  for (int c = 0; c < 2; ++c) {
+    const int r0 = 256 * c + 4 * lane;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      row_ok[4 * c + i] = r0 + i < R;
+      rl[4 * c + i] = r0 + i < Rpad ? row_lse[u * Rpad + r0 + i] : 0.f;
+    }
+  }
+  float4 v[kMassWaveBlocks][2];
+#pragma unroll
+  for (int k = 0; k < kMassWaveBlocks; ++k)
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int r0 = 256 * c + 4 * lane;  // r0 < Rpad implies r0 + 3 < Rpad (Rpad % 32 == 0)
+      v[k][c] = blk0 + k < nblk && r0 < Rpad ? *(const float4 *)(lse + (u * nblk + blk0 + k) * Rpad + r0)
+                                             : make_float4(kNegInf, kNegInf, kNegInf, kNegInf);
+    }
+#pragma unroll
+  for (int k = 0; k < kMassWaveBlocks; ++k) {
+    const float x[8] = {v[k][0].x, v[k][0].y, v[k][0].z, v[k][0].w, v[k][1].x, v[k][1].y, v[k][1].z, v[k][1].w};
+    float acc = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      if (row_ok[i] && x[i] != kNegInf) acc += __builtin_amdgcn_exp2f(x[i] - rl[i]);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) acc += __shfl_xor(acc, o);
+    if (lane == 0 && blk0 + k < nblk) {
+      const float m = acc / (float)R;
+      float *dst = mass + u * nblk + blk0 + k;
+      *dst = alpha == 1.f ? m : (1.f - alpha) * *dst + alpha * m;
+    }
   }
 }
 
@@ -493,8 +524,8 @@ extern "C" gkv_status gkv_observe_mass(const uint16_t *q_obs, int32_t n_obs, con
                      k_src, n_obs, G, Hkv, T, L.nblk, L.Rpad, sl2, lse, part);
   hipLaunchKernelGGL(obs_row_kernel, dim3((L.R + 3) / 4, Hkv, B), dim3(256), 0, s, part, L.R, L.Rpad, L.nslice, Hkv,
                      rows);
-  hipLaunchKernelGGL(obs_mass_kernel, dim3((L.nblk + 3) / 4, Hkv, B), dim3(256), 0, s, lse, rows, L.R, L.Rpad,
-                     L.nblk, Hkv, alpha, mass);
+  hipLaunchKernelGGL(obs_mass_kernel, dim3((L.nblk + kMassBlocks - 1) / kMassBlocks, Hkv, B), dim3(256), 0, s, lse,
+                     rows, L.R, L.Rpad, L.nblk, Hkv, alpha, mass);
   return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP;
 }
 
