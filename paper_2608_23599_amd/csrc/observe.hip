@@ -236,18 +236,12 @@ __global__ void __launch_bounds__(kObsThreads) obs_logit_kernel(const uint16_t *
   const uint8_t *qlane = qs + lane * 16;
   H8 a[2][8];
   if (nb > 0) load_keys(a, kb, T, blk0, j, hf);
-  uint32_t pf0 = 0, pf1 = 0;
   for (int k = 0; k < nb; ++k) {
+    // The keys of block blk are in flight: they were issued when the previous block's
+    // last MFMAs were out.  (Touching the next block's lines a block ahead, to warm the
+    // L2, made the fetched bytes grow by half: the lines a CU's waves touch ahead fill
+    // its XCD's L2 and leave before they are read.)
     const int blk = blk0 + k;
-    // The keys of block blk are in flight (issued when the previous block's last MFMAs
-    // were out).  Touch every 128-byte line of the next block now, so that its loads
-    // hit the L2 cache; the values only have to arrive before the next iteration.
-    asm volatile("" ::"v"(pf0), "v"(pf1));
-    if (k + 1 < nb) {
-      const int64_t lim = T * D - 2, e0 = (int64_t)(blk + 1) * P * D + lane * 64;
-      pf0 = *(const uint32_t *)(kb + (e0 < lim ? e0 : lim));
-      pf1 = *(const uint32_t *)(kb + (e0 + 4096 < lim ? e0 + 4096 : lim));
-    }
     const int64_t key0 = (int64_t)blk * P;
     float *lse_blk = lse + (u * nblk + blk) * Rpad + j;
     f16x cur[2];
