@@ -257,9 +257,11 @@ class Pool:
     def used(self, level):
         return int(_pool_used(self.h, level))
 
-    def __del__(self):
+    def __del__(self, _destroy=_pool_destroy):
+        # the destroy function is bound at definition: at interpreter exit the module's
+        # globals may already be gone when the last pools are collected
         if getattr(self, "h", None):
-            _pool_destroy(self.h)
+            _destroy(self.h)
             self.h = None
 
 
