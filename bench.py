@@ -61,6 +61,30 @@ def timed(fn, n=1):
     return s.elapsed_time(e) / n
 
 
+SETTLE_MS = 100.0
+
+
+def settle(fn, ms=SETTLE_MS):
+    """Run fn back to back, untimed, for about `ms` of GPU time, so that a timed region
+    starts at the clocks of continuous load.  On MI355X the clocks rise over the first
+    tens of milliseconds of load: decode steps of workload 4 on freshly built caches
+    took 157-160 us for the first 50 steps, 131 us for steps 100-200 and 124 us from
+    step 400 on, and the ramp starts again after half a second idle.  Returns the
+    number of calls."""
+    import torch
+    s = torch.cuda.Event(enable_timing=True)
+    e = torch.cuda.Event(enable_timing=True)
+    s.record()
+    fn()
+    e.record()
+    torch.cuda.synchronize()
+    n = int(ms / max(s.elapsed_time(e), 1e-3)) + 1
+    for _ in range(n):
+        fn()
+    torch.cuda.synchronize()
+    return n + 1
+
+
 def step_loop(caches, qs, outs, steps, warmup, pages=None):
     """Warmup, then `steps` timed decode steps with one event pair each."""
     import numpy as np
@@ -268,6 +292,8 @@ def quest_point(wq, ncopies, dev, cpu=None):
     for i in range(10):
         copies[i % n].quest_select(qq, wq.topk, out=pages[i % n])
         copies[i % n].decode(qq, pages=pages[i % n], out=qouts[i % n])
+    settle(lambda: (copies[0].quest_select(qq, wq.topk, out=pages[0]),
+                    copies[0].decode(qq, pages=pages[0], out=qouts[0])))
     reps = max(1, 24 // n)
     sel_ms = timed(lambda: [copies[i].quest_select(qq, wq.topk, out=pages[i]) for i in range(n)], reps) / n
     att_ms = timed(lambda: [copies[i].decode(qq, pages=pages[i], out=qouts[i]) for i in range(n)], reps) / n
@@ -369,7 +395,19 @@ def main():
     resident_measured = (caches[0].pool_bits() + res_store) / rates["values"]
     qs = [torch.from_numpy(synth.queries(wl.id, B, Hq, step=s).view(np.int16)).to(dev) for s in range(4)]
     outs = [torch.empty((B, Hq, 128), dtype=torch.float32, device=dev) for _ in range(2)]
-    log(f"[bench] decode loop: {args.warmup} warmup + {args.steps} timed steps")
+    # the same warm-up and timed steps first on the freshly built caches (reported as
+    # `cold`), then the settle period, then the timed steps of the headline
+    cold, _ = step_loop(caches, qs, outs, args.steps, args.warmup)
+    log(f"[bench] cold: median {np.median(cold):.1f} us, p90 {np.percentile(cold, 90):.1f} us")
+    ctr = [0]
+
+    def one_step():
+        i = ctr[0]
+        ctr[0] += 1
+        caches[i % 2].decode(qs[i % len(qs)], out=outs[i % 2])
+
+    nsettle = settle(one_step)
+    log(f"[bench] settled with {nsettle} untimed steps; decode loop: {args.warmup} warmup + {args.steps} timed steps")
     per, total_ms = step_loop(caches, qs, outs, args.steps, args.warmup)
     med, p90 = float(np.median(per)), float(np.percentile(per, 90))
     mean_us = float(per.mean())
@@ -419,8 +457,7 @@ def main():
         phases["accounting_host_us"] = round((time.perf_counter() - ta) / 100 * 1e6, 1)
         del small
         # the decode step with the attention error certificate (section 3.6)
-        for _ in range(3):
-            caches[0].decode_bound(qs[0])
+        settle(lambda: caches[0].decode_bound(qs[0]))
         phases["decode_with_certificate_us"] = round(timed(lambda: caches[0].decode_bound(qs[0]), 20) * 1e3, 1)
         _, bnd = caches[0].decode_bound(qs[0])
         phases["certificate_bound_mean_max"] = [round(float(bnd.mean()), 4), round(float(bnd.max()), 4)]
@@ -431,8 +468,7 @@ def main():
                                  .view(np.int16)).to(dev)
         ows = torch.empty(gkv.observe_ws_bytes(B, Hkv, Hq, T, n_obs), dtype=torch.uint8, device=dev)
         mass_o = torch.empty((B, Hkv, len(lv)), dtype=torch.float32, device=dev)
-        for _ in range(2):
-            gkv.observe_mass(q_obs, k, mass=mass_o, ws=ows)
+        settle(lambda: gkv.observe_mass(q_obs, k, mass=mass_o, ws=ows))
         obs_ms = timed(lambda: gkv.observe_mass(q_obs, k, mass=mass_o, ws=ows), 5)
         flops = 2.0 * B * Hq * n_obs * T * 128  # the logits' multiply-adds
         phases["observe_mass_n64_us"] = round(obs_ms * 1e3, 1)
@@ -497,6 +533,7 @@ def main():
         r2 = c2[0].account()
         b2 = r2["read_bits"] / 8.0
         n2 = max(args.steps // 2, 10)
+        settle(lambda: c2[0].decode(qs[0], out=outs[0]))
         per2, _ = step_loop(c2, qs, outs, n2, args.warmup)
         _, attn2, _ = staged_loop(c2, qs, outs, n2, args.warmup)
         rdv2 = {"workload": wl.name.split(",")[0] + f", B={B}, T={T}, RD-V2: 16 exact blocks + one-centroid base, "
@@ -515,6 +552,7 @@ def main():
         c3 = [build_cache(lv, nres, v_per_token=True)[0] for _ in range(2)]
         r3 = c3[0].account()
         b3 = r3["read_bits"] / 8.0
+        settle(lambda: c3[0].decode(qs[0], out=outs[0]))
         per3, _ = step_loop(c3, qs, outs, n2, args.warmup)
         _, attn3, _ = staged_loop(c3, qs, outs, n2, args.warmup)
         vtok = {"workload": wl.name + ", values quantised per token",
@@ -565,6 +603,7 @@ def main():
             steps5.append(tuple(torch.from_numpy(a.view(np.int16)).to(dev) for a in
                                 (kn, vn, synth.queries(w5.id, w5.B, w5.Hq, step=st))))
         torch.cuda.synchronize()
+        settle(lambda: (c5.quest_select(steps5[0][2], w5.topk, out=p5), c5.decode(steps5[0][2], pages=p5, out=o5)))
         for st in range(warm5 + w5.dynamic_steps):
             kn, vn, qq5 = steps5[st]
             i = st - warm5
@@ -612,6 +651,12 @@ def main():
         "p50_us": round(med, 2),
         "p90_us": round(p90, 2),
         "mean_us": round(mean_us, 2),
+        "settle": {"ms": SETTLE_MS, "untimed_steps": nsettle,
+                   "note": "untimed decode steps between the cold pass and the timed steps, so that these run "
+                           "at the clocks of continuous load"},
+        "cold": {"p50_us": round(float(np.median(cold)), 2), "p90_us": round(float(np.percentile(cold, 90)), 2),
+                 "warmup": args.warmup, "steps": args.steps,
+                 "note": "the same warm-up and timed steps on the freshly built caches, before the settle"},
         "achieved_GBps": round(gbps, 1),
         "pct_hbm_peak": round(100 * gbps / HBM_PEAK_GBPS, 2),
         "achieved_GBps_at_mean": round(alg_bytes / (mean_us * 1e-6) / 1e9, 1),
