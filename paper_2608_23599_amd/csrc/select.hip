@@ -141,6 +141,8 @@ struct SelShared {
   uint64_t prefix, pmask;
   int64_t remaining;
   int64_t wsum[kSelWaves][2];
+  uint32_t wpre[kSelWaves][2];  // exclusive prefix of the wavefront totals (scan2)
+  uint32_t wtot[2];
   int64_t base[2];
 };
 
@@ -190,24 +192,30 @@ __device__ __forceinline__ uint32_t wave_and(uint32_t x) {
 // Counts of one pass fit in 32 bits (at most 8192 keys per workgroup pass).
 __device__ __forceinline__ void scan2(SelShared &sh, int64_t &a, int64_t &b, int64_t &ta, int64_t &tb) {
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int64_t x = wave_scan((uint32_t)a), y = wave_scan((uint32_t)b);
+  const uint32_t x = wave_scan((uint32_t)a), y = wave_scan((uint32_t)b);
   if (lane == 63) {
     sh.wsum[wv][0] = x;
     sh.wsum[wv][1] = y;
   }
   __syncthreads();
-  int64_t bx = 0, by = 0;
-  ta = tb = 0;
-  for (int q = 0; q < kSelWaves; ++q) {
-    if (q < wv) {
-      bx += sh.wsum[q][0];
-      by += sh.wsum[q][1];
+  if (wv == 0) {  // one wavefront scans the wavefront totals
+    const uint32_t px = lane < kSelWaves ? (uint32_t)sh.wsum[lane][0] : 0u;
+    const uint32_t py = lane < kSelWaves ? (uint32_t)sh.wsum[lane][1] : 0u;
+    const uint32_t sx = wave_scan(px), sy = wave_scan(py);
+    if (lane < kSelWaves) {
+      sh.wpre[lane][0] = sx - px;
+      sh.wpre[lane][1] = sy - py;
     }
-    ta += sh.wsum[q][0];
-    tb += sh.wsum[q][1];
+    if (lane == 63) {
+      sh.wtot[0] = sx;
+      sh.wtot[1] = sy;
+    }
   }
-  a = bx + x - a;
-  b = by + y - b;
+  __syncthreads();
+  a = (int64_t)sh.wpre[wv][0] + x - a;
+  b = (int64_t)sh.wpre[wv][1] + y - b;
+  ta = sh.wtot[0];
+  tb = sh.wtot[1];
   __syncthreads();
 }
 
@@ -298,12 +306,38 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
     for (int64_t i = need + tid; i < k; i += kSelThreads) o[i] = -1;
   if (need == 0) return;
   uint64_t kr[KPT > 0 ? KPT : 1];
-  if (KPT > 0) {
+  if (KPT > 0 && !ix) {
+    // a contiguous slice: staged through LDS with lane-contiguous loads, then each
+    // thread takes its KPT consecutive keys (loads that each touch 64 scattered
+    // 8-byte words took three times as long)
+    extern __shared__ uint64_t stage[];  // KPT * kSelThreads keys (dynamic)
+    const uint64_t *src = key + base;
+    uint64_t t[KPT > 0 ? KPT : 1];
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) {  // unconditional loads (a clamped index): all in flight at once
+      const int64_t i = (int64_t)j * kSelThreads + tid;
+      t[j] = src[i < n ? i : n - 1];
+    }
 #pragma unroll
     for (int j = 0; j < KPT; ++j) {
-      const int64_t i = (int64_t)tid * KPT + j;
-      kr[j] = i < n ? key[ix ? (int64_t)ix[i] : base + i] : 0;
+      const int64_t i = (int64_t)j * kSelThreads + tid;
+      stage[i] = i < n ? t[j] : 0;
     }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) kr[j] = stage[tid * KPT + j];
+  } else if (KPT > 0) {
+    int32_t t[KPT > 0 ? KPT : 1];
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) {  // unconditional loads (a clamped index): all in flight at once
+      const int64_t i = (int64_t)tid * KPT + j;
+      t[j] = ix[i < n ? i : n - 1];
+    }
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) kr[j] = key[(int64_t)t[j]];
+#pragma unroll
+    for (int j = 0; j < KPT; ++j)
+      if ((int64_t)tid * KPT + j >= n) kr[j] = 0;
   }
   // bits that differ between keys: bytes above the highest differing byte are the
   // same in every key, so their digits are known without a pass
@@ -329,19 +363,20 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
     sh.wsum[wv][1] = (int64_t)kor;
   }
   __syncthreads();
-  if (tid == 0) {
-    uint64_t a = ~0ull, b = 0;
-    for (int q = 0; q < kSelWaves; ++q) {
-      a &= (uint64_t)sh.wsum[q][0];
-      b |= (uint64_t)sh.wsum[q][1];
-    }
+  if (wv == 0) {  // the wavefront values are combined by one wavefront (lane q reads wavefront q's)
+    const uint64_t la = lane < kSelWaves ? (uint64_t)sh.wsum[lane][0] : ~0ull;
+    const uint64_t lo = lane < kSelWaves ? (uint64_t)sh.wsum[lane][1] : 0ull;
+    const uint64_t a = ((uint64_t)wave_and((uint32_t)(la >> 32)) << 32) | wave_and((uint32_t)la);
+    const uint64_t b = ((uint64_t)wave_or((uint32_t)(lo >> 32)) << 32) | wave_or((uint32_t)lo);
     const uint64_t diff = a ^ b;
     const int hb = diff ? 63 - __builtin_clzll(diff) : -1;  // highest differing bit
     const uint64_t known = hb >= 63 ? 0ull : (~0ull << (hb + 1));
-    sh.prefix = a & known;
-    sh.pmask = known;
-    sh.remaining = need;
-    sh.base[0] = hb;
+    if (lane == 0) {
+      sh.prefix = a & known;
+      sh.pmask = known;
+      sh.remaining = need;
+      sh.base[0] = hb;
+    }
   }
   for (int i = tid; i < 256; i += kSelThreads) sh.hist[i] = 0;
   __syncthreads();
@@ -459,6 +494,7 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
 }
 
 constexpr int64_t kSelSlice = (int64_t)kSelKPT * kSelThreads;
+constexpr size_t kSelStageBytes = (size_t)kSelSlice * 8;  // the LDS staging of one slice
 
 // idx_ws: two index lists of `key_stride` entries per unit (the stages' candidates).
 // seq_len, Hkv, page: the per-unit limit of Compressed-Quest pages (seq_len null: none).
@@ -476,14 +512,16 @@ void launch_select(const uint64_t *keys, int64_t key_stride, int64_t n, int k, i
   for (int buf = 0; cur > kSelSlice; buf ^= 1) {
     const int64_t S = (cur + kSelSlice - 1) / kSelSlice;
     int32_t *dst = idx_ws + (int64_t)buf * units * key_stride;
-    hipLaunchKernelGGL(select_kernel<kSelKPT>, dim3((unsigned)S, units), dim3(kSelThreads), 0, s, keys, key_stride,
+    hipLaunchKernelGGL(select_kernel<kSelKPT>, dim3((unsigned)S, units), dim3(kSelThreads), kSelStageBytes, s, keys,
+                       key_stride,
                        idx, key_stride, cur, kSelSlice, k, dst, key_stride, (uint64_t *)nullptr, (int64_t)0,
                        (int64_t)0, seq_len, Hkv, page);
     const int64_t last = cur - (S - 1) * kSelSlice;
     cur = (S - 1) * k + (last < k ? last : k);
     idx = dst;
   }
-  hipLaunchKernelGGL(select_kernel<kSelKPT>, dim3(1, units), dim3(kSelThreads), 0, s, keys, key_stride, idx,
+  hipLaunchKernelGGL(select_kernel<kSelKPT>, dim3(1, units), dim3(kSelThreads), kSelStageBytes, s, keys, key_stride,
+                     idx,
                      key_stride, cur, cur, k, out, out_stride, mask, mask_stride, mask_words, seq_len, Hkv, page);
 }
 
