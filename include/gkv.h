@@ -287,9 +287,10 @@ gkv_status gkv_append(gkv_cache *c, const uint16_t *k_new, const uint16_t *v_new
 /* Compressed-Quest page selection (section 3.5): for every (b,h), rank the closed
  * pages 0 .. cur-1 (cur = (T-1)/page is always read, never ranked) by the box upper
  * bound UB_g(p) = sum_d q_gd * (q_gd >= 0 ? kmax_pd : kmin_pd), accumulated in
- * fp64 in channel order, maximised over the group's query heads; write the first
- * topk pages of the order (score desc, page asc) to pages [B][Hkv][topk] in
- * ascending order, -1 padded.  q: [B][Hq][128] fp16. */
+ * fp32 in channel order (each product of two fp16 values is exact in fp32, so every
+ * step rounds once), maximised over the group's query heads; write the first topk
+ * pages of the order (score desc, page asc) to pages [B][Hkv][topk] in ascending
+ * order, -1 padded.  q: [B][Hq][128] fp16, 4-byte aligned (GKV_E_ARG otherwise). */
 gkv_status gkv_quest_select(const uint16_t *q, const gkv_cache *c, int32_t topk, int32_t *pages, void *ws,
                             int64_t ws_bytes, void *stream);
 

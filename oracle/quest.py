@@ -12,11 +12,15 @@ Readings (listed in the design notes):
 * Pages are 16 tokens (the workloads' page size); page p covers tokens
   [16p, 16p + 16).  The current page is cur = floor((T - 1) / 16); it is always
   read and never ranked; pages 0 .. cur-1 are ranked.
-* The bound is evaluated in fp64 as a channel-ascending running sum
-  acc <- acc + q_d * (q_d >= 0 ? kmax_d : kmin_d); every product of two fp16
-  values is exact in fp64, so this is the same with or without a fused
-  multiply-add.  A -0 result is canonicalised to +0.  No 1/sqrt(d) scale (it
-  cannot change the order).
+* The paper fixes no precision for the bound; it is evaluated in fp32 as a
+  channel-ascending running sum acc <- acc + q_d * (q_d >= 0 ? kmax_d : kmin_d).
+  Every product of two fp16 values is exact in fp32 (at most 22 significant
+  bits, magnitudes between 2^-48 and 2^32, so no denormal and no overflow), so
+  each step rounds once, on the add, with or without a fused multiply-add.  A -0
+  result is canonicalised to +0.  No 1/sqrt(d) scale (it cannot change the
+  order).  Because the terms satisfy term_d >= q_d * k_d for every key k of the
+  page and round-to-nearest addition is monotone, the fp32 bound is never below
+  the same channel-ascending fp32 sum for any of the page's keys.
 * GQA: the KV head's page score is the maximum of the bound over the query
   heads of its group (the tightest bound on any group head's best logit).
 * Selection: the first k pages of the order (score descending, page index
@@ -50,17 +54,18 @@ def page_boxes(k_bits, page=PAGE):
 
 
 def box_upper_bounds(q_bits, kmin_bits, kmax_bits):
-    """q_bits [G][D], boxes [N][D] -> fp64 [G][N] channel-sequential bounds."""
-    q = fp16.to_f64(q_bits)
-    lo = fp16.to_f64(kmin_bits)
-    hi = fp16.to_f64(kmax_bits)
+    """q_bits [G][D], boxes [N][D] -> fp32 [G][N] channel-sequential bounds."""
+    q = fp16.to_f64(q_bits).astype(np.float32)  # fp16 values are exact in fp32
+    lo = fp16.to_f64(kmin_bits).astype(np.float32)
+    hi = fp16.to_f64(kmax_bits).astype(np.float32)
     G, Dd = q.shape
     N = lo.shape[0]
-    acc = np.zeros((G, N), dtype=np.float64)
+    acc = np.zeros((G, N), dtype=np.float32)
     for d in range(Dd):
         qd = q[:, d][:, None]
         bound = np.where(qd >= 0.0, hi[:, d][None, :], lo[:, d][None, :])
-        acc = acc + qd * bound
+        acc = acc + qd * bound  # float32 throughout: the product is exact, the add rounds
+    assert acc.dtype == np.float32
     return acc
 
 

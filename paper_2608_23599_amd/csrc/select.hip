@@ -24,40 +24,27 @@ __device__ __forceinline__ uint64_t order_key(double x) {
   return (bits >> 63) ? ~bits : (bits | 0x8000000000000000ull);
 }
 
-// Query coefficients of the box bound for one (sequence, KV head) as fp64, laid out
-// [HG][D][G / HG] (head g = hg * (G / HG) + j), so that the coefficients one
-// wavefront of the score kernel reads are contiguous.  grid (Hkv, B) x 256 threads.
-__global__ void __launch_bounds__(256) quest_qtab_kernel(const uint16_t *__restrict__ q, int G, int HG, int Hkv,
-                                                         double *__restrict__ qt) {
-  const int64_t u = (int64_t)blockIdx.y * Hkv + blockIdx.x;
-  const int hpw = G / HG;
-  for (int i = threadIdx.x; i < G * D; i += 256) {
-    const int g = i / D, d = i % D;
-    const int hg = g / hpw, j = g % hpw;
-    qt[u * G * D + ((int64_t)hg * D + d) * hpw + j] = (double)__builtin_bit_cast(_Float16, q[u * G * D + i]);
-  }
-}
-
 // Box upper bound of every ranked page for the G query heads of a KV head:
-// UB_g(p) = sum_d q_gd * (q_gd >= 0 ? kmax_pd : kmin_pd), channel-ascending in fp64
-// (each product of two fp16 values is exact, so the fused multiply-add rounds once,
-// like a separate add); page score = max_g UB_g.
+// UB_g(p) = sum_d q_gd * (q_gd >= 0 ? kmax_pd : kmin_pd), channel-ascending in fp32;
+// page score = max_g UB_g.  The product of two fp16 values is exact in fp32 (22
+// significant bits, magnitudes from 2^-48 to below 2^32, so neither a denormal nor an
+// overflow), so each step rounds once, on the add; v_fma_mix_f32 takes both fp16
+// operands as they are, with no conversion instructions.
 //
 // One wavefront covers 64 pages (lane = page) and G / HG of the heads; a workgroup is
 // four wavefronts: 4 / HG page groups times HG head groups, whose bounds meet in LDS.
-// Both halves of a box word are widened once per wavefront and each head picks one
-// by the sign of its coefficient.  The coefficients are wavefront-uniform and come
-// from the table through the scalar cache (contiguous per wavefront, so a few wide
-// scalar loads cover many channels).  grid (ceil(npages / (64 * 4 / HG)), Hkv, B) x
-// 256 threads.
+// The query is read as given (fp16 rows of 128 channels): a wavefront's heads and
+// channels are uniform, so its coefficients come through the scalar cache, two
+// channels per dword, and each head picks the half of a box word by the sign of its
+// coefficient.  grid (ceil(npages / (64 * 4 / HG)), Hkv, B) x 256 threads.
 constexpr int kScoreBatch = 32;  // box words in flight per lane
 template <int G, int HG>
-__global__ void __launch_bounds__(256) quest_score_kernel(const double *__restrict__ qt,
+__global__ void __launch_bounds__(256) quest_score_kernel(const uint16_t *__restrict__ q,
                                                           const uint16_t *__restrict__ boxes, int64_t npage_cap,
                                                           int64_t npages, int Hkv, uint64_t *__restrict__ keys,
                                                           const int64_t *__restrict__ seq_len, int page) {
   constexpr int HPW = G / HG;
-  __shared__ double ub[4][64];
+  __shared__ float ub[4][64];
   const int h = blockIdx.y, b = blockIdx.z;
   const int64_t u = (int64_t)b * Hkv + h;
   const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)), lane = threadIdx.x & 63;
@@ -65,27 +52,28 @@ __global__ void __launch_bounds__(256) quest_score_kernel(const double *__restri
   const int64_t pg0 = ((int64_t)blockIdx.x * (4 / HG) + w / HG) * 64;
   const int64_t pg = pg0 + lane;
   const bool on = pg < npages;
-  double best = 0.0;
+  float best = 0.0f;
   if (pg0 < npages) {
     // the whole 64-page group lies inside the box capacity (a multiple of 64 pages),
     // so every lane loads; lanes past the ranked pages drop their result
     const uint32_t *bx = (const uint32_t *)(boxes + u * npage_cap * 2 * D) + (box_index(pg0, 0) >> 1) + lane;
-    const double *qu = qt + u * G * D + (int64_t)hg * D * HPW;
-    double acc[HPW];
+    const uint32_t *qw = (const uint32_t *)(q + (u * G + (int64_t)hg * HPW) * D);  // this wavefront's heads
+    float acc[HPW];
 #pragma unroll
-    for (int j = 0; j < HPW; ++j) acc[j] = 0.0;
+    for (int j = 0; j < HPW; ++j) acc[j] = 0.0f;
     for (int d0 = 0; d0 < D; d0 += kScoreBatch) {
       uint32_t pr[kScoreBatch];
 #pragma unroll
       for (int e = 0; e < kScoreBatch; ++e) pr[e] = bx[(d0 + e) * 64];
 #pragma unroll
       for (int e = 0; e < kScoreBatch; ++e) {
-        const double lo = (double)(float)__builtin_bit_cast(_Float16, (uint16_t)pr[e]);          // kmin
-        const double hi = (double)(float)__builtin_bit_cast(_Float16, (uint16_t)(pr[e] >> 16));  // kmax
+        const _Float16 lo = __builtin_bit_cast(_Float16, (uint16_t)pr[e]);          // kmin
+        const _Float16 hi = __builtin_bit_cast(_Float16, (uint16_t)(pr[e] >> 16));  // kmax
 #pragma unroll
         for (int j = 0; j < HPW; ++j) {
-          const double qq = qu[(d0 + e) * HPW + j];
-          acc[j] = __builtin_fma(qq, qq >= 0.0 ? hi : lo, acc[j]);
+          const uint32_t q2 = qw[(j * D + d0 + e) >> 1];  // channels d0+e and its pair (d0 is even)
+          const _Float16 qq = __builtin_bit_cast(_Float16, (uint16_t)((e & 1) ? q2 >> 16 : q2));
+          acc[j] = __builtin_fmaf((float)qq, (float)(qq >= (_Float16)0.0f ? hi : lo), acc[j]);
         }
       }
     }
@@ -104,7 +92,7 @@ __global__ void __launch_bounds__(256) quest_score_kernel(const double *__restri
   // below every score: they rank last and the selection turns them into -1
   int64_t nown = npages;
   if (seq_len) nown = seq_len[b] > 0 ? (seq_len[b] - 1) / page : 0;
-  if (on) keys[u * npage_cap + pg] = pg < nown ? order_key(best) : 0ull;
+  if (on) keys[u * npage_cap + pg] = pg < nown ? order_key((double)best) : 0ull;
 }
 
 // Select the first k of the order (key desc, index asc) among keys[0..n) of one
@@ -592,11 +580,8 @@ __global__ void __launch_bounds__(256) res_off_kernel(const uint64_t *__restrict
 }  // namespace
 
 // ---------------------------------------------------------------- C ABI
-// keys (8 bytes) and two candidate index lists (4 bytes each) per ranked item; Quest
-// adds the fp64 query-coefficient table, G x D per (b,h)
-static int64_t quest_ws(const gkv_cache *c) {
-  return (int64_t)c->B * c->Hkv * (c->npage_cap * 16 + (int64_t)D * (c->Hq / c->Hkv) * 8);
-}
+// keys (8 bytes) and two candidate index lists (4 bytes each) per ranked item
+static int64_t quest_ws(const gkv_cache *c) { return (int64_t)c->B * c->Hkv * c->npage_cap * 16; }
 // the residual selection's keys and lists are strided by the block capacity in tokens,
 // so that one workspace serves the cache at any length
 static int64_t rd_stride(const gkv_cache *c) { return (int64_t)c->nblk_cap * P; }
@@ -615,6 +600,7 @@ extern "C" gkv_status gkv_quest_select(const uint16_t *q, const gkv_cache *c, in
   gkv_status st = gkv_validate_cache(c);
   if (st) return st;
   if (!q || !pages || !ws || topk <= 0) return GKV_E_ARG;
+  if ((uintptr_t)q & 3) return GKV_E_ARG;  // read two channels per dword
   if (!c->page) return GKV_E_ARG;
   if (c->T <= 0) return GKV_E_SHAPE;
   if (ws_bytes < quest_ws(c)) return GKV_E_WORKSPACE;
@@ -623,22 +609,20 @@ extern "C" gkv_status gkv_quest_select(const uint16_t *q, const gkv_cache *c, in
   if (ncur > c->npage_cap) return GKV_E_SHAPE;
   hipStream_t s = (hipStream_t)stream;
   uint64_t *keys = (uint64_t *)ws;
-  const int64_t units = (int64_t)c->B * c->Hkv;
-  double *qt = (double *)((int32_t *)(keys + units * c->npage_cap) + 2 * units * c->npage_cap);
   if (ncur > 0) {
-    // head groups per page group: two where the head count allows, four when that
-    // still leaves fewer than 16 wavefronts per compute unit
-    const int64_t groups = units * ((ncur + 63) / 64);
-    int HG = 1;
-    while (HG < 4 && G % (2 * HG) == 0 && (HG == 1 || groups * HG < 16 * (int64_t)gkv_device_cus())) HG *= 2;
+    // two head groups per page group (a wavefront then does half the arithmetic and the
+    // box words its sibling also reads come from the cache), four when that still
+    // leaves fewer than four wavefronts per compute unit
+    const int64_t groups = (int64_t)c->B * c->Hkv * ((ncur + 63) / 64);
+    int HG = G % 2 == 0 ? 2 : 1;
+    if (G % 4 == 0 && groups * 2 < 4 * (int64_t)gkv_device_cus()) HG = 4;
     const int per = 4 / HG;  // page groups per workgroup
     dim3 grid((unsigned)(((ncur + 63) / 64 + per - 1) / per), c->Hkv, c->B);
-    hipLaunchKernelGGL(quest_qtab_kernel, dim3(c->Hkv, c->B), dim3(256), 0, s, q, G, HG, c->Hkv, qt);
     switch (G * 4 + HG - 1) {
-#define GKV_SCORE(g, hg)                                                                                   \
-  case g * 4 + hg - 1:                                                                                     \
-    hipLaunchKernelGGL((quest_score_kernel<g, hg>), grid, dim3(256), 0, s, (const double *)qt, c->boxes,  \
-                       c->npage_cap, ncur, c->Hkv, keys, (const int64_t *)c->seq_len, c->page);            \
+#define GKV_SCORE(g, hg)                                                                                          \
+  case g * 4 + hg - 1:                                                                                            \
+    hipLaunchKernelGGL((quest_score_kernel<g, hg>), grid, dim3(256), 0, s, q, c->boxes, c->npage_cap, ncur, c->Hkv, \
+                       keys, (const int64_t *)c->seq_len, c->page);                                               \
     break;
       GKV_SCORE(1, 1) GKV_SCORE(3, 1) GKV_SCORE(5, 1) GKV_SCORE(7, 1) GKV_SCORE(9, 1) GKV_SCORE(11, 1)
       GKV_SCORE(13, 1) GKV_SCORE(15, 1)

@@ -21,17 +21,67 @@ def _seq_dot(q, k):
     return acc
 
 
+def _seq_dot_f32(q, k):
+    acc = np.float32(0.0)
+    for a, b in zip(q.astype(np.float32), k.astype(np.float32)):
+        acc = np.float32(acc + a * b)
+    return acc
+
+
 def test_box_bound_never_below_true_score():
+    """Every term of the bound is >= the key's term (exact fp32 products) and
+    round-to-nearest addition is monotone, so the fp32 bound is never below the same
+    channel-ascending fp32 sum for any key of the page."""
     k, _ = synth.kv_unit(201, 0, 0, 512)
     q = synth.queries(201, 1, 4)[0]
     kmin, kmax = quest.page_boxes(k)
     ub = quest.box_upper_bounds(q, kmin, kmax)
+    assert ub.dtype == np.float32
     kf, qf = fp16.to_f64(k), fp16.to_f64(q)
     for g in range(4):
         for p in range(kmin.shape[0]):
-            best = max(_seq_dot(qf[g], kf[j]) for j in range(16 * p, 16 * p + 16))
+            best = max(_seq_dot_f32(qf[g], kf[j]) for j in range(16 * p, 16 * p + 16))
             assert ub[g, p] >= best
     assert np.all(fp16.to_f64(kmin)[:, None, :] <= fp16.to_f64(k).reshape(32, 16, 128))
+
+
+def test_box_bound_within_fp32_error_of_exact_sum():
+    """The bound against its exact rational value: recursive summation of n terms
+    rounds to within (n - 1) * 2^-24 * sum |term| (each product is exact)."""
+    k, _ = synth.kv_unit(203, 0, 0, 256)
+    q = synth.queries(203, 1, 4)[0]
+    kmin, kmax = quest.page_boxes(k)
+    ub = quest.box_upper_bounds(q, kmin, kmax)
+    qf, lo, hi = fp16.to_f64(q), fp16.to_f64(kmin), fp16.to_f64(kmax)
+    for g in range(4):
+        for p in range(kmin.shape[0]):
+            terms = [Fraction(qf[g, d]) * Fraction(hi[p, d] if qf[g, d] >= 0 else lo[p, d]) for d in range(128)]
+            exact = sum(terms)
+            bound = 127 * Fraction(1, 2 ** 24) * sum(abs(t) for t in terms)
+            assert abs(Fraction(float(ub[g, p])) - exact) <= bound
+
+
+def test_box_bound_picks_corner_by_sign():
+    """q_d >= 0 takes kmax_d, q_d < 0 takes kmin_d (small integers: exact in any order)."""
+    q = np.zeros((1, 128))
+    lo, hi = np.zeros((1, 128)), np.zeros((1, 128))
+    q[0, :3], lo[0, :3], hi[0, :3] = [1, -1, 2], [-3, -5, 1], [2, 7, 4]
+    ub = quest.box_upper_bounds(fp16.from_f64(q), fp16.from_f64(lo), fp16.from_f64(hi))
+    assert ub[0, 0] == 1 * 2 + (-1) * (-5) + 2 * 4
+
+
+def test_box_bound_fp32_channel_order():
+    """The bound rounds to fp32 after every channel, in ascending channel order:
+    terms (2^24, 1, -2^24) sum to 0 (2^24 + 1 rounds to 2^24), terms (2^24, -2^24, 1)
+    to 1; fp64, or the descending order, would give 1 for the first."""
+    def bound(qs, ks):
+        q = np.zeros((1, 128))
+        k = np.zeros((1, 128))
+        q[0, :3], k[0, :3] = qs, ks
+        kb = fp16.from_f64(k)
+        return quest.box_upper_bounds(fp16.from_f64(q), kb, kb)[0, 0]
+    assert bound([2048, 1, -2048], [8192, 1, 8192]) == 0.0
+    assert bound([2048, -2048, 1], [8192, 8192, 1]) == 1.0
 
 
 def test_page_size_one_is_exact_topk():
