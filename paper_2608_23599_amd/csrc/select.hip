@@ -122,6 +122,7 @@ constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
 
 constexpr int kSelKPT = 8;  // keys per thread held in registers (n <= 8192)
+constexpr int kSelPad = 2;  // empty 8-byte words after each thread's keys in the LDS staging
 constexpr int kSelRank = 16;  // candidates ranked directly instead of another radix pass (<= 64)
 
 struct SelShared {
@@ -294,11 +295,28 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
     for (int64_t i = need + tid; i < k; i += kSelThreads) o[i] = -1;
   if (need == 0) return;
   uint64_t kr[KPT > 0 ? KPT : 1];
+  // bits that differ between keys: bytes above the highest differing byte are the
+  // same in every key, so their digits are known without a pass.  Each wavefront's
+  // AND and OR of its keys go to LDS before the barrier that the loads need anyway
+  // (a clamped load repeats a real key, which changes neither).
+  uint64_t kand = ~0ull, kor = 0;
+  const auto wave_andor = [&]() {
+    kand = ((uint64_t)wave_and((uint32_t)(kand >> 32)) << 32) | wave_and((uint32_t)kand);
+    kor = ((uint64_t)wave_or((uint32_t)(kor >> 32)) << 32) | wave_or((uint32_t)kor);
+    if (lane == 0) {
+      sh.wsum[wv][0] = (int64_t)kand;
+      sh.wsum[wv][1] = (int64_t)kor;
+    }
+  };
+  for (int i = tid; i < 256; i += kSelThreads) sh.hist[i] = 0;
   if (KPT > 0 && !ix) {
     // a contiguous slice: staged through LDS with lane-contiguous loads, then each
     // thread takes its KPT consecutive keys (loads that each touch 64 scattered
-    // 8-byte words took three times as long)
-    extern __shared__ uint64_t stage[];  // KPT * kSelThreads keys (dynamic)
+    // 8-byte words took three times as long).  Each thread's KPT keys are followed by
+    // kSelPad empty words, so that the 16-byte reads of eight neighbouring lanes fall
+    // on distinct banks (unpadded, the lanes' 64-byte stride put a wavefront's reads
+    // on two 8-byte bank pairs, and the reads took about 2 us)
+    extern __shared__ uint64_t stage[];  // kSelThreads * (KPT + kSelPad) words (dynamic)
     const uint64_t *src = key + base;
     uint64_t t[KPT > 0 ? KPT : 1];
 #pragma unroll
@@ -308,12 +326,15 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
     }
 #pragma unroll
     for (int j = 0; j < KPT; ++j) {
-      const int64_t i = (int64_t)j * kSelThreads + tid;
-      stage[i] = i < n ? t[j] : 0;
+      const int i = j * kSelThreads + tid;
+      stage[(i / KPT) * (KPT + kSelPad) + i % KPT] = i < n ? t[j] : 0;
+      kand &= t[j];
+      kor |= t[j];
     }
+    wave_andor();
     __syncthreads();
 #pragma unroll
-    for (int j = 0; j < KPT; ++j) kr[j] = stage[tid * KPT + j];
+    for (int j = 0; j < KPT; ++j) kr[j] = stage[tid * (KPT + kSelPad) + j];
   } else if (KPT > 0) {
     int32_t t[KPT > 0 ? KPT : 1];
 #pragma unroll
@@ -322,35 +343,25 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
       t[j] = ix[i < n ? i : n - 1];
     }
 #pragma unroll
-    for (int j = 0; j < KPT; ++j) kr[j] = key[(int64_t)t[j]];
+    for (int j = 0; j < KPT; ++j) {
+      kr[j] = key[(int64_t)t[j]];
+      kand &= kr[j];
+      kor |= kr[j];
+    }
 #pragma unroll
     for (int j = 0; j < KPT; ++j)
       if ((int64_t)tid * KPT + j >= n) kr[j] = 0;
-  }
-  // bits that differ between keys: bytes above the highest differing byte are the
-  // same in every key, so their digits are known without a pass
-  uint64_t kand = ~0ull, kor = 0;
-  if (KPT > 0) {
-#pragma unroll
-    for (int j = 0; j < KPT; ++j)
-      if ((int64_t)tid * KPT + j < n) {
-        kand &= kr[j];
-        kor |= kr[j];
-      }
+    wave_andor();
+    __syncthreads();
   } else {
     for (int64_t i = tid; i < n; i += kSelThreads) {
       const uint64_t kv = key[i];
       kand &= kv;
       kor |= kv;
     }
+    wave_andor();
+    __syncthreads();
   }
-  kand = ((uint64_t)wave_and((uint32_t)(kand >> 32)) << 32) | wave_and((uint32_t)kand);
-  kor = ((uint64_t)wave_or((uint32_t)(kor >> 32)) << 32) | wave_or((uint32_t)kor);
-  if (lane == 0) {
-    sh.wsum[wv][0] = (int64_t)kand;
-    sh.wsum[wv][1] = (int64_t)kor;
-  }
-  __syncthreads();
   if (wv == 0) {  // the wavefront values are combined by one wavefront (lane q reads wavefront q's)
     const uint64_t la = lane < kSelWaves ? (uint64_t)sh.wsum[lane][0] : ~0ull;
     const uint64_t lo = lane < kSelWaves ? (uint64_t)sh.wsum[lane][1] : 0ull;
@@ -366,7 +377,6 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
       sh.base[0] = hb;
     }
   }
-  for (int i = tid; i < 256; i += kSelThreads) sh.hist[i] = 0;
   __syncthreads();
   // digits of up to 8 bits from the highest differing bit down (the first digit
   // spreads the keys over all its buckets)
@@ -482,7 +492,7 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
 }
 
 constexpr int64_t kSelSlice = (int64_t)kSelKPT * kSelThreads;
-constexpr size_t kSelStageBytes = (size_t)kSelSlice * 8;  // the LDS staging of one slice
+constexpr size_t kSelStageBytes = (size_t)kSelThreads * (kSelKPT + kSelPad) * 8;  // the LDS staging of one slice
 
 // idx_ws: two index lists of `key_stride` entries per unit (the stages' candidates).
 // seq_len, Hkv, page: the per-unit limit of Compressed-Quest pages (seq_len null: none).
