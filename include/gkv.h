@@ -297,7 +297,9 @@ gkv_status gkv_quest_select(const uint16_t *q, const gkv_cache *c, int32_t topk,
 /* Fused dequant + online-softmax GQA decode attention (sections 3.1, 3.7): for every
  * query head g of every sequence b, out[b][g][:] = sum_j softmax_j(q.k_j/sqrt(128)) v_j
  * over the read set -- all tokens < T (pages == NULL) or the selected pages
- * [B][Hkv][topk] plus the current page (section 3.5).  Residual rows override their
+ * [B][Hkv][topk] (ascending and distinct; an entry below 0 or at or past the current
+ * page, such as gkv_quest_select's -1 padding, reads nothing) plus the current page
+ * (section 3.5).  Residual rows override their
  * tokens' graded entries in both reads (section 3.4).  q: [B][Hq][128] fp16;
  * out: [B][Hq][128] fp32.  Pages may be 16, 32 or 64 tokens (a selected page reads
  * its tiles of one block).  GKV_E_UNSUPPORTED for more than 32767 visits per (b,h)

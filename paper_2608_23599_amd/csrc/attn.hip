@@ -1578,60 +1578,87 @@ __host__ __device__ __forceinline__ int quest_pages_per_wave(int page, bool resi
   return (residual ? 4 : 8) / (page / 16);
 }
 
-// Wavefront w of W of (b, KV head) u in a Compressed-Quest read: the read pages are
-// the leading valid selected pages (ascending; the list ends at its first -1 or
-// out-of-range entry) and then the current page (T - 1) / page; the wavefront takes
-// pages [w n / W, (w + 1) n / W) of those n, joins consecutive pages of one block
-// into one visit, and writes the visits' items and units (as the dense plan expands
-// its visits) into `items` and `units` (LDS).  Returns (items, units).
+// A 64-bit value of lane l (l uniform).
+__device__ __forceinline__ int64_t lane64(int64_t x, int l) {
+  const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)x, l);
+  const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)x >> 32), l);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// Wavefront w of W of (b, KV head) u in a Compressed-Quest read: the read slots are
+// the topk selected pages (ascending; an entry below 0 or at or past the current
+// page, such as the -1 padding, reads nothing) and then the current page
+// (T - 1) / page.  The wavefront takes slots [w n / W, (w + 1) n / W) of those
+// n = topk + 1, joins consecutive pages of one block into one visit, and writes the
+// visits' items and units (as the dense plan expands its visits) into `items` and
+// `units` (LDS).  Lane s loads slot i0 + s's page and then its block's table entries,
+// so the lists cost two dependent memory round trips whatever the wavefront's page
+// count; the visits are then built from registers.  Returns (items, units).
 __device__ __forceinline__ uint2 quest_lists(const AttnParams &p, int64_t u, int w, int W, int lane,
                                              ItemDesc *items, UnitDesc *units) {
   const int32_t *pg = p.pages + u * p.topk;
   const int64_t Tu = unit_T(p, u);
   if (Tu == 0) return make_uint2(0, 0);  // an empty or retired sequence reads nothing
   const int64_t cur = (Tu - 1) / p.page;
-  int cnt = p.topk;
-  for (int base = 0; base < p.topk; base += 64) {
-    const int i = base + lane;
-    const uint64_t bad = __ballot(i < p.topk && (pg[i] < 0 || pg[i] >= cur));
-    if (bad) {
-      cnt = base + __builtin_ctzll(bad);
-      break;
-    }
-  }
-  const int n = cnt + 1;
+  const int n = p.topk + 1;
   const int i0 = (int)(((int64_t)w * n) / W), i1 = (int)(((int64_t)(w + 1) * n) / W);
   // page pg lies in block pg >> pshift and covers tiles page_tiles(pg) of it
   const int pshift = p.page == 16 ? 2 : (p.page == 32 ? 1 : 0), tpp = p.page / 16;
-  auto page_at = [&](int i) { return (int64_t)uni(i < cnt ? pg[i] : (int32_t)cur); };
   auto page_tiles = [&](int64_t q) { return ((1u << tpp) - 1) << ((q & ((1 << pshift) - 1)) * tpp); };
-  const int8_t *lvl = p.level + u * p.nblk_cap;
-  const int64_t *ko = p.koff + u * p.nblk_cap, *vo = p.voff + u * p.nblk_cap;
+  // this lane's slot: its page (-1: nothing to read) and its block's table entries
+  const int si = i0 + lane;
+  int64_t q = -1;
+  if (si < i1) {
+    if (si < p.topk) {
+      const int64_t x = pg[si];
+      q = x >= 0 && x < cur ? x : -1;
+    } else {
+      q = cur;
+    }
+  }
+  int64_t lv = 0, kof = 0, vof = 0, bmask = 0, roff = 0;
+  if (q >= 0) {
+    const int64_t blk = u * p.nblk_cap + (q >> pshift);
+    lv = p.level[blk];
+    kof = p.koff[blk];
+    vof = p.voff[blk];
+    if (p.nres) {
+      bmask = (int64_t)p.res_mask[blk];
+      roff = p.res_off[u * (p.nblk_cap + 1) + (q >> pshift)];
+    }
+  }
+  const int ns = i1 - i0;
   uint32_t ni = 0, nu = 0;
-  for (int i = i0; i < i1;) {
-    const int64_t q0 = page_at(i), blk = q0 >> pshift;
+  for (int s = 0; s < ns;) {
+    const int64_t q0 = lane64(q, s);
+    if (q0 < 0) {
+      ++s;
+      continue;
+    }
+    const int64_t blk = q0 >> pshift;
     uint32_t tl = page_tiles(q0);
-    int j = i + 1;
-    for (; j < i1; ++j) {
-      const int64_t qj = page_at(j);
-      if ((qj >> pshift) != blk) break;
-      tl |= page_tiles(qj);
+    int t = s + 1;
+    for (; t < ns; ++t) {
+      const int64_t qt = lane64(q, t);
+      if (qt < 0) continue;
+      if ((qt >> pshift) != blk) break;
+      tl |= page_tiles(qt);
     }
     VisitDesc d;
-    d.level = (int16_t)uni(lvl[blk]);
+    d.level = (int16_t)__builtin_amdgcn_readlane((int)lv, s);
     d.blk = 0xFFFF;
-    d.kp = (uint64_t)(uintptr_t)(p.arena + uni64(ko[blk]));
-    d.vp = (uint64_t)(uintptr_t)(p.arena + uni64(vo[blk]));
+    d.kp = (uint64_t)(uintptr_t)(p.arena + lane64(kof, s));
+    d.vp = (uint64_t)(uintptr_t)(p.arena + lane64(vof, s));
     uint64_t va = 0;
-    for (int t = 0; t < 4; ++t)
-      if (tl & (1u << t)) va |= 0xFFFFull << (16 * t);
+    for (int tt = 0; tt < 4; ++tt)
+      if (tl & (1u << tt)) va |= 0xFFFFull << (16 * tt);
     d.valid = va & token_mask(Tu - blk * P);
     d.cost = 0;
     // residual rows override their tokens (section 3.4): the graded tiles skip them
     // and the exact tiles of the residual that hold their rows are read instead
     uint64_t bm = 0, rm = 0;
     if (p.nres) {
-      bm = (uint64_t)uni64((int64_t)p.res_mask[u * p.nblk_cap + blk]);
+      bm = (uint64_t)lane64(bmask, s);
       rm = bm & d.valid;
       d.valid &= ~bm;
     }
@@ -1640,7 +1667,7 @@ __device__ __forceinline__ uint2 quest_lists(const AttnParams &p, int64_t u, int
     ni += c & 7u;
     nu += c >> 3;
     if (rm) {
-      const int32_t r0 = uni(p.res_off[u * (p.nblk_cap + 1) + blk]);
+      const int32_t r0 = __builtin_amdgcn_readlane((int)roff, s);
       auto row_of = [&](uint64_t t) { return r0 + __popcll(bm & ((1ull << t) - 1)); };
       while (rm) {  // the read tokens' rows, ascending: one exact tile item per 16 rows
         const int rt = row_of(__builtin_ctzll(rm)) >> 4;
@@ -1665,7 +1692,7 @@ __device__ __forceinline__ uint2 quest_lists(const AttnParams &p, int64_t u, int
         nu += 2;
       }
     }
-    i = j;
+    s = t;
   }
   return make_uint2(ni, nu);
 }
