@@ -1003,7 +1003,7 @@ __device__ __forceinline__ bool exact_run(const AttnParams &p, State &st, const 
   return true;
 }
 
-template <int BITS, bool PACK, bool CERT, bool VTOK>
+template <int BITS, bool PACK, bool CERT, bool VTOK, bool QUEST>
 __device__ __forceinline__ bool int_run(const AttnParams &p, State &st, const uint8_t *qs, Pipe &pp,
                                         uint32_t &meta, uint64_t &valid, int lane) {
   IntBlock ib;
@@ -1030,9 +1030,12 @@ __device__ __forceinline__ bool int_run(const AttnParams &p, State &st, const ui
       *(uint2 *)(pp.ebuf + 8 * lane) = *(const uint2 *)(sz + 2048 + 8 * lane);  // V scale/zero, kept
       pp.release(1);
     }
-    const uint8_t *kq = pp.template pop<0>();
-    const uint8_t *vq = BITS == 2 ? kq + 2048 : pp.template pop<1>();
     const int n = meta_ntiles(meta);
+    // K and V codes in one unit (V at +2048): int2 items, and in a Compressed-Quest read
+    // every item with at most 2 KB of codes per tensor
+    const bool one_unit = BITS == 2 || (QUEST && n * 256 * BITS <= 2048);
+    const uint8_t *kq = pp.template pop<0>();
+    const uint8_t *vq = one_unit ? kq + 2048 : pp.template pop<1>();
     uint32_t tl = meta_tiles(meta);
     int j = 0;
 #pragma unroll 1
@@ -1054,7 +1057,7 @@ __device__ __forceinline__ bool int_run(const AttnParams &p, State &st, const ui
       int_epilogue<BITS, VTOK>(st, ib, pp.ebuf, lane);
       if (CERT) cert_add(st, ib.pb[0], ib.kerr, ib.verr);
     }
-    pp.release(BITS == 2 ? 1 : 2);
+    pp.release(one_unit ? 1 : 2);
     if (!pp.template next_item<CERT>(meta, valid)) return false;
   } while (meta_lv(meta) == BITS);
   return true;
@@ -1157,9 +1160,9 @@ __device__ __forceinline__ bool mean_run(const AttnParams &p, State &st, const u
 // Compressed-Quest reads take no plan: each wavefront writes its own item and unit
 // lists (defined with the plan code below).
 __device__ __forceinline__ uint2 quest_lists(const AttnParams &p, int64_t u, int w, int W, int lane,
-                                             ItemDesc *items, UnitDesc *units);
+                                             ItemDesc *items, UnitDesc *units, bool kv_one);
 
-template <bool PACK, bool CERT, bool VTOK>
+template <bool PACK, bool CERT, bool VTOK, bool QUEST>
 __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   extern __shared__ __align__(16) uint8_t smem[];
   // Workgroup L of the one-dimensional grid serves (b, KV head) L % units as its
@@ -1197,9 +1200,11 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   pp.ilds = (uint32_t)uni((int32_t)(uintptr_t)pp.ichunk);
   pp.cert = CERT ? p.cert + u * p.nblk_cap * 4 : nullptr;
   pp.blk = 0xFFFFu;
-  if (!CERT && p.pages) {
+  if (QUEST || (!CERT && p.pages)) {
     // Compressed-Quest: this wavefront's share of the read pages, listed in LDS here
-    const uint2 n = quest_lists(p, u, w, W, lane, (ItemDesc *)pp.ichunk, (UnitDesc *)pp.uchunk);
+    // (the dense instantiations keep this path as well, unpacked: their code then stays
+    // the one that the dense step was tuned with)
+    const uint2 n = quest_lists(p, u, w, W, lane, (ItemDesc *)pp.ichunk, (UnitDesc *)pp.uchunk, QUEST);
     pp.isrc = pp.usrc = nullptr;
     pp.nitems = (uint32_t)uni((int32_t)n.x);
     pp.nunits = (uint32_t)uni((int32_t)n.y);
@@ -1244,9 +1249,9 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   while (more) {
     switch (meta_lv(meta)) {
       case GKV_EXACT: more = exact_run<PACK, CERT>(p, st, qs, pp, meta, valid, lane); break;
-      case GKV_INT8: more = int_run<8, PACK, CERT, VTOK>(p, st, qs, pp, meta, valid, lane); break;
-      case GKV_INT4: more = int_run<4, PACK, CERT, VTOK>(p, st, qs, pp, meta, valid, lane); break;
-      case GKV_INT2: more = int_run<2, PACK, CERT, VTOK>(p, st, qs, pp, meta, valid, lane); break;
+      case GKV_INT8: more = int_run<8, PACK, CERT, VTOK, QUEST>(p, st, qs, pp, meta, valid, lane); break;
+      case GKV_INT4: more = int_run<4, PACK, CERT, VTOK, QUEST>(p, st, qs, pp, meta, valid, lane); break;
+      case GKV_INT2: more = int_run<2, PACK, CERT, VTOK, QUEST>(p, st, qs, pp, meta, valid, lane); break;
       case GKV_CENTROID: more = centroid_run<PACK, CERT>(p, st, qs, pp, meta, valid, lane); break;
       default: more = mean_run<PACK, CERT>(p, st, qs, pp, meta, valid, lane); break;
     }
@@ -1470,7 +1475,7 @@ __device__ __forceinline__ uint64_t block_scan(uint64_t x, uint64_t *sh, uint64_
 }
 
 // Items and units of a visit (as visit_items writes them): items | units << 3.
-__device__ __forceinline__ uint32_t visit_counts(int lv, uint64_t valid) {
+__device__ __forceinline__ uint32_t visit_counts(int lv, uint64_t valid, bool kv_one = false) {
   if (run_blocks(lv) > 1) return 1u | (1u << 3);
   uint32_t tiles = 0;
   for (int t = 0; t < 4; ++t)
@@ -1479,15 +1484,16 @@ __device__ __forceinline__ uint32_t visit_counts(int lv, uint64_t valid) {
   if (lv == GKV_CENTROID || lv == GKV_MEAN) return 1u | (1u << 3);
   if (lv == GKV_EXACT) return (uint32_t)__builtin_popcount(tiles) * (1u | (2u << 3));
   const int tg = group_tiles(lv);
-  uint32_t k = 0;
+  uint32_t k = 0, m = 1;  // items; units (the scale/zero unit first)
   while (tiles) {
     const uint32_t t = __builtin_ctz(tiles);
     uint32_t n = 1;
     while ((int)n < tg && ((tiles >> (t + n)) & 1u)) ++n;
     tiles &= ~(((1u << n) - 1) << t);
     ++k;
+    m += lv == 2 || (kv_one && n * 256 * (uint32_t)lv <= 2048) ? 1u : 2u;  // K and V codes in one unit or two
   }
-  return k | ((k * (lv == 2 ? 1u : 2u) + 1) << 3);  // the items' units and the scale/zero unit
+  return k | (m << 3);
 }
 
 // A unit of part A (ba bytes from a) and part B (bb bytes from b); each part at most
@@ -1504,7 +1510,7 @@ __device__ __forceinline__ UnitDesc unit_desc(uint64_t a, uint32_t ba, uint64_t 
 }
 
 // Writes the items and units of a visit, in order.
-__device__ __forceinline__ void visit_items(const VisitDesc &v, ItemDesc *items, UnitDesc *units) {
+__device__ __forceinline__ void visit_items(const VisitDesc &v, ItemDesc *items, UnitDesc *units, bool kv_one = false) {
   uint32_t tiles = 0;
   for (int t = 0; t < 4; ++t)
     if ((v.valid >> (16 * t)) & 0xFFFFull) tiles |= 1u << t;
@@ -1556,7 +1562,7 @@ __device__ __forceinline__ void visit_items(const VisitDesc &v, ItemDesc *items,
     left &= ~taken;
     put(k++, kIntGroup, first, left == 0, taken, n, 0);
     const uint32_t off = kSZBytes + t * 256 * lv, span = n * 256 * lv;
-    if (lv == 2) {
+    if (lv == 2 || (kv_one && span <= 2048)) {  // the K and V codes share one unit (V at +2048)
       units[m++] = unit_desc(v.kp + off, span, v.vp + off, span);
     } else {
       const uint32_t pa = span < 2048 ? span : 2048, pb = span - pa;
@@ -1595,7 +1601,7 @@ __device__ __forceinline__ int64_t lane64(int64_t x, int l) {
 // so the lists cost two dependent memory round trips whatever the wavefront's page
 // count; the visits are then built from registers.  Returns (items, units).
 __device__ __forceinline__ uint2 quest_lists(const AttnParams &p, int64_t u, int w, int W, int lane,
-                                             ItemDesc *items, UnitDesc *units) {
+                                             ItemDesc *items, UnitDesc *units, bool kv_one) {
   const int32_t *pg = p.pages + u * p.topk;
   const int64_t Tu = unit_T(p, u);
   if (Tu == 0) return make_uint2(0, 0);  // an empty or retired sequence reads nothing
@@ -1662,8 +1668,8 @@ __device__ __forceinline__ uint2 quest_lists(const AttnParams &p, int64_t u, int
       rm = bm & d.valid;
       d.valid &= ~bm;
     }
-    const uint32_t c = visit_counts(d.level, d.valid);
-    if (lane == 0) visit_items(d, items + ni, units + nu);
+    const uint32_t c = visit_counts(d.level, d.valid, kv_one);
+    if (lane == 0) visit_items(d, items + ni, units + nu, kv_one);
     ni += c & 7u;
     nu += c >> 3;
     if (rm) {
@@ -2105,27 +2111,38 @@ static void launch_plan(const AttnParams &p, const gkv_cache *c, hipStream_t s) 
 static void launch_partials(const AttnParams &p, const gkv_cache *c, hipStream_t s) {
   const size_t lds = (size_t)kWaves * kWaveLds + 16 * kQRow;  // rings also hold the merge buffers
   const dim3 grid(p.nsplit * c->Hkv * c->B);
-  // the certificate sums and per-token value groups are separate instantiations: the
-  // plain decode keeps its registers
+  // the certificate sums, per-token value groups and Compressed-Quest lists are
+  // separate instantiations: the plain dense decode keeps its registers and code
   const bool pack = p.G <= 8, cert = p.bound != nullptr, vtok = c->v_per_token != 0;
+  const bool quest = p.pages != nullptr && !cert;  // the certificate is a dense read
   const dim3 blk(kThreads);
-  if (vtok) {
-    if (cert) {
-      if (pack) hipLaunchKernelGGL((attn_kernel<true, true, true>), grid, blk, lds, s, p);
-      else hipLaunchKernelGGL((attn_kernel<false, true, true>), grid, blk, lds, s, p);
+#define GKV_ATTN(a, b, c2, d) hipLaunchKernelGGL((attn_kernel<a, b, c2, d>), grid, blk, lds, s, p)
+  if (quest) {
+    if (vtok) {
+      if (pack) GKV_ATTN(true, false, true, true);
+      else GKV_ATTN(false, false, true, true);
     } else {
-      if (pack) hipLaunchKernelGGL((attn_kernel<true, false, true>), grid, blk, lds, s, p);
-      else hipLaunchKernelGGL((attn_kernel<false, false, true>), grid, blk, lds, s, p);
+      if (pack) GKV_ATTN(true, false, false, true);
+      else GKV_ATTN(false, false, false, true);
+    }
+  } else if (vtok) {
+    if (cert) {
+      if (pack) GKV_ATTN(true, true, true, false);
+      else GKV_ATTN(false, true, true, false);
+    } else {
+      if (pack) GKV_ATTN(true, false, true, false);
+      else GKV_ATTN(false, false, true, false);
     }
   } else {
     if (cert) {
-      if (pack) hipLaunchKernelGGL((attn_kernel<true, true, false>), grid, blk, lds, s, p);
-      else hipLaunchKernelGGL((attn_kernel<false, true, false>), grid, blk, lds, s, p);
+      if (pack) GKV_ATTN(true, true, false, false);
+      else GKV_ATTN(false, true, false, false);
     } else {
-      if (pack) hipLaunchKernelGGL((attn_kernel<true, false, false>), grid, blk, lds, s, p);
-      else hipLaunchKernelGGL((attn_kernel<false, false, false>), grid, blk, lds, s, p);
+      if (pack) GKV_ATTN(true, false, false, false);
+      else GKV_ATTN(false, false, false, false);
     }
   }
+#undef GKV_ATTN
 }
 static void launch_merge(const AttnParams &p, const gkv_cache *c, float *out, hipStream_t s) {
   hipLaunchKernelGGL(merge_kernel, dim3(p.G, c->Hkv * c->B), dim3(D), 0, s, (const float *)p.part, out, p.nsplit,
