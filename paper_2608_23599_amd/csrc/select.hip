@@ -274,7 +274,7 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
                                                              int32_t *__restrict__ out, int64_t out_stride,
                                                              uint64_t *mask, int64_t mask_stride,
                                                              int64_t mask_words, const int64_t *seq_len, int Hkv,
-                                                             int page) {
+                                                             int page, uint64_t *okeys, int64_t okey_stride) {
   __shared__ SelShared sh;
   const int64_t u = blockIdx.y, base = (int64_t)blockIdx.x * slice;
   int64_t limit = INT64_MAX;  // the unit's own ranked pages (last stage only)
@@ -286,6 +286,7 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
   const uint64_t *key = keys + u * key_stride;
   const int32_t *ix = idx ? idx + u * idx_stride + base : nullptr;  // KPT > 0 only
   int32_t *o = out + u * out_stride + (int64_t)blockIdx.x * k;
+  uint64_t *ok = okeys ? okeys + u * okey_stride + (int64_t)blockIdx.x * k : nullptr;
   uint64_t *mk = mask ? mask + u * mask_stride : nullptr;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   if (mk)
@@ -309,8 +310,10 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
     }
   };
   for (int i = tid; i < 256; i += kSelThreads) sh.hist[i] = 0;
-  if (KPT > 0 && !ix) {
-    // a contiguous slice: staged through LDS with lane-contiguous loads, then each
+  int32_t tix[KPT > 0 ? KPT : 1];  // a later stage: the candidates' original indices
+  if (KPT > 0) {
+    // a contiguous slice (the first stage's keys, or the previous stage's winners' keys
+    // in candidate order): staged through LDS with lane-contiguous loads, then each
     // thread takes its KPT consecutive keys (loads that each touch 64 scattered
     // 8-byte words took three times as long).  Each thread's KPT keys are followed by
     // kSelPad empty words, so that the 16-byte reads of eight neighbouring lanes fall
@@ -324,6 +327,13 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
       const int64_t i = (int64_t)j * kSelThreads + tid;
       t[j] = src[i < n ? i : n - 1];
     }
+    if (ix) {
+#pragma unroll
+      for (int j = 0; j < KPT; ++j) {  // this thread's candidates' indices, for the output
+        const int64_t i = (int64_t)tid * KPT + j;
+        tix[j] = ix[i < n ? i : n - 1];
+      }
+    }
 #pragma unroll
     for (int j = 0; j < KPT; ++j) {
       const int i = j * kSelThreads + tid;
@@ -335,24 +345,6 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < KPT; ++j) kr[j] = stage[tid * (KPT + kSelPad) + j];
-  } else if (KPT > 0) {
-    int32_t t[KPT > 0 ? KPT : 1];
-#pragma unroll
-    for (int j = 0; j < KPT; ++j) {  // unconditional loads (a clamped index): all in flight at once
-      const int64_t i = (int64_t)tid * KPT + j;
-      t[j] = ix[i < n ? i : n - 1];
-    }
-#pragma unroll
-    for (int j = 0; j < KPT; ++j) {
-      kr[j] = key[(int64_t)t[j]];
-      kand &= kr[j];
-      kor |= kr[j];
-    }
-#pragma unroll
-    for (int j = 0; j < KPT; ++j)
-      if ((int64_t)tid * KPT + j >= n) kr[j] = 0;
-    wave_andor();
-    __syncthreads();
   } else {
     for (int64_t i = tid; i < n; i += kSelThreads) {
       const uint64_t kv = key[i];
@@ -453,7 +445,8 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
       if (i < n) {
         const bool sel = kr[j] > thr || (kr[j] == thr && eq++ < eq_take);
         if (sel) {
-          const int64_t t = ix ? (int64_t)ix[i] : base + i;
+          const int64_t t = ix ? (int64_t)tix[j] : base + i;
+          if (ok) ok[pos] = kr[j];
           o[pos++] = t < limit ? (int32_t)t : -1;
           if (mk) atomicOr((unsigned long long *)&mk[t >> 6], 1ull << (t & 63));
         }
@@ -493,8 +486,12 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
 
 constexpr int64_t kSelSlice = (int64_t)kSelKPT * kSelThreads;
 constexpr size_t kSelStageBytes = (size_t)kSelThreads * (kSelKPT + kSelPad) * 8;  // the LDS staging of one slice
+// Entries per unit of a stage's winners' key list: a stage keeps at most k of every
+// slice with 2k <= kSelSlice, so at most n / 2 + kSelSlice / 2 of n candidates.
+static int64_t sel_ckey_stride(int64_t key_stride) { return key_stride / 2 + kSelSlice / 2; }
 
-// idx_ws: two index lists of `key_stride` entries per unit (the stages' candidates).
+// idx_ws: two index lists of `key_stride` entries per unit (the stages' candidates),
+// then two key lists of sel_ckey_stride(key_stride) entries per unit (their keys).
 // seq_len, Hkv, page: the per-unit limit of Compressed-Quest pages (seq_len null: none).
 void launch_select(const uint64_t *keys, int64_t key_stride, int64_t n, int k, int32_t *out, int64_t out_stride,
                    uint64_t *mask, int64_t mask_stride, int64_t mask_words, int units, int32_t *idx_ws,
@@ -502,25 +499,30 @@ void launch_select(const uint64_t *keys, int64_t key_stride, int64_t n, int k, i
   if (n > kSelSlice && 2 * (int64_t)k > kSelSlice) {  // too few candidates dropped per stage: one streamed pass
     hipLaunchKernelGGL(select_kernel<0>, dim3(1, units), dim3(kSelThreads), 0, s, keys, key_stride,
                        (const int32_t *)nullptr, (int64_t)0, n, n, k, out, out_stride, mask, mask_stride, mask_words,
-                       seq_len, Hkv, page);
+                       seq_len, Hkv, page, (uint64_t *)nullptr, (int64_t)0);
     return;
   }
   const int32_t *idx = nullptr;
-  int64_t cur = n;
+  const uint64_t *kin = keys;
+  int64_t kin_stride = key_stride, cur = n;
+  const int64_t cks = sel_ckey_stride(key_stride);
+  uint64_t *ckeys = (uint64_t *)(idx_ws + 2 * (int64_t)units * key_stride);
   for (int buf = 0; cur > kSelSlice; buf ^= 1) {
     const int64_t S = (cur + kSelSlice - 1) / kSelSlice;
     int32_t *dst = idx_ws + (int64_t)buf * units * key_stride;
-    hipLaunchKernelGGL(select_kernel<kSelKPT>, dim3((unsigned)S, units), dim3(kSelThreads), kSelStageBytes, s, keys,
-                       key_stride,
-                       idx, key_stride, cur, kSelSlice, k, dst, key_stride, (uint64_t *)nullptr, (int64_t)0,
-                       (int64_t)0, seq_len, Hkv, page);
+    uint64_t *kdst = ckeys + (int64_t)buf * units * cks;
+    hipLaunchKernelGGL(select_kernel<kSelKPT>, dim3((unsigned)S, units), dim3(kSelThreads), kSelStageBytes, s, kin,
+                       kin_stride, idx, key_stride, cur, kSelSlice, k, dst, key_stride, (uint64_t *)nullptr,
+                       (int64_t)0, (int64_t)0, seq_len, Hkv, page, kdst, cks);
     const int64_t last = cur - (S - 1) * kSelSlice;
     cur = (S - 1) * k + (last < k ? last : k);
     idx = dst;
+    kin = kdst;
+    kin_stride = cks;
   }
-  hipLaunchKernelGGL(select_kernel<kSelKPT>, dim3(1, units), dim3(kSelThreads), kSelStageBytes, s, keys, key_stride,
-                     idx,
-                     key_stride, cur, cur, k, out, out_stride, mask, mask_stride, mask_words, seq_len, Hkv, page);
+  hipLaunchKernelGGL(select_kernel<kSelKPT>, dim3(1, units), dim3(kSelThreads), kSelStageBytes, s, kin, kin_stride,
+                     idx, key_stride, cur, cur, k, out, out_stride, mask, mask_stride, mask_words, seq_len, Hkv, page,
+                     (uint64_t *)nullptr, (int64_t)0);
 }
 
 // Copy the exact key/value rows of the selected residual tokens into exact-format
@@ -590,12 +592,17 @@ __global__ void __launch_bounds__(256) res_off_kernel(const uint64_t *__restrict
 }  // namespace
 
 // ---------------------------------------------------------------- C ABI
-// keys (8 bytes) and two candidate index lists (4 bytes each) per ranked item
-static int64_t quest_ws(const gkv_cache *c) { return (int64_t)c->B * c->Hkv * c->npage_cap * 16; }
+// keys (8 bytes) and two candidate index lists (4 bytes each) per ranked item, then the
+// two key lists of the selection stages
+static int64_t quest_ws(const gkv_cache *c) {
+  return (int64_t)c->B * c->Hkv * (c->npage_cap * 16 + 2 * sel_ckey_stride(c->npage_cap) * 8);
+}
 // the residual selection's keys and lists are strided by the block capacity in tokens,
 // so that one workspace serves the cache at any length
 static int64_t rd_stride(const gkv_cache *c) { return (int64_t)c->nblk_cap * P; }
-static int64_t rd_ws(const gkv_cache *c) { return (int64_t)c->B * c->Hkv * rd_stride(c) * 16; }
+static int64_t rd_ws(const gkv_cache *c) {
+  return (int64_t)c->B * c->Hkv * (rd_stride(c) * 16 + 2 * sel_ckey_stride(rd_stride(c)) * 8);
+}
 
 extern "C" int64_t gkv_workspace_bytes(const gkv_cache *c, int32_t op, int32_t topk) {
   if (gkv_validate_cache(c)) return -1;
