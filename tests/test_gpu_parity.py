@@ -97,6 +97,29 @@ def test_quest_boxes_selection_and_sparse_attention(gpu, T, topk):
                 assert max_err(out[b, h * G:(h + 1) * G], uc.decode_dense(q_group(q, b, h, G))) <= TOL
 
 
+def test_quest_read_skips_invalid_entries(gpu):
+    """A Compressed-Quest read reads the ascending selected pages of the list and skips
+    every entry below 0 or at or past the current page, wherever it stands: the output
+    equals the oracle's read of the valid pages plus the current page."""
+    T, Hq, Hkv, topk = 4099, 8, 2, 24
+    ks, vs = kv_all(3, 1, Hkv, T)
+    lv = olad.ladder("graded", T)
+    cache = _build(gpu, ks, vs, Hq, lv, page=16)
+    G = Hq // Hkv
+    q = synth.queries(3, 1, Hq, step=5)
+    cur = (T - 1) // 16
+    lists = [[-1, 3, 4, -1, 17, 40, 41, 64, -1, 100, cur, 170, 200, cur + 3, 240, 255, -1, -1, 5000, -1, -1, -1, -1, -1],
+             [0, 1, 2, -1, -1, 63, 64, 65, 66, 67, 68, -1, 127, 128, 129, 130, 131, 200, 201, 202, 203, 250, -1, cur]]
+    assert all(len(x) == topk for x in lists)
+    pages = _torch().from_numpy(np.array(lists, dtype=np.int32)[None]).cuda()
+    out = cache.decode(q, pages=pages).cpu().numpy()
+    for h in range(Hkv):
+        uc = ocache.UnitCache(ks[0, h], vs[0, h], lv)
+        valid = np.array([x for x in lists[h] if 0 <= x < cur], dtype=np.int32)
+        ref = uc.decode_quest(q_group(q, 0, h, G), valid, 16)
+        assert max_err(out[0, h * G:(h + 1) * G], ref) <= TOL
+
+
 @pytest.mark.parametrize("page,T,topk", [(32, 6001, 40), (64, 8192, 30), (64, 3000, 50)])
 def test_quest_larger_pages(gpu, page, T, topk):
     """Compressed-Quest with 32- and 64-token pages (the paper's own box granularity is
