@@ -1160,7 +1160,7 @@ __device__ __forceinline__ bool mean_run(const AttnParams &p, State &st, const u
 // Compressed-Quest reads take no plan: each wavefront writes its own item and unit
 // lists (defined with the plan code below).
 __device__ __forceinline__ uint2 quest_lists(const AttnParams &p, int64_t u, int w, int W, int lane,
-                                             ItemDesc *items, UnitDesc *units, bool kv_one);
+                                             ItemDesc *items, UnitDesc *units);
 
 template <bool PACK, bool CERT, bool VTOK, bool QUEST>
 __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
@@ -1200,11 +1200,9 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   pp.ilds = (uint32_t)uni((int32_t)(uintptr_t)pp.ichunk);
   pp.cert = CERT ? p.cert + u * p.nblk_cap * 4 : nullptr;
   pp.blk = 0xFFFFu;
-  if (QUEST || (!CERT && p.pages)) {
+  if (QUEST) {
     // Compressed-Quest: this wavefront's share of the read pages, listed in LDS here
-    // (the dense instantiations keep this path as well, unpacked: their code then stays
-    // the one that the dense step was tuned with)
-    const uint2 n = quest_lists(p, u, w, W, lane, (ItemDesc *)pp.ichunk, (UnitDesc *)pp.uchunk, QUEST);
+    const uint2 n = quest_lists(p, u, w, W, lane, (ItemDesc *)pp.ichunk, (UnitDesc *)pp.uchunk);
     pp.isrc = pp.usrc = nullptr;
     pp.nitems = (uint32_t)uni((int32_t)n.x);
     pp.nunits = (uint32_t)uni((int32_t)n.y);
@@ -1599,9 +1597,10 @@ __device__ __forceinline__ int64_t lane64(int64_t x, int l) {
 // visits' items and units (as the dense plan expands its visits) into `items` and
 // `units` (LDS).  Lane s loads slot i0 + s's page and then its block's table entries,
 // so the lists cost two dependent memory round trips whatever the wavefront's page
-// count; the visits are then built from registers.  Returns (items, units).
+// count; the visits are then built from registers.  An int4/int8 item with at most 2 KB
+// of codes per tensor copies its K and V codes in one unit.  Returns (items, units).
 __device__ __forceinline__ uint2 quest_lists(const AttnParams &p, int64_t u, int w, int W, int lane,
-                                             ItemDesc *items, UnitDesc *units, bool kv_one) {
+                                             ItemDesc *items, UnitDesc *units) {
   const int32_t *pg = p.pages + u * p.topk;
   const int64_t Tu = unit_T(p, u);
   if (Tu == 0) return make_uint2(0, 0);  // an empty or retired sequence reads nothing
@@ -1668,8 +1667,8 @@ __device__ __forceinline__ uint2 quest_lists(const AttnParams &p, int64_t u, int
       rm = bm & d.valid;
       d.valid &= ~bm;
     }
-    const uint32_t c = visit_counts(d.level, d.valid, kv_one);
-    if (lane == 0) visit_items(d, items + ni, units + nu, kv_one);
+    const uint32_t c = visit_counts(d.level, d.valid, true);
+    if (lane == 0) visit_items(d, items + ni, units + nu, true);
     ni += c & 7u;
     nu += c >> 3;
     if (rm) {
