@@ -430,18 +430,46 @@ __global__ void __launch_bounds__(D) alloc_kernel(const uint16_t *__restrict__ k
     if (d == 0) levels[u * nblk + blk] = GKV_EXACT;
     return;
   }
-  const uint16_t *kb = k_src + (u * T + (int64_t)blk * P) * D + d;
-  double mn = (double)__builtin_bit_cast(_Float16, kb[0]), mx = mn;
-  for (int t = 1; t < P; ++t) {
-    const double x = (double)__builtin_bit_cast(_Float16, kb[(int64_t)t * D]);
-    mn = x < mn ? x : mn;
-    mx = x > mx ? x : mx;
+  // thread d reads channels 8 (d % 16) .. +7 of rows d / 16, d / 16 + 8, .. (eight
+  // 16-byte streaming loads, each row of the block read by 16 neighbouring lanes), then
+  // the eight row groups' minima and maxima meet in LDS: min and max are exact in fp16
+  const int cg = d & 15, rg = d >> 4;
+  const _Float16 *kb = (const _Float16 *)k_src + (u * T + (int64_t)blk * P + rg) * D + 8 * cg;
+  half8 v[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) v[j] = __builtin_nontemporal_load((const half8 *)(kb + (int64_t)8 * j * D));
+  half8 mn = v[0], mx = v[0];
+#pragma unroll
+  for (int j = 1; j < 8; ++j) {
+    mn = __builtin_elementwise_min(mn, v[j]);
+    mx = __builtin_elementwise_max(mx, v[j]);
   }
-  rng[d] = mx - mn;  // exact in fp64
+  __shared__ half8 smn[8][16], smx[8][16];
+  smn[rg][cg] = mn;
+  smx[rg][cg] = mx;
+  __syncthreads();
+  {
+    const int c = d >> 3, e = d & 7;  // channel d = 8 c + e
+    _Float16 lo = smn[0][c][e], hi = smx[0][c][e];
+#pragma unroll
+    for (int r = 1; r < 8; ++r) {
+      lo = smn[r][c][e] < lo ? smn[r][c][e] : lo;
+      hi = smx[r][c][e] > hi ? smx[r][c][e] : hi;
+    }
+    // the largest channel range (exact in fp64, and max needs no order): within each
+    // wavefront by shuffles, then over the two wavefronts
+    double r = (double)hi - (double)lo;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      const double t = __shfl_xor(r, o);
+      r = t > r ? t : r;
+    }
+    if ((d & 63) == 0) rng[d >> 6] = r;
+  }
   __syncthreads();
   if (d == 0) {
     double e = rng[0];
-    for (int i = 1; i < D; ++i) e = rng[i] > e ? rng[i] : e;
+    for (int i = 1; i < D / 64; ++i) e = rng[i] > e ? rng[i] : e;
     double x = c * qn[u];
     x = x * e;
     x = x * (double)nblk;
