@@ -505,6 +505,8 @@ __global__ void __launch_bounds__(128) append_kernel(const uint16_t *__restrict_
 }
 
 // Page boxes from token-major exact keys; one workgroup per 64 pages of one (b,h).
+typedef _Float16 bx8 __attribute__((ext_vector_type(8)));
+typedef uint32_t bw4 __attribute__((ext_vector_type(4)));
 __global__ void __launch_bounds__(kThreads) boxes_kernel(const uint16_t *__restrict__ k_src, int64_t T_src,
                                                          uint16_t *boxes, int64_t npage_cap, int page, int Hkv,
                                                          int64_t page_begin, int64_t page_end,
@@ -519,19 +521,32 @@ __global__ void __launch_bounds__(kThreads) boxes_kernel(const uint16_t *__restr
     const int64_t last = seq_len[b] < 0 ? 0 : seq_len[b] / page;
     page_end = page_end < last ? page_end : last;
   }
-  for (int i = threadIdx.x; i < 64 * D; i += kThreads) {
-    const int pi = i >> 7, d = i & 127;
+  // sixteen lanes per page, each with eight channels: sixteen 16-byte streaming row
+  // loads in flight per lane, then packed fp16 minima and maxima (exact)
+  constexpr int kPagesPerPass = kThreads / 16;
+  const int cg = threadIdx.x & 15;
+  for (int pi = threadIdx.x >> 4; pi < 64; pi += kPagesPerPass) {
     const int64_t p = p_lo + pi;
     if (p < page_begin || p >= page_end) continue;
-    const uint16_t *row = src + p * page * D + d;
-    _Float16 mn = __builtin_bit_cast(_Float16, row[0]), mx = mn;
-    for (int t = 1; t < page; ++t) {
-      const _Float16 v = __builtin_bit_cast(_Float16, row[(int64_t)t * D]);
-      mn = v < mn ? v : mn;
-      mx = v > mx ? v : mx;
+    const _Float16 *row = (const _Float16 *)src + p * page * D + 8 * cg;
+    bx8 mn, mx;
+    for (int t0 = 0; t0 < page; t0 += 16) {
+      bx8 v[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) v[j] = __builtin_nontemporal_load((const bx8 *)(row + (int64_t)(t0 + j) * D));
+      if (t0 == 0) mn = mx = v[0];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        mn = __builtin_elementwise_min(mn, v[j]);
+        mx = __builtin_elementwise_max(mx, v[j]);
+      }
     }
-    stage[d * 64 + pi] = (uint32_t)canon_zero(__builtin_bit_cast(uint16_t, mn)) |
-                         ((uint32_t)canon_zero(__builtin_bit_cast(uint16_t, mx)) << 16);
+    const bw4 lw = __builtin_bit_cast(bw4, mn), hw = __builtin_bit_cast(bw4, mx);  // channel pairs
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint16_t lo = (uint16_t)(lw[e >> 1] >> (16 * (e & 1))), hi = (uint16_t)(hw[e >> 1] >> (16 * (e & 1)));
+      stage[(8 * cg + e) * 64 + pi] = (uint32_t)canon_zero(lo) | ((uint32_t)canon_zero(hi) << 16);
+    }
   }
   __syncthreads();
   uint32_t *out = (uint32_t *)(boxes + u * npage_cap * 2 * D + box_index(p_lo, 0));
