@@ -123,6 +123,7 @@ constexpr int kSelWaves = kSelThreads / 64;
 
 constexpr int kSelKPT = 8;  // keys per thread held in registers (n <= 8192)
 constexpr int kSelPad = 2;  // empty 8-byte words after each thread's keys in the LDS staging
+constexpr int kSelStream = 8;  // keys in flight per thread in the streamed loops (a clamped index)
 constexpr int kSelRank = 16;  // candidates ranked directly instead of another radix pass (<= 64)
 
 struct SelShared {
@@ -233,12 +234,21 @@ __device__ __forceinline__ void small_candidates(SelShared &sh, const uint64_t *
       }
     }
   } else {
-    for (int64_t i = tid; i < n; i += kSelThreads) {
-      const uint64_t kv = key[i];
-      if ((kv & pm) == pre) {
-        const uint32_t at = atomicAdd(cnt, 1u);
-        ckey[at] = kv;
-        cidx[at] = (int32_t)i;
+    for (int64_t i0 = tid; i0 < n; i0 += (int64_t)kSelStream * kSelThreads) {
+      uint64_t kv[kSelStream];
+#pragma unroll
+      for (int j = 0; j < kSelStream; ++j) {
+        const int64_t i = i0 + (int64_t)j * kSelThreads;
+        kv[j] = key[i < n ? i : n - 1];
+      }
+#pragma unroll
+      for (int j = 0; j < kSelStream; ++j) {
+        const int64_t i = i0 + (int64_t)j * kSelThreads;
+        if (i < n && (kv[j] & pm) == pre) {
+          const uint32_t at = atomicAdd(cnt, 1u);
+          ckey[at] = kv[j];
+          cidx[at] = (int32_t)i;
+        }
       }
     }
   }
@@ -346,10 +356,14 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
 #pragma unroll
     for (int j = 0; j < KPT; ++j) kr[j] = stage[tid * (KPT + kSelPad) + j];
   } else {
-    for (int64_t i = tid; i < n; i += kSelThreads) {
-      const uint64_t kv = key[i];
-      kand &= kv;
-      kor |= kv;
+    for (int64_t i0 = tid; i0 < n; i0 += (int64_t)kSelStream * kSelThreads) {
+#pragma unroll
+      for (int j = 0; j < kSelStream; ++j) {  // a clamped load repeats a real key
+        const int64_t i = i0 + (int64_t)j * kSelThreads;
+        const uint64_t kv = key[i < n ? i : n - 1];
+        kand &= kv;
+        kor |= kv;
+      }
     }
     wave_andor();
     __syncthreads();
@@ -383,9 +397,17 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
         if (i < n && (kr[j] & pm) == pre) atomicAdd(&sh.hist[(kr[j] >> shift) & dmask], 1u);
       }
     } else {
-      for (int64_t i = tid; i < n; i += kSelThreads) {
-        const uint64_t kv = key[i];
-        if ((kv & pm) == pre) atomicAdd(&sh.hist[(kv >> shift) & dmask], 1u);
+      for (int64_t i0 = tid; i0 < n; i0 += (int64_t)kSelStream * kSelThreads) {
+        uint64_t kv[kSelStream];
+#pragma unroll
+        for (int j = 0; j < kSelStream; ++j) {
+          const int64_t i = i0 + (int64_t)j * kSelThreads;
+          kv[j] = key[i < n ? i : n - 1];
+        }
+#pragma unroll
+        for (int j = 0; j < kSelStream; ++j)
+          if (i0 + (int64_t)j * kSelThreads < n && (kv[j] & pm) == pre)
+            atomicAdd(&sh.hist[(kv[j] >> shift) & dmask], 1u);
       }
     }
     __syncthreads();
@@ -454,33 +476,40 @@ __global__ void __launch_bounds__(kSelThreads) select_kernel(const uint64_t *__r
     }
     return;
   }
-  // streamed: chunks of kSelThreads keys, one key per thread
-  if (tid == 0) {
-    sh.base[0] = 0;  // selected so far
-    sh.base[1] = 0;  // keys equal to thr so far
-  }
-  __syncthreads();
-  for (int64_t c0 = 0; c0 < n; c0 += kSelThreads) {
-    const int64_t i = c0 + tid;
-    const bool in = i < n;
-    const uint64_t kv = in ? key[i] : 0;
-    int64_t g = in && kv > thr, e = in && kv == thr;
-    const int64_t b0 = sh.base[0], b1 = sh.base[1];
+  // streamed: chunks of kSelStream * kSelThreads keys, kSelStream consecutive keys per
+  // thread; b0 (selected so far) and b1 (keys equal to thr so far) follow from the
+  // chunks' totals, the same in every thread
+  int64_t b0 = 0, b1 = 0;
+  const int64_t chunk = (int64_t)kSelStream * kSelThreads;
+  for (int64_t c0 = 0; c0 < n; c0 += chunk) {
+    const int64_t t0 = c0 + (int64_t)tid * kSelStream;
+    uint64_t kv[kSelStream];
+#pragma unroll
+    for (int j = 0; j < kSelStream; ++j) kv[j] = key[t0 + j < n ? t0 + j : n - 1];
+    int64_t g = 0, e = 0;
+#pragma unroll
+    for (int j = 0; j < kSelStream; ++j)
+      if (t0 + j < n) {
+        g += kv[j] > thr;
+        e += kv[j] == thr;
+      }
     int64_t tg, te;
-    const int64_t g0 = g, e0 = e;
-    scan2(sh, g, e, tg, te);
-    const int64_t eq_rank = b1 + e;
-    const bool sel = g0 || (e0 && eq_rank < eq_take);
-    const int64_t pos = b0 + g + (e < eq_take - b1 ? e : (eq_take - b1 > 0 ? eq_take - b1 : 0));
-    if (sel) {
-      o[pos] = i < limit ? (int32_t)i : -1;
-      if (mk) atomicOr((unsigned long long *)&mk[i >> 6], 1ull << (i & 63));
+    scan2(sh, g, e, tg, te);  // g, e: counts in the chunk's threads before this one
+    const int64_t left = eq_take - b1 > 0 ? eq_take - b1 : 0;  // equal keys still to take
+    int64_t pos = b0 + g + (e < left ? e : left);
+#pragma unroll
+    for (int j = 0; j < kSelStream; ++j) {
+      const int64_t i = t0 + j;
+      if (i < n) {
+        const bool sel = kv[j] > thr || (kv[j] == thr && e++ < left);
+        if (sel) {
+          o[pos++] = i < limit ? (int32_t)i : -1;
+          if (mk) atomicOr((unsigned long long *)&mk[i >> 6], 1ull << (i & 63));
+        }
+      }
     }
-    if (tid == 0) {
-      sh.base[0] = b0 + tg + (te < eq_take - b1 ? te : (eq_take - b1 > 0 ? eq_take - b1 : 0));
-      sh.base[1] = b1 + te;
-    }
-    __syncthreads();
+    b0 += tg + (te < left ? te : left);
+    b1 += te;
   }
 }
 
