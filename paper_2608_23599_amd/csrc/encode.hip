@@ -558,34 +558,171 @@ __global__ void __launch_bounds__(kThreads) boxes_kernel(const uint16_t *__restr
   }
 }
 
-// Rate-distortion token scores (section 3.4, Eq. rdscore) of one block:
-// s_t = a_t * sum_d fl(fl(v_td - v_hat_td)^2), channel-ascending, no FMA, written as
-// order-preserving 64-bit keys.  grid (nblk, Hkv, B).
-__global__ void __launch_bounds__(kThreads) rd_score_kernel(const uint16_t *__restrict__ v_src,
-                                                            const float *__restrict__ mass, int64_t T,
-                                                            const int8_t *__restrict__ level,
-                                                            const int64_t *__restrict__ voff,
-                                                            const uint8_t *__restrict__ arena, int Hkv,
-                                                            int nblk_cap, uint64_t *__restrict__ keys,
-                                                            int64_t key_stride, int vtok) {
-  extern __shared__ __align__(16) unsigned char smem[];
-  EncodeShared &S = *reinterpret_cast<EncodeShared *>(smem);
+// Rate-distortion token scores (section 3.4, Eq. rdscore):
+// s_t = a_t * sum_d fl(fl(v_td - v_hat_td)^2), channel-ascending, written as
+// order-preserving 64-bit keys.  One wavefront per block, lane = token: the block's
+// value record is staged in the wavefront's LDS (an exact record one half of its
+// channels at a time) and each lane runs its token's fp64 chain.  v_hat = code *
+// scale + zero and v - v_hat are exact in fp64 (all are multiples of 2^-24 below
+// 2^26), so forming v_hat with one fused multiply-add gives the same value as a
+// product and a sum; the square and each addition round once.  grid (nblk, Hkv, B),
+// 64 threads.
+//
+// Staged words: chunk ck (32 codes, 4 tokens x 8 channels) holds `wpc` words; the 16
+// chunks of one four-token group c = ck >> 4 are contiguous and each group starts
+// kRdGroup words after the last, so that the lanes of the 16 groups, which read the
+// same word of their own group, fall in different banks.
+constexpr int kRdGroup = 16 * 8 + 4;
+
+struct RdShared {
+  uint32_t w[16 * kRdGroup];  // staged record words (also the centroids as fp64)
+  double2 sz[D];              // per channel: (scale, zero); the one-centroid value in .x
+};
+
+__device__ __forceinline__ double h2d(uint32_t bits16) {
+  return (double)(float)__builtin_bit_cast(_Float16, (uint16_t)bits16);
+}
+
+// Stage the 256 chunks of a record, wpc words of each (chunk ck's at word
+// ck * src_wpc + src_off of `src`), into the group layout: wpc 16-byte pieces a lane.
+__device__ __forceinline__ void rd_stage(uint32_t *w, const uint8_t *src, int wpc, int src_wpc, int src_off,
+                                         int lane) {
+  const int gw = 16 * wpc;  // words of one group
+  for (int i = 0; i < wpc; ++i) {
+    const int w0 = (i * 64 + lane) * 4;  // staged word index without padding
+    const int ck = w0 / wpc, k = w0 % wpc;
+    const bw4 x = __builtin_nontemporal_load((const bw4 *)(src + ((int64_t)ck * src_wpc + src_off + k) * 4));
+    *(bw4 *)(w + (w0 / gw) * kRdGroup + w0 % gw) = x;
+  }
+}
+
+// This lane's code of channel d = 16 j + m (token t: group c = t >> 2, tq = t & 3):
+// code n = 4 j + tq of chunk 16 c + m, at bit pos[j & 3] = code_pos(BITS, n) of its word.
+template <int BITS>
+__device__ __forceinline__ uint32_t rd_code(const uint32_t *wl, int j, int m, const int (&pos)[4]) {
+  const uint32_t word = wl[m * BITS + 4 * j / (32 / BITS)];
+  return __builtin_amdgcn_ubfe(word, (uint32_t)pos[j & 3], BITS);
+}
+
+// The row as a value of this path only: the conversions of every level's chain are
+// then not merged and hoisted above the level branch (128 fp64 values live at once).
+__device__ __forceinline__ void rd_own(uint32_t (&vr)[64]) {
+#pragma unroll
+  for (int i = 0; i < 64; ++i) asm volatile("" : "+v"(vr[i]));
+}
+
+// e += (v_d - v_hat(d))^2 over the channels, ascending.
+template <class F>
+__device__ __forceinline__ void rd_chain(double &e, uint32_t (&vr)[64], F vhat) {
+  rd_own(vr);
+#pragma unroll
+  for (int d = 0; d < D; ++d) {
+    const double v = h2d(vr[d >> 1] >> (16 * (d & 1)));
+    const double diff = v - vhat(d);
+    const double sq = diff * diff;
+    e = e + sq;
+    // LDS reads are not hoisted past 16 channels (else the unrolled chain spills)
+    if ((d & 15) == 15) asm volatile("" ::: "memory");
+  }
+}
+
+__global__ void __launch_bounds__(64) rd_score_kernel(const uint16_t *__restrict__ v_src,
+                                                      const float *__restrict__ mass, int64_t T,
+                                                      const int8_t *__restrict__ level,
+                                                      const int64_t *__restrict__ voff,
+                                                      const uint8_t *__restrict__ arena, int Hkv, int nblk_cap,
+                                                      uint64_t *__restrict__ keys, int64_t key_stride, int vtok) {
+  __shared__ __align__(16) RdShared S;
   const int blk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int lane = threadIdx.x, c = lane >> 2, tq = lane & 3;
   const int64_t u = (int64_t)b * Hkv + h;
   const int64_t ti = u * nblk_cap + blk;
-  load_record(S, arena + voff[ti], level[ti], GKV_VALUES, vtok != 0);
-  __syncthreads();
-  const int t = threadIdx.x;
-  const int64_t tok = (int64_t)blk * P + t;
-  if (t < P && tok < T) {
-    const uint16_t *row = v_src + (u * T + tok) * D;
-    double e = 0.0;
-    for (int d = 0; d < D; ++d) {
-      const double diff = (double)__builtin_bit_cast(_Float16, row[d]) - getx(S, t, d);
-      const double sq = diff * diff;
-      e = e + sq;
+  const int64_t tok = (int64_t)blk * P + lane;
+  const int64_t tr = tok < T ? tok : T - 1;  // rows past T are read as the last row, not stored
+  const int lv = level[ti];
+  const uint8_t *rec = arena + voff[ti];
+
+  // this token's source row, 16 bytes at a time
+  uint32_t vr[64];
+  const bw4 *row = (const bw4 *)(v_src + (u * T + tr) * D);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const bw4 x = __builtin_nontemporal_load(row + i);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) vr[4 * i + k] = x[k];
+  }
+  const double a = (double)mass[u * T + tr];
+
+  double e = 0.0;
+  const uint32_t *wl = S.w + c * kRdGroup;
+  if (lv == GKV_EXACT) {  // chunk ck: 64 B; channels 16 j + m of token 4 c + tq at half 4 j + tq of chunk 16 c + m
+    rd_own(vr);
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      if (hf) __syncthreads();
+      rd_stage(S.w, rec, 8, 16, 8 * hf, lane);
+      __syncthreads();
+      const uint32_t *wh = wl + (tq >> 1);
+      const int sh = 16 * (tq & 1);
+#pragma unroll
+      for (int d = 64 * hf; d < 64 * hf + 64; ++d) {
+        const int j = (d >> 4) - 4 * hf, m = d & 15;
+        const double v = h2d(vr[d >> 1] >> (16 * (d & 1)));
+        const double diff = v - h2d(wh[m * 8 + 2 * j] >> sh);
+        const double sq = diff * diff;
+        e = e + sq;
+        if ((d & 15) == 15) asm volatile("" ::: "memory");
+      }
     }
-    double sc = (double)mass[u * T + tok] * e;
+  } else if (lv == GKV_MEAN || lv == GKV_CENTROID) {
+    const uint16_t *cc = (const uint16_t *)rec;
+    if (lv == GKV_MEAN) {
+      for (int d = lane; d < D; d += 64) S.sz[d].x = h2d(cc[d]);
+      __syncthreads();
+      rd_chain(e, vr, [&](int d) { return S.sz[d].x; });
+    } else {
+      double *cent = (double *)S.w;  // [KC][D + 1]
+      for (int i = lane; i < KC * D; i += 64) {
+        const int k = i >> 7, d = i & 127;
+        cent[k * (D + 1) + d] = h2d(cc[vcent_index(k, d)]);
+      }
+      const int id = (rec[KC * D * 2 + (lane >> 2)] >> (2 * (lane & 3))) & 3;
+      __syncthreads();
+      const double *ct = cent + id * (D + 1);
+      rd_chain(e, vr, [&](int d) { return ct[d]; });
+    }
+  } else {  // int8 / int4 / int2: (scale, zero) per channel or per token, then the codes
+    const uint16_t *sz = (const uint16_t *)rec;
+    double s = 0.0, z = 0.0;
+    if (vtok) {
+      s = h2d(sz[lane]);
+      z = h2d(sz[P + lane]);
+    } else {
+      for (int e2 = lane; e2 < D; e2 += 64) S.sz[sz_channel(GKV_VALUES, e2)] = make_double2(h2d(sz[e2]), h2d(sz[D + e2]));
+    }
+    int pos[4];  // bit positions of this lane's codes (the same every four channel groups j)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) pos[r] = code_pos(lv, 4 * r + tq);
+    const uint8_t *codes = rec + kSZBytes;
+    if (lv == GKV_INT8) rd_stage(S.w, codes, 8, 8, 0, lane);
+    else if (lv == GKV_INT4) rd_stage(S.w, codes, 4, 4, 0, lane);
+    else rd_stage(S.w, codes, 2, 2, 0, lane);
+    __syncthreads();
+#define GKV_RD_INT(BITS)                                                                                   \
+  if (vtok)                                                                                                \
+    rd_chain(e, vr, [&](int d) { return __builtin_fma((double)rd_code<BITS>(wl, d >> 4, d & 15, pos), s, z); }); \
+  else                                                                                                     \
+    rd_chain(e, vr, [&](int d) {                                                                           \
+      const double2 g = S.sz[d];                                                                           \
+      return __builtin_fma((double)rd_code<BITS>(wl, d >> 4, d & 15, pos), g.x, g.y);                       \
+    })
+    if (lv == GKV_INT8) GKV_RD_INT(8);
+    else if (lv == GKV_INT4) GKV_RD_INT(4);
+    else GKV_RD_INT(2);
+#undef GKV_RD_INT
+  }
+  if (tok < T) {
+    double sc = a * e;
     sc = sc + 0.0;  // -0 -> +0
     uint64_t bits;
     __builtin_memcpy(&bits, &sc, 8);
@@ -598,7 +735,7 @@ __global__ void __launch_bounds__(kThreads) rd_score_kernel(const uint16_t *__re
 void gkv_launch_rd_score(const gkv_cache *c, const uint16_t *v_src, const float *mass, uint64_t *keys,
                          int64_t key_stride, hipStream_t stream) {
   const int nblk = (int)((c->T + P - 1) / P);
-  hipLaunchKernelGGL(rd_score_kernel, dim3(nblk, c->Hkv, c->B), dim3(kThreads), sizeof(EncodeShared), stream, v_src,
+  hipLaunchKernelGGL(rd_score_kernel, dim3(nblk, c->Hkv, c->B), dim3(64), 0, stream, v_src,
                      mass, c->T, c->level, c->voff, c->arena, c->Hkv, c->nblk_cap, keys, key_stride, c->v_per_token);
 }
 

@@ -22,6 +22,24 @@ def _build(gpu, ks, vs, Hq, levels, **kw):
     return gpu.GradedCache.build(ks, vs, Hq=Hq, levels=levels, device="cuda", **kw)
 
 
+def _order_keys(s):
+    """Order-preserving 64-bit keys of fp64 scores (a +0 for -0), as the selection ranks them."""
+    b = (np.asarray(s, dtype=np.float64) + 0.0).view(np.uint64)
+    neg = (b >> np.uint64(63)) != 0
+    return np.where(neg, ~b, b | np.uint64(1 << 63))
+
+
+def check_rd_keys(cache, b, h, T, want_scores):
+    """The residual selection ranks the tokens of (b, h) by keys it leaves at the head of
+    its workspace, [B][Hkv][nblk_cap * 64] (tokens below T); they must be the oracle's
+    fp64 scores bit for bit, not only select the same rows."""
+    ws = cache.workspace(2)
+    stride = cache.nblk_cap * 64
+    keys = ws[: cache.B * cache.Hkv * stride * 8].view(_torch().int64).view(cache.B, cache.Hkv, stride)
+    got = keys[b, h, :T].cpu().numpy().view(np.uint64)
+    np.testing.assert_array_equal(got, _order_keys(want_scores))
+
+
 @pytest.mark.parametrize("T", [2048, 1000])
 def test_tiny_graded_codes_and_attention(gpu, T):
     """Workload 1 shapes (8 query / 2 KV heads, tiny ladder); T = 1000 leaves a
@@ -183,8 +201,9 @@ def test_rd_residual_selection_and_attention(gpu, T, Bn):
     for b in range(Bn):
         for h in range(Hkv):
             uc = ocache.UnitCache(ks[b, h], vs[b, h], lv)
-            want, _ = uc.select_residual(ks[b, h], vs[b, h], mass[b, h], n)
+            want, sc = uc.select_residual(ks[b, h], vs[b, h], mass[b, h], n)
             np.testing.assert_array_equal(idx[b, h, :n], want)
+            check_rd_keys(cache, b, h, T, sc)
             bits = np.zeros(len(lv), dtype=np.uint64)
             for t in want:
                 bits[t // 64] |= np.uint64(1) << np.uint64(t % 64)
@@ -394,8 +413,9 @@ def test_rd_residual_streamed_selection(gpu):
     mass = synth.mass_unit(4, 0, 0, T)[None, None]
     cache.rd_residual_select(ks, vs, mass, n)
     uc = ocache.UnitCache(ks[0, 0], vs[0, 0], lv)
-    want, _ = uc.select_residual(ks[0, 0], vs[0, 0], mass[0, 0], n)
+    want, sc = uc.select_residual(ks[0, 0], vs[0, 0], mass[0, 0], n)
     np.testing.assert_array_equal(cache.res_idx.cpu().numpy()[0, 0, :n], want)
+    check_rd_keys(cache, 0, 0, T, sc)
     q = synth.queries(4, 1, Hq)
     out = cache.decode(q).cpu().numpy()
     assert max_err(out[0], uc.decode_dense(q_group(q, 0, 0, Hq))) <= TOL
@@ -575,8 +595,9 @@ def test_rdv2_codes_residual_attention_and_bound(gpu, T, Bn):
             for blk in (0, 1, len(lv) // 2, len(lv) - 17, len(lv) - 16, len(lv) - 1):
                 compare_record(cache, uc, b, h, blk, 0)
                 compare_record(cache, uc, b, h, blk, 1)
-            want, _ = uc.select_residual(ks[b, h], vs[b, h], mass[b, h], n)
+            want, sc = uc.select_residual(ks[b, h], vs[b, h], mass[b, h], n)
             np.testing.assert_array_equal(idx[b, h, :n], want)
+            check_rd_keys(cache, b, h, T, sc)
             ref = uc.decode_dense(q_group(q, b, h, G))
             assert max_err(out[b, h * G:(h + 1) * G], ref) <= TOL
             _cert_compare(cache, uc, b, h)
@@ -689,8 +710,9 @@ def test_rd128k_full_size_sampled(gpu, prof, frac, vtok):
         for blk in (0, 1, 700, 1500, len(lv) - 17, len(lv) - 1):
             compare_record(cache, uc, b, h, blk, 0)
             compare_record(cache, uc, b, h, blk, 1)
-        want, _ = uc.select_residual(ks[b, h], vs[b, h], mass[b, h], n)
+        want, sc = uc.select_residual(ks[b, h], vs[b, h], mass[b, h], n)
         np.testing.assert_array_equal(idx[b, h, :n], want)
+        check_rd_keys(cache, b, h, T, sc)
         assert max_err(out[b, h * G:(h + 1) * G], uc.decode_dense(q_group(q, b, h, G))) <= TOL
 
 
@@ -753,8 +775,9 @@ def test_per_token_values_demotion_and_residual(gpu):
             idx = cache.res_idx.cpu().numpy()
             for (b, h), uc in ucs.items():
                 import copy
-                want, _ = copy.deepcopy(uc).select_residual(ks[b, h], vs[b, h], mass[b, h], n)
+                want, sc = copy.deepcopy(uc).select_residual(ks[b, h], vs[b, h], mass[b, h], n)
                 np.testing.assert_array_equal(idx[b, h, :n], want)
+                check_rd_keys(cache, b, h, T, sc)
     q = synth.queries(11, 1, Hq)
     mass = np.stack([synth.mass_unit(11, 0, h, T) for h in range(Hkv)])[None]
     out = cache.decode(q).cpu().numpy()
