@@ -374,7 +374,8 @@ gkv_status gkv_admit_sequence(gkv_cache *c, int32_t b, void *stream);
  * with v_hat its value at its block's level, keep the first nkeep of the order
  * (score desc, token asc) per (b,h), and store their exact K and V rows, ascending
  * indices and per-block override masks in the cache.  k_src, v_src:
- * [B][Hkv][T][128] fp16; mass: [B][Hkv][T] fp32.  Sets c->nres = nkeep.
+ * [B][Hkv][T][128] fp16, 16-byte aligned (rows are read 16 bytes at a time;
+ * GKV_E_ARG otherwise); mass: [B][Hkv][T] fp32.  Sets c->nres = nkeep.
  * GKV_E_UNSUPPORTED with per-sequence lengths (the selection runs at prefill, on a
  * batch of one length). */
 gkv_status gkv_rd_residual_select(gkv_cache *c, const uint16_t *k_src, const uint16_t *v_src,

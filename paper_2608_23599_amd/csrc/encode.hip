@@ -604,24 +604,17 @@ __device__ __forceinline__ uint32_t rd_code(const uint32_t *wl, int j, int m, co
   return __builtin_amdgcn_ubfe(word, (uint32_t)pos[j & 3], BITS);
 }
 
-// The row as a value of this path only: the conversions of every level's chain are
-// then not merged and hoisted above the level branch (128 fp64 values live at once).
-__device__ __forceinline__ void rd_own(uint32_t (&vr)[64]) {
-#pragma unroll
-  for (int i = 0; i < 64; ++i) asm volatile("" : "+v"(vr[i]));
-}
-
 // e += (v_d - v_hat(d))^2 over the channels, ascending.
 template <class F>
-__device__ __forceinline__ void rd_chain(double &e, uint32_t (&vr)[64], F vhat) {
-  rd_own(vr);
+__device__ __forceinline__ void rd_chain(double &e, const uint32_t (&vr)[64], F vhat) {
 #pragma unroll
   for (int d = 0; d < D; ++d) {
     const double v = h2d(vr[d >> 1] >> (16 * (d & 1)));
     const double diff = v - vhat(d);
     const double sq = diff * diff;
     e = e + sq;
-    // LDS reads are not hoisted past 16 channels (else the unrolled chain spills)
+    // LDS reads are not hoisted past 16 channels (else the unrolled chain keeps the
+    // reads of many more channels in registers)
     if ((d & 15) == 15) asm volatile("" ::: "memory");
   }
 }
@@ -642,12 +635,13 @@ __global__ void __launch_bounds__(64) rd_score_kernel(const uint16_t *__restrict
   const int lv = level[ti];
   const uint8_t *rec = arena + voff[ti];
 
-  // this token's source row, 16 bytes at a time
+  // this token's source row, 16 bytes at a time (cached loads: the eight loads of
+  // one 128-byte line by the same lane find it in the cache)
   uint32_t vr[64];
   const bw4 *row = (const bw4 *)(v_src + (u * T + tr) * D);
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
-    const bw4 x = __builtin_nontemporal_load(row + i);
+    const bw4 x = row[i];
 #pragma unroll
     for (int k = 0; k < 4; ++k) vr[4 * i + k] = x[k];
   }
@@ -656,7 +650,6 @@ __global__ void __launch_bounds__(64) rd_score_kernel(const uint16_t *__restrict
   double e = 0.0;
   const uint32_t *wl = S.w + c * kRdGroup;
   if (lv == GKV_EXACT) {  // chunk ck: 64 B; channels 16 j + m of token 4 c + tq at half 4 j + tq of chunk 16 c + m
-    rd_own(vr);
 #pragma unroll
     for (int hf = 0; hf < 2; ++hf) {
       if (hf) __syncthreads();

@@ -555,34 +555,49 @@ void launch_select(const uint64_t *keys, int64_t key_stride, int64_t n, int k, i
 }
 
 // Copy the exact key/value rows of the selected residual tokens into exact-format
-// pseudo-blocks.  grid (ceil(nkeep/64), Hkv, B), 256 threads.
+// pseudo-blocks.  grid (ceil(nkeep/64), Hkv, B), 256 threads.  Rows are read 16 bytes
+// (8 channels) at a time; a key record takes 8 consecutive channels of a row as one
+// 16-byte piece of a chunk, so keys are written straight from the loads; a value chunk
+// holds 4 rows x 8 channels 16 apart, so the value rows are staged in LDS and every
+// thread writes one whole 64-byte chunk.
 __global__ void __launch_bounds__(256) res_gather_kernel(const uint16_t *__restrict__ k_src,
                                                          const uint16_t *__restrict__ v_src, int64_t T,
                                                          const int32_t *__restrict__ res_idx, int nres_cap,
                                                          int nkeep, uint8_t *res_rows, int Hkv) {
+  constexpr int kRow = D + 8;  // padded LDS row (halves)
+  __shared__ __align__(16) uint16_t sv[P * kRow];
   const int rb = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int64_t u = (int64_t)b * Hkv + h;
   const int nrb = (nres_cap + P - 1) / P;
   uint16_t *kr = (uint16_t *)(res_rows + (u * nrb + rb) * (2 * kExactBytes));
   uint16_t *vr = kr + kExactBytes / 2;
-  for (int i = threadIdx.x; i < P * D; i += 256) {
-    const int slot = i >> 7, d = i & 127;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int pc = threadIdx.x + 256 * k, slot = pc >> 4, a = pc & 15;  // channels 8a .. 8a+7 of row slot
     const int r = rb * P + slot;
-    uint16_t kv = 0, vv = 0;
+    uint4 kv = make_uint4(0, 0, 0, 0), vv = kv;
     if (r < nkeep) {
-      const int64_t tok = res_idx[u * nres_cap + r];
-      kv = k_src[(u * T + tok) * D + d];
-      vv = v_src[(u * T + tok) * D + d];
+      const int64_t row = (u * T + res_idx[u * nres_cap + r]) * D + 8 * a;
+      kv = *(const uint4 *)(k_src + row);
+      vv = *(const uint4 *)(v_src + row);
     }
-    {  // key element (slot, d)
-      const int pg = slot >> 4, lane = ((d >> 3) & 3) * 16 + (slot & 15), n = ((d >> 5) << 3) | (d & 7);
-      kr[(pg * 64 + lane) * 32 + n] = kv;
-    }
-    {  // value element (slot, d)
-      const int pg = slot >> 4, lane = ((slot >> 2) & 3) * 16 + (d & 15), n = ((d >> 4) << 2) | (slot & 3);
-      vr[(pg * 64 + lane) * 32 + n] = vv;
-    }
+    // key chunk (page slot >> 4, lane (a & 3) * 16 + (slot & 15)), codes 8 (a >> 2) ..
+    const int lane = (a & 3) * 16 + (slot & 15);
+    *(uint4 *)(kr + ((slot >> 4) * 64 + lane) * 32 + 8 * (a >> 2)) = kv;
+    *(uint4 *)(sv + slot * kRow + 8 * a) = vv;
   }
+  __syncthreads();
+  // value chunk ck = (page, lane kg * 16 + m): element n is row 16 page + 4 kg + (n & 3),
+  // channel 16 (n >> 2) + m
+  const int ck = threadIdx.x, pg = ck >> 6, kg = (ck >> 4) & 3, m = ck & 15;
+  const uint16_t *s0 = sv + (16 * pg + 4 * kg) * kRow + m;
+  uint32_t w[16];
+#pragma unroll
+  for (int n = 0; n < 32; n += 2)
+    w[n >> 1] = (uint32_t)s0[(n & 3) * kRow + 16 * (n >> 2)] | ((uint32_t)s0[((n + 1) & 3) * kRow + 16 * ((n + 1) >> 2)] << 16);
+  uint4 *o = (uint4 *)(vr + ck * 32);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) o[q] = make_uint4(w[4 * q], w[4 * q + 1], w[4 * q + 2], w[4 * q + 3]);
 }
 
 // Residual rows before every block (res_off[blk] = sum over blocks < blk of the
@@ -691,6 +706,7 @@ extern "C" gkv_status gkv_rd_residual_select(gkv_cache *c, const uint16_t *k_src
   gkv_status st = gkv_validate_cache(c);
   if (st) return st;
   if (!k_src || !v_src || !mass || !ws || nkeep < 0) return GKV_E_ARG;
+  if (((uintptr_t)k_src | (uintptr_t)v_src) & 15) return GKV_E_ARG;  // 16-byte row loads
   if (c->seq_len_host) return GKV_E_UNSUPPORTED;  // prefill-time selection on one length
   if (c->T <= 0) return GKV_E_SHAPE;
   if (nkeep > c->nres_cap || nkeep > c->T) return GKV_E_SHAPE;
