@@ -143,10 +143,12 @@ typedef struct gkv_cache {
   int32_t v_per_token;       /* 1: the values' int levels are grouped per token (see
                                 the record layout); 0: per channel, like the keys     */
   uint64_t version;          /* stamp of the block tables' state: every call that
-                                changes level / koff / voff / res_mask / nres / T sets
-                                a new process-wide unique value; a caller that writes
-                                those tables itself calls gkv_cache_changed.  0 =
-                                unknown (dense attention plans are then never reused) */
+                                changes level / koff / voff / res_mask / nres or a
+                                sequence's block count (gkv_append only when it opens
+                                a block) sets a new process-wide unique value; a caller
+                                that writes those tables itself calls
+                                gkv_cache_changed.  0 = unknown (dense attention plans
+                                are then never reused)                                  */
   int64_t *seq_len;          /* device [B] or NULL: sequences of different lengths (the
                                 block manager of a serving batch).  seq_len[b] tokens
                                 of sequence b are present (0 <= seq_len[b] <= T, and
@@ -158,9 +160,10 @@ typedef struct gkv_cache {
 } gkv_cache;
 
 /* Stamps c->version with a new process-wide unique value: a caller that has written
- * the block tables (level, koff, voff, res_mask) or changed T or nres itself calls
- * this before the next attention call, so that a dense plan kept in a workspace for
- * the old tables is not reused.  The library's own calls stamp the cache themselves. */
+ * the block tables (level, koff, voff, res_mask) or changed nres or a sequence's block
+ * count itself calls this before the next attention call, so that a dense plan kept
+ * in a workspace for the old tables is not reused.  The library's own calls stamp the
+ * cache themselves. */
 void gkv_cache_changed(gkv_cache *c);
 
 /* ---------------------------------------------------------------- host helpers */
@@ -259,7 +262,8 @@ gkv_status gkv_quantize_block(const gkv_cache *c, int32_t which, const uint16_t 
  * decode) to to_level_host[i], writing the new K and V records at new_koff_host[i]
  * / new_voff_host[i] and updating the device and host level / offset tables.
  * Every job must lower the level (GKV_E_NOT_MONOTONE otherwise; nothing is
- * enqueued then).  The old slots are free once the stream has passed this call. */
+ * enqueued then).  A block its sequence does not fill stays exact (GKV_E_SHAPE).
+ * The old slots are free once the stream has passed this call. */
 gkv_status gkv_demote(gkv_cache *c, int32_t n, const int32_t *jobs_host, const int8_t *to_level_host,
                       const int64_t *new_koff_host, const int64_t *new_voff_host, void *stream);
 
@@ -308,12 +312,15 @@ gkv_status gkv_quest_select(const uint16_t *q, const gkv_cache *c, int32_t topk,
 gkv_status gkv_graded_decode_attn(const uint16_t *q, const gkv_cache *c, const int32_t *pages, int32_t topk,
                                   float *out, void *ws, int64_t ws_bytes, void *stream);
 /* Plan reuse.  The visit plan of a dense read depends only on the block tables, not
- * on the query.  A dense call whose cache has a nonzero version leaves a tag of the
- * planned state (version, T, nres, table addresses, split) in the workspace; the plan
- * kernel of a later dense call with the same workspace and an identical tag exits at
- * once and the attention reuses the plan.  The check runs on the device, so a captured
- * graph replays it correctly.  Compressed-Quest calls always plan (their pages change
- * with every query) and invalidate the tag. */
+ * on the query, and covers each sequence's blocks whole: the attention masks the
+ * tokens of a sequence's last (exact) block past its length at run time, so appends
+ * that open no block keep the plan.  A dense call whose cache has a nonzero version
+ * leaves a tag of the planned state (version, block count, nres, table addresses,
+ * split) in the workspace; the plan kernel of a later dense call with the same
+ * workspace and an identical tag exits at once and the attention reuses the plan.
+ * The check runs on the device, so a captured graph replays it correctly.
+ * Compressed-Quest calls always plan (their pages change with every query) and
+ * invalidate the tag. */
 
 /* gkv_graded_decode_attn for callers that cannot allocate or pass a workspace (code
  * under HIP graph capture, tight serving loops, harnesses that forbid allocation):

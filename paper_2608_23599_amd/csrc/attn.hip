@@ -233,6 +233,21 @@ struct AttnParams {
   uint64_t key[kTagWords];
 };
 
+// Tokens of (b, KV head) u: its sequence's length, 0 for a retired sequence.
+__device__ __forceinline__ int64_t unit_T(const AttnParams &p, int64_t u) {
+  if (!p.seq_len) return p.T;
+  const int64_t t = p.seq_len[u / p.Hkv];
+  return t > 0 ? t : 0;
+}
+
+// Tokens a dense plan covers in u: its length rounded up to whole blocks.  A sequence's
+// last block is always exact (a partial block is never demoted), and the attention
+// kernel masks that block's tokens past the length at run time, so one plan serves
+// every length inside the block (appends that open no block keep the plan).
+__device__ __forceinline__ int64_t plan_T(const AttnParams &p, int64_t u) {
+  return (unit_T(p, u) + P - 1) / P * P;
+}
+
 constexpr int kSlotBytes = 4096;  // one copy unit
 constexpr int kSlots = 4;         // ring slots per wavefront
 constexpr int kRing = kSlots * kSlotBytes;
@@ -381,6 +396,7 @@ struct Pipe {
   uint8_t *ebuf;    // value scale/zero of the current int block (LDS, 512 B)
   int lane;
   uint32_t blk;        // block index of the current item (0xFFFF: no block record)
+  int64_t tlim;        // tokens of this (b, KV head): exact tiles of a dense plan are masked there
   const float *cert;   // this (b, KV head)'s certificate rows, or null
 
   __device__ __forceinline__ void fetch(const uint8_t *src, uint32_t lds, uint32_t c) {
@@ -431,7 +447,7 @@ struct Pipe {
     const uint4 d = *(const uint4 *)(ichunk + ((ik / kChunk) & 1) * 512 + r * sizeof(ItemDesc));
     meta = (uint32_t)uni((int32_t)d.x);
     valid = (uint64_t)uni64((int64_t)(((uint64_t)d.w << 32) | d.z));
-    if (CERT) blk = (uint32_t)uni((int32_t)d.y);
+    blk = (uint32_t)uni((int32_t)d.y);
     ++ik;
     return true;
   }
@@ -997,7 +1013,12 @@ template <bool PACK, bool CERT>
 __device__ __forceinline__ bool exact_run(const AttnParams &p, State &st, const uint8_t *qs, Pipe &pp,
                                           uint32_t &meta, uint64_t &valid, int lane) {
   do {
-    exact_tile<PACK, CERT>(p, st, qs, pp, meta_tvalid(meta), lane);
+    uint32_t tv = meta_tvalid(meta);
+    if (pp.blk != 0xFFFFu) {  // a block's tile: its tokens at or past the length are not read
+      const int64_t left = pp.tlim - (int64_t)pp.blk * P - 16 * __builtin_ctz(meta_tiles(meta));
+      tv &= left >= 16 ? 0xFFFFu : (left <= 0 ? 0u : (1u << left) - 1u);
+    }
+    exact_tile<PACK, CERT>(p, st, qs, pp, tv, lane);
     if (!pp.template next_item<CERT>(meta, valid)) return false;
   } while (meta_lv(meta) == GKV_EXACT);
   return true;
@@ -1200,6 +1221,7 @@ __global__ void __launch_bounds__(kThreads, 2) attn_kernel(AttnParams p) {
   pp.ilds = (uint32_t)uni((int32_t)(uintptr_t)pp.ichunk);
   pp.cert = CERT ? p.cert + u * p.nblk_cap * 4 : nullptr;
   pp.blk = 0xFFFFu;
+  pp.tlim = uni64(unit_T(p, u));
   if (QUEST) {
     // Compressed-Quest: this wavefront's share of the read pages, listed in LDS here
     const uint2 n = quest_lists(p, u, w, W, lane, (ItemDesc *)pp.ichunk, (UnitDesc *)pp.uchunk);
@@ -1411,13 +1433,6 @@ __device__ __forceinline__ uint32_t balance_cost(int lv, uint64_t va) {
 
 __device__ __forceinline__ uint64_t token_mask(int64_t left) {  // tokens of a block below `left`
   return left >= P ? ~0ull : (left <= 0 ? 0ull : ((1ull << left) - 1));
-}
-
-// Tokens of (b, KV head) u: its sequence's length, 0 for a retired sequence.
-__device__ __forceinline__ int64_t unit_T(const AttnParams &p, int64_t u) {
-  if (!p.seq_len) return p.T;
-  const int64_t t = p.seq_len[u / p.Hkv];
-  return t > 0 ? t : 0;
 }
 
 // Wavefront inclusive scan of a 32-bit value in lane order: DPP row shifts within
@@ -1704,7 +1719,7 @@ __device__ __forceinline__ uint2 quest_lists(const AttnParams &p, int64_t u, int
 
 // Tokens read from block b of a dense read (residual rows excluded).
 __device__ __forceinline__ uint64_t dense_tokens(const AttnParams &p, int64_t u, int64_t b) {
-  uint64_t va = token_mask(unit_T(p, u) - b * P);
+  uint64_t va = token_mask(plan_T(p, u) - b * P);
   if (p.nres) va &= ~p.res_mask[u * p.nblk_cap + b];
   return va;
 }
@@ -1749,7 +1764,7 @@ __device__ __forceinline__ VisitDesc dense_visit(const AttnParams &p, int64_t u,
     d.blk = (uint16_t)v;
     d.kp = (uint64_t)(uintptr_t)(p.arena + p.koff[u * p.nblk_cap + v]);
     d.vp = (uint64_t)(uintptr_t)(p.arena + p.voff[u * p.nblk_cap + v]);
-    d.valid = token_mask(unit_T(p, u) - v * P);
+    d.valid = token_mask(plan_T(p, u) - v * P);
     if (p.nres) d.valid &= ~p.res_mask[u * p.nblk_cap + v];
     if (jn && d.level == GKV_MEAN && d.valid) mean_run_visit(p, u, v, jn, d);
   } else {
@@ -2082,10 +2097,10 @@ static gkv_status attn_setup(const uint16_t *q, const gkv_cache *c, const int32_
   p.fast = attn_fast(p.nsplit, (int64_t)c->B * c->Hkv);
   p.sl2 = 1.4426950408889634f / sqrtf((float)D);
   // the key of the planned state: a dense plan depends on the tables (version stamp
-  // and addresses), T, the residual count and the split
+  // and addresses), the block count, the residual count and the split
   p.cacheable = !pages && c->version != 0;
   const uint64_t key[kTagWords] = {c->version,
-                                   (uint64_t)c->T,
+                                   (uint64_t)((c->T + P - 1) / P),
                                    (uint64_t)(uint32_t)c->nres | ((uint64_t)(uint32_t)p.nsplit << 32),
                                    (uint64_t)(uint32_t)p.fast | ((uint64_t)(uint32_t)c->nblk_cap << 32),
                                    (uint64_t)(uintptr_t)c->level,

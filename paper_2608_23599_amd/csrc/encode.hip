@@ -785,7 +785,7 @@ extern "C" gkv_status gkv_demote(gkv_cache *c, int32_t n, const int32_t *jobs, c
     const int cur = c->level_host[((int64_t)b * c->Hkv + h) * c->nblk_cap + blk];
     if (level_rank(to[i]) < 0) return GKV_E_ARG;
     if (level_rank(to[i]) >= level_rank(cur)) return GKV_E_NOT_MONOTONE;
-    if ((int64_t)(blk + 1) * P > c->T) return GKV_E_SHAPE;  // a partial block stays exact
+    if ((int64_t)(blk + 1) * P > seq_tokens(c, b)) return GKV_E_SHAPE;  // a partial block stays exact
     const int64_t bb = block_bytes(to[i]);
     if (nk[i] < 0 || nv[i] < 0 || nk[i] + bb > c->arena_bytes || nv[i] + bb > c->arena_bytes) return GKV_E_ARG;
     for (int j = 0; j < i; ++j)
@@ -861,7 +861,6 @@ extern "C" gkv_status gkv_append(gkv_cache *c, const uint16_t *k_new, const uint
       }
     }
   }
-  (void)any_open;
   hipLaunchKernelGGL(append_kernel, dim3(c->Hkv, c->B), dim3(128), 0, (hipStream_t)stream, k_new, v_new, c->level,
                      c->koff, c->voff, c->arena, c->page ? c->boxes : nullptr, c->npage_cap, c->page ? c->page : 1,
                      c->Hkv, c->nblk_cap, c->T, c->seq_len, slots, c->cert);
@@ -876,6 +875,8 @@ extern "C" gkv_status gkv_append(gkv_cache *c, const uint16_t *k_new, const uint
     mx = T + 1 > mx ? T + 1 : mx;
   }
   c->T = c->seq_len_host ? mx : c->T + 1;
-  gkv_stamp(c);
+  // the tables change only when a block opens; a dense plan covers whole blocks, and
+  // the attention masks a block's tokens past the length at run time
+  if (any_open) gkv_stamp(c);
   return GKV_OK;
 }

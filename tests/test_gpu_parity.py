@@ -259,6 +259,47 @@ def test_demote_chain_bit_exact(gpu):
         assert max_err(out[b, 2 * h:2 * h + 2], uc.decode_dense(q_group(q, b, h, 2))) <= TOL
 
 
+def test_dense_plan_kept_through_appends_inside_a_block(gpu):
+    """An append that opens no block (and demotes nothing) leaves the block tables and
+    the version as they were, so a dense read keeps the plan in its workspace: the plan
+    covers the last block whole and the attention masks its tokens past the length.
+    Every step the kept-plan output equals, bit for bit, the output of a call with a
+    fresh workspace (which plans anew) and matches the oracle within tolerance."""
+    Hq, Hkv = 8, 2
+    T0 = 64 * 40 - 3
+    steps = 12  # step 3 opens block 40
+    ks, vs = kv_all(6, 1, Hkv, T0 + steps)
+    lv = olad.ladder("graded", T0)
+    cache = _build(gpu, ks[:, :, :T0], vs[:, :, :T0], Hq, lv, extra_blocks=2,
+                   slack={16: 8, 8: 8, 4: 8, 2: 8, 1: 8})
+    ucs = {h: ocache.UnitCache(ks[0, h, :T0], vs[0, h, :T0], lv) for h in range(Hkv)}
+    G = Hq // Hkv
+    kept = 0
+    for s in range(steps):
+        t = T0 + s
+        v0 = int(cache.c.version)
+        moves = cache.append(ks[:, :, t], vs[:, :, t], profile="graded")
+        for h in range(Hkv):
+            ucs[h].append(ks[0, h, t], vs[0, h, t], "graded")
+        if t % 64 or moves:
+            assert (int(cache.c.version) != v0) == bool(moves)
+        else:
+            assert int(cache.c.version) != v0
+        kept += int(cache.c.version) == v0
+        q = synth.queries(6, 1, Hq, step=s)
+        out = cache.decode(q)
+        ws = cache._ws[(1, 0)]
+        cache._ws[(1, 0)] = _torch().zeros_like(ws)
+        fresh = cache.decode(q)
+        cache._ws[(1, 0)] = ws
+        assert _torch().equal(out, fresh)
+        out = out.cpu().numpy()
+        for h in range(Hkv):
+            ref = ucs[h].decode_dense(q_group(q, 0, h, G))
+            assert max_err(out[0, h * G:(h + 1) * G], ref) <= TOL
+    assert kept >= steps - 3
+
+
 def test_append_demote_boxes_and_quest_steps(gpu):
     """Workload 5 step at a small length: every step appends one token per KV head
     (boxes of completed pages, new exact block every 64 tokens), demotes the blocks
