@@ -1411,8 +1411,8 @@ static_assert(sizeof(VisitDesc) == 32, "descriptor size");
 // its SIMD (about 8 cycles per unit).  Exact tiles are bound by the wavefront's
 // share of the bandwidth (8 KB each), int tiles by the dequantisation and softmax
 // work rather than by their bytes.
-constexpr uint32_t kCostExactTile = 523, kCostInt8Tile = 426, kCostInt4Tile = 305, kCostInt2Tile = 260,
-                   kCostCentroid = 711, kCostIntBlock = 248, kCostMean = 300, kCostMeanRun = 260,
+constexpr uint32_t kCostExactTile = 523, kCostInt8Tile = 426, kCostInt4Tile = 314, kCostInt2Tile = 295,
+                   kCostCentroid = 768, kCostIntBlock = 248, kCostMean = 300, kCostMeanRun = 260,
                    kCostMeanRunBlock = 45;
 
 // Blocks in a one-centroid run (1 for every other visit) and the visit's level.
@@ -1755,18 +1755,38 @@ __device__ __forceinline__ void mean_run_visit(const AttnParams &p, int64_t u, i
   d.level = (int16_t)(GKV_MEAN | ((n - 1) << 8));
 }
 
-// Visit v of a dense read: block v (v < nblk), else residual pseudo-block v - nblk.
+// Position, in a range of n blocks, of visit v.  The aligned groups of 8 blocks are
+// visited from the four quarters of the range in turn (a transpose of the first
+// 4 * (n / 32) groups; the blocks after them keep their places), so that every
+// wavefront's contiguous share holds blocks of the whole ladder: the old centroid and
+// int2 blocks, whose dequantisation keeps the VALU busy, beside int8 and exact blocks,
+// bound by their bytes.  The two wavefronts that share a SIMD then carry like mixes;
+// with shares of one level each, an int4 wavefront beside an int2 one ended 13 us after
+// the same int4 share beside a centroid one.  A group's blocks keep their order, so
+// one-centroid runs stay whole.
+__device__ __forceinline__ int64_t visit_block(int64_t v, int64_t n) {
+  const int64_t q = n / 32;  // groups per quarter
+  if (v >= 32 * q) return v;
+  const int64_t g = v >> 3;
+  return (((g & 3) * q + (g >> 2)) << 3) | (v & 7);
+}
+
+// Visit v of a dense read.  The blocks 0..nblk-1 and after them the residual
+// pseudo-blocks form one range, visited in the order of visit_block, so that the
+// residual's exact tiles spread over the last wavefronts' shares too.
 __device__ __forceinline__ VisitDesc dense_visit(const AttnParams &p, int64_t u, int64_t nblk, int64_t v,
                                                  const uint32_t *jn) {
   VisitDesc d;
+  v = visit_block(v, nblk + (p.nres + P - 1) / P);
   if (v < nblk) {
-    d.level = p.level[u * p.nblk_cap + v];
-    d.blk = (uint16_t)v;
-    d.kp = (uint64_t)(uintptr_t)(p.arena + p.koff[u * p.nblk_cap + v]);
-    d.vp = (uint64_t)(uintptr_t)(p.arena + p.voff[u * p.nblk_cap + v]);
-    d.valid = token_mask(plan_T(p, u) - v * P);
-    if (p.nres) d.valid &= ~p.res_mask[u * p.nblk_cap + v];
-    if (jn && d.level == GKV_MEAN && d.valid) mean_run_visit(p, u, v, jn, d);
+    const int64_t b = v;
+    d.level = p.level[u * p.nblk_cap + b];
+    d.blk = (uint16_t)b;
+    d.kp = (uint64_t)(uintptr_t)(p.arena + p.koff[u * p.nblk_cap + b]);
+    d.vp = (uint64_t)(uintptr_t)(p.arena + p.voff[u * p.nblk_cap + b]);
+    d.valid = token_mask(plan_T(p, u) - b * P);
+    if (p.nres) d.valid &= ~p.res_mask[u * p.nblk_cap + b];
+    if (jn && d.level == GKV_MEAN && d.valid) mean_run_visit(p, u, b, jn, d);
   } else {
     const int64_t rb = v - nblk;
     const uint8_t *kp = p.res_rows + (u * p.nrb_cap + rb) * (2 * kExactBytes);
@@ -1785,10 +1805,10 @@ __device__ __forceinline__ VisitDesc dense_visit(const AttnParams &p, int64_t u,
 // keeps the owners non-decreasing along the visits).
 // The first W1 wavefronts (those of the workgroups dispatched first, which win the
 // issue arbitration against the later ones on their SIMDs) get kFastCap capacity
-// units, the others kSlowCap (measured: 1.28 times the work in the same time).
+// units, the others kSlowCap (measured: 1.33 times the work in the same time).
 // The position is scaled by cap / (2 total), taken once per plan (a product with a
 // positive constant is monotone, so the owners stay non-decreasing).
-constexpr double kFastCap = 23.0, kSlowCap = 18.0;
+constexpr double kFastCap = 23.0, kSlowCap = 17.25;
 __device__ __forceinline__ double owner_scale(int W, int W1, uint64_t total) {
   return total ? (kFastCap * W1 + kSlowCap * (W - W1)) / (2.0 * (double)total) : 0.0;
 }
@@ -1886,7 +1906,7 @@ __device__ __forceinline__ void plan_dense_regs(const AttnParams &p, int64_t u, 
 #pragma unroll
     for (int j = 0; j < kPlanRegs; ++j)
       if (v0 + j < v1 && v0 + j < nblk && dv[j].level == GKV_MEAN && dv[j].valid) {
-        mean_run_visit(p, u, v0 + j, jn, dv[j]);
+        mean_run_visit(p, u, dv[j].blk, jn, dv[j]);
         dv[j].cost = balance_cost(dv[j].level, dv[j].valid) | (visit_counts(dv[j].level, dv[j].valid) << 24);
       }
   }
