@@ -1899,13 +1899,13 @@ __device__ __forceinline__ void plan_dense_regs(const AttnParams &p, int64_t u, 
   for (int j = 0; j < kPlanRegs; ++j)
     if (v0 + j < v1) {
       dv[j] = dense_visit(p, u, nblk, v0 + j, nullptr);
-      any_mean |= v0 + j < nblk && dv[j].level == GKV_MEAN;
+      any_mean |= dv[j].blk != 0xFFFFu && dv[j].level == GKV_MEAN;  // a block, not residual rows
     }
   // one-centroid runs, only when the cache holds one-centroid blocks
   if (const uint32_t *jn = build_joins(p, u, nblk, v0, v1, __syncthreads_or(any_mean), joins)) {
 #pragma unroll
     for (int j = 0; j < kPlanRegs; ++j)
-      if (v0 + j < v1 && v0 + j < nblk && dv[j].level == GKV_MEAN && dv[j].valid) {
+      if (v0 + j < v1 && dv[j].blk != 0xFFFFu && dv[j].level == GKV_MEAN && dv[j].valid) {
         mean_run_visit(p, u, dv[j].blk, jn, dv[j]);
         dv[j].cost = balance_cost(dv[j].level, dv[j].valid) | (visit_counts(dv[j].level, dv[j].valid) << 24);
       }

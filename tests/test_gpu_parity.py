@@ -610,12 +610,14 @@ def test_certificate_through_appends_and_demotions(gpu):
 # ---------------------------------------------------------------- one-centroid state, RD-V2
 
 
-@pytest.mark.parametrize("T,Bn", [(8192, 2), (3001, 1)])
+@pytest.mark.parametrize("T,Bn", [(8192, 2), (3001, 1), (7464, 1)])
 def test_rdv2_codes_residual_attention_and_bound(gpu, T, Bn):
     """RD-V2 (section 3.4): newest 16 blocks exact, older blocks one-centroid, and
     10.2% exact residual rows by Eq. rdscore against the block mean; 28 query / 4 KV
     heads.  Records, residual sets and masks bit-exact; attention and certificate
-    against the oracle."""
+    against the oracle.  T = 7464 (117 blocks, 12 residual pseudo-blocks) puts the
+    visit group that holds the last block and the first residual rows inside the
+    plan's reordered range, onto a group of one-centroid blocks."""
     torch = _torch()
     Hq, Hkv = 28, 4
     ks, vs = kv_all(9, Bn, Hkv, T)
