@@ -1411,8 +1411,8 @@ static_assert(sizeof(VisitDesc) == 32, "descriptor size");
 // its SIMD (about 8 cycles per unit).  Exact tiles are bound by the wavefront's
 // share of the bandwidth (8 KB each), int tiles by the dequantisation and softmax
 // work rather than by their bytes.
-constexpr uint32_t kCostExactTile = 523, kCostInt8Tile = 426, kCostInt4Tile = 314, kCostInt2Tile = 295,
-                   kCostCentroid = 768, kCostIntBlock = 248, kCostMean = 300, kCostMeanRun = 260,
+constexpr uint32_t kCostExactTile = 551, kCostInt8Tile = 426, kCostInt4Tile = 340, kCostInt2Tile = 306,
+                   kCostCentroid = 799, kCostIntBlock = 248, kCostMean = 300, kCostMeanRun = 260,
                    kCostMeanRunBlock = 45;
 
 // Blocks in a one-centroid run (1 for every other visit) and the visit's level.
