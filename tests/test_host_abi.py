@@ -164,6 +164,16 @@ def test_call_validation_errors(B):
     # quantize: an int block may not extend past the source rows
     src = np.zeros(16, dtype=np.uint16)
     assert B._quantize_block(ctypes.byref(c), 0, B._np_ptr(src), 1000, 0, 32, None) == -2
+    # residual selection: source rows must be 16-byte aligned
+    cr, keep_r = _host_cache(B, 1, 2, 8, T, olad.ladder("tiny", T), nres=64)
+    rows = np.zeros(2 * T * 128 + 8, dtype=np.uint16)
+    mass = np.zeros(2 * T, dtype=np.float32)
+    wsr = np.zeros(16, dtype=np.int64)
+    base = rows.ctypes.data + (-rows.ctypes.data) % 16
+    for kp, vp in ((base + 2, base), (base, base + 8)):
+        assert B._rd(ctypes.byref(cr), kp, vp, B._np_ptr(mass), 16, B._np_ptr(wsr), 1 << 40, None) == -1
+    # aligned rows pass that check and meet the workspace check after it
+    assert B._rd(ctypes.byref(cr), base, base, B._np_ptr(mass), 16, B._np_ptr(wsr), 8, None) == -4
     # G > 16 and a non-dividing head count
     c.Hq = 34
     assert B._attn(B._np_ptr(q), ctypes.byref(c), None, 0, B._np_ptr(out), B._np_ptr(ws), 1 << 30, None) == -2
@@ -464,6 +474,12 @@ def test_ragged_lengths_validation_crossings_and_accounting(B):
     assert n == len(want) and n > 0
     got = sorted((int(jobs[3 * i]), int(jobs[3 * i + 1]), int(jobs[3 * i + 2]), int(to[i])) for i in range(n))
     assert got == sorted(want)
+    # the last block of sequence 1 (7 of its 64 tokens) stays exact although the block
+    # ends below T: demoting it is rejected before anything is enqueued
+    assert int(keep["lv"][1, 0, 25]) == 16
+    nk = np.zeros(1, np.int64)
+    j1, t8 = np.array([1, 0, 25], np.int32), np.array([8], np.int8)
+    assert B._demote(ctypes.byref(c), 1, B._np_ptr(j1), B._np_ptr(t8), B._np_ptr(nk), B._np_ptr(nk), None) == -2
     rates = B.Rates()
     assert B._account(ctypes.byref(c), None, 0, None, ctypes.byref(rates)) == 0
     res = sum(2 * oacc.unit_rates(olad.ladder("graded", t), t)["resident_bits"] for t in lens if t > 0)
