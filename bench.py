@@ -324,10 +324,11 @@ def quest_point(wq, ncopies, dev, cpu=None):
     return {"workload": wq.name, "B": wq.B, "us_per_step": round(gr_ms * 1e3, 2),
             "us_per_step_eager": round(ev_ms * 1e3, 2), "select_us": round(sel_ms * 1e3, 2),
             "attn_us": round(att_ms * 1e3, 2),
-            "note": "us_per_step: the steps (selection + attention) replayed from one captured graph, the GPU's "
-                    "time; us_per_step_eager: the same steps called from Python, event-timed (at B=1 the host's "
-                    "two calls per step can take longer than the GPU); select_us, attn_us: each alone, replayed "
-                    "from a captured graph",
+            "note": "us_per_step: the steps (selection + attention) replayed from one captured graph; "
+                    "us_per_step_eager: the same steps called from Python, event-timed (at B=1 the host's two "
+                    "calls per step take longer than the GPU's work; where the GPU's work dominates, as at B=8, "
+                    "the eager steps can be the shorter, the graph adding a little per kernel node); select_us, "
+                    "attn_us: each alone, replayed from a captured graph",
             "read_bpv": round(r["read_bpv"], 4),
             "resident_bpv": round(r["resident_bpv"], 4), "algorithmic_bytes": int(qbytes),
             "achieved_GBps": round(qbytes / (gr_ms * 1e-3) / 1e9, 1),
