@@ -267,6 +267,8 @@ class Pool:
 
 def _as_bits(t, device):
     """fp16 bit patterns as an int16 device tensor."""
+    if isinstance(t, torch.Tensor) and t.dtype == torch.int16 and t.device == device and t.is_contiguous():
+        return t  # already in place: no conversion or copy (the decode loop's case)
     if isinstance(t, np.ndarray):
         t = torch.from_numpy(np.ascontiguousarray(t).view(np.int16))
     if t.dtype == torch.float16:
@@ -294,6 +296,7 @@ class GradedCache:
         self.nblk_cap = nblk_cap
         self.pool = Pool(caps)
         self.arena = torch.empty(max(self.pool.bytes, 256), dtype=torch.uint8, device=self.device)
+        self._dev = self.arena.device  # the concrete device (with its index), for the inputs' fast path
         self.level = torch.zeros((B, Hkv, nblk_cap), dtype=torch.int8, device=self.device)
         self.koff = torch.zeros((B, Hkv, nblk_cap), dtype=torch.int64, device=self.device)
         self.voff = torch.zeros((B, Hkv, nblk_cap), dtype=torch.int64, device=self.device)
@@ -439,24 +442,27 @@ class GradedCache:
         _check(_admit(ctypes.byref(self.c), int(b), _stream()), "admit_sequence")
 
     def workspace(self, op, topk=0):
+        """The workspace of call `op` (and top-k), allocated once: its size depends on the
+        cache's capacities only, which do not change."""
+        key = (op, topk)
+        ws = self._ws.get(key)
+        if ws is not None:
+            return ws
         n = int(_workspace_bytes(ctypes.byref(self.c), op, topk))
         if n < 0:
             raise GkvError(-1, "workspace_bytes")
-        key = (op, topk)
-        ws = self._ws.get(key)
-        if ws is None or ws.numel() < n:
-            ws = torch.zeros(max(n, 16), dtype=torch.uint8, device=self.device)
-            self._ws[key] = ws
+        ws = torch.zeros(max(n, 16), dtype=torch.uint8, device=self.device)
+        self._ws[key] = ws
         return ws
 
     # ------------------------------------------------------------ the six calls (+ append)
     def quantize_block(self, which, src, blk_begin, blk_end):
-        src = _as_bits(src, self.device)
+        src = _as_bits(src, self._dev)
         _check(_quantize_block(ctypes.byref(self.c), which, _dptr(src), src.shape[2], blk_begin, blk_end, _stream()),
                "quantize_block")
 
     def page_boxes(self, k_src, page_begin, page_end):
-        k_src = _as_bits(k_src, self.device)
+        k_src = _as_bits(k_src, self._dev)
         _check(_page_boxes(ctypes.byref(self.c), _dptr(k_src), k_src.shape[2], page_begin, page_end, _stream()),
                "page_boxes")
 
@@ -503,8 +509,8 @@ class GradedCache:
         """Append one token per (b,h) (k_new, v_new fp16 bits [B][Hkv][128]); then,
         with a ladder profile, demote every block whose level the profile lowers.
         Returns the demotions [(b, h, blk, old, new)]."""
-        kd = _as_bits(k_new, self.device)
-        vd = _as_bits(v_new, self.device)
+        kd = _as_bits(k_new, self._dev)
+        vd = _as_bits(v_new, self._dev)
         lens = self.lengths()
         opens = [b for b in range(self.B) if lens[b] >= 0 and lens[b] % P == 0]
         nk = nv = None
@@ -550,7 +556,7 @@ class GradedCache:
         return moves
 
     def quest_select(self, q, topk, out=None):
-        q = _as_bits(q, self.device)
+        q = _as_bits(q, self._dev)
         if out is None:
             out = torch.empty((self.B, self.Hkv, topk), dtype=torch.int32, device=self.device)
         ws = self.workspace(0)
@@ -559,7 +565,7 @@ class GradedCache:
         return out
 
     def graded_decode_attn(self, q, pages=None, out=None):
-        q = _as_bits(q, self.device)
+        q = _as_bits(q, self._dev)
         topk = int(pages.shape[-1]) if pages is not None else 0
         if out is None:
             out = torch.empty((self.B, self.Hq, D), dtype=torch.float32, device=self.device)
@@ -574,7 +580,7 @@ class GradedCache:
         """gkv_graded_decode_attn_noalloc: the same read with the library's own device
         scratch array as workspace (no workspace argument; out must be given by a
         caller that cannot allocate)."""
-        q = _as_bits(q, self.device)
+        q = _as_bits(q, self._dev)
         topk = int(pages.shape[-1]) if pages is not None else 0
         if out is None:
             out = torch.empty((self.B, self.Hq, D), dtype=torch.float32, device=self.device)
@@ -585,7 +591,7 @@ class GradedCache:
     def decode_bound(self, q, out=None, bound=None):
         """Dense decode plus the attention error certificate per query head:
         returns (out [B][Hq][128] fp32, bound [B][Hq] fp32)."""
-        q = _as_bits(q, self.device)
+        q = _as_bits(q, self._dev)
         if out is None:
             out = torch.empty((self.B, self.Hq, D), dtype=torch.float32, device=self.device)
         if bound is None:
@@ -602,7 +608,7 @@ class GradedCache:
         _check(_attn_plan(ctypes.byref(self.c), _dptr(pages), topk, _dptr(ws), ws.numel(), _stream()), "attn_plan")
 
     def attn_partials(self, q, pages=None):
-        q = _as_bits(q, self.device)
+        q = _as_bits(q, self._dev)
         topk = int(pages.shape[-1]) if pages is not None else 0
         ws = self.workspace(1, topk)
         _check(_attn_partials(_dptr(q), ctypes.byref(self.c), _dptr(pages), topk, _dptr(ws), ws.numel(), _stream()),
@@ -615,8 +621,8 @@ class GradedCache:
                "attn_merge")
 
     def rd_residual_select(self, k_src, v_src, mass, nkeep):
-        kd = _as_bits(k_src, self.device)
-        vd = _as_bits(v_src, self.device)
+        kd = _as_bits(k_src, self._dev)
+        vd = _as_bits(v_src, self._dev)
         if isinstance(mass, np.ndarray):
             mass = torch.from_numpy(np.ascontiguousarray(mass, dtype=np.float32))
         md = mass.to(self.device, torch.float32).contiguous()
