@@ -1350,18 +1350,23 @@ __global__ void __launch_bounds__(D) merge_kernel(const float *part, float *out,
     svm[d] = vm;
   }
   __syncthreads();
-  if (d == 0) {
+  if (d < 64) {  // the first wavefront: the split weights a_s and L, lane d over splits d, d + 64, ...
     float M = kNegInf;
-    for (int s2 = 0; s2 < nsplit; ++s2) M = fmaxf(M, sa[s2]);
+    for (int s2 = d; s2 < nsplit; s2 += 64) M = fmaxf(M, sa[s2]);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
     float L = 0.f;
-    for (int s2 = 0; s2 < nsplit; ++s2) {
+    for (int s2 = d; s2 < nsplit; s2 += 64) {
       const float a = sa[s2] == kNegInf ? 0.f : __builtin_amdgcn_exp2f(sa[s2] - M);
       sa[s2] = a;
       L = fmaf(a, sl[s2], L);
     }
-    sinv = L > 0.f ? 1.0f / L : 0.f;  // an empty sequence reads nothing: its output is zero
-    if (bound && !(L > 0.f)) bound[u * G + g] = 0.f;
-    if (bound && L > 0.f) {  // section 3.6: sum_b a_b verr_b + min(2, M+/M- - M-/M+) max_j ||v_j||
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) L += __shfl_xor(L, o);
+    if (d == 0) sinv = L > 0.f ? 1.0f / L : 0.f;  // an empty sequence reads nothing: its output is zero
+    // lane 0 reads the weights the wavefront's lanes wrote (LDS keeps one wavefront's order)
+    if (d == 0 && bound && !(L > 0.f)) bound[u * G + g] = 0.f;
+    if (d == 0 && bound && L > 0.f) {  // section 3.6: sum_b a_b verr_b + min(2, M+/M- - M-/M+) max_j ||v_j||
       float c1 = 0.f, c2 = 0.f, c3 = 0.f, vm = 0.f;
       for (int s2 = 0; s2 < nsplit; ++s2) {
         c1 = fmaf(sa[s2], base[s2 * stride + D + 2], c1);
