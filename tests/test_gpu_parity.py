@@ -166,6 +166,24 @@ def test_quest_larger_pages(gpu, page, T, topk):
             assert max_err(out[0, h * G:(h + 1) * G], uc.decode_dense(q_group(q, 0, h, G))) <= TOL
 
 
+def test_quest_read_with_more_splits_than_a_wavefront(gpu):
+    """One (b, KV head) with top-600 pages: one wavefront per read page puts 151
+    workgroups' partials into one merge, more than the 64 lanes that take the split
+    weights (three splits per lane).  Pages bit-exact, output against the oracle."""
+    T, Hq, Hkv, page, topk = 16384, 4, 1, 16, 600
+    ks, vs = kv_all(33, 1, Hkv, T)
+    lv = olad.ladder("graded", T)
+    cache = _build(gpu, ks, vs, Hq, lv, page=page)
+    q = synth.queries(33, 1, Hq)
+    pages = cache.quest_select(q, topk)
+    out = cache.decode(q, pages=pages).cpu().numpy()
+    kmin, kmax = oquest.page_boxes(ks[0, 0])
+    want = oquest.quest_select(q_group(q, 0, 0, Hq), kmin, kmax, T, topk)
+    np.testing.assert_array_equal(pages.cpu().numpy()[0, 0], want)
+    uc = ocache.UnitCache(ks[0, 0], vs[0, 0], lv)
+    assert max_err(out[0], uc.decode_quest(q_group(q, 0, 0, Hq), want)) <= TOL
+
+
 def test_quest_ties_go_to_lower_page(gpu):
     T, Hq, Hkv = 2048, 4, 1
     ks, vs = kv_all(31, 1, Hkv, T)
