@@ -569,9 +569,10 @@ __global__ void __launch_bounds__(kThreads) boxes_kernel(const uint16_t *__restr
 // 64 threads.
 //
 // Staged words: chunk ck (32 codes, 4 tokens x 8 channels) holds `wpc` words; the 16
-// chunks of one four-token group c = ck >> 4 are contiguous and each group starts
-// kRdGroup words after the last, so that the lanes of the 16 groups, which read the
-// same word of their own group, fall in different banks.
+// chunks of one four-token group c = ck >> 4 are contiguous, and group c starts at
+// word c * kRdGroup (4 words of padding after each group's 16 * wpc), so that the
+// lanes of the 16 groups, which read the same word of their own group, fall in
+// different banks.
 constexpr int kRdGroup = 16 * 8 + 4;
 
 struct RdShared {
