@@ -419,42 +419,15 @@ struct NewSlots {
   int64_t len[GKV_MAX_APPEND_UNITS];
 };
 
-__global__ void __launch_bounds__(128) append_kernel(const uint16_t *__restrict__ k_new,
-                                                     const uint16_t *__restrict__ v_new, int8_t *level,
-                                                     int64_t *koff, int64_t *voff, uint8_t *arena,
-                                                     uint16_t *boxes, int64_t npage_cap, int page, int Hkv,
-                                                     int nblk_cap, int64_t T_all, int64_t *seq_len, NewSlots slots,
-                                                     float *cert) {
-  __shared__ double vsq[D];
-  const int h = blockIdx.x, b = blockIdx.y, d = threadIdx.x;
-  const int64_t u = (int64_t)b * Hkv + h;
-  const int64_t T = seq_len ? slots.len[b] : T_all;
-  if (T < 0) return;  // a retired sequence
-  if (seq_len && h == 0 && d == 0) seq_len[b] = T + 1;
-  const int open_block = (T % P) == 0;
-  const int blk = (int)(T / P), tok = (int)(T % P);
-  const int64_t ti = u * nblk_cap + blk;
-  int64_t ko, vo;
-  if (open_block) {
-    ko = slots.k[u];
-    vo = slots.v[u];
-    if (d == 0) {
-      level[ti] = GKV_EXACT;
-      koff[ti] = ko;
-      voff[ti] = vo;
-    }
-  } else {
-    ko = koff[ti];
-    vo = voff[ti];
-  }
-  if (open_block) {  // a new block's other rows are defined (zero): reads mask them, but 0 * NaN is NaN
-    uint4 *kz = (uint4 *)(arena + ko), *vz = (uint4 *)(arena + vo);
-    for (int i = d; i < kExactBytes / 16; i += D) {
-      kz[i] = make_uint4(0, 0, 0, 0);
-      vz[i] = make_uint4(0, 0, 0, 0);
-    }
-    __syncthreads();
-  }
+// Writes the token of unit u at position T (row tok = T % 64 of the exact block at
+// key / value offsets ko / vo, record slot ti): its key and value rows, the value-norm
+// bound and, when the token completes a page, that page's box.  128 threads, one per
+// channel d.
+__device__ __forceinline__ void append_write(const uint16_t *__restrict__ k_new, const uint16_t *__restrict__ v_new,
+                                             uint8_t *arena, uint16_t *boxes, int64_t npage_cap, int page,
+                                             int64_t u, int64_t T, int64_t ti, int64_t ko, int64_t vo,
+                                             bool open_block, float *cert, double *vsq, int d) {
+  const int tok = (int)(T % P);
   const uint16_t kv = k_new[u * D + d], vv = v_new[u * D + d];
   if (cert) {  // an exact block: no error; the value norms grow by this row
     const double x = (double)__builtin_bit_cast(_Float16, vv);
@@ -502,6 +475,79 @@ __global__ void __launch_bounds__(128) append_kernel(const uint16_t *__restrict_
     bx[0] = canon_zero(__builtin_bit_cast(uint16_t, mn));
     bx[1] = canon_zero(__builtin_bit_cast(uint16_t, mx));
   }
+}
+
+__global__ void __launch_bounds__(128) append_kernel(const uint16_t *__restrict__ k_new,
+                                                     const uint16_t *__restrict__ v_new, int8_t *level,
+                                                     int64_t *koff, int64_t *voff, uint8_t *arena,
+                                                     uint16_t *boxes, int64_t npage_cap, int page, int Hkv,
+                                                     int nblk_cap, int64_t T_all, int64_t *seq_len, NewSlots slots,
+                                                     float *cert) {
+  __shared__ double vsq[D];
+  const int h = blockIdx.x, b = blockIdx.y, d = threadIdx.x;
+  const int64_t u = (int64_t)b * Hkv + h;
+  const int64_t T = seq_len ? slots.len[b] : T_all;
+  if (T < 0) return;  // a retired sequence
+  if (seq_len && h == 0 && d == 0) seq_len[b] = T + 1;
+  const int open_block = (T % P) == 0;
+  const int blk = (int)(T / P);
+  const int64_t ti = u * nblk_cap + blk;
+  int64_t ko, vo;
+  if (open_block) {
+    ko = slots.k[u];
+    vo = slots.v[u];
+    if (d == 0) {
+      level[ti] = GKV_EXACT;
+      koff[ti] = ko;
+      voff[ti] = vo;
+    }
+  } else {
+    ko = koff[ti];
+    vo = voff[ti];
+  }
+  if (open_block) {  // a new block's other rows are defined (zero): reads mask them, but 0 * NaN is NaN
+    uint4 *kz = (uint4 *)(arena + ko), *vz = (uint4 *)(arena + vo);
+    for (int i = d; i < kExactBytes / 16; i += D) {
+      kz[i] = make_uint4(0, 0, 0, 0);
+      vz[i] = make_uint4(0, 0, 0, 0);
+    }
+    __syncthreads();
+  }
+  append_write(k_new, v_new, arena, boxes, npage_cap, page, u, T, ti, ko, vo, open_block, cert, vsq, d);
+}
+
+// One decode step's appends for up to kAppendLayers layers of one batch in one launch,
+// when no sequence opens a block (the layers share B, Hkv, the block capacity and the
+// lengths; the newest block of every unit is exact).  grid (Hkv, B, layers).
+constexpr int kAppendLayers = 16;
+struct AppendLayer {
+  int64_t *koff, *voff;
+  uint8_t *arena;
+  uint16_t *boxes;
+  float *cert;
+  int64_t *seq_len;
+  int64_t npage_cap;
+  int32_t page;
+};
+struct AppendBatch {
+  AppendLayer l[kAppendLayers];
+  int64_t len[GKV_MAX_APPEND_UNITS];  // each sequence's length before the step (with per-sequence lengths)
+};
+
+__global__ void __launch_bounds__(128) append_layers_kernel(const uint16_t *__restrict__ k_new,
+                                                            const uint16_t *__restrict__ v_new, int64_t layer_stride,
+                                                            int Hkv, int nblk_cap, int64_t T_all, int ragged,
+                                                            AppendBatch ab) {
+  __shared__ double vsq[D];
+  const int h = blockIdx.x, b = blockIdx.y, l = blockIdx.z, d = threadIdx.x;
+  const AppendLayer &L = ab.l[l];
+  const int64_t u = (int64_t)b * Hkv + h;
+  const int64_t T = ragged ? ab.len[b] : T_all;
+  if (T < 0) return;  // a retired sequence
+  if (L.seq_len && h == 0 && d == 0) L.seq_len[b] = T + 1;
+  const int64_t ti = u * nblk_cap + T / P;
+  append_write(k_new + l * layer_stride, v_new + l * layer_stride, L.arena, L.boxes, L.npage_cap, L.page, u, T, ti,
+               L.koff[ti], L.voff[ti], false, L.cert, vsq, d);
 }
 
 // Page boxes from token-major exact keys; one workgroup per 64 pages of one (b,h).
@@ -866,6 +912,12 @@ extern "C" gkv_status gkv_append(gkv_cache *c, const uint16_t *k_new, const uint
                      c->koff, c->voff, c->arena, c->page ? c->boxes : nullptr, c->npage_cap, c->page ? c->page : 1,
                      c->Hkv, c->nblk_cap, c->T, c->seq_len, slots, c->cert);
   if (hipGetLastError() != hipSuccess) return GKV_E_HIP;
+  gkv_append_commit(c, any_open);
+  return GKV_OK;
+}
+
+// The host side of an enqueued append: the opened blocks' levels, the lengths and T.
+void gkv_append_commit(gkv_cache *c, bool any_open) {
   int64_t mx = 0;
   for (int b = 0; b < c->B; ++b) {
     const int64_t T = seq_tokens(c, b);
@@ -879,5 +931,29 @@ extern "C" gkv_status gkv_append(gkv_cache *c, const uint16_t *k_new, const uint
   // the tables change only when a block opens; a dense plan covers whole blocks, and
   // the attention masks a block's tokens past the length at run time
   if (any_open) gkv_stamp(c);
+}
+
+// One launch per kAppendLayers layers for a step that opens no block: the caller has
+// checked what gkv_append checks (same B, Hkv, capacity and lengths over the layers;
+// every newest block exact; page-box capacity).  Nothing of the host state changes.
+gkv_status gkv_launch_append_layers(gkv_cache *const *caches, int L, const uint16_t *k_new, const uint16_t *v_new,
+                                    hipStream_t stream) {
+  const gkv_cache *c0 = caches[0];
+  if (c0->seq_len_host && c0->B > GKV_MAX_APPEND_UNITS) return GKV_E_UNSUPPORTED;
+  const int64_t stride = (int64_t)c0->B * c0->Hkv * D;
+  for (int l0 = 0; l0 < L; l0 += kAppendLayers) {
+    const int n = L - l0 < kAppendLayers ? L - l0 : kAppendLayers;
+    AppendBatch ab;
+    for (int i = 0; i < n; ++i) {
+      const gkv_cache *c = caches[l0 + i];
+      ab.l[i] = AppendLayer{c->koff, c->voff, c->arena, c->page ? c->boxes : nullptr, c->cert, c->seq_len,
+                            c->npage_cap, c->page ? c->page : 1};
+    }
+    if (c0->seq_len_host)
+      for (int b = 0; b < c0->B; ++b) ab.len[b] = c0->seq_len_host[b];
+    hipLaunchKernelGGL(append_layers_kernel, dim3(c0->Hkv, c0->B, n), dim3(128), 0, stream, k_new + l0 * stride,
+                       v_new + l0 * stride, stride, c0->Hkv, c0->nblk_cap, c0->T, c0->seq_len_host ? 1 : 0, ab);
+    if (hipGetLastError() != hipSuccess) return GKV_E_HIP;
+  }
   return GKV_OK;
 }

@@ -154,3 +154,6 @@ int gkv_device_cus();
 // Sets c->version to a new process-wide unique stamp (host.cpp); every call that
 // changes the block tables, T or nres calls it on success.
 void gkv_stamp(gkv_cache *c);
+void gkv_append_commit(gkv_cache *c, bool any_open);
+gkv_status gkv_launch_append_layers(gkv_cache *const *caches, int L, const uint16_t *k_new, const uint16_t *v_new,
+                                    hipStream_t stream);

@@ -135,6 +135,14 @@ extern "C" int32_t gkv_layers_step(gkv_cache *const *caches, gkv_pool *const *po
       return GKV_E_ARG;
     }
   }
+  if (!any_open) {  // no block opens: one launch appends the token of every layer
+    const gkv_status st = gkv_launch_append_layers(caches, L, k_new, v_new, (hipStream_t)stream);
+    if (st) {  // nothing is appended
+      give_back_from(0);
+      return st;
+    }
+    for (int l = 0; l < L; ++l) gkv_append_commit(caches[l], false);
+  }
   int32_t total = 0;
   for (int l = 0; l < L; ++l) {
     gkv_cache *c = caches[l];
@@ -142,8 +150,8 @@ extern "C" int32_t gkv_layers_step(gkv_cache *const *caches, gkv_pool *const *po
     const int32_t n = cr[l].n;
     const int32_t *jobs = cr[l].jobs.data();
     const int8_t *to = cr[l].to.data();
-    gkv_status st = gkv_append(c, k_new + l * row, v_new + l * row, any_open ? nk[l].data() : nullptr,
-                               any_open ? nv[l].data() : nullptr, stream);
+    gkv_status st = any_open ? gkv_append(c, k_new + l * row, v_new + l * row, nk[l].data(), nv[l].data(), stream)
+                             : GKV_OK;
     if (st) {  // layers before l are stepped; nothing of layer l or later is
       give_back_from(l);
       return st;
