@@ -405,9 +405,11 @@ gkv_status gkv_rd_residual_select(gkv_cache *c, const uint16_t *k_src, const uin
  * layer's crossings are checked (GKV_E_NOT_MONOTONE when the profile would raise a
  * level of any layer), every slot is taken and checked against its layer's arena:
  * GKV_E_POOL, GKV_E_ARG (a slot past arena_bytes) or any other argument error leaves
- * every cache, pool and mirror unchanged.  Should the HIP runtime fail part-way, the
- * layers before the failing one stay stepped and every slot not yet in use goes back
- * to its pool.  Returns the number of blocks demoted over all layers (>= 0) or a
+ * every cache, pool and mirror unchanged.  A step that opens no block appends up to
+ * 16 layers per launch.  Should the HIP runtime fail part-way, the layers whose
+ * appends were enqueued keep them (their T advanced; the demotions of a layer after
+ * the failure point are not made) and every slot not yet in use goes back to its
+ * pool.  Returns the number of blocks demoted over all layers (>= 0) or a
  * negative gkv_status. */
 int32_t gkv_layers_step(gkv_cache *const *caches, gkv_pool *const *pools, int64_t *const *koff_host,
                         int64_t *const *voff_host, int32_t L, int32_t profile, const uint16_t *k_new,

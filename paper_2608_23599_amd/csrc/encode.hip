@@ -519,7 +519,7 @@ __global__ void __launch_bounds__(128) append_kernel(const uint16_t *__restrict_
 // One decode step's appends for up to kAppendLayers layers of one batch in one launch,
 // when no sequence opens a block (the layers share B, Hkv, the block capacity and the
 // lengths; the newest block of every unit is exact).  grid (Hkv, B, layers).
-constexpr int kAppendLayers = 16;
+constexpr int kAppendLayers = GKV_APPEND_LAYERS;
 struct AppendLayer {
   int64_t *koff, *voff;
   uint8_t *arena;
@@ -933,27 +933,25 @@ void gkv_append_commit(gkv_cache *c, bool any_open) {
   if (any_open) gkv_stamp(c);
 }
 
-// One launch per kAppendLayers layers for a step that opens no block: the caller has
-// checked what gkv_append checks (same B, Hkv, capacity and lengths over the layers;
-// every newest block exact; page-box capacity).  Nothing of the host state changes.
-gkv_status gkv_launch_append_layers(gkv_cache *const *caches, int L, const uint16_t *k_new, const uint16_t *v_new,
+// One launch for n <= GKV_APPEND_LAYERS layers of a step that opens no block (k_new,
+// v_new: their rows, layer after layer): the caller has checked what gkv_append
+// checks (same B, Hkv, capacity and lengths over the layers; every newest block
+// exact; page-box capacity).  Nothing of the host state changes.
+gkv_status gkv_launch_append_layers(gkv_cache *const *caches, int n, const uint16_t *k_new, const uint16_t *v_new,
                                     hipStream_t stream) {
   const gkv_cache *c0 = caches[0];
+  if (n < 1 || n > kAppendLayers) return GKV_E_ARG;
   if (c0->seq_len_host && c0->B > GKV_MAX_APPEND_UNITS) return GKV_E_UNSUPPORTED;
   const int64_t stride = (int64_t)c0->B * c0->Hkv * D;
-  for (int l0 = 0; l0 < L; l0 += kAppendLayers) {
-    const int n = L - l0 < kAppendLayers ? L - l0 : kAppendLayers;
-    AppendBatch ab;
-    for (int i = 0; i < n; ++i) {
-      const gkv_cache *c = caches[l0 + i];
-      ab.l[i] = AppendLayer{c->koff, c->voff, c->arena, c->page ? c->boxes : nullptr, c->cert, c->seq_len,
-                            c->npage_cap, c->page ? c->page : 1};
-    }
-    if (c0->seq_len_host)
-      for (int b = 0; b < c0->B; ++b) ab.len[b] = c0->seq_len_host[b];
-    hipLaunchKernelGGL(append_layers_kernel, dim3(c0->Hkv, c0->B, n), dim3(128), 0, stream, k_new + l0 * stride,
-                       v_new + l0 * stride, stride, c0->Hkv, c0->nblk_cap, c0->T, c0->seq_len_host ? 1 : 0, ab);
-    if (hipGetLastError() != hipSuccess) return GKV_E_HIP;
+  AppendBatch ab;
+  for (int i = 0; i < n; ++i) {
+    const gkv_cache *c = caches[i];
+    ab.l[i] = AppendLayer{c->koff, c->voff, c->arena, c->page ? c->boxes : nullptr, c->cert, c->seq_len,
+                          c->npage_cap, c->page ? c->page : 1};
   }
-  return GKV_OK;
+  if (c0->seq_len_host)
+    for (int b = 0; b < c0->B; ++b) ab.len[b] = c0->seq_len_host[b];
+  hipLaunchKernelGGL(append_layers_kernel, dim3(c0->Hkv, c0->B, n), dim3(128), 0, stream, k_new, v_new, stride,
+                     c0->Hkv, c0->nblk_cap, c0->T, c0->seq_len_host ? 1 : 0, ab);
+  return hipGetLastError() == hipSuccess ? GKV_OK : GKV_E_HIP;
 }

@@ -155,5 +155,6 @@ int gkv_device_cus();
 // changes the block tables, T or nres calls it on success.
 void gkv_stamp(gkv_cache *c);
 void gkv_append_commit(gkv_cache *c, bool any_open);
+constexpr int GKV_APPEND_LAYERS = 16;  // layers of one multi-layer append launch
 gkv_status gkv_launch_append_layers(gkv_cache *const *caches, int L, const uint16_t *k_new, const uint16_t *v_new,
                                     hipStream_t stream);

@@ -135,11 +135,17 @@ extern "C" int32_t gkv_layers_step(gkv_cache *const *caches, gkv_pool *const *po
       return GKV_E_ARG;
     }
   }
-  if (!any_open) {  // no block opens: one launch appends the token of every layer
-    const gkv_status st = gkv_launch_append_layers(caches, L, k_new, v_new, (hipStream_t)stream);
-    if (st) {  // nothing is appended
-      give_back_from(0);
-      return st;
+  if (!any_open) {  // no block opens: one launch appends the token of up to 16 layers
+    const size_t row = (size_t)units * D;
+    for (int l0 = 0; l0 < L; l0 += GKV_APPEND_LAYERS) {
+      const int n = L - l0 < GKV_APPEND_LAYERS ? L - l0 : GKV_APPEND_LAYERS;
+      const gkv_status st =
+          gkv_launch_append_layers(caches + l0, n, k_new + l0 * row, v_new + l0 * row, (hipStream_t)stream);
+      if (st) {  // the layers before l0 are appended (not yet demoted); the others are not
+        for (int l = 0; l < l0; ++l) gkv_append_commit(caches[l], false);
+        give_back_from(0);
+        return st;
+      }
     }
     for (int l = 0; l < L; ++l) gkv_append_commit(caches[l], false);
   }
