@@ -945,6 +945,38 @@ def test_layers_step_matches_per_layer_appends(gpu, skew):
         assert max_err(out[0, 0:G], uc.decode_dense(q_group(q, 0, 0, G))) <= TOL
 
 
+def test_layers_step_more_layers_than_one_launch(gpu):
+    """gkv_layers_step over 18 layers (more than the 16 one append launch serves),
+    through steps that open no block and one that does, against the same layers
+    appended one by one: identical levels, offsets, pool use and decode outputs."""
+    torch = _torch()
+    L, Hq, Hkv = 18, 4, 1
+    T0 = 64 * 6 - 3
+    steps = 5  # step 3 opens block 6
+    data = [kv_all(90 + l, 1, Hkv, T0 + steps) for l in range(L)]
+    lv = olad.ladder("graded", T0)
+    slack = {16: 4, 8: 4, 4: 4, 2: 4, 1: 4}
+    mk = lambda ks, vs: _build(gpu, ks[:, :, :T0], vs[:, :, :T0], Hq, lv, extra_blocks=2, slack=slack)
+    svc = gpu.LayerCaches([mk(*d) for d in data], "graded")
+    ref = [mk(*d) for d in data]
+    for s_ in range(steps):
+        t = T0 + s_
+        kn = np.stack([d[0][:, :, t] for d in data])
+        vn = np.stack([d[1][:, :, t] for d in data])
+        n = svc.step(kn, vn)
+        moves = [r.append(kn[l], vn[l], profile="graded") for l, r in enumerate(ref)]
+        assert sum(len(m) for m in moves) == n
+        q = synth.queries(91, 1, Hq, step=s_)
+        for l in range(L):
+            a, b = svc.caches[l], ref[l]
+            assert a.T == b.T == t + 1
+            np.testing.assert_array_equal(a.level_host, b.level_host)
+            np.testing.assert_array_equal(a.koff_host, b.koff_host)
+            np.testing.assert_array_equal(a.voff_host, b.voff_host)
+            assert all(a.pool.used(x) == b.pool.used(x) for x in gpu.LEVELS)
+            assert torch.equal(a.decode(q), b.decode(q))
+
+
 def test_opened_block_rows_are_defined(gpu):
     """A block opened by an append gets zero rows past the token: free slots filled
     with NaN bit patterns (as recycled records can hold) must not reach the output
