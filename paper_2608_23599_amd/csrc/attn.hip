@@ -1381,6 +1381,13 @@ __global__ void __launch_bounds__(D) merge_kernel(const float *part, float *out,
   __syncthreads();
   float o = 0.f;
   int s2 = 0;
+  for (; s2 + 16 <= nsplit; s2 += 16) {
+    float v[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) v[k] = base[(s2 + k) * stride + 2 + d];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) o = fmaf(sa[s2 + k], v[k], o);
+  }
   for (; s2 + 8 <= nsplit; s2 += 8) {
     float v[8];
 #pragma unroll
